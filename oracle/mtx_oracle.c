@@ -1,0 +1,705 @@
+/*
+ * CPU ORACLE for the data-parallel synchronous SGD step -- TEST INFRASTRUCTURE ONLY.
+ *
+ * This file is the plain, slow, obviously-correct reference that the GPU library is checked
+ * against.  Only the test-suite, the smoke check and the CPU-baseline leg of the benchmark may
+ * load it.  It shares no code, header, table or helper with the GPU library and it never calls
+ * into it.
+ *
+ * What it computes (paper: "User-transparent Distributed TensorFlow", arXiv 1704.04560):
+ *   - Sec. III-A / III-E: data parallelism with synchronous replicas.  The global batch B is
+ *     split into R equal shards; every replica holds the same weights and computes the gradient
+ *     of the mean loss of its own shard.
+ *   - Sec. II-B and Sec. III-D.2 (MPI_Allreduce operator): the replicas' gradients are combined
+ *     by an all-reduce "for averaging gradients", layer by layer in a fixed order, so the applied
+ *     gradient is (1/R) * sum_r g_r, which equals the full-batch mean gradient.
+ *   - Sec. III-D.2 and Sec. III-E: the result is equivalent to the sequential SGD step.  The
+ *     optimizer is the momentum method the paper lists among TensorFlow's optimizers (Sec. I):
+ *     v <- mu*v + g, w <- w - lr*v (TensorFlow 1.0 MomentumOptimizer form); mu == 0 is plain SGD.
+ *   - Sec. III-D.1 (Broadcast operator): replicas start identical.  Here every replica reads the
+ *     one weight vector, which is that property by construction.
+ *   - Fig. 1 (AlexNet: convolution + fully connected layers) and Sec. I (MLP / CNN): the layer
+ *     types: fully connected, convolution (stride, zero padding, groups), max-pooling, ReLU, and a
+ *     softmax cross-entropy loss (the paper trains 1000-class ImageNet classifiers, Table II).
+ *
+ * The paper gives no formula for any of these; the code below is the textbook definition of
+ * each, written as direct loops in double precision.  Readings taken where the paper is silent:
+ *   - mean (not sum) reduction; shard loss = mean over the shard's samples;
+ *   - momentum form v <- mu*v + g, w <- w - lr*v with v0 = 0; no weight decay, no Nesterov;
+ *   - relu'(0) = 0; max-pool ties resolve to the first maximal element in row-major window
+ *     order; pooling windows are "valid" (no padding);
+ *   - Glorot-uniform weights U(-a, a), a = sqrt(6 / (fan_in + fan_out)), biases zero, drawn from
+ *     a counter-based generator (first output of SplitMix64 seeded with seed ^ (layer << 32 | i));
+ *   - storage precision: in "fp32" mode every stored tensor (activations, gradients) is rounded
+ *     to float; in "bf16" mode the input, the weights used by the layers, every hidden-layer
+ *     output, the loss gradient and every data-gradient are rounded to bfloat16 (round to nearest
+ *     even) while logits, weight/bias gradients, averages and the update stay float.  All sums
+ *     are carried out in double.  An "exact" mode rounds nothing before the float outputs; it
+ *     exists so that the oracle itself can be pinned against finite differences and against
+ *     double-precision autograd.
+ *
+ * Build: gcc -O2 -fopenmp -shared -fPIC mtx_oracle.c -lm (OpenMP only parallelises over
+ * independent outputs; every individual sum is a sequential loop, so results do not depend on
+ * the thread count).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_FC 0
+#define ORC_CONV 1
+#define ORC_MAXPOOL 2
+
+#define ORC_OK 0
+#define ORC_EINVAL -1
+#define ORC_ENOMEM -2
+#define ORC_EHINT -6 /* a decision hint lies outside the oracle's own error bound */
+
+/* storage precision of the training step */
+#define ORC_PREC_F32 0   /* every stored tensor rounded to float */
+#define ORC_PREC_BF16 1  /* bfloat16 storage at the documented points, float elsewhere */
+#define ORC_PREC_EXACT 2 /* nothing rounded until the float outputs (used to pin the oracle) */
+
+typedef struct {
+    int kind, out, k, stride, pad, groups, relu;
+} orc_layer;
+
+typedef struct {
+    int kind, relu;
+    int c, h, w;    /* input shape (per sample) */
+    int oc, oh, ow; /* output shape (per sample) */
+    int k, s, p, g;
+    long w_off, w_len, b_off, b_len; /* offsets into the flat parameter vector */
+} orc_geom;
+
+/* ------------------------------------------------------------------------------------------ */
+/* rounding                                                                                   */
+/* ------------------------------------------------------------------------------------------ */
+
+static double rnd_f32(double x) { return (double)(float)x; }
+static double rnd_none(double x) { return x; }
+
+/* Round a value to bfloat16 the way an fp32 accumulator is stored: first to float, then keep the
+ * top 16 bits with round-to-nearest-even on the discarded half. */
+static double rnd_bf16(double x)
+{
+    float f = (float)x;
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) { /* NaN stays NaN */
+        u |= 0x00400000u;
+        u &= 0xffff0000u;
+    } else {
+        u = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
+    }
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+float orc_round_bf16(float x) { return (float)rnd_bf16((double)x); }
+
+/* ------------------------------------------------------------------------------------------ */
+/* geometry                                                                                   */
+/* ------------------------------------------------------------------------------------------ */
+
+int orc_plan(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, orc_geom* G,
+             long* n_params)
+{
+    int c = in_c, h = in_h, w = in_w;
+    long off = 0;
+    if (in_c < 1 || in_h < 1 || in_w < 1 || n_layers < 1 || !L) return ORC_EINVAL;
+    for (int i = 0; i < n_layers; i++) {
+        orc_geom* g = &G[i];
+        memset(g, 0, sizeof *g);
+        g->kind = L[i].kind;
+        g->relu = L[i].relu ? 1 : 0;
+        g->c = c; g->h = h; g->w = w;
+        if (L[i].kind == ORC_CONV) {
+            g->k = L[i].k; g->s = L[i].stride; g->p = L[i].pad; g->g = L[i].groups;
+            if (g->k < 1 || g->s < 1 || g->p < 0 || g->g < 1 || L[i].out < 1) return ORC_EINVAL;
+            if (c % g->g || L[i].out % g->g) return ORC_EINVAL;
+            g->oc = L[i].out;
+            g->oh = (h + 2 * g->p - g->k) / g->s + 1;
+            g->ow = (w + 2 * g->p - g->k) / g->s + 1;
+            if (h + 2 * g->p < g->k || w + 2 * g->p < g->k) return ORC_EINVAL;
+            g->w_len = (long)g->oc * (c / g->g) * g->k * g->k;
+            g->b_len = g->oc;
+        } else if (L[i].kind == ORC_FC) {
+            if (L[i].out < 1) return ORC_EINVAL;
+            g->k = 1; g->s = 1; g->p = 0; g->g = 1;
+            g->oc = L[i].out; g->oh = 1; g->ow = 1;
+            g->w_len = (long)g->oc * c * h * w;
+            g->b_len = g->oc;
+        } else if (L[i].kind == ORC_MAXPOOL) {
+            g->k = L[i].k; g->s = L[i].stride; g->p = 0; g->g = 1;
+            if (g->k < 1 || g->s < 1 || h < g->k || w < g->k || g->k > 16) return ORC_EINVAL;
+            if (g->relu) return ORC_EINVAL;
+            g->oc = c;
+            g->oh = (h - g->k) / g->s + 1;
+            g->ow = (w - g->k) / g->s + 1;
+        } else {
+            return ORC_EINVAL;
+        }
+        g->w_off = off; off += g->w_len;
+        g->b_off = off; off += g->b_len;
+        c = g->oc; h = g->oh; w = g->ow;
+    }
+    /* the network ends in a fully connected layer that produces the class scores */
+    if (L[n_layers - 1].kind != ORC_FC || L[n_layers - 1].relu) return ORC_EINVAL;
+    if (n_params) *n_params = off;
+    return ORC_OK;
+}
+
+int orc_param_count(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, long* n)
+{
+    orc_geom* G = (orc_geom*)calloc((size_t)n_layers, sizeof(orc_geom));
+    if (!G) return ORC_ENOMEM;
+    int rc = orc_plan(in_c, in_h, in_w, n_layers, L, G, n);
+    free(G);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* layers in double precision (textbook definitions)                                          */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Convolution, NCHW, weights [oc][c/g][k][k], zero padding p, stride s, g groups.
+ * y[n][o][i][j] = b[o] + sum_{c' , u, v} W[o][c'][u][v] * x[n][grp*c/g + c'][i*s - p + u][j*s - p + v] */
+void orc_conv_fwd(int N, int C, int H, int W, int OC, int K, int S, int P, int Gr,
+                  const double* x, const double* w, const double* b, double* y)
+{
+    int OH = (H + 2 * P - K) / S + 1, OW = (W + 2 * P - K) / S + 1;
+    int cg = C / Gr, og = OC / Gr;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int o = 0; o < OC; o++) {
+            int grp = o / og;
+            for (int i = 0; i < OH; i++)
+                for (int j = 0; j < OW; j++) {
+                    double acc = b ? b[o] : 0.0;
+                    for (int cc = 0; cc < cg; cc++)
+                        for (int u = 0; u < K; u++) {
+                            int hi = i * S - P + u;
+                            if (hi < 0 || hi >= H) continue;
+                            for (int v = 0; v < K; v++) {
+                                int wi = j * S - P + v;
+                                if (wi < 0 || wi >= W) continue;
+                                acc += w[(((long)o * cg + cc) * K + u) * K + v] *
+                                       x[(((long)n * C + grp * cg + cc) * H + hi) * W + wi];
+                            }
+                        }
+                    y[(((long)n * OC + o) * OH + i) * OW + j] = acc;
+                }
+        }
+}
+
+/* Gradients of the convolution: dW = sum over samples and output positions of dy times the
+ * input patch, db = sum of dy, dx = adjoint of the forward index map (dx may be NULL). */
+void orc_conv_bwd(int N, int C, int H, int W, int OC, int K, int S, int P, int Gr,
+                  const double* x, const double* w, const double* dy, double* dx, double* dw,
+                  double* db)
+{
+    int OH = (H + 2 * P - K) / S + 1, OW = (W + 2 * P - K) / S + 1;
+    int cg = C / Gr, og = OC / Gr;
+#pragma omp parallel for schedule(static)
+    for (int o = 0; o < OC; o++) {
+        int grp = o / og;
+        double sb = 0.0;
+        for (int n = 0; n < N; n++)
+            for (int i = 0; i < OH; i++)
+                for (int j = 0; j < OW; j++) sb += dy[(((long)n * OC + o) * OH + i) * OW + j];
+        if (db) db[o] = sb;
+        for (int cc = 0; cc < cg; cc++)
+            for (int u = 0; u < K; u++)
+                for (int v = 0; v < K; v++) {
+                    double acc = 0.0;
+                    for (int n = 0; n < N; n++)
+                        for (int i = 0; i < OH; i++) {
+                            int hi = i * S - P + u;
+                            if (hi < 0 || hi >= H) continue;
+                            for (int j = 0; j < OW; j++) {
+                                int wi = j * S - P + v;
+                                if (wi < 0 || wi >= W) continue;
+                                acc += dy[(((long)n * OC + o) * OH + i) * OW + j] *
+                                       x[(((long)n * C + grp * cg + cc) * H + hi) * W + wi];
+                            }
+                        }
+                    dw[(((long)o * cg + cc) * K + u) * K + v] = acc;
+                }
+    }
+    if (!dx) return;
+#pragma omp parallel for schedule(static)
+    for (int n = 0; n < N; n++) {
+        double* dxn = dx + (long)n * C * H * W;
+        for (long t = 0; t < (long)C * H * W; t++) dxn[t] = 0.0;
+        for (int o = 0; o < OC; o++) {
+            int grp = o / og;
+            for (int i = 0; i < OH; i++)
+                for (int j = 0; j < OW; j++) {
+                    double g = dy[(((long)n * OC + o) * OH + i) * OW + j];
+                    for (int cc = 0; cc < cg; cc++)
+                        for (int u = 0; u < K; u++) {
+                            int hi = i * S - P + u;
+                            if (hi < 0 || hi >= H) continue;
+                            for (int v = 0; v < K; v++) {
+                                int wi = j * S - P + v;
+                                if (wi < 0 || wi >= W) continue;
+                                dxn[((long)(grp * cg + cc) * H + hi) * W + wi] +=
+                                    g * w[(((long)o * cg + cc) * K + u) * K + v];
+                            }
+                        }
+                }
+        }
+    }
+}
+
+/* Fully connected: y[n][o] = b[o] + sum_i W[o][i] x[n][i], W stored [out][in]. */
+void orc_fc_fwd(int N, int IN, int OUT, const double* x, const double* w, const double* b,
+                double* y)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int o = 0; o < OUT; o++) {
+            double acc = b ? b[o] : 0.0;
+            for (int i = 0; i < IN; i++) acc += w[(long)o * IN + i] * x[(long)n * IN + i];
+            y[(long)n * OUT + o] = acc;
+        }
+}
+
+/* dW[o][i] = sum_n dy[n][o] x[n][i]; db[o] = sum_n dy[n][o]; dx[n][i] = sum_o dy[n][o] W[o][i]. */
+void orc_fc_bwd(int N, int IN, int OUT, const double* x, const double* w, const double* dy,
+                double* dx, double* dw, double* db)
+{
+#pragma omp parallel for schedule(static)
+    for (int o = 0; o < OUT; o++) {
+        double sb = 0.0;
+        for (int n = 0; n < N; n++) sb += dy[(long)n * OUT + o];
+        if (db) db[o] = sb;
+        for (int i = 0; i < IN; i++) {
+            double acc = 0.0;
+            for (int n = 0; n < N; n++) acc += dy[(long)n * OUT + o] * x[(long)n * IN + i];
+            dw[(long)o * IN + i] = acc;
+        }
+    }
+    if (!dx) return;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int i = 0; i < IN; i++) {
+            double acc = 0.0;
+            for (int o = 0; o < OUT; o++) acc += dy[(long)n * OUT + o] * w[(long)o * IN + i];
+            dx[(long)n * IN + i] = acc;
+        }
+}
+
+/* Max-pooling over valid K x K windows with stride S.  argmax = u*K + v of the first maximal
+ * element in row-major window order (strict '>' keeps the earliest). */
+void orc_maxpool_fwd(int N, int C, int H, int W, int K, int S, const double* x, double* y,
+                     int32_t* argmax)
+{
+    int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int c = 0; c < C; c++)
+            for (int i = 0; i < OH; i++)
+                for (int j = 0; j < OW; j++) {
+                    const double* xp = x + ((long)n * C + c) * H * W;
+                    double best = xp[(long)(i * S) * W + j * S];
+                    int bi = 0;
+                    for (int u = 0; u < K; u++)
+                        for (int v = 0; v < K; v++) {
+                            double t = xp[(long)(i * S + u) * W + j * S + v];
+                            if (t > best) { best = t; bi = u * K + v; }
+                        }
+                    long o = (((long)n * C + c) * OH + i) * OW + j;
+                    y[o] = best;
+                    argmax[o] = bi;
+                }
+}
+
+/* dx[argmax position] += dy (windows may overlap when S < K). */
+void orc_maxpool_bwd(int N, int C, int H, int W, int K, int S, const int32_t* argmax,
+                     const double* dy, double* dx)
+{
+    int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int c = 0; c < C; c++) {
+            double* dxp = dx + ((long)n * C + c) * H * W;
+            for (long t = 0; t < (long)H * W; t++) dxp[t] = 0.0;
+            for (int i = 0; i < OH; i++)
+                for (int j = 0; j < OW; j++) {
+                    long o = (((long)n * C + c) * OH + i) * OW + j;
+                    int u = argmax[o] / K, v = argmax[o] % K;
+                    dxp[(long)(i * S + u) * W + j * S + v] += dy[o];
+                }
+        }
+}
+
+/* Softmax cross-entropy per sample: loss[n] = logsumexp(z[n]) - z[n][y[n]];
+ * dz[n][c] = (softmax(z[n])[c] - [c == y[n]]) * scale.  logsumexp subtracts the row maximum. */
+void orc_softmax_xent(int N, int NC, const double* z, const int32_t* y, double scale,
+                      double* loss, double* dz)
+{
+    for (int n = 0; n < N; n++) {
+        const double* zn = z + (long)n * NC;
+        double m = zn[0];
+        for (int c = 1; c < NC; c++)
+            if (zn[c] > m) m = zn[c];
+        double s = 0.0;
+        for (int c = 0; c < NC; c++) s += exp(zn[c] - m);
+        double lse = m + log(s);
+        int yn = y[n];
+        loss[n] = (yn >= 0 && yn < NC) ? lse - zn[yn] : NAN;
+        if (dz)
+            for (int c = 0; c < NC; c++)
+                dz[(long)n * NC + c] = (exp(zn[c] - lse) - (c == yn ? 1.0 : 0.0)) * scale;
+    }
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* weight initialisation                                                                      */
+/* ------------------------------------------------------------------------------------------ */
+
+/* First output of a SplitMix64 generator whose state is `key` (Steele, Lea & Flood, OOPSLA 2014;
+ * constants of Vigna's public-domain splitmix64.c). */
+static uint64_t splitmix64_first(uint64_t key)
+{
+    uint64_t z = key + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+int orc_init_glorot(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L,
+                    uint64_t seed, float* w)
+{
+    orc_geom* G = (orc_geom*)calloc((size_t)n_layers, sizeof(orc_geom));
+    long P;
+    if (!G) return ORC_ENOMEM;
+    int rc = orc_plan(in_c, in_h, in_w, n_layers, L, G, &P);
+    if (rc) { free(G); return rc; }
+    for (int l = 0; l < n_layers; l++) {
+        orc_geom* g = &G[l];
+        if (g->kind == ORC_MAXPOOL) continue;
+        double fan_in, fan_out;
+        if (g->kind == ORC_CONV) {
+            fan_in = (double)(g->c / g->g) * g->k * g->k;
+            fan_out = (double)g->oc * g->k * g->k;
+        } else {
+            fan_in = (double)g->c * g->h * g->w;
+            fan_out = (double)g->oc;
+        }
+        double a = sqrt(6.0 / (fan_in + fan_out));
+        for (long i = 0; i < g->w_len; i++) {
+            uint64_t hsh = splitmix64_first(seed ^ (((uint64_t)l << 32) | (uint64_t)i));
+            double u = (double)(hsh >> 40) / 16777216.0;
+            w[g->w_off + i] = (float)(a * (2.0 * u - 1.0));
+        }
+        for (long i = 0; i < g->b_len; i++) w[g->b_off + i] = 0.0f;
+    }
+    free(G);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* the training step                                                                           */
+/* ------------------------------------------------------------------------------------------ */
+
+static long act_size(const orc_geom* g) { return (long)g->oc * g->oh * g->ow; }
+
+/* gamma(n) of the standard floating-point summation error bound for unit roundoff 2^-24. */
+static double gamma_f32(long n)
+{
+    double nu = (double)n * ldexp(1.0, -24);
+    return nu / (1.0 - nu);
+}
+
+static void layer_fwd(const orc_geom* g, int N, const double* a, const double* w, const double* b,
+                      double* z)
+{
+    if (g->kind == ORC_CONV)
+        orc_conv_fwd(N, g->c, g->h, g->w, g->oc, g->k, g->s, g->p, g->g, a, w, b, z);
+    else
+        orc_fc_fwd(N, g->c * g->h * g->w, g->oc, a, w, b, z);
+}
+
+/* One synchronous data-parallel SGD/momentum step.  See the file header for the method.
+ *   x [R*Nb][C][H][W], labels [R*Nb], w and v [P] (v may be NULL iff mu == 0).
+ *   Outputs: loss (mean over the batch), optional per-shard losses, optional per-shard gradients
+ *   grads[r*P + i], the averaged gradient gavg [P], optional updated w_new / v_new, optional
+ *   stored activations of every layer for the whole batch (concatenated in layer order), the
+ *   max-pool decisions (int32 window index, concatenated over pool layers) and the ReLU
+ *   decisions (int8, concatenated over ReLU layers).
+ *   pool_hint / relu_hint (optional, same layout, -1 = no hint) replace a decision by another one
+ *   only where the oracle's own rounding-error bound for a float computation of the forward pass
+ *   admits both; any other hint makes the call fail with ORC_EHINT. */
+int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, int R, int Nb,
+                   int prec, const float* x, const int32_t* labels, const float* w,
+                   const float* v, float lr, float mu, const int32_t* pool_hint,
+                   const int8_t* relu_hint, double* loss_out, float* shard_loss, float* grads,
+                   float* gavg, float* w_new, float* v_new, float* acts, int32_t* pool_argmax,
+                   int8_t* relu_mask)
+{
+    if (R < 1 || Nb < 1 || !x || !labels || !w || !gavg || (!v && mu != 0.0f)) return ORC_EINVAL;
+    orc_geom* G = (orc_geom*)calloc((size_t)n_layers, sizeof(orc_geom));
+    if (!G) return ORC_ENOMEM;
+    long P;
+    int rc = orc_plan(in_c, in_h, in_w, n_layers, L, G, &P);
+    if (rc) { free(G); return rc; }
+    const int B = R * Nb;
+    const long in_sz = (long)in_c * in_h * in_w;
+    const int track = (pool_hint || relu_hint) ? 1 : 0; /* error bounds needed for hints */
+    if (prec < ORC_PREC_F32 || prec > ORC_PREC_EXACT) { free(G); return ORC_EINVAL; }
+    const int bf16 = (prec == ORC_PREC_BF16);
+    /* storage rounding of activations and data-gradients; final-layer outputs use `store32` */
+    double (*store)(double) = bf16 ? rnd_bf16 : (prec == ORC_PREC_EXACT ? rnd_none : rnd_f32);
+    double (*store32)(double) = (prec == ORC_PREC_EXACT) ? rnd_none : rnd_f32;
+
+    /* per-layer offsets of the concatenated whole-batch output arrays */
+    long* act_off = (long*)calloc((size_t)n_layers + 1, sizeof(long));
+    long* pool_off = (long*)calloc((size_t)n_layers + 1, sizeof(long));
+    long* relu_off = (long*)calloc((size_t)n_layers + 1, sizeof(long));
+    double* wq = (double*)malloc(sizeof(double) * (size_t)P);
+    double* wabs = track ? (double*)malloc(sizeof(double) * (size_t)P) : NULL;
+    double* gsum = (double*)calloc((size_t)P, sizeof(double));
+    double** a = (double**)calloc((size_t)n_layers + 1, sizeof(double*));  /* stored outputs */
+    double** e = (double**)calloc((size_t)n_layers + 1, sizeof(double*));  /* error bounds */
+    double** z = (double**)calloc((size_t)n_layers, sizeof(double*));      /* pre-activations */
+    int32_t** am = (int32_t**)calloc((size_t)n_layers, sizeof(int32_t*));  /* pool argmax */
+    double* lossn = (double*)malloc(sizeof(double) * (size_t)Nb);
+    double* dbuf = NULL;
+    double* dbuf2 = NULL;
+    double* gw = (double*)malloc(sizeof(double) * (size_t)P);
+    if (!act_off || !pool_off || !relu_off || !wq || (track && !wabs) || !gsum || !a || !e || !z ||
+        !am || !lossn || !gw) {
+        rc = ORC_ENOMEM;
+        goto done;
+    }
+    {
+        long ao = 0, po = 0, ro = 0, maxact = in_sz;
+        for (int l = 0; l < n_layers; l++) {
+            act_off[l] = ao; ao += act_size(&G[l]) * B;
+            pool_off[l] = po; if (G[l].kind == ORC_MAXPOOL) po += act_size(&G[l]) * B;
+            relu_off[l] = ro; if (G[l].relu) ro += act_size(&G[l]) * B;
+            if (act_size(&G[l]) > maxact) maxact = act_size(&G[l]);
+        }
+        a[0] = (double*)malloc(sizeof(double) * (size_t)(in_sz * Nb));
+        e[0] = (double*)calloc((size_t)(in_sz * Nb), sizeof(double));
+        for (int l = 0; l < n_layers; l++) {
+            long sz = act_size(&G[l]) * Nb;
+            a[l + 1] = (double*)malloc(sizeof(double) * (size_t)sz);
+            z[l] = (double*)malloc(sizeof(double) * (size_t)sz);
+            if (track) e[l + 1] = (double*)calloc((size_t)sz, sizeof(double));
+            if (G[l].kind == ORC_MAXPOOL) am[l] = (int32_t*)malloc(sizeof(int32_t) * (size_t)sz);
+            if (!a[l + 1] || !z[l] || (track && !e[l + 1]) ||
+                (G[l].kind == ORC_MAXPOOL && !am[l])) {
+                rc = ORC_ENOMEM;
+                goto done;
+            }
+        }
+        dbuf = (double*)malloc(sizeof(double) * (size_t)(maxact * Nb));
+        dbuf2 = (double*)malloc(sizeof(double) * (size_t)(maxact * Nb));
+        if (!a[0] || !e[0] || !dbuf || !dbuf2) { rc = ORC_ENOMEM; goto done; }
+    }
+
+    /* weights as the layers use them: the float master weights, or their bfloat16 rounding */
+    for (long i = 0; i < P; i++) {
+        wq[i] = bf16 ? rnd_bf16((double)w[i]) : (double)w[i];
+        if (track) wabs[i] = fabs(wq[i]);
+    }
+    /* biases are added in float by both sides; they are never rounded to bfloat16 */
+    for (int l = 0; l < n_layers; l++)
+        for (long i = 0; i < G[l].b_len; i++) {
+            wq[G[l].b_off + i] = (double)w[G[l].b_off + i];
+            if (track) wabs[G[l].b_off + i] = fabs((double)w[G[l].b_off + i]);
+        }
+
+    double loss_total = 0.0;
+    for (int r = 0; r < R; r++) {
+        /* ---- forward on shard r (rows r*Nb .. r*Nb+Nb-1 of the batch) ---- */
+        for (long t = 0; t < in_sz * Nb; t++) a[0][t] = store((double)x[(long)r * Nb * in_sz + t]);
+        for (int l = 0; l < n_layers; l++) {
+            const orc_geom* g = &G[l];
+            long sz = act_size(g) * Nb;
+            const int last = (l == n_layers - 1);
+            if (g->kind == ORC_MAXPOOL) {
+                orc_maxpool_fwd(Nb, g->c, g->h, g->w, g->k, g->s, a[l], a[l + 1], am[l]);
+                if (track)
+                    for (long t = 0; t < sz; t++) {
+                        /* bound of a window maximum: the largest bound inside the window */
+                        long per = (long)g->oh * g->ow;
+                        long nc = t / per, ij = t % per;
+                        int i = (int)(ij / g->ow), j = (int)(ij % g->ow);
+                        double m = 0.0;
+                        for (int u = 0; u < g->k; u++)
+                            for (int vv = 0; vv < g->k; vv++) {
+                                double ev = e[l][nc * g->h * g->w + (long)(i * g->s + u) * g->w +
+                                                 j * g->s + vv];
+                                if (ev > m) m = ev;
+                            }
+                        e[l + 1][t] = m;
+                    }
+                if (pool_hint) {
+                    const int32_t* hint = pool_hint + pool_off[l] + (long)r * sz;
+                    long per = (long)g->oh * g->ow;
+                    for (long t = 0; t < sz; t++) {
+                        int hv = hint[t];
+                        if (hv < 0 || hv == am[l][t]) continue;
+                        if (hv >= g->k * g->k) { rc = ORC_EHINT; goto done; }
+                        long nc = t / per, ij = t % per;
+                        int i = (int)(ij / g->ow), j = (int)(ij % g->ow);
+                        int own = am[l][t];
+                        long base = nc * g->h * g->w + (long)(i * g->s) * g->w + j * g->s;
+                        long po = base + (long)(own / g->k) * g->w + own % g->k;
+                        long ph = base + (long)(hv / g->k) * g->w + hv % g->k;
+                        if (a[l][po] - a[l][ph] > e[l][po] + e[l][ph]) { rc = ORC_EHINT; goto done; }
+                        am[l][t] = hv;
+                        a[l + 1][t] = a[l][ph];
+                    }
+                }
+            } else {
+                layer_fwd(g, Nb, a[l], wq + g->w_off, wq + g->b_off, z[l]);
+                if (track) {
+                    /* forward error bound of a float evaluation in any summation order:
+                     * gamma(2(K+1)) * sum|w||a| + sum|w| e_in, then the storage rounding */
+                    long Kacc = (g->kind == ORC_CONV) ? (long)(g->c / g->g) * g->k * g->k
+                                                      : (long)g->c * g->h * g->w;
+                    double gam = gamma_f32(2 * (Kacc + 1));
+                    double* absa = dbuf;
+                    long insz = (long)g->c * g->h * g->w * Nb;
+                    for (long t = 0; t < insz; t++) absa[t] = fabs(a[l][t]);
+                    layer_fwd(g, Nb, absa, wabs + g->w_off, wabs + g->b_off, e[l + 1]);
+                    layer_fwd(g, Nb, e[l], wabs + g->w_off, NULL, dbuf2);
+                    double us = ldexp(1.0, -24) + (bf16 && !last ? ldexp(1.0, -8) : ldexp(1.0, -24));
+                    for (long t = 0; t < sz; t++) {
+                        double ez = gam * e[l + 1][t] + dbuf2[t];
+                        e[l + 1][t] = ez + 2.0 * us * (fabs(z[l][t]) + ez);
+                        dbuf2[t] = ez;     /* bound of the pre-activation itself */
+                    }
+                }
+                for (long t = 0; t < sz; t++) {
+                    double zt = z[l][t];
+                    int pass = 1;
+                    if (g->relu) {
+                        pass = zt > 0.0;
+                        if (relu_hint) {
+                            int8_t hv = relu_hint[relu_off[l] + (long)r * sz + t];
+                            if (hv >= 0 && hv != pass) {
+                                if (fabs(zt) > dbuf2[t]) { rc = ORC_EHINT; goto done; }
+                                pass = hv;
+                            }
+                        }
+                    }
+                    double out = pass ? zt : 0.0;
+                    a[l + 1][t] = last ? store32(out) : store(out);
+                    /* a hinted pass of a non-positive value stores a tiny value; keep the mask */
+                    if (g->relu) z[l][t] = pass ? 1.0 : 0.0;
+                }
+            }
+            /* export stored outputs and decisions of this shard */
+            if (acts)
+                for (long t = 0; t < sz; t++)
+                    acts[act_off[l] + (long)r * sz + t] = (float)a[l + 1][t];
+            if (pool_argmax && g->kind == ORC_MAXPOOL)
+                for (long t = 0; t < sz; t++) pool_argmax[pool_off[l] + (long)r * sz + t] = am[l][t];
+            if (relu_mask && g->relu)
+                for (long t = 0; t < sz; t++)
+                    relu_mask[relu_off[l] + (long)r * sz + t] = (int8_t)(z[l][t] > 0.0);
+        }
+
+        /* ---- loss: mean over the shard; gradient of the shard-mean loss ---- */
+        const orc_geom* gl = &G[n_layers - 1];
+        int NC = gl->oc;
+        double* dcur = dbuf;
+        orc_softmax_xent(Nb, NC, a[n_layers], labels + (long)r * Nb, 1.0 / Nb, lossn, dcur);
+        double ls = 0.0;
+        for (int n = 0; n < Nb; n++) ls += lossn[n];
+        ls /= Nb;
+        if (shard_loss) shard_loss[r] = (float)ls;
+        loss_total += ls;
+        for (long t = 0; t < (long)Nb * NC; t++) dcur[t] = store(dcur[t]);
+
+        /* ---- backward in reverse layer order ---- */
+        for (int l = n_layers - 1; l >= 0; l--) {
+            const orc_geom* g = &G[l];
+            long sz = act_size(g) * Nb;
+            long insz = (long)g->c * g->h * g->w * Nb;
+            double* dnext = (dcur == dbuf) ? dbuf2 : dbuf;
+            if (g->relu)
+                for (long t = 0; t < sz; t++)
+                    if (z[l][t] <= 0.0) dcur[t] = 0.0;
+            if (g->kind == ORC_MAXPOOL) {
+                orc_maxpool_bwd(Nb, g->c, g->h, g->w, g->k, g->s, am[l], dcur, dnext);
+                for (long t = 0; t < insz; t++) dnext[t] = store(dnext[t]);
+            } else {
+                double* dx = (l > 0) ? dnext : NULL;
+                if (g->kind == ORC_CONV)
+                    orc_conv_bwd(Nb, g->c, g->h, g->w, g->oc, g->k, g->s, g->p, g->g, a[l],
+                                 wq + g->w_off, dcur, dx, gw + g->w_off, gw + g->b_off);
+                else
+                    orc_fc_bwd(Nb, g->c * g->h * g->w, g->oc, a[l], wq + g->w_off, dcur, dx,
+                               gw + g->w_off, gw + g->b_off);
+                if (dx)
+                    for (long t = 0; t < insz; t++) dx[t] = store(dx[t]);
+                for (long i = 0; i < g->w_len + g->b_len; i++) {
+                    float gf = (float)gw[g->w_off + i];
+                    if (grads) grads[(long)r * P + g->w_off + i] = gf;
+                    gsum[g->w_off + i] += (double)gf;
+                }
+            }
+            dcur = dnext;
+        }
+    }
+
+    /* ---- average of the R replica gradients (the all-reduce of Sec. III-D.2) ---- */
+    for (long i = 0; i < P; i++) gavg[i] = (float)(gsum[i] / R);
+    /* ---- momentum / SGD update ---- */
+    for (long i = 0; i < P; i++) {
+        double gi = (double)gavg[i];
+        if (mu != 0.0f) {
+            double vn = (double)(float)((double)mu * (double)v[i] + gi);
+            if (v_new) v_new[i] = (float)vn;
+            if (w_new) w_new[i] = (float)((double)w[i] - (double)lr * vn);
+        } else {
+            if (v_new) v_new[i] = v ? v[i] : 0.0f;
+            if (w_new) w_new[i] = (float)((double)w[i] - (double)lr * gi);
+        }
+    }
+    if (loss_out) *loss_out = loss_total / R;
+    rc = ORC_OK;
+
+done:
+    if (a) for (int l = 0; l <= n_layers; l++) free(a[l]);
+    if (e) for (int l = 0; l <= n_layers; l++) free(e[l]);
+    if (z) for (int l = 0; l < n_layers; l++) free(z[l]);
+    if (am) for (int l = 0; l < n_layers; l++) free(am[l]);
+    free(a); free(e); free(z); free(am);
+    free(act_off); free(pool_off); free(relu_off);
+    free(wq); free(wabs); free(gsum); free(lossn); free(dbuf); free(dbuf2); free(gw); free(G);
+    return rc;
+}
+
+/* Average of R gradient buffers (row stride ld) fused with the momentum update, as the last two
+ * stages of the step above.  Exposed on its own for the gradient-average microbenchmark.
+ * v / v_new may be NULL iff mu == 0; gavg and w_new may be NULL. */
+int orc_average_update(const float* grads, int R, long n, long ld, float* w, float* v, float lr,
+                       float mu, float* gavg)
+{
+    if (!grads || R < 1 || n < 1 || ld < n || (!v && mu != 0.0f)) return ORC_EINVAL;
+    for (long i = 0; i < n; i++) {
+        double s = 0.0;
+        for (int r = 0; r < R; r++) s += (double)grads[(long)r * ld + i];
+        float gi = (float)(s / R);
+        if (gavg) gavg[i] = gi;
+        if (!w) continue;
+        if (mu != 0.0f) {
+            double vn = (double)(float)((double)mu * (double)v[i] + (double)gi);
+            v[i] = (float)vn;
+            w[i] = (float)((double)w[i] - (double)lr * vn);
+        } else {
+            w[i] = (float)((double)w[i] - (double)lr * (double)gi);
+        }
+    }
+    return ORC_OK;
+}

@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of one rank's synchronous data-parallel SGD step on one MI355X.
+
+A step is one mtx_train_step over one batch: forward and backward of every shard, the average
+of the R shard gradients and the momentum update.  Inputs are seeded synthetic tensors already
+resident in HBM when the timed region starts.
+
+    python bench.py [--steps K] [--warmup W] [--workload lenet|mlp|cifar|alexnet]
+                    [--no-cpu-baseline] [--no-microbench]
+
+Prints one JSON line.  `value` is samples/s of the whole job (one GPU); `roofline` covers the
+kernel that takes the most time in the step, timed in place with HIP events on the step's
+stream; `grad_avg_update` is the fused average + momentum kernel at the 61M-element, 16-buffer
+size; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"hbm_GBps": 8000.0, "f32_TFLOPs": 157.3, "bf16_TFLOPs": 2500.0}
+METRIC = "train samples/sec per GPU; grad-avg+update GB/s and conv/GEMM MFMA % of peak"
+
+
+def geometry(net):
+    """Per-layer shapes (the same definitions as the library's plan)."""
+    from paper_1704_04560_amd import workloads as wl
+    c, h, w = net.in_shape
+    out = []
+    for l in net.layers:
+        if l.kind == wl.CONV:
+            oc, oh, ow = l.out, (h + 2 * l.pad - l.k) // l.stride + 1, (w + 2 * l.pad - l.k) // l.stride + 1
+        elif l.kind == wl.FC:
+            oc, oh, ow = l.out, 1, 1
+        else:
+            oc, oh, ow = c, (h - l.k) // l.stride + 1, (w - l.k) // l.stride + 1
+        out.append(dict(layer=l, c=c, h=h, w=w, oc=oc, oh=oh, ow=ow))
+        c, h, w = oc, oh, ow
+    return out
+
+
+def site_work(name, layer, geo, wkl, es):
+    """Algorithmic work of one launch of a step's launch site: ("mfma", flops) for the matrix
+    kernels (2 x multiply-adds of the convolution / product), ("hbm", bytes) for the others
+    (each tensor read once and written once)."""
+    from paper_1704_04560_amd import workloads as wl
+    B, R, Nb = wkl.batch, wkl.shards, wkl.shard_batch
+    if layer >= 0:
+        g = geo[layer]
+        l = g["layer"]
+        if l.kind == wl.CONV:
+            macs = B * g["oh"] * g["ow"] * g["oc"] * (g["c"] // l.groups) * l.k * l.k
+        else:
+            macs = B * g["c"] * g["h"] * g["w"] * g["oc"]
+        in_sz = B * g["c"] * g["h"] * g["w"]
+        out_sz = B * g["oc"] * g["oh"] * g["ow"]
+        if name in ("fwd", "dgrad", "wgrad"):
+            return "mfma", 2.0 * macs
+        if name == "bias_grad":
+            return "hbm", out_sz * es + R * g["oc"] * 4
+        if name == "pool_fwd":
+            return "hbm", in_sz * es + out_sz * (es + 1)
+        if name == "pool_bwd":
+            return "hbm", out_sz * (es + 1) + in_sz * es * 2  # dy + argmax, mask + dx
+    P = wkl_params(wkl)
+    if name == "avg_update":
+        mom = wkl.momentum != 0.0
+        return "hbm", (R + (5 if mom else 3)) * 4 * P
+    if name == "cast_w":
+        return "hbm", 6 * P
+    if name == "cast_x":
+        c, h, w = wkl.net.in_shape
+        return "hbm", 6 * B * c * h * w
+    if name == "softmax_xent":
+        nc = wkl.net.num_classes
+        return "hbm", B * nc * (4 + es) + B * 8
+    if name == "mean_loss":
+        return "hbm", B * 4 + 4
+    return "hbm", 0.0
+
+
+_P = {}
+
+
+def wkl_params(wkl):
+    key = wkl.net.name
+    if key not in _P:
+        from paper_1704_04560_amd import mtx
+        from paper_1704_04560_amd import workloads as wl
+        d = mtx.make_desc(wkl.net.in_shape, wl.layer_tuples(wkl.net), wkl.net.dtype)
+        _P[key] = mtx.mtx_model_sizes(d, wkl.shards, wkl.shard_batch)[0]
+    return _P[key]
+
+
+def microbench_avg_update(torch, mtx, reps=20):
+    """Fused average + momentum update over R=16 buffers of 61,000,000 fp32 elements."""
+    R, n = 16, 61_000_000
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    grads = torch.randn(R * n, device="cuda", generator=gen) * 1e-3
+    w = torch.randn(n, device="cuda", generator=gen) * 0.05
+    v = torch.randn(n, device="cuda", generator=gen) * 1e-3
+    avg = torch.empty(n, device="cuda")
+    for _ in range(3):
+        mtx.mtx_sgd_update(w, v, grads, R, n, n, 0.01, 0.9, avg)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        mtx.mtx_sgd_update(w, v, grads, R, n, n, 0.01, 0.9, avg)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    nbytes = (R + 5) * 4 * n
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    del grads, w, v, avg
+    torch.cuda.empty_cache()
+    return {"R": R, "n": n, "bytes_per_call": nbytes, "ms": round(ms, 4),
+            "GBps": round(gbps, 1), "peak_GBps": PEAK["hbm_GBps"],
+            "frac": round(gbps / PEAK["hbm_GBps"], 4)}
+
+
+def cpu_baseline(wkl, budget_s=12.0):
+    """The CPU oracle on a bounded sample of the workload: whole steps (R shards of a reduced
+    shard batch) repeated until `budget_s` seconds have passed; samples/s over the sample."""
+    from oracle import oracle as orc
+    from paper_1704_04560_amd import workloads as wl
+    net = wkl.net
+    layers = wl.layer_tuples(net)
+    R = wkl.shards
+    nb = {"mlp": 32, "lenet": 16, "cifar": 1, "alexnet": 1}.get(net.name, 1)
+    x, y = wl.make_batch(net, R * nb, seed=0)
+    w = orc.init_glorot(net.in_shape, layers, 0)
+    v = None if wkl.momentum == 0.0 else w * 0
+    prec = "bf16" if net.dtype == wl.BF16 else "f32"
+    t0 = time.perf_counter()
+    steps = 0
+    while True:
+        orc.train_step(net.in_shape, layers, R, x, y, w, v, wkl.lr, wkl.momentum, prec=prec,
+                       want_grads=False)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {"value": round(steps * R * nb / el, 3), "unit": "samples/s",
+            "cores": orc.num_threads(), "kind": "oracle",
+            "sample": f"{steps} oracle steps of {R} shards x {nb} samples ({prec}), {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="lenet")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-microbench", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no cross-GPU path (the all-reduce across "
+              "GPUs is out of scope); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1704_04560_amd import mtx
+    from paper_1704_04560_amd import workloads as wl
+
+    mtx.lib()  # fails loudly if the HIP library is not built
+    wkl = wl.WORKLOADS[args.workload]
+    net = wkl.net
+    layers = wl.layer_tuples(net)
+    model = mtx.Model(net.in_shape, layers, net.dtype, wkl.shards, wkl.shard_batch, seed=0)
+    x, y = wl.make_batch(net, wkl.batch, seed=0)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    loss = torch.zeros(1, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
+    torch.cuda.synchronize()
+
+    mtx.mtx_set_timing(model.handle, True)
+    mtx.mtx_get_timing(model.handle, reset=True)
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / args.steps
+    sites = mtx.mtx_get_timing(model.handle)
+    mtx.mtx_set_timing(model.handle, False)
+    assert torch.isfinite(loss).item(), "non-finite loss"
+
+    es = 2 if net.dtype == wl.BF16 else 4
+    geo = geometry(net)
+    kernels = []
+    for (name, layer, launches, total) in sites:
+        if launches == 0:
+            continue
+        avg_ms = total / launches
+        bound, work = site_work(name, layer, geo, wkl, es)
+        kernels.append(dict(name=name, layer=layer, avg_ms=avg_ms, bound=bound, work=work))
+    kernel_sum = sum(k["avg_ms"] for k in kernels)
+    dom = max(kernels, key=lambda k: k["avg_ms"])
+    if dom["bound"] == "mfma":
+        peak = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
+        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s"}
+    else:
+        peak = PEAK["hbm_GBps"]
+        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": peak, "unit": "GB/s"}
+    roof["frac"] = round(ach / peak, 4)
+    roof["traffic"] = None
+    roof["kernel"] = f"{dom['name']} (layer {dom['layer']})"
+    roof["kernel_ms"] = round(dom["avg_ms"], 5)
+
+    mfma_ms = sum(k["avg_ms"] for k in kernels if k["bound"] == "mfma")
+    mfma_flops = sum(k["work"] for k in kernels if k["bound"] == "mfma")
+    peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
+    au = [k for k in kernels if k["name"] == "avg_update"][0]
+    out = {
+        "metric": METRIC,
+        "value": round(wkl.batch / (ms * 1e-3), 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if net.dtype == wl.BF16 else "f32",
+        "data": "synthetic (seeded; no dataset)",
+        "config": {"workload": wkl.description, "global_batch": wkl.batch, "shards": wkl.shards,
+                   "shard_batch": wkl.shard_batch, "lr": wkl.lr, "momentum": wkl.momentum,
+                   "parallelism": f"{wkl.shards} data-parallel shards on 1 GPU"},
+        "roofline": roof,
+        "gemm_mfma": {"achieved_TFLOPs": round(mfma_flops / (mfma_ms * 1e-3) / 1e12, 3),
+                      "peak_TFLOPs": peak_mm,
+                      "frac": round(mfma_flops / (mfma_ms * 1e-3) / 1e12 / peak_mm, 4)},
+        "step_avg_update": {"GBps": round(au["work"] / (au["avg_ms"] * 1e-3) / 1e9, 1),
+                            "ms": round(au["avg_ms"], 5)},
+        "kernel_ms_sum": round(kernel_sum, 5),
+        "kernels": [{"name": k["name"], "layer": k["layer"], "ms": round(k["avg_ms"], 5)}
+                    for k in kernels],
+    }
+    model.close()
+    del xd, yd
+    if not args.no_microbench:
+        out["grad_avg_update"] = microbench_avg_update(torch, mtx)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wkl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

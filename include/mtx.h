@@ -1,0 +1,192 @@
+/*
+ * mtx.h -- C ABI of the MI355X (gfx950) library for one rank's step of synchronous
+ * data-parallel SGD, after "User-transparent Distributed TensorFlow" (arXiv 1704.04560).
+ *
+ * The paper's method (Sec. III-A, III-D, III-E): every replica holds identical weights
+ * (Broadcast operator, Sec. III-D.1), computes the gradient of its own shard of the batch, the
+ * replicas' gradients are averaged by an all-reduce issued layer by layer in a fixed order
+ * (MPI_Allreduce operator, Sec. III-D.2; Sec. II-B uses the reduction "for averaging
+ * gradients"), and the optimizer step follows, so that the result equals sequential SGD
+ * (Sec. III-D.2, III-E).  The user's training loop stays unchanged (Sec. I problem statement,
+ * Sec. III-D, Fig. 3): here one mtx_train_step call on the whole batch hides the R replicas.
+ *
+ * On one GPU the R replicas are R shards of the batch processed against one shared weight
+ * copy; their gradients land in R separate buffers and are averaged on the device (the local
+ * half of the all-reduce), fused with the momentum update.
+ *
+ * Conventions for every call:
+ *   - Tensor pointers are DEVICE pointers unless the name ends in _host.  The caller owns all
+ *     device memory and the stream; the library never allocates device memory.  A model
+ *     handle owns only host-side metadata.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued asynchronously;
+ *     only the calls documented as synchronous wait for the stream.
+ *   - Every call returns an mtx_status.  Arguments are validated before anything is enqueued;
+ *     an invalid argument returns MTX_EINVAL (or MTX_EUNSUPPORTED) and changes nothing.  A HIP
+ *     launch or copy failure returns MTX_EHIP.  mtx_last_error() gives a message for the last
+ *     non-OK status of the calling thread.
+ *   - Floating-point tensors are fp32 unless stated.  Layouts are logical, row-major:
+ *     activations NCHW; fully connected weights W[out][in]; convolution weights
+ *     W[out][in/groups][k][k]; the input of a fully connected layer that follows a
+ *     convolution or pooling layer is the (c, h, w) flattening of that layer's output.
+ *   - The flat parameter vector holds the layers in forward order, each layer's W followed by
+ *     its bias b (the paper's ordered list of per-layer reductions, Sec. III-D.2).
+ *   - A model handle must not be used from two threads, or on two streams, at once.
+ */
+#ifndef MTX_H
+#define MTX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MTX_OK = 0,
+    MTX_EINVAL = -1,       /* invalid argument (null pointer, bad size, misaligned pointer) */
+    MTX_ENOMEM = -2,       /* host allocation failed, or a caller buffer is too small */
+    MTX_EHIP = -3,         /* a HIP runtime call failed */
+    MTX_EUNSUPPORTED = -4  /* a valid network the library does not implement */
+} mtx_status;
+
+typedef enum { MTX_F32 = 0, MTX_BF16 = 1 } mtx_dtype;
+
+typedef enum { MTX_FC = 0, MTX_CONV = 1, MTX_MAXPOOL = 2 } mtx_kind;
+
+/* One layer (Sec. I and Fig. 1: fully connected and convolution layers; pooling between
+ * convolutions).
+ *   MTX_FC:      out = number of outputs; relu = apply max(0, .) to the output.
+ *   MTX_CONV:    out = output channels, k x k kernel, stride >= 1, zero padding pad >= 0,
+ *                groups >= 1 dividing both channel counts; relu as above.
+ *   MTX_MAXPOOL: k x k window (k <= 16), stride >= 1, no padding ("valid" windows); out,
+ *                pad, groups and relu must be 0 (groups may also be 1).
+ * The last layer must be MTX_FC without ReLU; its outputs are the class scores of a softmax
+ * cross-entropy loss. */
+typedef struct {
+    int kind, out, k, stride, pad, groups, relu;
+} mtx_layer;
+
+typedef struct {
+    int in_c, in_h, in_w;     /* per-sample input shape */
+    int n_layers;
+    const mtx_layer* layers;  /* read during mtx_model_sizes / mtx_init_model only */
+    int compute;              /* mtx_dtype: MTX_F32, or MTX_BF16 = bfloat16 operands with fp32
+                                 accumulation and fp32 master weights */
+} mtx_model_desc;
+
+typedef struct {
+    size_t n_params;         /* P: length of the flat parameter vector */
+    size_t grad_stride;      /* elements between the R shard gradient buffers (>= P) */
+    size_t workspace_bytes;  /* device workspace mtx_init_model needs */
+} mtx_sizes;
+
+/* Device buffers of a model, all owned by the caller and 256-byte aligned:
+ *   w        [P]                  fp32 master weights (updated in place by mtx_train_step)
+ *   v        [P]                  fp32 momentum velocity (updated in place)
+ *   grads    [R][grad_stride]     per-shard gradients, written by every mtx_train_step
+ *   grad_avg [P]                  averaged gradient, written by every mtx_train_step
+ *   workspace, workspace_bytes    scratch for activations, decisions and partial sums
+ * The buffers must not overlap and must stay valid until mtx_free_model. */
+typedef struct {
+    float* w;
+    float* v;
+    float* grads;
+    float* grad_avg;
+    void* workspace;
+    size_t workspace_bytes;
+} mtx_buffers;
+
+typedef struct mtx_model mtx_model;
+
+/* Sizes for a network trained on R shards of shard_batch samples each (global batch
+ * B = R * shard_batch; strong scaling, Sec. IV-B).  Host only, enqueues nothing. */
+int mtx_model_sizes(const mtx_model_desc* desc, int R, int shard_batch, mtx_sizes* out);
+
+/* Create a model handle bound to `bufs`, and initialise the replicas identically (the
+ * Broadcast operator of Sec. III-D.1 -- on one GPU the R replicas share one weight vector):
+ * every weight tensor W is drawn Glorot-uniform U(-a, a), a = sqrt(6 / (fan_in + fan_out))
+ * (fully connected: fan_in = in, fan_out = out; convolution: fan_in = in/groups * k * k,
+ * fan_out = out * k * k), from the counter-based generator
+ *   h = SplitMix64 first output for state (seed XOR ((layer_index << 32) | element_index)),
+ *   u = (h >> 40) / 2^24,  value = (float)(a * (2u - 1)) evaluated in double,
+ * every bias is 0 and the velocity v is 0.  The copies are enqueued on `stream`; the call
+ * synchronises with `stream` before it returns.  On success *out receives the handle. */
+int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                   const mtx_buffers* bufs, void* stream, mtx_model** out);
+
+/* One synchronous data-parallel SGD step on the whole batch (Sec. III-D.2, III-E):
+ *   x [B][in_c][in_h][in_w] fp32 images, labels [B] int32 in [0, num_classes); shard r is
+ *   rows r*shard_batch .. (r+1)*shard_batch-1.
+ *   For each shard: forward pass, softmax cross-entropy loss averaged over the shard, and the
+ *   gradient of that loss into grads[r] (layer order, W then b).  Then
+ *     grad_avg = (1/R) sum_r grads[r];  v = momentum*v + grad_avg;  w = w - lr*v
+ *   (momentum == 0: w = w - lr*grad_avg and v is neither read nor written).
+ *   loss_out (device, nullable) receives the mean loss over the batch, fp32 [1].
+ * With MTX_BF16 compute, x, the weights, every hidden layer's output and every data gradient
+ * are rounded to bfloat16 (round to nearest even); sums, logits, weight gradients, the average
+ * and the update are fp32.  An out-of-range label gives that sample a NaN loss.  Asynchronous;
+ * results are deterministic run to run. */
+int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                   float momentum, float* loss_out, void* stream);
+
+/* avg[i] = (1/R) sum_{r<R} grads[r*ld + i] for i < n: the averaging of replica gradients
+ * (Sec. II-B, III-D.2) over R buffers held on this GPU.  Requires R >= 1, n >= 1, ld >= n;
+ * avg must not overlap grads.  Asynchronous. */
+int mtx_average_grads(const float* grads, int R, size_t n, size_t ld, float* avg, void* stream);
+
+/* The average above fused with the optimizer step (Sec. III-D.2, III-E; momentum method of
+ * Sec. I in TensorFlow 1.0 form):
+ *   g = (1/R) sum_r grads[r*ld + i];  v = momentum*v + g;  w = w - lr*v
+ * momentum == 0 gives plain SGD, w = w - lr*g, and then v may be NULL (it is not touched).
+ * avg_out (nullable) receives g.  w, v, avg_out must not overlap grads or each other.
+ * Asynchronous. */
+int mtx_sgd_update(float* w, float* v, const float* grads, int R, size_t n, size_t ld,
+                   float lr, float momentum, float* avg_out, void* stream);
+
+/* Copy the weights (and, if v_host != NULL, the velocity) to host memory [P], in the flat
+ * logical layout.  Synchronous (waits for the model's last stream). */
+int mtx_get_params(const mtx_model* m, float* w_host, float* v_host);
+
+/* Overwrite the weights (and, if v_host != NULL, the velocity) from host memory [P].
+ * Synchronous.  Used for checkpoint restore and for tests that inject parameters. */
+int mtx_set_params(mtx_model* m, const float* w_host, const float* v_host);
+
+/* Introspection of the last mtx_train_step, synchronous:
+ * mtx_get_layer_output copies layer `layer`'s stored output for the whole batch
+ * [B][c][h][w] (after bias and ReLU, or the pooled values) into host memory as fp32; `n` is
+ * the capacity of dst in elements and must be at least the output size.
+ * mtx_get_pool_argmax copies a max-pool layer's window decisions [B][c][oh][ow] (index
+ * u*k + v of the first maximal element) into host memory. */
+int mtx_get_layer_output(const mtx_model* m, int layer, float* dst_host, size_t n);
+int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t n);
+
+/* Kernel timing of mtx_train_step (measurement support; not part of the method).
+ * mtx_set_timing(m, 1) makes every later mtx_train_step record a HIP event pair on its stream
+ * around each kernel launch; mtx_set_timing(m, 0) stops it.  mtx_get_timing waits for the
+ * recorded events and fills up to `capacity` entries, one per launch site of the step, in launch
+ * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
+ * Launch-site names: "cast_w", "cast_x", "fwd", "pool_fwd", "softmax_xent", "mean_loss",
+ * "wgrad", "bias_grad", "dgrad", "pool_bwd", "avg_update" ("wgrad" includes the second pass of
+ * a split reduction).  Timing adds one event pair per launch; use it for measurement runs. */
+typedef struct {
+    char name[32];
+    int layer;        /* layer index, or -1 for a kernel that is not tied to one layer */
+    int launches;     /* number of timed launches */
+    double total_ms;  /* sum of the launches' durations */
+} mtx_kernel_time;
+
+int mtx_set_timing(mtx_model* m, int enable);
+int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count, int reset);
+
+/* Free the host handle (device buffers stay with the caller).  NULL is allowed. */
+void mtx_free_model(mtx_model* m);
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char* mtx_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MTX_H */

@@ -43,6 +43,9 @@
  * the thread count).
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -98,6 +101,16 @@ static double rnd_bf16(double x)
 }
 
 float orc_round_bf16(float x) { return (float)rnd_bf16((double)x); }
+
+/* Number of threads the oracle's parallel loops use. */
+int orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------------------------ */
 /* geometry                                                                                   */

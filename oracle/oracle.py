@@ -55,6 +55,10 @@ def _f64(a):
     return np.ascontiguousarray(a, dtype=np.float64)
 
 
+def num_threads() -> int:
+    return int(lib().orc_num_threads())
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     f = lib().orc_round_bf16
     flat = np.asarray(x, dtype=np.float32).ravel()

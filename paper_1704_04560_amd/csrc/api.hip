@@ -1,0 +1,649 @@
+// Host side of the C ABI declared in include/mtx.h: argument validation, the per-model plan
+// (layer geometry, flat parameter offsets, workspace carve-up) and the launch sequence of one
+// synchronous data-parallel SGD step on the caller's stream.
+#include "mtx.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace mtx;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what)
+{
+    return fail(MTX_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                        \
+    do {                                           \
+        hipError_t _e = (expr);                    \
+        if (_e != hipSuccess) return hip_fail(_e, what); \
+    } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr long long kMaxIndex = 2147483647LL;  // kernels index tensors with 32-bit ints
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct LayerPlan {
+    int kind, relu;
+    int c, h, w, oc, oh, ow, k, s, p, g;
+    size_t w_off, w_len, b_off, b_len;
+    size_t in_elems, out_elems;  // per sample
+    bool act_f32;                // stored output is fp32 (always in fp32 mode; logits)
+    size_t act_off;              // workspace byte offset of the output [B][...]
+    size_t am_off;               // max-pool decisions [B][...] (uint8)
+    int splits;                  // convolution weight gradient: reduction splits
+};
+
+struct Plan {
+    int R = 0, Nb = 0, B = 0, dt = 0;
+    int in_c = 0, in_h = 0, in_w = 0;
+    size_t P = 0, ld = 0;
+    std::vector<LayerPlan> L;
+    int first_param = -1;
+    size_t x16_off = 0, w16_off = 0, dbuf_off[2] = {0, 0}, loss_off = 0, partial_off = 0;
+    size_t ws_bytes = 0;
+};
+
+int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
+{
+    if (!d) return fail(MTX_EINVAL, "desc is NULL");
+    if (!d->layers || d->n_layers < 1) return fail(MTX_EINVAL, "the network has no layers");
+    if (d->in_c < 1 || d->in_h < 1 || d->in_w < 1) return fail(MTX_EINVAL, "input shape must be positive");
+    if (d->compute != MTX_F32 && d->compute != MTX_BF16) return fail(MTX_EINVAL, "compute must be MTX_F32 or MTX_BF16");
+    if (R < 1) return fail(MTX_EINVAL, "R must be >= 1 (got %d)", R);
+    if (Nb < 1) return fail(MTX_EINVAL, "shard_batch must be >= 1 (got %d)", Nb);
+    const long long B = (long long)R * Nb;
+    if (B > kMaxIndex) return fail(MTX_EINVAL, "batch too large");
+    pl.R = R; pl.Nb = Nb; pl.B = (int)B; pl.dt = d->compute;
+    pl.in_c = d->in_c; pl.in_h = d->in_h; pl.in_w = d->in_w;
+    const size_t es = d->compute == MTX_F32 ? 4 : 2;
+    if ((long long)d->in_c * d->in_h * d->in_w * B > kMaxIndex) return fail(MTX_EINVAL, "input too large");
+
+    int c = d->in_c, h = d->in_h, w = d->in_w;
+    size_t off = 0;
+    pl.L.clear();
+    for (int i = 0; i < d->n_layers; ++i) {
+        const mtx_layer& ly = d->layers[i];
+        LayerPlan lp{};
+        lp.kind = ly.kind;
+        lp.relu = ly.relu ? 1 : 0;
+        lp.c = c; lp.h = h; lp.w = w;
+        if (ly.kind == MTX_CONV) {
+            if (ly.out < 1 || ly.k < 1 || ly.stride < 1 || ly.pad < 0 || ly.groups < 1)
+                return fail(MTX_EINVAL, "layer %d: invalid convolution parameters", i);
+            if (c % ly.groups || ly.out % ly.groups)
+                return fail(MTX_EINVAL, "layer %d: groups must divide both channel counts", i);
+            if (h + 2 * ly.pad < ly.k || w + 2 * ly.pad < ly.k)
+                return fail(MTX_EINVAL, "layer %d: kernel larger than the padded input", i);
+            lp.k = ly.k; lp.s = ly.stride; lp.p = ly.pad; lp.g = ly.groups;
+            lp.oc = ly.out;
+            lp.oh = (h + 2 * ly.pad - ly.k) / ly.stride + 1;
+            lp.ow = (w + 2 * ly.pad - ly.k) / ly.stride + 1;
+            lp.w_len = (size_t)ly.out * (c / ly.groups) * ly.k * ly.k;
+            lp.b_len = ly.out;
+        } else if (ly.kind == MTX_FC) {
+            if (ly.out < 1) return fail(MTX_EINVAL, "layer %d: out must be >= 1", i);
+            if ((ly.k != 0 && ly.k != 1) || (ly.stride != 0 && ly.stride != 1) || ly.pad != 0 ||
+                (ly.groups != 0 && ly.groups != 1))
+                return fail(MTX_EINVAL, "layer %d: a fully connected layer takes only out and relu", i);
+            lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
+            lp.oc = ly.out; lp.oh = 1; lp.ow = 1;
+            lp.w_len = (size_t)ly.out * c * h * w;
+            lp.b_len = ly.out;
+        } else if (ly.kind == MTX_MAXPOOL) {
+            if (ly.k < 1 || ly.k > 16 || ly.stride < 1)
+                return fail(MTX_EINVAL, "layer %d: pooling needs 1 <= k <= 16 and stride >= 1", i);
+            if (ly.out != 0 || ly.pad != 0 || ly.relu || (ly.groups != 0 && ly.groups != 1))
+                return fail(MTX_EINVAL, "layer %d: pooling takes only k and stride", i);
+            if (h < ly.k || w < ly.k) return fail(MTX_EINVAL, "layer %d: window larger than the input", i);
+            lp.k = ly.k; lp.s = ly.stride; lp.p = 0; lp.g = 1;
+            lp.oc = c;
+            lp.oh = (h - ly.k) / ly.stride + 1;
+            lp.ow = (w - ly.k) / ly.stride + 1;
+            lp.w_len = 0; lp.b_len = 0;
+        } else {
+            return fail(MTX_EINVAL, "layer %d: unknown kind %d", i, ly.kind);
+        }
+        lp.in_elems = (size_t)c * h * w;
+        lp.out_elems = (size_t)lp.oc * lp.oh * lp.ow;
+        if ((long long)lp.out_elems * B > kMaxIndex || (long long)lp.w_len > kMaxIndex)
+            return fail(MTX_EINVAL, "layer %d: tensor too large for 32-bit indexing", i);
+        lp.w_off = off; off += lp.w_len;
+        lp.b_off = off; off += lp.b_len;
+        if (lp.w_len && pl.first_param < 0) pl.first_param = i;
+        pl.L.push_back(lp);
+        c = lp.oc; h = lp.oh; w = lp.ow;
+    }
+    const LayerPlan& last = pl.L.back();
+    if (last.kind != MTX_FC || last.relu)
+        return fail(MTX_EINVAL, "the last layer must be fully connected without ReLU (class scores)");
+    pl.P = off;
+    pl.ld = align_up(off, 64);
+
+    // workspace carve-up
+    size_t ws = 0;
+    size_t max_grad = (size_t)last.oc;  // data-gradient buffers: dz and every layer's input
+    size_t max_partial = 0;
+    for (size_t i = 0; i < pl.L.size(); ++i) {
+        LayerPlan& lp = pl.L[i];
+        lp.act_f32 = (pl.dt == MTX_F32) || (i + 1 == pl.L.size());
+        lp.act_off = ws;
+        ws = align_up(ws + lp.out_elems * pl.B * (lp.act_f32 ? 4 : es), kAlign);
+        if (lp.kind == MTX_MAXPOOL) {
+            lp.am_off = ws;
+            ws = align_up(ws + lp.out_elems * pl.B, kAlign);
+        }
+        if (lp.in_elems > max_grad) max_grad = lp.in_elems;
+        if (lp.out_elems > max_grad) max_grad = lp.out_elems;
+        lp.splits = 1;
+        if (lp.kind == MTX_CONV) {
+            ConvGeom g{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            lp.splits = conv_wgrad_splits((Dt)pl.dt, g, pl.R);
+            size_t pe = conv_wgrad_partial_elems(g, pl.R, lp.splits);
+            if (pe > max_partial) max_partial = pe;
+        }
+    }
+    if (pl.dt == MTX_BF16) {
+        pl.x16_off = ws;
+        ws = align_up(ws + (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B * 2, kAlign);
+        pl.w16_off = ws;
+        ws = align_up(ws + pl.P * 2, kAlign);
+    }
+    for (int k = 0; k < 2; ++k) {
+        pl.dbuf_off[k] = ws;
+        ws = align_up(ws + max_grad * pl.B * es, kAlign);
+    }
+    pl.loss_off = ws;
+    ws = align_up(ws + (size_t)pl.B * 4, kAlign);
+    pl.partial_off = ws;
+    ws = align_up(ws + max_partial * 4, kAlign);
+    pl.ws_bytes = ws;
+    return MTX_OK;
+}
+
+// First output of a SplitMix64 generator whose state is `key` (Steele, Lea & Flood 2014;
+// constants of Vigna's splitmix64.c).
+uint64_t splitmix64_first(uint64_t key)
+{
+    uint64_t z = key + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+void glorot_init_host(const Plan& pl, uint64_t seed, std::vector<float>& w)
+{
+    w.assign(pl.P, 0.0f);
+    for (size_t l = 0; l < pl.L.size(); ++l) {
+        const LayerPlan& lp = pl.L[l];
+        if (!lp.w_len) continue;
+        double fan_in, fan_out;
+        if (lp.kind == MTX_CONV) {
+            fan_in = (double)(lp.c / lp.g) * lp.k * lp.k;
+            fan_out = (double)lp.oc * lp.k * lp.k;
+        } else {
+            fan_in = (double)lp.in_elems;
+            fan_out = (double)lp.oc;
+        }
+        const double a = std::sqrt(6.0 / (fan_in + fan_out));
+        for (size_t i = 0; i < lp.w_len; ++i) {
+            const uint64_t hsh = splitmix64_first(seed ^ (((uint64_t)l << 32) | (uint64_t)i));
+            const double u = (double)(hsh >> 40) / 16777216.0;
+            w[lp.w_off + i] = (float)(a * (2.0 * u - 1.0));
+        }
+    }
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool overlap(const void* a, size_t abytes, const void* b, size_t bbytes)
+{
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + bbytes && y < x + abytes;
+}
+
+}  // namespace
+
+// Optional per-launch timing: every launch site of the step owns a small ring of event pairs;
+// a pair is read back (and its time accumulated) before it is reused or when asked for.
+struct Timer {
+    static constexpr int kDepth = 4;
+    struct Site {
+        std::string name;
+        int layer = -1;
+        hipEvent_t ev[kDepth][2] = {};
+        int head = 0, pending = 0;
+        long launches = 0;
+        double ms = 0.0;
+    };
+    bool on = false;
+    int cur = 0;
+    std::vector<Site> sites;
+
+    hipError_t retire(Site& st)
+    {
+        const int slot = (st.head - st.pending + kDepth) % kDepth;
+        hipError_t e = hipEventSynchronize(st.ev[slot][1]);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, st.ev[slot][0], st.ev[slot][1]);
+        if (e != hipSuccess) return e;
+        st.ms += ms;
+        st.launches += 1;
+        st.pending -= 1;
+        return hipSuccess;
+    }
+    hipError_t drain()
+    {
+        for (auto& st : sites)
+            while (st.pending) {
+                hipError_t e = retire(st);
+                if (e != hipSuccess) return e;
+            }
+        return hipSuccess;
+    }
+    void destroy()
+    {
+        for (auto& st : sites)
+            for (auto& pr : st.ev)
+                for (auto& e : pr)
+                    if (e) (void)hipEventDestroy(e);
+        sites.clear();
+    }
+};
+
+struct mtx_model {
+    Plan pl;
+    float* w;
+    float* v;
+    float* grads;
+    float* gavg;
+    char* ws;
+    hipStream_t last_stream;
+    Timer timer;
+};
+
+namespace {
+
+// Run one kernel launch (a callable returning hipError_t); with timing on, bracket it with an
+// event pair of its launch site.
+template <class F>
+hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s, F&& f)
+{
+    Timer& t = m->timer;
+    if (!t.on) return f();
+    if ((int)t.sites.size() <= t.cur) {
+        Timer::Site st;
+        st.name = name;
+        st.layer = layer;
+        for (auto& pr : st.ev)
+            for (auto& e : pr) {
+                hipError_t err = hipEventCreate(&e);
+                if (err != hipSuccess) return err;
+            }
+        t.sites.push_back(st);
+    }
+    Timer::Site& st = t.sites[t.cur++];
+    if (st.pending == Timer::kDepth) {
+        hipError_t e = t.retire(st);
+        if (e != hipSuccess) return e;
+    }
+    hipError_t e = hipEventRecord(st.ev[st.head][0], s);
+    if (e == hipSuccess) e = f();
+    if (e == hipSuccess) e = hipEventRecord(st.ev[st.head][1], s);
+    if (e != hipSuccess) return e;
+    st.head = (st.head + 1) % Timer::kDepth;
+    st.pending += 1;
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mtx_last_error(void) { return g_err.c_str(); }
+
+int mtx_model_sizes(const mtx_model_desc* desc, int R, int shard_batch, mtx_sizes* out)
+{
+    if (!out) return fail(MTX_EINVAL, "out is NULL");
+    Plan pl;
+    int rc = make_plan(desc, R, shard_batch, pl);
+    if (rc) return rc;
+    out->n_params = pl.P;
+    out->grad_stride = pl.ld;
+    out->workspace_bytes = pl.ws_bytes;
+    return MTX_OK;
+}
+
+int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                   const mtx_buffers* bufs, void* stream, mtx_model** out)
+{
+    if (!out) return fail(MTX_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!bufs) return fail(MTX_EINVAL, "bufs is NULL");
+    Plan pl;
+    int rc = make_plan(desc, R, shard_batch, pl);
+    if (rc) return rc;
+    if (!bufs->w || !bufs->v || !bufs->grads || !bufs->grad_avg || !bufs->workspace)
+        return fail(MTX_EINVAL, "a model buffer is NULL");
+    if (!aligned(bufs->w, 16) || !aligned(bufs->v, 16) || !aligned(bufs->grads, 16) ||
+        !aligned(bufs->grad_avg, 16) || !aligned(bufs->workspace, 256))
+        return fail(MTX_EINVAL, "model buffers must be 16-byte (workspace: 256-byte) aligned");
+    if (bufs->workspace_bytes < pl.ws_bytes)
+        return fail(MTX_ENOMEM, "workspace too small: %zu bytes given, %zu needed",
+                    bufs->workspace_bytes, pl.ws_bytes);
+    const size_t pb = pl.P * 4, gb = pl.ld * 4 * pl.R;
+    if (overlap(bufs->w, pb, bufs->v, pb) || overlap(bufs->w, pb, bufs->grads, gb) ||
+        overlap(bufs->w, pb, bufs->grad_avg, pb) || overlap(bufs->v, pb, bufs->grads, gb) ||
+        overlap(bufs->v, pb, bufs->grad_avg, pb) || overlap(bufs->grads, gb, bufs->grad_avg, pb) ||
+        overlap(bufs->workspace, pl.ws_bytes, bufs->w, pb) ||
+        overlap(bufs->workspace, pl.ws_bytes, bufs->v, pb) ||
+        overlap(bufs->workspace, pl.ws_bytes, bufs->grads, gb) ||
+        overlap(bufs->workspace, pl.ws_bytes, bufs->grad_avg, pb))
+        return fail(MTX_EINVAL, "model buffers overlap");
+
+    mtx_model* m = new (std::nothrow) mtx_model;
+    if (!m) return fail(MTX_ENOMEM, "host allocation failed");
+    m->pl = std::move(pl);
+    m->w = bufs->w; m->v = bufs->v; m->grads = bufs->grads; m->gavg = bufs->grad_avg;
+    m->ws = static_cast<char*>(bufs->workspace);
+    m->last_stream = static_cast<hipStream_t>(stream);
+
+    std::vector<float> w0;
+    glorot_init_host(m->pl, seed, w0);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        delete m;
+        return hip_fail(e, "mtx_init_model");
+    }
+    *out = m;
+    return MTX_OK;
+}
+
+void mtx_free_model(mtx_model* m)
+{
+    if (!m) return;
+    m->timer.destroy();
+    delete m;
+}
+
+int mtx_set_timing(mtx_model* m, int enable)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    m->timer.on = enable != 0;
+    return MTX_OK;
+}
+
+int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count, int reset)
+{
+    if (!m || !count || capacity < 0 || (capacity > 0 && !out))
+        return fail(MTX_EINVAL, "invalid arguments");
+    HIP_TRY(m->timer.drain(), "read timing events");
+    const int n = (int)m->timer.sites.size();
+    *count = n;
+    for (int i = 0; i < n && i < capacity; ++i) {
+        const Timer::Site& st = m->timer.sites[i];
+        std::memset(&out[i], 0, sizeof out[i]);
+        std::snprintf(out[i].name, sizeof out[i].name, "%s", st.name.c_str());
+        out[i].layer = st.layer;
+        out[i].launches = (int)st.launches;
+        out[i].total_ms = st.ms;
+    }
+    if (reset)
+        for (auto& st : m->timer.sites) {
+            st.ms = 0.0;
+            st.launches = 0;
+        }
+    return MTX_OK;
+}
+
+int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                   float momentum, float* loss_out, void* stream)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    if (!x || !labels) return fail(MTX_EINVAL, "x and labels must not be NULL");
+    if (!aligned(x, 4) || !aligned(labels, 4) || (loss_out && !aligned(loss_out, 4)))
+        return fail(MTX_EINVAL, "x, labels and loss_out must be 4-byte aligned");
+    if (!std::isfinite(lr) || !std::isfinite(momentum))
+        return fail(MTX_EINVAL, "lr and momentum must be finite");
+    const Plan& pl = m->pl;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    m->last_stream = s;
+    m->timer.cur = 0;
+    const Dt dt = (Dt)pl.dt;
+    const bool bf = pl.dt == MTX_BF16;
+    char* ws = m->ws;
+    const void* wT = bf ? static_cast<const void*>(ws + pl.w16_off) : static_cast<const void*>(m->w);
+    const void* x_in = bf ? static_cast<const void*>(ws + pl.x16_off) : static_cast<const void*>(x);
+    const size_t es = bf ? 2 : 4;
+
+    if (bf) {
+        HIP_TRY(launch_site(m, "cast_w", -1, s, [&] { return cast_bf16(m->w, ws + pl.w16_off, pl.P, s); }),
+                "cast weights");
+        HIP_TRY(launch_site(m, "cast_x", -1, s, [&] {
+                    return cast_bf16(x, ws + pl.x16_off, (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B, s);
+                }), "cast input");
+    }
+    auto wptr = [&](const LayerPlan& lp) {
+        return static_cast<const char*>(wT) + lp.w_off * es;
+    };
+    // ---- forward, all R shards at once (the weights are shared) ----
+    const void* in = x_in;
+    for (size_t l = 0; l < pl.L.size(); ++l) {
+        const LayerPlan& lp = pl.L[l];
+        void* out = ws + lp.act_off;
+        const float* bias = m->w + lp.b_off;
+        if (lp.kind == MTX_CONV) {
+            ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
+                        return conv_fwd(dt, g, in, wptr(lp), bias, out, lp.act_f32, lp.relu, s);
+                    }), "conv forward");
+        } else if (lp.kind == MTX_FC) {
+            HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
+                        return fc_fwd(dt, pl.B, (int)lp.in_elems, lp.oc, in, wptr(lp), bias, out,
+                                      lp.act_f32, lp.relu, s);
+                    }), "fc forward");
+        } else {
+            HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
+                        return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, in, out,
+                                        reinterpret_cast<uint8_t*>(ws + lp.am_off), s);
+                    }), "pool forward");
+        }
+        in = out;
+    }
+    // ---- loss and its gradient (shard-mean loss: scale 1/Nb) ----
+    const LayerPlan& last = pl.L.back();
+    void* cur = ws + pl.dbuf_off[0];
+    void* nxt = ws + pl.dbuf_off[1];
+    float* loss_rows = reinterpret_cast<float*>(ws + pl.loss_off);
+    HIP_TRY(launch_site(m, "softmax_xent", -1, s, [&] {
+                return softmax_xent(dt, pl.B, last.oc, pl.Nb,
+                                    reinterpret_cast<const float*>(ws + last.act_off), labels,
+                                    loss_rows, cur, s);
+            }), "softmax cross-entropy");
+    if (loss_out)
+        HIP_TRY(launch_site(m, "mean_loss", -1, s, [&] { return mean_loss(loss_rows, pl.B, loss_out, s); }),
+                "mean loss");
+
+    // ---- backward in reverse layer order; weight gradients per shard into grads[r] ----
+    float* partial = reinterpret_cast<float*>(ws + pl.partial_off);
+    const long long ld = (long long)pl.ld;
+    for (int l = (int)pl.L.size() - 1; l >= pl.first_param && l >= 0; --l) {
+        const LayerPlan& lp = pl.L[l];
+        const void* in_l = l == 0 ? x_in : static_cast<const void*>(ws + pl.L[l - 1].act_off);
+        const bool need_dx = l > pl.first_param;
+        const void* mask = (l > 0 && pl.L[l - 1].relu) ? ws + pl.L[l - 1].act_off : nullptr;
+        const bool mask_f32 = l > 0 && pl.L[l - 1].act_f32;
+        if (lp.kind == MTX_CONV) {
+            ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
+                        return conv_wgrad(dt, gs, pl.R, in_l, cur, m->grads, ld, (long long)lp.w_off,
+                                          partial, lp.splits, s);
+                    }), "conv weight gradient");
+            HIP_TRY(launch_site(m, "bias_grad", l, s, [&] {
+                        return bias_grad(dt, pl.R, pl.Nb, lp.oc, lp.oh * lp.ow, cur, m->grads, ld,
+                                         (long long)lp.b_off, s);
+                    }), "conv bias gradient");
+            if (need_dx) {
+                ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+                HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
+                            return conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32, s);
+                        }), "conv data gradient");
+            }
+        } else if (lp.kind == MTX_FC) {
+            HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
+                        return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, in_l, cur, m->grads,
+                                        ld, (long long)lp.w_off, s);
+                    }), "fc weight gradient");
+            HIP_TRY(launch_site(m, "bias_grad", l, s, [&] {
+                        return bias_grad(dt, pl.R, pl.Nb, lp.oc, 1, cur, m->grads, ld,
+                                         (long long)lp.b_off, s);
+                    }), "fc bias gradient");
+            if (need_dx)
+                HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
+                            return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, cur, wptr(lp), nxt,
+                                            mask, mask_f32, s);
+                        }), "fc data gradient");
+        } else {
+            if (!need_dx) continue;
+            HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
+                        return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s,
+                                        reinterpret_cast<const uint8_t*>(ws + lp.am_off), cur, nxt,
+                                        mask, mask_f32, s);
+                    }), "pool backward");
+        }
+        void* t = cur; cur = nxt; nxt = t;
+    }
+    // ---- average of the R shard gradients fused with the optimizer step ----
+    HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {
+                return average_update(m->grads, pl.R, pl.P, pl.ld, m->w, m->v, lr, momentum,
+                                      m->gavg, true, s);
+            }), "average + update");
+    return MTX_OK;
+}
+
+static int check_avg_args(const float* grads, int R, size_t n, size_t ld, const float* out)
+{
+    if (!grads || !out) return fail(MTX_EINVAL, "grads and the output must not be NULL");
+    if (R < 1) return fail(MTX_EINVAL, "R must be >= 1 (got %d)", R);
+    if (n < 1) return fail(MTX_EINVAL, "n must be >= 1");
+    if (ld < n) return fail(MTX_EINVAL, "ld must be >= n");
+    if (!aligned(grads, 4) || !aligned(out, 4)) return fail(MTX_EINVAL, "pointers must be 4-byte aligned");
+    if ((unsigned long long)ld * R > (1ull << 62)) return fail(MTX_EINVAL, "sizes overflow");
+    return MTX_OK;
+}
+
+int mtx_average_grads(const float* grads, int R, size_t n, size_t ld, float* avg, void* stream)
+{
+    int rc = check_avg_args(grads, R, n, ld, avg);
+    if (rc) return rc;
+    const size_t gb = ((size_t)(R - 1) * ld + n) * 4;
+    if (overlap(grads, gb, avg, n * 4)) return fail(MTX_EINVAL, "avg overlaps grads");
+    HIP_TRY(average_update(grads, R, n, ld, nullptr, nullptr, 0.f, 0.f, avg, false,
+                           static_cast<hipStream_t>(stream)), "mtx_average_grads");
+    return MTX_OK;
+}
+
+int mtx_sgd_update(float* w, float* v, const float* grads, int R, size_t n, size_t ld, float lr,
+                   float momentum, float* avg_out, void* stream)
+{
+    int rc = check_avg_args(grads, R, n, ld, w);
+    if (rc) return rc;
+    if (!std::isfinite(lr) || !std::isfinite(momentum))
+        return fail(MTX_EINVAL, "lr and momentum must be finite");
+    if (momentum != 0.0f && !v) return fail(MTX_EINVAL, "v must not be NULL when momentum != 0");
+    if ((v && !aligned(v, 4)) || (avg_out && !aligned(avg_out, 4)))
+        return fail(MTX_EINVAL, "pointers must be 4-byte aligned");
+    const size_t gb = ((size_t)(R - 1) * ld + n) * 4, nb = n * 4;
+    if (overlap(grads, gb, w, nb) || (v && overlap(grads, gb, v, nb)) ||
+        (avg_out && overlap(grads, gb, avg_out, nb)) || (v && overlap(w, nb, v, nb)) ||
+        (avg_out && overlap(w, nb, avg_out, nb)) || (v && avg_out && overlap(v, nb, avg_out, nb)))
+        return fail(MTX_EINVAL, "w, v, avg_out and grads must not overlap");
+    HIP_TRY(average_update(grads, R, n, ld, w, momentum != 0.0f ? v : nullptr, lr, momentum, avg_out,
+                           true, static_cast<hipStream_t>(stream)), "mtx_sgd_update");
+    return MTX_OK;
+}
+
+int mtx_get_params(const mtx_model* m, float* w_host, float* v_host)
+{
+    if (!m || !w_host) return fail(MTX_EINVAL, "model and w_host must not be NULL");
+    HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
+    HIP_TRY(hipMemcpy(w_host, m->w, m->pl.P * 4, hipMemcpyDeviceToHost), "copy w");
+    if (v_host) HIP_TRY(hipMemcpy(v_host, m->v, m->pl.P * 4, hipMemcpyDeviceToHost), "copy v");
+    return MTX_OK;
+}
+
+int mtx_set_params(mtx_model* m, const float* w_host, const float* v_host)
+{
+    if (!m || !w_host) return fail(MTX_EINVAL, "model and w_host must not be NULL");
+    HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
+    HIP_TRY(hipMemcpy(m->w, w_host, m->pl.P * 4, hipMemcpyHostToDevice), "copy w");
+    if (v_host) HIP_TRY(hipMemcpy(m->v, v_host, m->pl.P * 4, hipMemcpyHostToDevice), "copy v");
+    return MTX_OK;
+}
+
+int mtx_get_layer_output(const mtx_model* m, int layer, float* dst_host, size_t n)
+{
+    if (!m || !dst_host) return fail(MTX_EINVAL, "model and dst_host must not be NULL");
+    if (layer < 0 || layer >= (int)m->pl.L.size()) return fail(MTX_EINVAL, "layer out of range");
+    const LayerPlan& lp = m->pl.L[layer];
+    const size_t cnt = lp.out_elems * m->pl.B;
+    if (n < cnt) return fail(MTX_EINVAL, "dst_host holds %zu elements, %zu needed", n, cnt);
+    HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
+    if (lp.act_f32) {
+        HIP_TRY(hipMemcpy(dst_host, m->ws + lp.act_off, cnt * 4, hipMemcpyDeviceToHost), "copy");
+        return MTX_OK;
+    }
+    std::vector<uint16_t> tmp;
+    try {
+        tmp.resize(cnt);
+    } catch (...) {
+        return fail(MTX_ENOMEM, "host allocation failed");
+    }
+    HIP_TRY(hipMemcpy(tmp.data(), m->ws + lp.act_off, cnt * 2, hipMemcpyDeviceToHost), "copy");
+    for (size_t i = 0; i < cnt; ++i) {
+        const uint32_t u = static_cast<uint32_t>(tmp[i]) << 16;
+        std::memcpy(&dst_host[i], &u, 4);
+    }
+    return MTX_OK;
+}
+
+int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t n)
+{
+    if (!m || !dst_host) return fail(MTX_EINVAL, "model and dst_host must not be NULL");
+    if (layer < 0 || layer >= (int)m->pl.L.size() || m->pl.L[layer].kind != MTX_MAXPOOL)
+        return fail(MTX_EINVAL, "layer %d is not a max-pooling layer", layer);
+    const LayerPlan& lp = m->pl.L[layer];
+    const size_t cnt = lp.out_elems * m->pl.B;
+    if (n < cnt) return fail(MTX_EINVAL, "dst_host holds %zu elements, %zu needed", n, cnt);
+    HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
+    HIP_TRY(hipMemcpy(dst_host, m->ws + lp.am_off, cnt, hipMemcpyDeviceToHost), "copy");
+    return MTX_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Internal declarations shared by the host orchestration (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace mtx {
+
+enum Dt { DT_F32 = 0, DT_BF16 = 1 };
+
+// Geometry of one convolution (or of a fully connected layer viewed as C=in, H=W=K=1).
+struct ConvGeom {
+    int N;            // images in the launch (whole batch for fwd/dgrad, one shard for wgrad)
+    int C, H, W;      // input
+    int OC, OH, OW;   // output
+    int K, S, PD, G;  // kernel, stride, padding, groups
+};
+
+// Implicit-GEMM arguments.  Each operation (see igemm.hip) reads the fields it needs.
+struct GemmArgs {
+    const void* a;         // activation-like operand (x, dy or X)
+    const void* b;         // weights or second activation operand
+    void* out;             // output (activation, data gradient, or fp32 gradient rows)
+    const float* bias;     // forward: fp32 bias [OC]
+    const void* mask;      // data gradient: the previous layer's stored output (ReLU mask)
+    float* partial;        // weight gradient with split K: fp32 partial sums
+    long long out_ld;      // weight gradient: elements between shard gradient rows
+    long long out_off;     // weight gradient: offset of this layer's W in a gradient row
+    int N, C, H, W, OC, OH, OW, K, S, PD, G;
+    int cg, og, KK;        // C/G, OC/G, K*K
+    int Pdim, Qdim, Kdim;  // GEMM sizes: output rows, output columns, reduction length
+    int splits;            // weight gradient: reduction splits per shard
+    int kchunk;            // weight gradient: reduction length of one split (multiple of 32)
+    int R;                 // weight gradient: shards in the launch
+    int relu;              // forward: apply ReLU
+    int out_f32;           // forward: output stored as fp32 (otherwise the compute type)
+    int mask_f32;          // data gradient: mask tensor is fp32 (otherwise the compute type)
+};
+
+hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, const float* bias,
+                    void* y, bool y_f32, bool relu, hipStream_t s);
+hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+                      const void* mask, bool mask_f32, hipStream_t s);
+// Weight gradient of R shards of g.N images each; x and dy point at the first shard.
+hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
+                      float* grads, long long ld, long long w_off, float* partial, int splits,
+                      hipStream_t s);
+int conv_wgrad_splits(Dt dt, const ConvGeom& g, int R);
+size_t conv_wgrad_partial_elems(const ConvGeom& g, int R, int splits);
+
+hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, const float* bias,
+                  void* y, bool y_f32, bool relu, hipStream_t s);
+hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
+                    const void* mask, bool mask_f32, hipStream_t s);
+hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, const void* x, const void* dy,
+                    float* grads, long long ld, long long w_off, hipStream_t s);
+
+// elementwise.hip
+hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
+hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void* x, void* y,
+                    uint8_t* argmax, hipStream_t s);
+hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8_t* argmax,
+                    const void* dy, void* dx, const void* mask, bool mask_f32, hipStream_t s);
+hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
+                        const int32_t* labels, float* loss_rows, void* dz, hipStream_t s);
+hipError_t mean_loss(const float* loss_rows, int B, float* loss_out, hipStream_t s);
+hipError_t bias_grad(Dt dt, int R, int Nb, int OC, int HW, const void* dy, float* grads,
+                     long long ld, long long b_off, hipStream_t s);
+hipError_t wgrad_reduce(int R, int splits, int rows, int cols, const float* partial,
+                        float* grads, long long ld, long long w_off, hipStream_t s);
+hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
+                          float lr, float mu, float* avg, bool update, hipStream_t s);
+
+}  // namespace mtx

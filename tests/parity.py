@@ -1,0 +1,122 @@
+"""Comparison helpers for GPU-vs-oracle parity tests.
+
+Tolerances (per output tensor t, reference r):
+    ||t - r||_2 <= tol * ||r||_2   and   max|t - r| <= tol * max|r|
+with tol = 1e-4 for fp32 compute and 2e-2 for bf16 compute.  The updated weights are compared
+through the update they received, w' - w, with one fp32 unit in the last place of w' of slack
+per element (the rounding of w' itself), so that an error in lr*v cannot hide under w.
+
+Decisions taken in floating point (max-pool window argmax, ReLU sign) can legitimately differ
+between two float evaluations of the same forward pass when two candidates are within rounding
+error of each other.  The GPU's decisions are therefore compared with the oracle's first;
+where they differ, the oracle is run again with the GPU's choice as a hint, and the oracle
+rejects any hint that its own forward error bound does not admit.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import oracle as orc
+
+TOL = {0: 1e-4, 1: 2e-2}
+
+
+def rel_err(t, r):
+    t = np.asarray(t, np.float64)
+    r = np.asarray(r, np.float64)
+    nr = np.linalg.norm(r)
+    mr = np.max(np.abs(r)) if r.size else 0.0
+    d = t - r
+    nd = np.linalg.norm(d)
+    md = np.max(np.abs(d)) if d.size else 0.0
+    return (nd / nr if nr > 0 else nd), (md / mr if mr > 0 else md)
+
+
+def assert_tensor_close(t, r, tol, what=""):
+    a, b = rel_err(t, r)
+    assert a <= tol and b <= tol, f"{what}: rel-norm {a:.3g}, rel-max {b:.3g} > {tol}"
+
+
+def assert_update_close(w_new, w_ref_new, w_old, tol, what="w"):
+    """Per-tensor criterion on the update w' - w, after granting every element one fp32 ulp of
+    w' (its own rounding)."""
+    w_new = np.asarray(w_new, np.float64)
+    w_ref_new = np.asarray(w_ref_new, np.float64)
+    dref = w_ref_new - np.asarray(w_old, np.float64)
+    ulp = np.spacing(np.abs(w_ref_new).astype(np.float32)).astype(np.float64)
+    err = np.maximum(np.abs(w_new - w_ref_new) - ulp, 0.0)
+    nd, md = np.linalg.norm(dref), np.max(np.abs(dref))
+    a = np.linalg.norm(err) / nd if nd > 0 else np.linalg.norm(err)
+    b = np.max(err) / md if md > 0 else np.max(err)
+    assert a <= tol and b <= tol, f"{what}: update rel-norm {a:.3g}, rel-max {b:.3g} > {tol}"
+
+
+def gpu_decisions(model, geo):
+    """Concatenated max-pool argmax (int32) and ReLU decisions (int8) of the GPU's last step, in
+    the oracle's layout."""
+    pools, relus = [], []
+    for i, g in enumerate(geo):
+        if g["kind"] == 2:
+            pools.append(model.pool_argmax(i).astype(np.int32))
+        if g["relu"]:
+            relus.append((model.layer_output(i) > 0).astype(np.int8))
+    pool = np.concatenate(pools) if pools else np.zeros(0, np.int32)
+    relu = np.concatenate(relus) if relus else np.zeros(0, np.int8)
+    return pool, relu
+
+
+def oracle_step_matching(net, layers, R, x, y, w, v, lr, mu, prec, gpu_pool, gpu_relu,
+                         max_rounds=8):
+    """Oracle step whose decisions match the GPU's wherever the GPU's are valid alternatives.
+    A hinted decision can move values downstream by a rounding error and so expose further
+    near-ties; hints are therefore accumulated over a few rounds until the decisions agree.
+    Returns (result, number of hinted decisions)."""
+    res = orc.train_step(net.in_shape, layers, R, x, y, w, v, lr, mu, prec=prec,
+                         want_acts=True, want_decisions=True)
+    ph = np.full(gpu_pool.shape, -1, np.int32)
+    rh = np.full(gpu_relu.shape, -1, np.int8)
+    for _ in range(max_rounds):
+        dp = res.pool_argmax != gpu_pool
+        dr = res.relu_mask != gpu_relu
+        if not dp.any() and not dr.any():
+            return res, int((ph >= 0).sum() + (rh >= 0).sum())
+        ph = np.where(dp, gpu_pool, ph).astype(np.int32)
+        rh = np.where(dr, gpu_relu, rh).astype(np.int8)
+        res = orc.train_step(net.in_shape, layers, R, x, y, w, v, lr, mu, prec=prec,
+                             want_acts=True, want_decisions=True, pool_hint=ph, relu_hint=rh)
+    raise AssertionError("GPU and oracle decisions still differ after hinting: "
+                         f"{int((res.pool_argmax != gpu_pool).sum())} pool, "
+                         f"{int((res.relu_mask != gpu_relu).sum())} ReLU")
+
+
+def compare_step(model, net, layers, geo, R, res, w_old, v_old, mu, tol, loss_gpu,
+                 check_acts=True):
+    """Compare one GPU step (already run, state read back by the caller) with an oracle result."""
+    w_new, v_new = model.get_params()
+    grads = model.grads_host()
+    gavg = model.grad_avg.cpu().numpy()
+    assert abs(loss_gpu - res.loss) <= tol * abs(res.loss), (loss_gpu, res.loss)
+    for gi, g in enumerate(geo):
+        if not g["w_len"]:
+            continue
+        for name, off, ln in (("W", g["w_off"], g["w_len"]), ("b", g["b_off"], g["b_len"])):
+            sl = slice(off, off + ln)
+            for r in range(R):
+                assert_tensor_close(grads[r, sl], res.grads[r, sl], tol, f"layer {gi} {name} shard {r}")
+            assert_tensor_close(gavg[sl], res.gavg[sl], tol, f"layer {gi} {name} average")
+    if mu != 0.0:
+        assert_tensor_close(v_new, res.v_new, tol, "velocity")
+    else:
+        assert np.array_equal(v_new, v_old), "velocity must be untouched without momentum"
+    assert_update_close(w_new, res.w_new, w_old, tol)
+    if check_acts:
+        off = 0
+        for gi, g in enumerate(geo):
+            n = int(np.prod(g["out_shape"])) * x_batch(model)
+            assert_tensor_close(model.layer_output(gi), res.acts[off:off + n], tol,
+                                f"layer {gi} output")
+            off += n
+
+
+def x_batch(model):
+    return model.B

@@ -1,0 +1,137 @@
+"""GPU parity of mtx_train_step against the CPU oracle, through the C ABI.
+
+Every step starts both sides from the same state (the oracle's weights and velocity are copied
+into the model before the step), runs one step on the same seeded batch, and compares the loss,
+every shard's per-layer weight and bias gradients, the averaged gradient, the velocity, the
+weight update and every layer's stored output.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_1704_04560_amd import mtx
+from paper_1704_04560_amd import workloads as wl
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def run_case(tag, net, R, Nb, steps, seed, lr, mu, check_acts=True):
+    layers = wl.layer_tuples(net)
+    geo = orc.geometry(net.in_shape, layers)
+    prec = "bf16" if net.dtype == wl.BF16 else "f32"
+    tol = parity.TOL[net.dtype]
+    _say(f"[case] {tag}: B={R * Nb} R={R} dtype={prec} steps={steps}")
+    model = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=seed)
+    w = orc.init_glorot(net.in_shape, layers, seed)
+    v = np.zeros_like(w)
+    wg, vg = model.get_params()
+    assert np.array_equal(wg.view(np.uint32), w.view(np.uint32)), "initial weights differ"
+    assert np.all(vg == 0)
+    loss_dev = torch.zeros(1, device="cuda")
+    hinted = 0
+    for step in range(steps):
+        x, y = wl.make_batch(net, R * Nb, seed=seed * 1000 + step)
+        model.set_params(w, v)
+        model.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), lr, mu, loss_dev)
+        torch.cuda.synchronize()
+        gp, gr = parity.gpu_decisions(model, geo)
+        res, nh = parity.oracle_step_matching(net, layers, R, x, y, w, v if mu else None, lr, mu,
+                                              prec, gp, gr)
+        hinted += nh
+        parity.compare_step(model, net, layers, geo, R, res, w, v, mu, tol, float(loss_dev.item()),
+                            check_acts=check_acts)
+        w = res.w_new
+        if mu:
+            v = res.v_new
+    _say(f"[case] {tag}: ok ({hinted} hinted decisions)")
+    model.close()
+
+
+def _tiny(dtype):
+    layers = (wl.conv(6, 3, pad=1, relu=True), wl.conv(8, 3, stride=2, pad=1, groups=2, relu=True),
+              wl.maxpool(3, 2), wl.conv(5, 1), wl.fc(7, relu=True), wl.fc(4))
+    return wl.Net("tiny", (3, 13, 11), layers, dtype, "normal")
+
+
+def test_mlp_config():
+    run_case("mlp", wl.MLP, 2, 32, 3, 1, 0.01, 0.0)
+
+
+def test_mlp_with_momentum():
+    run_case("mlp-momentum", wl.MLP, 2, 32, 3, 2, 0.01, 0.9)
+
+
+def test_lenet_small():
+    run_case("lenet-small", wl.LENET, 4, 4, 3, 3, 0.01, 0.9)
+
+
+def test_lenet_config():
+    run_case("lenet", wl.LENET, 4, 64, 2, 4, 0.01, 0.9)
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_every_layer_type(dtype):
+    run_case(f"tiny-{dtype}", _tiny(dtype), 3, 5, 2, 5, 0.05, 0.9)
+
+
+def test_cifar_shapes_reduced_batch():
+    run_case("cifar-B16", wl.CIFAR, 8, 2, 2, 6, 0.01, 0.9)
+
+
+def test_alexnet_shapes_reduced_batch():
+    run_case("alexnet-B4", wl.ALEXNET, 4, 1, 1, 7, 0.01, 0.9, check_acts=False)
+
+
+@pytest.mark.parametrize("R,Nb", [(1, 1), (1, 7), (3, 5), (16, 1)])
+def test_edge_shard_shapes(R, Nb):
+    run_case(f"lenet-R{R}-Nb{Nb}", wl.LENET, R, Nb, 1, 8, 0.01, 0.9)
+
+
+def test_steps_are_deterministic():
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    _say("[case] determinism")
+    outs = []
+    for _ in range(2):
+        m = mtx.Model(net.in_shape, layers, net.dtype, 4, 16, seed=9)
+        x, y = wl.make_batch(net, 64, seed=9)
+        xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+        for _ in range(2):
+            m.train_step(xd, yd, 0.01, 0.9)
+        w, v = m.get_params()
+        outs.append((w, v, m.grads_host()))
+        m.close()
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_average_is_mean_of_shard_gradients_at_full_alexnet_size():
+    """Property that holds at any size: the stored average equals the mean of the R stored
+    shard gradients, and the update equals w - lr * (mu * v + avg)."""
+    net = wl.ALEXNET
+    layers = wl.layer_tuples(net)
+    R, Nb = 8, 32
+    _say("[case] alexnet full-size step properties")
+    m = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=1)
+    w0, v0 = m.get_params()
+    v0 = wl.make_velocity(m.P, seed=1)
+    m.set_params(w0, v0)
+    x, y = wl.make_batch(net, R * Nb, seed=1)
+    loss = torch.zeros(1, device="cuda")
+    m.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), 0.01, 0.9, loss)
+    torch.cuda.synchronize()
+    g = m.grads_host()
+    avg = m.grad_avg.cpu().numpy()
+    ref_avg, ref_w, ref_v = orc.average_update(g, w0, v0, 0.01, 0.9)
+    parity.assert_tensor_close(avg, ref_avg, 1e-6, "average")
+    w1, v1 = m.get_params()
+    parity.assert_tensor_close(v1, ref_v, 1e-6, "velocity")
+    parity.assert_update_close(w1, ref_w, w0, 1e-4)
+    assert np.isfinite(loss.item()) and abs(loss.item() - np.log(1000)) < 0.5
+    m.close()

@@ -160,6 +160,9 @@ def main():
     ap.add_argument("--workload", default="lenet")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-microbench", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 512 MiB device copy (torch copy_) so that hardware "
+                         "byte counters can be scaled against a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no cross-GPU path (the all-reduce across "
@@ -171,6 +174,13 @@ def main():
     from paper_1704_04560_amd import workloads as wl
 
     mtx.lib()  # fails loudly if the HIP library is not built
+    if args.copy_calibration:
+        src = torch.ones(128 * 1024 * 1024, device="cuda")  # 512 MiB of fp32
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wkl = wl.WORKLOADS[args.workload]
     net = wkl.net
     layers = wl.layer_tuples(net)

@@ -167,8 +167,9 @@ int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t
  * recorded events and fills up to `capacity` entries, one per launch site of the step, in launch
  * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
  * Launch-site names: "cast_w", "cast_x", "fwd", "pool_fwd", "softmax_xent", "mean_loss",
- * "wgrad", "bias_grad", "dgrad", "pool_bwd", "avg_update" ("wgrad" includes the second pass of
- * a split reduction).  Timing adds one event pair per launch; use it for measurement runs. */
+ * "wgrad" (weight and bias gradient), "dgrad", "pool_bwd", "avg_update"; a matrix site
+ * includes the second pass of a split reduction.  Timing adds one event pair per launch; use it
+ * for measurement runs. */
 typedef struct {
     char name[32];
     int layer;        /* layer index, or -1 for a kernel that is not tied to one layer */

@@ -54,7 +54,6 @@ struct LayerPlan {
     bool act_f32;                // stored output is fp32 (always in fp32 mode; logits)
     size_t act_off;              // workspace byte offset of the output [B][...]
     size_t am_off;               // max-pool decisions [B][...] (uint8)
-    int splits;                  // convolution weight gradient: reduction splits
 };
 
 struct Plan {
@@ -158,11 +157,23 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         }
         if (lp.in_elems > max_grad) max_grad = lp.in_elems;
         if (lp.out_elems > max_grad) max_grad = lp.out_elems;
-        lp.splits = 1;
+        // fp32 partial sums of the matrix launches whose reduction is split
+        GemmDims dims[3];
+        int nd = 0;
         if (lp.kind == MTX_CONV) {
-            ConvGeom g{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
-            lp.splits = conv_wgrad_splits((Dt)pl.dt, g, pl.R);
-            size_t pe = conv_wgrad_partial_elems(g, pl.R, lp.splits);
+            ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            ConvGeom gs = gb;
+            gs.N = pl.Nb;
+            dims[nd++] = conv_fwd_dims(gb);
+            dims[nd++] = conv_dgrad_dims(gb);
+            dims[nd++] = conv_wgrad_dims(gs, pl.R);
+        } else if (lp.kind == MTX_FC) {
+            dims[nd++] = fc_fwd_dims(pl.B, (int)lp.in_elems, lp.oc);
+            dims[nd++] = fc_dgrad_dims(pl.B, (int)lp.in_elems, lp.oc);
+            dims[nd++] = fc_wgrad_dims(pl.Nb, pl.R, (int)lp.in_elems, lp.oc);
+        }
+        for (int k = 0; k < nd; ++k) {
+            const size_t pe = partial_elems(pl.dt, dims[k]);
             if (pe > max_partial) max_partial = pe;
         }
     }
@@ -452,6 +463,7 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
     auto wptr = [&](const LayerPlan& lp) {
         return static_cast<const char*>(wT) + lp.w_off * es;
     };
+    float* partial = reinterpret_cast<float*>(ws + pl.partial_off);
     // ---- forward, all R shards at once (the weights are shared) ----
     const void* in = x_in;
     for (size_t l = 0; l < pl.L.size(); ++l) {
@@ -461,12 +473,12 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
         if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
-                        return conv_fwd(dt, g, in, wptr(lp), bias, out, lp.act_f32, lp.relu, s);
+                        return conv_fwd(dt, g, in, wptr(lp), bias, out, lp.act_f32, lp.relu, partial, s);
                     }), "conv forward");
         } else if (lp.kind == MTX_FC) {
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
                         return fc_fwd(dt, pl.B, (int)lp.in_elems, lp.oc, in, wptr(lp), bias, out,
-                                      lp.act_f32, lp.relu, s);
+                                      lp.act_f32, lp.relu, partial, s);
                     }), "fc forward");
         } else {
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
@@ -491,7 +503,6 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
                 "mean loss");
 
     // ---- backward in reverse layer order; weight gradients per shard into grads[r] ----
-    float* partial = reinterpret_cast<float*>(ws + pl.partial_off);
     const long long ld = (long long)pl.ld;
     for (int l = (int)pl.L.size() - 1; l >= pl.first_param && l >= 0; --l) {
         const LayerPlan& lp = pl.L[l];
@@ -503,31 +514,23 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
                         return conv_wgrad(dt, gs, pl.R, in_l, cur, m->grads, ld, (long long)lp.w_off,
-                                          partial, lp.splits, s);
+                                          (long long)lp.b_off, partial, s);
                     }), "conv weight gradient");
-            HIP_TRY(launch_site(m, "bias_grad", l, s, [&] {
-                        return bias_grad(dt, pl.R, pl.Nb, lp.oc, lp.oh * lp.ow, cur, m->grads, ld,
-                                         (long long)lp.b_off, s);
-                    }), "conv bias gradient");
             if (need_dx) {
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
-                            return conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32, s);
+                            return conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32, partial, s);
                         }), "conv data gradient");
             }
         } else if (lp.kind == MTX_FC) {
             HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
                         return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, in_l, cur, m->grads,
-                                        ld, (long long)lp.w_off, s);
+                                        ld, (long long)lp.w_off, (long long)lp.b_off, partial, s);
                     }), "fc weight gradient");
-            HIP_TRY(launch_site(m, "bias_grad", l, s, [&] {
-                        return bias_grad(dt, pl.R, pl.Nb, lp.oc, 1, cur, m->grads, ld,
-                                         (long long)lp.b_off, s);
-                    }), "fc bias gradient");
             if (need_dx)
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
                             return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, cur, wptr(lp), nxt,
-                                            mask, mask_f32, s);
+                                            mask, mask_f32, partial, s);
                         }), "fc data gradient");
         } else {
             if (!need_dx) continue;

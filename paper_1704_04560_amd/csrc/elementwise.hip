@@ -1,6 +1,5 @@
 // Memory-bound kernels of the training step: bfloat16 casts, max-pooling, the fused softmax
-// cross-entropy, bias gradients, the split-reduction pass of the weight gradient, and the
-// fused gradient average + momentum update.  All reductions run in a fixed order, so results
+// cross-entropy and the fused gradient average + momentum update.  All reductions run in a fixed order, so results
 // are identical from run to run.
 #include "device_common.h"
 #include "internal.h"
@@ -217,95 +216,6 @@ __global__ __launch_bounds__(256) void mean_loss_kernel(const float* __restrict_
 hipError_t mean_loss(const float* loss_rows, int B, float* loss_out, hipStream_t s)
 {
     hipLaunchKernelGGL(mean_loss_kernel, dim3(1), dim3(256), 0, s, loss_rows, B, loss_out);
-    return hipGetLastError();
-}
-
-// ---- bias gradient: db[r][c] = sum over the shard's samples and positions of dy ----------------
-
-// One block per (shard, channel) for convolution outputs (HW > 1).
-template <typename T>
-__global__ __launch_bounds__(256) void bias_grad_conv_kernel(int Nb, int OC, int HW,
-                                                             const T* __restrict__ dy,
-                                                             float* __restrict__ grads,
-                                                             long long ld, long long b_off)
-{
-    __shared__ float sh[256];
-    const int c = blockIdx.x, r = blockIdx.y;
-    const int n = Nb * HW;
-    float s = 0.f;
-    for (int e = threadIdx.x; e < n; e += 256) {
-        const int b = e / HW, hw = e - b * HW;
-        s += to_f32<T>(dy[((long long)(r * Nb + b) * OC + c) * HW + hw]);
-    }
-    sh[threadIdx.x] = s;
-    __syncthreads();
-    for (int o = 128; o >= 1; o >>= 1) {
-        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) grads[r * ld + b_off + c] = sh[0];
-}
-
-// One thread per (shard, unit) for fully connected outputs (HW == 1).
-template <typename T>
-__global__ __launch_bounds__(256) void bias_grad_fc_kernel(int R, int Nb, int OC,
-                                                           const T* __restrict__ dy,
-                                                           float* __restrict__ grads,
-                                                           long long ld, long long b_off)
-{
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= R * OC) return;
-    const int r = t / OC, c = t - r * OC;
-    float s = 0.f;
-    for (int b = 0; b < Nb; ++b) s += to_f32<T>(dy[(long long)(r * Nb + b) * OC + c]);
-    grads[r * ld + b_off + c] = s;
-}
-
-hipError_t bias_grad(Dt dt, int R, int Nb, int OC, int HW, const void* dy, float* grads,
-                     long long ld, long long b_off, hipStream_t s)
-{
-    if (HW == 1) {
-        if (dt == DT_F32)
-            hipLaunchKernelGGL(bias_grad_fc_kernel<float>, dim3(grid_for(R * OC, 256)),
-                               dim3(256), 0, s, R, Nb, OC, static_cast<const float*>(dy), grads,
-                               ld, b_off);
-        else
-            hipLaunchKernelGGL(bias_grad_fc_kernel<bf16_t>, dim3(grid_for(R * OC, 256)),
-                               dim3(256), 0, s, R, Nb, OC, static_cast<const bf16_t*>(dy),
-                               grads, ld, b_off);
-    } else {
-        if (dt == DT_F32)
-            hipLaunchKernelGGL(bias_grad_conv_kernel<float>, dim3(OC, R), dim3(256), 0, s, Nb,
-                               OC, HW, static_cast<const float*>(dy), grads, ld, b_off);
-        else
-            hipLaunchKernelGGL(bias_grad_conv_kernel<bf16_t>, dim3(OC, R), dim3(256), 0, s, Nb,
-                               OC, HW, static_cast<const bf16_t*>(dy), grads, ld, b_off);
-    }
-    return hipGetLastError();
-}
-
-// ---- second pass of a split weight-gradient reduction: sum the splits in ascending order ------
-
-__global__ __launch_bounds__(256) void wgrad_reduce_kernel(int splits, long long per_shard,
-                                                           const float* __restrict__ partial,
-                                                           float* __restrict__ grads,
-                                                           long long ld, long long w_off)
-{
-    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-    const int r = blockIdx.y;
-    if (t >= per_shard) return;
-    const float* p = partial + (long long)r * splits * per_shard + t;
-    float s = 0.f;
-    for (int k = 0; k < splits; ++k) s += p[(long long)k * per_shard];
-    grads[r * ld + w_off + t] = s;
-}
-
-hipError_t wgrad_reduce(int R, int splits, int rows, int cols, const float* partial,
-                        float* grads, long long ld, long long w_off, hipStream_t s)
-{
-    const long long per = (long long)rows * cols;
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(per, 256), R), dim3(256), 0, s, splits,
-                       per, partial, grads, ld, w_off);
     return hipGetLastError();
 }
 

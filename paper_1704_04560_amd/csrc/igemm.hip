@@ -1,18 +1,28 @@
 // Implicit-GEMM kernels on the gfx950 matrix cores for the convolution and fully connected
 // layers: forward (+bias, +ReLU), data gradient (+ReLU mask of the layer below) and weight
-// gradient (per shard, optional split of the reduction with a deterministic second pass).
+// gradient per shard (with the bias gradient as one extra output column).
 //
-// Every operation is written as C[p][q] = sum_k P[p][k] * Q[q][k].  An operation class
-// supplies element loaders for P and Q (which gather through the convolution index map, with
-// zero padding and tails returning 0) and an epilogue that scatters C into its tensor.  One
-// kernel template stages BP x BK and BQ x BK tiles in LDS (k contiguous within a row, rows
-// padded by 16 bytes) and runs 16x16 MFMA fragments over them:
-//   fp32: v_mfma_f32_16x16x4_f32, four per 16-byte LDS read (lane group g feeds k = 4g + t
-//         to the t-th instruction for both operands, so the product is unchanged);
+// Every operation is C[p][q] = sum_k P[p][k] * Q[q][k].  One kernel template stages BP x BK
+// and BQ x BK tiles in LDS (k contiguous within a row, rows padded by 16 bytes) and runs 16x16
+// MFMA fragments over them:
+//   fp32: v_mfma_f32_16x16x4_f32, four per 16-byte LDS read (lane group g feeds k = 4g + t to
+//         the t-th instruction for both operands, so the product is unchanged);
 //   bf16: v_mfma_f32_16x16x32_bf16, one per 16-byte read (8 values per lane).
-// 256 threads = 4 waves in a 2 x 2 grid; a wave owns FP x FQ fragments of 16 x 16.
-// MFMA output layout (16x16): lane l, register v holds row 4*(l/16) + v, column l%16, so the
-// epilogue's consecutive lanes walk consecutive q (the contiguous dimension of the output).
+// 256 threads = 4 waves in a 2 x 2 grid; a wave owns FP x FQ fragments of 16 x 16.  The MFMA
+// output layout (lane l, register v -> row 4*(l/16) + v, column l%16) makes consecutive lanes
+// walk consecutive q, the contiguous dimension of every output.
+//
+// Operand loading.  An operand tile is BR rows x BK reduction steps.  It is loaded either
+// "row-fast" (consecutive threads take consecutive rows, each thread keeps one row for the whole
+// kernel and steps through k) or "k-fast" (consecutive threads take consecutive k, each thread
+// keeps one k per tile and steps through rows); the choice follows the contiguous dimension in
+// memory.  Whatever is fixed per thread is decoded once; the part of the convolution index map
+// that varies per element comes from a table in LDS built at kernel start, so the inner loop
+// does no integer division.
+//
+// Reduction splits.  When a problem has too few output tiles to fill the GPU, the reduction is
+// split over blockIdx.z; every split writes fp32 partial sums and a second kernel adds them in
+// ascending split order and applies the operation's epilogue (deterministic, no atomics).
 #include "device_common.h"
 #include "internal.h"
 
@@ -26,8 +36,8 @@ template <typename T> struct Mma;
 
 template <> struct Mma<float> {
     typedef f32x4 frag;
-    static constexpr int VEC = 4;    // elements per 16-byte lane read
-    static constexpr int KSTEP = 16; // k covered by one read across the 4 lane groups
+    static constexpr int VEC = 4;     // elements per 16-byte lane read
+    static constexpr int KSTEP = 16;  // k covered by one read across the 4 lane groups
     __device__ __forceinline__ static void run(f32x4& acc, const frag& a, const frag& b)
     {
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);
@@ -50,39 +60,83 @@ template <> struct Mma<bf16_t> {
 };
 
 template <typename T> __device__ __forceinline__ T zero() { return T(0); }
+template <typename T> __device__ __forceinline__ T one();
+template <> __device__ __forceinline__ float one<float>() { return 1.0f; }
+template <> __device__ __forceinline__ bf16_t one<bf16_t>() { return (bf16_t)0x3f80; }
 
-// ------------------------------------------------------------------------------------------
-// Operations
-// ------------------------------------------------------------------------------------------
+// One entry of an index table: a flat offset and the two kernel-window coordinates it stands
+// for (needed for the zero-padding test).
+struct TabEnt {
+    int off;
+    short u, v;
+};
+
+constexpr int kMaxTab = 4096;  // largest reduction length with an LDS table (32 KB)
 
 struct Ctx {
     int grp, r, split, kbeg, kend, b0;
+    const TabEnt* tab;  // LDS table (operation specific), or null
 };
 
-// Convolution forward: p = output channel within the group, q = (image, oh, ow),
-// k = (input channel within the group, u, v).
+__device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c)
+{
+    const int z = blockIdx.z;
+    c.grp = z % a.G;
+    const int rest = z / a.G;
+    c.r = rest / a.splits;
+    c.split = rest - c.r * a.splits;
+    c.kbeg = c.split * a.kchunk;
+    c.kend = min(a.Kdim, c.kbeg + a.kchunk);
+    c.b0 = c.r * a.N;
+    c.tab = nullptr;
+}
+
+// ------------------------------------------------------------------------------------------
+// Convolution forward: p = output channel in the group, q = (image, oh, ow),
+// k = (input channel in the group, u, v).  P = weights (k-fast), Q = input patches (row-fast,
+// table over k).
+// ------------------------------------------------------------------------------------------
 template <typename T> struct ConvFwd {
     typedef T TT;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = true, QTAB = false;
+    __device__ static TabEnt ktab_entry(const GemmArgs& a, int k)
     {
-        c.grp = blockIdx.z; c.r = 0; c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = 0;
-    }
-    __device__ static T loadP(const GemmArgs& a, const Ctx& c, int p, int k)
-    {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.b)[(long long)(c.grp * a.og + p) * a.Kdim + k];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx& c, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
-        const int ohw = a.OH * a.OW;
-        const int b = q / ohw, hw = q - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
         const int ci = k / a.KK, rr = k - ci * a.KK, u = rr / a.K, v = rr - u * a.K;
-        const int hi = ho * a.S - a.PD + u, wi = wo * a.S - a.PD + v;
+        return TabEnt{(ci * a.H + u) * a.W + v, (short)u, (short)v};
+    }
+    // P: weights [og rows of this group][Kdim]
+    struct PK { long long base; bool ok; };
+    __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
+    {
+        return PK{(long long)c.grp * a.og * a.Kdim + k, k < c.kend};
+    }
+    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    {
+        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.b)[s.base + (long long)p * a.Kdim]
+                                    : zero<T>();
+    }
+    // Q: input patches, one fixed output position per thread
+    struct QR { long long base; int h0, w0; bool ok; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx& c, int q)
+    {
+        QR s;
+        s.ok = q < a.Qdim;
+        const int ohw = a.OH * a.OW;
+        const int qq = s.ok ? q : 0;
+        const int b = qq / ohw, hw = qq - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
+        s.h0 = ho * a.S - a.PD;
+        s.w0 = wo * a.S - a.PD;
+        s.base = ((long long)b * a.C + c.grp * a.cg) * a.H * a.W + (long long)s.h0 * a.W + s.w0;
+        return s;
+    }
+    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    {
+        if (!s.ok || k >= c.kend) return zero<T>();
+        const TabEnt e = c.tab ? c.tab[k - c.kbeg] : ktab_entry(a, k);
+        const int hi = s.h0 + e.u, wi = s.w0 + e.v;
         if ((unsigned)hi >= (unsigned)a.H || (unsigned)wi >= (unsigned)a.W) return zero<T>();
-        return static_cast<const T*>(a.a)[((long long)(b * a.C + c.grp * a.cg + ci) * a.H + hi) *
-                                              a.W + wi];
+        return static_cast<const T*>(a.a)[s.base + e.off];
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
@@ -96,38 +150,62 @@ template <typename T> struct ConvFwd {
     }
 };
 
-// Convolution data gradient: p = input channel within the group, q = (image, h, w),
-// k = (output channel within the group, u, v); dy is read where (h + pad - u) / stride lands
-// on an output row (and likewise for columns).
+// ------------------------------------------------------------------------------------------
+// Convolution data gradient: p = input channel in the group, q = (image, h, w),
+// k = (output channel in the group, u, v).  dy is read where (h + pad - u) / stride is an
+// output row inside the tensor (likewise for columns).  P = weights (k-fast), Q = dy (row-fast,
+// table over k for stride 1).
+// ------------------------------------------------------------------------------------------
 template <typename T> struct ConvDgrad {
     typedef T TT;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = true, QTAB = false;
+    __device__ static TabEnt ktab_entry(const GemmArgs& a, int k)
     {
-        c.grp = blockIdx.z; c.r = 0; c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = 0;
-    }
-    __device__ static T loadP(const GemmArgs& a, const Ctx& c, int p, int k)
-    {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        const int co = k / a.KK, rr = k - co * a.KK;
-        return static_cast<const T*>(a.b)[((long long)(c.grp * a.og + co) * a.cg + p) * a.KK + rr];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx& c, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
-        const int hw_in = a.H * a.W;
-        const int b = q / hw_in, hw = q - b * hw_in, h = hw / a.W, w = hw - h * a.W;
         const int co = k / a.KK, rr = k - co * a.KK, u = rr / a.K, v = rr - u * a.K;
-        int th = h + a.PD - u, tw = w + a.PD - v;
-        if (th < 0 || tw < 0) return zero<T>();
-        if (a.S > 1) {
-            if (th % a.S || tw % a.S) return zero<T>();
-            th /= a.S;
-            tw /= a.S;
+        return TabEnt{co * a.OH * a.OW - u * a.OW - v, (short)u, (short)v};
+    }
+    struct PK { long long base; bool ok; };
+    __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
+    {
+        const int co = k / a.KK, rr = k - co * a.KK;
+        return PK{((long long)(c.grp * a.og + co) * a.cg) * a.KK + rr, k < c.kend};
+    }
+    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    {
+        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.b)[s.base + (long long)p * a.KK]
+                                    : zero<T>();
+    }
+    struct QR { long long base; int hp, wp; bool ok; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx& c, int q)
+    {
+        QR s;
+        s.ok = q < a.Qdim;
+        const int hw_in = a.H * a.W;
+        const int qq = s.ok ? q : 0;
+        const int b = qq / hw_in, hw = qq - b * hw_in, h = hw / a.W, w = hw - h * a.W;
+        s.hp = h + a.PD;
+        s.wp = w + a.PD;
+        s.base = ((long long)b * a.OC + c.grp * a.og) * a.OH * a.OW;
+        if (a.S == 1) s.base += (long long)s.hp * a.OW + s.wp;
+        return s;
+    }
+    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    {
+        if (!s.ok || k >= c.kend) return zero<T>();
+        if (a.S == 1) {
+            const TabEnt e = c.tab ? c.tab[k - c.kbeg] : ktab_entry(a, k);
+            const int th = s.hp - e.u, tw = s.wp - e.v;
+            if ((unsigned)th >= (unsigned)a.OH || (unsigned)tw >= (unsigned)a.OW) return zero<T>();
+            return static_cast<const T*>(a.a)[s.base + e.off];
         }
+        const int co = k / a.KK, rr = k - co * a.KK, u = rr / a.K, v = rr - u * a.K;
+        int th = s.hp - u, tw = s.wp - v;
+        if (th < 0 || tw < 0 || th % a.S || tw % a.S) return zero<T>();
+        th /= a.S;
+        tw /= a.S;
         if (th >= a.OH || tw >= a.OW) return zero<T>();
-        return static_cast<const T*>(a.a)[((long long)(b * a.OC + c.grp * a.og + co) * a.OH + th) *
-                                              a.OW + tw];
+        return static_cast<const T*>(a.a)[s.base + ((long long)co * a.OH + th) * a.OW + tw];
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
@@ -143,70 +221,92 @@ template <typename T> struct ConvDgrad {
     }
 };
 
-// Convolution weight gradient of one shard: p = output channel within the group,
-// q = (input channel within the group, u, v), k = (image in the shard, oh, ow).
+// ------------------------------------------------------------------------------------------
+// Convolution weight gradient of one shard: p = output channel in the group,
+// q = (input channel in the group, u, v) plus one extra column q = cg*K*K of ones that yields
+// the bias gradient, k = (image in the shard, oh, ow).  Both operands k-fast; the q side of the
+// patch offset comes from a per-block table.
 // blockIdx.z = (shard * splits + split) * G + group.
+// ------------------------------------------------------------------------------------------
 template <typename T> struct ConvWgrad {
     typedef T TT;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = false;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = false, QTAB = true;
+    __device__ static TabEnt qtab_entry(const GemmArgs& a, int q)
     {
-        const int z = blockIdx.z;
-        c.grp = z % a.G;
-        const int rest = z / a.G;
-        c.r = rest / a.splits;
-        c.split = rest - c.r * a.splits;
-        c.kbeg = c.split * a.kchunk;
-        c.kend = min(a.Kdim, c.kbeg + a.kchunk);
-        c.b0 = c.r * a.N;
-    }
-    __device__ static T loadP(const GemmArgs& a, const Ctx& c, int p, int k)
-    {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        const int ohw = a.OH * a.OW;
-        const int b = k / ohw, hw = k - b * ohw;
-        return static_cast<const T*>(a.a)[((long long)(c.b0 + b) * a.OC + c.grp * a.og + p) * ohw +
-                                              hw];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx& c, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
         const int ci = q / a.KK, rr = q - ci * a.KK, u = rr / a.K, v = rr - u * a.K;
+        return TabEnt{(ci * a.H + u) * a.W + v, (short)u, (short)v};
+    }
+    struct PK { long long base; bool ok; };
+    __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
+    {
         const int ohw = a.OH * a.OW;
-        const int b = k / ohw, hw = k - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
-        const int hi = ho * a.S - a.PD + u, wi = wo * a.S - a.PD + v;
+        const int kk = k < c.kend ? k : 0;
+        const int b = kk / ohw, hw = kk - b * ohw;
+        return PK{((long long)(c.b0 + b) * a.OC + c.grp * a.og) * ohw + hw, k < c.kend};
+    }
+    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    {
+        return (s.ok && p < a.Pdim)
+                   ? static_cast<const T*>(a.a)[s.base + (long long)p * a.OH * a.OW]
+                   : zero<T>();
+    }
+    struct QK { long long base; int h0, w0; bool ok; };
+    __device__ static QK qk(const GemmArgs& a, const Ctx& c, int k)
+    {
+        QK s;
+        s.ok = k < c.kend;
+        const int ohw = a.OH * a.OW;
+        const int kk = s.ok ? k : 0;
+        const int b = kk / ohw, hw = kk - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
+        s.h0 = ho * a.S - a.PD;
+        s.w0 = wo * a.S - a.PD;
+        s.base = ((long long)(c.b0 + b) * a.C + c.grp * a.cg) * a.H * a.W +
+                 (long long)s.h0 * a.W + s.w0;
+        return s;
+    }
+    __device__ static T q_atk(const GemmArgs& a, const Ctx& c, const QK& s, int q, int q0)
+    {
+        if (!s.ok) return zero<T>();
+        const int nq = a.cg * a.KK;
+        if (q >= nq) return q == nq ? one<T>() : zero<T>();
+        const TabEnt e = c.tab ? c.tab[q - q0] : qtab_entry(a, q);
+        const int hi = s.h0 + e.u, wi = s.w0 + e.v;
         if ((unsigned)hi >= (unsigned)a.H || (unsigned)wi >= (unsigned)a.W) return zero<T>();
-        return static_cast<const T*>(a.b)[((long long)(c.b0 + b) * a.C + c.grp * a.cg + ci) *
-                                              a.H * a.W + (long long)hi * a.W + wi];
+        return static_cast<const T*>(a.b)[s.base + e.off];
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
         const int co = c.grp * a.og + p;
-        const long long row = (long long)a.cg * a.KK;
-        if (a.splits == 1)
-            static_cast<float*>(a.out)[c.r * a.out_ld + a.out_off + co * row + q] = acc;
-        else
-            a.partial[((long long)(c.r * a.splits + c.split) * a.OC + co) * row + q] = acc;
+        const int nq = a.cg * a.KK;
+        float* g = static_cast<float*>(a.out) + c.r * a.out_ld;
+        if (q < nq) g[a.out_off + (long long)co * nq + q] = acc;
+        else g[a.bias_off + co] = acc;
     }
 };
 
-// Fully connected forward: p = sample, q = output unit, k = input feature.
+// ------------------------------------------------------------------------------------------
+// Fully connected layers
+// ------------------------------------------------------------------------------------------
+
+// Forward: p = sample, q = output unit, k = input feature.  Both operands k-fast.
 template <typename T> struct FcFwd {
     typedef T TT;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = false;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = false, QTAB = false;
+    struct PK { int k; bool ok; };
+    __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
+    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
     {
-        c.grp = 0; c.r = 0; c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = 0;
+        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.a)[(long long)p * a.Kdim + s.k]
+                                    : zero<T>();
     }
-    __device__ static T loadP(const GemmArgs& a, const Ctx&, int p, int k)
+    typedef PK QK;
+    __device__ static QK qk(const GemmArgs&, const Ctx& c, int k) { return QK{k, k < c.kend}; }
+    __device__ static T q_atk(const GemmArgs& a, const Ctx&, const QK& s, int q, int)
     {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.a)[(long long)p * a.Kdim + k];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx&, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.b)[(long long)q * a.Kdim + k];
+        return (s.ok && q < a.Qdim) ? static_cast<const T*>(a.b)[(long long)q * a.Kdim + s.k]
+                                    : zero<T>();
     }
     __device__ static void store(const GemmArgs& a, const Ctx&, int p, int q, float acc)
     {
@@ -218,23 +318,24 @@ template <typename T> struct FcFwd {
     }
 };
 
-// Fully connected data gradient: p = sample, q = input feature, k = output unit.
+// Data gradient: p = sample, q = input feature, k = output unit.  P k-fast, Q row-fast.
 template <typename T> struct FcDgrad {
     typedef T TT;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = false, QTAB = false;
+    struct PK { int k; bool ok; };
+    __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
+    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
     {
-        c.grp = 0; c.r = 0; c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = 0;
+        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.a)[(long long)p * a.Kdim + s.k]
+                                    : zero<T>();
     }
-    __device__ static T loadP(const GemmArgs& a, const Ctx&, int p, int k)
+    struct QR { int q; bool ok; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx&, int q) { return QR{q, q < a.Qdim}; }
+    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
     {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.a)[(long long)p * a.Kdim + k];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx&, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.b)[(long long)k * a.Qdim + q];
+        return (s.ok && k < c.kend) ? static_cast<const T*>(a.b)[(long long)k * a.Qdim + s.q]
+                                    : zero<T>();
     }
     __device__ static void store(const GemmArgs& a, const Ctx&, int p, int q, float acc)
     {
@@ -248,36 +349,115 @@ template <typename T> struct FcDgrad {
     }
 };
 
-// Fully connected weight gradient of one shard: p = output unit, q = input feature,
-// k = sample in the shard.  blockIdx.z = shard.
+// Weight gradient of one shard: p = output unit, q = input feature plus the bias column
+// q = IN, k = sample in the shard.  Both operands row-fast.  blockIdx.z as for convolutions.
 template <typename T> struct FcWgrad {
     typedef T TT;
     static constexpr bool P_ROW_FAST = true, Q_ROW_FAST = true;
-    __device__ static void setup(const GemmArgs& a, Ctx& c)
+    static constexpr bool KTAB = false, QTAB = false;
+    struct PR { int p; bool ok; };
+    __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.Pdim}; }
+    __device__ static T p_atr(const GemmArgs& a, const Ctx& c, const PR& s, int k)
     {
-        c.grp = 0; c.r = blockIdx.z; c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = c.r * a.N;
+        return (s.ok && k < c.kend)
+                   ? static_cast<const T*>(a.a)[(long long)(c.b0 + k) * a.Pdim + s.p]
+                   : zero<T>();
     }
-    __device__ static T loadP(const GemmArgs& a, const Ctx& c, int p, int k)
+    struct QR { int q; bool ok; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx&, int q) { return QR{q, q < a.Qdim}; }
+    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
     {
-        if (p >= a.Pdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.a)[(long long)(c.b0 + k) * a.Pdim + p];
-    }
-    __device__ static T loadQ(const GemmArgs& a, const Ctx& c, int q, int k)
-    {
-        if (q >= a.Qdim || k >= a.Kdim) return zero<T>();
-        return static_cast<const T*>(a.b)[(long long)(c.b0 + k) * a.Qdim + q];
+        if (!s.ok || k >= c.kend) return zero<T>();
+        if (s.q == a.C) return one<T>();
+        return static_cast<const T*>(a.b)[(long long)(c.b0 + k) * a.C + s.q];
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
-        static_cast<float*>(a.out)[c.r * a.out_ld + a.out_off + (long long)p * a.Qdim + q] = acc;
+        float* g = static_cast<float*>(a.out) + c.r * a.out_ld;
+        if (q < a.C) g[a.out_off + (long long)p * a.C + q] = acc;
+        else g[a.bias_off + p] = acc;
     }
+};
+
+// ------------------------------------------------------------------------------------------
+// Operand tile loaders: the four (row-fast | k-fast) x (P | Q) cases
+// ------------------------------------------------------------------------------------------
+
+// P operand, k-fast: the thread's k is fixed within a tile, rows step by 256/BK.
+template <class Op, int BR, int BK, int N, bool RF> struct LoadP;
+template <class Op, int BR, int BK, int N> struct LoadP<Op, BR, BK, N, false> {
+    typedef typename Op::TT T;
+    struct St {};
+    __device__ static void init(const GemmArgs&, const Ctx&, St&, int, int) {}
+    __device__ static void load(const GemmArgs& a, const Ctx& c, const St&, int tid, int r0,
+                                int k0, T* out)
+    {
+        const typename Op::PK s = Op::pk(a, c, k0 + tid % BK);
+        const int row = r0 + tid / BK;
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = Op::p_at(a, s, row + i * (256 / BK));
+    }
+    __device__ static int row(int tid, int i) { return tid / BK + i * (256 / BK); }
+    __device__ static int kk(int tid, int) { return tid % BK; }
+};
+// P operand, row-fast: the thread's row is fixed for the whole kernel, k steps by 256/BR.
+template <class Op, int BR, int BK, int N> struct LoadP<Op, BR, BK, N, true> {
+    typedef typename Op::TT T;
+    typedef typename Op::PR St;
+    __device__ static void init(const GemmArgs& a, const Ctx& c, St& s, int tid, int r0)
+    {
+        s = Op::pr(a, c, r0 + tid % BR);
+    }
+    __device__ static void load(const GemmArgs& a, const Ctx& c, const St& s, int tid, int,
+                                int k0, T* out)
+    {
+        const int k = k0 + tid / BR;
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = Op::p_atr(a, c, s, k + i * (256 / BR));
+    }
+    __device__ static int row(int tid, int) { return tid % BR; }
+    __device__ static int kk(int tid, int i) { return tid / BR + i * (256 / BR); }
+};
+
+template <class Op, int BR, int BK, int N, bool RF> struct LoadQ;
+template <class Op, int BR, int BK, int N> struct LoadQ<Op, BR, BK, N, false> {
+    typedef typename Op::TT T;
+    struct St {};
+    __device__ static void init(const GemmArgs&, const Ctx&, St&, int, int) {}
+    __device__ static void load(const GemmArgs& a, const Ctx& c, const St&, int tid, int r0,
+                                int k0, T* out)
+    {
+        const typename Op::QK s = Op::qk(a, c, k0 + tid % BK);
+        const int row = r0 + tid / BK;
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = Op::q_atk(a, c, s, row + i * (256 / BK), r0);
+    }
+    __device__ static int row(int tid, int i) { return tid / BK + i * (256 / BK); }
+    __device__ static int kk(int tid, int) { return tid % BK; }
+};
+template <class Op, int BR, int BK, int N> struct LoadQ<Op, BR, BK, N, true> {
+    typedef typename Op::TT T;
+    typedef typename Op::QR St;
+    __device__ static void init(const GemmArgs& a, const Ctx& c, St& s, int tid, int r0)
+    {
+        s = Op::qr(a, c, r0 + tid % BR);
+    }
+    __device__ static void load(const GemmArgs& a, const Ctx& c, const St& s, int tid, int,
+                                int k0, T* out)
+    {
+        const int k = k0 + tid / BR;
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = Op::q_at(a, c, s, k + i * (256 / BR));
+    }
+    __device__ static int row(int tid, int) { return tid % BR; }
+    __device__ static int kk(int tid, int i) { return tid / BR + i * (256 / BR); }
 };
 
 // ------------------------------------------------------------------------------------------
 // The tiled MFMA kernel
 // ------------------------------------------------------------------------------------------
 
-template <class Op, int FP, int FQ, int BK>
+template <class Op, int FP, int FQ, int BK, bool TAB>
 __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 {
     typedef typename Op::TT T;
@@ -287,15 +467,34 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     constexpr int LDK = BK + VEC;  // 16 bytes of padding per row
     constexpr int NP = BP * BK / 256, NQ = BQ * BK / 256;
     static_assert(NP >= 1 && NQ >= 1 && (BP * BK) % 256 == 0 && (BQ * BK) % 256 == 0, "tile");
-    static_assert(BK % M::KSTEP == 0, "BK");
+    static_assert(BK % M::KSTEP == 0 && 256 % BK == 0 && 256 % BP == 0 && 256 % BQ == 0, "BK");
+    typedef LoadP<Op, BP, BK, NP, Op::P_ROW_FAST> LP;
+    typedef LoadQ<Op, BQ, BK, NQ, Op::Q_ROW_FAST> LQ;
 
     __shared__ __attribute__((aligned(16))) T sP[BP * LDK];
     __shared__ __attribute__((aligned(16))) T sQ[BQ * LDK];
+    extern __shared__ TabEnt tab[];  // sized at launch: kchunk (KTAB) or BQ (QTAB) entries
 
     Ctx c;
-    Op::setup(a, c);
+    decode_z(a, c);
     const int p0 = blockIdx.y * BP, q0 = blockIdx.x * BQ;
     const int tid = threadIdx.x;
+
+    if constexpr (TAB && Op::KTAB) {
+        for (int k = c.kbeg + tid; k < c.kend; k += 256) tab[k - c.kbeg] = Op::ktab_entry(a, k);
+        c.tab = tab;
+        __syncthreads();
+    }
+    if constexpr (TAB && Op::QTAB) {
+        if (tid < BQ) tab[tid] = Op::qtab_entry(a, min(q0 + tid, a.cg * a.KK - 1));
+        c.tab = tab;
+        __syncthreads();
+    }
+
+    typename LP::St sp;
+    typename LQ::St sq;
+    LP::init(a, c, sp, tid, p0);
+    LQ::init(a, c, sq, tid, q0);
     T rp[NP], rq[NQ];
 
     const int wave = tid >> 6, lane = tid & 63;
@@ -310,49 +509,18 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 
     int k0 = c.kbeg;
     if (k0 < c.kend) {
-#pragma unroll
-        for (int i = 0; i < NP; ++i) {
-            const int e = tid + 256 * i;
-            const int row = Op::P_ROW_FAST ? e % BP : e / BK, kk = Op::P_ROW_FAST ? e / BP : e % BK;
-            rp[i] = Op::loadP(a, c, p0 + row, k0 + kk);
-        }
-#pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-            const int e = tid + 256 * i;
-            const int row = Op::Q_ROW_FAST ? e % BQ : e / BK, kk = Op::Q_ROW_FAST ? e / BQ : e % BK;
-            rq[i] = Op::loadQ(a, c, q0 + row, k0 + kk);
-        }
+        LP::load(a, c, sp, tid, p0, k0, rp);
+        LQ::load(a, c, sq, tid, q0, k0, rq);
     }
     for (; k0 < c.kend; k0 += BK) {
 #pragma unroll
-        for (int i = 0; i < NP; ++i) {
-            const int e = tid + 256 * i;
-            const int row = Op::P_ROW_FAST ? e % BP : e / BK, kk = Op::P_ROW_FAST ? e / BP : e % BK;
-            sP[row * LDK + kk] = rp[i];
-        }
+        for (int i = 0; i < NP; ++i) sP[LP::row(tid, i) * LDK + LP::kk(tid, i)] = rp[i];
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-            const int e = tid + 256 * i;
-            const int row = Op::Q_ROW_FAST ? e % BQ : e / BK, kk = Op::Q_ROW_FAST ? e / BQ : e % BK;
-            sQ[row * LDK + kk] = rq[i];
-        }
+        for (int i = 0; i < NQ; ++i) sQ[LQ::row(tid, i) * LDK + LQ::kk(tid, i)] = rq[i];
         __syncthreads();
-        const int kn = k0 + BK;
-        if (kn < c.kend) {
-#pragma unroll
-            for (int i = 0; i < NP; ++i) {
-                const int e = tid + 256 * i;
-                const int row = Op::P_ROW_FAST ? e % BP : e / BK,
-                          kk = Op::P_ROW_FAST ? e / BP : e % BK;
-                rp[i] = Op::loadP(a, c, p0 + row, kn + kk);
-            }
-#pragma unroll
-            for (int i = 0; i < NQ; ++i) {
-                const int e = tid + 256 * i;
-                const int row = Op::Q_ROW_FAST ? e % BQ : e / BK,
-                          kk = Op::Q_ROW_FAST ? e / BQ : e % BK;
-                rq[i] = Op::loadQ(a, c, q0 + row, kn + kk);
-            }
+        if (k0 + BK < c.kend) {
+            LP::load(a, c, sp, tid, p0, k0 + BK, rp);
+            LQ::load(a, c, sq, tid, q0, k0 + BK, rq);
         }
 #pragma unroll
         for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
@@ -373,6 +541,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
         __syncthreads();
     }
 
+    const bool split = a.splits > 1;
+    float* part = a.partial + (long long)blockIdx.z * a.Pdim * a.Qdim;
 #pragma unroll
     for (int i = 0; i < FP; ++i)
 #pragma unroll
@@ -382,36 +552,105 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int p = p0 + wp * 16 * FP + i * 16 + lg * 4 + v;
-                if (p < a.Pdim) Op::store(a, c, p, q, acc[i][j][v]);
+                if (p >= a.Pdim) continue;
+                if (split) part[(long long)p * a.Qdim + q] = acc[i][j][v];
+                else Op::store(a, c, p, q, acc[i][j][v]);
             }
         }
 }
 
+// Second pass of a split reduction: sum the splits of every output in ascending order and
+// apply the operation's epilogue.  blockIdx.y = shard * G + group.
+template <class Op>
+__global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
+{
+    const long long per = (long long)a.Pdim * a.Qdim;
+    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (t >= per) return;
+    const int rg = blockIdx.y;
+    Ctx c;
+    c.grp = rg % a.G;
+    c.r = rg / a.G;
+    c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = c.r * a.N; c.tab = nullptr;
+    const float* src = a.partial + ((long long)c.r * a.splits * a.G + c.grp) * per + t;
+    float s = 0.f;
+    for (int k = 0; k < a.splits; ++k) s += src[(long long)k * a.G * per];
+    Op::store(a, c, (int)(t / a.Qdim), (int)(t % a.Qdim), s);
+}
+
 // ------------------------------------------------------------------------------------------
-// Launch: pick the tile shape from the problem size
+// Launch planning (shared by the workspace sizing and the launches)
 // ------------------------------------------------------------------------------------------
 
-template <class Op, int FP, int FQ>
+GemmPlan plan_gemm(int dt, int Pdim, int Qdim, int Kdim, int zdim, bool allow_split)
+{
+    GemmPlan g{};
+    g.FP = Pdim <= 32 ? 1 : 2;
+    const long long tp = (Pdim + 32 * g.FP - 1) / (32 * g.FP);
+    const long long t4 = (Qdim + 127) / 128;
+    g.FQ = (t4 * tp * zdim >= 256) ? 4 : 2;
+    const long long tiles = ((Qdim + 32 * g.FQ - 1) / (32 * g.FQ)) * tp * zdim;
+    if (dt == DT_F32) g.BK = Kdim >= 64 ? 32 : 16;
+    else g.BK = Kdim >= 128 ? 64 : 32;
+    const long long ktiles = (Kdim + g.BK - 1) / g.BK;
+    g.splits = 1;
+    if (allow_split)
+        while (tiles * g.splits < 512 && ktiles >= (long long)g.splits * 2 * 4 && g.splits < 64)
+            g.splits *= 2;
+    const int per = (Kdim + g.splits - 1) / g.splits;
+    g.kchunk = (per + g.BK - 1) / g.BK * g.BK;
+    g.splits = (Kdim + g.kchunk - 1) / g.kchunk;
+    if (g.splits < 1) g.splits = 1;
+    return g;
+}
+
+template <class Op, int FP, int FQ, int BK>
 static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
 {
-    constexpr int BK = sizeof(typename Op::TT) == 4 ? 16 : 32;
     dim3 grid((a.Qdim + 32 * FQ - 1) / (32 * FQ), (a.Pdim + 32 * FP - 1) / (32 * FP), gz);
     if (grid.y > 65535u || grid.z > 65535u) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK>), grid, dim3(256), 0, s, a);
+    const bool tab = Op::QTAB || (Op::KTAB && a.kchunk <= kMaxTab);
+    const size_t shm = !tab ? 0 : sizeof(TabEnt) * (Op::KTAB ? a.kchunk : 32 * FQ);
+    if (tab)
+        hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, true>), grid, dim3(256), shm, s, a);
+    else
+        hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, false>), grid, dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits <= 1) return e;
+    const long long per = (long long)a.Pdim * a.Qdim;
+    const int rg = gz / a.splits;
+    hipLaunchKernelGGL((split_epilogue<Op>), dim3((unsigned)((per + 255) / 256), rg), dim3(256), 0,
+                       s, a);
     return hipGetLastError();
 }
 
-template <class Op>
-static hipError_t dispatch(const GemmArgs& a, int gz, hipStream_t s)
+template <class Op, int BK>
+static hipError_t launch_bk(const GemmArgs& a, const GemmPlan& g, int gz, hipStream_t s)
 {
-    if (a.Pdim <= 0 || a.Qdim <= 0 || gz <= 0) return hipSuccess;
-    const long long q128 = (a.Qdim + 127) / 128;
-    if (a.Pdim <= 32) {
-        if (q128 * ((a.Pdim + 31) / 32) * gz >= 512) return launch_tile<Op, 1, 4>(a, gz, s);
-        return launch_tile<Op, 1, 2>(a, gz, s);
+    if (g.FP == 1) {
+        if (g.FQ == 4) return launch_tile<Op, 1, 4, BK>(a, gz, s);
+        return launch_tile<Op, 1, 2, BK>(a, gz, s);
     }
-    if (q128 * ((a.Pdim + 63) / 64) * gz >= 512) return launch_tile<Op, 2, 4>(a, gz, s);
-    return launch_tile<Op, 2, 2>(a, gz, s);
+    if (g.FQ == 4) return launch_tile<Op, 2, 4, BK>(a, gz, s);
+    return launch_tile<Op, 2, 2, BK>(a, gz, s);
+}
+
+template <class Op>
+static hipError_t dispatch(GemmArgs a, const GemmPlan& g, int zdim, float* partial, hipStream_t s)
+{
+    if (a.Pdim <= 0 || a.Qdim <= 0 || zdim <= 0) return hipSuccess;
+    a.splits = g.splits;
+    a.kchunk = g.kchunk;
+    a.partial = partial;
+    if (g.splits > 1 && !partial) return hipErrorInvalidValue;
+    const int gz = zdim * g.splits;
+    if constexpr (sizeof(typename Op::TT) == 4) {
+        if (g.BK == 16) return launch_bk<Op, 16>(a, g, gz, s);
+        return launch_bk<Op, 32>(a, g, gz, s);
+    } else {
+        if (g.BK == 32) return launch_bk<Op, 32>(a, g, gz, s);
+        return launch_bk<Op, 64>(a, g, gz, s);
+    }
 }
 
 static GemmArgs conv_args(const ConvGeom& g)
@@ -424,86 +663,111 @@ static GemmArgs conv_args(const ConvGeom& g)
     return a;
 }
 
+// GEMM sizes of every operation (P rows, Q columns, reduction, blockIdx.z extent before splits)
+GemmDims conv_fwd_dims(const ConvGeom& g)
+{
+    return GemmDims{g.OC / g.G, g.N * g.OH * g.OW, (g.C / g.G) * g.K * g.K, g.G, true};
+}
+GemmDims conv_dgrad_dims(const ConvGeom& g)
+{
+    return GemmDims{g.C / g.G, g.N * g.H * g.W, (g.OC / g.G) * g.K * g.K, g.G, true};
+}
+GemmDims conv_wgrad_dims(const ConvGeom& g, int R)
+{
+    return GemmDims{g.OC / g.G, (g.C / g.G) * g.K * g.K + 1, g.N * g.OH * g.OW, g.G * R, true};
+}
+GemmDims fc_fwd_dims(int B, int IN, int OUT) { return GemmDims{B, OUT, IN, 1, true}; }
+GemmDims fc_dgrad_dims(int B, int IN, int OUT) { return GemmDims{B, IN, OUT, 1, true}; }
+GemmDims fc_wgrad_dims(int Nb, int R, int IN, int OUT) { return GemmDims{OUT, IN + 1, Nb, R, true}; }
+
+GemmPlan plan_for(int dt, const GemmDims& d)
+{
+    return plan_gemm(dt, d.P, d.Q, d.K, d.Z, d.allow_split);
+}
+
+size_t partial_elems(int dt, const GemmDims& d)
+{
+    const GemmPlan g = plan_for(dt, d);
+    if (g.splits <= 1) return 0;
+    return (size_t)g.splits * d.Z * (size_t)d.P * d.Q;
+}
+
 hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, const float* bias,
-                    void* y, bool y_f32, bool relu, hipStream_t s)
+                    void* y, bool y_f32, bool relu, float* partial, hipStream_t s)
 {
     GemmArgs a = conv_args(g);
     a.a = x; a.b = w; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
-    a.Pdim = a.og; a.Qdim = g.N * g.OH * g.OW; a.Kdim = a.cg * a.KK;
-    return dt == DT_F32 ? dispatch<ConvFwd<float>>(a, g.G, s) : dispatch<ConvFwd<bf16_t>>(a, g.G, s);
+    const GemmDims d = conv_fwd_dims(g);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<ConvFwd<float>>(a, p, d.Z, partial, s)
+                        : dispatch<ConvFwd<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
-                      const void* mask, bool mask_f32, hipStream_t s)
+                      const void* mask, bool mask_f32, float* partial, hipStream_t s)
 {
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
-    a.Pdim = a.cg; a.Qdim = g.N * g.H * g.W; a.Kdim = a.og * a.KK;
-    return dt == DT_F32 ? dispatch<ConvDgrad<float>>(a, g.G, s)
-                        : dispatch<ConvDgrad<bf16_t>>(a, g.G, s);
-}
-
-int conv_wgrad_splits(Dt, const ConvGeom& g, int R)
-{
-    const long long og = g.OC / g.G, cols = (long long)(g.C / g.G) * g.K * g.K;
-    const long long tiles = ((og + (og <= 32 ? 31 : 63)) / (og <= 32 ? 32 : 64)) *
-                            ((cols + 127) / 128) * g.G * R;
-    const long long kdim = (long long)g.N * g.OH * g.OW;
-    long long splits = (1024 + tiles - 1) / tiles;
-    const long long max_by_k = kdim / 256;  // every split keeps at least 256 reduction steps
-    if (splits > max_by_k) splits = max_by_k;
-    if (splits > 64) splits = 64;
-    if (splits < 1) splits = 1;
-    return (int)splits;
-}
-
-size_t conv_wgrad_partial_elems(const ConvGeom& g, int R, int splits)
-{
-    if (splits <= 1) return 0;
-    return (size_t)R * splits * g.OC * (size_t)(g.C / g.G) * g.K * g.K;
+    const GemmDims d = conv_dgrad_dims(g);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<ConvDgrad<float>>(a, p, d.Z, partial, s)
+                        : dispatch<ConvDgrad<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
-                      float* grads, long long ld, long long w_off, float* partial, int splits,
-                      hipStream_t s)
+                      float* grads, long long ld, long long w_off, long long b_off,
+                      float* partial, hipStream_t s)
 {
     GemmArgs a = conv_args(g);
-    a.a = dy; a.b = x; a.out = grads; a.partial = partial; a.out_ld = ld; a.out_off = w_off;
-    a.Pdim = a.og; a.Qdim = a.cg * a.KK; a.Kdim = g.N * g.OH * g.OW;
-    a.R = R; a.splits = splits < 1 ? 1 : splits;
-    const int per = (a.Kdim + a.splits - 1) / a.splits;
-    a.kchunk = (per + 31) / 32 * 32;
-    hipError_t e = dt == DT_F32 ? dispatch<ConvWgrad<float>>(a, g.G * R * a.splits, s)
-                                : dispatch<ConvWgrad<bf16_t>>(a, g.G * R * a.splits, s);
-    if (e != hipSuccess || a.splits == 1) return e;
-    return wgrad_reduce(R, a.splits, g.OC, a.cg * a.KK, partial, grads, ld, w_off, s);
+    a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
+    a.R = R;
+    const GemmDims d = conv_wgrad_dims(g, R);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<ConvWgrad<float>>(a, p, d.Z, partial, s)
+                        : dispatch<ConvWgrad<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, const float* bias,
-                  void* y, bool y_f32, bool relu, hipStream_t s)
+                  void* y, bool y_f32, bool relu, float* partial, hipStream_t s)
 {
     GemmArgs a{};
     a.a = x; a.b = w; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
-    a.N = B; a.C = IN; a.OC = OUT; a.Pdim = B; a.Qdim = OUT; a.Kdim = IN;
-    return dt == DT_F32 ? dispatch<FcFwd<float>>(a, 1, s) : dispatch<FcFwd<bf16_t>>(a, 1, s);
+    a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1;
+    const GemmDims d = fc_fwd_dims(B, IN, OUT);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<FcFwd<float>>(a, p, d.Z, partial, s)
+                        : dispatch<FcFwd<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
-                    const void* mask, bool mask_f32, hipStream_t s)
+                    const void* mask, bool mask_f32, float* partial, hipStream_t s)
 {
     GemmArgs a{};
     a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
-    a.N = B; a.C = IN; a.OC = OUT; a.Pdim = B; a.Qdim = IN; a.Kdim = OUT;
-    return dt == DT_F32 ? dispatch<FcDgrad<float>>(a, 1, s) : dispatch<FcDgrad<bf16_t>>(a, 1, s);
+    a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1;
+    const GemmDims d = fc_dgrad_dims(B, IN, OUT);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<FcDgrad<float>>(a, p, d.Z, partial, s)
+                        : dispatch<FcDgrad<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, const void* x, const void* dy,
-                    float* grads, long long ld, long long w_off, hipStream_t s)
+                    float* grads, long long ld, long long w_off, long long b_off, float* partial,
+                    hipStream_t s)
 {
     GemmArgs a{};
-    a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off;
-    a.N = Nb; a.C = IN; a.OC = OUT; a.Pdim = OUT; a.Qdim = IN; a.Kdim = Nb; a.R = R;
-    return dt == DT_F32 ? dispatch<FcWgrad<float>>(a, R, s) : dispatch<FcWgrad<bf16_t>>(a, R, s);
+    a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
+    a.N = Nb; a.C = IN; a.OC = OUT; a.G = 1; a.R = R;
+    const GemmDims d = fc_wgrad_dims(Nb, R, IN, OUT);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    return dt == DT_F32 ? dispatch<FcWgrad<float>>(a, p, d.Z, partial, s)
+                        : dispatch<FcWgrad<bf16_t>>(a, p, d.Z, partial, s);
 }
 
 }  // namespace mtx

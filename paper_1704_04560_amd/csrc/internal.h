@@ -27,34 +27,54 @@ struct GemmArgs {
     float* partial;        // weight gradient with split K: fp32 partial sums
     long long out_ld;      // weight gradient: elements between shard gradient rows
     long long out_off;     // weight gradient: offset of this layer's W in a gradient row
+    long long bias_off;    // weight gradient: offset of this layer's b in a gradient row
     int N, C, H, W, OC, OH, OW, K, S, PD, G;
     int cg, og, KK;        // C/G, OC/G, K*K
     int Pdim, Qdim, Kdim;  // GEMM sizes: output rows, output columns, reduction length
-    int splits;            // weight gradient: reduction splits per shard
-    int kchunk;            // weight gradient: reduction length of one split (multiple of 32)
+    int splits;            // reduction splits (blockIdx.z = (shard * splits + split) * G + group)
+    int kchunk;            // reduction length of one split (multiple of the k tile)
     int R;                 // weight gradient: shards in the launch
     int relu;              // forward: apply ReLU
     int out_f32;           // forward: output stored as fp32 (otherwise the compute type)
     int mask_f32;          // data gradient: mask tensor is fp32 (otherwise the compute type)
 };
 
-hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, const float* bias,
-                    void* y, bool y_f32, bool relu, hipStream_t s);
-hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
-                      const void* mask, bool mask_f32, hipStream_t s);
-// Weight gradient of R shards of g.N images each; x and dy point at the first shard.
-hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
-                      float* grads, long long ld, long long w_off, float* partial, int splits,
-                      hipStream_t s);
-int conv_wgrad_splits(Dt dt, const ConvGeom& g, int R);
-size_t conv_wgrad_partial_elems(const ConvGeom& g, int R, int splits);
+// GEMM view of one operation: P output rows, Q output columns, K reduction length, Z blocks
+// along blockIdx.z before reduction splits (groups x shards).
+struct GemmDims {
+    int P, Q, K, Z;
+    bool allow_split;
+};
+// Launch shape: 32*FP x 32*FQ output tile, BK reduction tile, reduction splits of kchunk.
+struct GemmPlan {
+    int FP, FQ, BK, splits, kchunk;
+};
+GemmPlan plan_gemm(int dt, int Pdim, int Qdim, int Kdim, int zdim, bool allow_split);
+GemmPlan plan_for(int dt, const GemmDims& d);
+size_t partial_elems(int dt, const GemmDims& d);  // fp32 partial sums a launch needs (0 if none)
+GemmDims conv_fwd_dims(const ConvGeom& g);
+GemmDims conv_dgrad_dims(const ConvGeom& g);
+GemmDims conv_wgrad_dims(const ConvGeom& g, int R);
+GemmDims fc_fwd_dims(int B, int IN, int OUT);
+GemmDims fc_dgrad_dims(int B, int IN, int OUT);
+GemmDims fc_wgrad_dims(int Nb, int R, int IN, int OUT);
 
+// `partial` is fp32 scratch of at least partial_elems() elements (may be null when 0).
+hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, const float* bias,
+                    void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
+hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+                      const void* mask, bool mask_f32, float* partial, hipStream_t s);
+// Weight and bias gradient of R shards of g.N images each; x and dy point at the first shard.
+hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
+                      float* grads, long long ld, long long w_off, long long b_off,
+                      float* partial, hipStream_t s);
 hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, const float* bias,
-                  void* y, bool y_f32, bool relu, hipStream_t s);
+                  void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
 hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
-                    const void* mask, bool mask_f32, hipStream_t s);
+                    const void* mask, bool mask_f32, float* partial, hipStream_t s);
 hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, const void* x, const void* dy,
-                    float* grads, long long ld, long long w_off, hipStream_t s);
+                    float* grads, long long ld, long long w_off, long long b_off, float* partial,
+                    hipStream_t s);
 
 // elementwise.hip
 hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
@@ -65,10 +85,6 @@ hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
                         const int32_t* labels, float* loss_rows, void* dz, hipStream_t s);
 hipError_t mean_loss(const float* loss_rows, int B, float* loss_out, hipStream_t s);
-hipError_t bias_grad(Dt dt, int R, int Nb, int OC, int HW, const void* dy, float* grads,
-                     long long ld, long long b_off, hipStream_t s);
-hipError_t wgrad_reduce(int R, int splits, int rows, int cols, const float* partial,
-                        float* grads, long long ld, long long w_off, hipStream_t s);
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
                           float lr, float mu, float* avg, bool update, hipStream_t s);
 

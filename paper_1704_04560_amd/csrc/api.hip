@@ -43,6 +43,7 @@ int hip_fail(hipError_t e, const char* what)
 
 constexpr size_t kAlign = 256;
 constexpr long long kMaxIndex = 2147483647LL;  // kernels index tensors with 32-bit ints
+constexpr long long kMaxBytes = 2147483647LL;  // and read them through 32-bit buffer offsets
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -79,7 +80,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     pl.R = R; pl.Nb = Nb; pl.B = (int)B; pl.dt = d->compute;
     pl.in_c = d->in_c; pl.in_h = d->in_h; pl.in_w = d->in_w;
     const size_t es = d->compute == MTX_F32 ? 4 : 2;
-    if ((long long)d->in_c * d->in_h * d->in_w * B > kMaxIndex) return fail(MTX_EINVAL, "input too large");
+    if ((long long)d->in_c * d->in_h * d->in_w * B * 4 > kMaxBytes)
+        return fail(MTX_EINVAL, "input exceeds 2 GiB");
 
     int c = d->in_c, h = d->in_h, w = d->in_w;
     size_t off = 0;
@@ -128,8 +130,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         }
         lp.in_elems = (size_t)c * h * w;
         lp.out_elems = (size_t)lp.oc * lp.oh * lp.ow;
-        if ((long long)lp.out_elems * B > kMaxIndex || (long long)lp.w_len > kMaxIndex)
-            return fail(MTX_EINVAL, "layer %d: tensor too large for 32-bit indexing", i);
+        if ((long long)lp.out_elems * B * 4 > kMaxBytes || (long long)lp.w_len * 4 > kMaxBytes)
+            return fail(MTX_EINVAL, "layer %d: a tensor exceeds 2 GiB", i);
         lp.w_off = off; off += lp.w_len;
         lp.b_off = off; off += lp.b_len;
         if (lp.w_len && pl.first_param < 0) pl.first_param = i;
@@ -285,6 +287,36 @@ struct Timer {
     }
 };
 
+// Replay of a captured step.  The launch sequence of mtx_train_step depends only on the model
+// and on (x, labels, lr, momentum, loss_out); it is captured once into a HIP graph on a private
+// stream and replayed on the caller's stream while those arguments stay the same.
+struct GraphCache {
+    bool enabled = true;
+    hipStream_t capture_stream = nullptr;
+    hipGraphExec_t exec = nullptr;
+    const float* x = nullptr;
+    const int32_t* labels = nullptr;
+    float lr = 0.f, mu = 0.f;
+    float* loss = nullptr;
+    int misses = 0;  // consecutive captures; replay is abandoned after kMaxMisses
+    static constexpr int kMaxMisses = 3;
+    bool matches(const float* x_, const int32_t* l_, float lr_, float mu_, float* loss_) const
+    {
+        return exec && x == x_ && labels == l_ && lr == lr_ && mu == mu_ && loss == loss_;
+    }
+    void reset()
+    {
+        if (exec) (void)hipGraphExecDestroy(exec);
+        exec = nullptr;
+    }
+    void destroy()
+    {
+        reset();
+        if (capture_stream) (void)hipStreamDestroy(capture_stream);
+        capture_stream = nullptr;
+    }
+};
+
 struct mtx_model {
     Plan pl;
     float* w;
@@ -294,6 +326,7 @@ struct mtx_model {
     char* ws;
     hipStream_t last_stream;
     Timer timer;
+    GraphCache graph;
 };
 
 namespace {
@@ -399,6 +432,8 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
 void mtx_free_model(mtx_model* m)
 {
     if (!m) return;
+    (void)hipStreamSynchronize(m->last_stream);
+    m->graph.destroy();
     m->timer.destroy();
     delete m;
 }
@@ -433,18 +468,11 @@ int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count,
     return MTX_OK;
 }
 
-int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
-                   float momentum, float* loss_out, void* stream)
+// Enqueue the kernels of one step on stream s (eagerly, or into a capture).
+static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                        float momentum, float* loss_out, hipStream_t s)
 {
-    if (!m) return fail(MTX_EINVAL, "model is NULL");
-    if (!x || !labels) return fail(MTX_EINVAL, "x and labels must not be NULL");
-    if (!aligned(x, 4) || !aligned(labels, 4) || (loss_out && !aligned(loss_out, 4)))
-        return fail(MTX_EINVAL, "x, labels and loss_out must be 4-byte aligned");
-    if (!std::isfinite(lr) || !std::isfinite(momentum))
-        return fail(MTX_EINVAL, "lr and momentum must be finite");
     const Plan& pl = m->pl;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    m->last_stream = s;
     m->timer.cur = 0;
     const Dt dt = (Dt)pl.dt;
     const bool bf = pl.dt == MTX_BF16;
@@ -547,6 +575,83 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
                 return average_update(m->grads, pl.R, pl.P, pl.ld, m->w, m->v, lr, momentum,
                                       m->gavg, true, s);
             }), "average + update");
+    return MTX_OK;
+}
+
+// Capture one step into a new executable graph; on any failure the capture is abandoned and
+// the caller falls back to enqueuing the step directly.
+static bool capture_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                         float momentum, float* loss_out)
+{
+    GraphCache& gc = m->graph;
+    gc.reset();
+    if (!gc.capture_stream &&
+        hipStreamCreateWithFlags(&gc.capture_stream, hipStreamNonBlocking) != hipSuccess) {
+        gc.capture_stream = nullptr;
+        return false;
+    }
+    if (hipStreamBeginCapture(gc.capture_stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+        return false;
+    const std::string saved = g_err;
+    const int rc = enqueue_step(m, x, labels, lr, momentum, loss_out, gc.capture_stream);
+    hipGraph_t graph = nullptr;
+    const hipError_t e = hipStreamEndCapture(gc.capture_stream, &graph);
+    g_err = saved;
+    if (rc != MTX_OK || e != hipSuccess || !graph) {
+        if (graph) (void)hipGraphDestroy(graph);
+        (void)hipGetLastError();
+        return false;
+    }
+    hipGraphExec_t exec = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ei != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    gc.exec = exec;
+    gc.x = x; gc.labels = labels; gc.lr = lr; gc.mu = momentum; gc.loss = loss_out;
+    return true;
+}
+
+int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                   float momentum, float* loss_out, void* stream)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    if (!x || !labels) return fail(MTX_EINVAL, "x and labels must not be NULL");
+    if (!aligned(x, 4) || !aligned(labels, 4) || (loss_out && !aligned(loss_out, 4)))
+        return fail(MTX_EINVAL, "x, labels and loss_out must be 4-byte aligned");
+    if (!std::isfinite(lr) || !std::isfinite(momentum))
+        return fail(MTX_EINVAL, "lr and momentum must be finite");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    m->last_stream = s;
+    GraphCache& gc = m->graph;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    const bool caller_capturing =
+        hipStreamIsCapturing(s, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone;
+    (void)hipGetLastError();
+    if (gc.enabled && !m->timer.on && !caller_capturing && gc.misses < GraphCache::kMaxMisses) {
+        if (gc.matches(x, labels, lr, momentum, loss_out)) {
+            gc.misses = 0;
+            HIP_TRY(hipGraphLaunch(gc.exec, s), "graph launch");
+            return MTX_OK;
+        }
+        gc.misses += 1;
+        if (capture_step(m, x, labels, lr, momentum, loss_out)) {
+            HIP_TRY(hipGraphLaunch(gc.exec, s), "graph launch");
+            return MTX_OK;
+        }
+        gc.misses = GraphCache::kMaxMisses;  // capture is not possible here: stay eager
+    }
+    return enqueue_step(m, x, labels, lr, momentum, loss_out, s);
+}
+
+int mtx_set_graph_replay(mtx_model* m, int enable)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    m->graph.enabled = enable != 0;
+    m->graph.misses = 0;
+    if (!enable) m->graph.reset();
     return MTX_OK;
 }
 

@@ -91,6 +91,32 @@ __device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c)
     c.tab = nullptr;
 }
 
+// Operand reads go through raw buffer loads: the buffer resource carries the tensor's size in
+// bytes and the hardware returns 0 for any offset at or past it.  Zero padding and tile tails
+// therefore only select an out-of-range offset (kOOB); there is no branch, and no index can read
+// outside its tensor.
+constexpr unsigned kOOB = 0x80000000u;     // every tensor is smaller than 2 GiB
+constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
+
+template <typename T> struct Buf {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ Buf(const void* p, unsigned bytes)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                              (int)kRsrcWord3))
+    {
+    }
+    __device__ __forceinline__ T at(bool ok, int idx) const
+    {
+        const int off = ok ? idx * (int)sizeof(T) : (int)kOOB;
+        if constexpr (sizeof(T) == 4)
+            return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+        else
+            return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+    }
+};
+
+constexpr int kFar = 1 << 14;  // window coordinate that fails every bounds test
+
 // ------------------------------------------------------------------------------------------
 // Convolution forward: p = output channel in the group, q = (image, oh, ow),
 // k = (input channel in the group, u, v).  P = weights (k-fast), Q = input patches (row-fast,
@@ -98,53 +124,53 @@ __device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c)
 // ------------------------------------------------------------------------------------------
 template <typename T> struct ConvFwd {
     typedef T TT;
+    static constexpr bool P_IS_A = false;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
     static constexpr bool KTAB = true, QTAB = false;
-    __device__ static TabEnt ktab_entry(const GemmArgs& a, int k)
+    __device__ static TabEnt ktab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
-        const int ci = k / a.KK, rr = k - ci * a.KK, u = rr / a.K, v = rr - u * a.K;
-        return TabEnt{(ci * a.H + u) * a.W + v, (short)u, (short)v};
+        if (k >= c.kend) return TabEnt{0, (short)kFar, (short)kFar};
+        const unsigned ci = (unsigned)k / a.KK, rr = (unsigned)k - ci * a.KK;
+        const unsigned u = rr / a.K, v = rr - u * a.K;
+        return TabEnt{(int)((ci * a.H + u) * a.W + v), (short)u, (short)v};
     }
-    // P: weights [og rows of this group][Kdim]
-    struct PK { long long base; bool ok; };
+    struct PK { int base; bool ok; };
     __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
     {
-        return PK{(long long)c.grp * a.og * a.Kdim + k, k < c.kend};
+        return PK{c.grp * a.og * a.Kdim + k, k < c.kend};
     }
-    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    __device__ static T p_at(const GemmArgs& a, const Buf<T>& B, const PK& s, int p)
     {
-        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.b)[s.base + (long long)p * a.Kdim]
-                                    : zero<T>();
+        return B.at(s.ok && p < a.Pdim, s.base + p * a.Kdim);
     }
-    // Q: input patches, one fixed output position per thread
-    struct QR { long long base; int h0, w0; bool ok; };
+    struct QR { int base, h0, w0; };
     __device__ static QR qr(const GemmArgs& a, const Ctx& c, int q)
     {
         QR s;
-        s.ok = q < a.Qdim;
-        const int ohw = a.OH * a.OW;
-        const int qq = s.ok ? q : 0;
-        const int b = qq / ohw, hw = qq - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
-        s.h0 = ho * a.S - a.PD;
-        s.w0 = wo * a.S - a.PD;
-        s.base = ((long long)b * a.C + c.grp * a.cg) * a.H * a.W + (long long)s.h0 * a.W + s.w0;
+        const unsigned ohw = a.OH * a.OW;
+        const bool ok = q < a.Qdim;
+        const unsigned qq = ok ? q : 0;
+        const unsigned b = qq / ohw, hw = qq - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
+        s.h0 = ok ? (int)(ho * a.S) - a.PD : -kFar;
+        s.w0 = (int)(wo * a.S) - a.PD;
+        s.base = (int)(b * a.C + c.grp * a.cg) * a.H * a.W + s.h0 * a.W + s.w0;
         return s;
     }
-    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    template <bool TAB>
+    __device__ static T q_at(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        if (!s.ok || k >= c.kend) return zero<T>();
-        const TabEnt e = c.tab ? c.tab[k - c.kbeg] : ktab_entry(a, k);
+        const TabEnt e = TAB ? c.tab[k - c.kbeg] : ktab_entry(a, c, k);
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
-        if ((unsigned)hi >= (unsigned)a.H || (unsigned)wi >= (unsigned)a.W) return zero<T>();
-        return static_cast<const T*>(a.a)[s.base + e.off];
+        return B.at((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W, s.base + e.off);
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
-        const int co = c.grp * a.og + p, ohw = a.OH * a.OW;
-        const int b = q / ohw, hw = q - b * ohw;
+        const int co = c.grp * a.og + p;
+        const unsigned ohw = a.OH * a.OW;
+        const unsigned b = (unsigned)q / ohw, hw = (unsigned)q - b * ohw;
         float v = acc + a.bias[co];
         if (a.relu) v = v > 0.f ? v : 0.f;
-        const long long idx = ((long long)b * a.OC + co) * ohw + hw;
+        const int idx = (int)(b * a.OC + co) * (int)ohw + (int)hw;
         if (a.out_f32) static_cast<float*>(a.out)[idx] = v;
         else static_cast<T*>(a.out)[idx] = from_f32<T>(v);
     }
@@ -152,66 +178,71 @@ template <typename T> struct ConvFwd {
 
 // ------------------------------------------------------------------------------------------
 // Convolution data gradient: p = input channel in the group, q = (image, h, w),
-// k = (output channel in the group, u, v).  dy is read where (h + pad - u) / stride is an
-// output row inside the tensor (likewise for columns).  P = weights (k-fast), Q = dy (row-fast,
-// table over k for stride 1).
+// k = (output channel in the group, u, v); dy[oh][ow] contributes where h = oh*stride - pad + u
+// (likewise for columns).  P = weights (k-fast), Q = dy (row-fast).  STRIDE1: the table holds
+// the offset of (co, -u, -v) and the test is 0 <= h + pad - u < OH; otherwise the divisibility by
+// the stride is tested element by element.
 // ------------------------------------------------------------------------------------------
-template <typename T> struct ConvDgrad {
+template <typename T, bool STRIDE1> struct ConvDgrad {
     typedef T TT;
+    static constexpr bool P_IS_A = false;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
-    static constexpr bool KTAB = true, QTAB = false;
-    __device__ static TabEnt ktab_entry(const GemmArgs& a, int k)
+    static constexpr bool KTAB = STRIDE1, QTAB = false;
+    __device__ static TabEnt ktab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
-        const int co = k / a.KK, rr = k - co * a.KK, u = rr / a.K, v = rr - u * a.K;
-        return TabEnt{co * a.OH * a.OW - u * a.OW - v, (short)u, (short)v};
+        if (k >= c.kend) return TabEnt{0, (short)-kFar, (short)-kFar};
+        const unsigned co = (unsigned)k / a.KK, rr = (unsigned)k - co * a.KK;
+        const unsigned u = rr / a.K, v = rr - u * a.K;
+        return TabEnt{(int)(co * a.OH * a.OW) - (int)(u * a.OW) - (int)v, (short)u, (short)v};
     }
-    struct PK { long long base; bool ok; };
+    struct PK { int base; bool ok; };
     __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
     {
-        const int co = k / a.KK, rr = k - co * a.KK;
-        return PK{((long long)(c.grp * a.og + co) * a.cg) * a.KK + rr, k < c.kend};
+        const unsigned co = (unsigned)k / a.KK, rr = (unsigned)k - co * a.KK;
+        return PK{(int)((c.grp * a.og + co) * a.cg * a.KK + rr), k < c.kend};
     }
-    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    __device__ static T p_at(const GemmArgs& a, const Buf<T>& B, const PK& s, int p)
     {
-        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.b)[s.base + (long long)p * a.KK]
-                                    : zero<T>();
+        return B.at(s.ok && p < a.Pdim, s.base + p * a.KK);
     }
-    struct QR { long long base; int hp, wp; bool ok; };
+    struct QR { int base, hp, wp; };
     __device__ static QR qr(const GemmArgs& a, const Ctx& c, int q)
     {
         QR s;
-        s.ok = q < a.Qdim;
-        const int hw_in = a.H * a.W;
-        const int qq = s.ok ? q : 0;
-        const int b = qq / hw_in, hw = qq - b * hw_in, h = hw / a.W, w = hw - h * a.W;
-        s.hp = h + a.PD;
-        s.wp = w + a.PD;
-        s.base = ((long long)b * a.OC + c.grp * a.og) * a.OH * a.OW;
-        if (a.S == 1) s.base += (long long)s.hp * a.OW + s.wp;
+        const unsigned hw_in = a.H * a.W;
+        const bool ok = q < a.Qdim;
+        const unsigned qq = ok ? q : 0;
+        const unsigned b = qq / hw_in, hw = qq - b * hw_in, h = hw / a.W, w = hw - h * a.W;
+        s.hp = ok ? (int)h + a.PD : -kFar;
+        s.wp = (int)w + a.PD;
+        s.base = (int)(b * a.OC + c.grp * a.og) * a.OH * a.OW;
+        if (STRIDE1) s.base += s.hp * a.OW + s.wp;
         return s;
     }
-    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    template <bool TAB>
+    __device__ static T q_at(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        if (!s.ok || k >= c.kend) return zero<T>();
-        if (a.S == 1) {
-            const TabEnt e = c.tab ? c.tab[k - c.kbeg] : ktab_entry(a, k);
+        if constexpr (STRIDE1) {
+            const TabEnt e = TAB ? c.tab[k - c.kbeg] : ktab_entry(a, c, k);
             const int th = s.hp - e.u, tw = s.wp - e.v;
-            if ((unsigned)th >= (unsigned)a.OH || (unsigned)tw >= (unsigned)a.OW) return zero<T>();
-            return static_cast<const T*>(a.a)[s.base + e.off];
+            return B.at((unsigned)th < (unsigned)a.OH && (unsigned)tw < (unsigned)a.OW,
+                        s.base + e.off);
+        } else {
+            const unsigned co = (unsigned)k / a.KK, rr = (unsigned)k - co * a.KK;
+            const int u = (int)(rr / a.K), v = (int)(rr - (rr / a.K) * a.K);
+            const int th = s.hp - u, tw = s.wp - v;
+            const int oh = th / a.S, ow = tw / a.S;
+            const bool ok = k < c.kend && th >= 0 && tw >= 0 && oh * a.S == th &&
+                            ow * a.S == tw && oh < a.OH && ow < a.OW;
+            return B.at(ok, s.base + ((int)co * a.OH + oh) * a.OW + ow);
         }
-        const int co = k / a.KK, rr = k - co * a.KK, u = rr / a.K, v = rr - u * a.K;
-        int th = s.hp - u, tw = s.wp - v;
-        if (th < 0 || tw < 0 || th % a.S || tw % a.S) return zero<T>();
-        th /= a.S;
-        tw /= a.S;
-        if (th >= a.OH || tw >= a.OW) return zero<T>();
-        return static_cast<const T*>(a.a)[s.base + ((long long)co * a.OH + th) * a.OW + tw];
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
-        const int ci = c.grp * a.cg + p, hw_in = a.H * a.W;
-        const int b = q / hw_in, hw = q - b * hw_in;
-        const long long idx = ((long long)b * a.C + ci) * hw_in + hw;
+        const int ci = c.grp * a.cg + p;
+        const unsigned hw_in = a.H * a.W;
+        const unsigned b = (unsigned)q / hw_in, hw = (unsigned)q - b * hw_in;
+        const int idx = (int)(b * a.C + ci) * (int)hw_in + (int)hw;
         if (a.mask) {
             const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[idx]
                                        : to_f32<T>(static_cast<const T*>(a.mask)[idx]);
@@ -224,63 +255,63 @@ template <typename T> struct ConvDgrad {
 // ------------------------------------------------------------------------------------------
 // Convolution weight gradient of one shard: p = output channel in the group,
 // q = (input channel in the group, u, v) plus one extra column q = cg*K*K of ones that yields
-// the bias gradient, k = (image in the shard, oh, ow).  Both operands k-fast; the q side of the
-// patch offset comes from a per-block table.
-// blockIdx.z = (shard * splits + split) * G + group.
+// the bias gradient, k = (image in the shard, oh, ow).  Both operands k-fast; the q part of the
+// patch offset comes from a per-block table.  blockIdx.z = (shard * splits + split) * G + group.
 // ------------------------------------------------------------------------------------------
 template <typename T> struct ConvWgrad {
     typedef T TT;
+    static constexpr bool P_IS_A = true;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = false;
     static constexpr bool KTAB = false, QTAB = true;
     __device__ static TabEnt qtab_entry(const GemmArgs& a, int q)
     {
-        const int ci = q / a.KK, rr = q - ci * a.KK, u = rr / a.K, v = rr - u * a.K;
-        return TabEnt{(ci * a.H + u) * a.W + v, (short)u, (short)v};
+        if (q >= a.cg * a.KK) return TabEnt{0, (short)kFar, (short)kFar};
+        const unsigned ci = (unsigned)q / a.KK, rr = (unsigned)q - ci * a.KK;
+        const unsigned u = rr / a.K, v = rr - u * a.K;
+        return TabEnt{(int)((ci * a.H + u) * a.W + v), (short)u, (short)v};
     }
-    struct PK { long long base; bool ok; };
+    struct PK { int base; bool ok; };
     __device__ static PK pk(const GemmArgs& a, const Ctx& c, int k)
     {
-        const int ohw = a.OH * a.OW;
-        const int kk = k < c.kend ? k : 0;
-        const int b = kk / ohw, hw = kk - b * ohw;
-        return PK{((long long)(c.b0 + b) * a.OC + c.grp * a.og) * ohw + hw, k < c.kend};
+        const unsigned ohw = a.OH * a.OW;
+        const bool ok = k < c.kend;
+        const unsigned kk = ok ? k : c.kbeg;
+        const unsigned b = kk / ohw, hw = kk - b * ohw;
+        return PK{(int)(((c.b0 + b) * a.OC + c.grp * a.og) * ohw + hw), ok};
     }
-    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    __device__ static T p_at(const GemmArgs& a, const Buf<T>& B, const PK& s, int p)
     {
-        return (s.ok && p < a.Pdim)
-                   ? static_cast<const T*>(a.a)[s.base + (long long)p * a.OH * a.OW]
-                   : zero<T>();
+        return B.at(s.ok && p < a.Pdim, s.base + p * a.OH * a.OW);
     }
-    struct QK { long long base; int h0, w0; bool ok; };
+    struct QK { int base, h0, w0; bool ok; };
     __device__ static QK qk(const GemmArgs& a, const Ctx& c, int k)
     {
         QK s;
+        const unsigned ohw = a.OH * a.OW;
         s.ok = k < c.kend;
-        const int ohw = a.OH * a.OW;
-        const int kk = s.ok ? k : 0;
-        const int b = kk / ohw, hw = kk - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
-        s.h0 = ho * a.S - a.PD;
-        s.w0 = wo * a.S - a.PD;
-        s.base = ((long long)(c.b0 + b) * a.C + c.grp * a.cg) * a.H * a.W +
-                 (long long)s.h0 * a.W + s.w0;
+        const unsigned kk = s.ok ? k : c.kbeg;
+        const unsigned b = kk / ohw, hw = kk - b * ohw, ho = hw / a.OW, wo = hw - ho * a.OW;
+        s.h0 = s.ok ? (int)(ho * a.S) - a.PD : -kFar;
+        s.w0 = (int)(wo * a.S) - a.PD;
+        s.base = (int)((c.b0 + b) * a.C + c.grp * a.cg) * a.H * a.W + s.h0 * a.W + s.w0;
         return s;
     }
-    __device__ static T q_atk(const GemmArgs& a, const Ctx& c, const QK& s, int q, int q0)
+    template <bool TAB>
+    __device__ static T q_atk(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QK& s, int q,
+                              int q0)
     {
-        if (!s.ok) return zero<T>();
-        const int nq = a.cg * a.KK;
-        if (q >= nq) return q == nq ? one<T>() : zero<T>();
-        const TabEnt e = c.tab ? c.tab[q - q0] : qtab_entry(a, q);
+        const TabEnt e = TAB ? c.tab[q - q0] : qtab_entry(a, q);
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
-        if ((unsigned)hi >= (unsigned)a.H || (unsigned)wi >= (unsigned)a.W) return zero<T>();
-        return static_cast<const T*>(a.b)[s.base + e.off];
+        const T v = B.at((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W,
+                         s.base + e.off);
+        return (q == a.cg * a.KK) ? (s.ok ? one<T>() : zero<T>()) : v;
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
         const int co = c.grp * a.og + p;
         const int nq = a.cg * a.KK;
         float* g = static_cast<float*>(a.out) + c.r * a.out_ld;
-        if (q < nq) g[a.out_off + (long long)co * nq + q] = acc;
+        if (q < nq) g[a.out_off + co * nq + q] = acc;
         else g[a.bias_off + co] = acc;
     }
 };
@@ -292,27 +323,28 @@ template <typename T> struct ConvWgrad {
 // Forward: p = sample, q = output unit, k = input feature.  Both operands k-fast.
 template <typename T> struct FcFwd {
     typedef T TT;
+    static constexpr bool P_IS_A = true;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = false;
     static constexpr bool KTAB = false, QTAB = false;
     struct PK { int k; bool ok; };
     __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
-    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    __device__ static T p_at(const GemmArgs& a, const Buf<T>& B, const PK& s, int p)
     {
-        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.a)[(long long)p * a.Kdim + s.k]
-                                    : zero<T>();
+        return B.at(s.ok && p < a.Pdim, p * a.Kdim + s.k);
     }
     typedef PK QK;
     __device__ static QK qk(const GemmArgs&, const Ctx& c, int k) { return QK{k, k < c.kend}; }
-    __device__ static T q_atk(const GemmArgs& a, const Ctx&, const QK& s, int q, int)
+    template <bool TAB>
+    __device__ static T q_atk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const QK& s, int q,
+                              int)
     {
-        return (s.ok && q < a.Qdim) ? static_cast<const T*>(a.b)[(long long)q * a.Kdim + s.k]
-                                    : zero<T>();
+        return B.at(s.ok && q < a.Qdim, q * a.Kdim + s.k);
     }
     __device__ static void store(const GemmArgs& a, const Ctx&, int p, int q, float acc)
     {
         float v = acc + a.bias[q];
         if (a.relu) v = v > 0.f ? v : 0.f;
-        const long long idx = (long long)p * a.Qdim + q;
+        const int idx = p * a.Qdim + q;
         if (a.out_f32) static_cast<float*>(a.out)[idx] = v;
         else static_cast<T*>(a.out)[idx] = from_f32<T>(v);
     }
@@ -321,25 +353,25 @@ template <typename T> struct FcFwd {
 // Data gradient: p = sample, q = input feature, k = output unit.  P k-fast, Q row-fast.
 template <typename T> struct FcDgrad {
     typedef T TT;
+    static constexpr bool P_IS_A = true;
     static constexpr bool P_ROW_FAST = false, Q_ROW_FAST = true;
     static constexpr bool KTAB = false, QTAB = false;
     struct PK { int k; bool ok; };
     __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
-    __device__ static T p_at(const GemmArgs& a, const PK& s, int p)
+    __device__ static T p_at(const GemmArgs& a, const Buf<T>& B, const PK& s, int p)
     {
-        return (s.ok && p < a.Pdim) ? static_cast<const T*>(a.a)[(long long)p * a.Kdim + s.k]
-                                    : zero<T>();
+        return B.at(s.ok && p < a.Pdim, p * a.Kdim + s.k);
     }
     struct QR { int q; bool ok; };
     __device__ static QR qr(const GemmArgs& a, const Ctx&, int q) { return QR{q, q < a.Qdim}; }
-    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    template <bool TAB>
+    __device__ static T q_at(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        return (s.ok && k < c.kend) ? static_cast<const T*>(a.b)[(long long)k * a.Qdim + s.q]
-                                    : zero<T>();
+        return B.at(s.ok && k < c.kend, k * a.Qdim + s.q);
     }
     __device__ static void store(const GemmArgs& a, const Ctx&, int p, int q, float acc)
     {
-        const long long idx = (long long)p * a.Qdim + q;
+        const int idx = p * a.Qdim + q;
         if (a.mask) {
             const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[idx]
                                        : to_f32<T>(static_cast<const T*>(a.mask)[idx]);
@@ -353,23 +385,23 @@ template <typename T> struct FcDgrad {
 // q = IN, k = sample in the shard.  Both operands row-fast.  blockIdx.z as for convolutions.
 template <typename T> struct FcWgrad {
     typedef T TT;
+    static constexpr bool P_IS_A = true;
     static constexpr bool P_ROW_FAST = true, Q_ROW_FAST = true;
     static constexpr bool KTAB = false, QTAB = false;
     struct PR { int p; bool ok; };
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.Pdim}; }
-    __device__ static T p_atr(const GemmArgs& a, const Ctx& c, const PR& s, int k)
+    __device__ static T p_atr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
     {
-        return (s.ok && k < c.kend)
-                   ? static_cast<const T*>(a.a)[(long long)(c.b0 + k) * a.Pdim + s.p]
-                   : zero<T>();
+        return B.at(s.ok && k < c.kend, (c.b0 + k) * a.Pdim + s.p);
     }
     struct QR { int q; bool ok; };
     __device__ static QR qr(const GemmArgs& a, const Ctx&, int q) { return QR{q, q < a.Qdim}; }
-    __device__ static T q_at(const GemmArgs& a, const Ctx& c, const QR& s, int k)
+    template <bool TAB>
+    __device__ static T q_at(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        if (!s.ok || k >= c.kend) return zero<T>();
-        if (s.q == a.C) return one<T>();
-        return static_cast<const T*>(a.b)[(long long)(c.b0 + k) * a.C + s.q];
+        const bool ok = s.ok && k < c.kend;
+        const T v = B.at(ok && s.q < a.C, (c.b0 + k) * a.C + s.q);
+        return (s.q == a.C) ? (ok ? one<T>() : zero<T>()) : v;
     }
     __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
     {
@@ -384,70 +416,71 @@ template <typename T> struct FcWgrad {
 // ------------------------------------------------------------------------------------------
 
 // P operand, k-fast: the thread's k is fixed within a tile, rows step by 256/BK.
-template <class Op, int BR, int BK, int N, bool RF> struct LoadP;
-template <class Op, int BR, int BK, int N> struct LoadP<Op, BR, BK, N, false> {
+template <class Op, int BR, int BK, int N, bool RF, bool TAB> struct LoadP;
+template <class Op, int BR, int BK, int N, bool TAB> struct LoadP<Op, BR, BK, N, false, TAB> {
     typedef typename Op::TT T;
     struct St {};
     __device__ static void init(const GemmArgs&, const Ctx&, St&, int, int) {}
-    __device__ static void load(const GemmArgs& a, const Ctx& c, const St&, int tid, int r0,
-                                int k0, T* out)
+    __device__ static void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const St&,
+                                int tid, int r0, int k0, T* out)
     {
         const typename Op::PK s = Op::pk(a, c, k0 + tid % BK);
         const int row = r0 + tid / BK;
 #pragma unroll
-        for (int i = 0; i < N; ++i) out[i] = Op::p_at(a, s, row + i * (256 / BK));
+        for (int i = 0; i < N; ++i) out[i] = Op::p_at(a, B, s, row + i * (256 / BK));
     }
     __device__ static int row(int tid, int i) { return tid / BK + i * (256 / BK); }
     __device__ static int kk(int tid, int) { return tid % BK; }
 };
 // P operand, row-fast: the thread's row is fixed for the whole kernel, k steps by 256/BR.
-template <class Op, int BR, int BK, int N> struct LoadP<Op, BR, BK, N, true> {
+template <class Op, int BR, int BK, int N, bool TAB> struct LoadP<Op, BR, BK, N, true, TAB> {
     typedef typename Op::TT T;
     typedef typename Op::PR St;
     __device__ static void init(const GemmArgs& a, const Ctx& c, St& s, int tid, int r0)
     {
         s = Op::pr(a, c, r0 + tid % BR);
     }
-    __device__ static void load(const GemmArgs& a, const Ctx& c, const St& s, int tid, int,
-                                int k0, T* out)
+    __device__ static void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const St& s,
+                                int tid, int, int k0, T* out)
     {
         const int k = k0 + tid / BR;
 #pragma unroll
-        for (int i = 0; i < N; ++i) out[i] = Op::p_atr(a, c, s, k + i * (256 / BR));
+        for (int i = 0; i < N; ++i) out[i] = Op::p_atr(a, B, c, s, k + i * (256 / BR));
     }
     __device__ static int row(int tid, int) { return tid % BR; }
     __device__ static int kk(int tid, int i) { return tid / BR + i * (256 / BR); }
 };
 
-template <class Op, int BR, int BK, int N, bool RF> struct LoadQ;
-template <class Op, int BR, int BK, int N> struct LoadQ<Op, BR, BK, N, false> {
+template <class Op, int BR, int BK, int N, bool RF, bool TAB> struct LoadQ;
+template <class Op, int BR, int BK, int N, bool TAB> struct LoadQ<Op, BR, BK, N, false, TAB> {
     typedef typename Op::TT T;
     struct St {};
     __device__ static void init(const GemmArgs&, const Ctx&, St&, int, int) {}
-    __device__ static void load(const GemmArgs& a, const Ctx& c, const St&, int tid, int r0,
-                                int k0, T* out)
+    __device__ static void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const St&,
+                                int tid, int r0, int k0, T* out)
     {
         const typename Op::QK s = Op::qk(a, c, k0 + tid % BK);
         const int row = r0 + tid / BK;
 #pragma unroll
-        for (int i = 0; i < N; ++i) out[i] = Op::q_atk(a, c, s, row + i * (256 / BK), r0);
+        for (int i = 0; i < N; ++i)
+            out[i] = Op::template q_atk<TAB>(a, B, c, s, row + i * (256 / BK), r0);
     }
     __device__ static int row(int tid, int i) { return tid / BK + i * (256 / BK); }
     __device__ static int kk(int tid, int) { return tid % BK; }
 };
-template <class Op, int BR, int BK, int N> struct LoadQ<Op, BR, BK, N, true> {
+template <class Op, int BR, int BK, int N, bool TAB> struct LoadQ<Op, BR, BK, N, true, TAB> {
     typedef typename Op::TT T;
     typedef typename Op::QR St;
     __device__ static void init(const GemmArgs& a, const Ctx& c, St& s, int tid, int r0)
     {
         s = Op::qr(a, c, r0 + tid % BR);
     }
-    __device__ static void load(const GemmArgs& a, const Ctx& c, const St& s, int tid, int,
-                                int k0, T* out)
+    __device__ static void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const St& s,
+                                int tid, int, int k0, T* out)
     {
         const int k = k0 + tid / BR;
 #pragma unroll
-        for (int i = 0; i < N; ++i) out[i] = Op::q_at(a, c, s, k + i * (256 / BR));
+        for (int i = 0; i < N; ++i) out[i] = Op::template q_at<TAB>(a, B, c, s, k + i * (256 / BR));
     }
     __device__ static int row(int tid, int) { return tid % BR; }
     __device__ static int kk(int tid, int i) { return tid / BR + i * (256 / BR); }
@@ -468,8 +501,12 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     constexpr int NP = BP * BK / 256, NQ = BQ * BK / 256;
     static_assert(NP >= 1 && NQ >= 1 && (BP * BK) % 256 == 0 && (BQ * BK) % 256 == 0, "tile");
     static_assert(BK % M::KSTEP == 0 && 256 % BK == 0 && 256 % BP == 0 && 256 % BQ == 0, "BK");
-    typedef LoadP<Op, BP, BK, NP, Op::P_ROW_FAST> LP;
-    typedef LoadQ<Op, BQ, BK, NQ, Op::Q_ROW_FAST> LQ;
+    typedef LoadP<Op, BP, BK, NP, Op::P_ROW_FAST, TAB> LP;
+    typedef LoadQ<Op, BQ, BK, NQ, Op::Q_ROW_FAST, TAB> LQ;
+    // P reads tensor `a` for the weight-gradient and fully connected ops whose P side is an
+    // activation, tensor `b` (the weights) for the convolution forward and data gradient.
+    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
 
     __shared__ __attribute__((aligned(16))) T sP[BP * LDK];
     __shared__ __attribute__((aligned(16))) T sQ[BQ * LDK];
@@ -481,12 +518,13 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     const int tid = threadIdx.x;
 
     if constexpr (TAB && Op::KTAB) {
-        for (int k = c.kbeg + tid; k < c.kend; k += 256) tab[k - c.kbeg] = Op::ktab_entry(a, k);
+        for (int k = c.kbeg + tid; k < c.kbeg + a.kchunk; k += 256)
+            tab[k - c.kbeg] = Op::ktab_entry(a, c, k);
         c.tab = tab;
         __syncthreads();
     }
     if constexpr (TAB && Op::QTAB) {
-        if (tid < BQ) tab[tid] = Op::qtab_entry(a, min(q0 + tid, a.cg * a.KK - 1));
+        if (tid < BQ) tab[tid] = Op::qtab_entry(a, q0 + tid);
         c.tab = tab;
         __syncthreads();
     }
@@ -509,8 +547,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 
     int k0 = c.kbeg;
     if (k0 < c.kend) {
-        LP::load(a, c, sp, tid, p0, k0, rp);
-        LQ::load(a, c, sq, tid, q0, k0, rq);
+        LP::load(a, bufP, c, sp, tid, p0, k0, rp);
+        LQ::load(a, bufQ, c, sq, tid, q0, k0, rq);
     }
     for (; k0 < c.kend; k0 += BK) {
 #pragma unroll
@@ -519,8 +557,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
         for (int i = 0; i < NQ; ++i) sQ[LQ::row(tid, i) * LDK + LQ::kk(tid, i)] = rq[i];
         __syncthreads();
         if (k0 + BK < c.kend) {
-            LP::load(a, c, sp, tid, p0, k0 + BK, rp);
-            LQ::load(a, c, sq, tid, q0, k0 + BK, rq);
+            LP::load(a, bufP, c, sp, tid, p0, k0 + BK, rp);
+            LQ::load(a, bufQ, c, sq, tid, q0, k0 + BK, rq);
         }
 #pragma unroll
         for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
@@ -697,6 +735,9 @@ hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, cons
 {
     GemmArgs a = conv_args(g);
     a.a = x; a.b = w; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * g.C * g.H * g.W * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
     const GemmDims d = conv_fwd_dims(g);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
@@ -709,11 +750,17 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, v
 {
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
     const GemmDims d = conv_dgrad_dims(g);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
-    return dt == DT_F32 ? dispatch<ConvDgrad<float>>(a, p, d.Z, partial, s)
-                        : dispatch<ConvDgrad<bf16_t>>(a, p, d.Z, partial, s);
+    if (g.S == 1)
+        return dt == DT_F32 ? dispatch<ConvDgrad<float, true>>(a, p, d.Z, partial, s)
+                            : dispatch<ConvDgrad<bf16_t, true>>(a, p, d.Z, partial, s);
+    return dt == DT_F32 ? dispatch<ConvDgrad<float, false>>(a, p, d.Z, partial, s)
+                        : dispatch<ConvDgrad<bf16_t, false>>(a, p, d.Z, partial, s);
 }
 
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
@@ -723,6 +770,9 @@ hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
     a.R = R;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)R * g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)R * g.N * g.C * g.H * g.W * es);
     const GemmDims d = conv_wgrad_dims(g, R);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
@@ -736,6 +786,9 @@ hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, c
     GemmArgs a{};
     a.a = x; a.b = w; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
     a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)B * IN * es);
+    a.b_bytes = (unsigned)((size_t)OUT * IN * es);
     const GemmDims d = fc_fwd_dims(B, IN, OUT);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
@@ -749,6 +802,9 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
     GemmArgs a{};
     a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
     a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)B * OUT * es);
+    a.b_bytes = (unsigned)((size_t)OUT * IN * es);
     const GemmDims d = fc_dgrad_dims(B, IN, OUT);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
@@ -763,6 +819,9 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, const void* x, const 
     GemmArgs a{};
     a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
     a.N = Nb; a.C = IN; a.OC = OUT; a.G = 1; a.R = R;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)R * Nb * OUT * es);
+    a.b_bytes = (unsigned)((size_t)R * Nb * IN * es);
     const GemmDims d = fc_wgrad_dims(Nb, R, IN, OUT);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);

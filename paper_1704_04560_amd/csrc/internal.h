@@ -37,6 +37,8 @@ struct GemmArgs {
     int relu;              // forward: apply ReLU
     int out_f32;           // forward: output stored as fp32 (otherwise the compute type)
     int mask_f32;          // data gradient: mask tensor is fp32 (otherwise the compute type)
+    unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)
+    unsigned b_bytes;      // size of tensor b in bytes
 };
 
 // GEMM view of one operation: P output rows, Q output columns, K reduction length, Z blocks

@@ -135,3 +135,36 @@ def test_average_is_mean_of_shard_gradients_at_full_alexnet_size():
     parity.assert_update_close(w1, ref_w, w0, 1e-4)
     assert np.isfinite(loss.item()) and abs(loss.item() - np.log(1000)) < 0.5
     m.close()
+
+
+@pytest.mark.parametrize("name", ["lenet", "cifar"])
+def test_graph_replay_matches_direct_launches(name):
+    """Replaying the captured step gives bit-identical results to enqueuing it directly, on
+    every step, with host copies and synchronisations between the replays."""
+    net = {"lenet": wl.LENET, "cifar": wl.CIFAR}[name]
+    layers = wl.layer_tuples(net)
+    R, Nb = (4, 16) if name == "lenet" else (8, 2)
+    _say(f"[case] graph replay vs direct {name}")
+    a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
+    b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
+    mtx.mtx_set_graph_replay(b.handle, False)
+    x, y = wl.make_batch(net, R * Nb, seed=3)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    la, lb = torch.zeros(1, device="cuda"), torch.zeros(1, device="cuda")
+    for step in range(4):
+        a.train_step(xd, yd, 0.01, 0.9, la)
+        b.train_step(xd, yd, 0.01, 0.9, lb)
+        torch.cuda.synchronize()
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
+        assert np.array_equal(a.grads_host().view(np.uint32), b.grads_host().view(np.uint32))
+        assert la.item() == lb.item()
+    # a new learning rate forces a new capture; results still match
+    a.train_step(xd, yd, 0.02, 0.9, la)
+    b.train_step(xd, yd, 0.02, 0.9, lb)
+    torch.cuda.synchronize()
+    assert np.array_equal(a.get_params()[0].view(np.uint32), b.get_params()[0].view(np.uint32))
+    a.close()
+    b.close()

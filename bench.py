@@ -79,9 +79,7 @@ def site_work(name, layer, geo, wkl, es):
         return "hbm", 6 * B * c * h * w
     if name == "softmax_xent":
         nc = wkl.net.num_classes
-        return "hbm", B * nc * (4 + es) + B * 8
-    if name == "mean_loss":
-        return "hbm", B * 4 + 4
+        return "hbm", B * nc * (4 + es) + B * 4 + 4
     return "hbm", 0.0
 
 

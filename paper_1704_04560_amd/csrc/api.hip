@@ -53,6 +53,7 @@ struct LayerPlan {
     size_t w_off, w_len, b_off, b_len;
     size_t in_elems, out_elems;  // per sample
     bool act_f32;                // stored output is fp32 (always in fp32 mode; logits)
+    bool dgrad_col;              // convolution data gradient through col + col2im
     size_t act_off;              // workspace byte offset of the output [B][...]
     size_t am_off;               // max-pool decisions [B][...] (uint8)
 };
@@ -64,6 +65,7 @@ struct Plan {
     std::vector<LayerPlan> L;
     int first_param = -1;
     size_t x16_off = 0, w16_off = 0, dbuf_off[2] = {0, 0}, loss_off = 0, partial_off = 0;
+    size_t col_off = 0, sync_off = 0;
     size_t ws_bytes = 0;
 };
 
@@ -147,7 +149,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     // workspace carve-up
     size_t ws = 0;
     size_t max_grad = (size_t)last.oc;  // data-gradient buffers: dz and every layer's input
-    size_t max_partial = 0;
+    size_t max_partial = 0, max_col = 0;
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.act_f32 = (pl.dt == MTX_F32) || (i + 1 == pl.L.size());
@@ -167,7 +169,13 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             ConvGeom gs = gb;
             gs.N = pl.Nb;
             dims[nd++] = conv_fwd_dims(gb);
-            dims[nd++] = conv_dgrad_dims(gb);
+            lp.dgrad_col = conv_dgrad_use_col(gb);
+            if (lp.dgrad_col) {
+                dims[nd++] = conv_dgrad_col_dims(gb);
+                if (conv_dgrad_col_elems(gb) > max_col) max_col = conv_dgrad_col_elems(gb);
+            } else {
+                dims[nd++] = conv_dgrad_dims(gb);
+            }
             dims[nd++] = conv_wgrad_dims(gs, pl.R);
         } else if (lp.kind == MTX_FC) {
             dims[nd++] = fc_fwd_dims(pl.B, (int)lp.in_elems, lp.oc);
@@ -189,10 +197,13 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         pl.dbuf_off[k] = ws;
         ws = align_up(ws + max_grad * pl.B * es, kAlign);
     }
-    pl.loss_off = ws;
-    ws = align_up(ws + (size_t)pl.B * 4, kAlign);
+    pl.loss_off = ws;  // per-block loss sums of the softmax launch, then its counter
+    pl.sync_off = align_up(ws + (size_t)((pl.B + 3) / 4) * 4, kAlign);
+    ws = pl.sync_off + kAlign;
     pl.partial_off = ws;
     ws = align_up(ws + max_partial * 4, kAlign);
+    pl.col_off = ws;
+    ws = align_up(ws + max_col * 4, kAlign);
     pl.ws_bytes = ws;
     return MTX_OK;
 }
@@ -420,6 +431,7 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
+    if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         delete m;
@@ -520,15 +532,13 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     const LayerPlan& last = pl.L.back();
     void* cur = ws + pl.dbuf_off[0];
     void* nxt = ws + pl.dbuf_off[1];
-    float* loss_rows = reinterpret_cast<float*>(ws + pl.loss_off);
+    float* block_sums = reinterpret_cast<float*>(ws + pl.loss_off);
+    unsigned* sync = reinterpret_cast<unsigned*>(ws + pl.sync_off);
     HIP_TRY(launch_site(m, "softmax_xent", -1, s, [&] {
                 return softmax_xent(dt, pl.B, last.oc, pl.Nb,
-                                    reinterpret_cast<const float*>(ws + last.act_off), labels,
-                                    loss_rows, cur, s);
+                                    reinterpret_cast<const float*>(ws + last.act_off), labels, cur,
+                                    block_sums, sync, loss_out, s);
             }), "softmax cross-entropy");
-    if (loss_out)
-        HIP_TRY(launch_site(m, "mean_loss", -1, s, [&] { return mean_loss(loss_rows, pl.B, loss_out, s); }),
-                "mean loss");
 
     // ---- backward in reverse layer order; weight gradients per shard into grads[r] ----
     const long long ld = (long long)pl.ld;
@@ -546,8 +556,13 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                     }), "conv weight gradient");
             if (need_dx) {
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+                float* col = reinterpret_cast<float*>(ws + pl.col_off);
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
-                            return conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32, partial, s);
+                            return lp.dgrad_col
+                                       ? conv_dgrad_col(dt, g, cur, wptr(lp), nxt, mask, mask_f32,
+                                                        col, partial, s)
+                                       : conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32,
+                                                    partial, s);
                         }), "conv data gradient");
             }
         } else if (lp.kind == MTX_FC) {

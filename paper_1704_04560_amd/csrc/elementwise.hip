@@ -39,28 +39,42 @@ hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s)
 }
 
 // ---- max-pooling ----------------------------------------------------------------------------
+// KT / ST > 0: window and stride known at compile time (2/2 and 3/2 are the common cases).
 
 // One thread per output: the first maximal element of the K x K window in row-major order.
-template <typename T>
-__global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int H, int W, int K, int S,
+template <typename T, int KT, int ST>
+__global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int H, int W, int Kr, int Sr,
                                                        int OH, int OW, const T* __restrict__ x,
                                                        T* __restrict__ y,
                                                        uint8_t* __restrict__ argmax)
 {
+    const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
     const int o = blockIdx.x * 256 + threadIdx.x;
     if (o >= total) return;
-    const int ohw = OH * OW;
-    const int nc = o / ohw, hw = o - nc * ohw, i = hw / OW, j = hw - i * OW;
+    const unsigned ohw = OH * OW;
+    const unsigned nc = (unsigned)o / ohw, hw = (unsigned)o - nc * ohw;
+    const unsigned i = hw / OW, j = hw - i * OW;
     const T* xp = x + (long long)nc * H * W + (long long)(i * S) * W + j * S;
     T best = xp[0];
     float bv = to_f32<T>(best);
     int bi = 0;
-    for (int u = 0; u < K; ++u)
-        for (int v = 0; v < K; ++v) {
-            const T t = xp[u * W + v];
-            const float tv = to_f32<T>(t);
-            if (tv > bv) { bv = tv; best = t; bi = u * K + v; }
-        }
+    if constexpr (KT > 0) {
+#pragma unroll
+        for (int u = 0; u < KT; ++u)
+#pragma unroll
+            for (int v = 0; v < KT; ++v) {
+                const T t = xp[u * W + v];
+                const float tv = to_f32<T>(t);
+                if (tv > bv) { bv = tv; best = t; bi = u * KT + v; }
+            }
+    } else {
+        for (int u = 0; u < K; ++u)
+            for (int v = 0; v < K; ++v) {
+                const T t = xp[u * W + v];
+                const float tv = to_f32<T>(t);
+                if (tv > bv) { bv = tv; best = t; bi = u * K + v; }
+            }
+    }
     y[o] = best;
     argmax[o] = (uint8_t)bi;
 }
@@ -71,22 +85,28 @@ hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void*
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
     const int total = N * C * OH * OW;
     if (total <= 0) return hipSuccess;
-    if (dt == DT_F32)
-        hipLaunchKernelGGL(pool_fwd_kernel<float>, dim3(grid_for(total, 256)), dim3(256), 0, s,
-                           total, H, W, K, S, OH, OW, static_cast<const float*>(x),
-                           static_cast<float*>(y), argmax);
-    else
-        hipLaunchKernelGGL(pool_fwd_kernel<bf16_t>, dim3(grid_for(total, 256)), dim3(256), 0, s,
-                           total, H, W, K, S, OH, OW, static_cast<const bf16_t*>(x),
-                           static_cast<bf16_t*>(y), argmax);
+    dim3 g(grid_for(total, 256)), b(256);
+#define POOL_FWD(TY, KK, SS)                                                                  \
+    hipLaunchKernelGGL((pool_fwd_kernel<TY, KK, SS>), g, b, 0, s, total, H, W, K, S, OH, OW, \
+                       static_cast<const TY*>(x), static_cast<TY*>(y), argmax)
+    if (dt == DT_F32) {
+        if (K == 2 && S == 2) POOL_FWD(float, 2, 2);
+        else if (K == 3 && S == 2) POOL_FWD(float, 3, 2);
+        else POOL_FWD(float, 0, 0);
+    } else {
+        if (K == 2 && S == 2) POOL_FWD(bf16_t, 2, 2);
+        else if (K == 3 && S == 2) POOL_FWD(bf16_t, 3, 2);
+        else POOL_FWD(bf16_t, 0, 0);
+    }
+#undef POOL_FWD
     return hipGetLastError();
 }
 
 // One thread per input element: the sum, in ascending window order, of the output gradients
 // of the windows whose maximum sits here (windows overlap when S < K), times the ReLU mask of
 // the layer that produced the pooled tensor.  Gathering keeps the result free of atomics.
-template <typename T>
-__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, int K, int S,
+template <typename T, int KT, int ST>
+__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, int Kr, int Sr,
                                                        int OH, int OW,
                                                        const uint8_t* __restrict__ argmax,
                                                        const T* __restrict__ dy,
@@ -94,23 +114,34 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, 
                                                        const void* __restrict__ mask,
                                                        int mask_f32)
 {
+    const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
     const int t = blockIdx.x * 256 + threadIdx.x;
     if (t >= total) return;
-    const int hw_in = H * W;
-    const int nc = t / hw_in, hw = t - nc * hw_in, h = hw / W, w = hw - h * W;
-    // windows i with i*S <= h <= i*S + K - 1
-    const int ilo = h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S;
-    const int ihi = min(h / S, OH - 1);
-    const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
-    const int jhi = min(w / S, OW - 1);
-    float acc = 0.f;
+    const unsigned hw_in = H * W;
+    const unsigned nc = (unsigned)t / hw_in, hw = (unsigned)t - nc * hw_in;
+    const int h = (int)(hw / W), w = (int)(hw - (hw / W) * W);
     const long long base = (long long)nc * OH * OW;
-    for (int i = ilo; i <= ihi; ++i)
-        for (int j = jlo; j <= jhi; ++j) {
+    float acc = 0.f;
+    if (KT > 0 && KT == ST) {
+        // non-overlapping windows: at most one window holds this element
+        const int i = h / KT, j = w / KT;
+        if (i < OH && j < OW) {
             const long long o = base + (long long)i * OW + j;
-            const int here = (h - i * S) * K + (w - j * S);
-            if (argmax[o] == here) acc += to_f32<T>(dy[o]);
+            if (argmax[o] == (h - i * KT) * KT + (w - j * KT)) acc = to_f32<T>(dy[o]);
         }
+    } else {
+        // windows i with i*S <= h <= i*S + K - 1
+        const int ilo = h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S;
+        const int ihi = min(h / S, OH - 1);
+        const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
+        const int jhi = min(w / S, OW - 1);
+        for (int i = ilo; i <= ihi; ++i)
+            for (int j = jlo; j <= jhi; ++j) {
+                const long long o = base + (long long)i * OW + j;
+                const int here = (h - i * S) * K + (w - j * S);
+                if (argmax[o] == here) acc += to_f32<T>(dy[o]);
+            }
+    }
     if (mask) {
         const float m = mask_f32 ? static_cast<const float*>(mask)[t]
                                  : to_f32<T>(static_cast<const T*>(mask)[t]);
@@ -125,14 +156,21 @@ hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
     const int total = N * C * H * W;
     if (total <= 0) return hipSuccess;
-    if (dt == DT_F32)
-        hipLaunchKernelGGL(pool_bwd_kernel<float>, dim3(grid_for(total, 256)), dim3(256), 0, s,
-                           total, H, W, K, S, OH, OW, argmax, static_cast<const float*>(dy),
-                           static_cast<float*>(dx), mask, (int)mask_f32);
-    else
-        hipLaunchKernelGGL(pool_bwd_kernel<bf16_t>, dim3(grid_for(total, 256)), dim3(256), 0, s,
-                           total, H, W, K, S, OH, OW, argmax, static_cast<const bf16_t*>(dy),
-                           static_cast<bf16_t*>(dx), mask, (int)mask_f32);
+    dim3 g(grid_for(total, 256)), b(256);
+#define POOL_BWD(TY, KK, SS)                                                                   \
+    hipLaunchKernelGGL((pool_bwd_kernel<TY, KK, SS>), g, b, 0, s, total, H, W, K, S, OH, OW,  \
+                       argmax, static_cast<const TY*>(dy), static_cast<TY*>(dx), mask,        \
+                       (int)mask_f32)
+    if (dt == DT_F32) {
+        if (K == 2 && S == 2) POOL_BWD(float, 2, 2);
+        else if (K == 3 && S == 2) POOL_BWD(float, 3, 2);
+        else POOL_BWD(float, 0, 0);
+    } else {
+        if (K == 2 && S == 2) POOL_BWD(bf16_t, 2, 2);
+        else if (K == 3 && S == 2) POOL_BWD(bf16_t, 3, 2);
+        else POOL_BWD(bf16_t, 0, 0);
+    }
+#undef POOL_BWD
     return hipGetLastError();
 }
 
@@ -154,68 +192,82 @@ __device__ __forceinline__ float wave_sum(float v)
 
 // One wave per sample: loss = logsumexp(z) - z[y] with the row maximum subtracted, and
 // dz = (softmax(z) - onehot(y)) / Nb (the gradient of the shard-mean loss), stored in the
-// compute type.
+// compute type.  With loss_out set, the batch-mean loss is formed in the same launch: every
+// block writes the sum of its four rows, and the block that finishes last adds those block sums
+// in block order (a counter in `sync` elects it and is reset by it), so the value does not
+// depend on the order in which blocks run.
 template <typename T>
 __global__ __launch_bounds__(256) void softmax_xent_kernel(int B, int NC, float inv_nb,
                                                            const float* __restrict__ z,
                                                            const int32_t* __restrict__ labels,
-                                                           float* __restrict__ loss_rows,
-                                                           T* __restrict__ dz)
+                                                           T* __restrict__ dz,
+                                                           float* __restrict__ block_sums,
+                                                           unsigned* __restrict__ sync,
+                                                           float* __restrict__ loss_out)
 {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    __shared__ float rows[4];
+    __shared__ bool last;
+    const int wave = threadIdx.x >> 6;
+    const int row = blockIdx.x * 4 + wave;
     const int lane = threadIdx.x & 63;
-    if (row >= B) return;
-    const float* zr = z + (long long)row * NC;
-    float m = -INFINITY;
-    for (int c = lane; c < NC; c += 64) m = fmaxf(m, zr[c]);
-    m = wave_max(m);
-    float se = 0.f;
-    for (int c = lane; c < NC; c += 64) se += expf(zr[c] - m);
-    se = wave_sum(se);
-    const float lse = m + logf(se);
-    const int y = labels[row];
-    const bool valid = y >= 0 && y < NC;
-    for (int c = lane; c < NC; c += 64) {
-        const float p = expf(zr[c] - lse);
-        dz[(long long)row * NC + c] = from_f32<T>((p - (c == y ? 1.f : 0.f)) * inv_nb);
+    float loss = 0.f;
+    if (row < B) {
+        const float* zr = z + (long long)row * NC;
+        float m = -INFINITY;
+        for (int c = lane; c < NC; c += 64) m = fmaxf(m, zr[c]);
+        m = wave_max(m);
+        float se = 0.f;
+        for (int c = lane; c < NC; c += 64) se += expf(zr[c] - m);
+        se = wave_sum(se);
+        const float lse = m + logf(se);
+        const int y = labels[row];
+        const bool valid = y >= 0 && y < NC;
+        for (int c = lane; c < NC; c += 64) {
+            const float p = expf(zr[c] - lse);
+            dz[(long long)row * NC + c] = from_f32<T>((p - (c == y ? 1.f : 0.f)) * inv_nb);
+        }
+        loss = valid ? lse - zr[y] : __int_as_float(0x7fc00000);
     }
-    if (lane == 0) loss_rows[row] = valid ? lse - zr[y] : __int_as_float(0x7fc00000);
+    if (!loss_out) return;
+    if (lane == 0) rows[wave] = loss;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(&block_sums[blockIdx.x], ((rows[0] + rows[1]) + rows[2]) + rows[3],
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __threadfence();
+        last = atomicAdd(sync, 1u) == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!last) return;
+    // the last block: every thread fetches block sums k = tid, tid+256, ... and adds them in
+    // that order; thread 0 then adds the 256 results in thread order.
+    __shared__ float part[256];
+    __threadfence();
+    float acc = 0.f;
+    for (unsigned k = threadIdx.x; k < gridDim.x; k += 256)
+        acc += __hip_atomic_load(&block_sums[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float tot = 0.f;
+        for (int k = 0; k < 256; ++k) tot += part[k];
+        loss_out[0] = tot / (float)B;
+        *sync = 0u;
+    }
 }
 
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
-                        const int32_t* labels, float* loss_rows, void* dz, hipStream_t s)
+                        const int32_t* labels, void* dz, float* block_sums, unsigned* sync,
+                        float* loss_out, hipStream_t s)
 {
     const float inv = 1.0f / (float)Nb;
     dim3 grid((B + 3) / 4);
     if (dt == DT_F32)
         hipLaunchKernelGGL(softmax_xent_kernel<float>, grid, dim3(256), 0, s, B, NC, inv, logits,
-                           labels, loss_rows, static_cast<float*>(dz));
+                           labels, static_cast<float*>(dz), block_sums, sync, loss_out);
     else
         hipLaunchKernelGGL(softmax_xent_kernel<bf16_t>, grid, dim3(256), 0, s, B, NC, inv,
-                           logits, labels, loss_rows, static_cast<bf16_t*>(dz));
-    return hipGetLastError();
-}
-
-// Mean of the per-sample losses in a fixed order (one block): the batch-mean loss, which is
-// also the mean of the R shard-mean losses since the shards are equal.
-__global__ __launch_bounds__(256) void mean_loss_kernel(const float* __restrict__ rows, int B,
-                                                        float* __restrict__ out)
-{
-    __shared__ float sh[256];
-    float s = 0.f;
-    for (int i = threadIdx.x; i < B; i += 256) s += rows[i];
-    sh[threadIdx.x] = s;
-    __syncthreads();
-    for (int o = 128; o >= 1; o >>= 1) {
-        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) out[0] = sh[0] / (float)B;
-}
-
-hipError_t mean_loss(const float* loss_rows, int B, float* loss_out, hipStream_t s)
-{
-    hipLaunchKernelGGL(mean_loss_kernel, dim3(1), dim3(256), 0, s, loss_rows, B, loss_out);
+                           logits, labels, static_cast<bf16_t*>(dz), block_sums, sync, loss_out);
     return hipGetLastError();
 }
 

@@ -317,6 +317,111 @@ template <typename T> struct ConvWgrad {
 };
 
 // ------------------------------------------------------------------------------------------
+// Convolution data gradient in two passes, for convolutions whose implicit data-gradient GEMM
+// would spend much of its reduction on taps outside dy (unpadded convolutions): first
+//   col[g][(ci, u, v)][(image, oh, ow)] = sum_co W[g*og + co][ci][u][v] * dy[image][g*og + co][oh][ow]
+// as an exact GEMM (p = (ci, u, v), q = (image, oh, ow), k = co; both operands row-fast), then
+// col2im_kernel gathers dx from it.  col is fp32, [G][cg*K*K][N*OH*OW].
+// ------------------------------------------------------------------------------------------
+template <typename T> struct ConvDgradCol {
+    typedef T TT;
+    static constexpr bool P_IS_A = false;
+    static constexpr bool P_ROW_FAST = true, Q_ROW_FAST = true;
+    static constexpr bool KTAB = false, QTAB = false;
+    struct PR { int base; bool ok; };
+    __device__ static PR pr(const GemmArgs& a, const Ctx& c, int p)
+    {
+        return PR{c.grp * a.og * a.cg * a.KK + p, p < a.Pdim};
+    }
+    __device__ static T p_atr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
+    {
+        return B.at(s.ok && k < c.kend, s.base + k * a.cg * a.KK);
+    }
+    struct QR { int base; bool ok; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx& c, int q)
+    {
+        const unsigned ohw = a.OH * a.OW;
+        const bool ok = q < a.Qdim;
+        const unsigned qq = ok ? q : 0;
+        const unsigned b = qq / ohw, hw = qq - b * ohw;
+        return QR{(int)((b * a.OC + c.grp * a.og) * ohw + hw), ok};
+    }
+    template <bool TAB>
+    __device__ static T q_at(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
+    {
+        return B.at(s.ok && k < c.kend, s.base + k * a.OH * a.OW);
+    }
+    __device__ static void store(const GemmArgs& a, const Ctx& c, int p, int q, float acc)
+    {
+        static_cast<float*>(a.out)[((long long)c.grp * a.Pdim + p) * a.Qdim + q] = acc;
+    }
+};
+
+// dx[b][ci][h][w] = sum over (u, v) in ascending order of col[g][(ci', u, v)][(b, oh, ow)] with
+// oh*stride = h + pad - u (likewise for columns), times the ReLU mask of the layer below.
+// KT > 0: kernel size known at compile time, stride 1 (the loops unroll; no division).
+template <typename T, int KT>
+__global__ __launch_bounds__(256) void col2im_kernel(const GemmArgs a, const float* __restrict__ col)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int total = a.N * a.C * a.H * a.W;
+    if (t >= total) return;
+    const unsigned hw_in = a.H * a.W;
+    const unsigned bc = (unsigned)t / hw_in, hw = (unsigned)t - bc * hw_in;
+    const unsigned b = bc / a.C, ci = bc - b * a.C;
+    const int h = (int)(hw / a.W), w = (int)(hw - (hw / a.W) * a.W);
+    const unsigned grp = ci / a.cg, cl = ci - grp * a.cg;
+    const long long Q = (long long)a.N * a.OH * a.OW;
+    const float* cp = col + ((long long)grp * a.cg * a.KK + (long long)cl * a.KK) * Q +
+                      (long long)b * a.OH * a.OW;
+    float acc = 0.f;
+    if constexpr (KT > 0) {
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            const int oh = h + a.PD - u;
+            const bool okh = (unsigned)oh < (unsigned)a.OH;
+#pragma unroll
+            for (int v = 0; v < KT; ++v) {
+                const int ow = w + a.PD - v;
+                const bool ok = okh && (unsigned)ow < (unsigned)a.OW;
+                const float x = cp[ok ? (long long)(u * KT + v) * Q + oh * a.OW + ow : 0];
+                acc += ok ? x : 0.f;
+            }
+        }
+    } else {
+        for (int u = 0; u < a.K; ++u) {
+            const int th = h + a.PD - u;
+            if (th < 0) break;
+            const int oh = th / a.S;
+            if (oh * a.S != th || oh >= a.OH) continue;
+            for (int v = 0; v < a.K; ++v) {
+                const int tw = w + a.PD - v;
+                if (tw < 0) break;
+                const int ow = tw / a.S;
+                if (ow * a.S != tw || ow >= a.OW) continue;
+                acc += cp[(long long)(u * a.K + v) * Q + oh * a.OW + ow];
+            }
+        }
+    }
+    if (a.mask) {
+        const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[t]
+                                   : to_f32<T>(static_cast<const T*>(a.mask)[t]);
+        if (!(m > 0.f)) acc = 0.f;
+    }
+    static_cast<T*>(a.out)[t] = from_f32<T>(acc);
+}
+
+template <typename T>
+static void launch_col2im(const GemmArgs& c, const float* col, hipStream_t s)
+{
+    const long long total = (long long)c.N * c.C * c.H * c.W;
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (c.S == 1 && c.K == 3) hipLaunchKernelGGL((col2im_kernel<T, 3>), grid, dim3(256), 0, s, c, col);
+    else if (c.S == 1 && c.K == 5) hipLaunchKernelGGL((col2im_kernel<T, 5>), grid, dim3(256), 0, s, c, col);
+    else hipLaunchKernelGGL((col2im_kernel<T, 0>), grid, dim3(256), 0, s, c, col);
+}
+
+// ------------------------------------------------------------------------------------------
 // Fully connected layers
 // ------------------------------------------------------------------------------------------
 
@@ -597,23 +702,36 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
         }
 }
 
-// Second pass of a split reduction: sum the splits of every output in ascending order and
-// apply the operation's epilogue.  blockIdx.y = shard * G + group.
-template <class Op>
+// Second pass of a split reduction: the splits of every output are added in a fixed order and
+// the operation's epilogue is applied.  A block covers 256/SL consecutive outputs of one
+// (shard, group) with SL threads per output: thread l adds splits l, l+SL, l+2SL, ... in
+// ascending order, then the SL partial sums are added in ascending l.  blockIdx.y = shard*G+group.
+template <class Op, int SL>
 __global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
 {
+    constexpr int OPB = 256 / SL;
+    __shared__ float sh[SL][OPB];
     const long long per = (long long)a.Pdim * a.Qdim;
-    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (t >= per) return;
+    const int ol = threadIdx.x % OPB, l = threadIdx.x / OPB;
+    const long long t = (long long)blockIdx.x * OPB + ol;
     const int rg = blockIdx.y;
     Ctx c;
     c.grp = rg % a.G;
     c.r = rg / a.G;
     c.split = 0; c.kbeg = 0; c.kend = a.Kdim; c.b0 = c.r * a.N; c.tab = nullptr;
-    const float* src = a.partial + ((long long)c.r * a.splits * a.G + c.grp) * per + t;
     float s = 0.f;
-    for (int k = 0; k < a.splits; ++k) s += src[(long long)k * a.G * per];
-    Op::store(a, c, (int)(t / a.Qdim), (int)(t % a.Qdim), s);
+    if (t < per) {
+        const float* src = a.partial + ((long long)c.r * a.splits * a.G + c.grp) * per + t;
+        for (int k = l; k < a.splits; k += SL) s += src[(long long)k * a.G * per];
+    }
+    sh[l][ol] = s;
+    __syncthreads();
+    if (l == 0 && t < per) {
+        float tot = sh[0][ol];
+#pragma unroll
+        for (int j = 1; j < SL; ++j) tot += sh[j][ol];
+        Op::store(a, c, (int)(t / a.Qdim), (int)(t % a.Qdim), tot);
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -657,8 +775,15 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     if (e != hipSuccess || a.splits <= 1) return e;
     const long long per = (long long)a.Pdim * a.Qdim;
     const int rg = gz / a.splits;
-    hipLaunchKernelGGL((split_epilogue<Op>), dim3((unsigned)((per + 255) / 256), rg), dim3(256), 0,
-                       s, a);
+    if (a.splits >= 16)
+        hipLaunchKernelGGL((split_epilogue<Op, 16>), dim3((unsigned)((per + 15) / 16), rg),
+                           dim3(256), 0, s, a);
+    else if (a.splits >= 4)
+        hipLaunchKernelGGL((split_epilogue<Op, 4>), dim3((unsigned)((per + 63) / 64), rg),
+                           dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((split_epilogue<Op, 1>), dim3((unsigned)((per + 255) / 256), rg),
+                           dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -714,6 +839,20 @@ GemmDims conv_wgrad_dims(const ConvGeom& g, int R)
 {
     return GemmDims{g.OC / g.G, (g.C / g.G) * g.K * g.K + 1, g.N * g.OH * g.OW, g.G * R, true};
 }
+GemmDims conv_dgrad_col_dims(const ConvGeom& g)
+{
+    return GemmDims{(g.C / g.G) * g.K * g.K, g.N * g.OH * g.OW, g.OC / g.G, g.G, true};
+}
+size_t conv_dgrad_col_elems(const ConvGeom& g)
+{
+    return (size_t)g.C * g.K * g.K * (size_t)g.N * g.OH * g.OW;
+}
+bool conv_dgrad_use_col(const ConvGeom& g)
+{
+    // taps the implicit GEMM visits per useful multiply-add (stride 1: H*W / (OH*OW))
+    const double waste = (double)g.H * g.W / ((double)g.OH * g.OW * g.S * g.S);
+    return waste >= 1.5 && conv_dgrad_col_elems(g) * 4 <= (size_t)512 << 20;
+}
 GemmDims fc_fwd_dims(int B, int IN, int OUT) { return GemmDims{B, OUT, IN, 1, true}; }
 GemmDims fc_dgrad_dims(int B, int IN, int OUT) { return GemmDims{B, IN, OUT, 1, true}; }
 GemmDims fc_wgrad_dims(int Nb, int R, int IN, int OUT) { return GemmDims{OUT, IN + 1, Nb, R, true}; }
@@ -761,6 +900,28 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, v
                             : dispatch<ConvDgrad<bf16_t, true>>(a, p, d.Z, partial, s);
     return dt == DT_F32 ? dispatch<ConvDgrad<float, false>>(a, p, d.Z, partial, s)
                         : dispatch<ConvDgrad<bf16_t, false>>(a, p, d.Z, partial, s);
+}
+
+hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+                          const void* mask, bool mask_f32, float* col, float* partial,
+                          hipStream_t s)
+{
+    GemmArgs a = conv_args(g);
+    a.a = dy; a.b = w; a.out = col;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
+    const GemmDims d = conv_dgrad_col_dims(g);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    hipError_t e = dt == DT_F32 ? dispatch<ConvDgradCol<float>>(a, p, d.Z, partial, s)
+                                : dispatch<ConvDgradCol<bf16_t>>(a, p, d.Z, partial, s);
+    if (e != hipSuccess) return e;
+    GemmArgs c = conv_args(g);
+    c.out = dx; c.mask = mask; c.mask_f32 = mask_f32;
+    if (dt == DT_F32) launch_col2im<float>(c, col, s);
+    else launch_col2im<bf16_t>(c, col, s);
+    return hipGetLastError();
 }
 
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,

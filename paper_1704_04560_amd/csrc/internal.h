@@ -57,6 +57,9 @@ size_t partial_elems(int dt, const GemmDims& d);  // fp32 partial sums a launch 
 GemmDims conv_fwd_dims(const ConvGeom& g);
 GemmDims conv_dgrad_dims(const ConvGeom& g);
 GemmDims conv_wgrad_dims(const ConvGeom& g, int R);
+GemmDims conv_dgrad_col_dims(const ConvGeom& g);
+size_t conv_dgrad_col_elems(const ConvGeom& g);
+bool conv_dgrad_use_col(const ConvGeom& g);  // data gradient through col + col2im
 GemmDims fc_fwd_dims(int B, int IN, int OUT);
 GemmDims fc_dgrad_dims(int B, int IN, int OUT);
 GemmDims fc_wgrad_dims(int Nb, int R, int IN, int OUT);
@@ -66,6 +69,10 @@ hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, cons
                     void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
 hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
                       const void* mask, bool mask_f32, float* partial, hipStream_t s);
+// Data gradient through an fp32 col buffer of conv_dgrad_col_elems() elements.
+hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+                          const void* mask, bool mask_f32, float* col, float* partial,
+                          hipStream_t s);
 // Weight and bias gradient of R shards of g.N images each; x and dy point at the first shard.
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
                       float* grads, long long ld, long long w_off, long long b_off,
@@ -84,9 +91,11 @@ hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void*
                     uint8_t* argmax, hipStream_t s);
 hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8_t* argmax,
                     const void* dy, void* dx, const void* mask, bool mask_f32, hipStream_t s);
+// Softmax cross-entropy of B rows; with loss_out set, also the batch-mean loss (block_sums holds
+// ceil(B/4) floats; *sync must be 0 before the first launch and is 0 again after every launch).
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
-                        const int32_t* labels, float* loss_rows, void* dz, hipStream_t s);
-hipError_t mean_loss(const float* loss_rows, int B, float* loss_out, hipStream_t s);
+                        const int32_t* labels, void* dz, float* block_sums, unsigned* sync,
+                        float* loss_out, hipStream_t s);
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
                           float lr, float mu, float* avg, bool update, hipStream_t s);
 

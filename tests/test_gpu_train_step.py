@@ -75,9 +75,22 @@ def test_lenet_config():
     run_case("lenet", wl.LENET, 4, 64, 2, 4, 0.01, 0.9)
 
 
+def _tiny_unpadded(dtype):
+    """Unpadded convolutions below the first layer, grouped and strided: their data gradient
+    goes through the col + col2im path."""
+    layers = (wl.conv(4, 3, pad=1, relu=True), wl.conv(6, 5, stride=2, groups=2, relu=True),
+              wl.conv(4, 3, groups=2), wl.fc(5, relu=True), wl.fc(3))
+    return wl.Net("tiny2", (2, 11, 11), layers, dtype, "normal")
+
+
 @pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
 def test_every_layer_type(dtype):
     run_case(f"tiny-{dtype}", _tiny(dtype), 3, 5, 2, 5, 0.05, 0.9)
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_unpadded_grouped_strided_convolutions(dtype):
+    run_case(f"tiny2-{dtype}", _tiny_unpadded(dtype), 2, 3, 2, 6, 0.05, 0.9)
 
 
 def test_cifar_shapes_reduced_batch():

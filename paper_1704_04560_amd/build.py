@@ -14,7 +14,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmtx.so")
-SOURCES = ["api.hip", "igemm.hip", "elementwise.hip"]
+SOURCES = ["api.hip", "plan.hip", "igemm_fwd.hip", "igemm_dgrad.hip", "igemm_wgrad.hip",
+           "elementwise.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

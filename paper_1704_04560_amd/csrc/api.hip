@@ -44,6 +44,7 @@ int hip_fail(hipError_t e, const char* what)
 constexpr size_t kAlign = 256;
 constexpr long long kMaxIndex = 2147483647LL;  // kernels index tensors with 32-bit ints
 constexpr long long kMaxBytes = 2147483647LL;  // and read them through 32-bit buffer offsets
+constexpr int kFarLimit = 8192;  // spatial sizes stay far below the kernels' out-of-window marker
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -54,9 +55,15 @@ struct LayerPlan {
     size_t in_elems, out_elems;  // per sample
     bool act_f32;                // stored output is fp32 (always in fp32 mode; logits)
     bool dgrad_col;              // convolution data gradient through col + col2im
+    bool need_dx;                // the data gradient of this layer's input is computed
+    bool nhwc;                   // stored output is NHWC (convolution and pooling layers)
+    int perm_c, perm_hw;         // fully connected after a spatial layer: input in (h, w, c)
     size_t act_off;              // workspace byte offset of the output [B][...]
     size_t am_off;               // max-pool decisions [B][...] (uint8)
+    size_t fw_off, bw_off;       // prepared forward / data-gradient weights (elements)
 };
+
+constexpr size_t kNone = ~(size_t)0;
 
 struct Plan {
     int R = 0, Nb = 0, B = 0, dt = 0;
@@ -64,8 +71,13 @@ struct Plan {
     size_t P = 0, ld = 0;
     std::vector<LayerPlan> L;
     int first_param = -1;
-    size_t x16_off = 0, w16_off = 0, dbuf_off[2] = {0, 0}, loss_off = 0, partial_off = 0;
-    size_t col_off = 0, sync_off = 0;
+    bool x_convert = false;      // the input is converted (layout and/or type) before use
+    int x_c = 1, x_hw = 1;       // conversion as NCHW -> NHWC with these channels / positions
+    std::vector<PrepJob> jobs;   // weight preparation
+    int prep_blocks = 0;
+    size_t prep_elems = 0;
+    size_t xin_off = 0, prep_off = 0, jobs_off = 0, dbuf_off[2] = {0, 0}, loss_off = 0;
+    size_t partial_off = 0, col_off = 0, sync_off = 0;
     size_t ws_bytes = 0;
 };
 
@@ -146,6 +158,74 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     pl.P = off;
     pl.ld = align_up(off, 64);
 
+    // which layers propagate a data gradient, output layouts, input permutations
+    for (size_t i = 0; i < pl.L.size(); ++i) {
+        LayerPlan& lp = pl.L[i];
+        lp.need_dx = (int)i > pl.first_param && pl.first_param >= 0;
+        lp.nhwc = lp.kind != MTX_FC;
+        lp.perm_c = 1;
+        lp.perm_hw = 1;
+        if (lp.kind == MTX_FC && i > 0 && pl.L[i - 1].nhwc && lp.c > 1 && lp.h * lp.w > 1) {
+            lp.perm_c = lp.c;
+            lp.perm_hw = lp.h * lp.w;
+        }
+        if (lp.kind != MTX_FC && (lp.h >= kFarLimit || lp.w >= kFarLimit))
+            return fail(MTX_EINVAL, "layer %d: spatial size must be below %d", (int)i, kFarLimit);
+    }
+    const LayerPlan& first = pl.L.front();
+    if (first.kind == MTX_FC) {
+        pl.x_c = 1;
+        pl.x_hw = (int)first.in_elems;
+    } else {
+        pl.x_c = pl.in_c;
+        pl.x_hw = pl.in_h * pl.in_w;
+    }
+    pl.x_convert = pl.dt == MTX_BF16 || (pl.x_c > 1 && pl.x_hw > 1);
+
+    // weight preparation jobs; every prepared tensor starts 16-byte aligned
+    size_t pe = 0;
+    int blocks = 0;
+    pl.jobs.clear();
+    auto add_job = [&](PrepJob j) {
+        j.dst = (long long)pe;
+        j.block0 = blocks;
+        prep_fill_divisors(j);
+        blocks += prep_blocks(j.n);
+        pe = align_up(pe + (size_t)j.n, 8);
+        pl.jobs.push_back(j);
+        return (size_t)j.dst;
+    };
+    for (size_t i = 0; i < pl.L.size(); ++i) {
+        LayerPlan& lp = pl.L[i];
+        lp.fw_off = lp.bw_off = kNone;
+        if (!lp.w_len) continue;
+        PrepJob j{};
+        j.n = (int)lp.w_len;
+        j.src = (long long)lp.w_off;
+        if (lp.kind == MTX_CONV) {
+            j.g = lp.g; j.cg = lp.c / lp.g; j.og = lp.oc / lp.g; j.KK = lp.k * lp.k;
+            j.kind = PREP_CONV_F;
+            lp.fw_off = add_job(j);
+            if (lp.need_dx) {
+                ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+                lp.dgrad_col = conv_dgrad_use_col(gb);
+                j.kind = lp.dgrad_col ? PREP_CONV_C : PREP_CONV_D;
+                lp.bw_off = add_job(j);
+            }
+        } else {
+            if (lp.perm_c > 1) {
+                j.kind = PREP_FC_PERM;
+                j.C = lp.perm_c; j.HW = lp.perm_hw; j.IN = (int)lp.in_elems;
+            } else {
+                j.kind = PREP_CAST;
+            }
+            lp.fw_off = add_job(j);
+            lp.bw_off = lp.fw_off;
+        }
+    }
+    pl.prep_blocks = blocks;
+    pl.prep_elems = pe;
+
     // workspace carve-up
     size_t ws = 0;
     size_t max_grad = (size_t)last.oc;  // data-gradient buffers: dz and every layer's input
@@ -168,31 +248,34 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             ConvGeom gs = gb;
             gs.N = pl.Nb;
-            dims[nd++] = conv_fwd_dims(gb);
-            lp.dgrad_col = conv_dgrad_use_col(gb);
-            if (lp.dgrad_col) {
-                dims[nd++] = conv_dgrad_col_dims(gb);
-                if (conv_dgrad_col_elems(gb) > max_col) max_col = conv_dgrad_col_elems(gb);
-            } else {
-                dims[nd++] = conv_dgrad_dims(gb);
+            dims[nd++] = conv_fwd_dims(pl.dt, gb);
+            if (lp.need_dx) {
+                if (lp.dgrad_col) {
+                    dims[nd++] = conv_dgrad_col_dims(pl.dt, gb);
+                    if (conv_dgrad_col_elems(gb) > max_col) max_col = conv_dgrad_col_elems(gb);
+                } else {
+                    dims[nd++] = conv_dgrad_dims(pl.dt, gb);
+                }
             }
-            dims[nd++] = conv_wgrad_dims(gs, pl.R);
+            dims[nd++] = conv_wgrad_dims(pl.dt, gs, pl.R);
         } else if (lp.kind == MTX_FC) {
-            dims[nd++] = fc_fwd_dims(pl.B, (int)lp.in_elems, lp.oc);
-            dims[nd++] = fc_dgrad_dims(pl.B, (int)lp.in_elems, lp.oc);
-            dims[nd++] = fc_wgrad_dims(pl.Nb, pl.R, (int)lp.in_elems, lp.oc);
+            dims[nd++] = fc_fwd_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
+            if (lp.need_dx) dims[nd++] = fc_dgrad_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
+            dims[nd++] = fc_wgrad_dims(pl.dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc);
         }
         for (int k = 0; k < nd; ++k) {
-            const size_t pe = partial_elems(pl.dt, dims[k]);
-            if (pe > max_partial) max_partial = pe;
+            const size_t pz = partial_elems(pl.dt, dims[k]);
+            if (pz > max_partial) max_partial = pz;
         }
     }
-    if (pl.dt == MTX_BF16) {
-        pl.x16_off = ws;
-        ws = align_up(ws + (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B * 2, kAlign);
-        pl.w16_off = ws;
-        ws = align_up(ws + pl.P * 2, kAlign);
+    if (pl.x_convert) {
+        pl.xin_off = ws;
+        ws = align_up(ws + (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B * es, kAlign);
     }
+    pl.prep_off = ws;
+    ws = align_up(ws + pl.prep_elems * es, kAlign);
+    pl.jobs_off = ws;
+    ws = align_up(ws + pl.jobs.size() * sizeof(PrepJob), kAlign);
     for (int k = 0; k < 2; ++k) {
         pl.dbuf_off[k] = ws;
         ws = align_up(ws + max_grad * pl.B * es, kAlign);
@@ -432,6 +515,9 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     hipError_t e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
+    if (e == hipSuccess && !m->pl.jobs.empty())
+        e = hipMemcpyAsync(m->ws + m->pl.jobs_off, m->pl.jobs.data(),
+                           m->pl.jobs.size() * sizeof(PrepJob), hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         delete m;
@@ -489,20 +575,22 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     const Dt dt = (Dt)pl.dt;
     const bool bf = pl.dt == MTX_BF16;
     char* ws = m->ws;
-    const void* wT = bf ? static_cast<const void*>(ws + pl.w16_off) : static_cast<const void*>(m->w);
-    const void* x_in = bf ? static_cast<const void*>(ws + pl.x16_off) : static_cast<const void*>(x);
     const size_t es = bf ? 2 : 4;
+    const char* prep = ws + pl.prep_off;
+    const void* x_in = pl.x_convert ? static_cast<const void*>(ws + pl.xin_off)
+                                    : static_cast<const void*>(x);
 
-    if (bf) {
-        HIP_TRY(launch_site(m, "cast_w", -1, s, [&] { return cast_bf16(m->w, ws + pl.w16_off, pl.P, s); }),
-                "cast weights");
-        HIP_TRY(launch_site(m, "cast_x", -1, s, [&] {
-                    return cast_bf16(x, ws + pl.x16_off, (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B, s);
-                }), "cast input");
-    }
-    auto wptr = [&](const LayerPlan& lp) {
-        return static_cast<const char*>(wT) + lp.w_off * es;
-    };
+    // ---- weights in the layouts the GEMMs read, input in the compute type and layout ----
+    HIP_TRY(launch_site(m, "prep_w", -1, s, [&] {
+                return prep_weights(dt, reinterpret_cast<const PrepJob*>(ws + pl.jobs_off),
+                                    (int)pl.jobs.size(), pl.prep_blocks, m->w, ws + pl.prep_off, s);
+            }), "weight preparation");
+    if (pl.x_convert)
+        HIP_TRY(launch_site(m, "prep_x", -1, s, [&] {
+                    return to_nhwc(dt, x, ws + pl.xin_off, pl.B, pl.x_c, pl.x_hw, s);
+                }), "input conversion");
+    auto fwd_w = [&](const LayerPlan& lp) { return prep + lp.fw_off * es; };
+    auto bwd_w = [&](const LayerPlan& lp) { return prep + lp.bw_off * es; };
     float* partial = reinterpret_cast<float*>(ws + pl.partial_off);
     // ---- forward, all R shards at once (the weights are shared) ----
     const void* in = x_in;
@@ -513,11 +601,11 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
-                        return conv_fwd(dt, g, in, wptr(lp), bias, out, lp.act_f32, lp.relu, partial, s);
+                        return conv_fwd(dt, g, in, fwd_w(lp), bias, out, lp.act_f32, lp.relu, partial, s);
                     }), "conv forward");
         } else if (lp.kind == MTX_FC) {
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
-                        return fc_fwd(dt, pl.B, (int)lp.in_elems, lp.oc, in, wptr(lp), bias, out,
+                        return fc_fwd(dt, pl.B, (int)lp.in_elems, lp.oc, in, fwd_w(lp), bias, out,
                                       lp.act_f32, lp.relu, partial, s);
                     }), "fc forward");
         } else {
@@ -545,7 +633,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     for (int l = (int)pl.L.size() - 1; l >= pl.first_param && l >= 0; --l) {
         const LayerPlan& lp = pl.L[l];
         const void* in_l = l == 0 ? x_in : static_cast<const void*>(ws + pl.L[l - 1].act_off);
-        const bool need_dx = l > pl.first_param;
+        const bool need_dx = lp.need_dx;
         const void* mask = (l > 0 && pl.L[l - 1].relu) ? ws + pl.L[l - 1].act_off : nullptr;
         const bool mask_f32 = l > 0 && pl.L[l - 1].act_f32;
         if (lp.kind == MTX_CONV) {
@@ -559,20 +647,21 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                 float* col = reinterpret_cast<float*>(ws + pl.col_off);
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
                             return lp.dgrad_col
-                                       ? conv_dgrad_col(dt, g, cur, wptr(lp), nxt, mask, mask_f32,
+                                       ? conv_dgrad_col(dt, g, cur, bwd_w(lp), nxt, mask, mask_f32,
                                                         col, partial, s)
-                                       : conv_dgrad(dt, g, cur, wptr(lp), nxt, mask, mask_f32,
+                                       : conv_dgrad(dt, g, cur, bwd_w(lp), nxt, mask, mask_f32,
                                                     partial, s);
                         }), "conv data gradient");
             }
         } else if (lp.kind == MTX_FC) {
             HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
-                        return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, in_l, cur, m->grads,
-                                        ld, (long long)lp.w_off, (long long)lp.b_off, partial, s);
+                        return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, lp.perm_c,
+                                        lp.perm_hw, in_l, cur, m->grads, ld, (long long)lp.w_off,
+                                        (long long)lp.b_off, partial, s);
                     }), "fc weight gradient");
             if (need_dx)
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
-                            return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, cur, wptr(lp), nxt,
+                            return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, cur, bwd_w(lp), nxt,
                                             mask, mask_f32, partial, s);
                         }), "fc data gradient");
         } else {
@@ -730,6 +819,8 @@ int mtx_set_params(mtx_model* m, const float* w_host, const float* v_host)
     return MTX_OK;
 }
 
+// Host copy of a stored layer output in NCHW order (NHWC on the device for convolution and
+// pooling layers), as fp32.
 int mtx_get_layer_output(const mtx_model* m, int layer, float* dst_host, size_t n)
 {
     if (!m || !dst_host) return fail(MTX_EINVAL, "model and dst_host must not be NULL");
@@ -738,24 +829,36 @@ int mtx_get_layer_output(const mtx_model* m, int layer, float* dst_host, size_t 
     const size_t cnt = lp.out_elems * m->pl.B;
     if (n < cnt) return fail(MTX_EINVAL, "dst_host holds %zu elements, %zu needed", n, cnt);
     HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
-    if (lp.act_f32) {
-        HIP_TRY(hipMemcpy(dst_host, m->ws + lp.act_off, cnt * 4, hipMemcpyDeviceToHost), "copy");
-        return MTX_OK;
-    }
+    std::vector<float> dev;
     std::vector<uint16_t> tmp;
     try {
-        tmp.resize(cnt);
+        dev.resize(cnt);
+        if (!lp.act_f32) tmp.resize(cnt);
     } catch (...) {
         return fail(MTX_ENOMEM, "host allocation failed");
     }
-    HIP_TRY(hipMemcpy(tmp.data(), m->ws + lp.act_off, cnt * 2, hipMemcpyDeviceToHost), "copy");
-    for (size_t i = 0; i < cnt; ++i) {
-        const uint32_t u = static_cast<uint32_t>(tmp[i]) << 16;
-        std::memcpy(&dst_host[i], &u, 4);
+    if (lp.act_f32) {
+        HIP_TRY(hipMemcpy(dev.data(), m->ws + lp.act_off, cnt * 4, hipMemcpyDeviceToHost), "copy");
+    } else {
+        HIP_TRY(hipMemcpy(tmp.data(), m->ws + lp.act_off, cnt * 2, hipMemcpyDeviceToHost), "copy");
+        for (size_t i = 0; i < cnt; ++i) {
+            const uint32_t u = static_cast<uint32_t>(tmp[i]) << 16;
+            std::memcpy(&dev[i], &u, 4);
+        }
     }
+    if (!lp.nhwc) {
+        std::memcpy(dst_host, dev.data(), cnt * 4);
+        return MTX_OK;
+    }
+    const size_t C = lp.oc, HW = (size_t)lp.oh * lp.ow;
+    for (size_t b = 0; b < (size_t)m->pl.B; ++b)
+        for (size_t hw = 0; hw < HW; ++hw)
+            for (size_t c = 0; c < C; ++c)
+                dst_host[(b * C + c) * HW + hw] = dev[(b * HW + hw) * C + c];
     return MTX_OK;
 }
 
+// Host copy of a max-pooling layer's window decisions in NCHW order.
 int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t n)
 {
     if (!m || !dst_host) return fail(MTX_EINVAL, "model and dst_host must not be NULL");
@@ -765,7 +868,18 @@ int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t
     const size_t cnt = lp.out_elems * m->pl.B;
     if (n < cnt) return fail(MTX_EINVAL, "dst_host holds %zu elements, %zu needed", n, cnt);
     HIP_TRY(hipStreamSynchronize(m->last_stream), "synchronise");
-    HIP_TRY(hipMemcpy(dst_host, m->ws + lp.am_off, cnt, hipMemcpyDeviceToHost), "copy");
+    std::vector<uint8_t> dev;
+    try {
+        dev.resize(cnt);
+    } catch (...) {
+        return fail(MTX_ENOMEM, "host allocation failed");
+    }
+    HIP_TRY(hipMemcpy(dev.data(), m->ws + lp.am_off, cnt, hipMemcpyDeviceToHost), "copy");
+    const size_t C = lp.oc, HW = (size_t)lp.oh * lp.ow;
+    for (size_t b = 0; b < (size_t)m->pl.B; ++b)
+        for (size_t hw = 0; hw < HW; ++hw)
+            for (size_t c = 0; c < C; ++c)
+                dst_host[(b * C + c) * HW + hw] = dev[(b * HW + hw) * C + c];
     return MTX_OK;
 }
 

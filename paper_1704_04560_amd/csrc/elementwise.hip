@@ -1,5 +1,6 @@
-// Memory-bound kernels of the training step: bfloat16 casts, max-pooling, the fused softmax
-// cross-entropy and the fused gradient average + momentum update.  All reductions run in a fixed order, so results
+// Memory-bound kernels of the training step: layout conversions and the per-step weight
+// preparation, max-pooling, the fused softmax cross-entropy and the fused gradient average +
+// momentum update.  All reductions run in a fixed order, so results
 // are identical from run to run.
 #include "device_common.h"
 #include "internal.h"
@@ -38,23 +39,159 @@ hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s)
     return hipGetLastError();
 }
 
-// ---- max-pooling ----------------------------------------------------------------------------
+// ---- layout conversions --------------------------------------------------------------------
+
+__device__ __forceinline__ unsigned fdivu(const FastDiv& f, unsigned n)
+{
+    return (__umulhi(n, f.m) + n) >> f.s;
+}
+
+// dst[n][hw][c] = x[n][c][hw], one thread per destination element (coalesced writes).
+template <typename T>
+__global__ __launch_bounds__(256) void to_nhwc_kernel(const float* __restrict__ x,
+                                                      T* __restrict__ dst, int total, int C,
+                                                      int HW, FastDiv fc, FastDiv fhw)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= total) return;
+    const unsigned pos = fdivu(fc, (unsigned)t), c = (unsigned)t - pos * (unsigned)C;
+    const unsigned n = fdivu(fhw, pos), hw = pos - n * (unsigned)HW;
+    dst[t] = from_f32<T>(x[((long long)n * C + c) * HW + hw]);
+}
+
+hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipStream_t s)
+{
+    const long long total = (long long)N * C * HW;
+    if (total <= 0) return hipSuccess;
+    const FastDiv fc = make_fastdiv((unsigned)C), fhw = make_fastdiv((unsigned)HW);
+    dim3 g(grid_for((size_t)total, 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(to_nhwc_kernel<float>, g, dim3(256), 0, s, x, static_cast<float*>(dst),
+                           (int)total, C, HW, fc, fhw);
+    else
+        hipLaunchKernelGGL(to_nhwc_kernel<bf16_t>, g, dim3(256), 0, s, x,
+                           static_cast<bf16_t*>(dst), (int)total, C, HW, fc, fhw);
+    return hipGetLastError();
+}
+
+// ---- weight preparation ---------------------------------------------------------------------
+// One launch serves every job; job j owns blocks [block0_j, block0_{j+1}) and each block
+// converts kPrepPerBlock consecutive destination elements.  The source index of a destination
+// element follows from its layout (see PrepKind).
+
+constexpr int kPrepPerThread = 4, kPrepPerBlock = 256 * kPrepPerThread;
+
+int prep_blocks(int n) { return (n + kPrepPerBlock - 1) / kPrepPerBlock; }
+
+void prep_fill_divisors(PrepJob& j)
+{
+    switch (j.kind) {
+    case PREP_CONV_F:
+        j.f0 = make_fastdiv((unsigned)(j.KK * j.cg));
+        j.f1 = make_fastdiv((unsigned)j.cg);
+        break;
+    case PREP_CONV_D:
+        j.f0 = make_fastdiv((unsigned)j.og);
+        j.f1 = make_fastdiv((unsigned)j.KK);
+        j.f2 = make_fastdiv((unsigned)j.cg);
+        break;
+    case PREP_CONV_C:
+        j.f0 = make_fastdiv((unsigned)j.og);
+        j.f1 = make_fastdiv((unsigned)j.cg);
+        j.f2 = make_fastdiv((unsigned)j.KK);
+        break;
+    case PREP_FC_PERM:
+        j.f0 = make_fastdiv((unsigned)j.IN);
+        j.f1 = make_fastdiv((unsigned)j.C);
+        break;
+    default:
+        break;
+    }
+}
+
+__device__ __forceinline__ long long prep_src(const PrepJob& j, unsigned d)
+{
+    switch (j.kind) {
+    case PREP_CONV_F: {  // d = co*(KK*cg) + uv*cg + ci
+        const unsigned co = fdivu(j.f0, d), r = d - co * (unsigned)(j.KK * j.cg);
+        const unsigned uv = fdivu(j.f1, r), ci = r - uv * (unsigned)j.cg;
+        return ((long long)co * j.cg + ci) * j.KK + uv;
+    }
+    case PREP_CONV_D: {  // d = ((g*cg + ci)*KK + uv)*og + co
+        const unsigned r1 = fdivu(j.f0, d), co = d - r1 * (unsigned)j.og;
+        const unsigned r2 = fdivu(j.f1, r1), uv = r1 - r2 * (unsigned)j.KK;
+        const unsigned g = fdivu(j.f2, r2), ci = r2 - g * (unsigned)j.cg;
+        return (((long long)g * j.og + co) * j.cg + ci) * j.KK + uv;
+    }
+    case PREP_CONV_C: {  // d = ((g*KK + uv)*cg + ci)*og + co
+        const unsigned r1 = fdivu(j.f0, d), co = d - r1 * (unsigned)j.og;
+        const unsigned r2 = fdivu(j.f1, r1), ci = r1 - r2 * (unsigned)j.cg;
+        const unsigned g = fdivu(j.f2, r2), uv = r2 - g * (unsigned)j.KK;
+        return (((long long)g * j.og + co) * j.cg + ci) * j.KK + uv;
+    }
+    case PREP_FC_PERM: {  // d = o*IN + hw*C + c
+        const unsigned o = fdivu(j.f0, d), r = d - o * (unsigned)j.IN;
+        const unsigned hw = fdivu(j.f1, r), c = r - hw * (unsigned)j.C;
+        return (long long)o * j.IN + (long long)c * j.HW + hw;
+    }
+    default:
+        return d;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void prep_kernel(const PrepJob* __restrict__ jobs, int njobs,
+                                                   const float* __restrict__ w,
+                                                   T* __restrict__ dst)
+{
+    int jx = 0;
+    for (int k = 1; k < njobs; ++k)
+        if (jobs[k].block0 <= (int)blockIdx.x) jx = k;
+    const PrepJob j = jobs[jx];
+    const int base = ((int)blockIdx.x - j.block0) * kPrepPerBlock + threadIdx.x;
+    const float* src = w + j.src;
+    T* out = dst + j.dst;
+#pragma unroll
+    for (int e = 0; e < kPrepPerThread; ++e) {
+        const int d = base + e * 256;
+        if (d < j.n) out[d] = from_f32<T>(src[prep_src(j, (unsigned)d)]);
+    }
+}
+
+hipError_t prep_weights(Dt dt, const PrepJob* jobs, int njobs, int blocks, const float* w,
+                        void* dst, hipStream_t s)
+{
+    if (njobs <= 0 || blocks <= 0) return hipSuccess;
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(prep_kernel<float>, dim3(blocks), dim3(256), 0, s, jobs, njobs, w,
+                           static_cast<float*>(dst));
+    else
+        hipLaunchKernelGGL(prep_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, jobs, njobs, w,
+                           static_cast<bf16_t*>(dst));
+    return hipGetLastError();
+}
+
+// ---- max-pooling over NHWC tensors ------------------------------------------------------------
 // KT / ST > 0: window and stride known at compile time (2/2 and 3/2 are the common cases).
 
-// One thread per output: the first maximal element of the K x K window in row-major order.
+// One thread per output (channels fastest): the first maximal element of the K x K window in
+// row-major window order; argmax holds its window position u*K + v.
 template <typename T, int KT, int ST>
-__global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int H, int W, int Kr, int Sr,
-                                                       int OH, int OW, const T* __restrict__ x,
+__global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, int W, int Kr,
+                                                       int Sr, int OH, int OW, FastDiv fc,
+                                                       FastDiv fow, FastDiv foh,
+                                                       const T* __restrict__ x,
                                                        T* __restrict__ y,
                                                        uint8_t* __restrict__ argmax)
 {
     const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
     const int o = blockIdx.x * 256 + threadIdx.x;
     if (o >= total) return;
-    const unsigned ohw = OH * OW;
-    const unsigned nc = (unsigned)o / ohw, hw = (unsigned)o - nc * ohw;
-    const unsigned i = hw / OW, j = hw - i * OW;
-    const T* xp = x + (long long)nc * H * W + (long long)(i * S) * W + j * S;
+    const unsigned pos = fdivu(fc, (unsigned)o), c = (unsigned)o - pos * (unsigned)C;
+    const unsigned r = fdivu(fow, pos), j = pos - r * (unsigned)OW;
+    const unsigned n = fdivu(foh, r), i = r - n * (unsigned)OH;
+    const T* xp = x + (((long long)n * H + i * S) * W + j * S) * C + c;
+    const long long rs = (long long)W * C;
     T best = xp[0];
     float bv = to_f32<T>(best);
     int bi = 0;
@@ -63,14 +200,14 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int H, int W, 
         for (int u = 0; u < KT; ++u)
 #pragma unroll
             for (int v = 0; v < KT; ++v) {
-                const T t = xp[u * W + v];
+                const T t = xp[u * rs + v * C];
                 const float tv = to_f32<T>(t);
                 if (tv > bv) { bv = tv; best = t; bi = u * KT + v; }
             }
     } else {
         for (int u = 0; u < K; ++u)
             for (int v = 0; v < K; ++v) {
-                const T t = xp[u * W + v];
+                const T t = xp[u * rs + v * C];
                 const float tv = to_f32<T>(t);
                 if (tv > bv) { bv = tv; best = t; bi = u * K + v; }
             }
@@ -85,10 +222,12 @@ hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void*
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
     const int total = N * C * OH * OW;
     if (total <= 0) return hipSuccess;
+    const FastDiv fc = make_fastdiv((unsigned)C), fow = make_fastdiv((unsigned)OW),
+                  foh = make_fastdiv((unsigned)OH);
     dim3 g(grid_for(total, 256)), b(256);
-#define POOL_FWD(TY, KK, SS)                                                                  \
-    hipLaunchKernelGGL((pool_fwd_kernel<TY, KK, SS>), g, b, 0, s, total, H, W, K, S, OH, OW, \
-                       static_cast<const TY*>(x), static_cast<TY*>(y), argmax)
+#define POOL_FWD(TY, KK, SS)                                                                   \
+    hipLaunchKernelGGL((pool_fwd_kernel<TY, KK, SS>), g, b, 0, s, total, C, H, W, K, S, OH, OW, \
+                       fc, fow, foh, static_cast<const TY*>(x), static_cast<TY*>(y), argmax)
     if (dt == DT_F32) {
         if (K == 2 && S == 2) POOL_FWD(float, 2, 2);
         else if (K == 3 && S == 2) POOL_FWD(float, 3, 2);
@@ -102,12 +241,14 @@ hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void*
     return hipGetLastError();
 }
 
-// One thread per input element: the sum, in ascending window order, of the output gradients
-// of the windows whose maximum sits here (windows overlap when S < K), times the ReLU mask of
-// the layer that produced the pooled tensor.  Gathering keeps the result free of atomics.
+// One thread per input element (channels fastest): the sum, in ascending window order, of the
+// output gradients of the windows whose maximum sits here (windows overlap when S < K), times
+// the ReLU mask of the layer that produced the pooled tensor.  Gathering keeps the result free
+// of atomics.
 template <typename T, int KT, int ST>
-__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, int Kr, int Sr,
-                                                       int OH, int OW,
+__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, int W, int Kr,
+                                                       int Sr, int OH, int OW, FastDiv fc,
+                                                       FastDiv fw, FastDiv fh,
                                                        const uint8_t* __restrict__ argmax,
                                                        const T* __restrict__ dy,
                                                        T* __restrict__ dx,
@@ -117,16 +258,17 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, 
     const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
     const int t = blockIdx.x * 256 + threadIdx.x;
     if (t >= total) return;
-    const unsigned hw_in = H * W;
-    const unsigned nc = (unsigned)t / hw_in, hw = (unsigned)t - nc * hw_in;
-    const int h = (int)(hw / W), w = (int)(hw - (hw / W) * W);
-    const long long base = (long long)nc * OH * OW;
+    const unsigned pos = fdivu(fc, (unsigned)t), c = (unsigned)t - pos * (unsigned)C;
+    const unsigned r = fdivu(fw, pos), wu = pos - r * (unsigned)W;
+    const unsigned n = fdivu(fh, r), hu = r - n * (unsigned)H;
+    const int h = (int)hu, w = (int)wu;
+    const long long base = (long long)n * OH * OW;
     float acc = 0.f;
     if (KT > 0 && KT == ST) {
         // non-overlapping windows: at most one window holds this element
         const int i = h / KT, j = w / KT;
         if (i < OH && j < OW) {
-            const long long o = base + (long long)i * OW + j;
+            const long long o = (base + (long long)i * OW + j) * C + c;
             if (argmax[o] == (h - i * KT) * KT + (w - j * KT)) acc = to_f32<T>(dy[o]);
         }
     } else {
@@ -137,7 +279,7 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int H, int W, 
         const int jhi = min(w / S, OW - 1);
         for (int i = ilo; i <= ihi; ++i)
             for (int j = jlo; j <= jhi; ++j) {
-                const long long o = base + (long long)i * OW + j;
+                const long long o = (base + (long long)i * OW + j) * C + c;
                 const int here = (h - i * S) * K + (w - j * S);
                 if (argmax[o] == here) acc += to_f32<T>(dy[o]);
             }
@@ -156,11 +298,13 @@ hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
     const int total = N * C * H * W;
     if (total <= 0) return hipSuccess;
+    const FastDiv fc = make_fastdiv((unsigned)C), fw = make_fastdiv((unsigned)W),
+                  fh = make_fastdiv((unsigned)H);
     dim3 g(grid_for(total, 256)), b(256);
-#define POOL_BWD(TY, KK, SS)                                                                   \
-    hipLaunchKernelGGL((pool_bwd_kernel<TY, KK, SS>), g, b, 0, s, total, H, W, K, S, OH, OW,  \
-                       argmax, static_cast<const TY*>(dy), static_cast<TY*>(dx), mask,        \
-                       (int)mask_f32)
+#define POOL_BWD(TY, KK, SS)                                                                    \
+    hipLaunchKernelGGL((pool_bwd_kernel<TY, KK, SS>), g, b, 0, s, total, C, H, W, K, S, OH, OW, \
+                       fc, fw, fh, argmax, static_cast<const TY*>(dy), static_cast<TY*>(dx),    \
+                       mask, (int)mask_f32)
     if (dt == DT_F32) {
         if (K == 2 && S == 2) POOL_BWD(float, 2, 2);
         else if (K == 3 && S == 2) POOL_BWD(float, 3, 2);

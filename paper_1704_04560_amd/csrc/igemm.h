@@ -1,0 +1,571 @@
+// Implicit-GEMM machinery on the gfx950 matrix cores, shared by the forward, data-gradient and
+// weight-gradient kernel files: operand loaders, LDS tile layout, the tiled MFMA kernel, the
+// split-reduction epilogue and the launch dispatch.  The operations themselves (index maps and
+// epilogues) are in igemm_ops.h.
+//
+// Every operation is C[p][q] = sum_k P[p][k] * Q[q][k].  A block of 256 threads (4 waves in a
+// 2 x 2 grid) computes a 32*FP x 32*FQ tile of C; a wave owns FP x FQ fragments of 16 x 16:
+//   fp32: v_mfma_f32_16x16x4_f32, four per 16-byte LDS read (lane group g supplies
+//         k = 4g + t to the t-th instruction for both operands, so the sum is unchanged);
+//   bf16: v_mfma_f32_16x16x32_bf16, one per 16-byte read (8 values per lane).
+// Fragment output layout: lane l, register v -> row 4*(l/16) + v, column l%16, so each lane
+// ends with four consecutive rows p of one column q.
+//
+// LDS tiles hold BR rows x BK reduction steps, k contiguous, rows padded by 16 bytes; the
+// 16-byte granules of row r are rotated by r/8, which keeps the fragment reads, the 16-byte
+// tile writes and the transposing writes below free of bank conflicts.
+//
+// Operand loaders (per operand, chosen by the operation and the alignment of its tensor):
+//   SK  scalar, k-fast: a thread keeps one k per tile and steps over rows;
+//   SR  scalar, row-fast: a thread keeps one row for the whole kernel and steps over k;
+//   KV  16 bytes along k (one LDS store per load);
+//   RV  16 bytes along the rows (weight-gradient operands, whose reduction index is the
+//       position): the chunk is transposed on its way into LDS (bf16: two loads at k, k+1 are
+//       packed so that every LDS store writes a k pair).
+// All global reads are raw buffer loads: the resource holds the tensor's size and the hardware
+// returns 0 past it, so zero padding, tile tails and invalid rows only select an out-of-range
+// offset, without branches.
+//
+// Reduction splits: when the output tiles alone cannot fill the GPU, the reduction is split
+// over blockIdx.z; every split writes fp32 partial sums and split_epilogue adds them in a
+// fixed order and applies the operation's epilogue (deterministic, no atomics).
+#pragma once
+
+#include <type_traits>
+
+#include "device_common.h"
+#include "internal.h"
+
+namespace mtx {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T> struct Mma;
+
+template <> struct Mma<float> {
+    typedef f32x4 frag;
+    static constexpr int VEC = 4;     // elements per 16 bytes
+    static constexpr int KSTEP = 16;  // k covered by one 16-byte read across the 4 lane groups
+    __device__ __forceinline__ static void run(f32x4& acc, const frag& a, const frag& b)
+    {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc, 0, 0, 0);
+    }
+};
+
+template <> struct Mma<bf16_t> {
+    typedef s16x8 frag;
+    static constexpr int VEC = 8;
+    static constexpr int KSTEP = 32;
+    __device__ __forceinline__ static void run(f32x4& acc, const frag& a, const frag& b)
+    {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                      0, 0);
+    }
+};
+
+// k tile per compute type: two MFMA k steps
+template <typename T> constexpr int tile_k() { return 2 * Mma<T>::KSTEP; }
+
+template <typename T> __device__ __forceinline__ T zero() { return T(0); }
+template <typename T> __device__ __forceinline__ T one();
+template <> __device__ __forceinline__ float one<float>() { return 1.0f; }
+template <> __device__ __forceinline__ bf16_t one<bf16_t>() { return (bf16_t)0x3f80; }
+
+// 16 bytes holding the value 1 followed by zeros (first chunk of a bias row)
+template <typename T> __device__ __forceinline__ u32x4 one_chunk()
+{
+    if constexpr (sizeof(T) == 4) return u32x4{0x3f800000u, 0u, 0u, 0u};
+    else return u32x4{0x3f80u, 0u, 0u, 0u};
+}
+
+__device__ __forceinline__ unsigned fdiv(const FastDiv& f, unsigned n)
+{
+    return (__umulhi(n, f.m) + n) >> f.s;
+}
+
+// ---- buffer loads -------------------------------------------------------------------------
+constexpr unsigned kOOB = 0x80000000u;        // every tensor is smaller than 2 GiB
+constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
+
+template <typename T> struct Buf {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ Buf(const void* p, unsigned bytes)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                              (int)kRsrcWord3))
+    {
+    }
+    __device__ __forceinline__ T at(bool ok, int idx) const
+    {
+        const int off = ok ? idx * (int)sizeof(T) : (int)kOOB;
+        if constexpr (sizeof(T) == 4)
+            return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+        else
+            return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+    }
+    // 16 bytes starting at element idx (idx is a multiple of 16 / sizeof(T))
+    __device__ __forceinline__ u32x4 at16(bool ok, int idx) const
+    {
+        const int off = ok ? idx * (int)sizeof(T) : (int)kOOB;
+        return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    }
+};
+
+constexpr int kFar = 1 << 14;  // window coordinate that fails every bounds test
+
+// One entry of an index table: an element offset and the two window coordinates it stands
+// for (for the zero-padding test).
+struct TabEnt {
+    int off;
+    short u, v;
+};
+
+struct Ctx {
+    int grp, r, split, kbeg, kend, b0;
+    const TabEnt* tab;  // LDS index table over [kbeg, kbeg + kchunk), or null
+};
+
+__device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c)
+{
+    const int z = blockIdx.z;
+    c.grp = z % a.G;
+    const int rest = z / a.G;
+    c.r = rest / a.splits;
+    c.split = rest - c.r * a.splits;
+    c.kbeg = c.split * a.kchunk;
+    c.kend = min(a.Kdim, c.kbeg + a.kchunk);
+    c.b0 = c.r * a.N;
+    c.tab = nullptr;
+}
+
+// ---- epilogue helpers -----------------------------------------------------------------------
+
+// Store np (<= 4) consecutive values at element idx of an fp32 tensor or of a tensor of the
+// compute type; one vector store when all four are present and aligned.
+template <typename T>
+__device__ __forceinline__ void store_vals(void* out, bool f32, int idx, const float* v, int np)
+{
+    if (f32 || sizeof(T) == 4) {
+        float* o = static_cast<float*>(out) + idx;
+        if (np == 4 && (idx & 3) == 0) {
+            *reinterpret_cast<f32x4*>(o) = f32x4{v[0], v[1], v[2], v[3]};
+        } else {
+            for (int i = 0; i < np; ++i) o[i] = v[i];
+        }
+    } else {
+        bf16_t* o = static_cast<bf16_t*>(out) + idx;
+        if (np == 4 && (idx & 3) == 0) {
+            const unsigned lo = (unsigned)f32_to_bf16(v[0]) | ((unsigned)f32_to_bf16(v[1]) << 16);
+            const unsigned hi = (unsigned)f32_to_bf16(v[2]) | ((unsigned)f32_to_bf16(v[3]) << 16);
+            *reinterpret_cast<u32x2*>(o) = u32x2{lo, hi};
+        } else {
+            for (int i = 0; i < np; ++i) o[i] = f32_to_bf16(v[i]);
+        }
+    }
+}
+
+// Zero the values whose ReLU mask (the stored output of the layer below, same index) is not
+// positive.
+template <typename T>
+__device__ __forceinline__ void apply_mask(const GemmArgs& a, int idx, float* v, int np)
+{
+    if (!a.mask) return;
+    for (int i = 0; i < np; ++i) {
+        const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[idx + i]
+                                   : to_f32<T>(static_cast<const T*>(a.mask)[idx + i]);
+        if (!(m > 0.f)) v[i] = 0.f;
+    }
+}
+
+// ---- LDS tile addressing --------------------------------------------------------------------
+template <int BK, int VEC> struct Lds {
+    static constexpr int LDK = BK + VEC;  // row stride (16 bytes of padding)
+    static constexpr int NG = BK / VEC;   // 16-byte granules per row (a power of 2)
+    __device__ __forceinline__ static int at(int row, int k)
+    {
+        const int g = ((k / VEC) + (row >> 3)) & (NG - 1);
+        return row * LDK + g * VEC + (k & (VEC - 1));
+    }
+};
+
+// ---- operand loaders --------------------------------------------------------------------------
+enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3 };
+
+// Per-thread loader state: the operation's type for the (side, loader) pair.
+template <class Op, bool ISP, int KIND> struct LState;
+template <class Op, bool ISP> struct LState<Op, ISP, L_SK> { struct type {}; };
+template <class Op> struct LState<Op, true, L_SR> { typedef typename Op::PR type; };
+template <class Op> struct LState<Op, true, L_KV> { typedef typename Op::PV type; };
+template <class Op> struct LState<Op, true, L_RV> { typedef typename Op::PC type; };
+template <class Op> struct LState<Op, false, L_SR> { typedef typename Op::QR type; };
+template <class Op> struct LState<Op, false, L_KV> { typedef typename Op::QV type; };
+template <class Op> struct LState<Op, false, L_RV> { typedef typename Op::QC type; };
+
+template <class Op, bool ISP, int KIND, int BR, int BK> struct Loader;
+
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_SK, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int RPP = 256 / BK;  // rows per pass
+    static constexpr int N = (BR + RPP - 1) / RPP;
+    T reg[N];
+    __device__ __forceinline__ void init(const GemmArgs&, const Ctx&, int, int) {}
+    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
+                                         int r0, int k0)
+    {
+        const int k = k0 + tid % BK;
+        const int rt = tid / BK;
+        if constexpr (ISP) {
+            const auto s = Op::pk(a, c, k);
+#pragma unroll
+            for (int i = 0; i < N; ++i)
+                if (RPP * N <= BR || rt + i * RPP < BR) reg[i] = Op::p_sk(a, B, c, s, r0 + rt + i * RPP);
+        } else {
+            const auto s = Op::qk(a, c, k);
+#pragma unroll
+            for (int i = 0; i < N; ++i)
+                if (RPP * N <= BR || rt + i * RPP < BR) reg[i] = Op::q_sk(a, B, c, s, r0 + rt + i * RPP);
+        }
+    }
+    __device__ __forceinline__ void stage(T* lds, int tid) const
+    {
+        const int kk = tid % BK, row = tid / BK;
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            if (RPP * N <= BR || row + i * RPP < BR) lds[Lds<BK, VEC>::at(row + i * RPP, kk)] = reg[i];
+    }
+};
+
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_SR, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int KPP = 256 / BR;  // k per pass
+    static constexpr int N = (BK + KPP - 1) / KPP;
+    typename LState<Op, ISP, L_SR>::type s;
+    T reg[N];
+    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
+    {
+        if constexpr (ISP) s = Op::pr(a, c, r0 + tid % BR);
+        else s = Op::qr(a, c, r0 + tid % BR);
+    }
+    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
+                                         int, int k0)
+    {
+        const int k = k0 + tid / BR;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if constexpr (ISP) reg[i] = Op::p_sr(a, B, c, s, k + i * KPP);
+            else reg[i] = Op::q_sr(a, B, c, s, k + i * KPP);
+        }
+    }
+    __device__ __forceinline__ void stage(T* lds, int tid) const
+    {
+        const int row = tid % BR, kk = tid / BR;
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            if (KPP * N <= BK || kk + i * KPP < BK) lds[Lds<BK, VEC>::at(row, kk + i * KPP)] = reg[i];
+    }
+};
+
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KV, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int NG = BK / VEC;   // granules per row
+    static constexpr int RPP = 256 / NG;  // rows per pass
+    static constexpr int N = (BR + RPP - 1) / RPP;
+    typename LState<Op, ISP, L_KV>::type s[N];
+    u32x4 reg[N];
+    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
+    {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int row = r0 + tid / NG + i * RPP;
+            if constexpr (ISP) s[i] = Op::pv(a, c, row);
+            else s[i] = Op::qv(a, c, row);
+        }
+    }
+    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
+                                         int, int k0)
+    {
+        const int k = k0 + (tid % NG) * VEC;
+        const int rt = tid / NG;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (!(RPP * N <= BR || rt + i * RPP < BR)) continue;
+            if constexpr (ISP) reg[i] = Op::p_kv(a, B, c, s[i], k);
+            else reg[i] = Op::q_kv(a, B, c, s[i], k);
+        }
+    }
+    __device__ __forceinline__ void stage(T* lds, int tid) const
+    {
+        const int g = tid % NG, row = tid / NG;
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            if (RPP * N <= BR || row + i * RPP < BR)
+                *reinterpret_cast<u32x4*>(&lds[Lds<BK, VEC>::at(row + i * RPP, g * VEC)]) = reg[i];
+    }
+};
+
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RV, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int KW = sizeof(T) == 2 ? 2 : 1;  // k values per thread step
+    static constexpr int RCH = BR / VEC;                // row chunks per tile
+    static constexpr int KPP = (256 / RCH) * KW;        // k per pass
+    static constexpr int N = (BK + KPP - 1) / KPP;
+    static_assert(BR % VEC == 0 && 256 % RCH == 0, "RV tile");
+    typename LState<Op, ISP, L_RV>::type s;
+    u32x4 reg[N][KW];
+    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
+    {
+        const int row0 = r0 + (tid % RCH) * VEC;
+        if constexpr (ISP) s = Op::pc(a, c, row0);
+        else s = Op::qc(a, c, row0);
+    }
+    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
+                                         int, int k0)
+    {
+        const int kt = (tid / RCH) * KW;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (!(KPP * N <= BK || kt + i * KPP < BK)) continue;  // idle beyond the tile
+#pragma unroll
+            for (int w = 0; w < KW; ++w) {
+                const int k = k0 + kt + i * KPP + w;
+                if constexpr (ISP) reg[i][w] = Op::p_rv(a, B, c, s, k);
+                else reg[i][w] = Op::q_rv(a, B, c, s, k);
+            }
+        }
+    }
+    __device__ __forceinline__ void stage(T* lds, int tid) const
+    {
+        typedef Lds<BK, VEC> L;
+        const int row0 = (tid % RCH) * VEC, kk = (tid / RCH) * KW;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int kb = kk + i * KPP;
+            if (!(KPP * N <= BK || kb < BK)) continue;
+            if constexpr (KW == 1) {
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    reinterpret_cast<unsigned*>(lds)[L::at(row0 + j, kb)] = reg[i][0][j];
+            } else {
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) {
+                    const unsigned w0 = reg[i][0][j >> 1], w1 = reg[i][1][j >> 1];
+                    const unsigned pr = (j & 1) ? ((w0 >> 16) | (w1 & 0xffff0000u))
+                                                : ((w0 & 0xffffu) | (w1 << 16));
+                    *reinterpret_cast<unsigned*>(&lds[L::at(row0 + j, kb)]) = pr;
+                }
+            }
+        }
+    }
+};
+
+// ---- the tiled MFMA kernel --------------------------------------------------------------------
+
+template <class Op, int FP, int FQ, int PK, int QK>
+__global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
+{
+    typedef typename Op::TT T;
+    typedef Mma<T> M;
+    constexpr int BK = tile_k<T>();
+    constexpr int BP = 32 * FP, BQ = 32 * FQ;
+    constexpr int VEC = M::VEC;
+    typedef Lds<BK, VEC> L;
+    static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
+
+    __shared__ __attribute__((aligned(16))) T sP[BP * L::LDK];
+    __shared__ __attribute__((aligned(16))) T sQ[BQ * L::LDK];
+    extern __shared__ TabEnt tab[];  // sized at launch
+
+    Ctx c;
+    decode_z(a, c);
+    const int p0 = blockIdx.y * BP, q0 = blockIdx.x * BQ;
+    const int tid = threadIdx.x;
+
+    if constexpr (Op::TAB) {
+        // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
+        constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+        const int n = a.kchunk / TS;
+        for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
+        c.tab = tab;
+        __syncthreads();
+    }
+
+    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
+    Loader<Op, true, PK, BP, BK> lp;
+    Loader<Op, false, QK, BQ, BK> lq;
+    lp.init(a, c, tid, p0);
+    lq.init(a, c, tid, q0);
+
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wp = wave >> 1, wq = wave & 1;
+    const int lr = lane & 15, lg = lane >> 4;
+
+    f32x4 acc[FP][FQ];
+#pragma unroll
+    for (int i = 0; i < FP; ++i)
+#pragma unroll
+        for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    int k0 = c.kbeg;
+    if (k0 < c.kend) {
+        lp.load(a, bufP, c, tid, p0, k0);
+        lq.load(a, bufQ, c, tid, q0, k0);
+    }
+    for (; k0 < c.kend; k0 += BK) {
+        lp.stage(sP, tid);
+        lq.stage(sQ, tid);
+        __syncthreads();
+        if (k0 + BK < c.kend) {
+            lp.load(a, bufP, c, tid, p0, k0 + BK);
+            lq.load(a, bufQ, c, tid, q0, k0 + BK);
+        }
+#pragma unroll
+        for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
+            typename M::frag fa[FP], fb[FQ];
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+                fa[i] = *reinterpret_cast<const typename M::frag*>(
+                    &sP[L::at(wp * 16 * FP + i * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+#pragma unroll
+            for (int j = 0; j < FQ; ++j)
+                fb[j] = *reinterpret_cast<const typename M::frag*>(
+                    &sQ[L::at(wq * 16 * FQ + j * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+        }
+        __syncthreads();
+    }
+
+    const bool split = a.splits > 1;
+    float* part = a.partial + (long long)blockIdx.z * a.Pdim * a.Qdim;
+#pragma unroll
+    for (int i = 0; i < FP; ++i)
+#pragma unroll
+        for (int j = 0; j < FQ; ++j) {
+            const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+            const int p = p0 + wp * 16 * FP + i * 16 + lg * 4;
+            if (q >= a.Qdim || p >= a.Pdim) continue;
+            const int np = min(4, a.Pdim - p);
+            if (split) {
+                // partial sums are stored [z][q][p]
+                float* o = part + (long long)q * a.Pdim + p;
+                if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
+                else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
+            } else {
+                Op::store4(a, c, p, q, acc[i][j], np);
+            }
+        }
+}
+
+// Second pass of a split reduction.  A block covers OPB = 256/SL consecutive outputs t =
+// q * Pdim + p of one (shard, group) with SL threads per output: thread l adds splits l,
+// l + SL, ... in ascending order, then the SL partial sums are added in ascending l.
+// blockIdx.y = shard * G + group.
+template <class Op, int SL>
+__global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
+{
+    constexpr int OPB = 256 / SL;
+    __shared__ float sh[SL][OPB];
+    const long long per = (long long)a.Pdim * a.Qdim;
+    const int ol = threadIdx.x % OPB, l = threadIdx.x / OPB;
+    const long long t = (long long)blockIdx.x * OPB + ol;
+    const int rg = blockIdx.y;
+    Ctx c;
+    c.grp = rg % a.G;
+    c.r = rg / a.G;
+    c.split = 0;
+    c.kbeg = 0;
+    c.kend = a.Kdim;
+    c.b0 = c.r * a.N;
+    c.tab = nullptr;
+    float s = 0.f;
+    if (t < per) {
+        const float* src = a.partial + ((long long)c.r * a.splits * a.G + c.grp) * per + t;
+        for (int k = l; k < a.splits; k += SL) s += src[(long long)k * a.G * per];
+    }
+    sh[l][ol] = s;
+    __syncthreads();
+    if (l == 0 && t < per) {
+        float tot = sh[0][ol];
+#pragma unroll
+        for (int j = 1; j < SL; ++j) tot += sh[j][ol];
+        const int q = (int)(t / a.Pdim), p = (int)(t - (long long)q * a.Pdim);
+        Op::store4(a, c, p, q, f32x4{tot, 0.f, 0.f, 0.f}, 1);
+    }
+}
+
+// ---- launch ---------------------------------------------------------------------------------
+
+template <class Op, int FP, int FQ, int PK, int QK>
+static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
+{
+    typedef typename Op::TT T;
+    constexpr int VEC = 16 / sizeof(T);
+    dim3 grid((a.Qdim + 32 * FQ - 1) / (32 * FQ), (a.Pdim + 32 * FP - 1) / (32 * FP), gz);
+    if (grid.y > 65535u || grid.z > 65535u) return hipErrorInvalidConfiguration;
+    size_t shm = 0;
+    if constexpr (Op::TAB) {
+        const int ts = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+        const int n = a.kchunk / ts;
+        if (n > kMaxTab) return hipErrorInvalidValue;  // the plan keeps chunks within the table
+        shm = sizeof(TabEnt) * (size_t)n;
+    }
+    hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, PK, QK>), grid, dim3(256), shm, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits <= 1) return e;
+    const long long per = (long long)a.Pdim * a.Qdim;
+    const int rg = gz / a.splits;
+    if (a.splits >= 16)
+        hipLaunchKernelGGL((split_epilogue<Op, 16>), dim3((unsigned)((per + 15) / 16), rg),
+                           dim3(256), 0, s, a);
+    else if (a.splits >= 4)
+        hipLaunchKernelGGL((split_epilogue<Op, 4>), dim3((unsigned)((per + 63) / 64), rg),
+                           dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((split_epilogue<Op, 1>), dim3((unsigned)((per + 255) / 256), rg),
+                           dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// Tile shapes: (FP, FQ) in {(1,2), (1,4), (2,2), (2,4), (4,4)}.
+template <class Op, int PK, int QK>
+static hipError_t launch_shape(const GemmArgs& a, const GemmPlan& g, int gz, hipStream_t s)
+{
+    if (g.FP == 1) {
+        if (g.FQ == 4) return launch_tile<Op, 1, 4, PK, QK>(a, gz, s);
+        return launch_tile<Op, 1, 2, PK, QK>(a, gz, s);
+    }
+    if (g.FP == 2) {
+        if (g.FQ == 4) return launch_tile<Op, 2, 4, PK, QK>(a, gz, s);
+        return launch_tile<Op, 2, 2, PK, QK>(a, gz, s);
+    }
+    return launch_tile<Op, 4, 4, PK, QK>(a, gz, s);
+}
+
+// Runs operation Op with loaders (PK, QK) under plan g; zdim = blocks along z before splits.
+template <class Op, int PK, int QK>
+static hipError_t run_gemm(GemmArgs a, const GemmPlan& g, int zdim, float* partial, hipStream_t s)
+{
+    if (a.Pdim <= 0 || a.Qdim <= 0 || zdim <= 0) return hipSuccess;
+    if (g.BK != tile_k<typename Op::TT>()) return hipErrorInvalidValue;
+    a.splits = g.splits;
+    a.kchunk = g.kchunk;
+    a.partial = partial;
+    if (g.splits > 1 && !partial) return hipErrorInvalidValue;
+    return launch_shape<Op, PK, QK>(a, g, zdim * g.splits, s);
+}
+
+}  // namespace mtx

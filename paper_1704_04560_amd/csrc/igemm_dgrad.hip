@@ -1,0 +1,150 @@
+// Data-gradient launches: convolution (implicit GEMM, or col GEMM + col2im) and fully
+// connected.
+#include "igemm_ops.h"
+
+namespace mtx {
+
+// dx (NHWC) = sum over (u, v) in ascending order of col[g][(n, oh, ow)][(u, v, ci')] with
+// oh*stride = h + pad - u (likewise for columns), times the ReLU mask of the layer below.
+// One thread per element of dx, channels fastest.  KT > 0: kernel size known at compile time
+// and stride 1.
+template <typename T, int KT>
+__global__ __launch_bounds__(256) void col2im_kernel(const GemmArgs a, const float* __restrict__ col)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int total = a.N * a.C * a.H * a.W;
+    if (t >= total) return;
+    const unsigned pos = fdiv(a.fd_c, (unsigned)t), ci = (unsigned)t - pos * (unsigned)a.C;
+    const unsigned b = fdiv(a.fd_hw, pos), hw = pos - b * (unsigned)(a.H * a.W);
+    const unsigned hq = fdiv(a.fd_w, hw);
+    const int h = (int)hq, w = (int)(hw - hq * (unsigned)a.W);
+    const int grp = (int)ci / a.cg, cl = (int)ci - grp * a.cg;
+    const long long Q = (long long)a.N * a.OH * a.OW, P = (long long)a.KK * a.cg;
+    const float* cp = col + (long long)grp * Q * P + (long long)b * a.OH * a.OW * P + cl;
+    float acc = 0.f;
+    if constexpr (KT > 0) {
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            const int oh = h + a.PD - u;
+            const bool okh = (unsigned)oh < (unsigned)a.OH;
+#pragma unroll
+            for (int v = 0; v < KT; ++v) {
+                const int ow = w + a.PD - v;
+                const bool ok = okh && (unsigned)ow < (unsigned)a.OW;
+                const float x = cp[ok ? ((long long)oh * a.OW + ow) * P + (u * KT + v) * a.cg : 0];
+                acc += ok ? x : 0.f;
+            }
+        }
+    } else {
+        for (int u = 0; u < a.K; ++u) {
+            const int th = h + a.PD - u;
+            if (th < 0) break;
+            const int oh = th / a.S;
+            if (oh * a.S != th || oh >= a.OH) continue;
+            for (int v = 0; v < a.K; ++v) {
+                const int tw = w + a.PD - v;
+                if (tw < 0) break;
+                const int ow = tw / a.S;
+                if (ow * a.S != tw || ow >= a.OW) continue;
+                acc += cp[((long long)oh * a.OW + ow) * P + (u * a.K + v) * a.cg];
+            }
+        }
+    }
+    if (a.mask) {
+        const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[t]
+                                   : to_f32<T>(static_cast<const T*>(a.mask)[t]);
+        if (!(m > 0.f)) acc = 0.f;
+    }
+    static_cast<T*>(a.out)[t] = from_f32<T>(acc);
+}
+
+template <typename T>
+static void launch_col2im(const GemmArgs& c, const float* col, hipStream_t s)
+{
+    const long long total = (long long)c.N * c.C * c.H * c.W;
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (c.S == 1 && c.K == 3) hipLaunchKernelGGL((col2im_kernel<T, 3>), grid, dim3(256), 0, s, c, col);
+    else if (c.S == 1 && c.K == 5) hipLaunchKernelGGL((col2im_kernel<T, 5>), grid, dim3(256), 0, s, c, col);
+    else hipLaunchKernelGGL((col2im_kernel<T, 0>), grid, dim3(256), 0, s, c, col);
+}
+
+hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, void* dx,
+                      const void* mask, bool mask_f32, float* partial, hipStream_t s)
+{
+    GemmArgs a = conv_args(g);
+    a.a = dy; a.b = wd; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
+    const GemmDims d = conv_dgrad_dims(dt, g);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool v = a.og % vec_elems(dt) == 0;  // then OC and Kdim are multiples too
+    if (g.S == 1) {
+        if (dt == DT_F32) {
+            if (v) return run_gemm<ConvDgrad<float, true>, L_KV, L_KV>(a, p, d.Z, partial, s);
+            return run_gemm<ConvDgrad<float, true>, L_SK, L_SR>(a, p, d.Z, partial, s);
+        }
+        if (v) return run_gemm<ConvDgrad<bf16_t, true>, L_KV, L_KV>(a, p, d.Z, partial, s);
+        return run_gemm<ConvDgrad<bf16_t, true>, L_SK, L_SR>(a, p, d.Z, partial, s);
+    }
+    if (dt == DT_F32) return run_gemm<ConvDgrad<float, false>, L_SK, L_SR>(a, p, d.Z, partial, s);
+    return run_gemm<ConvDgrad<bf16_t, false>, L_SK, L_SR>(a, p, d.Z, partial, s);
+}
+
+hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* wc, void* dx,
+                          const void* mask, bool mask_f32, float* col, float* partial,
+                          hipStream_t s)
+{
+    GemmArgs a = conv_args(g);
+    a.a = dy; a.b = wc; a.out = col;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
+    const GemmDims d = conv_dgrad_col_dims(dt, g);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool v = a.og % vec_elems(dt) == 0;
+    hipError_t e;
+    if (dt == DT_F32)
+        e = v ? run_gemm<ConvDgradCol<float>, L_KV, L_KV>(a, p, d.Z, partial, s)
+              : run_gemm<ConvDgradCol<float>, L_SK, L_SK>(a, p, d.Z, partial, s);
+    else
+        e = v ? run_gemm<ConvDgradCol<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s)
+              : run_gemm<ConvDgradCol<bf16_t>, L_SK, L_SK>(a, p, d.Z, partial, s);
+    if (e != hipSuccess) return e;
+    GemmArgs c = conv_args(g);
+    c.out = dx; c.mask = mask; c.mask_f32 = mask_f32;
+    if (dt == DT_F32) launch_col2im<float>(c, col, s);
+    else launch_col2im<bf16_t>(c, col, s);
+    return hipGetLastError();
+}
+
+hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
+                    const void* mask, bool mask_f32, float* partial, hipStream_t s)
+{
+    GemmArgs a{};
+    a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
+    a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1; a.perm_c = 1; a.perm_hw = 1;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)B * OUT * es);
+    a.b_bytes = (unsigned)((size_t)OUT * IN * es);
+    const GemmDims d = fc_dgrad_dims(dt, B, IN, OUT);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool pv = IN % vec_elems(dt) == 0, qv = OUT % vec_elems(dt) == 0;
+    if (dt == DT_F32) {
+        typedef FcDgrad<float> Op;
+        if (pv && qv) return run_gemm<Op, L_RV, L_KV>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RV, L_SK>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_KV>(a, p, d.Z, partial, s);
+        return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
+    }
+    typedef FcDgrad<bf16_t> Op;
+    if (pv && qv) return run_gemm<Op, L_RV, L_KV>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RV, L_SK>(a, p, d.Z, partial, s);
+    if (qv) return run_gemm<Op, L_SR, L_KV>(a, p, d.Z, partial, s);
+    return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
+}
+
+}  // namespace mtx

@@ -1,0 +1,63 @@
+// Weight-gradient launches (per shard, bias gradient included): convolution and fully
+// connected.
+#include "igemm_ops.h"
+
+namespace mtx {
+
+hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
+                      float* grads, long long ld, long long w_off, long long b_off,
+                      float* partial, hipStream_t s)
+{
+    GemmArgs a = conv_args(g);
+    a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
+    a.R = R;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)R * g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)R * g.N * g.C * g.H * g.W * es);
+    const GemmDims d = conv_wgrad_dims(dt, g, R);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool pv = a.og % vec_elems(dt) == 0, qv = a.cg % vec_elems(dt) == 0;
+    if (dt == DT_F32) {
+        typedef ConvWgrad<float> Op;
+        if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+        return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
+    }
+    typedef ConvWgrad<bf16_t> Op;
+    if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
+    if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
+}
+
+hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
+                    const void* x, const void* dy, float* grads, long long ld, long long w_off,
+                    long long b_off, float* partial, hipStream_t s)
+{
+    GemmArgs a{};
+    a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
+    a.N = Nb; a.C = IN; a.OC = OUT; a.G = 1; a.R = R; a.perm_c = perm_c; a.perm_hw = perm_hw;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)R * Nb * OUT * es);
+    a.b_bytes = (unsigned)((size_t)R * Nb * IN * es);
+    const GemmDims d = fc_wgrad_dims(dt, Nb, R, IN, OUT);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool pv = IN % vec_elems(dt) == 0, qv = OUT % vec_elems(dt) == 0;
+    if (dt == DT_F32) {
+        typedef FcWgrad<float> Op;
+        if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+        return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
+    }
+    typedef FcWgrad<bf16_t> Op;
+    if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
+    if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
+}
+
+}  // namespace mtx

@@ -1,4 +1,15 @@
 // Internal declarations shared by the host orchestration (api.hip) and the kernel files.
+//
+// Data layouts on the device (per step):
+//   activations and data gradients of convolution and pooling layers: NHWC [n][h][w][c];
+//   the input of a first convolution: NHWC in the compute type (converted from the caller's NCHW);
+//   fully connected inputs: the producing layer's layout ((h, w, c) order after a spatial layer);
+//   weights as the GEMMs read them (prepared every step from the fp32 master copy):
+//     convolution forward        Wf [co][u][v][ci]           (ci = channel within the group)
+//     convolution data gradient  Wd [g][ci][u][v][co]        (implicit GEMM)
+//                            or  Wc [g][u][v][ci][co]        (col + col2im)
+//     fully connected            W  [o][i], with i in (h, w, c) order after a spatial layer;
+//   gradients: fp32 in the logical parameter order ([co][ci][u][v], [o][(c, h, w)], bias).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -9,7 +20,14 @@ namespace mtx {
 
 enum Dt { DT_F32 = 0, DT_BF16 = 1 };
 
-// Geometry of one convolution (or of a fully connected layer viewed as C=in, H=W=K=1).
+// Division by an invariant divisor d (1 <= d < 2^31) for dividends below 2^31:
+// q = (umulhi(n, m) + n) >> s with s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1.
+struct FastDiv {
+    unsigned m, s;
+};
+FastDiv make_fastdiv(unsigned d);
+
+// Geometry of one convolution.
 struct ConvGeom {
     int N;            // images in the launch (whole batch for fwd/dgrad, one shard for wgrad)
     int C, H, W;      // input
@@ -17,14 +35,16 @@ struct ConvGeom {
     int K, S, PD, G;  // kernel, stride, padding, groups
 };
 
-// Implicit-GEMM arguments.  Each operation (see igemm.hip) reads the fields it needs.
+constexpr int kMaxTab = 2048;  // largest LDS index table (entries of 8 bytes, 16 KB)
+
+// Implicit-GEMM arguments.  Each operation (see igemm.h) reads the fields it needs.
 struct GemmArgs {
-    const void* a;         // activation-like operand (x, dy or X)
-    const void* b;         // weights or second activation operand
-    void* out;             // output (activation, data gradient, or fp32 gradient rows)
-    const float* bias;     // forward: fp32 bias [OC]
+    const void* a;         // activation-like operand (x, dy)
+    const void* b;         // weights, or the second activation operand of a weight gradient
+    void* out;             // output (activation, data gradient, col, or fp32 gradient rows)
+    const float* bias;     // forward: fp32 bias
     const void* mask;      // data gradient: the previous layer's stored output (ReLU mask)
-    float* partial;        // weight gradient with split K: fp32 partial sums
+    float* partial;        // split reduction: fp32 partial sums [z][q][p]
     long long out_ld;      // weight gradient: elements between shard gradient rows
     long long out_off;     // weight gradient: offset of this layer's W in a gradient row
     long long bias_off;    // weight gradient: offset of this layer's b in a gradient row
@@ -37,40 +57,45 @@ struct GemmArgs {
     int relu;              // forward: apply ReLU
     int out_f32;           // forward: output stored as fp32 (otherwise the compute type)
     int mask_f32;          // data gradient: mask tensor is fp32 (otherwise the compute type)
+    int perm_c, perm_hw;   // fully connected weight gradient after a spatial layer: its input
+                           // is in (h, w, c) order with perm_c channels and perm_hw positions
     unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)
     unsigned b_bytes;      // size of tensor b in bytes
+    FastDiv fd_ohw, fd_ow, fd_hw, fd_w, fd_c;
 };
 
 // GEMM view of one operation: P output rows, Q output columns, K reduction length, Z blocks
-// along blockIdx.z before reduction splits (groups x shards).
+// along blockIdx.z before reduction splits (groups x shards), kmax the largest reduction chunk
+// one block may take (0: no limit).
 struct GemmDims {
-    int P, Q, K, Z;
-    bool allow_split;
+    int P, Q, K, Z, kmax;
 };
 // Launch shape: 32*FP x 32*FQ output tile, BK reduction tile, reduction splits of kchunk.
 struct GemmPlan {
     int FP, FQ, BK, splits, kchunk;
 };
-GemmPlan plan_gemm(int dt, int Pdim, int Qdim, int Kdim, int zdim, bool allow_split);
 GemmPlan plan_for(int dt, const GemmDims& d);
 size_t partial_elems(int dt, const GemmDims& d);  // fp32 partial sums a launch needs (0 if none)
-GemmDims conv_fwd_dims(const ConvGeom& g);
-GemmDims conv_dgrad_dims(const ConvGeom& g);
-GemmDims conv_wgrad_dims(const ConvGeom& g, int R);
-GemmDims conv_dgrad_col_dims(const ConvGeom& g);
+GemmDims conv_fwd_dims(int dt, const ConvGeom& g);
+GemmDims conv_dgrad_dims(int dt, const ConvGeom& g);
+GemmDims conv_wgrad_dims(int dt, const ConvGeom& g, int R);
+GemmDims conv_dgrad_col_dims(int dt, const ConvGeom& g);
 size_t conv_dgrad_col_elems(const ConvGeom& g);
 bool conv_dgrad_use_col(const ConvGeom& g);  // data gradient through col + col2im
-GemmDims fc_fwd_dims(int B, int IN, int OUT);
-GemmDims fc_dgrad_dims(int B, int IN, int OUT);
-GemmDims fc_wgrad_dims(int Nb, int R, int IN, int OUT);
+GemmDims fc_fwd_dims(int dt, int B, int IN, int OUT);
+GemmDims fc_dgrad_dims(int dt, int B, int IN, int OUT);
+GemmDims fc_wgrad_dims(int dt, int Nb, int R, int IN, int OUT);
+int vec_elems(int dt);  // elements per 16-byte load
 
 // `partial` is fp32 scratch of at least partial_elems() elements (may be null when 0).
-hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* w, const float* bias,
+// x, y: NHWC.  wf: Wf.  y_f32: store fp32 (always in fp32 mode).
+hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* wf, const float* bias,
                     void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
-hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+// dy, dx: NHWC.  wd: Wd.
+hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, void* dx,
                       const void* mask, bool mask_f32, float* partial, hipStream_t s);
-// Data gradient through an fp32 col buffer of conv_dgrad_col_elems() elements.
-hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* w, void* dx,
+// Data gradient through an fp32 col buffer of conv_dgrad_col_elems() elements; wc: Wc.
+hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* wc, void* dx,
                           const void* mask, bool mask_f32, float* col, float* partial,
                           hipStream_t s);
 // Weight and bias gradient of R shards of g.N images each; x and dy point at the first shard.
@@ -81,12 +106,41 @@ hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, c
                   void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
 hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
                     const void* mask, bool mask_f32, float* partial, hipStream_t s);
-hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, const void* x, const void* dy,
-                    float* grads, long long ld, long long w_off, long long b_off, float* partial,
-                    hipStream_t s);
+// perm_c, perm_hw: see GemmArgs (1, 1 when the input is in logical order).
+hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
+                    const void* x, const void* dy, float* grads, long long ld, long long w_off,
+                    long long b_off, float* partial, hipStream_t s);
 
 // elementwise.hip
+
+// Weight preparation: one launch converts the fp32 master weights into every layout above.
+enum PrepKind {
+    PREP_CAST = 0,   // dst[i] = src[i]
+    PREP_CONV_F,     // Wf from W[co][ci][u][v]
+    PREP_CONV_D,     // Wd
+    PREP_CONV_C,     // Wc
+    PREP_FC_PERM,    // W[o][(c, h, w)] -> W[o][(h, w, c)]
+};
+struct PrepJob {
+    int kind;
+    int n;             // elements
+    long long src;     // element offset in the fp32 weights
+    long long dst;     // element offset in the prepared buffer
+    int g, cg, og, KK; // convolution: groups, channels per group in / out, K*K
+    int C, HW, IN;     // fully connected permutation
+    int block0;        // first block of this job in the launch
+    FastDiv f0, f1, f2;
+};
+// jobs: device array of njobs entries, blocks = total blocks (sum over jobs).
+hipError_t prep_weights(Dt dt, const PrepJob* jobs, int njobs, int blocks, const float* w,
+                        void* dst, hipStream_t s);
+int prep_blocks(int n);  // blocks one job of n elements takes
+void prep_fill_divisors(PrepJob& j);
+
+// NCHW fp32 -> NHWC compute type (C == 1 or H*W == 1: a plain copy / cast).
+hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipStream_t s);
 hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
+// Max pooling over NHWC tensors; argmax holds the window position (u*K + v) per output.
 hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void* x, void* y,
                     uint8_t* argmax, hipStream_t s);
 hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8_t* argmax,

@@ -1,0 +1,103 @@
+// Launch planning for the implicit GEMMs (host only), shared by the workspace sizing in
+// api.hip and by the launches, so that both always agree.
+#include "internal.h"
+
+namespace mtx {
+
+FastDiv make_fastdiv(unsigned d)
+{
+    FastDiv f{};
+    if (d == 0) d = 1;
+    unsigned s = 0;
+    while ((1ull << s) < d) ++s;
+    f.m = (unsigned)((((1ull << 32) * ((1ull << s) - d)) / d) + 1);
+    f.s = s;
+    return f;
+}
+
+int vec_elems(int dt) { return dt == DT_F32 ? 4 : 8; }
+
+static long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+// Tile: the largest of 128x128, 64x128, 64x64, 32x128, 32x64 (rows x columns) that still gives
+// at least two blocks per compute unit (the smallest when none does), with rows limited by P.
+// Reduction splits then double while the launch has fewer than four blocks per compute unit and
+// every split keeps at least two k tiles.  kmax (an LDS table limit) can force more splits; the
+// fp32 partial sums are capped at 64M elements.
+GemmPlan plan_for(int dt, const GemmDims& d)
+{
+    constexpr long long kTargetTiles = 512, kTargetBlocks = 1024, kMaxPartial = 64ll << 20;
+    GemmPlan g{};
+    g.BK = dt == DT_F32 ? 32 : 64;
+    const int fpmax = d.P <= 32 ? 1 : (d.P <= 64 ? 2 : 4);
+    static const int cand[5][2] = {{4, 4}, {2, 4}, {2, 2}, {1, 4}, {1, 2}};
+    auto tiles = [&](int fp, int fq) {
+        return cdiv(d.P, 32 * fp) * cdiv(d.Q, 32 * fq) * (long long)d.Z;
+    };
+    g.FP = 1;
+    g.FQ = 2;
+    for (const auto& c : cand) {
+        if (c[0] > fpmax) continue;
+        if (tiles(c[0], c[1]) >= kTargetTiles) {
+            g.FP = c[0];
+            g.FQ = c[1];
+            break;
+        }
+    }
+    const long long t = tiles(g.FP, g.FQ);
+    const long long ktiles = cdiv(d.K, g.BK);
+    long long splits = 1;
+    while (t * splits < kTargetBlocks && ktiles >= 4 * splits && splits < 256) splits *= 2;
+    const long long per_split = (long long)d.P * d.Q * d.Z;
+    while (splits > 1 && splits * per_split > kMaxPartial) splits /= 2;
+    long long kchunk = cdiv(cdiv(d.K, splits), g.BK) * g.BK;
+    if (d.kmax > 0 && kchunk > d.kmax) kchunk = (d.kmax / g.BK) * g.BK;
+    if (kchunk < g.BK) kchunk = g.BK;
+    g.kchunk = (int)kchunk;
+    g.splits = (int)cdiv(d.K, kchunk);
+    if (g.splits < 1) g.splits = 1;
+    return g;
+}
+
+size_t partial_elems(int dt, const GemmDims& d)
+{
+    const GemmPlan g = plan_for(dt, d);
+    if (g.splits <= 1) return 0;
+    return (size_t)g.splits * d.Z * (size_t)d.P * d.Q;
+}
+
+// GEMM sizes of every operation (P rows, Q columns, reduction, blockIdx.z extent before
+// splits, largest reduction chunk with an index table)
+GemmDims conv_fwd_dims(int dt, const ConvGeom& g)
+{
+    const int cg = g.C / g.G, step = cg % vec_elems(dt) == 0 ? vec_elems(dt) : 1;
+    return GemmDims{g.OC / g.G, g.N * g.OH * g.OW, g.K * g.K * cg, g.G, kMaxTab * step};
+}
+GemmDims conv_dgrad_dims(int dt, const ConvGeom& g)
+{
+    const int og = g.OC / g.G, step = og % vec_elems(dt) == 0 ? vec_elems(dt) : 1;
+    return GemmDims{g.C / g.G, g.N * g.H * g.W, g.K * g.K * og, g.G, g.S == 1 ? kMaxTab * step : 0};
+}
+GemmDims conv_wgrad_dims(int, const ConvGeom& g, int R)
+{
+    return GemmDims{g.OC / g.G, g.K * g.K * (g.C / g.G) + 1, g.N * g.OH * g.OW, g.G * R, kMaxTab};
+}
+GemmDims conv_dgrad_col_dims(int, const ConvGeom& g)
+{
+    return GemmDims{g.K * g.K * (g.C / g.G), g.N * g.OH * g.OW, g.OC / g.G, g.G, 0};
+}
+size_t conv_dgrad_col_elems(const ConvGeom& g)
+{
+    return (size_t)g.C * g.K * g.K * (size_t)g.N * g.OH * g.OW;
+}
+bool conv_dgrad_use_col(const ConvGeom& g)
+{
+    // taps the implicit GEMM visits per useful multiply-add (stride 1: H*W / (OH*OW))
+    const double waste = (double)g.H * g.W / ((double)g.OH * g.OW * g.S * g.S);
+    return waste >= 1.5 && conv_dgrad_col_elems(g) * 4 <= (size_t)512 << 20;
+}
+GemmDims fc_fwd_dims(int, int B, int IN, int OUT) { return GemmDims{OUT, B, IN, 1, 0}; }
+GemmDims fc_dgrad_dims(int, int B, int IN, int OUT) { return GemmDims{IN, B, OUT, 1, 0}; }
+GemmDims fc_wgrad_dims(int, int Nb, int R, int IN, int OUT) { return GemmDims{IN + 1, OUT, Nb, R, 0}; }
+
+}  // namespace mtx

@@ -125,8 +125,9 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
  *   loss_out (device, nullable) receives the mean loss over the batch, fp32 [1].
  * With MTX_BF16 compute, x, the weights, every hidden layer's output and every data gradient
  * are rounded to bfloat16 (round to nearest even); sums, logits, weight gradients, the average
- * and the update are fp32.  An out-of-range label gives that sample a NaN loss.  Asynchronous;
- * results are deterministic run to run. */
+ * and the update are fp32.  An out-of-range label gives that sample a NaN loss.  x must be
+ * 16-byte aligned (it is read with 16-byte loads), labels and loss_out 4-byte aligned.
+ * Asynchronous; results are deterministic run to run. */
 int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
                    float momentum, float* loss_out, void* stream);
 

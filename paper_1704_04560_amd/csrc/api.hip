@@ -162,7 +162,9 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.need_dx = (int)i > pl.first_param && pl.first_param >= 0;
-        lp.nhwc = lp.kind != MTX_FC;
+        // a pooled tensor that feeds a fully connected layer is stored NCHW
+        lp.nhwc = lp.kind == MTX_CONV ||
+                  (lp.kind == MTX_MAXPOOL && !(i + 1 < pl.L.size() && pl.L[i + 1].kind == MTX_FC));
         lp.perm_c = 1;
         lp.perm_hw = 1;
         if (lp.kind == MTX_FC && i > 0 && pl.L[i - 1].nhwc && lp.c > 1 && lp.h * lp.w > 1) {
@@ -610,7 +612,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                     }), "fc forward");
         } else {
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
-                        return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, in, out,
+                        return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc, in, out,
                                         reinterpret_cast<uint8_t*>(ws + lp.am_off), s);
                     }), "pool forward");
         }
@@ -667,7 +669,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         } else {
             if (!need_dx) continue;
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
-                        return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s,
+                        return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
                                         reinterpret_cast<const uint8_t*>(ws + lp.am_off), cur, nxt,
                                         mask, mask_f32, s);
                     }), "pool backward");
@@ -723,8 +725,8 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
 {
     if (!m) return fail(MTX_EINVAL, "model is NULL");
     if (!x || !labels) return fail(MTX_EINVAL, "x and labels must not be NULL");
-    if (!aligned(x, 4) || !aligned(labels, 4) || (loss_out && !aligned(loss_out, 4)))
-        return fail(MTX_EINVAL, "x, labels and loss_out must be 4-byte aligned");
+    if (!aligned(x, 16) || !aligned(labels, 4) || (loss_out && !aligned(loss_out, 4)))
+        return fail(MTX_EINVAL, "x must be 16-byte aligned, labels and loss_out 4-byte aligned");
     if (!std::isfinite(lr) || !std::isfinite(momentum))
         return fail(MTX_EINVAL, "lr and momentum must be finite");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -875,6 +877,10 @@ int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t
         return fail(MTX_ENOMEM, "host allocation failed");
     }
     HIP_TRY(hipMemcpy(dev.data(), m->ws + lp.am_off, cnt, hipMemcpyDeviceToHost), "copy");
+    if (!lp.nhwc) {
+        std::memcpy(dst_host, dev.data(), cnt);
+        return MTX_OK;
+    }
     const size_t C = lp.oc, HW = (size_t)lp.oh * lp.ow;
     for (size_t b = 0; b < (size_t)m->pl.B; ++b)
         for (size_t hw = 0; hw < HW; ++hw)

@@ -173,82 +173,131 @@ hipError_t prep_weights(Dt dt, const PrepJob* jobs, int njobs, int blocks, const
 
 // ---- max-pooling over NHWC tensors ------------------------------------------------------------
 // KT / ST > 0: window and stride known at compile time (2/2 and 3/2 are the common cases).
+// CV channels per thread (16 bytes of channels when C allows it, else 1).  A pooled tensor that
+// feeds a fully connected layer is stored NCHW instead (the (c, h, w) order that layer reads);
+// argmax always follows the layout of the pooled tensor.
 
-// One thread per output (channels fastest): the first maximal element of the K x K window in
+template <typename T, int CV> struct Chans {
+    T v[CV];
+};
+
+template <typename T, int CV>
+__device__ __forceinline__ Chans<T, CV> load_chans(const T* p)
+{
+    Chans<T, CV> r;
+    if constexpr (CV * sizeof(T) == 16) {
+        *reinterpret_cast<uint4*>(r.v) = *reinterpret_cast<const uint4*>(p);
+    } else {
+#pragma unroll
+        for (int i = 0; i < CV; ++i) r.v[i] = p[i];
+    }
+    return r;
+}
+
+template <typename T, int CV>
+__device__ __forceinline__ void store_chans(T* p, const Chans<T, CV>& r)
+{
+    if constexpr (CV * sizeof(T) == 16) {
+        *reinterpret_cast<uint4*>(p) = *reinterpret_cast<const uint4*>(r.v);
+    } else {
+#pragma unroll
+        for (int i = 0; i < CV; ++i) p[i] = r.v[i];
+    }
+}
+
+// One thread per CV channels of one output: the first maximal element of the K x K window in
 // row-major window order; argmax holds its window position u*K + v.
-template <typename T, int KT, int ST>
+template <typename T, int KT, int ST, int CV>
 __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, int W, int Kr,
-                                                       int Sr, int OH, int OW, FastDiv fc,
-                                                       FastDiv fow, FastDiv foh,
+                                                       int Sr, int OH, int OW, int out_nchw,
+                                                       FastDiv fcv, FastDiv fow, FastDiv foh,
                                                        const T* __restrict__ x,
                                                        T* __restrict__ y,
                                                        uint8_t* __restrict__ argmax)
 {
     const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
-    const int o = blockIdx.x * 256 + threadIdx.x;
-    if (o >= total) return;
-    const unsigned pos = fdivu(fc, (unsigned)o), c = (unsigned)o - pos * (unsigned)C;
+    const int t = blockIdx.x * 256 + threadIdx.x;  // over N*OH*OW*(C/CV)
+    if (t >= total) return;
+    const unsigned CG = (unsigned)(C / CV);
+    const unsigned pos = fdivu(fcv, (unsigned)t), c0 = ((unsigned)t - pos * CG) * CV;
     const unsigned r = fdivu(fow, pos), j = pos - r * (unsigned)OW;
     const unsigned n = fdivu(foh, r), i = r - n * (unsigned)OH;
-    const T* xp = x + (((long long)n * H + i * S) * W + j * S) * C + c;
+    const T* xp = x + (((long long)n * H + i * S) * W + j * S) * C + c0;
     const long long rs = (long long)W * C;
-    T best = xp[0];
-    float bv = to_f32<T>(best);
-    int bi = 0;
-    if constexpr (KT > 0) {
+    Chans<T, CV> best = load_chans<T, CV>(xp);
+    float bv[CV];
+    uint8_t bi[CV];
 #pragma unroll
-        for (int u = 0; u < KT; ++u)
+    for (int e = 0; e < CV; ++e) { bv[e] = to_f32<T>(best.v[e]); bi[e] = 0; }
+    for (int u = 0; u < K; ++u)
+        for (int v = 0; v < K; ++v) {
+            const Chans<T, CV> cur = load_chans<T, CV>(xp + u * rs + v * C);
 #pragma unroll
-            for (int v = 0; v < KT; ++v) {
-                const T t = xp[u * rs + v * C];
-                const float tv = to_f32<T>(t);
-                if (tv > bv) { bv = tv; best = t; bi = u * KT + v; }
+            for (int e = 0; e < CV; ++e) {
+                const float tv = to_f32<T>(cur.v[e]);
+                if (tv > bv[e]) { bv[e] = tv; best.v[e] = cur.v[e]; bi[e] = (uint8_t)(u * K + v); }
             }
-    } else {
-        for (int u = 0; u < K; ++u)
-            for (int v = 0; v < K; ++v) {
-                const T t = xp[u * rs + v * C];
-                const float tv = to_f32<T>(t);
-                if (tv > bv) { bv = tv; best = t; bi = u * K + v; }
-            }
+        }
+    if (out_nchw) {
+#pragma unroll
+        for (int e = 0; e < CV; ++e) {
+            const long long o = (((long long)n * C + c0 + e) * OH + i) * OW + j;
+            y[o] = best.v[e];
+            argmax[o] = bi[e];
+        }
+        return;
     }
-    y[o] = best;
-    argmax[o] = (uint8_t)bi;
+    const long long o = (long long)pos * C + c0;
+    store_chans<T, CV>(y + o, best);
+#pragma unroll
+    for (int e = 0; e < CV; ++e) argmax[o + e] = bi[e];
 }
 
-hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void* x, void* y,
-                    uint8_t* argmax, hipStream_t s)
+template <typename T, int CV>
+static void pool_fwd_launch(int N, int C, int H, int W, int K, int S, bool out_nchw,
+                            const void* x, void* y, uint8_t* argmax, hipStream_t s)
 {
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
-    const int total = N * C * OH * OW;
-    if (total <= 0) return hipSuccess;
-    const FastDiv fc = make_fastdiv((unsigned)C), fow = make_fastdiv((unsigned)OW),
+    const int total = N * OH * OW * (C / CV);
+    const FastDiv fcv = make_fastdiv((unsigned)(C / CV)), fow = make_fastdiv((unsigned)OW),
                   foh = make_fastdiv((unsigned)OH);
     dim3 g(grid_for(total, 256)), b(256);
-#define POOL_FWD(TY, KK, SS)                                                                   \
-    hipLaunchKernelGGL((pool_fwd_kernel<TY, KK, SS>), g, b, 0, s, total, C, H, W, K, S, OH, OW, \
-                       fc, fow, foh, static_cast<const TY*>(x), static_cast<TY*>(y), argmax)
+    const T* xx = static_cast<const T*>(x);
+    T* yy = static_cast<T*>(y);
+    if (K == 2 && S == 2)
+        hipLaunchKernelGGL((pool_fwd_kernel<T, 2, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)out_nchw, fcv, fow, foh, xx, yy, argmax);
+    else if (K == 3 && S == 2)
+        hipLaunchKernelGGL((pool_fwd_kernel<T, 3, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)out_nchw, fcv, fow, foh, xx, yy, argmax);
+    else
+        hipLaunchKernelGGL((pool_fwd_kernel<T, 0, 0, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)out_nchw, fcv, fow, foh, xx, yy, argmax);
+}
+
+hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, bool out_nchw,
+                    const void* x, void* y, uint8_t* argmax, hipStream_t s)
+{
+    const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
+    if ((long long)N * C * OH * OW <= 0) return hipSuccess;
     if (dt == DT_F32) {
-        if (K == 2 && S == 2) POOL_FWD(float, 2, 2);
-        else if (K == 3 && S == 2) POOL_FWD(float, 3, 2);
-        else POOL_FWD(float, 0, 0);
+        if (C % 4 == 0) pool_fwd_launch<float, 4>(N, C, H, W, K, S, out_nchw, x, y, argmax, s);
+        else pool_fwd_launch<float, 1>(N, C, H, W, K, S, out_nchw, x, y, argmax, s);
     } else {
-        if (K == 2 && S == 2) POOL_FWD(bf16_t, 2, 2);
-        else if (K == 3 && S == 2) POOL_FWD(bf16_t, 3, 2);
-        else POOL_FWD(bf16_t, 0, 0);
+        if (C % 8 == 0) pool_fwd_launch<bf16_t, 8>(N, C, H, W, K, S, out_nchw, x, y, argmax, s);
+        else pool_fwd_launch<bf16_t, 1>(N, C, H, W, K, S, out_nchw, x, y, argmax, s);
     }
-#undef POOL_FWD
     return hipGetLastError();
 }
 
-// One thread per input element (channels fastest): the sum, in ascending window order, of the
+// One thread per CV channels of one input element: the sum, in ascending window order, of the
 // output gradients of the windows whose maximum sits here (windows overlap when S < K), times
 // the ReLU mask of the layer that produced the pooled tensor.  Gathering keeps the result free
-// of atomics.
-template <typename T, int KT, int ST>
+// of atomics.  dy and argmax are NCHW when dy_nchw is set.
+template <typename T, int KT, int ST, int CV>
 __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, int W, int Kr,
-                                                       int Sr, int OH, int OW, FastDiv fc,
-                                                       FastDiv fw, FastDiv fh,
+                                                       int Sr, int OH, int OW, int dy_nchw,
+                                                       FastDiv fcv, FastDiv fw, FastDiv fh,
                                                        const uint8_t* __restrict__ argmax,
                                                        const T* __restrict__ dy,
                                                        T* __restrict__ dx,
@@ -256,65 +305,92 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, 
                                                        int mask_f32)
 {
     const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
-    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int t = blockIdx.x * 256 + threadIdx.x;  // over N*H*W*(C/CV)
     if (t >= total) return;
-    const unsigned pos = fdivu(fc, (unsigned)t), c = (unsigned)t - pos * (unsigned)C;
+    const unsigned CG = (unsigned)(C / CV);
+    const unsigned pos = fdivu(fcv, (unsigned)t), c0 = ((unsigned)t - pos * CG) * CV;
     const unsigned r = fdivu(fw, pos), wu = pos - r * (unsigned)W;
     const unsigned n = fdivu(fh, r), hu = r - n * (unsigned)H;
     const int h = (int)hu, w = (int)wu;
-    const long long base = (long long)n * OH * OW;
-    float acc = 0.f;
-    if (KT > 0 && KT == ST) {
-        // non-overlapping windows: at most one window holds this element
-        const int i = h / KT, j = w / KT;
-        if (i < OH && j < OW) {
-            const long long o = (base + (long long)i * OW + j) * C + c;
-            if (argmax[o] == (h - i * KT) * KT + (w - j * KT)) acc = to_f32<T>(dy[o]);
-        }
-    } else {
-        // windows i with i*S <= h <= i*S + K - 1
-        const int ilo = h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S;
-        const int ihi = min(h / S, OH - 1);
-        const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
-        const int jhi = min(w / S, OW - 1);
-        for (int i = ilo; i <= ihi; ++i)
-            for (int j = jlo; j <= jhi; ++j) {
-                const long long o = (base + (long long)i * OW + j) * C + c;
-                const int here = (h - i * S) * K + (w - j * S);
-                if (argmax[o] == here) acc += to_f32<T>(dy[o]);
+    float acc[CV];
+#pragma unroll
+    for (int e = 0; e < CV; ++e) acc[e] = 0.f;
+    // windows i with i*S <= h <= i*S + K - 1 (one at most when the windows do not overlap)
+    const int ilo = h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S;
+    const int ihi = min(h / S, OH - 1);
+    const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
+    const int jhi = min(w / S, OW - 1);
+    for (int i = ilo; i <= ihi; ++i)
+        for (int j = jlo; j <= jhi; ++j) {
+            const uint8_t here = (uint8_t)((h - i * S) * K + (w - j * S));
+            if (dy_nchw) {
+#pragma unroll
+                for (int e = 0; e < CV; ++e) {
+                    const long long o = (((long long)n * C + c0 + e) * OH + i) * OW + j;
+                    if (argmax[o] == here) acc[e] += to_f32<T>(dy[o]);
+                }
+            } else {
+                const long long o = (((long long)n * OH + i) * OW + j) * C + c0;
+                const Chans<T, CV> g = load_chans<T, CV>(dy + o);
+                uint8_t am[CV];
+                if constexpr (CV == 8) *reinterpret_cast<uint2*>(am) = *reinterpret_cast<const uint2*>(argmax + o);
+                else if constexpr (CV == 4) *reinterpret_cast<unsigned*>(am) = *reinterpret_cast<const unsigned*>(argmax + o);
+                else am[0] = argmax[o];
+#pragma unroll
+                for (int e = 0; e < CV; ++e)
+                    if (am[e] == here) acc[e] += to_f32<T>(g.v[e]);
             }
-    }
+        }
+    const long long xo = (long long)pos * C + c0;
     if (mask) {
-        const float m = mask_f32 ? static_cast<const float*>(mask)[t]
-                                 : to_f32<T>(static_cast<const T*>(mask)[t]);
-        if (!(m > 0.f)) acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < CV; ++e) {
+            const float m = mask_f32 ? static_cast<const float*>(mask)[xo + e]
+                                     : to_f32<T>(static_cast<const T*>(mask)[xo + e]);
+            if (!(m > 0.f)) acc[e] = 0.f;
+        }
     }
-    dx[t] = from_f32<T>(acc);
+    Chans<T, CV> out;
+#pragma unroll
+    for (int e = 0; e < CV; ++e) out.v[e] = from_f32<T>(acc[e]);
+    store_chans<T, CV>(dx + xo, out);
 }
 
-hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8_t* argmax,
-                    const void* dy, void* dx, const void* mask, bool mask_f32, hipStream_t s)
+template <typename T, int CV>
+static void pool_bwd_launch(int N, int C, int H, int W, int K, int S, bool dy_nchw,
+                            const uint8_t* argmax, const void* dy, void* dx, const void* mask,
+                            bool mask_f32, hipStream_t s)
 {
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
-    const int total = N * C * H * W;
-    if (total <= 0) return hipSuccess;
-    const FastDiv fc = make_fastdiv((unsigned)C), fw = make_fastdiv((unsigned)W),
+    const int total = N * H * W * (C / CV);
+    const FastDiv fcv = make_fastdiv((unsigned)(C / CV)), fw = make_fastdiv((unsigned)W),
                   fh = make_fastdiv((unsigned)H);
     dim3 g(grid_for(total, 256)), b(256);
-#define POOL_BWD(TY, KK, SS)                                                                    \
-    hipLaunchKernelGGL((pool_bwd_kernel<TY, KK, SS>), g, b, 0, s, total, C, H, W, K, S, OH, OW, \
-                       fc, fw, fh, argmax, static_cast<const TY*>(dy), static_cast<TY*>(dx),    \
-                       mask, (int)mask_f32)
+    const T* d = static_cast<const T*>(dy);
+    T* o = static_cast<T*>(dx);
+    if (K == 2 && S == 2)
+        hipLaunchKernelGGL((pool_bwd_kernel<T, 2, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
+    else if (K == 3 && S == 2)
+        hipLaunchKernelGGL((pool_bwd_kernel<T, 3, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
+    else
+        hipLaunchKernelGGL((pool_bwd_kernel<T, 0, 0, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
+                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
+}
+
+hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, bool dy_nchw,
+                    const uint8_t* argmax, const void* dy, void* dx, const void* mask,
+                    bool mask_f32, hipStream_t s)
+{
+    if ((long long)N * C * H * W <= 0) return hipSuccess;
     if (dt == DT_F32) {
-        if (K == 2 && S == 2) POOL_BWD(float, 2, 2);
-        else if (K == 3 && S == 2) POOL_BWD(float, 3, 2);
-        else POOL_BWD(float, 0, 0);
+        if (C % 4 == 0) pool_bwd_launch<float, 4>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
+        else pool_bwd_launch<float, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
     } else {
-        if (K == 2 && S == 2) POOL_BWD(bf16_t, 2, 2);
-        else if (K == 3 && S == 2) POOL_BWD(bf16_t, 3, 2);
-        else POOL_BWD(bf16_t, 0, 0);
+        if (C % 8 == 0) pool_bwd_launch<bf16_t, 8>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
+        else pool_bwd_launch<bf16_t, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
     }
-#undef POOL_BWD
     return hipGetLastError();
 }
 

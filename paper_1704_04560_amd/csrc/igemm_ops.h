@@ -442,23 +442,34 @@ template <typename T> struct FcDgrad {
     }
 };
 
-// Weight gradient of one shard: p = input feature i plus the bias row p = IN, q = output unit o,
-// k = sample in the shard.  P = x^T (tensor b), Q = dy^T (tensor a); both row-contiguous.
-// blockIdx.z as for convolutions (G = 1).
+// Weight gradient of one shard: p = input feature i (logical (c, h, w) order) plus the bias
+// row p = IN, q = output unit o, k = sample in the shard.  P = x^T (tensor b), Q = dy^T
+// (tensor a); both row-contiguous.  When the input is stored in (h, w, c) order (perm_c,
+// perm_hw > 1) the row-fast scalar loader maps each logical row to its stored column, so the
+// gradient is written in logical order either way.  blockIdx.z as for convolutions (G = 1).
 template <typename T> struct FcWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     struct PR { int i; bool ok, bias; };
-    __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.C, p == a.C}; }
+    __device__ static PR pr(const GemmArgs& a, const Ctx&, int p)
+    {
+        int i = p;
+        if (a.perm_c > 1 && a.perm_hw > 1 && p < a.C) {
+            const int ch = p / a.perm_hw, hw = p - ch * a.perm_hw;
+            i = hw * a.perm_c + ch;
+        }
+        return PR{i, p < a.C, p == a.C};
+    }
     __device__ static T p_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
     {
         const bool kok = k < c.kend;
         const T x = B.at(s.ok && kok, (c.b0 + k) * a.C + s.i);
         return s.bias ? (kok ? one<T>() : zero<T>()) : x;
     }
+    // (16-byte loads only for inputs in logical order)
     typedef PR PC;
-    __device__ static PC pc(const GemmArgs& a, const Ctx& c, int p0) { return pr(a, c, p0); }
+    __device__ static PC pc(const GemmArgs& a, const Ctx&, int p0) { return PC{p0, p0 < a.C, p0 == a.C}; }
     __device__ static u32x4 p_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PC& s, int k)
     {
         const bool kok = k < c.kend;
@@ -478,28 +489,18 @@ template <typename T> struct FcWgrad {
     {
         return B.at16(s.ok && k < c.kend, (c.b0 + k) * a.Qdim + s.off);
     }
-    // grads[r][w_off + o * IN + i] with i mapped back to (c, h, w) order, or the bias
+    // grads[r][w_off + o * IN + i], or the bias
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
     {
         float* g = static_cast<float*>(a.out) + (long long)c.r * a.out_ld;
         const long long row = a.out_off + (long long)q * a.C;
-        const bool perm = a.perm_c > 1 && a.perm_hw > 1;
-        if (!perm && p + 3 < a.C && ((row + p + (long long)c.r * a.out_ld) & 3) == 0) {
+        if (p + 3 < a.C && ((row + p + (long long)c.r * a.out_ld) & 3) == 0) {
             *reinterpret_cast<f32x4*>(g + row + p) = acc;
             return;
         }
         for (int i = 0; i < np; ++i) {
-            const int ii = p + i;
-            if (ii == a.C) {
-                g[a.bias_off + q] = acc[i];
-            } else {
-                int li = ii;
-                if (perm) {
-                    const int hw = ii / a.perm_c, ch = ii - hw * a.perm_c;
-                    li = ch * a.perm_hw + hw;
-                }
-                g[row + li] = acc[i];
-            }
+            if (p + i == a.C) g[a.bias_off + q] = acc[i];
+            else g[row + p + i] = acc[i];
         }
     }
 };

@@ -45,7 +45,8 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
     const GemmDims d = fc_wgrad_dims(dt, Nb, R, IN, OUT);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
-    const bool pv = IN % vec_elems(dt) == 0, qv = OUT % vec_elems(dt) == 0;
+    const bool perm = perm_c > 1 && perm_hw > 1;
+    const bool pv = IN % vec_elems(dt) == 0 && !perm, qv = OUT % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef FcWgrad<float> Op;
         if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);

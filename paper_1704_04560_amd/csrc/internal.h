@@ -1,7 +1,8 @@
 // Internal declarations shared by the host orchestration (api.hip) and the kernel files.
 //
 // Data layouts on the device (per step):
-//   activations and data gradients of convolution and pooling layers: NHWC [n][h][w][c];
+//   activations and data gradients of convolution and pooling layers: NHWC [n][h][w][c],
+//   except a pooling layer that feeds a fully connected layer (NCHW, the order it reads);
 //   the input of a first convolution: NHWC in the compute type (converted from the caller's NCHW);
 //   fully connected inputs: the producing layer's layout ((h, w, c) order after a spatial layer);
 //   weights as the GEMMs read them (prepared every step from the fp32 master copy):
@@ -140,11 +141,13 @@ void prep_fill_divisors(PrepJob& j);
 // NCHW fp32 -> NHWC compute type (C == 1 or H*W == 1: a plain copy / cast).
 hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipStream_t s);
 hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
-// Max pooling over NHWC tensors; argmax holds the window position (u*K + v) per output.
-hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, const void* x, void* y,
-                    uint8_t* argmax, hipStream_t s);
-hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, const uint8_t* argmax,
-                    const void* dy, void* dx, const void* mask, bool mask_f32, hipStream_t s);
+// Max pooling over NHWC tensors; argmax holds the window position (u*K + v) per output.  The
+// pooled tensor (and argmax) is NCHW when out_nchw / dy_nchw is set.
+hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, bool out_nchw,
+                    const void* x, void* y, uint8_t* argmax, hipStream_t s);
+hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, bool dy_nchw,
+                    const uint8_t* argmax, const void* dy, void* dx, const void* mask,
+                    bool mask_f32, hipStream_t s);
 // Softmax cross-entropy of B rows; with loss_out set, also the batch-mean loss (block_sums holds
 // ceil(B/4) floats; *sync must be 0 before the first launch and is 0 again after every launch).
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,

@@ -71,9 +71,6 @@ template <> struct Mma<bf16_t> {
     }
 };
 
-// k tile per compute type: two MFMA k steps
-template <typename T> constexpr int tile_k() { return 2 * Mma<T>::KSTEP; }
-
 template <typename T> __device__ __forceinline__ T zero() { return T(0); }
 template <typename T> __device__ __forceinline__ T one();
 template <> __device__ __forceinline__ float one<float>() { return 1.0f; }
@@ -371,12 +368,11 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RV, BR, B
 
 // ---- the tiled MFMA kernel --------------------------------------------------------------------
 
-template <class Op, int FP, int FQ, int PK, int QK>
+template <class Op, int FP, int FQ, int BK, int PK, int QK>
 __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 {
     typedef typename Op::TT T;
     typedef Mma<T> M;
-    constexpr int BK = tile_k<T>();
     constexpr int BP = 32 * FP, BQ = 32 * FQ;
     constexpr int VEC = M::VEC;
     typedef Lds<BK, VEC> L;
@@ -509,11 +505,12 @@ __global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
 
 // ---- launch ---------------------------------------------------------------------------------
 
-template <class Op, int FP, int FQ, int PK, int QK>
+template <class Op, int FP, int FQ, int BK, int PK, int QK>
 static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
 {
     typedef typename Op::TT T;
     constexpr int VEC = 16 / sizeof(T);
+    if (a.kchunk % BK != 0) return hipErrorInvalidValue;  // plan and kernel disagree
     dim3 grid((a.Qdim + 32 * FQ - 1) / (32 * FQ), (a.Pdim + 32 * FP - 1) / (32 * FP), gz);
     if (grid.y > 65535u || grid.z > 65535u) return hipErrorInvalidConfiguration;
     size_t shm = 0;
@@ -523,7 +520,7 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
         if (n > kMaxTab) return hipErrorInvalidValue;  // the plan keeps chunks within the table
         shm = sizeof(TabEnt) * (size_t)n;
     }
-    hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, PK, QK>), grid, dim3(256), shm, s, a);
+    hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
     const long long per = (long long)a.Pdim * a.Qdim;
@@ -540,32 +537,35 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     return hipGetLastError();
 }
 
-// Tile shapes: (FP, FQ) in {(1,2), (1,4), (2,2), (2,4), (4,4)}.
-template <class Op, int PK, int QK>
-static hipError_t launch_shape(const GemmArgs& a, const GemmPlan& g, int gz, hipStream_t s)
+// Tile shapes (FP, FQ) in {(1,2), (1,4), (2,2), (2,4), (4,4)}, k tile 32 or 64.
+template <class Op, int BK, int PK, int QK>
+static hipError_t launch_shape_bk(const GemmArgs& a, const GemmPlan& g, int gz, hipStream_t s)
 {
     if (g.FP == 1) {
-        if (g.FQ == 4) return launch_tile<Op, 1, 4, PK, QK>(a, gz, s);
-        return launch_tile<Op, 1, 2, PK, QK>(a, gz, s);
+        if (g.FQ == 4) return launch_tile<Op, 1, 4, BK, PK, QK>(a, gz, s);
+        return launch_tile<Op, 1, 2, BK, PK, QK>(a, gz, s);
     }
     if (g.FP == 2) {
-        if (g.FQ == 4) return launch_tile<Op, 2, 4, PK, QK>(a, gz, s);
-        return launch_tile<Op, 2, 2, PK, QK>(a, gz, s);
+        if (g.FQ == 4) return launch_tile<Op, 2, 4, BK, PK, QK>(a, gz, s);
+        return launch_tile<Op, 2, 2, BK, PK, QK>(a, gz, s);
     }
-    return launch_tile<Op, 4, 4, PK, QK>(a, gz, s);
+    return launch_tile<Op, 4, 4, BK, PK, QK>(a, gz, s);
 }
 
 // Runs operation Op with loaders (PK, QK) under plan g; zdim = blocks along z before splits.
 template <class Op, int PK, int QK>
-static hipError_t run_gemm(GemmArgs a, const GemmPlan& g, int zdim, float* partial, hipStream_t s)
+static hipError_t run_gemm(GemmArgs a, const GemmPlan& g, int zdim, float* partial,
+                           hipStream_t s)
 {
     if (a.Pdim <= 0 || a.Qdim <= 0 || zdim <= 0) return hipSuccess;
-    if (g.BK != tile_k<typename Op::TT>()) return hipErrorInvalidValue;
     a.splits = g.splits;
     a.kchunk = g.kchunk;
     a.partial = partial;
     if (g.splits > 1 && !partial) return hipErrorInvalidValue;
-    return launch_shape<Op, PK, QK>(a, g, zdim * g.splits, s);
+    const int gz = zdim * g.splits;
+    if (g.BK == 32) return launch_shape_bk<Op, 32, PK, QK>(a, g, gz, s);
+    if (g.BK == 64) return launch_shape_bk<Op, 64, PK, QK>(a, g, gz, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace mtx

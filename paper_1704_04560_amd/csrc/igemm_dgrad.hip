@@ -93,8 +93,8 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, 
 }
 
 hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* wc, void* dx,
-                          const void* mask, bool mask_f32, float* col, float* partial,
-                          hipStream_t s)
+                          const void* mask, bool mask_f32, float* col,
+                          float* partial, hipStream_t s)
 {
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = wc; a.out = col;

@@ -97,8 +97,8 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, 
                       const void* mask, bool mask_f32, float* partial, hipStream_t s);
 // Data gradient through an fp32 col buffer of conv_dgrad_col_elems() elements; wc: Wc.
 hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* wc, void* dx,
-                          const void* mask, bool mask_f32, float* col, float* partial,
-                          hipStream_t s);
+                          const void* mask, bool mask_f32, float* col,
+                          float* partial, hipStream_t s);
 // Weight and bias gradient of R shards of g.N images each; x and dy point at the first shard.
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
                       float* grads, long long ld, long long w_off, long long b_off,

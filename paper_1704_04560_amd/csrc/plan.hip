@@ -1,5 +1,7 @@
 // Launch planning for the implicit GEMMs (host only), shared by the workspace sizing in
 // api.hip and by the launches, so that both always agree.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace mtx {
@@ -19,31 +21,38 @@ int vec_elems(int dt) { return dt == DT_F32 ? 4 : 8; }
 
 static long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
-// Tile: the largest of 128x128, 64x128, 64x64, 32x128, 32x64 (rows x columns) that still gives
-// at least two blocks per compute unit (the smallest when none does), with rows limited by P.
-// Reduction splits then double while the launch has fewer than four blocks per compute unit and
-// every split keeps at least two k tiles.  kmax (an LDS table limit) can force more splits; the
-// fp32 partial sums are capped at 64M elements.
+// Tile: the largest of 128x128, 64x128, 64x64, 32x128, 32x64 (rows x columns) that gives at
+// least two blocks per compute unit, or at least 64 tiles and a reduction long enough for splits
+// to fill the GPU (the smallest tile when none does); rows are limited by P.  Reduction splits
+// then double while the launch has fewer than four blocks per compute unit and every split
+// keeps at least two k tiles.  kmax (an LDS table limit) can force more splits; the fp32
+// partial sums are capped at 64M elements.
 GemmPlan plan_for(int dt, const GemmDims& d)
 {
     constexpr long long kTargetTiles = 512, kTargetBlocks = 1024, kMaxPartial = 64ll << 20;
     GemmPlan g{};
-    g.BK = dt == DT_F32 ? 32 : 64;
     const int fpmax = d.P <= 32 ? 1 : (d.P <= 64 ? 2 : 4);
     static const int cand[5][2] = {{4, 4}, {2, 4}, {2, 2}, {1, 4}, {1, 2}};
     auto tiles = [&](int fp, int fq) {
         return cdiv(d.P, 32 * fp) * cdiv(d.Q, 32 * fq) * (long long)d.Z;
     };
+    // k tile: 64, or 32 for short reductions and for the fp32 128 x 128 tile (LDS size)
+    auto bk_of = [&](int fp, int fq) {
+        return (d.K <= 32 || (dt == DT_F32 && fp == 4 && fq == 4)) ? 32 : 64;
+    };
     g.FP = 1;
     g.FQ = 2;
     for (const auto& c : cand) {
         if (c[0] > fpmax) continue;
-        if (tiles(c[0], c[1]) >= kTargetTiles) {
+        const long long t = tiles(c[0], c[1]);
+        const long long ks = std::min(cdiv(d.K, bk_of(c[0], c[1])) / 8, 32ll);
+        if (t >= kTargetTiles || (t >= 64 && t * ks >= kTargetBlocks)) {
             g.FP = c[0];
             g.FQ = c[1];
             break;
         }
     }
+    g.BK = bk_of(g.FP, g.FQ);
     const long long t = tiles(g.FP, g.FQ);
     const long long ktiles = cdiv(d.K, g.BK);
     long long splits = 1;

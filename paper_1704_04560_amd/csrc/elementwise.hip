@@ -46,31 +46,34 @@ __device__ __forceinline__ unsigned fdivu(const FastDiv& f, unsigned n)
     return (__umulhi(n, f.m) + n) >> f.s;
 }
 
-// dst[n][hw][c] = x[n][c][hw], one thread per destination element (coalesced writes).
+// dst[n][hw][c] = x[n][c][hw]: one thread per (n, hw) position, channels in a loop, so that
+// the reads (consecutive hw per channel plane) and the writes (consecutive positions) both
+// coalesce.
 template <typename T>
 __global__ __launch_bounds__(256) void to_nhwc_kernel(const float* __restrict__ x,
-                                                      T* __restrict__ dst, int total, int C,
-                                                      int HW, FastDiv fc, FastDiv fhw)
+                                                      T* __restrict__ dst, int positions, int C,
+                                                      int HW, FastDiv fhw)
 {
     const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= total) return;
-    const unsigned pos = fdivu(fc, (unsigned)t), c = (unsigned)t - pos * (unsigned)C;
-    const unsigned n = fdivu(fhw, pos), hw = pos - n * (unsigned)HW;
-    dst[t] = from_f32<T>(x[((long long)n * C + c) * HW + hw]);
+    if (t >= positions) return;
+    const unsigned n = fdivu(fhw, (unsigned)t), hw = (unsigned)t - n * (unsigned)HW;
+    const float* src = x + (long long)n * C * HW + hw;
+    T* out = dst + (long long)t * C;
+    for (int c = 0; c < C; ++c) out[c] = from_f32<T>(src[(long long)c * HW]);
 }
 
 hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipStream_t s)
 {
-    const long long total = (long long)N * C * HW;
-    if (total <= 0) return hipSuccess;
-    const FastDiv fc = make_fastdiv((unsigned)C), fhw = make_fastdiv((unsigned)HW);
-    dim3 g(grid_for((size_t)total, 256));
+    const long long positions = (long long)N * HW;
+    if (positions <= 0 || C <= 0) return hipSuccess;
+    const FastDiv fhw = make_fastdiv((unsigned)HW);
+    dim3 g(grid_for((size_t)positions, 256));
     if (dt == DT_F32)
         hipLaunchKernelGGL(to_nhwc_kernel<float>, g, dim3(256), 0, s, x, static_cast<float*>(dst),
-                           (int)total, C, HW, fc, fhw);
+                           (int)positions, C, HW, fhw);
     else
         hipLaunchKernelGGL(to_nhwc_kernel<bf16_t>, g, dim3(256), 0, s, x,
-                           static_cast<bf16_t*>(dst), (int)total, C, HW, fc, fhw);
+                           static_cast<bf16_t*>(dst), (int)positions, C, HW, fhw);
     return hipGetLastError();
 }
 
@@ -79,7 +82,7 @@ hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipSt
 // converts kPrepPerBlock consecutive destination elements.  The source index of a destination
 // element follows from its layout (see PrepKind).
 
-constexpr int kPrepPerThread = 4, kPrepPerBlock = 256 * kPrepPerThread;
+constexpr int kPrepPerThread = 16, kPrepPerBlock = 256 * kPrepPerThread;
 
 int prep_blocks(int n) { return (n + kPrepPerBlock - 1) / kPrepPerBlock; }
 
@@ -109,33 +112,33 @@ void prep_fill_divisors(PrepJob& j)
     }
 }
 
-__device__ __forceinline__ long long prep_src(const PrepJob& j, unsigned d)
+__device__ __forceinline__ int prep_src(const PrepJob& j, unsigned d)
 {
     switch (j.kind) {
     case PREP_CONV_F: {  // d = co*(KK*cg) + uv*cg + ci
         const unsigned co = fdivu(j.f0, d), r = d - co * (unsigned)(j.KK * j.cg);
         const unsigned uv = fdivu(j.f1, r), ci = r - uv * (unsigned)j.cg;
-        return ((long long)co * j.cg + ci) * j.KK + uv;
+        return ((int)co * j.cg + (int)ci) * j.KK + (int)uv;
     }
     case PREP_CONV_D: {  // d = ((g*cg + ci)*KK + uv)*og + co
         const unsigned r1 = fdivu(j.f0, d), co = d - r1 * (unsigned)j.og;
         const unsigned r2 = fdivu(j.f1, r1), uv = r1 - r2 * (unsigned)j.KK;
         const unsigned g = fdivu(j.f2, r2), ci = r2 - g * (unsigned)j.cg;
-        return (((long long)g * j.og + co) * j.cg + ci) * j.KK + uv;
+        return (((int)g * j.og + (int)co) * j.cg + (int)ci) * j.KK + (int)uv;
     }
     case PREP_CONV_C: {  // d = ((g*KK + uv)*cg + ci)*og + co
         const unsigned r1 = fdivu(j.f0, d), co = d - r1 * (unsigned)j.og;
         const unsigned r2 = fdivu(j.f1, r1), ci = r1 - r2 * (unsigned)j.cg;
         const unsigned g = fdivu(j.f2, r2), uv = r2 - g * (unsigned)j.KK;
-        return (((long long)g * j.og + co) * j.cg + ci) * j.KK + uv;
+        return (((int)g * j.og + (int)co) * j.cg + (int)ci) * j.KK + (int)uv;
     }
     case PREP_FC_PERM: {  // d = o*IN + hw*C + c
         const unsigned o = fdivu(j.f0, d), r = d - o * (unsigned)j.IN;
         const unsigned hw = fdivu(j.f1, r), c = r - hw * (unsigned)j.C;
-        return (long long)o * j.IN + (long long)c * j.HW + hw;
+        return (int)o * j.IN + (int)c * j.HW + (int)hw;
     }
     default:
-        return d;
+        return (int)d;
     }
 }
 
@@ -222,8 +225,8 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, 
     const unsigned pos = fdivu(fcv, (unsigned)t), c0 = ((unsigned)t - pos * CG) * CV;
     const unsigned r = fdivu(fow, pos), j = pos - r * (unsigned)OW;
     const unsigned n = fdivu(foh, r), i = r - n * (unsigned)OH;
-    const T* xp = x + (((long long)n * H + i * S) * W + j * S) * C + c0;
-    const long long rs = (long long)W * C;
+    const T* xp = x + (((int)n * H + (int)i * S) * W + (int)j * S) * C + (int)c0;
+    const int rs = W * C;
     Chans<T, CV> best = load_chans<T, CV>(xp);
     float bv[CV];
     uint8_t bi[CV];
@@ -241,13 +244,13 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, 
     if (out_nchw) {
 #pragma unroll
         for (int e = 0; e < CV; ++e) {
-            const long long o = (((long long)n * C + c0 + e) * OH + i) * OW + j;
+            const int o = (((int)n * C + (int)c0 + e) * OH + (int)i) * OW + (int)j;
             y[o] = best.v[e];
             argmax[o] = bi[e];
         }
         return;
     }
-    const long long o = (long long)pos * C + c0;
+    const int o = (int)pos * C + (int)c0;
     store_chans<T, CV>(y + o, best);
 #pragma unroll
     for (int e = 0; e < CV; ++e) argmax[o + e] = bi[e];
@@ -326,11 +329,11 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, 
             if (dy_nchw) {
 #pragma unroll
                 for (int e = 0; e < CV; ++e) {
-                    const long long o = (((long long)n * C + c0 + e) * OH + i) * OW + j;
+                    const int o = (((int)n * C + (int)c0 + e) * OH + i) * OW + j;
                     if (argmax[o] == here) acc[e] += to_f32<T>(dy[o]);
                 }
             } else {
-                const long long o = (((long long)n * OH + i) * OW + j) * C + c0;
+                const int o = (((int)n * OH + i) * OW + j) * C + (int)c0;
                 const Chans<T, CV> g = load_chans<T, CV>(dy + o);
                 uint8_t am[CV];
                 if constexpr (CV == 8) *reinterpret_cast<uint2*>(am) = *reinterpret_cast<const uint2*>(argmax + o);
@@ -341,7 +344,7 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, 
                     if (am[e] == here) acc[e] += to_f32<T>(g.v[e]);
             }
         }
-    const long long xo = (long long)pos * C + c0;
+    const int xo = (int)pos * C + (int)c0;
     if (mask) {
 #pragma unroll
         for (int e = 0; e < CV; ++e) {

@@ -12,8 +12,10 @@
 // ends with four consecutive rows p of one column q.
 //
 // LDS tiles hold BR rows x BK reduction steps, k contiguous, rows padded by 16 bytes; the
-// 16-byte granules of row r are rotated by r/8, which keeps the fragment reads, the 16-byte
-// tile writes and the transposing writes below free of bank conflicts.
+// 16-byte granules of row r are rotated by r/16.  With 64 banks of 4 bytes, the 16 rows of a
+// fragment read then fall on distinct banks (row stride = 4 mod 64 dwords-groups), and the
+// transposing writes, whose lanes step through rows 8 (bf16) or 4 (fp32) apart, are spread by
+// the rotation instead of piling onto two banks.
 //
 // Operand loaders (per operand, chosen by the operation and the alignment of its tensor):
 //   SK  scalar, k-fast: a thread keeps one k per tile and steps over rows;
@@ -124,6 +126,19 @@ struct TabEnt {
     short u, v;
 };
 
+// One 8-byte LDS read per entry.
+__device__ __forceinline__ TabEnt ld_tab(const TabEnt* p)
+{
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    return TabEnt{(int)w[0], (short)(w[1] & 0xffffu), (short)(w[1] >> 16)};
+}
+
+// Window bounds test without short-circuit branches.
+__device__ __forceinline__ bool inside(int h, int w, int H, int W)
+{
+    return ((unsigned)h < (unsigned)H) & ((unsigned)w < (unsigned)W);
+}
+
 struct Ctx {
     int grp, r, split, kbeg, kend, b0;
     const TabEnt* tab;  // LDS index table over [kbeg, kbeg + kchunk), or null
@@ -187,7 +202,7 @@ template <int BK, int VEC> struct Lds {
     static constexpr int NG = BK / VEC;   // 16-byte granules per row (a power of 2)
     __device__ __forceinline__ static int at(int row, int k)
     {
-        const int g = ((k / VEC) + (row >> 3)) & (NG - 1);
+        const int g = ((k / VEC) + (row >> 4)) & (NG - 1);
         return row * LDK + g * VEC + (k & (VEC - 1));
     }
 };

@@ -35,6 +35,10 @@ static inline GemmArgs conv_args(const ConvGeom& g)
     a.fd_hw = make_fastdiv((unsigned)(g.H * g.W));
     a.fd_w = make_fastdiv((unsigned)g.W);
     a.fd_c = make_fastdiv((unsigned)g.C);
+    a.fd_kcg = make_fastdiv((unsigned)(g.K * a.cg));
+    a.fd_cg = make_fastdiv((unsigned)a.cg);
+    a.fd_kog = make_fastdiv((unsigned)(g.K * a.og));
+    a.fd_og = make_fastdiv((unsigned)a.og);
     return a;
 }
 
@@ -50,8 +54,8 @@ template <typename T> struct ConvFwd {
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
         if (k >= c.kend) return TabEnt{0, (short)kFar, (short)kFar};
-        const int kc = a.K * a.cg;
-        const int u = k / kc, rem = k - u * kc, v = rem / a.cg, ci = rem - v * a.cg;
+        const int u = (int)fdiv(a.fd_kcg, (unsigned)k), rem = k - u * a.K * a.cg;
+        const int v = (int)fdiv(a.fd_cg, (unsigned)rem), ci = rem - v * a.cg;
         return TabEnt{(u * a.W + v) * a.C + ci, (short)u, (short)v};
     }
     // P: Wf[(g*og + p) * Kdim + k]
@@ -62,7 +66,7 @@ template <typename T> struct ConvFwd {
     }
     __device__ static T p_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const PK& s, int p)
     {
-        return B.at(s.ok && p < a.Pdim, s.base + p * a.Kdim);
+        return B.at(s.ok & (p < a.Pdim), s.base + p * a.Kdim);
     }
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx& c, int p)
@@ -71,7 +75,7 @@ template <typename T> struct ConvFwd {
     }
     __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     // Q: x[n][oh*S - PD + u][ow*S - PD + v][g*cg + ci]
     struct QR { int base, h0, w0; };
@@ -90,18 +94,17 @@ template <typename T> struct ConvFwd {
     }
     __device__ static T q_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        const TabEnt e = c.tab[k - c.kbeg];
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
-        return B.at((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W, s.base + e.off);
+        return B.at(inside(hi, wi, a.H, a.W), s.base + e.off);
     }
     typedef QR QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx& c, int q) { return qr(a, c, q); }
     __device__ static u32x4 q_kv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QV& s, int k)
     {
-        const TabEnt e = c.tab[(k - c.kbeg) / (16 / (int)sizeof(T))];
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
-        return B.at16((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W,
-                      s.base + e.off);
+        return B.at16(inside(hi, wi, a.H, a.W), s.base + e.off);
     }
     // y[q][g*og + p] = acc + bias, ReLU
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
@@ -131,8 +134,8 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
         if (k >= c.kend) return TabEnt{0, (short)-kFar, (short)-kFar};
-        const int kc = a.K * a.og;
-        const int u = k / kc, rem = k - u * kc, v = rem / a.og, co = rem - v * a.og;
+        const int u = (int)fdiv(a.fd_kog, (unsigned)k), rem = k - u * a.K * a.og;
+        const int v = (int)fdiv(a.fd_og, (unsigned)rem), co = rem - v * a.og;
         return TabEnt{-(u * a.OW + v) * a.OC + co, (short)u, (short)v};
     }
     // P: Wd[(g*cg + p) * Kdim + k]
@@ -143,7 +146,7 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     }
     __device__ static T p_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const PK& s, int p)
     {
-        return B.at(s.ok && p < a.Pdim, s.base + p * a.Kdim);
+        return B.at(s.ok & (p < a.Pdim), s.base + p * a.Kdim);
     }
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx& c, int p)
@@ -152,7 +155,7 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     }
     __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     // Q: dy
     struct QR { int base, hp, wp, b; };
@@ -173,10 +176,9 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     __device__ static T q_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
         if constexpr (STRIDE1) {
-            const TabEnt e = c.tab[k - c.kbeg];
+            const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
             const int th = s.hp - e.u, tw = s.wp - e.v;
-            return B.at((unsigned)th < (unsigned)a.OH && (unsigned)tw < (unsigned)a.OW,
-                        s.base + e.off);
+            return B.at(inside(th, tw, a.OH, a.OW), s.base + e.off);
         } else {
             const bool kok = k < c.kend;
             const int kk = kok ? k : 0;
@@ -193,10 +195,9 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     __device__ static QV qv(const GemmArgs& a, const Ctx& c, int q) { return qr(a, c, q); }
     __device__ static u32x4 q_kv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QV& s, int k)
     {
-        const TabEnt e = c.tab[(k - c.kbeg) / (16 / (int)sizeof(T))];
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         const int th = s.hp - e.u, tw = s.wp - e.v;
-        return B.at16((unsigned)th < (unsigned)a.OH && (unsigned)tw < (unsigned)a.OW,
-                      s.base + e.off);
+        return B.at16(inside(th, tw, a.OH, a.OW), s.base + e.off);
     }
     // dx[q][g*cg + p] = acc, times the ReLU mask of the layer below
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
@@ -226,7 +227,7 @@ template <typename T> struct ConvDgradCol {
     }
     __device__ static T p_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const PK& s, int p)
     {
-        return B.at(s.ok && p < a.Pdim, s.base + p * a.og);
+        return B.at(s.ok & (p < a.Pdim), s.base + p * a.og);
     }
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx& c, int p)
@@ -235,7 +236,7 @@ template <typename T> struct ConvDgradCol {
     }
     __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     // Q: dy[q * OC + g*og + k]
     struct QK { int off; bool ok; };
@@ -245,7 +246,7 @@ template <typename T> struct ConvDgradCol {
     }
     __device__ static T q_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const QK& s, int q)
     {
-        return B.at(s.ok && q < a.Qdim, q * a.OC + s.off);
+        return B.at(s.ok & (q < a.Qdim), q * a.OC + s.off);
     }
     typedef RowOk QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx& c, int q)
@@ -254,7 +255,7 @@ template <typename T> struct ConvDgradCol {
     }
     __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
     {
@@ -294,13 +295,13 @@ template <typename T> struct ConvWgrad {
     }
     __device__ static T p_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
     {
-        return B.at(s.ok && k < c.kend, s.off + k * a.OC);
+        return B.at(s.ok & (k < c.kend), s.off + k * a.OC);
     }
     typedef RowOk PC;
     __device__ static PC pc(const GemmArgs& a, const Ctx& c, int p0) { return pr(a, c, p0); }
     __device__ static u32x4 p_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PC& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k * a.OC);
+        return B.at16(s.ok & (k < c.kend), s.off + k * a.OC);
     }
     // Q: x at window tap (u, v) of position k, channel g*cg + ci
     struct QR { int off, u, v; bool ok, bias; };
@@ -321,20 +322,18 @@ template <typename T> struct ConvWgrad {
     }
     __device__ static T q_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        const TabEnt e = c.tab[k - c.kbeg];
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
         const int hi = e.u + s.u, wi = e.v + s.v;
-        const T x = B.at(s.ok && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W,
-                         e.off + s.off);
+        const T x = B.at(s.ok & inside(hi, wi, a.H, a.W), e.off + s.off);
         return s.bias ? (k < c.kend ? one<T>() : zero<T>()) : x;
     }
     typedef QR QC;
     __device__ static QC qc(const GemmArgs& a, const Ctx& c, int q0) { return qr(a, c, q0); }
     __device__ static u32x4 q_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QC& s, int k)
     {
-        const TabEnt e = c.tab[k - c.kbeg];
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
         const int hi = e.u + s.u, wi = e.v + s.v;
-        const u32x4 x = B.at16(s.ok && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W,
-                               e.off + s.off);
+        const u32x4 x = B.at16(s.ok & inside(hi, wi, a.H, a.W), e.off + s.off);
         if (s.bias) return k < c.kend ? one_chunk<T>() : u32x4{0u, 0u, 0u, 0u};
         return x;
     }
@@ -369,25 +368,25 @@ template <typename T> struct FcFwd {
     __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
     __device__ static T p_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const PK& s, int p)
     {
-        return B.at(s.ok && p < a.Pdim, p * a.Kdim + s.k);
+        return B.at(s.ok & (p < a.Pdim), p * a.Kdim + s.k);
     }
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx&, int p) { return PV{p * a.Kdim, p < a.Pdim}; }
     __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     typedef PK QK;
     __device__ static QK qk(const GemmArgs&, const Ctx& c, int k) { return QK{k, k < c.kend}; }
     __device__ static T q_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const QK& s, int q)
     {
-        return B.at(s.ok && q < a.Qdim, q * a.Kdim + s.k);
+        return B.at(s.ok & (q < a.Qdim), q * a.Kdim + s.k);
     }
     typedef RowOk QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx&, int q) { return QV{q * a.Kdim, q < a.Qdim}; }
     __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     // y[q][p] = acc + bias[p], ReLU
     __device__ static void store4(const GemmArgs& a, const Ctx&, int p, int q, f32x4 acc, int np)
@@ -412,25 +411,25 @@ template <typename T> struct FcDgrad {
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.Pdim}; }
     __device__ static T p_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
     {
-        return B.at(s.ok && k < c.kend, k * a.Pdim + s.off);
+        return B.at(s.ok & (k < c.kend), k * a.Pdim + s.off);
     }
     typedef RowOk PC;
     __device__ static PC pc(const GemmArgs& a, const Ctx&, int p0) { return PC{p0, p0 < a.Pdim}; }
     __device__ static u32x4 p_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PC& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, k * a.Pdim + s.off);
+        return B.at16(s.ok & (k < c.kend), k * a.Pdim + s.off);
     }
     struct QK { int k; bool ok; };
     __device__ static QK qk(const GemmArgs&, const Ctx& c, int k) { return QK{k, k < c.kend}; }
     __device__ static T q_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const QK& s, int q)
     {
-        return B.at(s.ok && q < a.Qdim, q * a.Kdim + s.k);
+        return B.at(s.ok & (q < a.Qdim), q * a.Kdim + s.k);
     }
     typedef RowOk QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx&, int q) { return QV{q * a.Kdim, q < a.Qdim}; }
     __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, s.off + k);
+        return B.at16(s.ok & (k < c.kend), s.off + k);
     }
     // dx[q][p] = acc, times the ReLU mask of the layer below
     __device__ static void store4(const GemmArgs& a, const Ctx&, int p, int q, f32x4 acc, int np)
@@ -464,7 +463,7 @@ template <typename T> struct FcWgrad {
     __device__ static T p_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
     {
         const bool kok = k < c.kend;
-        const T x = B.at(s.ok && kok, (c.b0 + k) * a.C + s.i);
+        const T x = B.at(s.ok & kok, (c.b0 + k) * a.C + s.i);
         return s.bias ? (kok ? one<T>() : zero<T>()) : x;
     }
     // (16-byte loads only for inputs in logical order)
@@ -473,7 +472,7 @@ template <typename T> struct FcWgrad {
     __device__ static u32x4 p_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PC& s, int k)
     {
         const bool kok = k < c.kend;
-        const u32x4 x = B.at16(s.ok && kok, (c.b0 + k) * a.C + s.i);
+        const u32x4 x = B.at16(s.ok & kok, (c.b0 + k) * a.C + s.i);
         if (s.bias) return kok ? one_chunk<T>() : u32x4{0u, 0u, 0u, 0u};
         return x;
     }
@@ -481,13 +480,13 @@ template <typename T> struct FcWgrad {
     __device__ static QR qr(const GemmArgs& a, const Ctx&, int q) { return QR{q, q < a.Qdim}; }
     __device__ static T q_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
     {
-        return B.at(s.ok && k < c.kend, (c.b0 + k) * a.Qdim + s.off);
+        return B.at(s.ok & (k < c.kend), (c.b0 + k) * a.Qdim + s.off);
     }
     typedef RowOk QC;
     __device__ static QC qc(const GemmArgs& a, const Ctx& c, int q0) { return qr(a, c, q0); }
     __device__ static u32x4 q_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QC& s, int k)
     {
-        return B.at16(s.ok && k < c.kend, (c.b0 + k) * a.Qdim + s.off);
+        return B.at16(s.ok & (k < c.kend), (c.b0 + k) * a.Qdim + s.off);
     }
     // grads[r][w_off + o * IN + i], or the bias
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)

@@ -63,6 +63,7 @@ struct GemmArgs {
     unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)
     unsigned b_bytes;      // size of tensor b in bytes
     FastDiv fd_ohw, fd_ow, fd_hw, fd_w, fd_c;
+    FastDiv fd_kcg, fd_cg, fd_kog, fd_og;  // K*cg, cg, K*og, og (index tables)
 };
 
 // GEMM view of one operation: P output rows, Q output columns, K reduction length, Z blocks

@@ -6,12 +6,14 @@ of the R shard gradients and the momentum update.  Inputs are seeded synthetic t
 resident in HBM when the timed region starts.
 
     python bench.py [--steps K] [--warmup W] [--workload lenet|mlp|cifar|alexnet]
-                    [--no-cpu-baseline] [--no-microbench]
+                    [--no-cpu-baseline] [--no-microbench] [--no-extra]
 
 Prints one JSON line.  `value` is samples/s of the whole job (one GPU); `roofline` covers the
 kernel that takes the most time in the step, timed in place with HIP events on the step's
-stream; `grad_avg_update` is the fused average + momentum kernel at the 61M-element, 16-buffer
-size; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same workload.
+stream (its `traffic` comes from a committed rocprofv3 counter summary of the same kernel
+sources, else null); `grad_avg_update` is the fused average + momentum kernel at the
+61M-element, 16-buffer size; `other_workloads` are short runs of the bf16 CIFAR and AlexNet
+workloads; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -48,7 +50,7 @@ def geometry(net):
 def site_work(name, layer, geo, wkl, es):
     """Algorithmic work of one launch of a step's launch site: ("mfma", flops) for the matrix
     kernels (2 x multiply-adds of the convolution / product), ("hbm", bytes) for the others
-    (each tensor read once and written once)."""
+    (each tensor read once and written once), (None, 0) when not modelled."""
     from paper_1704_04560_amd import workloads as wl
     B, R, Nb = wkl.batch, wkl.shards, wkl.shard_batch
     if layer >= 0:
@@ -62,25 +64,37 @@ def site_work(name, layer, geo, wkl, es):
         out_sz = B * g["oc"] * g["oh"] * g["ow"]
         if name in ("fwd", "dgrad", "wgrad"):
             return "mfma", 2.0 * macs
-        if name == "bias_grad":
-            return "hbm", out_sz * es + R * g["oc"] * 4
+        if name == "dgrad_col2im":  # fp32 col read once, dx written, mask read
+            return "hbm", 4.0 * l.k * l.k * g["c"] * B * g["oh"] * g["ow"] + 2 * es * in_sz
         if name == "pool_fwd":
             return "hbm", in_sz * es + out_sz * (es + 1)
         if name == "pool_bwd":
             return "hbm", out_sz * (es + 1) + in_sz * es * 2  # dy + argmax, mask + dx
+        return None, 0.0
     P = wkl_params(wkl)
     if name == "avg_update":
         mom = wkl.momentum != 0.0
         return "hbm", (R + (5 if mom else 3)) * 4 * P
-    if name == "cast_w":
-        return "hbm", 6 * P
-    if name == "cast_x":
+    if name == "prep_w":
+        # every weight tensor is read once (fp32) and written once per layout it is prepared in
+        # (convolutions below the first parameter layer need a data-gradient layout too)
+        first = min(i for i, g in enumerate(geo) if g["layer"].kind in (wl.CONV, wl.FC))
+        tot = 0.0
+        for i, g in enumerate(geo):
+            l = g["layer"]
+            if l.kind == wl.CONV:
+                n = g["oc"] * (g["c"] // l.groups) * l.k * l.k
+                tot += n * (4 + es) * (2 if i > first else 1)
+            elif l.kind == wl.FC:
+                tot += g["oc"] * g["c"] * g["h"] * g["w"] * (4 + es)
+        return "hbm", tot
+    if name == "prep_x":
         c, h, w = wkl.net.in_shape
-        return "hbm", 6 * B * c * h * w
+        return "hbm", (4 + es) * B * c * h * w
     if name == "softmax_xent":
         nc = wkl.net.num_classes
         return "hbm", B * nc * (4 + es) + B * 4 + 4
-    return "hbm", 0.0
+    return None, 0.0
 
 
 _P = {}
@@ -150,6 +164,128 @@ def cpu_baseline(wkl, budget_s=12.0):
             "sample": f"{steps} oracle steps of {R} shards x {nb} samples ({prec}), {el:.1f} s"}
 
 
+def source_hash():
+    """sha256 over the HIP sources and the C header (identifies the kernels a stored counter
+    summary was taken from)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1704_04560_amd", "csrc")
+    for f in sorted(os.listdir(csrc)) + ["../../include/mtx.h"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(workload, site, layer):
+    """HBM bytes per launch of a kernel from a committed rocprofv3 counter summary under
+    profiles/ (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy of known size), or None when no
+    summary covers it or the kernels have changed since it was taken."""
+    d = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(d):
+        return None
+    want = source_hash()
+    for f in sorted(os.listdir(d)):
+        if not f.endswith(".md"):
+            continue
+        with open(os.path.join(d, f)) as fh:
+            for line in fh:
+                if not line.startswith("traffic-json: "):
+                    continue
+                rec = json.loads(line[len("traffic-json: "):])
+                if (rec.get("workload") == workload and rec.get("site") == site
+                        and rec.get("layer") == layer and rec.get("source_sha256") == want):
+                    return rec["bytes_per_launch"]
+    return None
+
+
+def measure(torch, mtx, wl, name, steps, warmup):
+    """Timed steps of one workload; returns the bench fields of that workload."""
+    wkl = wl.WORKLOADS[name]
+    net = wkl.net
+    layers = wl.layer_tuples(net)
+    model = mtx.Model(net.in_shape, layers, net.dtype, wkl.shards, wkl.shard_batch, seed=0)
+    x, y = wl.make_batch(net, wkl.batch, seed=0)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    del x, y
+    loss = torch.zeros(1, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(warmup):
+        model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
+    torch.cuda.synchronize()
+
+    def timed(k):
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for _ in range(k):
+            model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_end) / k
+
+    # timed region: K steps as a training loop runs them (graph replay of the step)
+    ms = timed(steps)
+    assert torch.isfinite(loss).item(), "non-finite loss"
+    # second timed region of K steps with a HIP event pair around every kernel (on the step's
+    # stream), for the per-kernel durations behind the roofline figures
+    mtx.mtx_set_timing(model.handle, True)
+    mtx.mtx_get_timing(model.handle, reset=True)
+    ms_events = timed(steps)
+    sites = mtx.mtx_get_timing(model.handle)
+    mtx.mtx_set_timing(model.handle, False)
+    model.close()
+    del xd, yd
+
+    es = 2 if net.dtype == wl.BF16 else 4
+    geo = geometry(net)
+    kernels = []
+    for (sname, layer, launches, total) in sites:
+        if launches == 0:
+            continue
+        bound, work = site_work(sname, layer, geo, wkl, es)
+        kernels.append(dict(name=sname, layer=layer, avg_ms=total / launches, bound=bound,
+                            work=work))
+    peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
+    # the dominant kernel: the longest one whose algorithmic work is modelled
+    dom = max((k for k in kernels if k["bound"]), key=lambda k: k["avg_ms"])
+    if dom["bound"] == "mfma":
+        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak_mm, "unit": "TFLOP/s"}
+        roof["frac"] = round(ach / peak_mm, 4)
+    else:
+        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_GBps"],
+                "unit": "GB/s"}
+        roof["frac"] = round(ach / PEAK["hbm_GBps"], 4)
+    roof["traffic"] = stored_traffic(name, dom["name"], dom["layer"])
+    roof["kernel"] = f"{dom['name']} (layer {dom['layer']})"
+    roof["kernel_ms"] = round(dom["avg_ms"], 5)
+    roof["work_per_launch"] = dom["work"]
+
+    mfma_ms = sum(k["avg_ms"] for k in kernels if k["bound"] == "mfma")
+    mfma_flops = sum(k["work"] for k in kernels if k["bound"] == "mfma")
+    au = [k for k in kernels if k["name"] == "avg_update"][0]
+    return {
+        "wkl": wkl,
+        "value": round(wkl.batch / (ms * 1e-3), 1),
+        "ms_per_step": round(ms, 5),
+        "dtype": "bf16" if net.dtype == wl.BF16 else "f32",
+        "roofline": roof,
+        "gemm_mfma": {"achieved_TFLOPs": round(mfma_flops / (mfma_ms * 1e-3) / 1e12, 3),
+                      "peak_TFLOPs": peak_mm,
+                      "frac": round(mfma_flops / (mfma_ms * 1e-3) / 1e12 / peak_mm, 4)},
+        "step_avg_update": {"GBps": round(au["work"] / (au["avg_ms"] * 1e-3) / 1e9, 1),
+                            "ms": round(au["avg_ms"], 5)},
+        "kernel_ms_sum": round(sum(k["avg_ms"] for k in kernels), 5),
+        "ms_per_step_with_kernel_events": round(ms_events, 5),
+        "kernels": [{"name": k["name"], "layer": k["layer"], "ms": round(k["avg_ms"], 5)}
+                    for k in kernels],
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -158,6 +294,8 @@ def main():
     ap.add_argument("--workload", default="lenet")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-microbench", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the short runs of the bf16 CIFAR and AlexNet workloads")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy (torch copy_) so that hardware "
                          "byte counters can be scaled against a kernel of known traffic")
@@ -179,100 +317,41 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    wkl = wl.WORKLOADS[args.workload]
-    net = wkl.net
-    layers = wl.layer_tuples(net)
-    model = mtx.Model(net.in_shape, layers, net.dtype, wkl.shards, wkl.shard_batch, seed=0)
-    x, y = wl.make_batch(net, wkl.batch, seed=0)
-    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
-    loss = torch.zeros(1, device="cuda")
-    stream = torch.cuda.current_stream()
 
-    for _ in range(args.warmup):
-        model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
-    torch.cuda.synchronize()
-
-    def timed(steps):
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_end = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t_start.record(stream)
-        for _ in range(steps):
-            model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
-        t_end.record(stream)
-        torch.cuda.synchronize()
-        return t_start.elapsed_time(t_end) / steps
-
-    # timed region: K steps as a training loop runs them
-    ms = timed(args.steps)
-    assert torch.isfinite(loss).item(), "non-finite loss"
-    # second timed region of K steps with a HIP event pair around every kernel launch (on the
-    # step's stream), for the per-kernel durations behind the roofline figures
-    mtx.mtx_set_timing(model.handle, True)
-    mtx.mtx_get_timing(model.handle, reset=True)
-    ms_events = timed(args.steps)
-    sites = mtx.mtx_get_timing(model.handle)
-    mtx.mtx_set_timing(model.handle, False)
-
-    es = 2 if net.dtype == wl.BF16 else 4
-    geo = geometry(net)
-    kernels = []
-    for (name, layer, launches, total) in sites:
-        if launches == 0:
-            continue
-        avg_ms = total / launches
-        bound, work = site_work(name, layer, geo, wkl, es)
-        kernels.append(dict(name=name, layer=layer, avg_ms=avg_ms, bound=bound, work=work))
-    kernel_sum = sum(k["avg_ms"] for k in kernels)
-    dom = max(kernels, key=lambda k: k["avg_ms"])
-    if dom["bound"] == "mfma":
-        peak = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
-        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s"}
-    else:
-        peak = PEAK["hbm_GBps"]
-        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": peak, "unit": "GB/s"}
-    roof["frac"] = round(ach / peak, 4)
-    roof["traffic"] = None
-    roof["kernel"] = f"{dom['name']} (layer {dom['layer']})"
-    roof["kernel_ms"] = round(dom["avg_ms"], 5)
-
-    mfma_ms = sum(k["avg_ms"] for k in kernels if k["bound"] == "mfma")
-    mfma_flops = sum(k["work"] for k in kernels if k["bound"] == "mfma")
-    peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
-    au = [k for k in kernels if k["name"] == "avg_update"][0]
+    r = measure(torch, mtx, wl, args.workload, args.steps, args.warmup)
+    wkl = r.pop("wkl")
     out = {
         "metric": METRIC,
-        "value": round(wkl.batch / (ms * 1e-3), 1),
+        "value": r.pop("value"),
         "unit": "samples/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 5),
+        "ms_per_step": r.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if net.dtype == wl.BF16 else "f32",
+        "dtype": r.pop("dtype"),
         "data": "synthetic (seeded; no dataset)",
         "config": {"workload": wkl.description, "global_batch": wkl.batch, "shards": wkl.shards,
                    "shard_batch": wkl.shard_batch, "lr": wkl.lr, "momentum": wkl.momentum,
                    "parallelism": f"{wkl.shards} data-parallel shards on 1 GPU"},
-        "roofline": roof,
-        "gemm_mfma": {"achieved_TFLOPs": round(mfma_flops / (mfma_ms * 1e-3) / 1e12, 3),
-                      "peak_TFLOPs": peak_mm,
-                      "frac": round(mfma_flops / (mfma_ms * 1e-3) / 1e12 / peak_mm, 4)},
-        "step_avg_update": {"GBps": round(au["work"] / (au["avg_ms"] * 1e-3) / 1e9, 1),
-                            "ms": round(au["avg_ms"], 5)},
-        "kernel_ms_sum": round(kernel_sum, 5),
-        "ms_per_step_with_kernel_events": round(ms_events, 5),
-        "kernels": [{"name": k["name"], "layer": k["layer"], "ms": round(k["avg_ms"], 5)}
-                    for k in kernels],
     }
-    model.close()
-    del xd, yd
+    out.update(r)
     if not args.no_microbench:
         out["grad_avg_update"] = microbench_avg_update(torch, mtx)
+    if not args.no_extra:
+        extra = {}
+        for name in ("cifar", "alexnet"):
+            if name == args.workload:
+                continue
+            e = measure(torch, mtx, wl, name, 20, 3)
+            extra[name] = {"workload": e["wkl"].description, "samples_per_s": e["value"],
+                           "ms_per_step": e["ms_per_step"], "dtype": e["dtype"],
+                           "roofline": e["roofline"], "gemm_mfma": e["gemm_mfma"],
+                           "step_avg_update": e["step_avg_update"]}
+            torch.cuda.empty_cache()
+        out["other_workloads"] = extra
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wkl)
     print(json.dumps(out), flush=True)

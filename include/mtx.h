@@ -175,10 +175,11 @@ int mtx_set_graph_replay(mtx_model* m, int enable);
  * around each kernel launch; mtx_set_timing(m, 0) stops it.  mtx_get_timing waits for the
  * recorded events and fills up to `capacity` entries, one per launch site of the step, in launch
  * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
- * Launch-site names: "cast_w", "cast_x", "fwd", "pool_fwd", "softmax_xent" (with the loss
- * mean), "wgrad" (weight and bias gradient), "dgrad", "pool_bwd", "avg_update"; a matrix site
- * includes the second pass of a split reduction.  Timing adds one event pair per launch; use it
- * for measurement runs. */
+ * Launch-site names: "prep_w" (weight layouts), "prep_x" (input layout), "fwd", "pool_fwd",
+ * "softmax_xent" (with the loss mean), "wgrad" (weight and bias gradient), "dgrad", "pool_bwd",
+ * "avg_update"; the second kernel of an operation is a site of its own: "<site>_reduce" (the
+ * second pass of a split reduction) and "dgrad_col2im".  Timing adds one event pair per kernel;
+ * use it for measurement runs. */
 typedef struct {
     char name[32];
     int layer;        /* layer index, or -1 for a kernel that is not tied to one layer */

@@ -427,13 +427,20 @@ struct mtx_model {
 
 namespace {
 
-// Run one kernel launch (a callable returning hipError_t); with timing on, bracket it with an
-// event pair of its launch site.
-template <class F>
-hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s, F&& f)
+// Timing context of the launch site being enqueued (timing runs are single-threaded per model;
+// the context lives only while a site's launches are enqueued).
+struct TimingCtx {
+    mtx_model* m = nullptr;
+    std::string base;
+    int layer = -1;
+    int site = -1;
+};
+thread_local TimingCtx g_tctx;
+
+// Start site number t.cur (creating it on the first step), recording its start event.
+hipError_t begin_site(mtx_model* m, const std::string& name, int layer, hipStream_t s, int* idx)
 {
     Timer& t = m->timer;
-    if (!t.on) return f();
     if ((int)t.sites.size() <= t.cur) {
         Timer::Site st;
         st.name = name;
@@ -445,21 +452,53 @@ hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s,
             }
         t.sites.push_back(st);
     }
-    Timer::Site& st = t.sites[t.cur++];
+    *idx = t.cur++;
+    Timer::Site& st = t.sites[*idx];
     if (st.pending == Timer::kDepth) {
         hipError_t e = t.retire(st);
         if (e != hipSuccess) return e;
     }
-    hipError_t e = hipEventRecord(st.ev[st.head][0], s);
-    if (e == hipSuccess) e = f();
-    if (e == hipSuccess) e = hipEventRecord(st.ev[st.head][1], s);
+    return hipEventRecord(st.ev[st.head][0], s);
+}
+
+hipError_t end_site(mtx_model* m, int idx, hipStream_t s)
+{
+    Timer::Site& st = m->timer.sites[idx];
+    hipError_t e = hipEventRecord(st.ev[st.head][1], s);
     if (e != hipSuccess) return e;
     st.head = (st.head + 1) % Timer::kDepth;
     st.pending += 1;
     return hipSuccess;
 }
 
+// Run one launch site (a callable returning hipError_t); with timing on, bracket it with an
+// event pair.  A site that launches several kernels marks the boundaries with timing_split, so
+// that every kernel is timed on its own.
+template <class F>
+hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s, F&& f)
+{
+    if (!m->timer.on) return f();
+    g_tctx.m = m;
+    g_tctx.base = name;
+    g_tctx.layer = layer;
+    hipError_t e = begin_site(m, name, layer, s, &g_tctx.site);
+    if (e == hipSuccess) e = f();
+    if (e == hipSuccess) e = end_site(m, g_tctx.site, s);
+    g_tctx.m = nullptr;
+    return e;
+}
+
 }  // namespace
+
+namespace mtx {
+void timing_split(hipStream_t s, const char* part)
+{
+    TimingCtx& c = g_tctx;
+    if (!c.m) return;
+    if (end_site(c.m, c.site, s) != hipSuccess) return;
+    if (begin_site(c.m, c.base + "_" + part, c.layer, s, &c.site) != hipSuccess) c.m = nullptr;
+}
+}  // namespace mtx
 
 extern "C" {
 

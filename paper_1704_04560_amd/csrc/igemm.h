@@ -538,6 +538,7 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
+    timing_split(s, "reduce");
     const long long per = (long long)a.Pdim * a.Qdim;
     const int rg = gz / a.splits;
     if (a.splits >= 16)

@@ -113,6 +113,7 @@ hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* 
         e = v ? run_gemm<ConvDgradCol<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s)
               : run_gemm<ConvDgradCol<bf16_t>, L_SK, L_SK>(a, p, d.Z, partial, s);
     if (e != hipSuccess) return e;
+    timing_split(s, "col2im");
     GemmArgs c = conv_args(g);
     c.out = dx; c.mask = mask; c.mask_f32 = mask_f32;
     if (dt == DT_F32) launch_col2im<float>(c, col, s);

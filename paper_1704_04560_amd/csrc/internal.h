@@ -113,6 +113,11 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
                     const void* x, const void* dy, float* grads, long long ld, long long w_off,
                     long long b_off, float* partial, hipStream_t s);
 
+// Kernel timing (api.hip): a launcher that enqueues several kernels for one operation calls
+// this between them; with timing on, the kernels before and after are timed as separate sites
+// (the later one named <site>_<part>).  No effect otherwise.
+void timing_split(hipStream_t s, const char* part);
+
 // elementwise.hip
 
 // Weight preparation: one launch converts the fp32 master weights into every layout above.

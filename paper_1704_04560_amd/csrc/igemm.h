@@ -144,9 +144,30 @@ struct Ctx {
     const TabEnt* tab;  // LDS index table over [kbeg, kbeg + kchunk), or null
 };
 
-__device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c)
+// Blocks are dispatched to the 8 XCDs round-robin by linear block id, and each XCD has its own
+// L2.  The tile a block computes is taken from a renumbering in which every XCD owns one
+// contiguous range of tiles, ordered so that neighbouring tiles read the same rows of the
+// larger operand: with SHARE_Q (convolutions: the activations are the large operand) the p
+// tiles of one q tile are neighbours, otherwise (fully connected: the weights) the q tiles of
+// one p tile; the reduction range (blockIdx.z) varies slowest.
+struct TileId {
+    int bx, by, bz;
+};
+template <bool SHARE_Q>
+__device__ __forceinline__ TileId xcd_tile()
 {
-    const int z = blockIdx.z;
+    constexpr unsigned kXcd = 8;
+    const unsigned nb = gridDim.x * gridDim.y * gridDim.z;
+    const unsigned hw = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const unsigned q = nb / kXcd, r = nb % kXcd, x = hw % kXcd;
+    const unsigned lid = x * q + min(x, r) + hw / kXcd;
+    const unsigned xy = gridDim.x * gridDim.y, bz = lid / xy, l2 = lid - bz * xy;
+    if (SHARE_Q) return TileId{(int)(l2 / gridDim.y), (int)(l2 % gridDim.y), (int)bz};
+    return TileId{(int)(l2 % gridDim.x), (int)(l2 / gridDim.x), (int)bz};
+}
+
+__device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c, int z)
+{
     c.grp = z % a.G;
     const int rest = z / a.G;
     c.r = rest / a.splits;
@@ -397,9 +418,10 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     __shared__ __attribute__((aligned(16))) T sQ[BQ * L::LDK];
     extern __shared__ TabEnt tab[];  // sized at launch
 
+    const TileId tile = xcd_tile<Op::SHARE_Q>();
     Ctx c;
-    decode_z(a, c);
-    const int p0 = blockIdx.y * BP, q0 = blockIdx.x * BQ;
+    decode_z(a, c, tile.bz);
+    const int p0 = tile.by * BP, q0 = tile.bx * BQ;
     const int tid = threadIdx.x;
 
     if constexpr (Op::TAB) {
@@ -461,7 +483,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     }
 
     const bool split = a.splits > 1;
-    float* part = a.partial + (long long)blockIdx.z * a.Pdim * a.Qdim;
+    float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
 #pragma unroll
     for (int i = 0; i < FP; ++i)
 #pragma unroll

@@ -3,6 +3,7 @@
 //
 // Interface of an operation Op (only the members its loaders use need to exist):
 //   TT                compute type; P_IS_A: P reads tensor a (else tensor b, Q the other)
+//   SHARE_Q           neighbouring tiles share q (see xcd_tile)
 //   TAB, TAB_CHUNK    an LDS table over the block's k range exists; for 16-byte Q loads it
 //                     has one entry per chunk; tab_entry(a, c, k) builds an entry
 //   pk/p_sk           SK loader on P: state for column k, element of row p
@@ -50,6 +51,7 @@ static inline GemmArgs conv_args(const ConvGeom& g)
 template <typename T> struct ConvFwd {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = true;
     static constexpr bool TAB = true, TAB_CHUNK = true;
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
@@ -130,6 +132,7 @@ template <typename T> struct ConvFwd {
 template <typename T, bool STRIDE1> struct ConvDgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = true;
     static constexpr bool TAB = STRIDE1, TAB_CHUNK = true;
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
@@ -218,6 +221,7 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
 template <typename T> struct ConvDgradCol {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = true;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     // P: Wc[(g*KK*cg + p) * og + k]
     struct PK { int base; bool ok; };
@@ -276,6 +280,7 @@ template <typename T> struct ConvDgradCol {
 template <typename T> struct ConvWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = true;
+    static constexpr bool SHARE_Q = true;
     static constexpr bool TAB = true, TAB_CHUNK = false;
     // entry for position k of the shard: the offset of x[b0 + n][oh*S - PD][ow*S - PD][0] and
     // the window origin (oh*S - PD, ow*S - PD)
@@ -363,6 +368,7 @@ template <typename T> struct ConvWgrad {
 template <typename T> struct FcFwd {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     struct PK { int k; bool ok; };
     __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
@@ -406,6 +412,7 @@ template <typename T> struct FcFwd {
 template <typename T> struct FcDgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     typedef RowOk PR;
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.Pdim}; }
@@ -449,6 +456,7 @@ template <typename T> struct FcDgrad {
 template <typename T> struct FcWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     struct PR { int i; bool ok, bias; };
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p)

@@ -162,13 +162,24 @@ int mtx_set_params(mtx_model* m, const float* w_host, const float* v_host);
 int mtx_get_layer_output(const mtx_model* m, int layer, float* dst_host, size_t n);
 int mtx_get_pool_argmax(const mtx_model* m, int layer, uint8_t* dst_host, size_t n);
 
-/* Graph replay (execution option; default on).  mtx_train_step records its kernel sequence
+/* Graph replay (execution option; default off: on MI355X direct launches of the step measured
+ * faster than replaying it from a graph).  With it on, mtx_train_step records its kernel sequence
  * into a HIP graph on a private stream and replays it on the caller's stream for as long as
  * (x, labels, lr, momentum, loss_out) stay the same; other arguments trigger a new capture, and
  * after three captures in a row the model stays on direct launches.  Steps run directly, without
  * a graph, while kernel timing is on or when the caller's stream is itself being captured.  The
  * results do not depend on this option.  enable = 0 switches it off (and frees the graph). */
 int mtx_set_graph_replay(mtx_model* m, int enable);
+
+/* Overlap (execution option; default on when a step's matrix work is at least 50 GFLOP, where
+ * it measured faster, off for smaller steps).  The data gradients of a step form a chain from the
+ * last layer to the first; each layer's weight gradient needs only that layer's output
+ * gradient and input.  With overlap on, mtx_train_step runs the weight gradients on a second
+ * stream of the model, forked from the caller's stream after each output gradient is written
+ * and joined back before the average + update, so they run beside the chain.  The results do
+ * not depend on this option.  Steps run on the caller's stream alone while kernel timing is
+ * on.  enable = 0 switches it off. */
+int mtx_set_overlap(mtx_model* m, int enable);
 
 /* Kernel timing of mtx_train_step (measurement support; not part of the method).
  * mtx_set_timing(m, 1) makes every later mtx_train_step record a HIP event pair on its stream

@@ -59,6 +59,7 @@ struct LayerPlan {
     bool nhwc;                   // stored output is NHWC (convolution and pooling layers)
     int perm_c, perm_hw;         // fully connected after a spatial layer: input in (h, w, c)
     size_t act_off;              // workspace byte offset of the output [B][...]
+    size_t dy_off;               // gradient of the loss with respect to that output
     size_t am_off;               // max-pool decisions [B][...] (uint8)
     size_t fw_off, bw_off;       // prepared forward / data-gradient weights (elements)
 };
@@ -76,8 +77,10 @@ struct Plan {
     std::vector<PrepJob> jobs;   // weight preparation
     int prep_blocks = 0;
     size_t prep_elems = 0;
-    size_t xin_off = 0, prep_off = 0, jobs_off = 0, dbuf_off[2] = {0, 0}, loss_off = 0;
-    size_t partial_off = 0, col_off = 0, sync_off = 0;
+    size_t xin_off = 0, prep_off = 0, jobs_off = 0, loss_off = 0;
+    size_t partial_off = 0, partial_w_off = 0, col_off = 0, sync_off = 0;
+    int n_wgrad = 0;             // layers with a weight gradient
+    double gemm_flops = 0;       // multiply-adds x 2 of every matrix launch of a step
     size_t ws_bytes = 0;
 };
 
@@ -230,8 +233,9 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
 
     // workspace carve-up
     size_t ws = 0;
-    size_t max_grad = (size_t)last.oc;  // data-gradient buffers: dz and every layer's input
-    size_t max_partial = 0, max_col = 0;
+    // fp32 partial sums: one region for the forward and data-gradient launches, one for the
+    // weight gradients (which may run concurrently on a second stream)
+    size_t max_partial = 0, max_partial_w = 0, max_col = 0;
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.act_f32 = (pl.dt == MTX_F32) || (i + 1 == pl.L.size());
@@ -241,9 +245,12 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             lp.am_off = ws;
             ws = align_up(ws + lp.out_elems * pl.B, kAlign);
         }
-        if (lp.in_elems > max_grad) max_grad = lp.in_elems;
-        if (lp.out_elems > max_grad) max_grad = lp.out_elems;
-        // fp32 partial sums of the matrix launches whose reduction is split
+        if ((int)i >= pl.first_param) {
+            lp.dy_off = ws;
+            ws = align_up(ws + lp.out_elems * pl.B * es, kAlign);
+        }
+        // fp32 partial sums of the matrix launches whose reduction is split (the last entry of
+        // dims is the weight gradient)
         GemmDims dims[3];
         int nd = 0;
         if (lp.kind == MTX_CONV) {
@@ -267,7 +274,16 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         }
         for (int k = 0; k < nd; ++k) {
             const size_t pz = partial_elems(pl.dt, dims[k]);
-            if (pz > max_partial) max_partial = pz;
+            const bool wgrad = k == nd - 1;
+            size_t& mx = wgrad ? max_partial_w : max_partial;
+            if (pz > mx) mx = pz;
+        }
+        if (lp.w_len) {
+            pl.n_wgrad += 1;
+            const double macs = lp.kind == MTX_CONV
+                                    ? (double)pl.B * lp.oh * lp.ow * lp.oc * (lp.c / lp.g) * lp.k * lp.k
+                                    : (double)pl.B * lp.in_elems * lp.oc;
+            pl.gemm_flops += 2.0 * macs * (lp.need_dx ? 3 : 2);
         }
     }
     if (pl.x_convert) {
@@ -278,15 +294,13 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     ws = align_up(ws + pl.prep_elems * es, kAlign);
     pl.jobs_off = ws;
     ws = align_up(ws + pl.jobs.size() * sizeof(PrepJob), kAlign);
-    for (int k = 0; k < 2; ++k) {
-        pl.dbuf_off[k] = ws;
-        ws = align_up(ws + max_grad * pl.B * es, kAlign);
-    }
     pl.loss_off = ws;  // per-block loss sums of the softmax launch, then its counter
     pl.sync_off = align_up(ws + (size_t)((pl.B + 3) / 4) * 4, kAlign);
     ws = pl.sync_off + kAlign;
     pl.partial_off = ws;
     ws = align_up(ws + max_partial * 4, kAlign);
+    pl.partial_w_off = ws;
+    ws = align_up(ws + max_partial_w * 4, kAlign);
     pl.col_off = ws;
     ws = align_up(ws + max_col * 4, kAlign);
     pl.ws_bytes = ws;
@@ -387,7 +401,7 @@ struct Timer {
 // and on (x, labels, lr, momentum, loss_out); it is captured once into a HIP graph on a private
 // stream and replayed on the caller's stream while those arguments stay the same.
 struct GraphCache {
-    bool enabled = true;
+    bool enabled = false;
     hipStream_t capture_stream = nullptr;
     hipGraphExec_t exec = nullptr;
     const float* x = nullptr;
@@ -423,6 +437,11 @@ struct mtx_model {
     hipStream_t last_stream;
     Timer timer;
     GraphCache graph;
+    // second stream for the weight gradients (overlapped with the data-gradient chain)
+    bool overlap = false;
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> fork;  // per weight-gradient launch: its output gradient is ready
+    hipEvent_t join = nullptr;     // every weight gradient is done
 };
 
 namespace {
@@ -490,6 +509,19 @@ hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s,
 
 }  // namespace
 
+namespace {
+void destroy_streams(mtx_model* m)
+{
+    for (hipEvent_t& e : m->fork)
+        if (e) (void)hipEventDestroy(e);
+    m->fork.clear();
+    if (m->join) (void)hipEventDestroy(m->join);
+    m->join = nullptr;
+    if (m->side) (void)hipStreamDestroy(m->side);
+    m->side = nullptr;
+}
+}  // namespace
+
 namespace mtx {
 void timing_split(hipStream_t s, const char* part)
 {
@@ -549,11 +581,21 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     m->w = bufs->w; m->v = bufs->v; m->grads = bufs->grads; m->gavg = bufs->grad_avg;
     m->ws = static_cast<char*>(bufs->workspace);
     m->last_stream = static_cast<hipStream_t>(stream);
+    // Measured on MI355X: running the weight gradients beside the data-gradient chain gains a
+    // few percent when the step's matrix work is large (CIFAR-, AlexNet-sized steps) and loses
+    // on small steps, whose kernels each fill the GPU on their own (LeNet).
+    m->overlap = m->pl.gemm_flops >= 50e9;
 
     std::vector<float> w0;
     glorot_init_host(m->pl, seed, w0);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
+    hipError_t e = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking);
+    if (e != hipSuccess) m->side = nullptr;
+    m->fork.assign(m->pl.n_wgrad, nullptr);
+    for (size_t i = 0; i < m->fork.size() && e == hipSuccess; ++i)
+        e = hipEventCreateWithFlags(&m->fork[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&m->join, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
     if (e == hipSuccess && !m->pl.jobs.empty())
@@ -561,6 +603,7 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
                            m->pl.jobs.size() * sizeof(PrepJob), hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
+        destroy_streams(m);
         delete m;
         return hip_fail(e, "mtx_init_model");
     }
@@ -572,9 +615,19 @@ void mtx_free_model(mtx_model* m)
 {
     if (!m) return;
     (void)hipStreamSynchronize(m->last_stream);
+    if (m->side) (void)hipStreamSynchronize(m->side);
     m->graph.destroy();
     m->timer.destroy();
+    destroy_streams(m);
     delete m;
+}
+
+int mtx_set_overlap(mtx_model* m, int enable)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    m->overlap = enable != 0;
+    m->graph.reset();  // the captured launch sequence depends on it
+    return MTX_OK;
 }
 
 int mtx_set_timing(mtx_model* m, int enable)
@@ -659,61 +712,75 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     }
     // ---- loss and its gradient (shard-mean loss: scale 1/Nb) ----
     const LayerPlan& last = pl.L.back();
-    void* cur = ws + pl.dbuf_off[0];
-    void* nxt = ws + pl.dbuf_off[1];
     float* block_sums = reinterpret_cast<float*>(ws + pl.loss_off);
     unsigned* sync = reinterpret_cast<unsigned*>(ws + pl.sync_off);
     HIP_TRY(launch_site(m, "softmax_xent", -1, s, [&] {
                 return softmax_xent(dt, pl.B, last.oc, pl.Nb,
-                                    reinterpret_cast<const float*>(ws + last.act_off), labels, cur,
-                                    block_sums, sync, loss_out, s);
+                                    reinterpret_cast<const float*>(ws + last.act_off), labels,
+                                    ws + last.dy_off, block_sums, sync, loss_out, s);
             }), "softmax cross-entropy");
 
     // ---- backward in reverse layer order; weight gradients per shard into grads[r] ----
+    // The data gradients form a chain on stream s.  A weight gradient needs only its layer's
+    // output gradient and input, so (unless kernels are being timed) it runs on the second
+    // stream, forked after its output gradient is written and joined before the update.
+    const bool overlap = m->overlap && !m->timer.on;
+    float* partial_w = overlap ? reinterpret_cast<float*>(ws + pl.partial_w_off) : partial;
     const long long ld = (long long)pl.ld;
+    int nfork = 0;
     for (int l = (int)pl.L.size() - 1; l >= pl.first_param && l >= 0; --l) {
         const LayerPlan& lp = pl.L[l];
         const void* in_l = l == 0 ? x_in : static_cast<const void*>(ws + pl.L[l - 1].act_off);
-        const bool need_dx = lp.need_dx;
+        const void* dy = ws + lp.dy_off;
+        void* dx = lp.need_dx ? ws + pl.L[l - 1].dy_off : nullptr;
         const void* mask = (l > 0 && pl.L[l - 1].relu) ? ws + pl.L[l - 1].act_off : nullptr;
         const bool mask_f32 = l > 0 && pl.L[l - 1].act_f32;
+        hipStream_t sw = s;
+        if (lp.w_len && overlap) {
+            HIP_TRY(hipEventRecord(m->fork[nfork], s), "fork");
+            HIP_TRY(hipStreamWaitEvent(m->side, m->fork[nfork], 0), "fork");
+            ++nfork;
+            sw = m->side;
+        }
         if (lp.kind == MTX_CONV) {
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
-            HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
-                        return conv_wgrad(dt, gs, pl.R, in_l, cur, m->grads, ld, (long long)lp.w_off,
-                                          (long long)lp.b_off, partial, s);
+            HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
+                        return conv_wgrad(dt, gs, pl.R, in_l, dy, m->grads, ld, (long long)lp.w_off,
+                                          (long long)lp.b_off, partial_w, sw);
                     }), "conv weight gradient");
-            if (need_dx) {
+            if (lp.need_dx) {
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
                 float* col = reinterpret_cast<float*>(ws + pl.col_off);
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
                             return lp.dgrad_col
-                                       ? conv_dgrad_col(dt, g, cur, bwd_w(lp), nxt, mask, mask_f32,
+                                       ? conv_dgrad_col(dt, g, dy, bwd_w(lp), dx, mask, mask_f32,
                                                         col, partial, s)
-                                       : conv_dgrad(dt, g, cur, bwd_w(lp), nxt, mask, mask_f32,
+                                       : conv_dgrad(dt, g, dy, bwd_w(lp), dx, mask, mask_f32,
                                                     partial, s);
                         }), "conv data gradient");
             }
         } else if (lp.kind == MTX_FC) {
-            HIP_TRY(launch_site(m, "wgrad", l, s, [&] {
+            HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
                         return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, lp.perm_c,
-                                        lp.perm_hw, in_l, cur, m->grads, ld, (long long)lp.w_off,
-                                        (long long)lp.b_off, partial, s);
+                                        lp.perm_hw, in_l, dy, m->grads, ld, (long long)lp.w_off,
+                                        (long long)lp.b_off, partial_w, sw);
                     }), "fc weight gradient");
-            if (need_dx)
+            if (lp.need_dx)
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
-                            return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, cur, bwd_w(lp), nxt,
+                            return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, dy, bwd_w(lp), dx,
                                             mask, mask_f32, partial, s);
                         }), "fc data gradient");
-        } else {
-            if (!need_dx) continue;
+        } else if (lp.need_dx) {
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
                         return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
-                                        reinterpret_cast<const uint8_t*>(ws + lp.am_off), cur, nxt,
+                                        reinterpret_cast<const uint8_t*>(ws + lp.am_off), dy, dx,
                                         mask, mask_f32, s);
                     }), "pool backward");
         }
-        void* t = cur; cur = nxt; nxt = t;
+    }
+    if (nfork) {
+        HIP_TRY(hipEventRecord(m->join, m->side), "join");
+        HIP_TRY(hipStreamWaitEvent(s, m->join, 0), "join");
     }
     // ---- average of the R shard gradients fused with the optimizer step ----
     HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {

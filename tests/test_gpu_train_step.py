@@ -160,6 +160,7 @@ def test_graph_replay_matches_direct_launches(name):
     _say(f"[case] graph replay vs direct {name}")
     a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
     b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
+    mtx.mtx_set_graph_replay(a.handle, True)
     mtx.mtx_set_graph_replay(b.handle, False)
     x, y = wl.make_batch(net, R * Nb, seed=3)
     xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
@@ -179,5 +180,35 @@ def test_graph_replay_matches_direct_launches(name):
     b.train_step(xd, yd, 0.02, 0.9, lb)
     torch.cuda.synchronize()
     assert np.array_equal(a.get_params()[0].view(np.uint32), b.get_params()[0].view(np.uint32))
+    a.close()
+    b.close()
+
+
+@pytest.mark.parametrize("name", ["lenet", "tiny", "alexnet"])
+def test_overlapped_weight_gradients_match_one_stream(name):
+    """Weight gradients on the second stream give bit-identical results to the one-stream
+    order, over several graph-replayed and direct steps."""
+    net = {"lenet": wl.LENET, "tiny": _tiny(wl.BF16), "alexnet": wl.ALEXNET}[name]
+    layers = wl.layer_tuples(net)
+    R, Nb = {"lenet": (4, 16), "tiny": (3, 5), "alexnet": (2, 2)}[name]
+    _say(f"[case] overlap vs one stream {name}")
+    a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=4)
+    b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=4)
+    mtx.mtx_set_overlap(a.handle, True)
+    mtx.mtx_set_graph_replay(a.handle, True)
+    mtx.mtx_set_overlap(b.handle, False)
+    x, y = wl.make_batch(net, R * Nb, seed=4)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    for step in range(3):
+        if step == 2:
+            mtx.mtx_set_graph_replay(a.handle, False)
+        a.train_step(xd, yd, 0.01, 0.9)
+        b.train_step(xd, yd, 0.01, 0.9)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.grads_host().view(np.uint32), b.grads_host().view(np.uint32)), step
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
     a.close()
     b.close()

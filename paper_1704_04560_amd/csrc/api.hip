@@ -62,6 +62,8 @@ struct LayerPlan {
     size_t dy_off;               // gradient of the loss with respect to that output
     size_t am_off;               // max-pool decisions [B][...] (uint8)
     size_t fw_off, bw_off;       // prepared forward / data-gradient weights (elements)
+    bool run;                    // first convolution over the padded input (conv_fwd_run)
+    RunGeom rg;                  // its padded input geometry
 };
 
 constexpr size_t kNone = ~(size_t)0;
@@ -77,7 +79,7 @@ struct Plan {
     std::vector<PrepJob> jobs;   // weight preparation
     int prep_blocks = 0;
     size_t prep_elems = 0;
-    size_t xin_off = 0, prep_off = 0, jobs_off = 0, loss_off = 0;
+    size_t xin_off = 0, xin_bytes = 0, prep_off = 0, jobs_off = 0, loss_off = 0;
     size_t partial_off = 0, partial_w_off = 0, col_off = 0, sync_off = 0;
     int n_wgrad = 0;             // layers with a weight gradient
     double gemm_flops = 0;       // multiply-adds x 2 of every matrix launch of a step
@@ -177,7 +179,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         if (lp.kind != MTX_FC && (lp.h >= kFarLimit || lp.w >= kFarLimit))
             return fail(MTX_EINVAL, "layer %d: spatial size must be below %d", (int)i, kFarLimit);
     }
-    const LayerPlan& first = pl.L.front();
+    LayerPlan& first = pl.L.front();
     if (first.kind == MTX_FC) {
         pl.x_c = 1;
         pl.x_hw = (int)first.in_elems;
@@ -186,6 +188,23 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         pl.x_hw = pl.in_h * pl.in_w;
     }
     pl.x_convert = pl.dt == MTX_BF16 || (pl.x_c > 1 && pl.x_hw > 1);
+    // A first convolution whose channel count rules out 16-byte loads reads a padded input
+    // instead (see conv_fwd_run), when that adds at most 3x to its multiply-adds.
+    first.run = false;
+    if (first.kind == MTX_CONV && first.g == 1 && first.c % vec_elems(pl.dt) != 0) {
+        const int vecb = 16 / (int)es;  // elements per 16 bytes
+        int cp = first.c;
+        while ((first.s * cp) % vecb) ++cp;
+        const int run = (first.k * cp + vecb - 1) / vecb * vecb;
+        int wp = first.w + 2 * first.p;
+        while ((wp * cp) % vecb) ++wp;
+        const double inflate = (double)first.k * run / ((double)first.k * first.k * first.c);
+        if (inflate <= 3.0) {
+            first.run = true;
+            first.rg = RunGeom{first.h + 2 * first.p, wp, cp, run};
+            pl.x_convert = true;
+        }
+    }
 
     // weight preparation jobs; every prepared tensor starts 16-byte aligned
     size_t pe = 0;
@@ -207,7 +226,12 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         PrepJob j{};
         j.n = (int)lp.w_len;
         j.src = (long long)lp.w_off;
-        if (lp.kind == MTX_CONV) {
+        if (lp.kind == MTX_CONV && lp.run) {
+            j.kind = PREP_CONV_RUN;
+            j.n = lp.oc * lp.k * lp.rg.RUN;
+            j.C = lp.c; j.Cp = lp.rg.Cp; j.K = lp.k; j.RUN = lp.rg.RUN;
+            lp.fw_off = add_job(j);
+        } else if (lp.kind == MTX_CONV) {
             j.g = lp.g; j.cg = lp.c / lp.g; j.og = lp.oc / lp.g; j.KK = lp.k * lp.k;
             j.kind = PREP_CONV_F;
             lp.fw_off = add_job(j);
@@ -257,7 +281,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             ConvGeom gs = gb;
             gs.N = pl.Nb;
-            dims[nd++] = conv_fwd_dims(pl.dt, gb);
+            dims[nd++] = lp.run ? conv_fwd_run_dims(pl.dt, gb, lp.rg) : conv_fwd_dims(pl.dt, gb);
             if (lp.need_dx) {
                 if (lp.dgrad_col) {
                     dims[nd++] = conv_dgrad_col_dims(pl.dt, gb);
@@ -266,7 +290,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
                     dims[nd++] = conv_dgrad_dims(pl.dt, gb);
                 }
             }
-            dims[nd++] = conv_wgrad_dims(pl.dt, gs, pl.R);
+            dims[nd++] = lp.run ? conv_wgrad_run_dims(pl.dt, gs, lp.rg, pl.R)
+                                : conv_wgrad_dims(pl.dt, gs, pl.R);
         } else if (lp.kind == MTX_FC) {
             dims[nd++] = fc_fwd_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
             if (lp.need_dx) dims[nd++] = fc_dgrad_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
@@ -288,7 +313,11 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     }
     if (pl.x_convert) {
         pl.xin_off = ws;
-        ws = align_up(ws + (size_t)pl.in_c * pl.in_h * pl.in_w * pl.B * es, kAlign);
+        const size_t xe = first.run ? (size_t)first.rg.Hp * first.rg.Wp * first.rg.Cp
+                                    : (size_t)pl.in_c * pl.in_h * pl.in_w;
+        if ((long long)xe * pl.B * es > kMaxBytes) return fail(MTX_EINVAL, "input exceeds 2 GiB");
+        pl.xin_bytes = xe * pl.B * es;
+        ws = align_up(ws + pl.xin_bytes, kAlign);
     }
     pl.prep_off = ws;
     ws = align_up(ws + pl.prep_elems * es, kAlign);
@@ -598,6 +627,9 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     if (e == hipSuccess) e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
+    // the padded input's border and extra channels are never written by a step
+    if (e == hipSuccess && m->pl.L.front().run)
+        e = hipMemsetAsync(m->ws + m->pl.xin_off, 0, m->pl.xin_bytes, s);
     if (e == hipSuccess && !m->pl.jobs.empty())
         e = hipMemcpyAsync(m->ws + m->pl.jobs_off, m->pl.jobs.data(),
                            m->pl.jobs.size() * sizeof(PrepJob), hipMemcpyHostToDevice, s);
@@ -679,9 +711,12 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                 return prep_weights(dt, reinterpret_cast<const PrepJob*>(ws + pl.jobs_off),
                                     (int)pl.jobs.size(), pl.prep_blocks, m->w, ws + pl.prep_off, s);
             }), "weight preparation");
+    const LayerPlan& l0 = pl.L.front();
     if (pl.x_convert)
         HIP_TRY(launch_site(m, "prep_x", -1, s, [&] {
-                    return to_nhwc(dt, x, ws + pl.xin_off, pl.B, pl.x_c, pl.x_hw, s);
+                    return l0.run ? to_nhwc_padded(dt, x, ws + pl.xin_off, pl.B, l0.c, l0.h, l0.w,
+                                                   l0.p, l0.rg, s)
+                                  : to_nhwc(dt, x, ws + pl.xin_off, pl.B, pl.x_c, pl.x_hw, s);
                 }), "input conversion");
     auto fwd_w = [&](const LayerPlan& lp) { return prep + lp.fw_off * es; };
     auto bwd_w = [&](const LayerPlan& lp) { return prep + lp.bw_off * es; };
@@ -695,7 +730,10 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
-                        return conv_fwd(dt, g, in, fwd_w(lp), bias, out, lp.act_f32, lp.relu, partial, s);
+                        return lp.run ? conv_fwd_run(dt, g, lp.rg, in, fwd_w(lp), bias, out,
+                                                     lp.act_f32, lp.relu, partial, s)
+                                      : conv_fwd(dt, g, in, fwd_w(lp), bias, out, lp.act_f32,
+                                                 lp.relu, partial, s);
                     }), "conv forward");
         } else if (lp.kind == MTX_FC) {
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
@@ -745,8 +783,12 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         if (lp.kind == MTX_CONV) {
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
-                        return conv_wgrad(dt, gs, pl.R, in_l, dy, m->grads, ld, (long long)lp.w_off,
-                                          (long long)lp.b_off, partial_w, sw);
+                        return lp.run ? conv_wgrad_run(dt, gs, lp.rg, pl.R, in_l, dy, m->grads, ld,
+                                                       (long long)lp.w_off, (long long)lp.b_off,
+                                                       partial_w, sw)
+                                      : conv_wgrad(dt, gs, pl.R, in_l, dy, m->grads, ld,
+                                                   (long long)lp.w_off, (long long)lp.b_off,
+                                                   partial_w, sw);
                     }), "conv weight gradient");
             if (lp.need_dx) {
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};

@@ -77,6 +77,41 @@ hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipSt
     return hipGetLastError();
 }
 
+// X'[n][PD + h][PD + w][c] = x[n][c][h][w] for c < C: one thread per pixel, channels in a loop.
+template <typename T>
+__global__ __launch_bounds__(256) void to_nhwc_padded_kernel(const float* __restrict__ x,
+                                                             T* __restrict__ dst, int pixels,
+                                                             int C, int H, int W, int PD,
+                                                             int Hp, int Wp, int Cp, FastDiv fw,
+                                                             FastDiv fh)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= pixels) return;
+    const unsigned r = fdivu(fw, (unsigned)t), w = (unsigned)t - r * (unsigned)W;
+    const unsigned n = fdivu(fh, r), h = r - n * (unsigned)H;
+    const float* src = x + ((long long)n * C * H + h) * W + w;
+    T* out = dst + (((long long)n * Hp + PD + h) * Wp + PD + w) * Cp;
+    for (int c = 0; c < C; ++c) out[c] = from_f32<T>(src[(long long)c * H * W]);
+}
+
+hipError_t to_nhwc_padded(Dt dt, const float* x, void* dst, int N, int C, int H, int W,
+                          int PD, const RunGeom& r, hipStream_t s)
+{
+    const long long pixels = (long long)N * H * W;
+    if (pixels <= 0 || C <= 0) return hipSuccess;
+    const FastDiv fw = make_fastdiv((unsigned)W), fh = make_fastdiv((unsigned)H);
+    dim3 g(grid_for((size_t)pixels, 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(to_nhwc_padded_kernel<float>, g, dim3(256), 0, s, x,
+                           static_cast<float*>(dst), (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp,
+                           fw, fh);
+    else
+        hipLaunchKernelGGL(to_nhwc_padded_kernel<bf16_t>, g, dim3(256), 0, s, x,
+                           static_cast<bf16_t*>(dst), (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp,
+                           fw, fh);
+    return hipGetLastError();
+}
+
 // ---- weight preparation ---------------------------------------------------------------------
 // One launch serves every job; job j owns blocks [block0_j, block0_{j+1}) and each block
 // converts kPrepPerBlock consecutive destination elements.  The source index of a destination
@@ -107,6 +142,10 @@ void prep_fill_divisors(PrepJob& j)
         j.f0 = make_fastdiv((unsigned)j.IN);
         j.f1 = make_fastdiv((unsigned)j.C);
         break;
+    case PREP_CONV_RUN:
+        j.f0 = make_fastdiv((unsigned)j.RUN);
+        j.f1 = make_fastdiv((unsigned)j.Cp);
+        break;
     default:
         break;
     }
@@ -131,6 +170,13 @@ __device__ __forceinline__ int prep_src(const PrepJob& j, unsigned d)
         const unsigned r2 = fdivu(j.f1, r1), ci = r1 - r2 * (unsigned)j.cg;
         const unsigned g = fdivu(j.f2, r2), uv = r2 - g * (unsigned)j.KK;
         return (((int)g * j.og + (int)co) * j.cg + (int)ci) * j.KK + (int)uv;
+    }
+    case PREP_CONV_RUN: {  // d = (co*K + u)*RUN + j, j = v*Cp + ci; -1 for padding taps
+        const unsigned r = fdivu(j.f0, d), jj = d - r * (unsigned)j.RUN;
+        const unsigned co = r / (unsigned)j.K, u = r - co * (unsigned)j.K;
+        const unsigned v = fdivu(j.f1, jj), ci = jj - v * (unsigned)j.Cp;
+        if (v >= (unsigned)j.K || ci >= (unsigned)j.C) return -1;
+        return (((int)co * j.C + (int)ci) * j.K + (int)u) * j.K + (int)v;
     }
     case PREP_FC_PERM: {  // d = o*IN + hw*C + c
         const unsigned o = fdivu(j.f0, d), r = d - o * (unsigned)j.IN;
@@ -157,7 +203,10 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepJob* __restrict__ j
 #pragma unroll
     for (int e = 0; e < kPrepPerThread; ++e) {
         const int d = base + e * 256;
-        if (d < j.n) out[d] = from_f32<T>(src[prep_src(j, (unsigned)d)]);
+        if (d < j.n) {
+            const int si = prep_src(j, (unsigned)d);
+            out[d] = from_f32<T>(si >= 0 ? src[si] : 0.f);
+        }
     }
 }
 

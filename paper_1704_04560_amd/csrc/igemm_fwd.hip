@@ -23,6 +23,25 @@ hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* wf, con
     return run_gemm<ConvFwd<bf16_t>, L_SK, L_SR>(a, p, d.Z, partial, s);
 }
 
+hipError_t conv_fwd_run(Dt dt, const ConvGeom& g, const RunGeom& r, const void* xp,
+                        const void* wr, const float* bias, void* y, bool y_f32, bool relu,
+                        float* partial, hipStream_t s)
+{
+    if (g.G != 1) return hipErrorInvalidValue;
+    GemmArgs a = conv_args(g);
+    a.Hp = r.Hp; a.Wp = r.Wp; a.Cp = r.Cp; a.RUN = r.RUN;
+    a.fd_run = make_fastdiv((unsigned)r.RUN);
+    a.a = xp; a.b = wr; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)g.N * r.Hp * r.Wp * r.Cp * es);
+    a.b_bytes = (unsigned)((size_t)g.OC * g.K * r.RUN * es);
+    const GemmDims d = conv_fwd_run_dims(dt, g, r);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    if (dt == DT_F32) return run_gemm<ConvFwdRun<float>, L_KV, L_KV>(a, p, d.Z, partial, s);
+    return run_gemm<ConvFwdRun<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s);
+}
+
 hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, const float* bias,
                   void* y, bool y_f32, bool relu, float* partial, hipStream_t s)
 {

@@ -40,6 +40,7 @@ static inline GemmArgs conv_args(const ConvGeom& g)
     a.fd_cg = make_fastdiv((unsigned)a.cg);
     a.fd_kog = make_fastdiv((unsigned)(g.K * a.og));
     a.fd_og = make_fastdiv((unsigned)a.og);
+    a.fd_run = make_fastdiv(1u);
     return a;
 }
 
@@ -356,6 +357,125 @@ template <typename T> struct ConvWgrad {
         const int u = q / kc, rem = q - u * kc, v = rem / a.cg, ci = rem - v * a.cg;
         const long long col = (long long)ci * a.KK + u * a.K + v;
         for (int i = 0; i < np; ++i) g[a.out_off + (long long)(co + i) * nq + col] = acc[i];
+    }
+};
+
+// ------------------------------------------------------------------------------------------
+// First-layer convolution over the padded input X'[n][Hp][Wp][Cp] (groups 1): k = (u, j),
+// j < RUN, and the K*Cp inputs of kernel row u of output position q are contiguous at
+// X'[n][oh*S + u][ow*S][0..], so every operand load is 16 bytes and needs no bounds test
+// (the border of X' holds the zero padding).  Taps j >= K*Cp read neighbouring inputs and meet
+// zero weights.
+// ------------------------------------------------------------------------------------------
+template <typename T> struct ConvFwdRun {
+    typedef T TT;
+    static constexpr bool P_IS_A = false;
+    static constexpr bool SHARE_Q = true;
+    static constexpr bool TAB = true, TAB_CHUNK = true;
+    // entry for the chunk starting at k: offset of (u, j) from the window origin
+    __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
+    {
+        if (k >= c.kend) return TabEnt{0, 0, 0};
+        const int u = (int)fdiv(a.fd_run, (unsigned)k), j = k - u * a.RUN;
+        return TabEnt{u * a.Wp * a.Cp + j, 0, 0};
+    }
+    // P: Wr[p * Kdim + k]
+    typedef RowOk PV;
+    __device__ static PV pv(const GemmArgs& a, const Ctx&, int p) { return PV{p * a.Kdim, p < a.Pdim}; }
+    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    {
+        return B.at16(s.ok & (k < c.kend), s.off + k);
+    }
+    // Q: window origin of output position q
+    typedef RowOk QV;
+    __device__ static QV qv(const GemmArgs& a, const Ctx&, int q)
+    {
+        const bool ok = q < a.Qdim;
+        const unsigned qq = ok ? q : 0;
+        const unsigned b = fdiv(a.fd_ohw, qq), hw = qq - b * (unsigned)(a.OH * a.OW);
+        const unsigned oh = fdiv(a.fd_ow, hw), ow = hw - oh * (unsigned)a.OW;
+        return QV{(((int)b * a.Hp + (int)oh * a.S) * a.Wp + (int)ow * a.S) * a.Cp, ok};
+    }
+    __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    {
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
+        return B.at16(s.ok, s.off + e.off);
+    }
+    __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
+    {
+        ConvFwd<T>::store4(a, c, p, q, acc, np);
+    }
+};
+
+// Weight gradient of one shard for the same layer: p = output channel, q = (u, j) plus the
+// bias row q = K*RUN, k = position in the shard.  Outputs for padding taps are discarded.
+template <typename T> struct ConvWgradRun {
+    typedef T TT;
+    static constexpr bool P_IS_A = true;
+    static constexpr bool SHARE_Q = true;
+    static constexpr bool TAB = true, TAB_CHUNK = false;
+    // entry for position k of the shard: offset of its window origin in X'
+    __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
+    {
+        if (k >= c.kend) return TabEnt{0, 0, 0};
+        const unsigned b = fdiv(a.fd_ohw, (unsigned)k), hw = (unsigned)k - b * (unsigned)(a.OH * a.OW);
+        const unsigned oh = fdiv(a.fd_ow, hw), ow = hw - oh * (unsigned)a.OW;
+        return TabEnt{(((c.b0 + (int)b) * a.Hp + (int)oh * a.S) * a.Wp + (int)ow * a.S) * a.Cp, 0, 0};
+    }
+    // P: dy^T, as for ConvWgrad
+    typedef RowOk PR;
+    __device__ static PR pr(const GemmArgs& a, const Ctx& c, int p)
+    {
+        return PR{c.b0 * a.OH * a.OW * a.OC + p, p < a.Pdim};
+    }
+    __device__ static T p_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PR& s, int k)
+    {
+        return B.at(s.ok & (k < c.kend), s.off + k * a.OC);
+    }
+    typedef RowOk PC;
+    __device__ static PC pc(const GemmArgs& a, const Ctx& c, int p0) { return pr(a, c, p0); }
+    __device__ static u32x4 p_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const PC& s, int k)
+    {
+        return B.at16(s.ok & (k < c.kend), s.off + k * a.OC);
+    }
+    // Q: X' at (u, j) of the window of position k
+    struct QR { int off; bool ok, bias; };
+    __device__ static QR qr(const GemmArgs& a, const Ctx&, int q)
+    {
+        const int nq = a.K * a.RUN;
+        const int qq = q < nq ? q : 0;
+        const int u = (int)fdiv(a.fd_run, (unsigned)qq), j = qq - u * a.RUN;
+        return QR{u * a.Wp * a.Cp + j, q < nq, q == nq};
+    }
+    __device__ static T q_sr(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QR& s, int k)
+    {
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
+        const T x = B.at(s.ok, e.off + s.off);
+        return s.bias ? (k < c.kend ? one<T>() : zero<T>()) : x;
+    }
+    typedef QR QC;
+    __device__ static QC qc(const GemmArgs& a, const Ctx& c, int q0) { return qr(a, c, q0); }
+    __device__ static u32x4 q_rv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QC& s, int k)
+    {
+        const TabEnt e = ld_tab(c.tab + (k - c.kbeg));
+        const u32x4 x = B.at16(s.ok, e.off + s.off);
+        if (s.bias) return k < c.kend ? one_chunk<T>() : u32x4{0u, 0u, 0u, 0u};
+        return x;
+    }
+    // grads[r][w_off + co * C*K*K + ci*K*K + u*K + v] for the real taps, or the bias
+    __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
+    {
+        const int nq = a.K * a.RUN;
+        float* g = static_cast<float*>(a.out) + (long long)c.r * a.out_ld;
+        if (q == nq) {
+            for (int i = 0; i < np; ++i) g[a.bias_off + p + i] = acc[i];
+            return;
+        }
+        const int u = q / a.RUN, j = q - u * a.RUN, v = j / a.Cp, ci = j - v * a.Cp;
+        if (v >= a.K || ci >= a.C) return;
+        const int nw = a.C * a.KK;
+        const long long col = (long long)ci * a.KK + u * a.K + v;
+        for (int i = 0; i < np; ++i) g[a.out_off + (long long)(p + i) * nw + col] = acc[i];
     }
 };
 

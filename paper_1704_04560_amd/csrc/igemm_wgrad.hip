@@ -32,6 +32,33 @@ hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void
     return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
 }
 
+hipError_t conv_wgrad_run(Dt dt, const ConvGeom& g, const RunGeom& r, int R, const void* xp,
+                          const void* dy, float* grads, long long ld, long long w_off,
+                          long long b_off, float* partial, hipStream_t s)
+{
+    if (g.G != 1) return hipErrorInvalidValue;
+    GemmArgs a = conv_args(g);
+    a.Hp = r.Hp; a.Wp = r.Wp; a.Cp = r.Cp; a.RUN = r.RUN;
+    a.fd_run = make_fastdiv((unsigned)r.RUN);
+    a.a = dy; a.b = xp; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
+    a.R = R;
+    const unsigned es = dt == DT_F32 ? 4 : 2;
+    a.a_bytes = (unsigned)((size_t)R * g.N * g.OC * g.OH * g.OW * es);
+    a.b_bytes = (unsigned)((size_t)R * g.N * r.Hp * r.Wp * r.Cp * es);
+    const GemmDims d = conv_wgrad_run_dims(dt, g, r, R);
+    a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
+    const GemmPlan p = plan_for(dt, d);
+    const bool pv = g.OC % vec_elems(dt) == 0;
+    if (dt == DT_F32) {
+        typedef ConvWgradRun<float> Op;
+        if (pv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+        return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    }
+    typedef ConvWgradRun<bf16_t> Op;
+    if (pv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
+    return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+}
+
 hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
                     const void* x, const void* dy, float* grads, long long ld, long long w_off,
                     long long b_off, float* partial, hipStream_t s)

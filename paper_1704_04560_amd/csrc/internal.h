@@ -62,7 +62,9 @@ struct GemmArgs {
                            // is in (h, w, c) order with perm_c channels and perm_hw positions
     unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)
     unsigned b_bytes;      // size of tensor b in bytes
+    int Hp, Wp, Cp, RUN;   // first-layer convolution over a padded input (see conv_fwd_run)
     FastDiv fd_ohw, fd_ow, fd_hw, fd_w, fd_c;
+    FastDiv fd_run;
     FastDiv fd_kcg, fd_cg, fd_kog, fd_og;  // K*cg, cg, K*og, og (index tables)
 };
 
@@ -104,6 +106,22 @@ hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* 
 hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
                       float* grads, long long ld, long long w_off, long long b_off,
                       float* partial, hipStream_t s);
+// First-layer convolution (groups 1) over the padded input X'[n][Hp][Wp][Cp]: a zero border of
+// PD around the image, Cp >= C channels (the extra ones zero), so that the K*Cp inputs of one
+// kernel row are contiguous.  The reduction runs over k = (u, j) with j < RUN (K*Cp rounded up
+// to the vector width); the prepared weights Wr[co][u][j] are zero where j does not stand for a
+// real (v, ci).  RunGeom holds the padded sizes.
+struct RunGeom {
+    int Hp, Wp, Cp, RUN;
+};
+GemmDims conv_fwd_run_dims(int dt, const ConvGeom& g, const RunGeom& r);
+GemmDims conv_wgrad_run_dims(int dt, const ConvGeom& g, const RunGeom& r, int R);
+hipError_t conv_fwd_run(Dt dt, const ConvGeom& g, const RunGeom& r, const void* xp,
+                        const void* wr, const float* bias, void* y, bool y_f32, bool relu,
+                        float* partial, hipStream_t s);
+hipError_t conv_wgrad_run(Dt dt, const ConvGeom& g, const RunGeom& r, int R, const void* xp,
+                          const void* dy, float* grads, long long ld, long long w_off,
+                          long long b_off, float* partial, hipStream_t s);
 hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, const float* bias,
                   void* y, bool y_f32, bool relu, float* partial, hipStream_t s);
 hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w, void* dx,
@@ -127,6 +145,7 @@ enum PrepKind {
     PREP_CONV_D,     // Wd
     PREP_CONV_C,     // Wc
     PREP_FC_PERM,    // W[o][(c, h, w)] -> W[o][(h, w, c)]
+    PREP_CONV_RUN,   // Wr[co][u][j] of a first-layer convolution over a padded input
 };
 struct PrepJob {
     int kind;
@@ -134,7 +153,8 @@ struct PrepJob {
     long long src;     // element offset in the fp32 weights
     long long dst;     // element offset in the prepared buffer
     int g, cg, og, KK; // convolution: groups, channels per group in / out, K*K
-    int C, HW, IN;     // fully connected permutation
+    int C, HW, IN;     // fully connected permutation; C, Cp, K, RUN of a padded first layer
+    int Cp, K, RUN;
     int block0;        // first block of this job in the launch
     FastDiv f0, f1, f2;
 };
@@ -146,6 +166,10 @@ void prep_fill_divisors(PrepJob& j);
 
 // NCHW fp32 -> NHWC compute type (C == 1 or H*W == 1: a plain copy / cast).
 hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipStream_t s);
+// NCHW fp32 -> the padded input X'[n][PD + h][PD + w][c] of conv_fwd_run (interior channels
+// c < C only; the border and the extra channels are never written and must be zero).
+hipError_t to_nhwc_padded(Dt dt, const float* x, void* dst, int N, int C, int H, int W,
+                          int PD, const RunGeom& r, hipStream_t s);
 hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
 // Max pooling over NHWC tensors; argmax holds the window position (u*K + v) per output.  The
 // pooled tensor (and argmax) is NCHW when out_nchw / dy_nchw is set.

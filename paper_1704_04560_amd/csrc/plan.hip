@@ -105,6 +105,14 @@ bool conv_dgrad_use_col(const ConvGeom& g)
     const double waste = (double)g.H * g.W / ((double)g.OH * g.OW * g.S * g.S);
     return waste >= 1.5 && conv_dgrad_col_elems(g) * 4 <= (size_t)512 << 20;
 }
+GemmDims conv_fwd_run_dims(int dt, const ConvGeom& g, const RunGeom& r)
+{
+    return GemmDims{g.OC, g.N * g.OH * g.OW, g.K * r.RUN, 1, kMaxTab * vec_elems(dt)};
+}
+GemmDims conv_wgrad_run_dims(int, const ConvGeom& g, const RunGeom& r, int R)
+{
+    return GemmDims{g.OC, g.K * r.RUN + 1, g.N * g.OH * g.OW, R, kMaxTab};
+}
 GemmDims fc_fwd_dims(int, int B, int IN, int OUT) { return GemmDims{OUT, B, IN, 1, 0}; }
 GemmDims fc_dgrad_dims(int, int B, int IN, int OUT) { return GemmDims{IN, B, OUT, 1, 0}; }
 GemmDims fc_wgrad_dims(int, int Nb, int R, int IN, int OUT) { return GemmDims{IN + 1, OUT, Nb, R, 0}; }

@@ -181,20 +181,22 @@ __device__ __forceinline__ void decode_z(const GemmArgs& a, Ctx& c, int z)
 // ---- epilogue helpers -----------------------------------------------------------------------
 
 // Store np (<= 4) consecutive values at element idx of an fp32 tensor or of a tensor of the
-// compute type; one vector store when all four are present and aligned.
+// compute type; one vector store when all four are present and the launch's rows are aligned
+// (vec: uniform over the launch).
 template <typename T>
-__device__ __forceinline__ void store_vals(void* out, bool f32, int idx, const float* v, int np)
+__device__ __forceinline__ void store_vals(void* out, bool f32, int idx, const float* v, int np,
+                                           bool vec)
 {
     if (f32 || sizeof(T) == 4) {
         float* o = static_cast<float*>(out) + idx;
-        if (np == 4 && (idx & 3) == 0) {
+        if (np == 4 && vec) {
             *reinterpret_cast<f32x4*>(o) = f32x4{v[0], v[1], v[2], v[3]};
         } else {
             for (int i = 0; i < np; ++i) o[i] = v[i];
         }
     } else {
         bf16_t* o = static_cast<bf16_t*>(out) + idx;
-        if (np == 4 && (idx & 3) == 0) {
+        if (np == 4 && vec) {
             const unsigned lo = (unsigned)f32_to_bf16(v[0]) | ((unsigned)f32_to_bf16(v[1]) << 16);
             const unsigned hi = (unsigned)f32_to_bf16(v[2]) | ((unsigned)f32_to_bf16(v[3]) << 16);
             *reinterpret_cast<u32x2*>(o) = u32x2{lo, hi};
@@ -210,11 +212,41 @@ template <typename T>
 __device__ __forceinline__ void apply_mask(const GemmArgs& a, int idx, float* v, int np)
 {
     if (!a.mask) return;
-    for (int i = 0; i < np; ++i) {
-        const float m = a.mask_f32 ? static_cast<const float*>(a.mask)[idx + i]
-                                   : to_f32<T>(static_cast<const T*>(a.mask)[idx + i]);
-        if (!(m > 0.f)) v[i] = 0.f;
+    float m[4] = {0.f, 0.f, 0.f, 0.f};
+    if (np == 4 && a.vec_out) {
+        if (a.mask_f32) {
+            const f32x4 mm = *reinterpret_cast<const f32x4*>(static_cast<const float*>(a.mask) + idx);
+            m[0] = mm[0]; m[1] = mm[1]; m[2] = mm[2]; m[3] = mm[3];
+        } else if constexpr (sizeof(T) == 2) {
+            const u32x2 w = *reinterpret_cast<const u32x2*>(static_cast<const T*>(a.mask) + idx);
+            m[0] = __uint_as_float(w[0] << 16); m[1] = __uint_as_float(w[0] & 0xffff0000u);
+            m[2] = __uint_as_float(w[1] << 16); m[3] = __uint_as_float(w[1] & 0xffff0000u);
+        } else {
+            const f32x4 mm = *reinterpret_cast<const f32x4*>(static_cast<const T*>(a.mask) + idx);
+            m[0] = mm[0]; m[1] = mm[1]; m[2] = mm[2]; m[3] = mm[3];
+        }
+    } else {
+        for (int i = 0; i < np; ++i)
+            m[i] = a.mask_f32 ? static_cast<const float*>(a.mask)[idx + i]
+                              : to_f32<T>(static_cast<const T*>(a.mask)[idx + i]);
     }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        if (!(m[i] > 0.f)) v[i] = 0.f;
+}
+
+// Bias of output rows p..p+np-1 for the operations that have one (read once per row group).
+template <class Op>
+__device__ __forceinline__ f32x4 row_bias(const GemmArgs& a, const Ctx& c, int p, int np)
+{
+    f32x4 b = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (Op::HAS_BIAS) {
+        const float* bp = a.bias + Op::bias_index(a, c, p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (i < np) b[i] = bp[i];
+    }
+    return b;
 }
 
 // ---- LDS tile addressing --------------------------------------------------------------------
@@ -485,22 +517,30 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     const bool split = a.splits > 1;
     float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
 #pragma unroll
-    for (int i = 0; i < FP; ++i)
+    for (int i = 0; i < FP; ++i) {
+        const int p = p0 + wp * 16 * FP + i * 16 + lg * 4;
+        if (p >= a.Pdim) continue;
+        const int np = min(4, a.Pdim - p);
+        if (split) {
 #pragma unroll
-        for (int j = 0; j < FQ; ++j) {
-            const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-            const int p = p0 + wp * 16 * FP + i * 16 + lg * 4;
-            if (q >= a.Qdim || p >= a.Pdim) continue;
-            const int np = min(4, a.Pdim - p);
-            if (split) {
+            for (int j = 0; j < FQ; ++j) {
+                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                if (q >= a.Qdim) continue;
                 // partial sums are stored [z][q][p]
                 float* o = part + (long long)q * a.Pdim + p;
                 if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
                 else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
-            } else {
-                Op::store4(a, c, p, q, acc[i][j], np);
+            }
+        } else {
+            const f32x4 rb = row_bias<Op>(a, c, p, np);
+#pragma unroll
+            for (int j = 0; j < FQ; ++j) {
+                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                if (q >= a.Qdim) continue;
+                Op::store4(a, c, p, q, acc[i][j] + rb, np);
             }
         }
+    }
 }
 
 // Second pass of a split reduction.  A block covers OPB = 256/SL consecutive outputs t =
@@ -536,7 +576,7 @@ __global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
 #pragma unroll
         for (int j = 1; j < SL; ++j) tot += sh[j][ol];
         const int q = (int)(t / a.Pdim), p = (int)(t - (long long)q * a.Pdim);
-        Op::store4(a, c, p, q, f32x4{tot, 0.f, 0.f, 0.f}, 1);
+        Op::store4(a, c, p, q, f32x4{tot + row_bias<Op>(a, c, p, 1)[0], 0.f, 0.f, 0.f}, 1);
     }
 }
 

@@ -73,6 +73,7 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, 
 {
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = wd; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
+    a.vec_out = g.C % 4 == 0 && a.cg % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
     a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
@@ -98,6 +99,7 @@ hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* 
 {
     GemmArgs a = conv_args(g);
     a.a = dy; a.b = wc; a.out = col;
+    a.vec_out = (a.KK * a.cg) % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)g.N * g.OC * g.OH * g.OW * es);
     a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
@@ -127,6 +129,7 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
     GemmArgs a{};
     a.a = dy; a.b = w; a.out = dx; a.mask = mask; a.mask_f32 = mask_f32;
     a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1; a.perm_c = 1; a.perm_hw = 1;
+    a.vec_out = IN % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)B * OUT * es);
     a.b_bytes = (unsigned)((size_t)OUT * IN * es);

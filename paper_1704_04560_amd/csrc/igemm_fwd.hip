@@ -8,6 +8,7 @@ hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* wf, con
 {
     GemmArgs a = conv_args(g);
     a.a = x; a.b = wf; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
+    a.vec_out = g.OC % 4 == 0 && a.og % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)g.N * g.C * g.H * g.W * es);
     a.b_bytes = (unsigned)((size_t)g.OC * a.cg * a.KK * es);
@@ -32,6 +33,7 @@ hipError_t conv_fwd_run(Dt dt, const ConvGeom& g, const RunGeom& r, const void* 
     a.Hp = r.Hp; a.Wp = r.Wp; a.Cp = r.Cp; a.RUN = r.RUN;
     a.fd_run = make_fastdiv((unsigned)r.RUN);
     a.a = xp; a.b = wr; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
+    a.vec_out = g.OC % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)g.N * r.Hp * r.Wp * r.Cp * es);
     a.b_bytes = (unsigned)((size_t)g.OC * g.K * r.RUN * es);
@@ -48,6 +50,7 @@ hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, c
     GemmArgs a{};
     a.a = x; a.b = w; a.out = y; a.bias = bias; a.relu = relu; a.out_f32 = y_f32 || dt == DT_F32;
     a.N = B; a.C = IN; a.OC = OUT; a.G = 1; a.R = 1; a.perm_c = 1; a.perm_hw = 1;
+    a.vec_out = OUT % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)B * IN * es);
     a.b_bytes = (unsigned)((size_t)OUT * IN * es);

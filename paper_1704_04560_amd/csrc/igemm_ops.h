@@ -109,17 +109,16 @@ template <typename T> struct ConvFwd {
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
         return B.at16(inside(hi, wi, a.H, a.W), s.base + e.off);
     }
-    // y[q][g*og + p] = acc + bias, ReLU
+    static constexpr bool HAS_BIAS = true;
+    __device__ static int bias_index(const GemmArgs& a, const Ctx& c, int p) { return c.grp * a.og + p; }
+    // y[q][g*og + p] = acc (bias included), ReLU
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
     {
         const int co = c.grp * a.og + p;
         float v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            v[i] = acc[i] + (i < np ? a.bias[co + i] : 0.f);
-            if (a.relu) v[i] = v[i] > 0.f ? v[i] : 0.f;
-        }
-        store_vals<T>(a.out, a.out_f32, q * a.OC + co, v, np);
+        for (int i = 0; i < 4; ++i) v[i] = a.relu ? fmaxf(acc[i], 0.f) : acc[i];
+        store_vals<T>(a.out, a.out_f32, q * a.OC + co, v, np, a.vec_out);
     }
 };
 
@@ -134,6 +133,7 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
     static constexpr bool SHARE_Q = true;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = STRIDE1, TAB_CHUNK = true;
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
     {
@@ -209,7 +209,7 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
         const int idx = q * a.C + c.grp * a.cg + p;
         float v[4] = {acc[0], acc[1], acc[2], acc[3]};
         apply_mask<T>(a, idx, v, np);
-        store_vals<T>(a.out, false, idx, v, np);
+        store_vals<T>(a.out, false, idx, v, np, a.vec_out);
     }
 };
 
@@ -223,6 +223,7 @@ template <typename T> struct ConvDgradCol {
     typedef T TT;
     static constexpr bool P_IS_A = false;
     static constexpr bool SHARE_Q = true;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     // P: Wc[(g*KK*cg + p) * og + k]
     struct PK { int base; bool ok; };
@@ -266,7 +267,7 @@ template <typename T> struct ConvDgradCol {
     {
         const long long idx = ((long long)c.grp * a.Qdim + q) * a.Pdim + p;
         float* o = static_cast<float*>(a.out) + idx;
-        if (np == 4 && (idx & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc;
+        if (np == 4 && a.vec_out) *reinterpret_cast<f32x4*>(o) = acc;
         else for (int i = 0; i < np; ++i) o[i] = acc[i];
     }
 };
@@ -282,6 +283,7 @@ template <typename T> struct ConvWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = true;
     static constexpr bool SHARE_Q = true;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = true, TAB_CHUNK = false;
     // entry for position k of the shard: the offset of x[b0 + n][oh*S - PD][ow*S - PD][0] and
     // the window origin (oh*S - PD, ow*S - PD)
@@ -401,6 +403,8 @@ template <typename T> struct ConvFwdRun {
         const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         return B.at16(s.ok, s.off + e.off);
     }
+    static constexpr bool HAS_BIAS = true;
+    __device__ static int bias_index(const GemmArgs&, const Ctx&, int p) { return p; }
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
     {
         ConvFwd<T>::store4(a, c, p, q, acc, np);
@@ -413,6 +417,7 @@ template <typename T> struct ConvWgradRun {
     typedef T TT;
     static constexpr bool P_IS_A = true;
     static constexpr bool SHARE_Q = true;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = true, TAB_CHUNK = false;
     // entry for position k of the shard: offset of its window origin in X'
     __device__ static TabEnt tab_entry(const GemmArgs& a, const Ctx& c, int k)
@@ -514,16 +519,15 @@ template <typename T> struct FcFwd {
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
-    // y[q][p] = acc + bias[p], ReLU
+    static constexpr bool HAS_BIAS = true;
+    __device__ static int bias_index(const GemmArgs&, const Ctx&, int p) { return p; }
+    // y[q][p] = acc (bias included), ReLU
     __device__ static void store4(const GemmArgs& a, const Ctx&, int p, int q, f32x4 acc, int np)
     {
         float v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            v[i] = acc[i] + (i < np ? a.bias[p + i] : 0.f);
-            if (a.relu) v[i] = v[i] > 0.f ? v[i] : 0.f;
-        }
-        store_vals<T>(a.out, a.out_f32, q * a.Pdim + p, v, np);
+        for (int i = 0; i < 4; ++i) v[i] = a.relu ? fmaxf(acc[i], 0.f) : acc[i];
+        store_vals<T>(a.out, a.out_f32, q * a.Pdim + p, v, np, a.vec_out);
     }
 };
 
@@ -533,6 +537,7 @@ template <typename T> struct FcDgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
     static constexpr bool SHARE_Q = false;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     typedef RowOk PR;
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p) { return PR{p, p < a.Pdim}; }
@@ -564,7 +569,7 @@ template <typename T> struct FcDgrad {
         const int idx = q * a.Pdim + p;
         float v[4] = {acc[0], acc[1], acc[2], acc[3]};
         apply_mask<T>(a, idx, v, np);
-        store_vals<T>(a.out, false, idx, v, np);
+        store_vals<T>(a.out, false, idx, v, np, a.vec_out);
     }
 };
 
@@ -577,6 +582,7 @@ template <typename T> struct FcWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
     static constexpr bool SHARE_Q = false;
+    static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     struct PR { int i; bool ok, bias; };
     __device__ static PR pr(const GemmArgs& a, const Ctx&, int p)
@@ -621,7 +627,7 @@ template <typename T> struct FcWgrad {
     {
         float* g = static_cast<float*>(a.out) + (long long)c.r * a.out_ld;
         const long long row = a.out_off + (long long)q * a.C;
-        if (p + 3 < a.C && ((row + p + (long long)c.r * a.out_ld) & 3) == 0) {
+        if (p + 3 < a.C && a.vec_out) {
             *reinterpret_cast<f32x4*>(g + row + p) = acc;
             return;
         }

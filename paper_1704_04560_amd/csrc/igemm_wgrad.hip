@@ -66,6 +66,7 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
     GemmArgs a{};
     a.a = dy; a.b = x; a.out = grads; a.out_ld = ld; a.out_off = w_off; a.bias_off = b_off;
     a.N = Nb; a.C = IN; a.OC = OUT; a.G = 1; a.R = R; a.perm_c = perm_c; a.perm_hw = perm_hw;
+    a.vec_out = IN % 4 == 0 && w_off % 4 == 0 && ld % 4 == 0;
     const unsigned es = dt == DT_F32 ? 4 : 2;
     a.a_bytes = (unsigned)((size_t)R * Nb * OUT * es);
     a.b_bytes = (unsigned)((size_t)R * Nb * IN * es);

@@ -58,6 +58,7 @@ struct GemmArgs {
     int relu;              // forward: apply ReLU
     int out_f32;           // forward: output stored as fp32 (otherwise the compute type)
     int mask_f32;          // data gradient: mask tensor is fp32 (otherwise the compute type)
+    int vec_out;           // epilogue rows of 4 outputs (and of the mask) are 16-byte aligned
     int perm_c, perm_hw;   // fully connected weight gradient after a spatial layer: its input
                            // is in (h, w, c) order with perm_c channels and perm_hw positions
     unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)

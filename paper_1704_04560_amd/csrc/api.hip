@@ -816,7 +816,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
                         return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
                                         reinterpret_cast<const uint8_t*>(ws + lp.am_off), dy, dx,
-                                        mask, mask_f32, s);
+                                        mask ? ws + lp.act_off : nullptr, s);
                     }), "pool backward");
         }
     }

@@ -2,6 +2,8 @@
 // preparation, max-pooling, the fused softmax cross-entropy and the fused gradient average +
 // momentum update.  All reductions run in a fixed order, so results
 // are identical from run to run.
+#include <algorithm>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -78,7 +80,9 @@ hipError_t to_nhwc(Dt dt, const float* x, void* dst, int N, int C, int HW, hipSt
 }
 
 // X'[n][PD + h][PD + w][c] = x[n][c][h][w] for c < C: one thread per pixel, channels in a loop.
-template <typename T>
+// CP > 0 (= Cp, 8 or 16 bytes of channels): the pixel's channels, zeros included, go out as one
+// vector store, so every byte of the written lines is written.
+template <typename T, int CP>
 __global__ __launch_bounds__(256) void to_nhwc_padded_kernel(const float* __restrict__ x,
                                                              T* __restrict__ dst, int pixels,
                                                              int C, int H, int W, int PD,
@@ -91,7 +95,16 @@ __global__ __launch_bounds__(256) void to_nhwc_padded_kernel(const float* __rest
     const unsigned n = fdivu(fh, r), h = r - n * (unsigned)H;
     const float* src = x + ((long long)n * C * H + h) * W + w;
     T* out = dst + (((long long)n * Hp + PD + h) * Wp + PD + w) * Cp;
-    for (int c = 0; c < C; ++c) out[c] = from_f32<T>(src[(long long)c * H * W]);
+    if constexpr (CP > 0) {
+        static_assert(CP * sizeof(T) == 8 || CP * sizeof(T) == 16, "vector width");
+        T v[CP];
+#pragma unroll
+        for (int c = 0; c < CP; ++c) v[c] = from_f32<T>(c < C ? src[(long long)c * H * W] : 0.f);
+        if constexpr (CP * sizeof(T) == 16) *reinterpret_cast<uint4*>(out) = *reinterpret_cast<const uint4*>(v);
+        else *reinterpret_cast<uint2*>(out) = *reinterpret_cast<const uint2*>(v);
+    } else {
+        for (int c = 0; c < C; ++c) out[c] = from_f32<T>(src[(long long)c * H * W]);
+    }
 }
 
 hipError_t to_nhwc_padded(Dt dt, const float* x, void* dst, int N, int C, int H, int W,
@@ -101,14 +114,29 @@ hipError_t to_nhwc_padded(Dt dt, const float* x, void* dst, int N, int C, int H,
     if (pixels <= 0 || C <= 0) return hipSuccess;
     const FastDiv fw = make_fastdiv((unsigned)W), fh = make_fastdiv((unsigned)H);
     dim3 g(grid_for((size_t)pixels, 256));
-    if (dt == DT_F32)
-        hipLaunchKernelGGL(to_nhwc_padded_kernel<float>, g, dim3(256), 0, s, x,
-                           static_cast<float*>(dst), (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp,
-                           fw, fh);
-    else
-        hipLaunchKernelGGL(to_nhwc_padded_kernel<bf16_t>, g, dim3(256), 0, s, x,
-                           static_cast<bf16_t*>(dst), (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp,
-                           fw, fh);
+    if (dt == DT_F32) {
+        float* o = static_cast<float*>(dst);
+        if (r.Cp == 2)
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<float, 2>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+        else if (r.Cp == 4)
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<float, 4>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+        else
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<float, 0>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+    } else {
+        bf16_t* o = static_cast<bf16_t*>(dst);
+        if (r.Cp == 4)
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<bf16_t, 4>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+        else if (r.Cp == 8)
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<bf16_t, 8>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+        else
+            hipLaunchKernelGGL((to_nhwc_padded_kernel<bf16_t, 0>), g, dim3(256), 0, s, x, o,
+                               (int)pixels, C, H, W, PD, r.Hp, r.Wp, r.Cp, fw, fh);
+    }
     return hipGetLastError();
 }
 
@@ -197,9 +225,29 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepJob* __restrict__ j
     for (int k = 1; k < njobs; ++k)
         if (jobs[k].block0 <= (int)blockIdx.x) jx = k;
     const PrepJob j = jobs[jx];
-    const int base = ((int)blockIdx.x - j.block0) * kPrepPerBlock + threadIdx.x;
     const float* src = w + j.src;
-    T* out = dst + j.dst;
+    T* out = dst + j.dst;  // 16-byte aligned
+    if (j.kind == PREP_CAST && ((uintptr_t)src & 15) == 0) {
+        // plain conversion: 8 consecutive elements per thread and step, 16-byte accesses
+        const int b0 = ((int)blockIdx.x - j.block0) * kPrepPerBlock;
+#pragma unroll
+        for (int e = 0; e < kPrepPerThread / 8; ++e) {
+            const int d = b0 + (e * 256 + (int)threadIdx.x) * 8;
+            if (d + 8 <= j.n) {
+                const float4 lo = *reinterpret_cast<const float4*>(src + d);
+                const float4 hi = *reinterpret_cast<const float4*>(src + d + 4);
+                T v[8] = {from_f32<T>(lo.x), from_f32<T>(lo.y), from_f32<T>(lo.z), from_f32<T>(lo.w),
+                          from_f32<T>(hi.x), from_f32<T>(hi.y), from_f32<T>(hi.z), from_f32<T>(hi.w)};
+                uint4* o = reinterpret_cast<uint4*>(out + d);
+                o[0] = reinterpret_cast<const uint4*>(v)[0];
+                if constexpr (sizeof(T) == 4) o[1] = reinterpret_cast<const uint4*>(v)[1];
+            } else {
+                for (int i = d; i < j.n; ++i) out[i] = from_f32<T>(src[i]);
+            }
+        }
+        return;
+    }
+    const int base = ((int)blockIdx.x - j.block0) * kPrepPerBlock + threadIdx.x;
 #pragma unroll
     for (int e = 0; e < kPrepPerThread; ++e) {
         const int d = base + e * 256;
@@ -342,21 +390,30 @@ hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, bool out_nc
     return hipGetLastError();
 }
 
-// One thread per CV channels of one input element: the sum, in ascending window order, of the
-// output gradients of the windows whose maximum sits here (windows overlap when S < K), times
-// the ReLU mask of the layer that produced the pooled tensor.  Gathering keeps the result free
-// of atomics.  dy and argmax are NCHW when dy_nchw is set.
-template <typename T, int KT, int ST, int CV>
-__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, int W, int Kr,
-                                                       int Sr, int OH, int OW, int dy_nchw,
-                                                       FastDiv fcv, FastDiv fw, FastDiv fh,
+// The ReLU mask of the layer that produced a pooled tensor, as seen by the pooling backward:
+// a window's output gradient goes to the position of its maximum, and the value there is the
+// window's pooled output, so a window whose pooled output is not positive contributes nothing.
+// The gate is that pooled output (same index as the output gradient), or null without ReLU.
+template <typename T>
+__device__ __forceinline__ bool gate_open(const T* gate, long long o)
+{
+    return !gate || to_f32<T>(gate[o]) > 0.f;
+}
+
+// Input gradient of a pooling, general window and stride, NHWC (the output gradient NCHW when
+// dy_nchw is set): one thread per CV channels of one input element, the sum in ascending window
+// order of the output gradients of the windows whose maximum sits there (windows overlap when
+// S < K); gathering keeps it free of atomics.
+template <typename T, int CV>
+__global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, int W, int K,
+                                                       int S, int OH, int OW, int dy_nchw,
+                                                       FastDiv fcv,
+                                                       FastDiv fw, FastDiv fh,
                                                        const uint8_t* __restrict__ argmax,
                                                        const T* __restrict__ dy,
-                                                       T* __restrict__ dx,
-                                                       const void* __restrict__ mask,
-                                                       int mask_f32)
+                                                       const T* __restrict__ gate,
+                                                       T* __restrict__ dx)
 {
-    const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
     const int t = blockIdx.x * 256 + threadIdx.x;  // over N*H*W*(C/CV)
     if (t >= total) return;
     const unsigned CG = (unsigned)(C / CV);
@@ -367,7 +424,7 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, 
     float acc[CV];
 #pragma unroll
     for (int e = 0; e < CV; ++e) acc[e] = 0.f;
-    // windows i with i*S <= h <= i*S + K - 1 (one at most when the windows do not overlap)
+    // windows i with i*S <= h <= i*S + K - 1
     const int ilo = h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S;
     const int ihi = min(h / S, OH - 1);
     const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
@@ -375,73 +432,218 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(int total, int C, int H, 
     for (int i = ilo; i <= ihi; ++i)
         for (int j = jlo; j <= jhi; ++j) {
             const uint8_t here = (uint8_t)((h - i * S) * K + (w - j * S));
-            if (dy_nchw) {
 #pragma unroll
-                for (int e = 0; e < CV; ++e) {
-                    const int o = (((int)n * C + (int)c0 + e) * OH + i) * OW + j;
-                    if (argmax[o] == here) acc[e] += to_f32<T>(dy[o]);
-                }
-            } else {
-                const int o = (((int)n * OH + i) * OW + j) * C + (int)c0;
-                const Chans<T, CV> g = load_chans<T, CV>(dy + o);
-                uint8_t am[CV];
-                if constexpr (CV == 8) *reinterpret_cast<uint2*>(am) = *reinterpret_cast<const uint2*>(argmax + o);
-                else if constexpr (CV == 4) *reinterpret_cast<unsigned*>(am) = *reinterpret_cast<const unsigned*>(argmax + o);
-                else am[0] = argmax[o];
-#pragma unroll
-                for (int e = 0; e < CV; ++e)
-                    if (am[e] == here) acc[e] += to_f32<T>(g.v[e]);
+            for (int e = 0; e < CV; ++e) {
+                const int o = dy_nchw ? (((int)n * C + (int)c0 + e) * OH + i) * OW + j
+                                      : (((int)n * OH + i) * OW + j) * C + (int)c0 + e;
+                if (argmax[o] == here && gate_open(gate, o)) acc[e] += to_f32<T>(dy[o]);
             }
         }
-    const int xo = (int)pos * C + (int)c0;
-    if (mask) {
-#pragma unroll
-        for (int e = 0; e < CV; ++e) {
-            const float m = mask_f32 ? static_cast<const float*>(mask)[xo + e]
-                                     : to_f32<T>(static_cast<const T*>(mask)[xo + e]);
-            if (!(m > 0.f)) acc[e] = 0.f;
-        }
-    }
     Chans<T, CV> out;
 #pragma unroll
     for (int e = 0; e < CV; ++e) out.v[e] = from_f32<T>(acc[e]);
-    store_chans<T, CV>(dx + xo, out);
+    store_chans<T, CV>(dx + (int)pos * C + (int)c0, out);
+}
+
+// The same for stride 2 and a 2 x 2 or 3 x 3 window, NHWC: one thread per CV channels of a
+// 2 x 2 block of input positions.  The windows touching the block (one for K = 2, up to four
+// for K = 3) are read once and each routes its output gradient to the block position that holds
+// its maximum; every position adds its windows in ascending (i, j) order, as above.
+template <typename T, int K, int CV>
+__global__ __launch_bounds__(256) void pool_bwd_s2_kernel(int total, int C, int H, int W, int OH,
+                                                          int OW, int BH, int BW, FastDiv fcv,
+                                                          FastDiv fbw, FastDiv fbh,
+                                                          const uint8_t* __restrict__ argmax,
+                                                          const T* __restrict__ dy,
+                                                          const T* __restrict__ gate,
+                                                          T* __restrict__ dx)
+{
+    static_assert(K == 2 || K == 3, "window");
+    const int t = blockIdx.x * 256 + threadIdx.x;  // over N*BH*BW*(C/CV)
+    if (t >= total) return;
+    const unsigned CG = (unsigned)(C / CV);
+    const unsigned pos = fdivu(fcv, (unsigned)t), c0 = ((unsigned)t - pos * CG) * CV;
+    const unsigned r = fdivu(fbw, pos), bw = pos - r * (unsigned)BW;
+    const unsigned n = fdivu(fbh, r), bh = r - n * (unsigned)BH;
+    float acc[2][2][CV];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int e = 0; e < CV; ++e) acc[a][b][e] = 0.f;
+#pragma unroll
+    for (int di = 0; di < K - 1; ++di) {
+        const int i = (int)bh - (K - 2) + di;  // window row; block row 2*bh sits at u = 2*(bh-i)
+        if (i < 0 || i >= OH) continue;
+#pragma unroll
+        for (int dj = 0; dj < K - 1; ++dj) {
+            const int j = (int)bw - (K - 2) + dj;
+            if (j < 0 || j >= OW) continue;
+            const int o = (((int)n * OH + i) * OW + j) * C + (int)c0;
+            const Chans<T, CV> g = load_chans<T, CV>(dy + o);
+            uint8_t am[CV];
+            if constexpr (CV == 8) *reinterpret_cast<uint2*>(am) = *reinterpret_cast<const uint2*>(argmax + o);
+            else if constexpr (CV == 4) *reinterpret_cast<unsigned*>(am) = *reinterpret_cast<const unsigned*>(argmax + o);
+            else am[0] = argmax[o];
+            float gv[CV];
+#pragma unroll
+            for (int e = 0; e < CV; ++e) gv[e] = to_f32<T>(g.v[e]);
+            if (gate) {
+                const Chans<T, CV> y = load_chans<T, CV>(gate + o);
+#pragma unroll
+                for (int e = 0; e < CV; ++e)
+                    if (!(to_f32<T>(y.v[e]) > 0.f)) gv[e] = 0.f;
+            }
+#pragma unroll
+            for (int dh = 0; dh < 2; ++dh) {
+                const int u = dh + 2 * (K - 2) - 2 * di;
+                if (u < 0 || u >= K) continue;
+#pragma unroll
+                for (int dw = 0; dw < 2; ++dw) {
+                    const int v = dw + 2 * (K - 2) - 2 * dj;
+                    if (v < 0 || v >= K) continue;
+#pragma unroll
+                    for (int e = 0; e < CV; ++e)
+                        if (am[e] == u * K + v) acc[dh][dw][e] += gv[e];
+                }
+            }
+        }
+    }
+    const int h0 = 2 * (int)bh, w0 = 2 * (int)bw;
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+        for (int dw = 0; dw < 2; ++dw) {
+            if (h0 + dh >= H || w0 + dw >= W) continue;
+            Chans<T, CV> out;
+#pragma unroll
+            for (int e = 0; e < CV; ++e) out.v[e] = from_f32<T>(acc[dh][dw][e]);
+            store_chans<T, CV>(dx + (((int)n * H + h0 + dh) * W + w0 + dw) * C + (int)c0, out);
+        }
+}
+
+// Pooling backward whose output gradient is NCHW (the pooled tensor feeds a fully connected
+// layer) and whose input gradient is NHWC.  A block takes one sample, cb channels and a band of
+// input rows: it reads the output gradients (gated) and window maxima of the windows over that
+// band, contiguous per channel, into LDS (channel rows padded to an odd length), then one thread
+// per (position, channel), channels fastest, gathers in ascending window order and writes NHWC.
+constexpr int kPoolCB = 64;            // channels per block at most
+constexpr size_t kPoolLds = 64 << 10;  // LDS bytes per block at most
+template <typename T, int KT, int ST>
+__global__ __launch_bounds__(256) void pool_bwd_nchw_kernel(int C, int H, int W, int Kr, int Sr,
+                                                            int OH, int OW, int cb, int pst,
+                                                            int rows, FastDiv fcb, FastDiv fw,
+                                                            const uint8_t* __restrict__ argmax,
+                                                            const T* __restrict__ dy,
+                                                            const T* __restrict__ gate,
+                                                            T* __restrict__ dx)
+{
+    const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
+    extern __shared__ float sg[];  // [cb][pst] gradients, then [cb][pst] maxima
+    uint8_t* sa = reinterpret_cast<uint8_t*>(sg + cb * pst);
+    const int n = blockIdx.y, cb0 = blockIdx.x * cb;
+    const int h0 = blockIdx.z * rows, h1 = min(H, h0 + rows);
+    if (h0 >= H) return;
+    // windows over rows [h0, h1): i in [ilo, ihi]
+    const int ilo = h0 - K + 1 <= 0 ? 0 : (h0 - K + 1 + S - 1) / S;
+    const int ihi = min((h1 - 1) / S, OH - 1);
+    const int nwin = (ihi - ilo + 1) * OW;
+    const long long base = ((long long)n * C + cb0) * OH * OW + (long long)ilo * OW;
+    for (int e = threadIdx.x; e < cb * nwin; e += 256) {
+        const int cl = e / nwin, ij = e - cl * nwin;
+        const long long g = base + (long long)cl * OH * OW + ij;
+        sg[cl * pst + ij] = gate_open(gate, g) ? to_f32<T>(dy[g]) : 0.f;
+        sa[cl * pst + ij] = argmax[g];
+    }
+    __syncthreads();
+    const int cnt = (h1 - h0) * W * cb;
+    for (int e = threadIdx.x; e < cnt; e += 256) {
+        const unsigned hw = fdivu(fcb, (unsigned)e), cl = (unsigned)e - hw * (unsigned)cb;
+        const unsigned hr = fdivu(fw, hw);
+        const int h = h0 + (int)hr, w = (int)(hw - hr * (unsigned)W);
+        const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
+        const int jhi = min(w / S, OW - 1);
+        const int il = max(ilo, h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S);
+        const int ih = min(h / S, OH - 1);
+        float acc = 0.f;
+        for (int i = il; i <= ih; ++i)
+            for (int j = jlo; j <= jhi; ++j) {
+                const int idx = (int)cl * pst + (i - ilo) * OW + j;
+                if (sa[idx] == (uint8_t)((h - i * S) * K + (w - j * S))) acc += sg[idx];
+            }
+        dx[(((long long)n * H + h) * W + w) * C + cb0 + (int)cl] = from_f32<T>(acc);
+    }
 }
 
 template <typename T, int CV>
 static void pool_bwd_launch(int N, int C, int H, int W, int K, int S, bool dy_nchw,
-                            const uint8_t* argmax, const void* dy, void* dx, const void* mask,
-                            bool mask_f32, hipStream_t s)
+                            const uint8_t* argmax, const void* dy, void* dx, const void* gate,
+                            hipStream_t s)
 {
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
-    const int total = N * H * W * (C / CV);
-    const FastDiv fcv = make_fastdiv((unsigned)(C / CV)), fw = make_fastdiv((unsigned)W),
-                  fh = make_fastdiv((unsigned)H);
-    dim3 g(grid_for(total, 256)), b(256);
     const T* d = static_cast<const T*>(dy);
+    const T* gt = static_cast<const T*>(gate);
     T* o = static_cast<T*>(dx);
-    if (K == 2 && S == 2)
-        hipLaunchKernelGGL((pool_bwd_kernel<T, 2, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
-                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
-    else if (K == 3 && S == 2)
-        hipLaunchKernelGGL((pool_bwd_kernel<T, 3, 2, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
-                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
-    else
-        hipLaunchKernelGGL((pool_bwd_kernel<T, 0, 0, CV>), g, b, 0, s, total, C, H, W, K, S, OH,
-                           OW, (int)dy_nchw, fcv, fw, fh, argmax, d, o, mask, (int)mask_f32);
+    dim3 b(256);
+    if (dy_nchw) {
+        // channels per block: the largest divisor of C within the limits; row bands so that
+        // the launch has at least about 2048 blocks
+        const int pst = (OH * OW) | 1;
+        const int cmax = (int)std::min<size_t>(kPoolCB, kPoolLds / ((size_t)pst * (sizeof(float) + 1)));
+        int cb = 0;
+        for (int c = std::min(cmax, C); c >= 1 && !cb; --c)
+            if (C % c == 0) cb = c;
+        if (cb > 0) {
+            const long long pairs = (long long)N * (C / cb);
+            const int bands = (int)std::max(1ll, std::min<long long>(H, (2048 + pairs - 1) / pairs));
+            const int rows = (H + bands - 1) / bands;
+            const size_t shm = (size_t)cb * pst * (sizeof(float) + 1);
+            dim3 g((unsigned)(C / cb), (unsigned)N, (unsigned)((H + rows - 1) / rows));
+            const FastDiv fcb = make_fastdiv((unsigned)cb), fw = make_fastdiv((unsigned)W);
+            if (K == 2 && S == 2)
+                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 2, 2>), g, b, shm, s, C, H, W, K, S,
+                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+            else if (K == 3 && S == 2)
+                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 3, 2>), g, b, shm, s, C, H, W, K, S,
+                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+            else
+                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 0, 0>), g, b, shm, s, C, H, W, K, S,
+                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+            return;
+        }
+    }
+    const FastDiv fcv = make_fastdiv((unsigned)(C / CV));
+    if (!dy_nchw && S == 2 && (K == 2 || K == 3)) {
+        const int BH = (H + 1) / 2, BW = (W + 1) / 2;
+        const int total = N * BH * BW * (C / CV);
+        const FastDiv fbw = make_fastdiv((unsigned)BW), fbh = make_fastdiv((unsigned)BH);
+        dim3 g(grid_for(total, 256));
+        if (K == 2)
+            hipLaunchKernelGGL((pool_bwd_s2_kernel<T, 2, CV>), g, b, 0, s, total, C, H, W, OH,
+                               OW, BH, BW, fcv, fbw, fbh, argmax, d, gt, o);
+        else
+            hipLaunchKernelGGL((pool_bwd_s2_kernel<T, 3, CV>), g, b, 0, s, total, C, H, W, OH,
+                               OW, BH, BW, fcv, fbw, fbh, argmax, d, gt, o);
+        return;
+    }
+    const int total = N * H * W * (C / CV);
+    const FastDiv fw = make_fastdiv((unsigned)W), fh = make_fastdiv((unsigned)H);
+    hipLaunchKernelGGL((pool_bwd_kernel<T, CV>), dim3(grid_for(total, 256)), b, 0, s, total, C,
+                       H, W, K, S, OH, OW, (int)dy_nchw, fcv, fw, fh, argmax, d, gt, o);
 }
 
 hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, bool dy_nchw,
-                    const uint8_t* argmax, const void* dy, void* dx, const void* mask,
-                    bool mask_f32, hipStream_t s)
+                    const uint8_t* argmax, const void* dy, void* dx, const void* gate,
+                    hipStream_t s)
 {
     if ((long long)N * C * H * W <= 0) return hipSuccess;
     if (dt == DT_F32) {
-        if (C % 4 == 0) pool_bwd_launch<float, 4>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
-        else pool_bwd_launch<float, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
+        if (C % 4 == 0) pool_bwd_launch<float, 4>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, gate, s);
+        else pool_bwd_launch<float, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, gate, s);
     } else {
-        if (C % 8 == 0) pool_bwd_launch<bf16_t, 8>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
-        else pool_bwd_launch<bf16_t, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, mask, mask_f32, s);
+        if (C % 8 == 0) pool_bwd_launch<bf16_t, 8>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, gate, s);
+        else pool_bwd_launch<bf16_t, 1>(N, C, H, W, K, S, dy_nchw, argmax, dy, dx, gate, s);
     }
     return hipGetLastError();
 }

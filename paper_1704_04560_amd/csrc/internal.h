@@ -176,9 +176,12 @@ hipError_t cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
 // pooled tensor (and argmax) is NCHW when out_nchw / dy_nchw is set.
 hipError_t pool_fwd(Dt dt, int N, int C, int H, int W, int K, int S, bool out_nchw,
                     const void* x, void* y, uint8_t* argmax, hipStream_t s);
+// Max-pool backward.  gate: the pooled output (same layout as dy) when the pooled tensor is a
+// ReLU output, else null; a window whose pooled output is not positive passes no gradient, which
+// applies the ReLU mask of the layer below.
 hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, bool dy_nchw,
-                    const uint8_t* argmax, const void* dy, void* dx, const void* mask,
-                    bool mask_f32, hipStream_t s);
+                    const uint8_t* argmax, const void* dy, void* dx, const void* gate,
+                    hipStream_t s);
 // Softmax cross-entropy of B rows; with loss_out set, also the batch-mean loss (block_sums holds
 // ceil(B/4) floats; *sync must be 0 before the first launch and is 0 again after every launch).
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,

@@ -93,6 +93,19 @@ def test_unpadded_grouped_strided_convolutions(dtype):
     run_case(f"tiny2-{dtype}", _tiny_unpadded(dtype), 2, 3, 2, 6, 0.05, 0.9)
 
 
+def _tiny_pools(dtype):
+    """Pooling windows other than 2/2 and 3/2 (overlapping and not, with and without a ReLU
+    below), and a 3/2 window feeding a fully connected layer."""
+    layers = (wl.conv(4, 3, pad=1, relu=True), wl.maxpool(2, 1), wl.conv(6, 3), wl.maxpool(3, 3),
+              wl.conv(8, 1, relu=True), wl.maxpool(3, 2), wl.fc(3))
+    return wl.Net("tiny3", (3, 17, 15), layers, dtype, "normal")
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_pool_windows_and_strides(dtype):
+    run_case(f"tiny3-{dtype}", _tiny_pools(dtype), 2, 3, 2, 10, 0.05, 0.9)
+
+
 def test_cifar_shapes_reduced_batch():
     run_case("cifar-B16", wl.CIFAR, 8, 2, 2, 6, 0.01, 0.9)
 

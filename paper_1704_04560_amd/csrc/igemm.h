@@ -261,13 +261,63 @@ template <int BK, int VEC> struct Lds {
 };
 
 // ---- operand loaders --------------------------------------------------------------------------
-enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3 };
+enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3, L_KD = 4 };
+
+// ---- direct loads (KD): 16 bytes along k from global memory straight into LDS -----------------
+// buffer_load_dwordx4 with the LDS flag: lane l of a wave writes LDS bytes [16 l, 16 l + 16) after
+// the wave-uniform base in M0, so one load fills 1 KB of the tile.  The tile rows are unpadded
+// (BK elements); granule g of row r sits at slot g ^ swz(r), swz(r) = (r / RW) mod NG with RW
+// rows per 256 bytes, which lets the 16 rows x 4 granules of a fragment read cover distinct
+// banks (measured on gfx950: 4.6 clocks per ds_read_b128 per compute unit, as for the padded
+// layout, against 16.6 without the swizzle).  The lane that fills slot s of row r loads granule
+// s ^ swz(r).  Loads past the tensor return zeros, as for the register loads.
+template <int BK, int VEC> struct LdsD {
+    static constexpr int NG = BK / VEC;
+    static constexpr int RW = 16 / NG > 0 ? 16 / NG : 1;
+    static constexpr int SIZE_ROWS = BK;  // elements per row
+    __device__ __forceinline__ static int swz(int row) { return (row / RW) & (NG - 1); }
+    __device__ __forceinline__ static int at(int row, int k)
+    {
+        return row * BK + (((k / VEC) ^ swz(row)) * VEC) + (k & (VEC - 1));
+    }
+};
+
+template <typename T> struct BufD {
+    __amdgpu_buffer_rsrc_t r;
+    mutable T* lds;  // wave-uniform LDS destination of the next load
+    __device__ __forceinline__ BufD(const void* p, unsigned bytes)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                              (int)kRsrcWord3)),
+          lds(nullptr)
+    {
+    }
+    __device__ __forceinline__ u32x4 at16(bool ok, int idx) const
+    {
+        const int off = ok ? idx * (int)sizeof(T) : (int)kOOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+        return u32x4{0u, 0u, 0u, 0u};
+    }
+};
+
+// LDS tile of one operand: the padded layout for register-staged loaders, the swizzled one for
+// direct loads; ELEMS per stage.
+template <int KIND, int BR, int BK, int VEC> struct TileOf {
+    typedef Lds<BK, VEC> L;
+    static constexpr int ELEMS = BR * L::LDK;
+};
+template <int BR, int BK, int VEC> struct TileOf<L_KD, BR, BK, VEC> {
+    typedef LdsD<BK, VEC> L;
+    static constexpr int ELEMS = BR * BK;
+};
 
 // Per-thread loader state: the operation's type for the (side, loader) pair.
 template <class Op, bool ISP, int KIND> struct LState;
 template <class Op, bool ISP> struct LState<Op, ISP, L_SK> { struct type {}; };
 template <class Op> struct LState<Op, true, L_SR> { typedef typename Op::PR type; };
 template <class Op> struct LState<Op, true, L_KV> { typedef typename Op::PV type; };
+template <class Op> struct LState<Op, true, L_KD> { typedef typename Op::PV type; };
+template <class Op> struct LState<Op, false, L_KD> { typedef typename Op::QV type; };
 template <class Op> struct LState<Op, true, L_RV> { typedef typename Op::PC type; };
 template <class Op> struct LState<Op, false, L_SR> { typedef typename Op::QR type; };
 template <class Op> struct LState<Op, false, L_KV> { typedef typename Op::QV type; };
@@ -434,6 +484,41 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RV, BR, B
     }
 };
 
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KD, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int NG = BK / VEC;   // granules per row
+    static constexpr int RPP = 256 / NG;  // rows per pass (four waves)
+    static constexpr int RPW = 64 / NG;   // rows per wave and load
+    static constexpr int N = (BR + RPP - 1) / RPP;
+    typedef LdsD<BK, VEC> L;
+    static_assert(BR % RPW == 0, "KD tile");
+    typename LState<Op, ISP, L_KD>::type s[N];
+    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
+    {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int row = r0 + tid / NG + i * RPP;
+            if constexpr (ISP) s[i] = Op::pv(a, c, row);
+            else s[i] = Op::qv(a, c, row);
+        }
+    }
+    // issue the loads of the tile at k0 into the LDS stage dst
+    __device__ __forceinline__ void load(const GemmArgs& a, const BufD<T>& B, const Ctx& c, int tid,
+                                         int wave, T* dst, int k0)
+    {
+        const int rt = tid / NG;  // row within a pass; swz(rt + i * RPP) == swz(rt)
+        const int k = k0 + ((tid % NG) ^ L::swz(rt)) * VEC;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (!(RPP * N <= BR || i * RPP + wave * RPW < BR)) continue;  // wave beyond the tile
+            B.lds = dst + (i * RPP + wave * RPW) * BK;
+            if constexpr (ISP) (void)Op::p_kv(a, B, c, s[i], k);
+            else (void)Op::q_kv(a, B, c, s[i], k);
+        }
+    }
+};
+
 // ---- the tiled MFMA kernel --------------------------------------------------------------------
 
 template <class Op, int FP, int FQ, int BK, int PK, int QK>
@@ -543,6 +628,144 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     }
 }
 
+// The same product with at least one operand loaded straight into LDS (KD).  Two LDS stages: the
+// loads of the next k tile (direct ones into the other stage, register ones into registers,
+// staged there after the products) overlap the products of this tile, and one barrier per k
+// tile separates the stages.
+template <class Op, int FP, int FQ, int BK, int PK, int QK>
+__global__ __launch_bounds__(256) void igemm_direct_kernel(const GemmArgs a)
+{
+    typedef typename Op::TT T;
+    typedef Mma<T> M;
+    constexpr int BP = 32 * FP, BQ = 32 * FQ;
+    constexpr int VEC = M::VEC;
+    typedef TileOf<PK, BP, BK, VEC> TP;
+    typedef TileOf<QK, BQ, BK, VEC> TQ;
+    typedef typename TP::L LP;
+    typedef typename TQ::L LQ;
+    static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
+    static_assert(PK == L_KD || QK == L_KD, "direct kernel without a direct operand");
+
+    // one array per stage, so that the compiler can tell the loads into one stage from the
+    // reads of the other and does not wait for the loads in flight before reading
+    __shared__ __attribute__((aligned(16))) T sP0[TP::ELEMS];
+    __shared__ __attribute__((aligned(16))) T sP1[TP::ELEMS];
+    __shared__ __attribute__((aligned(16))) T sQ0[TQ::ELEMS];
+    __shared__ __attribute__((aligned(16))) T sQ1[TQ::ELEMS];
+    extern __shared__ TabEnt tab[];  // sized at launch
+
+    const TileId tile = xcd_tile<Op::SHARE_Q>();
+    Ctx c;
+    decode_z(a, c, tile.bz);
+    const int p0 = tile.by * BP, q0 = tile.bx * BQ;
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+
+    if constexpr (Op::TAB) {
+        constexpr int TS = (Op::TAB_CHUNK && (QK == L_KV || QK == L_KD)) ? VEC : 1;
+        const int n = a.kchunk / TS;
+        for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
+        c.tab = tab;
+        __syncthreads();
+    }
+
+    typedef std::conditional_t<PK == L_KD, BufD<T>, Buf<T>> BPt;
+    typedef std::conditional_t<QK == L_KD, BufD<T>, Buf<T>> BQt;
+    const BPt bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+    const BQt bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
+    Loader<Op, true, PK, BP, BK> lp;
+    Loader<Op, false, QK, BQ, BK> lq;
+    lp.init(a, c, tid, p0);
+    lq.init(a, c, tid, q0);
+
+    const int wp = wave >> 1, wq = wave & 1;
+    const int lr = lane & 15, lg = lane >> 4;
+
+    f32x4 acc[FP][FQ];
+#pragma unroll
+    for (int i = 0; i < FP; ++i)
+#pragma unroll
+        for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // issue the loads of the tile at k into stage (dp, dq); register loaders: into registers
+    auto issue = [&](T* dp, T* dq, int k) {
+        if constexpr (PK == L_KD) lp.load(a, bufP, c, tid, wave, dp, k);
+        else lp.load(a, bufP, c, tid, p0, k);
+        if constexpr (QK == L_KD) lq.load(a, bufQ, c, tid, wave, dq, k);
+        else lq.load(a, bufQ, c, tid, q0, k);
+    };
+    auto stage_regs = [&](T* dp, T* dq) {
+        if constexpr (PK != L_KD) lp.stage(dp, tid);
+        if constexpr (QK != L_KD) lq.stage(dq, tid);
+    };
+    // one k tile: wait until the stage (tp, tq) is complete in every wave, start the next tile
+    // into (np_, nq_), multiply, then stage the next tile's register loads
+    auto step = [&](const T* tp, const T* tq, T* np_, T* nq_, int k0) {
+        __syncthreads();
+        const bool more = k0 + BK < c.kend;
+        if (more) issue(np_, nq_, k0 + BK);
+#pragma unroll
+        for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
+            typename M::frag fa[FP], fb[FQ];
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+                fa[i] = *reinterpret_cast<const typename M::frag*>(
+                    &tp[LP::at(wp * 16 * FP + i * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+#pragma unroll
+            for (int j = 0; j < FQ; ++j)
+                fb[j] = *reinterpret_cast<const typename M::frag*>(
+                    &tq[LQ::at(wq * 16 * FQ + j * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+        }
+        if (more) stage_regs(np_, nq_);
+        return more;
+    };
+
+    int k0 = c.kbeg;
+    if (k0 < c.kend) {
+        issue(sP0, sQ0, k0);
+        stage_regs(sP0, sQ0);
+        // the barrier in step() follows this wave's waits for its own loads (the fence of
+        // __syncthreads), so every stage is complete in all waves before it is read
+        for (;;) {
+            if (!step(sP0, sQ0, sP1, sQ1, k0)) break;
+            k0 += BK;
+            if (!step(sP1, sQ1, sP0, sQ0, k0)) break;
+            k0 += BK;
+        }
+    }
+
+    const bool split = a.splits > 1;
+    float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
+#pragma unroll
+    for (int i = 0; i < FP; ++i) {
+        const int p = p0 + wp * 16 * FP + i * 16 + lg * 4;
+        if (p >= a.Pdim) continue;
+        const int np = min(4, a.Pdim - p);
+        if (split) {
+#pragma unroll
+            for (int j = 0; j < FQ; ++j) {
+                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                if (q >= a.Qdim) continue;
+                float* o = part + (long long)q * a.Pdim + p;
+                if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
+                else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
+            }
+        } else {
+            const f32x4 rb = row_bias<Op>(a, c, p, np);
+#pragma unroll
+            for (int j = 0; j < FQ; ++j) {
+                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                if (q >= a.Qdim) continue;
+                Op::store4(a, c, p, q, acc[i][j] + rb, np);
+            }
+        }
+    }
+}
+
 // Second pass of a split reduction.  A block covers OPB = 256/SL consecutive outputs t =
 // q * Pdim + p of one (shard, group) with SL threads per output: thread l adds splits l,
 // l + SL, ... in ascending order, then the SL partial sums are added in ascending l.
@@ -592,12 +815,16 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     if (grid.y > 65535u || grid.z > 65535u) return hipErrorInvalidConfiguration;
     size_t shm = 0;
     if constexpr (Op::TAB) {
-        const int ts = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+        const int ts = (Op::TAB_CHUNK && (QK == L_KV || QK == L_KD)) ? VEC : 1;
         const int n = a.kchunk / ts;
         if (n > kMaxTab) return hipErrorInvalidValue;  // the plan keeps chunks within the table
         shm = sizeof(TabEnt) * (size_t)n;
     }
-    hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
+    if constexpr (PK == L_KD || QK == L_KD)
+        hipLaunchKernelGGL((igemm_direct_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s,
+                           a);
+    else
+        hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
     timing_split(s, "reduce");

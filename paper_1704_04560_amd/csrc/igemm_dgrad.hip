@@ -83,7 +83,7 @@ hipError_t conv_dgrad(Dt dt, const ConvGeom& g, const void* dy, const void* wd, 
     const bool v = a.og % vec_elems(dt) == 0;  // then OC and Kdim are multiples too
     if (g.S == 1) {
         if (dt == DT_F32) {
-            if (v) return run_gemm<ConvDgrad<float, true>, L_KV, L_KV>(a, p, d.Z, partial, s);
+            if (v) return run_gemm<ConvDgrad<float, true>, L_KD, L_KD>(a, p, d.Z, partial, s);
             return run_gemm<ConvDgrad<float, true>, L_SK, L_SR>(a, p, d.Z, partial, s);
         }
         if (v) return run_gemm<ConvDgrad<bf16_t, true>, L_KV, L_KV>(a, p, d.Z, partial, s);
@@ -109,7 +109,7 @@ hipError_t conv_dgrad_col(Dt dt, const ConvGeom& g, const void* dy, const void* 
     const bool v = a.og % vec_elems(dt) == 0;
     hipError_t e;
     if (dt == DT_F32)
-        e = v ? run_gemm<ConvDgradCol<float>, L_KV, L_KV>(a, p, d.Z, partial, s)
+        e = v ? run_gemm<ConvDgradCol<float>, L_KD, L_KD>(a, p, d.Z, partial, s)
               : run_gemm<ConvDgradCol<float>, L_SK, L_SK>(a, p, d.Z, partial, s);
     else
         e = v ? run_gemm<ConvDgradCol<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s)
@@ -139,9 +139,9 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
     const bool pv = IN % vec_elems(dt) == 0, qv = OUT % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef FcDgrad<float> Op;
-        if (pv && qv) return run_gemm<Op, L_RV, L_KV>(a, p, d.Z, partial, s);
+        if (pv && qv) return run_gemm<Op, L_RV, L_KD>(a, p, d.Z, partial, s);
         if (pv) return run_gemm<Op, L_RV, L_SK>(a, p, d.Z, partial, s);
-        if (qv) return run_gemm<Op, L_SR, L_KV>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_KD>(a, p, d.Z, partial, s);
         return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
     }
     typedef FcDgrad<bf16_t> Op;

@@ -17,7 +17,7 @@ hipError_t conv_fwd(Dt dt, const ConvGeom& g, const void* x, const void* wf, con
     const GemmPlan p = plan_for(dt, d);
     const bool v = a.cg % vec_elems(dt) == 0;  // then C (= G*cg) and Kdim are multiples too
     if (dt == DT_F32) {
-        if (v) return run_gemm<ConvFwd<float>, L_KV, L_KV>(a, p, d.Z, partial, s);
+        if (v) return run_gemm<ConvFwd<float>, L_KD, L_KD>(a, p, d.Z, partial, s);
         return run_gemm<ConvFwd<float>, L_SK, L_SR>(a, p, d.Z, partial, s);
     }
     if (v) return run_gemm<ConvFwd<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s);
@@ -40,7 +40,7 @@ hipError_t conv_fwd_run(Dt dt, const ConvGeom& g, const RunGeom& r, const void* 
     const GemmDims d = conv_fwd_run_dims(dt, g, r);
     a.Pdim = d.P; a.Qdim = d.Q; a.Kdim = d.K;
     const GemmPlan p = plan_for(dt, d);
-    if (dt == DT_F32) return run_gemm<ConvFwdRun<float>, L_KV, L_KV>(a, p, d.Z, partial, s);
+    if (dt == DT_F32) return run_gemm<ConvFwdRun<float>, L_KD, L_KD>(a, p, d.Z, partial, s);
     return run_gemm<ConvFwdRun<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s);
 }
 
@@ -59,7 +59,7 @@ hipError_t fc_fwd(Dt dt, int B, int IN, int OUT, const void* x, const void* w, c
     const GemmPlan p = plan_for(dt, d);
     const bool v = IN % vec_elems(dt) == 0;
     if (dt == DT_F32) {
-        if (v) return run_gemm<FcFwd<float>, L_KV, L_KV>(a, p, d.Z, partial, s);
+        if (v) return run_gemm<FcFwd<float>, L_KD, L_KD>(a, p, d.Z, partial, s);
         return run_gemm<FcFwd<float>, L_SK, L_SK>(a, p, d.Z, partial, s);
     }
     if (v) return run_gemm<FcFwd<bf16_t>, L_KV, L_KV>(a, p, d.Z, partial, s);

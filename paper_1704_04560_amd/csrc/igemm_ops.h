@@ -8,7 +8,8 @@
 //                     has one entry per chunk; tab_entry(a, c, k) builds an entry
 //   pk/p_sk           SK loader on P: state for column k, element of row p
 //   pr/p_sr           SR loader on P: state for row p, element at k
-//   pv/p_kv           KV loader on P: state for row p, 16 bytes at k
+//   pv/p_kv           KV and KD loaders on P: state for row p, 16 bytes at k (B.at16 on the
+//                     buffer given: a register load, or a load straight into LDS)
 //   pc/p_rv           RV loader on P: state for rows p0..p0+VEC-1, 16 bytes at k
 //   qk/q_sk, qr/q_sr, qv/q_kv, qc/q_rv   the same for Q
 //   store4(a, c, p, q, acc, np)   epilogue for rows p..p+np-1 of column q
@@ -76,7 +77,8 @@ template <typename T> struct ConvFwd {
     {
         return PV{(c.grp * a.og + p) * a.Kdim, p < a.Pdim};
     }
-    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    template <class BT>
+    __device__ static u32x4 p_kv(const GemmArgs&, const BT& B, const Ctx& c, const PV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -103,7 +105,8 @@ template <typename T> struct ConvFwd {
     }
     typedef QR QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx& c, int q) { return qr(a, c, q); }
-    __device__ static u32x4 q_kv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs& a, const BT& B, const Ctx& c, const QV& s, int k)
     {
         const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         const int hi = s.h0 + e.u, wi = s.w0 + e.v;
@@ -157,7 +160,8 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     {
         return PV{(c.grp * a.cg + p) * a.Kdim, p < a.Pdim};
     }
-    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    template <class BT>
+    __device__ static u32x4 p_kv(const GemmArgs&, const BT& B, const Ctx& c, const PV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -197,7 +201,8 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
     }
     typedef QR QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx& c, int q) { return qr(a, c, q); }
-    __device__ static u32x4 q_kv(const GemmArgs& a, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs& a, const BT& B, const Ctx& c, const QV& s, int k)
     {
         const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         const int th = s.hp - e.u, tw = s.wp - e.v;
@@ -240,7 +245,8 @@ template <typename T> struct ConvDgradCol {
     {
         return PV{(c.grp * a.KK * a.cg + p) * a.og, p < a.Pdim};
     }
-    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    template <class BT>
+    __device__ static u32x4 p_kv(const GemmArgs&, const BT& B, const Ctx& c, const PV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -259,7 +265,8 @@ template <typename T> struct ConvDgradCol {
     {
         return QV{q * a.OC + c.grp * a.og, q < a.Qdim};
     }
-    __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs&, const BT& B, const Ctx& c, const QV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -384,7 +391,8 @@ template <typename T> struct ConvFwdRun {
     // P: Wr[p * Kdim + k]
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx&, int p) { return PV{p * a.Kdim, p < a.Pdim}; }
-    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    template <class BT>
+    __device__ static u32x4 p_kv(const GemmArgs&, const BT& B, const Ctx& c, const PV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -398,7 +406,8 @@ template <typename T> struct ConvFwdRun {
         const unsigned oh = fdiv(a.fd_ow, hw), ow = hw - oh * (unsigned)a.OW;
         return QV{(((int)b * a.Hp + (int)oh * a.S) * a.Wp + (int)ow * a.S) * a.Cp, ok};
     }
-    __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs&, const BT& B, const Ctx& c, const QV& s, int k)
     {
         const TabEnt e = ld_tab(c.tab + (k - c.kbeg) / (16 / (int)sizeof(T)));
         return B.at16(s.ok, s.off + e.off);
@@ -503,7 +512,8 @@ template <typename T> struct FcFwd {
     }
     typedef RowOk PV;
     __device__ static PV pv(const GemmArgs& a, const Ctx&, int p) { return PV{p * a.Kdim, p < a.Pdim}; }
-    __device__ static u32x4 p_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const PV& s, int k)
+    template <class BT>
+    __device__ static u32x4 p_kv(const GemmArgs&, const BT& B, const Ctx& c, const PV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -515,7 +525,8 @@ template <typename T> struct FcFwd {
     }
     typedef RowOk QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx&, int q) { return QV{q * a.Kdim, q < a.Qdim}; }
-    __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs&, const BT& B, const Ctx& c, const QV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }
@@ -559,7 +570,8 @@ template <typename T> struct FcDgrad {
     }
     typedef RowOk QV;
     __device__ static QV qv(const GemmArgs& a, const Ctx&, int q) { return QV{q * a.Kdim, q < a.Qdim}; }
-    __device__ static u32x4 q_kv(const GemmArgs&, const Buf<T>& B, const Ctx& c, const QV& s, int k)
+    template <class BT>
+    __device__ static u32x4 q_kv(const GemmArgs&, const BT& B, const Ctx& c, const QV& s, int k)
     {
         return B.at16(s.ok & (k < c.kend), s.off + k);
     }

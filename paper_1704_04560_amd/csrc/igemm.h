@@ -282,20 +282,31 @@ template <int BK, int VEC> struct LdsD {
     }
 };
 
+// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector-memory operations of the
+// wave are outstanding, with no wait on the other counters
+constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+// The direct load is written as inline assembly: the compiler then does not count it, so it
+// neither waits for loads into one stage before reading another nor makes every barrier wait
+// for all of them; the kernels wait for them explicitly (waitcnt_vm) before the barrier that
+// opens a stage.  M0 (the wave's LDS destination) is an operand of the statement.
 template <typename T> struct BufD {
-    __amdgpu_buffer_rsrc_t r;
+    u32x4 r;         // raw buffer resource: base, size in bytes, 32-bit format
     mutable T* lds;  // wave-uniform LDS destination of the next load
-    __device__ __forceinline__ BufD(const void* p, unsigned bytes)
-        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
-                                              (int)kRsrcWord3)),
-          lds(nullptr)
+    __device__ __forceinline__ BufD(const void* p, unsigned bytes) : lds(nullptr)
     {
+        const unsigned long long b = reinterpret_cast<unsigned long long>(p);
+        r = u32x4{(unsigned)b, (unsigned)(b >> 32) & 0xffffu, bytes, kRsrcWord3};
     }
     __device__ __forceinline__ u32x4 at16(bool ok, int idx) const
     {
         const int off = ok ? idx * (int)sizeof(T) : (int)kOOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+        const unsigned m0 = (unsigned)reinterpret_cast<unsigned long long>(
+            (__attribute__((address_space(3))) T*)lds);
+        asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+                     :
+                     : "v"(off), "s"(r), "{m0}"(m0)
+                     : "memory");
         return u32x4{0u, 0u, 0u, 0u};
     }
 };
@@ -646,8 +657,8 @@ __global__ __launch_bounds__(256) void igemm_direct_kernel(const GemmArgs a)
     static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
     static_assert(PK == L_KD || QK == L_KD, "direct kernel without a direct operand");
 
-    // one array per stage, so that the compiler can tell the loads into one stage from the
-    // reads of the other and does not wait for the loads in flight before reading
+    // one array per stage; the loop is unrolled over the two so that each step's stages are
+    // known at compile time
     __shared__ __attribute__((aligned(16))) T sP0[TP::ELEMS];
     __shared__ __attribute__((aligned(16))) T sP1[TP::ELEMS];
     __shared__ __attribute__((aligned(16))) T sQ0[TQ::ELEMS];
@@ -701,6 +712,7 @@ __global__ __launch_bounds__(256) void igemm_direct_kernel(const GemmArgs a)
     // one k tile: wait until the stage (tp, tq) is complete in every wave, start the next tile
     // into (np_, nq_), multiply, then stage the next tile's register loads
     auto step = [&](const T* tp, const T* tq, T* np_, T* nq_, int k0) {
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // this wave's direct loads of the stage
         __syncthreads();
         const bool more = k0 + BK < c.kend;
         if (more) issue(np_, nq_, k0 + BK);
@@ -728,8 +740,8 @@ __global__ __launch_bounds__(256) void igemm_direct_kernel(const GemmArgs a)
     if (k0 < c.kend) {
         issue(sP0, sQ0, k0);
         stage_regs(sP0, sQ0);
-        // the barrier in step() follows this wave's waits for its own loads (the fence of
-        // __syncthreads), so every stage is complete in all waves before it is read
+        // the barrier in step() follows this wave's wait for its own loads, so every stage is
+        // complete in all waves before it is read
         for (;;) {
             if (!step(sP0, sQ0, sP1, sQ1, k0)) break;
             k0 += BK;

@@ -226,7 +226,7 @@ def measure(torch, mtx, wl, name, steps, warmup):
         torch.cuda.synchronize()
         return t_start.elapsed_time(t_end) / k
 
-    # timed region: K steps as a training loop runs them (graph replay of the step)
+    # timed region: K steps as a training loop runs them
     ms = timed(steps)
     assert torch.isfinite(loss).item(), "non-finite loss"
     # second timed region of K steps with a HIP event pair around every kernel (on the step's

@@ -258,10 +258,16 @@ template <int BK, int VEC> struct Lds {
         const int g = ((k / VEC) + (row >> 4)) & (NG - 1);
         return row * LDK + g * VEC + (k & (VEC - 1));
     }
+    // 16 bytes of row rb + lr at k = kc * ks + lg * VEC (one MFMA operand fragment)
+    template <typename F, typename T>
+    __device__ __forceinline__ static F frag(const T* t, int rb, int lr, int lg, int kc, int ks)
+    {
+        return *reinterpret_cast<const F*>(&t[at(rb + lr, kc * ks + lg * VEC)]);
+    }
 };
 
 // ---- operand loaders --------------------------------------------------------------------------
-enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3, L_KD = 4 };
+enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3, L_KD = 4, L_RT = 5 };
 
 // ---- direct loads (KD): 16 bytes along k from global memory straight into LDS -----------------
 // buffer_load_dwordx4 with the LDS flag: lane l of a wave writes LDS bytes [16 l, 16 l + 16) after
@@ -279,6 +285,42 @@ template <int BK, int VEC> struct LdsD {
     __device__ __forceinline__ static int at(int row, int k)
     {
         return row * BK + (((k / VEC) ^ swz(row)) * VEC) + (k & (VEC - 1));
+    }
+    template <typename F, typename T>
+    __device__ __forceinline__ static F frag(const T* t, int rb, int lr, int lg, int kc, int ks)
+    {
+        return *reinterpret_cast<const F*>(&t[at(rb + lr, kc * ks + lg * VEC)]);
+    }
+};
+
+// ---- k-major tiles read with the transposing LDS load (RT, bf16) ---------------------------
+// The weight-gradient operands arrive 16 bytes along the rows (8 rows at one k).  They are
+// stored as loaded, T[k][row], and the MFMA fragments (8 consecutive k of one row per lane)
+// come from ds_read_b64_tr_b16: within each group of 16 lanes, output lane i, element c is
+// element i % 4 of the 8 bytes addressed by lane 4c + i / 4 (measured on gfx950).  So lane j of
+// a group addresses rows rb + 4 (j % 4) .. + 3 at k = k0 + j / 4, and lane i receives k0 .. k0+3
+// of row rb + i; a second read at k0 + 4 completes the 8 values.  The 32-byte units (16 rows) of
+// k-row k sit at unit u ^ sw(k), sw(k) = (k & 3) | ((k >> 1) & 4), so that the 8 k-rows read
+// together by two lane groups fall on distinct banks.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+template <int BR, int BK> struct LdsT {
+    static constexpr int NU = BR / 16;  // 32-byte units per k-row
+    __device__ __forceinline__ static int sw(int k) { return ((k & 3) | ((k >> 1) & 4)) & (NU - 1); }
+    __device__ __forceinline__ static int at(int k, int row)
+    {
+        return k * BR + ((((row >> 4) ^ sw(k)) << 4) | (row & 15));
+    }
+    template <typename F, typename T>
+    __device__ __forceinline__ static F frag(const T* t, int rb, int lr, int lg, int kc, int ks)
+    {
+        static_assert(sizeof(T) == 2, "transposing reads are for 16-bit elements");
+        const int k0 = kc * ks + lg * 8 + (lr >> 2), row = rb + 4 * (lr & 3);
+        typedef __attribute__((address_space(3))) s16x4* P3;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (P3)(__attribute__((address_space(3))) T*)&t[at(k0, row)]);
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (P3)(__attribute__((address_space(3))) T*)&t[at(k0 + 4, row)]);
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
 };
 
@@ -321,6 +363,10 @@ template <int BR, int BK, int VEC> struct TileOf<L_KD, BR, BK, VEC> {
     typedef LdsD<BK, VEC> L;
     static constexpr int ELEMS = BR * BK;
 };
+template <int BR, int BK, int VEC> struct TileOf<L_RT, BR, BK, VEC> {
+    typedef LdsT<BR, BK> L;
+    static constexpr int ELEMS = BR * BK;
+};
 
 // Per-thread loader state: the operation's type for the (side, loader) pair.
 template <class Op, bool ISP, int KIND> struct LState;
@@ -330,6 +376,8 @@ template <class Op> struct LState<Op, true, L_KV> { typedef typename Op::PV type
 template <class Op> struct LState<Op, true, L_KD> { typedef typename Op::PV type; };
 template <class Op> struct LState<Op, false, L_KD> { typedef typename Op::QV type; };
 template <class Op> struct LState<Op, true, L_RV> { typedef typename Op::PC type; };
+template <class Op> struct LState<Op, true, L_RT> { typedef typename Op::PC type; };
+template <class Op> struct LState<Op, false, L_RT> { typedef typename Op::QC type; };
 template <class Op> struct LState<Op, false, L_SR> { typedef typename Op::QR type; };
 template <class Op> struct LState<Op, false, L_KV> { typedef typename Op::QV type; };
 template <class Op> struct LState<Op, false, L_RV> { typedef typename Op::QC type; };
@@ -495,6 +543,45 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RV, BR, B
     }
 };
 
+// RT: 16 bytes along the rows (8 rows at one k), stored as loaded into the k-major tile.
+template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RT, BR, BK> {
+    typedef typename Op::TT T;
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int RCH = BR / VEC;  // row chunks per tile
+    static constexpr int KPP = 256 / RCH;  // k per pass
+    static constexpr int N = (BK + KPP - 1) / KPP;
+    static_assert(sizeof(T) == 2 && BR % VEC == 0 && 256 % RCH == 0, "RT tile");
+    typedef LdsT<BR, BK> L;
+    typename LState<Op, ISP, L_RT>::type s;
+    u32x4 reg[N];
+    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
+    {
+        const int row0 = r0 + (tid % RCH) * VEC;
+        if constexpr (ISP) s = Op::pc(a, c, row0);
+        else s = Op::qc(a, c, row0);
+    }
+    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
+                                         int, int k0)
+    {
+        const int kt = tid / RCH;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (!(KPP * N <= BK || kt + i * KPP < BK)) continue;
+            if constexpr (ISP) reg[i] = Op::p_rv(a, B, c, s, k0 + kt + i * KPP);
+            else reg[i] = Op::q_rv(a, B, c, s, k0 + kt + i * KPP);
+        }
+    }
+    __device__ __forceinline__ void stage(T* lds, int tid) const
+    {
+        const int row0 = (tid % RCH) * VEC, kt = tid / RCH;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (!(KPP * N <= BK || kt + i * KPP < BK)) continue;
+            *reinterpret_cast<u32x4*>(&lds[L::at(kt + i * KPP, row0)]) = reg[i];
+        }
+    }
+};
+
 template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KD, BR, BK> {
     typedef typename Op::TT T;
     static constexpr int VEC = 16 / sizeof(T);
@@ -539,11 +626,14 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     typedef Mma<T> M;
     constexpr int BP = 32 * FP, BQ = 32 * FQ;
     constexpr int VEC = M::VEC;
-    typedef Lds<BK, VEC> L;
+    typedef TileOf<PK, BP, BK, VEC> TP;
+    typedef TileOf<QK, BQ, BK, VEC> TQ;
+    typedef typename TP::L LP;
+    typedef typename TQ::L LQ;
     static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
 
-    __shared__ __attribute__((aligned(16))) T sP[BP * L::LDK];
-    __shared__ __attribute__((aligned(16))) T sQ[BQ * L::LDK];
+    __shared__ __attribute__((aligned(16))) T sP[TP::ELEMS];
+    __shared__ __attribute__((aligned(16))) T sQ[TQ::ELEMS];
     extern __shared__ TabEnt tab[];  // sized at launch
 
     const TileId tile = xcd_tile<Op::SHARE_Q>();
@@ -596,12 +686,12 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
             typename M::frag fa[FP], fb[FQ];
 #pragma unroll
             for (int i = 0; i < FP; ++i)
-                fa[i] = *reinterpret_cast<const typename M::frag*>(
-                    &sP[L::at(wp * 16 * FP + i * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+                fa[i] = LP::template frag<typename M::frag>(sP, wp * 16 * FP + i * 16, lr, lg,
+                                                            kc, M::KSTEP);
 #pragma unroll
             for (int j = 0; j < FQ; ++j)
-                fb[j] = *reinterpret_cast<const typename M::frag*>(
-                    &sQ[L::at(wq * 16 * FQ + j * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+                fb[j] = LQ::template frag<typename M::frag>(sQ, wq * 16 * FQ + j * 16, lr, lg,
+                                                            kc, M::KSTEP);
 #pragma unroll
             for (int i = 0; i < FP; ++i)
 #pragma unroll
@@ -721,12 +811,12 @@ __global__ __launch_bounds__(256) void igemm_direct_kernel(const GemmArgs a)
             typename M::frag fa[FP], fb[FQ];
 #pragma unroll
             for (int i = 0; i < FP; ++i)
-                fa[i] = *reinterpret_cast<const typename M::frag*>(
-                    &tp[LP::at(wp * 16 * FP + i * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+                fa[i] = LP::template frag<typename M::frag>(tp, wp * 16 * FP + i * 16, lr, lg,
+                                                            kc, M::KSTEP);
 #pragma unroll
             for (int j = 0; j < FQ; ++j)
-                fb[j] = *reinterpret_cast<const typename M::frag*>(
-                    &tq[LQ::at(wq * 16 * FQ + j * 16 + lr, kc * M::KSTEP + lg * VEC)]);
+                fb[j] = LQ::template frag<typename M::frag>(tq, wq * 16 * FQ + j * 16, lr, lg,
+                                                            kc, M::KSTEP);
 #pragma unroll
             for (int i = 0; i < FP; ++i)
 #pragma unroll

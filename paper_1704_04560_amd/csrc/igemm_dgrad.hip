@@ -145,8 +145,8 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
         return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
     }
     typedef FcDgrad<bf16_t> Op;
-    if (pv && qv) return run_gemm<Op, L_RV, L_KV>(a, p, d.Z, partial, s);
-    if (pv) return run_gemm<Op, L_RV, L_SK>(a, p, d.Z, partial, s);
+    if (pv && qv) return run_gemm<Op, L_RT, L_KV>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RT, L_SK>(a, p, d.Z, partial, s);
     if (qv) return run_gemm<Op, L_SR, L_KV>(a, p, d.Z, partial, s);
     return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
 }

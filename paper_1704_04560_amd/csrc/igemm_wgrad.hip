@@ -26,9 +26,9 @@ hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void
         return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
     }
     typedef ConvWgrad<bf16_t> Op;
-    if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-    if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
-    if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    if (pv && qv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RT, L_SR>(a, p, d.Z, partial, s);
+    if (qv) return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
     return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
 }
 
@@ -55,8 +55,8 @@ hipError_t conv_wgrad_run(Dt dt, const ConvGeom& g, const RunGeom& r, int R, con
         return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
     }
     typedef ConvWgradRun<bf16_t> Op;
-    if (pv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-    return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+    return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
 }
 
 hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
@@ -83,9 +83,9 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
         return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
     }
     typedef FcWgrad<bf16_t> Op;
-    if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-    if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
-    if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+    if (pv && qv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+    if (pv) return run_gemm<Op, L_RT, L_SR>(a, p, d.Z, partial, s);
+    if (qv) return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
     return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
 }
 

@@ -300,12 +300,19 @@ template <int BK, int VEC> struct LdsD {
 // element i % 4 of the 8 bytes addressed by lane 4c + i / 4 (measured on gfx950).  So lane j of
 // a group addresses rows rb + 4 (j % 4) .. + 3 at k = k0 + j / 4, and lane i receives k0 .. k0+3
 // of row rb + i; a second read at k0 + 4 completes the 8 values.  The 32-byte units (16 rows) of
-// k-row k sit at unit u ^ sw(k), sw(k) = (k & 3) | ((k >> 1) & 4), so that the 8 k-rows read
-// together by two lane groups fall on distinct banks.
+// k-row k sit at unit u ^ sw(k).  Two lane groups read k-rows {k0 .. k0+3, k0+8 .. k0+11}
+// together; sw spreads those 8 over distinct 32-byte bank slots given how many k-rows share a
+// 256-byte bank window (one for 128 rows, two for 64, four for 32).
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 template <int BR, int BK> struct LdsT {
     static constexpr int NU = BR / 16;  // 32-byte units per k-row
-    __device__ __forceinline__ static int sw(int k) { return ((k & 3) | ((k >> 1) & 4)) & (NU - 1); }
+    static_assert(NU == 2 || NU == 4 || NU == 8, "k-major tile rows");
+    __device__ __forceinline__ static int sw(int k)
+    {
+        if constexpr (NU == 8) return (k & 3) | ((k >> 1) & 4);
+        else if constexpr (NU == 4) return ((k >> 1) & 1) | ((k >> 2) & 2);
+        else return (k >> 3) & 1;
+    }
     __device__ __forceinline__ static int at(int k, int row)
     {
         return k * BR + ((((row >> 4) ^ sw(k)) << 4) | (row & 15));

@@ -612,12 +612,12 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KD, BR, B
     __device__ __forceinline__ void load(const GemmArgs& a, const BufD<T>& B, const Ctx& c, int tid,
                                          int wave, T* dst, int k0)
     {
-        const int rt = tid / NG;  // row within a pass; swz(rt + i * RPP) == swz(rt)
-        const int k = k0 + ((tid % NG) ^ L::swz(rt)) * VEC;
+        const int rt = tid / NG;  // row within a pass
 #pragma unroll
         for (int i = 0; i < N; ++i) {
             if (!(RPP * N <= BR || i * RPP + wave * RPW < BR)) continue;  // wave beyond the tile
             B.lds = dst + (i * RPP + wave * RPW) * BK;
+            const int k = k0 + ((tid % NG) ^ L::swz(rt + i * RPP)) * VEC;
             if constexpr (ISP) (void)Op::p_kv(a, B, c, s[i], k);
             else (void)Op::q_kv(a, B, c, s[i], k);
         }

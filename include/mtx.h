@@ -181,6 +181,17 @@ int mtx_set_graph_replay(mtx_model* m, int enable);
  * on.  enable = 0 switches it off. */
 int mtx_set_overlap(mtx_model* m, int enable);
 
+/* Layer-wise average + update (execution option, default off; Sec. III-D.2 reduces the
+ * gradients one layer at a time, in layer order).  With it on, mtx_train_step averages and
+ * updates each layer's parameters (its W and b slice of w, v, grad_avg) on a third stream of the
+ * model as soon as that layer's R shard gradients are written, beside the rest of the backward
+ * pass, instead of once over all P parameters at the end; the step still returns after every
+ * layer's update (the caller's stream waits for them).  Each element's arithmetic is the same,
+ * so the results are bit-identical either way.  Measured on MI355X it was not faster: the
+ * bandwidth-bound updates slowed the concurrent backward kernels by as much as they overlapped.
+ * Ignored while kernel timing is on.  Returns MTX_EINVAL for a NULL model. */
+int mtx_set_layerwise_update(mtx_model* m, int enable);
+
 /* Kernel timing of mtx_train_step (measurement support; not part of the method).
  * mtx_set_timing(m, 1) makes every later mtx_train_step record a HIP event pair on its stream
  * around each kernel launch; mtx_set_timing(m, 0) stops it.  mtx_get_timing waits for the

@@ -466,11 +466,16 @@ struct mtx_model {
     hipStream_t last_stream;
     Timer timer;
     GraphCache graph;
-    // second stream for the weight gradients (overlapped with the data-gradient chain)
+    // second stream for the weight gradients (overlapped with the data-gradient chain), third
+    // stream for the layer-wise average + update that follows each layer's weight gradients
     bool overlap = false;
     hipStream_t side = nullptr;
     std::vector<hipEvent_t> fork;  // per weight-gradient launch: its output gradient is ready
     hipEvent_t join = nullptr;     // every weight gradient is done
+    bool layerwise = false;         // average + update per layer on the third stream
+    hipStream_t upd = nullptr;
+    std::vector<hipEvent_t> wdone;  // per parameter layer: its weight gradients are done
+    hipEvent_t upd_join = nullptr;  // every layer's update is done
 };
 
 namespace {
@@ -539,6 +544,17 @@ hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s,
 }  // namespace
 
 namespace {
+void release_update_stream(mtx_model* m)
+{
+    for (hipEvent_t& e : m->wdone)
+        if (e) (void)hipEventDestroy(e);
+    m->wdone.clear();
+    if (m->upd_join) (void)hipEventDestroy(m->upd_join);
+    m->upd_join = nullptr;
+    if (m->upd) (void)hipStreamDestroy(m->upd);
+    m->upd = nullptr;
+}
+
 void destroy_streams(mtx_model* m)
 {
     for (hipEvent_t& e : m->fork)
@@ -548,6 +564,7 @@ void destroy_streams(mtx_model* m)
     m->join = nullptr;
     if (m->side) (void)hipStreamDestroy(m->side);
     m->side = nullptr;
+    release_update_stream(m);
 }
 }  // namespace
 
@@ -648,6 +665,7 @@ void mtx_free_model(mtx_model* m)
     if (!m) return;
     (void)hipStreamSynchronize(m->last_stream);
     if (m->side) (void)hipStreamSynchronize(m->side);
+    if (m->upd) (void)hipStreamSynchronize(m->upd);
     m->graph.destroy();
     m->timer.destroy();
     destroy_streams(m);
@@ -658,6 +676,35 @@ int mtx_set_overlap(mtx_model* m, int enable)
 {
     if (!m) return fail(MTX_EINVAL, "model is NULL");
     m->overlap = enable != 0;
+    m->graph.reset();  // the captured launch sequence depends on it
+    return MTX_OK;
+}
+
+int mtx_set_layerwise_update(mtx_model* m, int enable)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    // the third stream exists only while it is used: the box exposes few hardware queues, and
+    // an idle extra stream can leave the weight-gradient stream sharing one with the caller's
+    if (enable && !m->upd) {
+        hipError_t e = hipStreamCreateWithFlags(&m->upd, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            m->upd = nullptr;
+            return hip_fail(e, "mtx_set_layerwise_update");
+        }
+        m->wdone.assign(m->pl.n_wgrad, nullptr);
+        for (size_t i = 0; i < m->wdone.size() && e == hipSuccess; ++i)
+            e = hipEventCreateWithFlags(&m->wdone[i], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&m->upd_join, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            release_update_stream(m);
+            return hip_fail(e, "mtx_set_layerwise_update");
+        }
+    }
+    if (!enable && m->upd) {
+        (void)hipStreamSynchronize(m->upd);
+        release_update_stream(m);
+    }
+    m->layerwise = enable != 0;
     m->graph.reset();  // the captured launch sequence depends on it
     return MTX_OK;
 }
@@ -763,9 +810,10 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     // output gradient and input, so (unless kernels are being timed) it runs on the second
     // stream, forked after its output gradient is written and joined before the update.
     const bool overlap = m->overlap && !m->timer.on;
+    const bool layerwise = m->layerwise && !m->timer.on;
     float* partial_w = overlap ? reinterpret_cast<float*>(ws + pl.partial_w_off) : partial;
     const long long ld = (long long)pl.ld;
-    int nfork = 0;
+    int nfork = 0, nlayer = 0;
     for (int l = (int)pl.L.size() - 1; l >= pl.first_param && l >= 0; --l) {
         const LayerPlan& lp = pl.L[l];
         const void* in_l = l == 0 ? x_in : static_cast<const void*>(ws + pl.L[l - 1].act_off);
@@ -819,10 +867,31 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                         mask ? ws + lp.act_off : nullptr, s);
                     }), "pool backward");
         }
+        // Layer-wise averaging (the paper issues one reduction per layer, in layer order): this
+        // layer's parameters are averaged and updated on the third stream as soon as its R
+        // shard gradients are written, beside the rest of the backward pass.  Nothing later in
+        // the step reads this layer's master weights: the data gradients read the prepared
+        // copies.
+        if (lp.w_len && layerwise) {
+            HIP_TRY(hipEventRecord(m->wdone[nlayer], sw), "layer gradients done");
+            HIP_TRY(hipStreamWaitEvent(m->upd, m->wdone[nlayer], 0), "layer gradients done");
+            ++nlayer;
+            const size_t off = lp.w_off, len = lp.w_len + lp.b_len;
+            HIP_TRY(launch_site(m, "avg_update", l, m->upd, [&] {
+                        return average_update(m->grads + off, pl.R, len, pl.ld, m->w + off,
+                                              m->v + off, lr, momentum, m->gavg + off, true,
+                                              m->upd);
+                    }), "layer average + update");
+        }
     }
     if (nfork) {
         HIP_TRY(hipEventRecord(m->join, m->side), "join");
         HIP_TRY(hipStreamWaitEvent(s, m->join, 0), "join");
+    }
+    if (nlayer) {
+        HIP_TRY(hipEventRecord(m->upd_join, m->upd), "join");
+        HIP_TRY(hipStreamWaitEvent(s, m->upd_join, 0), "join");
+        return MTX_OK;
     }
     // ---- average of the R shard gradients fused with the optimizer step ----
     HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {

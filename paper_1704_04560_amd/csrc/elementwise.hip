@@ -754,16 +754,43 @@ hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+template <bool MOM, bool AVG, bool UPD>
+__device__ __forceinline__ void avg_update_one(const float* __restrict__ grads, int R, long long ld,
+                                               long long i, float* __restrict__ w,
+                                               float* __restrict__ v, float lr, float mu,
+                                               float* __restrict__ avg)
+{
+    float s = grads[i];
+    for (int r = 1; r < R; ++r) s += grads[(long long)r * ld + i];
+    float g = s / (float)R;
+    if (AVG) avg[i] = g;
+    if (UPD) {
+        if (MOM) {
+            const float vn = fmaf(mu, v[i], g);
+            v[i] = vn;
+            g = vn;
+        }
+        w[i] = fmaf(-lr, g, w[i]);
+    }
+}
+
+// n elements: threads below n / 4 take four each; the next one takes the n % 4 left over.
 template <int RT, bool MOM, bool AVG, bool UPD>
 __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__ grads, int Rrt,
-                                                       long long n4, long long ld,
+                                                       long long n, long long ld,
                                                        float* __restrict__ w,
                                                        float* __restrict__ v, float lr, float mu,
                                                        float* __restrict__ avg)
 {
     const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (t >= n4) return;
+    const long long n4 = n / 4;
     const int R = RT > 0 ? RT : Rrt;
+    if (t >= n4) {
+        if (t == n4)
+            for (long long i = 4 * n4; i < n; ++i)
+                avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
+        return;
+    }
     const f32x4* g4 = reinterpret_cast<const f32x4*>(grads) + t;
     const long long ld4 = ld / 4;
     f32x4 s = __builtin_nontemporal_load(g4);
@@ -803,18 +830,7 @@ __global__ __launch_bounds__(256) void avg_update_scalar(const float* __restrict
 {
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
-    float s = grads[i];
-    for (int r = 1; r < R; ++r) s += grads[(long long)r * ld + i];
-    float g = s / (float)R;
-    if (AVG) avg[i] = g;
-    if (UPD) {
-        if (MOM) {
-            const float vn = fmaf(mu, v[i], g);
-            v[i] = vn;
-            g = vn;
-        }
-        w[i] = fmaf(-lr, g, w[i]);
-    }
+    avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
 }
 
 template <bool MOM, bool AVG, bool UPD>
@@ -822,18 +838,18 @@ static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t 
                                     float* v, float lr, float mu, float* avg, hipStream_t s)
 {
     auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
-    const bool vec = (n % 4 == 0) && (ld % 4 == 0) && al(grads) && (!AVG || al(avg)) &&
-                     (!UPD || al(w)) && (!MOM || al(v));
+    const bool vec = (ld % 4 == 0) && al(grads) && (!AVG || al(avg)) && (!UPD || al(w)) &&
+                     (!MOM || al(v));
     if (vec) {
-        const long long n4 = (long long)(n / 4);
-        dim3 grid(grid_for(n / 4, 256));
+        const long long nn = (long long)n;
+        dim3 grid(grid_for(n / 4 + 1, 256));
         switch (R) {
-        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
-        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
-        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
-        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
-        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
-        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, n4, (long long)ld, w, v, lr, mu, avg); break;
+        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
         }
     } else {
         hipLaunchKernelGGL((avg_update_scalar<MOM, AVG, UPD>), dim3(grid_for(n, 256)), dim3(256),

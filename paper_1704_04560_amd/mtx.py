@@ -22,7 +22,8 @@ MTX_FC, MTX_CONV, MTX_MAXPOOL = 0, 1, 2
 
 EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_train_step", "mtx_average_grads",
            "mtx_sgd_update", "mtx_get_params", "mtx_set_params", "mtx_get_layer_output",
-           "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap", "mtx_set_timing",
+           "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
+           "mtx_set_layerwise_update", "mtx_set_timing",
            "mtx_get_timing", "mtx_free_model", "mtx_last_error")
 
 
@@ -80,6 +81,7 @@ def lib() -> C.CDLL:
             "mtx_get_layer_output": (i32, [vp, i32, vp, sz]),
             "mtx_get_pool_argmax": (i32, [vp, i32, vp, sz]),
             "mtx_set_graph_replay": (i32, [vp, i32]),
+            "mtx_set_layerwise_update": (i32, [vp, i32]),
             "mtx_set_overlap": (i32, [vp, i32]),
             "mtx_set_timing": (i32, [vp, i32]),
             "mtx_get_timing": (i32, [vp, C.POINTER(mtx_kernel_time), i32, C.POINTER(i32), i32]),
@@ -185,6 +187,10 @@ def mtx_set_graph_replay(handle, enable: bool):
 
 def mtx_set_overlap(handle, enable: bool):
     _check(lib().mtx_set_overlap(handle, 1 if enable else 0))
+
+
+def mtx_set_layerwise_update(handle, enable: bool):
+    _check(lib().mtx_set_layerwise_update(handle, 1 if enable else 0))
 
 
 def mtx_set_timing(handle, enable: bool):

@@ -197,17 +197,23 @@ def test_graph_replay_matches_direct_launches(name):
     b.close()
 
 
-@pytest.mark.parametrize("name", ["lenet", "tiny", "alexnet"])
-def test_overlapped_weight_gradients_match_one_stream(name):
-    """Weight gradients on the second stream give bit-identical results to the one-stream
-    order, over several graph-replayed and direct steps."""
-    net = {"lenet": wl.LENET, "tiny": _tiny(wl.BF16), "alexnet": wl.ALEXNET}[name]
+@pytest.mark.parametrize("name,layerwise", [("lenet", False), ("tiny", False), ("tiny", True),
+                                            ("cifar", True), ("alexnet", False),
+                                            ("alexnet", True)])
+def test_overlapped_weight_gradients_match_one_stream(name, layerwise):
+    """Weight gradients on the second stream (and, with layerwise, each layer's average + update
+    on a third stream as soon as its gradients are written) give bit-identical results to the
+    one-stream order with one average + update at the end, over several graph-replayed and
+    direct steps."""
+    net = {"lenet": wl.LENET, "tiny": _tiny(wl.BF16), "cifar": wl.CIFAR,
+           "alexnet": wl.ALEXNET}[name]
     layers = wl.layer_tuples(net)
-    R, Nb = {"lenet": (4, 16), "tiny": (3, 5), "alexnet": (2, 2)}[name]
-    _say(f"[case] overlap vs one stream {name}")
+    R, Nb = {"lenet": (4, 16), "tiny": (3, 5), "cifar": (2, 2), "alexnet": (2, 2)}[name]
+    _say(f"[case] overlap vs one stream {name} layerwise={layerwise}")
     a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=4)
     b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=4)
     mtx.mtx_set_overlap(a.handle, True)
+    mtx.mtx_set_layerwise_update(a.handle, layerwise)
     mtx.mtx_set_graph_replay(a.handle, True)
     mtx.mtx_set_overlap(b.handle, False)
     x, y = wl.make_batch(net, R * Nb, seed=4)
@@ -223,5 +229,34 @@ def test_overlapped_weight_gradients_match_one_stream(name):
         wb, vb = b.get_params()
         assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
         assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
+        ga, gb = a.grad_avg.cpu().numpy(), b.grad_avg.cpu().numpy()
+        assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
+    a.close()
+    b.close()
+
+
+def test_layerwise_update_on_one_stream_matches():
+    """Layer-wise updates without the second stream (weight gradients on the caller's stream,
+    each layer's update on the third) match the plain order bit for bit."""
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    _say("[case] layerwise update, one weight-gradient stream")
+    a = mtx.Model(net.in_shape, layers, net.dtype, 4, 8, seed=5)
+    b = mtx.Model(net.in_shape, layers, net.dtype, 4, 8, seed=5)
+    mtx.mtx_set_overlap(a.handle, False)
+    mtx.mtx_set_layerwise_update(a.handle, True)
+    mtx.mtx_set_overlap(b.handle, False)
+    x, y = wl.make_batch(net, 32, seed=5)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    for step in range(2):
+        a.train_step(xd, yd, 0.01, 0.9)
+        b.train_step(xd, yd, 0.01, 0.9)
+        torch.cuda.synchronize()
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
+        ga, gb = a.grad_avg.cpu().numpy(), b.grad_avg.cpu().numpy()
+        assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
     a.close()
     b.close()

@@ -13,7 +13,9 @@ kernel that takes the most time in the step, timed in place with HIP events on t
 stream (its `traffic` comes from a committed rocprofv3 counter summary of the same kernel
 sources, else null); `grad_avg_update` is the fused average + momentum kernel at the
 61M-element, 16-buffer size; `other_workloads` are short runs of the bf16 CIFAR and AlexNet
-workloads; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same workload.
+workloads; `shard_sweep` is samples/s of the same workload at the same global batch for shard
+counts R = 1 .. 16; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same
+workload.
 """
 from __future__ import annotations
 
@@ -108,6 +110,41 @@ def wkl_params(wkl):
         d = mtx.make_desc(wkl.net.in_shape, wl.layer_tuples(wkl.net), wkl.net.dtype)
         _P[key] = mtx.mtx_model_sizes(d, wkl.shards, wkl.shard_batch)[0]
     return _P[key]
+
+
+def shard_sweep(torch, mtx, wl, name, shard_counts=(1, 2, 4, 8, 16), steps=20, warmup=3):
+    """Samples/s of one workload at a fixed global batch over several shard counts R (the
+    paper's strong scaling, Sec. IV, with the R replicas on one GPU): each point is a whole
+    training step (R shard gradients, their average and the update)."""
+    import dataclasses
+    base = wl.WORKLOADS[name]
+    net = base.net
+    layers = wl.layer_tuples(net)
+    x, y = wl.make_batch(net, base.batch, seed=0)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    stream = torch.cuda.current_stream()
+    points = []
+    for R in shard_counts:
+        if base.batch % R:
+            continue
+        wkl = dataclasses.replace(base, shards=R)
+        model = mtx.Model(net.in_shape, layers, net.dtype, R, wkl.shard_batch, seed=0)
+        for _ in range(warmup):
+            model.train_step(xd, yd, wkl.lr, wkl.momentum, None, stream)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(steps):
+            model.train_step(xd, yd, wkl.lr, wkl.momentum, None, stream)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / steps
+        model.close()
+        points.append({"R": R, "shard_batch": wkl.shard_batch, "ms_per_step": round(ms, 5),
+                       "samples_per_s": round(base.batch / (ms * 1e-3), 1)})
+    return {"workload": base.description.split(",")[0], "global_batch": base.batch,
+            "points": points}
 
 
 def microbench_avg_update(torch, mtx, reps=20):
@@ -352,6 +389,8 @@ def main():
                            "step_avg_update": e["step_avg_update"]}
             torch.cuda.empty_cache()
         out["other_workloads"] = extra
+    if not args.no_extra:
+        out["shard_sweep"] = shard_sweep(torch, mtx, wl, args.workload)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wkl)
     print(json.dumps(out), flush=True)

@@ -260,3 +260,31 @@ def test_layerwise_update_on_one_stream_matches():
         assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
     a.close()
     b.close()
+
+
+@pytest.mark.parametrize("net_name", ["lenet", "cifar"])
+def test_shard_count_invariance(net_name):
+    """Synchronous SGD does not depend on how the batch is split (Sec. III-E): three steps on
+    the same batches with R = 1, 2, 4, 8 shards give the same weight change up to rounding (the
+    averages of shard means are summed in another order)."""
+    net = {"lenet": wl.LENET, "cifar": wl.CIFAR}[net_name]
+    layers = wl.layer_tuples(net)
+    B = 16
+    tol = parity.TOL[net.dtype]
+    _say(f"[case] shard-count invariance {net_name}")
+    deltas = {}
+    for R in (1, 2, 4, 8):
+        m = mtx.Model(net.in_shape, layers, net.dtype, R, B // R, seed=11)
+        w0, _ = m.get_params()
+        for step in range(3):
+            x, y = wl.make_batch(net, B, seed=100 + step)
+            m.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), 0.01, 0.9)
+        torch.cuda.synchronize()
+        w3, _ = m.get_params()
+        deltas[R] = w3.astype(np.float64) - w0.astype(np.float64)
+        m.close()
+    ref = deltas[1]
+    for R in (2, 4, 8):
+        d = deltas[R]
+        assert np.linalg.norm(d - ref) <= tol * np.linalg.norm(ref), R
+        assert np.max(np.abs(d - ref)) <= tol * np.max(np.abs(ref)) + 1e-7, R

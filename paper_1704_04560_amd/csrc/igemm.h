@@ -424,13 +424,17 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_SK, BR, B
     }
 };
 
+// SR: a thread keeps one row for the whole kernel and loads VEC consecutive k of it per pass
+// (scalar loads; neighbouring threads read neighbouring rows, so each load instruction is
+// contiguous), then stores them with one 16-byte LDS store.
 template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_SR, BR, BK> {
     typedef typename Op::TT T;
     static constexpr int VEC = 16 / sizeof(T);
-    static constexpr int KPP = 256 / BR;  // k per pass
+    static constexpr int GP = 256 / BR;   // k groups per pass
+    static constexpr int KPP = GP * VEC;  // k per pass
     static constexpr int N = (BK + KPP - 1) / KPP;
     typename LState<Op, ISP, L_SR>::type s;
-    T reg[N];
+    T reg[N][VEC];
     __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
     {
         if constexpr (ISP) s = Op::pr(a, c, r0 + tid % BR);
@@ -439,19 +443,26 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_SR, BR, B
     __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
                                          int, int k0)
     {
-        const int k = k0 + tid / BR;
+        const int kg = (tid / BR) * VEC;
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            if constexpr (ISP) reg[i] = Op::p_sr(a, B, c, s, k + i * KPP);
-            else reg[i] = Op::q_sr(a, B, c, s, k + i * KPP);
+            if (!(KPP * N <= BK || kg + i * KPP < BK)) continue;  // idle beyond the tile
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const int k = k0 + kg + i * KPP + e;
+                if constexpr (ISP) reg[i][e] = Op::p_sr(a, B, c, s, k);
+                else reg[i][e] = Op::q_sr(a, B, c, s, k);
+            }
         }
     }
     __device__ __forceinline__ void stage(T* lds, int tid) const
     {
-        const int row = tid % BR, kk = tid / BR;
+        const int row = tid % BR, kg = (tid / BR) * VEC;
 #pragma unroll
         for (int i = 0; i < N; ++i)
-            if (KPP * N <= BK || kk + i * KPP < BK) lds[Lds<BK, VEC>::at(row, kk + i * KPP)] = reg[i];
+            if (KPP * N <= BK || kg + i * KPP < BK)
+                *reinterpret_cast<u32x4*>(&lds[Lds<BK, VEC>::at(row, kg + i * KPP)]) =
+                    *reinterpret_cast<const u32x4*>(reg[i]);
     }
 };
 

@@ -11,19 +11,22 @@
 // Fragment output layout: lane l, register v -> row 4*(l/16) + v, column l%16, so each lane
 // ends with four consecutive rows p of one column q.
 //
-// LDS tiles hold BR rows x BK reduction steps, k contiguous, rows padded by 32 bytes, and the
-// 16-byte granules of row r rotated by r/16.  Measured on gfx950 (LDS bank-conflict counters
-// over the exact access patterns of this kernel): fragment reads run at the full 256 bytes per
-// clock, 16-byte tile writes at the write rate, and the transposing writes at 1-2x the minimum
-// instead of up to 16x without the rotation; 16 bytes of padding would halve the read rate.
+// Register-staged k-contiguous LDS tiles hold BR rows x BK reduction steps, rows padded by 32
+// bytes, and the 16-byte granules of row r rotated by r/16.  Measured on gfx950 (LDS
+// bank-conflict counters over the exact access patterns of this kernel): fragment reads run at
+// the full 256 bytes per clock and 16-byte tile writes at the write rate; 16 bytes of padding
+// would halve the read rate.  Direct (KD) and k-major (RT) tiles have layouts of their own,
+// described with them.
 //
 // Operand loaders (per operand, chosen by the operation and the alignment of its tensor):
 //   SK  scalar, k-fast: a thread keeps one k per tile and steps over rows;
-//   SR  scalar, row-fast: a thread keeps one row for the whole kernel and steps over k;
-//   KV  16 bytes along k (one LDS store per load);
-//   RV  16 bytes along the rows (weight-gradient operands, whose reduction index is the
-//       position): the chunk is transposed on its way into LDS (bf16: two loads at k, k+1 are
-//       packed so that every LDS store writes a k pair).
+//   SR  scalar, row-fast: a thread keeps one row for the whole kernel and loads VEC
+//       consecutive k of it per pass (one 16-byte LDS store);
+//   KV  16 bytes along k through registers (one LDS store per load);
+//   KD  16 bytes along k straight into LDS (fp32);
+//   RT  16 bytes along the rows (weight-gradient operands, whose reduction index is the
+//       position), stored as loaded into a k-major tile; bf16 fragments come back through the
+//       transposing LDS read, fp32 ones as four 4-byte reads.
 // All global reads are raw buffer loads: the resource holds the tensor's size and the hardware
 // returns 0 past it, so zero padding, tile tails and invalid rows only select an out-of-range
 // offset, without branches.
@@ -267,7 +270,7 @@ template <int BK, int VEC> struct Lds {
 };
 
 // ---- operand loaders --------------------------------------------------------------------------
-enum { L_SK = 0, L_SR = 1, L_KV = 2, L_RV = 3, L_KD = 4, L_RT = 5 };
+enum { L_SK = 0, L_SR = 1, L_KV = 2, L_KD = 4, L_RT = 5 };
 
 // ---- direct loads (KD): 16 bytes along k from global memory straight into LDS -----------------
 // buffer_load_dwordx4 with the LDS flag: lane l of a wave writes LDS bytes [16 l, 16 l + 16) after
@@ -370,8 +373,31 @@ template <int BR, int BK, int VEC> struct TileOf<L_KD, BR, BK, VEC> {
     typedef LdsD<BK, VEC> L;
     static constexpr int ELEMS = BR * BK;
 };
+// fp32 k-major tile: the MFMA takes one value per lane and instruction, so a fragment is four
+// 4-byte reads (k = 4 lg + t for the t-th instruction) and no transposing load is needed.  The
+// 64-byte units (16 rows) of k-row k sit at unit u ^ (((k >> 2) & 3) mod units), which puts the
+// four k-rows a read touches (k, k+4, k+8, k+12) on distinct bank slots for 64 rows or more.
+template <int BR, int BK> struct LdsT32 {
+    static constexpr int NU = BR / 16;  // 64-byte units per k-row
+    static_assert(NU == 2 || NU == 4 || NU == 8, "k-major tile rows");
+    __device__ __forceinline__ static int sw(int k) { return ((k >> 2) & 3) & (NU - 1); }
+    __device__ __forceinline__ static int at(int k, int row)
+    {
+        return k * BR + ((((row >> 4) ^ sw(k)) << 4) | (row & 15));
+    }
+    template <typename F, typename T>
+    __device__ __forceinline__ static F frag(const T* t, int rb, int lr, int lg, int kc, int ks)
+    {
+        static_assert(sizeof(T) == 4, "fp32 k-major tile");
+        F f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) f[u] = t[at(kc * ks + 4 * lg + u, rb + lr)];
+        return f;
+    }
+};
+
 template <int BR, int BK, int VEC> struct TileOf<L_RT, BR, BK, VEC> {
-    typedef LdsT<BR, BK> L;
+    typedef std::conditional_t<VEC == 8, LdsT<BR, BK>, LdsT32<BR, BK>> L;
     static constexpr int ELEMS = BR * BK;
 };
 
@@ -382,12 +408,10 @@ template <class Op> struct LState<Op, true, L_SR> { typedef typename Op::PR type
 template <class Op> struct LState<Op, true, L_KV> { typedef typename Op::PV type; };
 template <class Op> struct LState<Op, true, L_KD> { typedef typename Op::PV type; };
 template <class Op> struct LState<Op, false, L_KD> { typedef typename Op::QV type; };
-template <class Op> struct LState<Op, true, L_RV> { typedef typename Op::PC type; };
 template <class Op> struct LState<Op, true, L_RT> { typedef typename Op::PC type; };
 template <class Op> struct LState<Op, false, L_RT> { typedef typename Op::QC type; };
 template <class Op> struct LState<Op, false, L_SR> { typedef typename Op::QR type; };
 template <class Op> struct LState<Op, false, L_KV> { typedef typename Op::QV type; };
-template <class Op> struct LState<Op, false, L_RV> { typedef typename Op::QC type; };
 
 template <class Op, bool ISP, int KIND, int BR, int BK> struct Loader;
 
@@ -505,71 +529,15 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KV, BR, B
     }
 };
 
-template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RV, BR, BK> {
-    typedef typename Op::TT T;
-    static constexpr int VEC = 16 / sizeof(T);
-    static constexpr int KW = sizeof(T) == 2 ? 2 : 1;  // k values per thread step
-    static constexpr int RCH = BR / VEC;                // row chunks per tile
-    static constexpr int KPP = (256 / RCH) * KW;        // k per pass
-    static constexpr int N = (BK + KPP - 1) / KPP;
-    static_assert(BR % VEC == 0 && 256 % RCH == 0, "RV tile");
-    typename LState<Op, ISP, L_RV>::type s;
-    u32x4 reg[N][KW];
-    __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)
-    {
-        const int row0 = r0 + (tid % RCH) * VEC;
-        if constexpr (ISP) s = Op::pc(a, c, row0);
-        else s = Op::qc(a, c, row0);
-    }
-    __device__ __forceinline__ void load(const GemmArgs& a, const Buf<T>& B, const Ctx& c, int tid,
-                                         int, int k0)
-    {
-        const int kt = (tid / RCH) * KW;
-#pragma unroll
-        for (int i = 0; i < N; ++i) {
-            if (!(KPP * N <= BK || kt + i * KPP < BK)) continue;  // idle beyond the tile
-#pragma unroll
-            for (int w = 0; w < KW; ++w) {
-                const int k = k0 + kt + i * KPP + w;
-                if constexpr (ISP) reg[i][w] = Op::p_rv(a, B, c, s, k);
-                else reg[i][w] = Op::q_rv(a, B, c, s, k);
-            }
-        }
-    }
-    __device__ __forceinline__ void stage(T* lds, int tid) const
-    {
-        typedef Lds<BK, VEC> L;
-        const int row0 = (tid % RCH) * VEC, kk = (tid / RCH) * KW;
-#pragma unroll
-        for (int i = 0; i < N; ++i) {
-            const int kb = kk + i * KPP;
-            if (!(KPP * N <= BK || kb < BK)) continue;
-            if constexpr (KW == 1) {
-#pragma unroll
-                for (int j = 0; j < VEC; ++j)
-                    reinterpret_cast<unsigned*>(lds)[L::at(row0 + j, kb)] = reg[i][0][j];
-            } else {
-#pragma unroll
-                for (int j = 0; j < VEC; ++j) {
-                    const unsigned w0 = reg[i][0][j >> 1], w1 = reg[i][1][j >> 1];
-                    const unsigned pr = (j & 1) ? ((w0 >> 16) | (w1 & 0xffff0000u))
-                                                : ((w0 & 0xffffu) | (w1 << 16));
-                    *reinterpret_cast<unsigned*>(&lds[L::at(row0 + j, kb)]) = pr;
-                }
-            }
-        }
-    }
-};
-
-// RT: 16 bytes along the rows (8 rows at one k), stored as loaded into the k-major tile.
+// RT: 16 bytes along the rows (VEC rows at one k), stored as loaded into the k-major tile.
 template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_RT, BR, BK> {
     typedef typename Op::TT T;
     static constexpr int VEC = 16 / sizeof(T);
     static constexpr int RCH = BR / VEC;  // row chunks per tile
     static constexpr int KPP = 256 / RCH;  // k per pass
     static constexpr int N = (BK + KPP - 1) / KPP;
-    static_assert(sizeof(T) == 2 && BR % VEC == 0 && 256 % RCH == 0, "RT tile");
-    typedef LdsT<BR, BK> L;
+    static_assert(BR % VEC == 0 && 256 % RCH == 0, "RT tile");
+    typedef typename TileOf<L_RT, BR, BK, VEC>::L L;
     typename LState<Op, ISP, L_RT>::type s;
     u32x4 reg[N];
     __device__ __forceinline__ void init(const GemmArgs& a, const Ctx& c, int tid, int r0)

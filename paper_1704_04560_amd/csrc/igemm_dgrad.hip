@@ -139,8 +139,8 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
     const bool pv = IN % vec_elems(dt) == 0, qv = OUT % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef FcDgrad<float> Op;
-        if (pv && qv) return run_gemm<Op, L_RV, L_KD>(a, p, d.Z, partial, s);
-        if (pv) return run_gemm<Op, L_RV, L_SK>(a, p, d.Z, partial, s);
+        if (pv && qv) return run_gemm<Op, L_RT, L_KD>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RT, L_SK>(a, p, d.Z, partial, s);
         if (qv) return run_gemm<Op, L_SR, L_KD>(a, p, d.Z, partial, s);
         return run_gemm<Op, L_SR, L_SK>(a, p, d.Z, partial, s);
     }

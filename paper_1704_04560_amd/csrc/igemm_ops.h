@@ -10,7 +10,7 @@
 //   pr/p_sr           SR loader on P: state for row p, element at k
 //   pv/p_kv           KV and KD loaders on P: state for row p, 16 bytes at k (B.at16 on the
 //                     buffer given: a register load, or a load straight into LDS)
-//   pc/p_rv           RV loader on P: state for rows p0..p0+VEC-1, 16 bytes at k
+//   pc/p_rv           RT loader on P: state for rows p0..p0+VEC-1, 16 bytes at k
 //   qk/q_sk, qr/q_sr, qv/q_kv, qc/q_rv   the same for Q
 //   store4(a, c, p, q, acc, np)   epilogue for rows p..p+np-1 of column q
 #pragma once

@@ -20,9 +20,9 @@ hipError_t conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void
     const bool pv = a.og % vec_elems(dt) == 0, qv = a.cg % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef ConvWgrad<float> Op;
-        if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-        if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
-        if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+        if (pv && qv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RT, L_SR>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
         return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
     }
     typedef ConvWgrad<bf16_t> Op;
@@ -51,8 +51,8 @@ hipError_t conv_wgrad_run(Dt dt, const ConvGeom& g, const RunGeom& r, int R, con
     const bool pv = g.OC % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef ConvWgradRun<float> Op;
-        if (pv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-        return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+        return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
     }
     typedef ConvWgradRun<bf16_t> Op;
     if (pv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
@@ -77,9 +77,9 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
     const bool pv = IN % vec_elems(dt) == 0 && !perm, qv = OUT % vec_elems(dt) == 0;
     if (dt == DT_F32) {
         typedef FcWgrad<float> Op;
-        if (pv && qv) return run_gemm<Op, L_RV, L_RV>(a, p, d.Z, partial, s);
-        if (pv) return run_gemm<Op, L_RV, L_SR>(a, p, d.Z, partial, s);
-        if (qv) return run_gemm<Op, L_SR, L_RV>(a, p, d.Z, partial, s);
+        if (pv && qv) return run_gemm<Op, L_RT, L_RT>(a, p, d.Z, partial, s);
+        if (pv) return run_gemm<Op, L_RT, L_SR>(a, p, d.Z, partial, s);
+        if (qv) return run_gemm<Op, L_SR, L_RT>(a, p, d.Z, partial, s);
         return run_gemm<Op, L_SR, L_SR>(a, p, d.Z, partial, s);
     }
     typedef FcWgrad<bf16_t> Op;

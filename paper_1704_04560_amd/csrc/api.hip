@@ -67,6 +67,9 @@ struct LayerPlan {
 };
 
 constexpr size_t kNone = ~(size_t)0;
+// blocks of a layer-wise update (it runs beside the backward kernels: a capped grid leaves them
+// most of the compute units)
+constexpr unsigned kLayerUpdateBlocks = 256;
 
 struct Plan {
     int R = 0, Nb = 0, B = 0, dt = 0;
@@ -810,7 +813,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     // output gradient and input, so (unless kernels are being timed) it runs on the second
     // stream, forked after its output gradient is written and joined before the update.
     const bool overlap = m->overlap && !m->timer.on;
-    const bool layerwise = m->layerwise && !m->timer.on;
+    const bool layerwise = m->layerwise && m->upd && !m->timer.on;
     float* partial_w = overlap ? reinterpret_cast<float*>(ws + pl.partial_w_off) : partial;
     const long long ld = (long long)pl.ld;
     int nfork = 0, nlayer = 0;
@@ -880,7 +883,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             HIP_TRY(launch_site(m, "avg_update", l, m->upd, [&] {
                         return average_update(m->grads + off, pl.R, len, pl.ld, m->w + off,
                                               m->v + off, lr, momentum, m->gavg + off, true,
-                                              m->upd);
+                                              m->upd, kLayerUpdateBlocks);
                     }), "layer average + update");
         }
     }

@@ -782,14 +782,14 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
                                                        float* __restrict__ v, float lr, float mu,
                                                        float* __restrict__ avg)
 {
-    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
     const long long n4 = n / 4;
     const int R = RT > 0 ? RT : Rrt;
-    if (t >= n4) {
-        if (t == n4)
-            for (long long i = 4 * n4; i < n; ++i)
-                avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
-        return;
+    for (long long t = (long long)blockIdx.x * 256 + threadIdx.x; t <= n4;
+         t += (long long)gridDim.x * 256) {
+    if (t == n4) {
+        for (long long i = 4 * n4; i < n; ++i)
+            avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
+        break;
     }
     const f32x4* g4 = reinterpret_cast<const f32x4*>(grads) + t;
     const long long ld4 = ld / 4;
@@ -819,6 +819,7 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
         for (int j = 0; j < 4; ++j) wv[j] = fmaf(-lr, g[j], wv[j]);
         reinterpret_cast<f32x4*>(w)[t] = wv;
     }
+    }
 }
 
 template <bool MOM, bool AVG, bool UPD>
@@ -835,7 +836,8 @@ __global__ __launch_bounds__(256) void avg_update_scalar(const float* __restrict
 
 template <bool MOM, bool AVG, bool UPD>
 static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t ld, float* w,
-                                    float* v, float lr, float mu, float* avg, hipStream_t s)
+                                    float* v, float lr, float mu, float* avg, unsigned max_blocks,
+                                    hipStream_t s)
 {
     auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
     const bool vec = (ld % 4 == 0) && al(grads) && (!AVG || al(avg)) && (!UPD || al(w)) &&
@@ -843,6 +845,7 @@ static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t 
     if (vec) {
         const long long nn = (long long)n;
         dim3 grid(grid_for(n / 4 + 1, 256));
+        if (max_blocks && grid.x > max_blocks) grid.x = max_blocks;
         switch (R) {
         case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
         case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
@@ -859,17 +862,18 @@ static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t 
 }
 
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
-                          float lr, float mu, float* avg, bool update, hipStream_t s)
+                          float lr, float mu, float* avg, bool update, hipStream_t s,
+                          unsigned max_blocks)
 {
     const bool mom = update && mu != 0.0f;
     const bool wavg = avg != nullptr;
-    if (!update) return avg_update_launch<false, true, false>(grads, R, n, ld, w, v, lr, mu, avg, s);
+    if (!update) return avg_update_launch<false, true, false>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
     if (mom) {
-        if (wavg) return avg_update_launch<true, true, true>(grads, R, n, ld, w, v, lr, mu, avg, s);
-        return avg_update_launch<true, false, true>(grads, R, n, ld, w, v, lr, mu, avg, s);
+        if (wavg) return avg_update_launch<true, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
+        return avg_update_launch<true, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
     }
-    if (wavg) return avg_update_launch<false, true, true>(grads, R, n, ld, w, v, lr, mu, avg, s);
-    return avg_update_launch<false, false, true>(grads, R, n, ld, w, v, lr, mu, avg, s);
+    if (wavg) return avg_update_launch<false, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
+    return avg_update_launch<false, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
 }
 
 }  // namespace mtx

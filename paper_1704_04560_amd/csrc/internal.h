@@ -187,7 +187,10 @@ hipError_t pool_bwd(Dt dt, int N, int C, int H, int W, int K, int S, bool dy_nch
 hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
                         const int32_t* labels, void* dz, float* block_sums, unsigned* sync,
                         float* loss_out, hipStream_t s);
+// max_blocks > 0 caps the grid (the kernel strides over the range), so that an update running
+// beside other kernels occupies only part of the GPU.
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
-                          float lr, float mu, float* avg, bool update, hipStream_t s);
+                          float lr, float mu, float* avg, bool update, hipStream_t s,
+                          unsigned max_blocks = 0);
 
 }  // namespace mtx

@@ -145,7 +145,7 @@ hipError_t to_nhwc_padded(Dt dt, const float* x, void* dst, int N, int C, int H,
 // converts kPrepPerBlock consecutive destination elements.  The source index of a destination
 // element follows from its layout (see PrepKind).
 
-constexpr int kPrepPerThread = 16, kPrepPerBlock = 256 * kPrepPerThread;
+constexpr int kPrepPerThread = 8, kPrepPerBlock = 256 * kPrepPerThread;
 
 int prep_blocks(int n) { return (n + kPrepPerBlock - 1) / kPrepPerBlock; }
 
@@ -227,23 +227,38 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepJob* __restrict__ j
     const PrepJob j = jobs[jx];
     const float* src = w + j.src;
     T* out = dst + j.dst;  // 16-byte aligned
-    if (j.kind == PREP_CAST && ((uintptr_t)src & 15) == 0) {
-        // plain conversion: 8 consecutive elements per thread and step, 16-byte accesses
-        const int b0 = ((int)blockIdx.x - j.block0) * kPrepPerBlock;
-#pragma unroll
-        for (int e = 0; e < kPrepPerThread / 8; ++e) {
-            const int d = b0 + (e * 256 + (int)threadIdx.x) * 8;
-            if (d + 8 <= j.n) {
+    if (j.kind == PREP_CAST) {
+        // plain conversion: 8 consecutive elements per thread, read 16 or 8 bytes at a time as
+        // the source's alignment allows (a layer's weights start anywhere in the flat vector),
+        // written with 16-byte stores
+        static_assert(kPrepPerThread == 8, "cast step");
+        const int d = ((int)blockIdx.x - j.block0) * kPrepPerBlock + (int)threadIdx.x * 8;
+        if (d + 8 <= j.n) {
+            float f[8];
+            if (((uintptr_t)src & 15) == 0) {
                 const float4 lo = *reinterpret_cast<const float4*>(src + d);
                 const float4 hi = *reinterpret_cast<const float4*>(src + d + 4);
-                T v[8] = {from_f32<T>(lo.x), from_f32<T>(lo.y), from_f32<T>(lo.z), from_f32<T>(lo.w),
-                          from_f32<T>(hi.x), from_f32<T>(hi.y), from_f32<T>(hi.z), from_f32<T>(hi.w)};
-                uint4* o = reinterpret_cast<uint4*>(out + d);
-                o[0] = reinterpret_cast<const uint4*>(v)[0];
-                if constexpr (sizeof(T) == 4) o[1] = reinterpret_cast<const uint4*>(v)[1];
+                f[0] = lo.x; f[1] = lo.y; f[2] = lo.z; f[3] = lo.w;
+                f[4] = hi.x; f[5] = hi.y; f[6] = hi.z; f[7] = hi.w;
+            } else if (((uintptr_t)src & 7) == 0) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float2 t = *reinterpret_cast<const float2*>(src + d + 2 * i);
+                    f[2 * i] = t.x;
+                    f[2 * i + 1] = t.y;
+                }
             } else {
-                for (int i = d; i < j.n; ++i) out[i] = from_f32<T>(src[i]);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) f[i] = src[d + i];
             }
+            T v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = from_f32<T>(f[i]);
+            uint4* o = reinterpret_cast<uint4*>(out + d);
+            o[0] = reinterpret_cast<const uint4*>(v)[0];
+            if constexpr (sizeof(T) == 4) o[1] = reinterpret_cast<const uint4*>(v)[1];
+        } else {
+            for (int i = d; i < j.n; ++i) out[i] = from_f32<T>(src[i]);
         }
         return;
     }

@@ -16,6 +16,8 @@
  *   - Sec. III-D.2 and Sec. III-E: the result is equivalent to the sequential SGD step.  The
  *     optimizer is the momentum method the paper lists among TensorFlow's optimizers (Sec. I):
  *     v <- mu*v + g, w <- w - lr*v (TensorFlow 1.0 MomentumOptimizer form); mu == 0 is plain SGD.
+ *     The two other update rules Sec. I names, AdaGrad and Adam, follow the averaged gradient in
+ *     orc_average_adagrad / orc_average_adam, each as defined in the work the paper cites.
  *   - Sec. III-D.1 (Broadcast operator): replicas start identical.  Here every replica reads the
  *     one weight vector, which is that property by construction.
  *   - Fig. 1 (AlexNet: convolution + fully connected layers) and Sec. I (MLP / CNN): the layer
@@ -713,6 +715,56 @@ int orc_average_update(const float* grads, int R, long n, long ld, float* w, flo
         } else {
             w[i] = (float)((double)w[i] - (double)lr * (double)gi);
         }
+    }
+    return ORC_OK;
+}
+
+/* The same average followed by the other update rules that Sec. I lists among TensorFlow's
+ * gradient-descent improvements.  The paper gives no formula for them; each is the definition
+ * in the work it cites.  Every state and weight is rounded to float once per step, as the
+ * step stores them; the arithmetic in between is double.
+ *
+ * Adam (Kingma and Ba, cited in Sec. I; Algorithm 1 of that work), at step t >= 1:
+ *   m <- b1*m + (1-b1)*g,  v <- b2*v + (1-b2)*g^2,
+ *   w <- w - lr * (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps).
+ * The constant eps is added to the square root of the bias-corrected second moment, as in
+ * that algorithm (TensorFlow's own kernel adds it before the bias correction instead). */
+int orc_average_adam(const float* grads, int R, long n, long ld, float* w, float* m, float* v,
+                     float lr, float b1, float b2, float eps, long step, float* gavg)
+{
+    if (!grads || !w || !m || !v || R < 1 || n < 1 || ld < n || step < 1) return ORC_EINVAL;
+    const double bc1 = 1.0 - pow((double)b1, (double)step);
+    const double bc2 = 1.0 - pow((double)b2, (double)step);
+    for (long i = 0; i < n; i++) {
+        double s = 0.0;
+        for (int r = 0; r < R; r++) s += (double)grads[(long)r * ld + i];
+        const double g = (double)(float)(s / R);
+        if (gavg) gavg[i] = (float)g;
+        const double mi = (double)(float)((double)b1 * m[i] + (1.0 - (double)b1) * g);
+        const double vi = (double)(float)((double)b2 * v[i] + (1.0 - (double)b2) * g * g);
+        m[i] = (float)mi;
+        v[i] = (float)vi;
+        const double mhat = mi / bc1, vhat = vi / bc2;
+        w[i] = (float)((double)w[i] - (double)lr * mhat / (sqrt(vhat) + (double)eps));
+    }
+    return ORC_OK;
+}
+
+/* AdaGrad (Duchi, Hazan and Singer, cited in Sec. I), diagonal form with the accumulated sum of
+ * squared gradients G (its initial value is whatever acc holds, zero for a fresh start):
+ *   G <- G + g^2,  w <- w - lr * g / (sqrt(G) + eps). */
+int orc_average_adagrad(const float* grads, int R, long n, long ld, float* w, float* acc,
+                        float lr, float eps, float* gavg)
+{
+    if (!grads || !w || !acc || R < 1 || n < 1 || ld < n) return ORC_EINVAL;
+    for (long i = 0; i < n; i++) {
+        double s = 0.0;
+        for (int r = 0; r < R; r++) s += (double)grads[(long)r * ld + i];
+        const double g = (double)(float)(s / R);
+        if (gavg) gavg[i] = (float)g;
+        const double G = (double)(float)((double)acc[i] + g * g);
+        acc[i] = (float)G;
+        w[i] = (float)((double)w[i] - (double)lr * g / (sqrt(G) + (double)eps));
     }
     return ORC_OK;
 }

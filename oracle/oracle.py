@@ -269,3 +269,34 @@ def average_update(grads, w, v, lr, mu, n=None):
     if rc:
         raise RuntimeError(f"orc_average_update rc={rc}")
     return gavg, w2, v2
+
+
+def average_adam(grads, w, m, v, lr, b1, b2, eps, step, n=None):
+    """Average of the rows of grads (R x ld, first n columns) followed by one Adam step number
+    `step` (>= 1).  Returns (gavg, w_new, m_new, v_new)."""
+    grads = np.ascontiguousarray(grads, dtype=np.float32)
+    R, ld = grads.shape
+    n = ld if n is None else n
+    w2, m2, v2 = (np.array(a, dtype=np.float32, copy=True) for a in (w, m, v))
+    gavg = np.empty(n, dtype=np.float32)
+    rc = lib().orc_average_adam(_p(grads), C.c_int(R), C.c_long(n), C.c_long(ld), _p(w2),
+                                _p(m2), _p(v2), C.c_float(lr), C.c_float(b1), C.c_float(b2),
+                                C.c_float(eps), C.c_long(step), _p(gavg))
+    if rc:
+        raise RuntimeError(f"orc_average_adam rc={rc}")
+    return gavg, w2, m2, v2
+
+
+def average_adagrad(grads, w, acc, lr, eps, n=None):
+    """Average of the rows of grads followed by one AdaGrad step.  Returns
+    (gavg, w_new, acc_new)."""
+    grads = np.ascontiguousarray(grads, dtype=np.float32)
+    R, ld = grads.shape
+    n = ld if n is None else n
+    w2, a2 = (np.array(a, dtype=np.float32, copy=True) for a in (w, acc))
+    gavg = np.empty(n, dtype=np.float32)
+    rc = lib().orc_average_adagrad(_p(grads), C.c_int(R), C.c_long(n), C.c_long(ld), _p(w2),
+                                   _p(a2), C.c_float(lr), C.c_float(eps), _p(gavg))
+    if rc:
+        raise RuntimeError(f"orc_average_adagrad rc={rc}")
+    return gavg, w2, a2

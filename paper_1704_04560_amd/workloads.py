@@ -16,7 +16,8 @@ Gradient-average microbenchmark: R=16 buffers of n elements, N(0, 1e-3) gradient
 weights, N(0, 1e-3) velocity, momentum 0.9, lr 0.01.
 
 Random streams: numpy.random.default_rng([seed, stream]) with stream 0 = input images,
-1 = labels, 2 = weights (when a test draws its own), 3 = velocity, 4 = gradient buffers.
+1 = labels, 2 = weights (when a test draws its own), 3 = velocity, 4 = gradient buffers,
+5 = second optimizer state (Adam's second moment, AdaGrad's accumulator).
 """
 from __future__ import annotations
 
@@ -28,7 +29,7 @@ import numpy as np
 FC, CONV, MAXPOOL = 0, 1, 2
 F32, BF16 = 0, 1
 
-STREAM_X, STREAM_LABELS, STREAM_W, STREAM_V, STREAM_G = 0, 1, 2, 3, 4
+STREAM_X, STREAM_LABELS, STREAM_W, STREAM_V, STREAM_G, STREAM_S2 = 0, 1, 2, 3, 4, 5
 
 
 @dataclass(frozen=True)
@@ -153,6 +154,13 @@ def make_avg_update_inputs(R: int, n: int, seed: int = 0, ld: int | None = None)
     w = rng(seed, STREAM_W).normal(0.0, spec["w_std"], size=n).astype(np.float32)
     v = rng(seed, STREAM_V).normal(0.0, spec["v_std"], size=n).astype(np.float32)
     return grads, w, v
+
+
+def make_square_state(n: int, seed: int = 0, terms: int = 1) -> np.ndarray:
+    """Non-negative state of the size a running sum or average of squared gradients takes:
+    the sum of `terms` squares of N(0, 1e-3) draws, as float32 [n]."""
+    z = rng(seed, STREAM_S2).normal(0.0, AVG_UPDATE["grad_std"], size=(terms, n))
+    return (z * z).sum(axis=0).astype(np.float32)
 
 
 def layer_tuples(net: Net) -> List[Tuple[int, int, int, int, int, int, int]]:

@@ -86,3 +86,116 @@ def test_bf16_rounding_matches_torch_and_ties_to_even():
     assert np.array_equal(orc.round_bf16(r), torch.tensor(r).to(torch.bfloat16).float().numpy())
     nan = orc.round_bf16(np.array([np.nan], np.float32))
     assert np.isnan(nan[0])
+
+
+# ---- Adam and AdaGrad (the update rules Sec. I names, as defined in the works it cites) --------
+
+def _exact_rows(n, R, seed, scale=1e-2):
+    """R identical rows of values with few significant bits, so that their average is exact."""
+    g = np.random.default_rng(seed).normal(0, scale, n)
+    g = (np.round(g * 2 ** 14) / 2 ** 14).astype(np.float32)
+    g[g == 0] = np.float32(2 ** -14)
+    return g, np.tile(g, (R, 1))
+
+
+def test_adam_matches_torch_optim_adam():
+    """Five steps with a fresh random gradient each step against torch.optim.Adam in float64
+    (Kingma and Ba's algorithm, the same placement of eps); the oracle keeps its state in float,
+    so the comparison allows float rounding of the states and the updates."""
+    R, n, lr, b1, b2, eps = 3, 513, 1e-3, 0.9, 0.999, 1e-8
+    rng = np.random.default_rng(5)
+    w0 = rng.normal(0, 0.05, n).astype(np.float32)
+    w, m, v = w0.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32)
+    p = torch.nn.Parameter(torch.tensor(w0, dtype=torch.float64))
+    f = lambda x: float(np.float32(x))  # the oracle takes its hyperparameters as float
+    opt = torch.optim.Adam([p], lr=f(lr), betas=(f(b1), f(b2)), eps=f(eps))
+    for t in range(1, 6):
+        grads = rng.normal(0, 1e-3, (R, n)).astype(np.float32)
+        gavg, w, m, v = orc.average_adam(grads, w, m, v, lr, b1, b2, eps, t)
+        assert np.allclose(gavg, grads.astype(np.float64).mean(0), rtol=1e-6, atol=1e-12)
+        p.grad = torch.tensor(gavg, dtype=torch.float64)
+        opt.step()
+    st = opt.state[p]
+    mr, vr = st["exp_avg"].numpy(), st["exp_avg_sq"].numpy()
+    # the float state carries one rounding of its running value per step
+    assert np.allclose(m, mr, rtol=1e-5, atol=1e-6 * np.abs(mr).max())
+    assert np.allclose(v, vr, rtol=1e-5, atol=1e-6 * vr.max())
+    dref = p.detach().numpy() - w0
+    assert np.allclose(w - w0, dref, rtol=1e-4, atol=1e-8)
+    assert np.abs(dref).max() > 1e-3  # the weights moved by several lr
+
+
+@pytest.mark.parametrize("b1,b2", [(0.9, 0.999), (0.5, 0.75), (0.0, 0.0)])
+def test_adam_constant_gradient_closed_form(b1, b2):
+    """With a constant gradient g and zero initial moments the bias-corrected moments are g and
+    g^2 at every step, so each step moves w by lr * g / (|g| + eps)."""
+    R, n, lr, eps, steps = 4, 300, 1e-3, 1e-8, 7
+    g, grads = _exact_rows(n, R, seed=2)
+    w0 = np.random.default_rng(3).normal(0, 1, n).astype(np.float32)
+    w, m, v = w0.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32)
+    for t in range(1, steps + 1):
+        gavg, w, m, v = orc.average_adam(grads, w, m, v, lr, b1, b2, eps, t)
+        assert np.array_equal(gavg, g)
+    g64 = g.astype(np.float64)
+    assert np.allclose(m, g64 * (1 - b1 ** steps), rtol=1e-6)
+    assert np.allclose(v, g64 * g64 * (1 - b2 ** steps), rtol=1e-6)
+    wk = w0 - steps * lr * g64 / (np.abs(g64) + eps)
+    assert np.allclose(w, wk, rtol=0, atol=steps * 1e-7 + 1e-6 * steps * lr)
+
+
+def test_adam_power_of_two_gradient_scale_leaves_update_unchanged():
+    """With eps = 0 the step m_hat / sqrt(v_hat) is invariant to scaling every gradient by a
+    power of two, bit for bit (the scaling commutes with every rounding)."""
+    R, n = 4, 1001
+    grads, w, _ = wl.make_avg_update_inputs(R, n, seed=8)
+    m0 = wl.make_velocity(n, seed=8)
+    v0 = wl.make_square_state(n, seed=8, terms=3)
+    out1 = orc.average_adam(grads, w, m0, v0, 1e-3, 0.9, 0.999, 0.0, 3)
+    out2 = orc.average_adam(grads * 8, w, m0 * 8, v0 * 64, 1e-3, 0.9, 0.999, 0.0, 3)
+    assert np.array_equal(out1[1], out2[1])
+    assert np.array_equal(out1[2] * 8, out2[2])
+    assert np.array_equal(out1[3] * 64, out2[3])
+    assert not np.array_equal(out1[1], w)
+
+
+def test_adagrad_matches_torch_optim_adagrad():
+    R, n, lr, eps = 2, 257, 0.05, 1e-10
+    rng = np.random.default_rng(11)
+    w0 = rng.normal(0, 0.05, n).astype(np.float32)
+    w, acc = w0.copy(), np.zeros(n, np.float32)
+    p = torch.nn.Parameter(torch.tensor(w0, dtype=torch.float64))
+    opt = torch.optim.Adagrad([p], lr=float(np.float32(lr)), eps=float(np.float32(eps)))
+    for _ in range(5):
+        grads = rng.normal(0, 1e-3, (R, n)).astype(np.float32)
+        gavg, w, acc = orc.average_adagrad(grads, w, acc, lr, eps)
+        p.grad = torch.tensor(gavg, dtype=torch.float64)
+        opt.step()
+    assert np.allclose(acc, opt.state[p]["sum"].numpy(), rtol=1e-5, atol=0)
+    dref = p.detach().numpy() - w0
+    assert np.allclose(w - w0, dref, rtol=1e-4, atol=1e-8)
+    assert np.abs(dref).max() > 0.05
+
+
+def test_adagrad_constant_gradient_closed_form():
+    """G_k = k g^2 from a zero accumulator, so step k moves w by lr g / (sqrt(k) |g| + eps)."""
+    R, n, lr, eps, steps = 3, 200, 0.01, 1e-6, 9
+    g, grads = _exact_rows(n, R, seed=4)
+    w0 = np.random.default_rng(5).normal(0, 1, n).astype(np.float32)
+    w, acc = w0.copy(), np.zeros(n, np.float32)
+    for _ in range(steps):
+        _, w, acc = orc.average_adagrad(grads, w, acc, lr, eps)
+    g64 = g.astype(np.float64)
+    assert np.allclose(acc, steps * g64 * g64, rtol=1e-6)
+    wk = w0 - lr * g64 * sum(1.0 / (np.sqrt(k) * np.abs(g64) + eps) for k in range(1, steps + 1))
+    assert np.allclose(w, wk, rtol=0, atol=steps * 1e-7 + 1e-5 * steps * lr)
+
+
+def test_adagrad_keeps_a_given_initial_accumulator():
+    """A non-zero starting accumulator (TensorFlow starts it at 0.1) enters the denominator."""
+    R, n, lr = 1, 64, 0.1
+    g, grads = _exact_rows(n, R, seed=6)
+    w0 = np.zeros(n, np.float32)
+    _, w, acc = orc.average_adagrad(grads, w0, np.full(n, 0.1, np.float32), lr, 0.0)
+    g64 = g.astype(np.float64)
+    assert np.allclose(acc, 0.1 + g64 * g64, rtol=1e-6)
+    assert np.allclose(w, -lr * g64 / np.sqrt(0.1 + g64 * g64), rtol=1e-6)

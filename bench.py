@@ -147,31 +147,57 @@ def shard_sweep(torch, mtx, wl, name, shard_counts=(1, 2, 4, 8, 16), steps=20, w
             "points": points}
 
 
-def microbench_avg_update(torch, mtx, reps=20):
-    """Fused average + momentum update over R=16 buffers of 61,000,000 fp32 elements."""
-    R, n = 16, 61_000_000
-    gen = torch.Generator(device="cuda").manual_seed(0)
-    grads = torch.randn(R * n, device="cuda", generator=gen) * 1e-3
-    w = torch.randn(n, device="cuda", generator=gen) * 0.05
-    v = torch.randn(n, device="cuda", generator=gen) * 1e-3
-    avg = torch.empty(n, device="cuda")
+def _time_calls(torch, fn, reps):
     for _ in range(3):
-        mtx.mtx_sgd_update(w, v, grads, R, n, n, 0.01, 0.9, avg)
+        fn()
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
     for _ in range(reps):
-        mtx.mtx_sgd_update(w, v, grads, R, n, n, 0.01, 0.9, avg)
+        fn()
     e.record()
     torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / reps
-    nbytes = (R + 5) * 4 * n
+    return s.elapsed_time(e) / reps
+
+
+def _rate(nbytes, ms):
     gbps = nbytes / (ms * 1e-3) / 1e9
-    del grads, w, v, avg
-    torch.cuda.empty_cache()
-    return {"R": R, "n": n, "bytes_per_call": nbytes, "ms": round(ms, 4),
-            "GBps": round(gbps, 1), "peak_GBps": PEAK["hbm_GBps"],
-            "frac": round(gbps / PEAK["hbm_GBps"], 4)}
+    return {"bytes_per_call": nbytes, "ms": round(ms, 4), "GBps": round(gbps, 1),
+            "peak_GBps": PEAK["hbm_GBps"], "frac": round(gbps / PEAK["hbm_GBps"], 4)}
+
+
+def microbench_avg_update(torch, mtx, reps=20):
+    """Fused average + update over R=16 flattened fp32 gradient buffers: the momentum update at
+    n = 61,000,000 and 250,000,000 elements, and Adam / AdaGrad after the same average at
+    n = 61,000,000.  Bytes per element: (R + 5) * 4 for momentum (R grads, w and v read; the
+    average, w and v written), (R + 7) * 4 for Adam (m as well), (R + 5) * 4 for AdaGrad (the
+    accumulator in place of v)."""
+    R = 16
+    out = {}
+    for n in (61_000_000, 250_000_000):
+        gen = torch.Generator(device="cuda").manual_seed(0)
+        grads = torch.randn(R * n, device="cuda", generator=gen) * 1e-3
+        w = torch.randn(n, device="cuda", generator=gen) * 0.05
+        v = torch.randn(n, device="cuda", generator=gen) * 1e-3
+        avg = torch.empty(n, device="cuda")
+        ms = _time_calls(torch, lambda: mtx.mtx_sgd_update(w, v, grads, R, n, n, 0.01, 0.9, avg),
+                         reps if n < 100_000_000 else reps // 2)
+        rec = {"R": R, "n": n, **_rate((R + 5) * 4 * n, ms)}
+        if n == 61_000_000:
+            out.update(rec)
+            m2 = (torch.randn(n, device="cuda", generator=gen) * 1e-3) ** 2
+            ms = _time_calls(torch, lambda: mtx.mtx_adam_update(
+                w, v, m2, grads, R, n, n, 1e-3, 0.9, 0.999, 1e-8, 10, avg), reps)
+            out["adam"] = {"R": R, "n": n, **_rate((R + 7) * 4 * n, ms)}
+            ms = _time_calls(torch, lambda: mtx.mtx_adagrad_update(
+                w, m2, grads, R, n, n, 0.01, 1e-10, avg), reps)
+            out["adagrad"] = {"R": R, "n": n, **_rate((R + 5) * 4 * n, ms)}
+            del m2
+        else:
+            out["n250M"] = rec
+        del grads, w, v, avg
+        torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(wkl, budget_s=12.0):

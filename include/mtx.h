@@ -145,6 +145,28 @@ int mtx_average_grads(const float* grads, int R, size_t n, size_t ld, float* avg
 int mtx_sgd_update(float* w, float* v, const float* grads, int R, size_t n, size_t ld,
                    float lr, float momentum, float* avg_out, void* stream);
 
+/* The average above followed by Adam, one of the update rules Sec. I lists among the
+ * improvements to gradient descent that TensorFlow offers; the paper gives no formula, so the
+ * rule is Algorithm 1 of the work it cites (Kingma and Ba), at step number `step` (>= 1):
+ *   g = (1/R) sum_r grads[r*ld + i];  m = beta1*m + (1-beta1)*g;  v = beta2*v + (1-beta2)*g^2;
+ *   w = w - lr * (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * g is summed in double and rounded to float once (the step divides by about |g|, so the
+ * average's rounding must not be amplified where it nearly cancels).  w, m, v [n] fp32 are
+ * updated in place (m = v = 0 before the first step); avg_out (nullable) receives g.  Requires 0 <= beta1, beta2 < 1, eps >= 0, finite lr; w, m, v, avg_out and grads
+ * must not overlap.  Asynchronous. */
+int mtx_adam_update(float* w, float* m, float* v, const float* grads, int R, size_t n,
+                    size_t ld, float lr, float beta1, float beta2, float eps, long long step,
+                    float* avg_out, void* stream);
+
+/* The average followed by AdaGrad (diagonal form of the work Sec. I cites, Duchi, Hazan and
+ * Singer):  g = (1/R) sum_r grads[r*ld + i];  acc = acc + g^2;  w = w - lr * g / (sqrt(acc) + eps)
+ * g is summed in double and rounded once, as for Adam.  w, acc [n] fp32 are updated in place
+ * (acc holds its initial value before the first step);
+ * avg_out (nullable) receives g.  Requires eps >= 0 and finite lr; buffers must not overlap.
+ * Asynchronous. */
+int mtx_adagrad_update(float* w, float* acc, const float* grads, int R, size_t n, size_t ld,
+                       float lr, float eps, float* avg_out, void* stream);
+
 /* Copy the weights (and, if v_host != NULL, the velocity) to host memory [P], in the flat
  * logical layout.  Synchronous (waits for the model's last stream). */
 int mtx_get_params(const mtx_model* m, float* w_host, float* v_host);

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
 #include <vector>
@@ -1020,6 +1021,82 @@ int mtx_sgd_update(float* w, float* v, const float* grads, int R, size_t n, size
         return fail(MTX_EINVAL, "w, v, avg_out and grads must not overlap");
     HIP_TRY(average_update(grads, R, n, ld, w, momentum != 0.0f ? v : nullptr, lr, momentum, avg_out,
                            true, static_cast<hipStream_t>(stream)), "mtx_sgd_update");
+    return MTX_OK;
+}
+
+// Pairwise overlap test over the non-null buffers of an update (grads spans gb bytes, every
+// other buffer n floats).
+static bool any_overlap(const float* grads, size_t gb, size_t nb, std::initializer_list<const float*> bufs)
+{
+    std::vector<const float*> b;
+    for (const float* p : bufs)
+        if (p) b.push_back(p);
+    for (size_t i = 0; i < b.size(); ++i) {
+        if (overlap(grads, gb, b[i], nb)) return true;
+        for (size_t j = i + 1; j < b.size(); ++j)
+            if (overlap(b[i], nb, b[j], nb)) return true;
+    }
+    return false;
+}
+
+int mtx_adam_update(float* w, float* m, float* v, const float* grads, int R, size_t n, size_t ld,
+                    float lr, float beta1, float beta2, float eps, long long step, float* avg_out,
+                    void* stream)
+{
+    int rc = check_avg_args(grads, R, n, ld, w);
+    if (rc) return rc;
+    if (!m || !v) return fail(MTX_EINVAL, "m and v must not be NULL");
+    if (!aligned(m, 4) || !aligned(v, 4) || (avg_out && !aligned(avg_out, 4)))
+        return fail(MTX_EINVAL, "pointers must be 4-byte aligned");
+    if (!std::isfinite(lr) || !std::isfinite(eps) || eps < 0.0f)
+        return fail(MTX_EINVAL, "lr must be finite and eps finite and >= 0");
+    if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+        return fail(MTX_EINVAL, "beta1 and beta2 must lie in [0, 1)");
+    if (step < 1) return fail(MTX_EINVAL, "step must be >= 1 (got %lld)", step);
+    const size_t gb = ((size_t)(R - 1) * ld + n) * 4, nb = n * 4;
+    if (any_overlap(grads, gb, nb, {w, m, v, avg_out}))
+        return fail(MTX_EINVAL, "w, m, v, avg_out and grads must not overlap");
+    AdaptParams p;
+    p.w = w;
+    p.s1 = m;
+    p.s2 = v;
+    p.avg = avg_out;
+    p.lr = lr;
+    p.b1 = beta1;
+    p.c1 = (float)(1.0 - (double)beta1);
+    p.b2 = beta2;
+    p.c2 = (float)(1.0 - (double)beta2);
+    p.ib1 = (float)(1.0 / (1.0 - std::pow((double)beta1, (double)step)));
+    p.ib2 = (float)(1.0 / (1.0 - std::pow((double)beta2, (double)step)));
+    p.eps = eps;
+    HIP_TRY(average_adapt(grads, R, n, ld, true, p, static_cast<hipStream_t>(stream)),
+            "mtx_adam_update");
+    return MTX_OK;
+}
+
+int mtx_adagrad_update(float* w, float* acc, const float* grads, int R, size_t n, size_t ld,
+                       float lr, float eps, float* avg_out, void* stream)
+{
+    int rc = check_avg_args(grads, R, n, ld, w);
+    if (rc) return rc;
+    if (!acc) return fail(MTX_EINVAL, "acc must not be NULL");
+    if (!aligned(acc, 4) || (avg_out && !aligned(avg_out, 4)))
+        return fail(MTX_EINVAL, "pointers must be 4-byte aligned");
+    if (!std::isfinite(lr) || !std::isfinite(eps) || eps < 0.0f)
+        return fail(MTX_EINVAL, "lr must be finite and eps finite and >= 0");
+    const size_t gb = ((size_t)(R - 1) * ld + n) * 4, nb = n * 4;
+    if (any_overlap(grads, gb, nb, {w, acc, avg_out}))
+        return fail(MTX_EINVAL, "w, acc, avg_out and grads must not overlap");
+    AdaptParams p;
+    p.w = w;
+    p.s1 = acc;
+    p.s2 = nullptr;
+    p.avg = avg_out;
+    p.lr = lr;
+    p.b1 = p.c1 = p.b2 = p.c2 = p.ib1 = p.ib2 = 0.0f;
+    p.eps = eps;
+    HIP_TRY(average_adapt(grads, R, n, ld, false, p, static_cast<hipStream_t>(stream)),
+            "mtx_adagrad_update");
     return MTX_OK;
 }
 

@@ -891,4 +891,151 @@ hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float*
     return avg_update_launch<false, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
 }
 
+
+// ---- gradient average + Adam or AdaGrad ----------------------------------------------------
+//
+// The average g, summed in double in ascending r and divided by R before one rounding to float,
+// followed by an adaptive update:
+//   Adam (Kingma and Ba):  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g^2;
+//                          w = w - lr * (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)
+//   AdaGrad (Duchi et al.): G = G + g^2;  w = w - lr * g / (sqrt(G) + eps)
+// The update divides by a square root of squared averages, so where the average nearly cancels
+// (|g| near eps) its absolute rounding error would be amplified into the step; the double sum of
+// at most a few dozen floats is exact in practice, so g is the correctly rounded average.  The
+// update itself is fp32 with correctly rounded division and square root; the bias corrections
+// enter as their reciprocals, computed on the host in double.  Four consecutive elements per
+// thread when every row and state vector is 16-byte aligned.
+
+template <bool ADAM>
+__device__ __forceinline__ void adapt_apply(float g, float& w, float& s1, float& s2,
+                                            const AdaptParams& p)
+{
+    if (ADAM) {
+        const float m = fmaf(p.b1, s1, p.c1 * g);
+        const float v = fmaf(p.b2, s2, p.c2 * (g * g));
+        s1 = m;
+        s2 = v;
+        w = fmaf(-p.lr, (m * p.ib1) / (sqrtf(v * p.ib2) + p.eps), w);
+    } else {
+        const float G = fmaf(g, g, s1);
+        s1 = G;
+        w = fmaf(-p.lr, g / (sqrtf(G) + p.eps), w);
+    }
+}
+
+template <bool ADAM, bool AVG>
+__device__ __forceinline__ void adapt_one(const float* __restrict__ grads, int R, long long ld,
+                                          long long i, const AdaptParams& p)
+{
+    double s = (double)grads[i];
+    for (int r = 1; r < R; ++r) s += (double)grads[(long long)r * ld + i];
+    const float g = (float)(s / (double)R);
+    if (AVG) p.avg[i] = g;
+    float w = p.w[i], s1 = p.s1[i], s2 = ADAM ? p.s2[i] : 0.f;
+    adapt_apply<ADAM>(g, w, s1, s2, p);
+    p.w[i] = w;
+    p.s1[i] = s1;
+    if (ADAM) p.s2[i] = s2;
+}
+
+// n elements: threads below n / 4 take four each; the next one takes the n % 4 left over.
+template <int RT, bool ADAM, bool AVG>
+__global__ __launch_bounds__(256) void avg_adapt_vec4(const float* __restrict__ grads, int Rrt,
+                                                      long long n, long long ld,
+                                                      const AdaptParams p)
+{
+    const long long n4 = n / 4;
+    const int R = RT > 0 ? RT : Rrt;
+    for (long long t = (long long)blockIdx.x * 256 + threadIdx.x; t <= n4;
+         t += (long long)gridDim.x * 256) {
+        if (t == n4) {
+            for (long long i = 4 * n4; i < n; ++i) adapt_one<ADAM, AVG>(grads, R, ld, i, p);
+            break;
+        }
+        const f32x4* g4 = reinterpret_cast<const f32x4*>(grads) + t;
+        const long long ld4 = ld / 4;
+        const f32x4 g0 = __builtin_nontemporal_load(g4);
+        double s[4] = {(double)g0[0], (double)g0[1], (double)g0[2], (double)g0[3]};
+        if (RT > 0) {
+            f32x4 buf[RT > 1 ? RT - 1 : 1];
+#pragma unroll
+            for (int r = 1; r < RT; ++r) buf[r - 1] = __builtin_nontemporal_load(g4 + r * ld4);
+#pragma unroll
+            for (int r = 1; r < RT; ++r)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s[j] += (double)buf[r - 1][j];
+        } else {
+            for (int r = 1; r < R; ++r) {
+                const f32x4 x = __builtin_nontemporal_load(g4 + r * ld4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s[j] += (double)x[j];
+            }
+        }
+        const double dr = (double)R;
+        const f32x4 g = {(float)(s[0] / dr), (float)(s[1] / dr), (float)(s[2] / dr),
+                         (float)(s[3] / dr)};
+        if (AVG) __builtin_nontemporal_store(g, reinterpret_cast<f32x4*>(p.avg) + t);
+        f32x4 wv = reinterpret_cast<f32x4*>(p.w)[t];
+        f32x4 a1 = reinterpret_cast<f32x4*>(p.s1)[t];
+        f32x4 a2 = ADAM ? reinterpret_cast<f32x4*>(p.s2)[t] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float wj = wv[j], x1 = a1[j], x2 = a2[j];
+            adapt_apply<ADAM>(g[j], wj, x1, x2, p);
+            wv[j] = wj;
+            a1[j] = x1;
+            a2[j] = x2;
+        }
+        reinterpret_cast<f32x4*>(p.w)[t] = wv;
+        reinterpret_cast<f32x4*>(p.s1)[t] = a1;
+        if (ADAM) reinterpret_cast<f32x4*>(p.s2)[t] = a2;
+    }
+}
+
+template <bool ADAM, bool AVG>
+__global__ __launch_bounds__(256) void avg_adapt_scalar(const float* __restrict__ grads, int R,
+                                                        long long n, long long ld,
+                                                        const AdaptParams p)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    adapt_one<ADAM, AVG>(grads, R, ld, i, p);
+}
+
+template <bool ADAM, bool AVG>
+static hipError_t avg_adapt_launch(const float* grads, int R, size_t n, size_t ld,
+                                   const AdaptParams& p, hipStream_t s)
+{
+    auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    const bool vec = (ld % 4 == 0) && al(grads) && al(p.w) && al(p.s1) && (!ADAM || al(p.s2)) &&
+                     (!AVG || al(p.avg));
+    const long long nn = (long long)n, ll = (long long)ld;
+    if (vec) {
+        const dim3 grid(grid_for(n / 4 + 1, 256));
+        switch (R) {
+        case 1: hipLaunchKernelGGL((avg_adapt_vec4<1, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        case 2: hipLaunchKernelGGL((avg_adapt_vec4<2, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        case 4: hipLaunchKernelGGL((avg_adapt_vec4<4, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        case 8: hipLaunchKernelGGL((avg_adapt_vec4<8, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        case 16: hipLaunchKernelGGL((avg_adapt_vec4<16, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        default: hipLaunchKernelGGL((avg_adapt_vec4<0, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        }
+    } else {
+        hipLaunchKernelGGL((avg_adapt_scalar<ADAM, AVG>), dim3(grid_for(n, 256)), dim3(256), 0, s,
+                           grads, R, nn, ll, p);
+    }
+    return hipGetLastError();
+}
+
+hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool adam,
+                         const AdaptParams& p, hipStream_t s)
+{
+    if (adam) {
+        if (p.avg) return avg_adapt_launch<true, true>(grads, R, n, ld, p, s);
+        return avg_adapt_launch<true, false>(grads, R, n, ld, p, s);
+    }
+    if (p.avg) return avg_adapt_launch<false, true>(grads, R, n, ld, p, s);
+    return avg_adapt_launch<false, false>(grads, R, n, ld, p, s);
+}
+
 }  // namespace mtx

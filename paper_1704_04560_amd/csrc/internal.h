@@ -193,4 +193,17 @@ hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float*
                           float lr, float mu, float* avg, bool update, hipStream_t s,
                           unsigned max_blocks = 0);
 
+// Parameters of the adaptive updates after the average (Adam: s1 = first moment m, s2 =
+// second moment v; AdaGrad: s1 = accumulated squared gradients, s2 unused).  c1 = 1 - b1,
+// c2 = 1 - b2, ib1 = 1 / (1 - b1^t), ib2 = 1 / (1 - b2^t).  avg (nullable) receives the average.
+struct AdaptParams {
+    float* w;
+    float* s1;
+    float* s2;
+    float* avg;
+    float lr, b1, c1, b2, c2, ib1, ib2, eps;
+};
+hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool adam,
+                         const AdaptParams& p, hipStream_t s);
+
 }  // namespace mtx

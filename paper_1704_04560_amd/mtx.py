@@ -21,7 +21,8 @@ MTX_F32, MTX_BF16 = 0, 1
 MTX_FC, MTX_CONV, MTX_MAXPOOL = 0, 1, 2
 
 EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_train_step", "mtx_average_grads",
-           "mtx_sgd_update", "mtx_get_params", "mtx_set_params", "mtx_get_layer_output",
+           "mtx_sgd_update", "mtx_adam_update", "mtx_adagrad_update", "mtx_get_params",
+           "mtx_set_params", "mtx_get_layer_output",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
            "mtx_set_layerwise_update", "mtx_set_timing",
            "mtx_get_timing", "mtx_free_model", "mtx_last_error")
@@ -76,6 +77,9 @@ def lib() -> C.CDLL:
             "mtx_train_step": (i32, [vp, vp, vp, f32, f32, vp, vp]),
             "mtx_average_grads": (i32, [vp, i32, sz, sz, vp, vp]),
             "mtx_sgd_update": (i32, [vp, vp, vp, i32, sz, sz, f32, f32, vp, vp]),
+            "mtx_adam_update": (i32, [vp, vp, vp, vp, i32, sz, sz, f32, f32, f32, f32,
+                                      C.c_longlong, vp, vp]),
+            "mtx_adagrad_update": (i32, [vp, vp, vp, i32, sz, sz, f32, f32, vp, vp]),
             "mtx_get_params": (i32, [vp, vp, vp]),
             "mtx_set_params": (i32, [vp, vp, vp]),
             "mtx_get_layer_output": (i32, [vp, i32, vp, sz]),
@@ -161,6 +165,17 @@ def mtx_average_grads(grads, R, n, ld, avg, stream=None):
 def mtx_sgd_update(w, v, grads, R, n, ld, lr, momentum, avg_out=None, stream=None):
     _check(lib().mtx_sgd_update(_ptr(w), _ptr(v), _ptr(grads), R, n, ld, lr, momentum,
                                 _ptr(avg_out), _stream(stream)))
+
+
+def mtx_adam_update(w, m, v, grads, R, n, ld, lr, beta1, beta2, eps, step, avg_out=None,
+                    stream=None):
+    _check(lib().mtx_adam_update(_ptr(w), _ptr(m), _ptr(v), _ptr(grads), R, n, ld, lr, beta1,
+                                 beta2, eps, step, _ptr(avg_out), _stream(stream)))
+
+
+def mtx_adagrad_update(w, acc, grads, R, n, ld, lr, eps, avg_out=None, stream=None):
+    _check(lib().mtx_adagrad_update(_ptr(w), _ptr(acc), _ptr(grads), R, n, ld, lr, eps,
+                                    _ptr(avg_out), _stream(stream)))
 
 
 def mtx_get_params(handle, w_host: np.ndarray, v_host: Optional[np.ndarray] = None):

@@ -42,6 +42,7 @@ def test_sizes_match_oracle(name):
 
 def _err(fn, *args):
     kw = {"stream": 0} if fn in (mtx.mtx_average_grads, mtx.mtx_sgd_update,
+                                 mtx.mtx_adam_update, mtx.mtx_adagrad_update,
                                  mtx.mtx_train_step) else {}
     with pytest.raises(mtx.MtxError) as e:
         fn(*args, **kw)
@@ -81,6 +82,24 @@ def test_update_argument_errors_need_no_device():
     assert _err(mtx.mtx_sgd_update, w, None, g, 4, 16, 16, float("nan"), 0.0, None) == mtx.MTX_EINVAL
     mis = g.ctypes.data + 2
     assert _err(mtx.mtx_average_grads, mis, 1, 4, 4, a) == mtx.MTX_EINVAL       # misaligned
+
+
+def test_adaptive_update_argument_errors_need_no_device():
+    g = np.zeros(64, np.float32)
+    w, m, v = (np.zeros(16, np.float32) for _ in range(3))
+    ok = (0.001, 0.9, 0.999, 1e-8, 1)
+    assert _err(mtx.mtx_adam_update, w, None, v, g, 4, 16, 16, *ok) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adam_update, w, m, m, g, 4, 16, 16, *ok) == mtx.MTX_EINVAL     # m = v
+    assert _err(mtx.mtx_adam_update, w, m, v, g, 4, 16, 16, 0.001, 1.0, 0.999, 1e-8, 1) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adam_update, w, m, v, g, 4, 16, 16, 0.001, 0.9, -0.1, 1e-8, 1) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adam_update, w, m, v, g, 4, 16, 16, 0.001, 0.9, 0.999, -1.0, 1) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adam_update, w, m, v, g, 4, 16, 16, 0.001, 0.9, 0.999, 1e-8, 0) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adam_update, w, m, v, g, 4, 16, 8, *ok) == mtx.MTX_EINVAL      # ld < n
+    assert _err(mtx.mtx_adam_update, w, m, g[4:], g, 4, 16, 16, *ok) == mtx.MTX_EINVAL  # overlap
+    assert _err(mtx.mtx_adagrad_update, w, None, g, 4, 16, 16, 0.1, 1e-10) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adagrad_update, w, w, g, 4, 16, 16, 0.1, 1e-10) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adagrad_update, w, m, g, 0, 16, 16, 0.1, 1e-10) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_adagrad_update, w, m, g, 4, 16, 16, float("inf"), 1e-10) == mtx.MTX_EINVAL
 
 
 def test_model_call_errors_need_no_device():

@@ -77,3 +77,109 @@ def test_microbench_size_sampled():
     parity.assert_tensor_close(avg[it].cpu().numpy(), ref_avg, 1e-6, "average")
     parity.assert_tensor_close(vd[it].cpu().numpy(), ref_v, 1e-6, "velocity")
     parity.assert_update_close(wd[it].cpu().numpy(), ref_w, w[idx], 1e-4)
+
+
+# ---- the average followed by Adam or AdaGrad ----------------------------------------------------
+
+ADAM = dict(lr=1e-3, b1=0.9, b2=0.999, eps=1e-8)
+
+
+@pytest.mark.parametrize("R", [1, 3, 4, 16])
+@pytest.mark.parametrize("n,pad", [(1, 0), (7, 0), (1000003, 0), (4099, 5), (4096, 64)])
+@pytest.mark.parametrize("with_avg", [True, False])
+def test_adam_update_matches_oracle(R, n, pad, with_avg):
+    """Three chained steps (t = 1, 2, 3) from zero moments, new gradients each step; the moments
+    stay on the GPU between steps and in the oracle's arrays on the host."""
+    ld = n + pad
+    print(f"[case] adam_update R={R} n={n} ld={ld} avg={with_avg}", flush=True)
+    _, w, _ = wl.make_avg_update_inputs(R, n, seed=R * 11 + n, ld=ld)
+    m, v = np.zeros(n, np.float32), np.zeros(n, np.float32)
+    wd, md, vd = _dev(w), _dev(m), _dev(v)
+    avg = torch.empty(n, device="cuda") if with_avg else None
+    for t in (1, 2, 3):
+        grads, _, _ = wl.make_avg_update_inputs(R, n, seed=R * 11 + n + 100 * t, ld=ld)
+        ref_avg, ref_w, m, v = orc.average_adam(grads, w, m, v, ADAM["lr"], ADAM["b1"],
+                                                ADAM["b2"], ADAM["eps"], t, n=n)
+        mtx.mtx_adam_update(wd, md, vd, _dev(grads), R, n, ld, ADAM["lr"], ADAM["b1"],
+                            ADAM["b2"], ADAM["eps"], t, avg)
+        torch.cuda.synchronize()
+        if with_avg:
+            parity.assert_tensor_close(avg.cpu().numpy(), ref_avg, 1e-6, f"average t={t}")
+        parity.assert_tensor_close(md.cpu().numpy(), m, 1e-5, f"m t={t}")
+        parity.assert_tensor_close(vd.cpu().numpy(), v, 1e-5, f"v t={t}")
+        parity.assert_update_close(wd.cpu().numpy(), ref_w, w, 1e-4, f"w t={t}")
+        w = ref_w
+        # continue from the oracle's state so that every step is compared from equal inputs
+        wd.copy_(_dev(w))
+        md.copy_(_dev(m))
+        vd.copy_(_dev(v))
+
+
+@pytest.mark.parametrize("b1,b2,eps,t", [(0.5, 0.75, 1e-6, 7), (0.0, 0.0, 0.0, 1)])
+def test_adam_update_other_hyperparameters(b1, b2, eps, t):
+    """Non-default betas at a later step number with non-zero incoming moments, and the
+    degenerate betas = 0 (m = g, v = g^2, so the update is lr * sign(g) up to eps = 0)."""
+    R, n = 4, 20011
+    print(f"[case] adam_update b1={b1} b2={b2} eps={eps} t={t}", flush=True)
+    grads, w, m = wl.make_avg_update_inputs(R, n, seed=9)
+    v = wl.make_square_state(n, seed=9, terms=3)
+    ref_avg, ref_w, ref_m, ref_v = orc.average_adam(grads, w, m, v, 0.01, b1, b2, eps, t)
+    wd, md, vd = _dev(w), _dev(m), _dev(v)
+    avg = torch.empty(n, device="cuda")
+    mtx.mtx_adam_update(wd, md, vd, _dev(grads), R, n, n, 0.01, b1, b2, eps, t, avg)
+    torch.cuda.synchronize()
+    parity.assert_tensor_close(avg.cpu().numpy(), ref_avg, 1e-6, "average")
+    parity.assert_tensor_close(md.cpu().numpy(), ref_m, 1e-5, "m")
+    parity.assert_tensor_close(vd.cpu().numpy(), ref_v, 1e-5, "v")
+    parity.assert_update_close(wd.cpu().numpy(), ref_w, w, 1e-4)
+
+
+@pytest.mark.parametrize("R", [1, 2, 8, 16])
+@pytest.mark.parametrize("n,pad", [(1, 0), (7, 0), (1000003, 0), (4099, 5)])
+@pytest.mark.parametrize("with_avg", [True, False])
+def test_adagrad_update_matches_oracle(R, n, pad, with_avg):
+    """Three chained steps from an accumulator holding earlier squared gradients."""
+    ld = n + pad
+    print(f"[case] adagrad_update R={R} n={n} ld={ld} avg={with_avg}", flush=True)
+    _, w, _ = wl.make_avg_update_inputs(R, n, seed=R * 13 + n, ld=ld)
+    acc = wl.make_square_state(n, seed=R, terms=2)
+    wd, ad = _dev(w), _dev(acc)
+    avg = torch.empty(n, device="cuda") if with_avg else None
+    for t in (1, 2, 3):
+        grads, _, _ = wl.make_avg_update_inputs(R, n, seed=R * 13 + n + 100 * t, ld=ld)
+        ref_avg, ref_w, acc = orc.average_adagrad(grads, w, acc, 0.01, 1e-10, n=n)
+        mtx.mtx_adagrad_update(wd, ad, _dev(grads), R, n, ld, 0.01, 1e-10, avg)
+        torch.cuda.synchronize()
+        if with_avg:
+            parity.assert_tensor_close(avg.cpu().numpy(), ref_avg, 1e-6, f"average t={t}")
+        parity.assert_tensor_close(ad.cpu().numpy(), acc, 1e-5, f"accumulator t={t}")
+        parity.assert_update_close(wd.cpu().numpy(), ref_w, w, 1e-4, f"w t={t}")
+        w = ref_w
+        wd.copy_(_dev(w))
+        ad.copy_(_dev(acc))
+
+
+def test_adam_microbench_size_sampled():
+    """Adam after the average at the full microbenchmark size (R = 16, n = 61,000,000), checked
+    against the oracle at 20,000 sampled elements plus the tail."""
+    R, n = 16, 61_000_000
+    print(f"[case] adam_update full size R={R} n={n}", flush=True)
+    grads, w, m = wl.make_avg_update_inputs(R, n, seed=0)
+    v = wl.make_square_state(n, seed=0, terms=2)
+    idx = np.unique(np.concatenate([np.random.default_rng(1).choice(n, 20000, replace=False),
+                                    np.arange(n - 7, n)]))
+    ref_avg, ref_w, ref_m, ref_v = orc.average_adam(grads[:, idx], w[idx], m[idx], v[idx],
+                                                    ADAM["lr"], ADAM["b1"], ADAM["b2"],
+                                                    ADAM["eps"], 5)
+    gd = _dev(grads)
+    del grads
+    wd, md, vd = _dev(w), _dev(m), _dev(v)
+    avg = torch.empty(n, device="cuda")
+    mtx.mtx_adam_update(wd, md, vd, gd, R, n, n, ADAM["lr"], ADAM["b1"], ADAM["b2"],
+                        ADAM["eps"], 5, avg)
+    torch.cuda.synchronize()
+    it = torch.from_numpy(idx).cuda()
+    parity.assert_tensor_close(avg[it].cpu().numpy(), ref_avg, 1e-6, "average")
+    parity.assert_tensor_close(md[it].cpu().numpy(), ref_m, 1e-5, "m")
+    parity.assert_tensor_close(vd[it].cpu().numpy(), ref_v, 1e-5, "v")
+    parity.assert_update_close(wd[it].cpu().numpy(), ref_w, w[idx], 1e-4)

@@ -605,7 +605,12 @@ template <class Op, bool ISP, int BR, int BK> struct Loader<Op, ISP, L_KD, BR, B
 
 // ---- the tiled MFMA kernel --------------------------------------------------------------------
 
-template <class Op, int FP, int FQ, int BK, int PK, int QK>
+// An operation that declares INTERLEAVE = true gets the interleaved scheduling order below.
+template <class Op, class = void> struct Interleave : std::false_type {};
+template <class Op>
+struct Interleave<Op, std::void_t<decltype(Op::INTERLEAVE)>> : std::bool_constant<Op::INTERLEAVE> {};
+
+template <class Op, int FP, int FQ, int BK, int PK, int QK, bool SCHED = false>
 __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 {
     typedef typename Op::TT T;
@@ -682,6 +687,22 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
             for (int i = 0; i < FP; ++i)
 #pragma unroll
                 for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+        }
+        if constexpr (SCHED) {
+            // Scheduling order: the first k chunk's fragment reads, then one fragment read of a
+            // later chunk and one global load after each MFMA, so that their latencies overlap
+            // the MFMAs instead of being waited for in clusters (measured: the bf16 convolution
+            // weight gradients, whose operands both come through k-major tiles, run 10-25%
+            // faster; forward and data-gradient kernels, and the output-bound fully connected
+            // weight gradients, run slower with it).
+            constexpr int NM = FP * FQ * (BK / M::KSTEP);
+            __builtin_amdgcn_sched_group_barrier(0x100, FP + FQ, 0);  // LDS reads
+#pragma unroll
+            for (int m = 0; m < NM; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+            }
         }
         __syncthreads();
     }
@@ -892,7 +913,6 @@ __global__ __launch_bounds__(256) void split_epilogue(const GemmArgs a)
 }
 
 // ---- launch ---------------------------------------------------------------------------------
-
 template <class Op, int FP, int FQ, int BK, int PK, int QK>
 static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
 {
@@ -910,6 +930,9 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     }
     if constexpr (PK == L_KD || QK == L_KD)
         hipLaunchKernelGGL((igemm_direct_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s,
+                           a);
+    else if constexpr (Interleave<Op>::value && sizeof(typename Op::TT) == 2)
+        hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK, true>), grid, dim3(256), shm, s,
                            a);
     else
         hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);

@@ -13,6 +13,7 @@
 //   pc/p_rv           RT loader on P: state for rows p0..p0+VEC-1, 16 bytes at k
 //   qk/q_sk, qr/q_sr, qv/q_kv, qc/q_rv   the same for Q
 //   store4(a, c, p, q, acc, np)   epilogue for rows p..p+np-1 of column q
+//   INTERLEAVE        (optional) schedule fragment reads and loads between the MFMAs
 #pragma once
 
 #include "igemm.h"
@@ -290,6 +291,7 @@ template <typename T> struct ConvWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = true;
     static constexpr bool SHARE_Q = true;
+    static constexpr bool INTERLEAVE = true;
     static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = true, TAB_CHUNK = false;
     // entry for position k of the shard: the offset of x[b0 + n][oh*S - PD][ow*S - PD][0] and

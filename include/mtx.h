@@ -214,6 +214,23 @@ int mtx_set_overlap(mtx_model* m, int enable);
  * Ignored while kernel timing is on.  Returns MTX_EINVAL for a NULL model. */
 int mtx_set_layerwise_update(mtx_model* m, int enable);
 
+/* Update rule that mtx_train_step applies after the average of the R shard gradients.
+ * MTX_OPT_MOMENTUM (the default): the momentum rule above, with the lr and momentum arguments
+ * of each mtx_train_step.  MTX_OPT_ADAM and MTX_OPT_ADAGRAD: the rules of mtx_adam_update and
+ * mtx_adagrad_update (the other update rules Sec. I names), with the lr argument of each step
+ * and the momentum argument ignored:
+ *   Adam: first moment in the model's v buffer, second moment in s2 (device, P floats, 16-byte
+ *         aligned, owned by the caller, which zeroes it before the first step, as v = 0 after
+ *         mtx_init_model); beta1, beta2 in [0, 1), eps >= 0; the step number t counts the
+ *         mtx_train_step calls since this call (1 for the first).
+ *   AdaGrad: accumulator in the model's v buffer (its content is the initial accumulator;
+ *         mtx_set_params sets it); eps >= 0; beta1, beta2 and s2 unused.
+ * mtx_get_params / mtx_set_params read and write v as that state.  A step with Adam is never
+ * replayed from a graph (its bias correction changes every step).  Returns MTX_EINVAL for an
+ * unknown kind, invalid hyperparameters, or an s2 that overlaps the model's buffers. */
+typedef enum { MTX_OPT_MOMENTUM = 0, MTX_OPT_ADAM = 1, MTX_OPT_ADAGRAD = 2 } mtx_optimizer;
+int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float eps, float* s2);
+
 /* Kernel timing of mtx_train_step (measurement support; not part of the method).
  * mtx_set_timing(m, 1) makes every later mtx_train_step record a HIP event pair on its stream
  * around each kernel launch; mtx_set_timing(m, 0) stops it.  mtx_get_timing waits for the

@@ -480,6 +480,12 @@ struct mtx_model {
     hipStream_t upd = nullptr;
     std::vector<hipEvent_t> wdone;  // per parameter layer: its weight gradients are done
     hipEvent_t upd_join = nullptr;  // every layer's update is done
+    // update rule after the average (mtx_set_optimizer): momentum, or Adam / AdaGrad with their
+    // first state in v, Adam's second moment in s2, and the number of steps taken since
+    int opt = MTX_OPT_MOMENTUM;
+    float b1 = 0.9f, b2 = 0.999f, eps = 0.0f;
+    float* s2 = nullptr;
+    long long opt_step = 0;
 };
 
 namespace {
@@ -744,6 +750,36 @@ int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count,
 }
 
 // Enqueue the kernels of one step on stream s (eagerly, or into a capture).
+// The average of the R shard gradients of parameters [off, off + len) fused with the model's
+// update rule (Adam at step number m->opt_step, already advanced for this step).
+static hipError_t update_slice(mtx_model* m, size_t off, size_t len, float lr, float momentum,
+                               hipStream_t s, unsigned max_blocks)
+{
+    const Plan& pl = m->pl;
+    if (m->opt == MTX_OPT_MOMENTUM)
+        return average_update(m->grads + off, pl.R, len, pl.ld, m->w + off, m->v + off, lr,
+                              momentum, m->gavg + off, true, s, max_blocks);
+    AdaptParams p;
+    p.w = m->w + off;
+    p.s1 = m->v + off;
+    p.s2 = m->opt == MTX_OPT_ADAM ? m->s2 + off : nullptr;
+    p.avg = m->gavg + off;
+    p.lr = lr;
+    p.eps = m->eps;
+    p.b1 = p.c1 = p.b2 = p.c2 = p.ib1 = p.ib2 = 0.0f;
+    if (m->opt == MTX_OPT_ADAM) {
+        const double t = (double)m->opt_step;
+        p.b1 = m->b1;
+        p.c1 = (float)(1.0 - (double)m->b1);
+        p.b2 = m->b2;
+        p.c2 = (float)(1.0 - (double)m->b2);
+        p.ib1 = (float)(1.0 / (1.0 - std::pow((double)m->b1, t)));
+        p.ib2 = (float)(1.0 / (1.0 - std::pow((double)m->b2, t)));
+    }
+    return average_adapt(m->grads + off, pl.R, len, pl.ld, m->opt == MTX_OPT_ADAM, p, s,
+                         max_blocks);
+}
+
 static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
                         float momentum, float* loss_out, hipStream_t s)
 {
@@ -882,9 +918,8 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             ++nlayer;
             const size_t off = lp.w_off, len = lp.w_len + lp.b_len;
             HIP_TRY(launch_site(m, "avg_update", l, m->upd, [&] {
-                        return average_update(m->grads + off, pl.R, len, pl.ld, m->w + off,
-                                              m->v + off, lr, momentum, m->gavg + off, true,
-                                              m->upd, kLayerUpdateBlocks);
+                        return update_slice(m, off, len, lr, momentum, m->upd,
+                                            kLayerUpdateBlocks);
                     }), "layer average + update");
         }
     }
@@ -899,8 +934,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     }
     // ---- average of the R shard gradients fused with the optimizer step ----
     HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {
-                return average_update(m->grads, pl.R, pl.P, pl.ld, m->w, m->v, lr, momentum,
-                                      m->gavg, true, s);
+                return update_slice(m, 0, pl.P, lr, momentum, s, 0);
             }), "average + update");
     return MTX_OK;
 }
@@ -952,12 +986,15 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
         return fail(MTX_EINVAL, "lr and momentum must be finite");
     hipStream_t s = static_cast<hipStream_t>(stream);
     m->last_stream = s;
+    ++m->opt_step;
     GraphCache& gc = m->graph;
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     const bool caller_capturing =
         hipStreamIsCapturing(s, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone;
     (void)hipGetLastError();
-    if (gc.enabled && !m->timer.on && !caller_capturing && gc.misses < GraphCache::kMaxMisses) {
+    // Adam's bias correction changes every step, so its steps are not replayed from a graph
+    if (gc.enabled && !m->timer.on && !caller_capturing && m->opt != MTX_OPT_ADAM &&
+        gc.misses < GraphCache::kMaxMisses) {
         if (gc.matches(x, labels, lr, momentum, loss_out)) {
             gc.misses = 0;
             HIP_TRY(hipGraphLaunch(gc.exec, s), "graph launch");
@@ -971,6 +1008,33 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
         gc.misses = GraphCache::kMaxMisses;  // capture is not possible here: stay eager
     }
     return enqueue_step(m, x, labels, lr, momentum, loss_out, s);
+}
+
+int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float eps, float* s2)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    if (kind != MTX_OPT_MOMENTUM && kind != MTX_OPT_ADAM && kind != MTX_OPT_ADAGRAD)
+        return fail(MTX_EINVAL, "unknown optimizer %d", kind);
+    if (kind != MTX_OPT_MOMENTUM && (!std::isfinite(eps) || eps < 0.0f))
+        return fail(MTX_EINVAL, "eps must be finite and >= 0");
+    if (kind == MTX_OPT_ADAM) {
+        if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+            return fail(MTX_EINVAL, "beta1 and beta2 must lie in [0, 1)");
+        if (!s2 || !aligned(s2, 16))
+            return fail(MTX_EINVAL, "Adam needs a 16-byte aligned second-moment buffer");
+        const size_t nb = m->pl.P * 4;
+        if (overlap(s2, nb, m->w, nb) || overlap(s2, nb, m->v, nb) ||
+            overlap(s2, nb, m->gavg, nb) || overlap(s2, nb, m->grads, m->pl.ld * m->pl.R * 4))
+            return fail(MTX_EINVAL, "the second-moment buffer overlaps the model's buffers");
+    }
+    m->opt = kind;
+    m->b1 = beta1;
+    m->b2 = beta2;
+    m->eps = eps;
+    m->s2 = kind == MTX_OPT_ADAM ? s2 : nullptr;
+    m->opt_step = 0;
+    m->graph.reset();  // a recorded step holds the previous update rule
+    return MTX_OK;
 }
 
 int mtx_set_graph_replay(mtx_model* m, int enable)

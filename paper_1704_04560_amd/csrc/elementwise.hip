@@ -1004,14 +1004,15 @@ __global__ __launch_bounds__(256) void avg_adapt_scalar(const float* __restrict_
 
 template <bool ADAM, bool AVG>
 static hipError_t avg_adapt_launch(const float* grads, int R, size_t n, size_t ld,
-                                   const AdaptParams& p, hipStream_t s)
+                                   const AdaptParams& p, hipStream_t s, unsigned max_blocks)
 {
     auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
     const bool vec = (ld % 4 == 0) && al(grads) && al(p.w) && al(p.s1) && (!ADAM || al(p.s2)) &&
                      (!AVG || al(p.avg));
     const long long nn = (long long)n, ll = (long long)ld;
     if (vec) {
-        const dim3 grid(grid_for(n / 4 + 1, 256));
+        dim3 grid(grid_for(n / 4 + 1, 256));
+        if (max_blocks && grid.x > max_blocks) grid.x = max_blocks;
         switch (R) {
         case 1: hipLaunchKernelGGL((avg_adapt_vec4<1, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
         case 2: hipLaunchKernelGGL((avg_adapt_vec4<2, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
@@ -1028,14 +1029,14 @@ static hipError_t avg_adapt_launch(const float* grads, int R, size_t n, size_t l
 }
 
 hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool adam,
-                         const AdaptParams& p, hipStream_t s)
+                         const AdaptParams& p, hipStream_t s, unsigned max_blocks)
 {
     if (adam) {
-        if (p.avg) return avg_adapt_launch<true, true>(grads, R, n, ld, p, s);
-        return avg_adapt_launch<true, false>(grads, R, n, ld, p, s);
+        if (p.avg) return avg_adapt_launch<true, true>(grads, R, n, ld, p, s, max_blocks);
+        return avg_adapt_launch<true, false>(grads, R, n, ld, p, s, max_blocks);
     }
-    if (p.avg) return avg_adapt_launch<false, true>(grads, R, n, ld, p, s);
-    return avg_adapt_launch<false, false>(grads, R, n, ld, p, s);
+    if (p.avg) return avg_adapt_launch<false, true>(grads, R, n, ld, p, s, max_blocks);
+    return avg_adapt_launch<false, false>(grads, R, n, ld, p, s, max_blocks);
 }
 
 }  // namespace mtx

@@ -203,7 +203,8 @@ struct AdaptParams {
     float* avg;
     float lr, b1, c1, b2, c2, ib1, ib2, eps;
 };
+// max_blocks > 0 caps the grid as for average_update.
 hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool adam,
-                         const AdaptParams& p, hipStream_t s);
+                         const AdaptParams& p, hipStream_t s, unsigned max_blocks = 0);
 
 }  // namespace mtx

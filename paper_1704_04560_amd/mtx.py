@@ -19,10 +19,11 @@ LIB_PATH = os.path.join(HERE, "libmtx.so")
 MTX_OK, MTX_EINVAL, MTX_ENOMEM, MTX_EHIP, MTX_EUNSUPPORTED = 0, -1, -2, -3, -4
 MTX_F32, MTX_BF16 = 0, 1
 MTX_FC, MTX_CONV, MTX_MAXPOOL = 0, 1, 2
+MTX_OPT_MOMENTUM, MTX_OPT_ADAM, MTX_OPT_ADAGRAD = 0, 1, 2
 
 EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_train_step", "mtx_average_grads",
            "mtx_sgd_update", "mtx_adam_update", "mtx_adagrad_update", "mtx_get_params",
-           "mtx_set_params", "mtx_get_layer_output",
+           "mtx_set_params", "mtx_get_layer_output", "mtx_set_optimizer",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
            "mtx_set_layerwise_update", "mtx_set_timing",
            "mtx_get_timing", "mtx_free_model", "mtx_last_error")
@@ -85,6 +86,7 @@ def lib() -> C.CDLL:
             "mtx_get_layer_output": (i32, [vp, i32, vp, sz]),
             "mtx_get_pool_argmax": (i32, [vp, i32, vp, sz]),
             "mtx_set_graph_replay": (i32, [vp, i32]),
+            "mtx_set_optimizer": (i32, [vp, i32, f32, f32, f32, vp]),
             "mtx_set_layerwise_update": (i32, [vp, i32]),
             "mtx_set_overlap": (i32, [vp, i32]),
             "mtx_set_timing": (i32, [vp, i32]),
@@ -178,6 +180,10 @@ def mtx_adagrad_update(w, acc, grads, R, n, ld, lr, eps, avg_out=None, stream=No
                                     _ptr(avg_out), _stream(stream)))
 
 
+def mtx_set_optimizer(handle, kind, beta1=0.9, beta2=0.999, eps=1e-8, s2=None):
+    _check(lib().mtx_set_optimizer(handle, kind, beta1, beta2, eps, _ptr(s2)))
+
+
 def mtx_get_params(handle, w_host: np.ndarray, v_host: Optional[np.ndarray] = None):
     _check(lib().mtx_get_params(handle, _ptr(w_host), _ptr(v_host)))
 
@@ -265,6 +271,14 @@ class Model:
 
     def train_step(self, x, labels, lr, momentum, loss_out=None, stream=None):
         mtx_train_step(self.handle, x, labels, lr, momentum, loss_out, stream)
+
+    def set_optimizer(self, kind, beta1=0.9, beta2=0.999, eps=1e-8):
+        """Select the update rule of train_step; Adam gets a zeroed second-moment buffer."""
+        import torch
+        self.s2 = None
+        if kind == MTX_OPT_ADAM:
+            self.s2 = torch.zeros(self.P, dtype=torch.float32, device=self.w.device)
+        mtx_set_optimizer(self.handle, kind, beta1, beta2, eps, self.s2)
 
     def get_params(self):
         w = np.empty(self.P, np.float32)

@@ -104,6 +104,7 @@ def test_adaptive_update_argument_errors_need_no_device():
 
 def test_model_call_errors_need_no_device():
     assert _err(mtx.mtx_train_step, None, 16, 16, 0.1, 0.0) == mtx.MTX_EINVAL
+    assert _err(mtx.mtx_set_optimizer, None, mtx.MTX_OPT_ADAM) == mtx.MTX_EINVAL
     assert _err(mtx.mtx_get_params, None, np.zeros(4, np.float32)) == mtx.MTX_EINVAL
     L = wl.layer_tuples(wl.MLP)
     d = mtx.make_desc((784, 1, 1), L, wl.F32)

@@ -288,3 +288,142 @@ def test_shard_count_invariance(net_name):
         d = deltas[R]
         assert np.linalg.norm(d - ref) <= tol * np.linalg.norm(ref), R
         assert np.max(np.abs(d - ref)) <= tol * np.max(np.abs(ref)) + 1e-7, R
+
+
+@pytest.mark.parametrize("net_name,R,Nb,steps,lr,mu", [("mlp", 2, 32, 10, 0.01, 0.0),
+                                                        ("lenet", 4, 8, 10, 0.01, 0.9),
+                                                        ("lenet", 1, 32, 10, 0.01, 0.9)])
+def test_free_running_trajectory_matches_oracle(net_name, R, Nb, steps, lr, mu):
+    """Several steps with no state copied between the two sides (the analogue of the paper's
+    loss curves, Fig. 5): the GPU model and the oracle each start from the same initial weights
+    and run `steps` steps on the same batches from their own state.  The per-step losses and
+    the total weight change must agree to the parity tolerance; with fp32 compute the rounding
+    differences that accumulate over the steps stay well inside it.  (bf16 steps are compared
+    from a shared state each step, in the tests above: once two bf16 trajectories differ by
+    rounding, ReLU and pooling decisions near ties flip, which no per-step hint can follow; over
+    four CIFAR steps that moved the total weight change by 8% with the losses still agreeing to
+    2e-2.)"""
+    net = {"mlp": wl.MLP, "lenet": wl.LENET}[net_name]
+    layers = wl.layer_tuples(net)
+    prec = "f32"
+    tol = parity.TOL[net.dtype]
+    _say(f"[case] free-running trajectory {net_name} R={R} Nb={Nb} steps={steps}")
+    model = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=21)
+    w0 = orc.init_glorot(net.in_shape, layers, 21)
+    w, v = w0.copy(), np.zeros_like(w0)
+    loss_dev = torch.zeros(1, device="cuda")
+    lg, lo = [], []
+    for step in range(steps):
+        x, y = wl.make_batch(net, R * Nb, seed=5000 + step)
+        model.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), lr, mu, loss_dev)
+        res = orc.train_step(net.in_shape, layers, R, x, y, w, v if mu else None, lr, mu,
+                             prec=prec, want_grads=False)
+        lg.append(float(loss_dev.item()))
+        lo.append(res.loss)
+        w = res.w_new
+        if mu:
+            v = res.v_new
+    torch.cuda.synchronize()
+    wg, vg = model.get_params()
+    model.close()
+    lg, lo = np.array(lg), np.array(lo)
+    assert np.all(np.abs(lg - lo) <= tol * np.abs(lo)), (lg, lo)
+    parity.assert_update_close(wg, w, w0, tol, "w after the trajectory")
+    if mu:
+        parity.assert_tensor_close(vg, v, tol, "velocity after the trajectory")
+    # the trajectory went somewhere: the loss moved over the steps
+    assert abs(lo[-1] - lo[0]) > 10 * tol * abs(lo[0])
+
+
+# ---- Adam and AdaGrad as the update rule of the training step ----------------------------------
+
+ADAM = (0.9, 0.999, 1e-8)
+
+
+@pytest.mark.parametrize("kind", [mtx.MTX_OPT_ADAM, mtx.MTX_OPT_ADAGRAD])
+@pytest.mark.parametrize("layerwise", [False, True])
+def test_train_step_with_adaptive_update_equals_gradients_then_update(kind, layerwise):
+    """A step with Adam / AdaGrad selected is bit-identical to a step that only computes the
+    gradients (lr = 0, no momentum) followed by mtx_adam_update / mtx_adagrad_update on them
+    (whose arithmetic the update tests compare with the oracle), over three steps; also with the
+    per-layer update on the third stream."""
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    R, Nb, lr = 4, 8, 1e-3
+    _say(f"[case] adaptive update in the step kind={kind} layerwise={layerwise}")
+    a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
+    b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=3)
+    a.set_optimizer(kind, *ADAM)
+    w_init, _ = a.get_params()
+    if layerwise:
+        mtx.mtx_set_overlap(a.handle, True)
+        mtx.mtx_set_layerwise_update(a.handle, True)
+    if kind == mtx.MTX_OPT_ADAGRAD:
+        w0, _ = a.get_params()
+        acc0 = wl.make_square_state(a.P, seed=3, terms=2)
+        a.set_params(w0, acc0)
+        b.set_params(w0, acc0)
+    s2b = torch.zeros(b.P, device="cuda")
+    avg_b = torch.empty(b.P, device="cuda")
+    for t in (1, 2, 3):
+        x, y = wl.make_batch(net, R * Nb, seed=70 + t)
+        xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+        a.train_step(xd, yd, lr, 0.0)
+        b.train_step(xd, yd, 0.0, 0.0)
+        if kind == mtx.MTX_OPT_ADAM:
+            mtx.mtx_adam_update(b.w, b.v, s2b, b.grads, R, b.P, b.ld, lr, *ADAM, t, avg_b)
+        else:
+            mtx.mtx_adagrad_update(b.w, b.v, b.grads, R, b.P, b.ld, lr, ADAM[2], avg_b)
+        torch.cuda.synchronize()
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), t
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), t
+        assert torch.equal(a.grad_avg, avg_b), t
+        if kind == mtx.MTX_OPT_ADAM:
+            assert torch.equal(a.s2, s2b), t
+    assert np.abs(wa - w_init).max() > 0  # the steps moved the weights
+    a.close()
+    b.close()
+
+
+@pytest.mark.parametrize("kind", [mtx.MTX_OPT_ADAM, mtx.MTX_OPT_ADAGRAD])
+def test_train_step_with_adaptive_update_matches_oracle(kind):
+    """Three steps of LeNet (B = 32, R = 4) with Adam / AdaGrad inside mtx_train_step against the
+    oracle's step gradients followed by its Adam / AdaGrad, each step from the same state.  The
+    incoming second moment (Adam) and accumulator (AdaGrad) are non-zero, so the update is
+    well-conditioned and the gradients' own rounding differences stay within tolerance."""
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    geo = orc.geometry(net.in_shape, layers)
+    R, Nb, lr = 4, 8, 1e-3
+    tol = parity.TOL[net.dtype]
+    _say(f"[case] adaptive update vs oracle kind={kind}")
+    model = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=8)
+    model.set_optimizer(kind, *ADAM)
+    P = model.P
+    w = orc.init_glorot(net.in_shape, layers, 8)
+    s1 = wl.make_velocity(P, seed=8) if kind == mtx.MTX_OPT_ADAM else wl.make_square_state(P, seed=8, terms=4)
+    s2 = wl.make_square_state(P, seed=9, terms=4)
+    for t in (1, 2, 3):
+        x, y = wl.make_batch(net, R * Nb, seed=90 + t)
+        model.set_params(w, s1)
+        if kind == mtx.MTX_OPT_ADAM:
+            model.s2.copy_(torch.from_numpy(s2).cuda())
+        model.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), lr, 0.0)
+        torch.cuda.synchronize()
+        gp, gr = parity.gpu_decisions(model, geo)
+        res, _ = parity.oracle_step_matching(net, layers, R, x, y, w, None, 0.0, 0.0, "f32", gp, gr)
+        if kind == mtx.MTX_OPT_ADAM:
+            gavg, w_new, s1_new, s2_new = orc.average_adam(res.grads, w, s1, s2, lr, *ADAM, t)
+        else:
+            gavg, w_new, s1_new = orc.average_adagrad(res.grads, w, s1, lr, ADAM[2])
+        wg, s1g = model.get_params()
+        parity.assert_tensor_close(model.grad_avg.cpu().numpy(), gavg, tol, f"average t={t}")
+        parity.assert_tensor_close(s1g, s1_new, tol, f"first state t={t}")
+        parity.assert_update_close(wg, w_new, w, tol, f"w t={t}")
+        if kind == mtx.MTX_OPT_ADAM:
+            parity.assert_tensor_close(model.s2.cpu().numpy(), s2_new, tol, f"second moment t={t}")
+            s2 = s2_new
+        w, s1 = w_new, s1_new
+    model.close()

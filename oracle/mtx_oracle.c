@@ -23,6 +23,16 @@
  *   - Fig. 1 (AlexNet: convolution + fully connected layers) and Sec. I (MLP / CNN): the layer
  *     types: fully connected, convolution (stride, zero padding, groups), max-pooling, ReLU, and a
  *     softmax cross-entropy loss (the paper trains 1000-class ImageNet classifiers, Table II).
+ *   - Table II also lists ResNet-50 and InceptionV3, whose building blocks add two layer types:
+ *     batch normalisation and the residual addition.  Batch normalisation (Ioffe and Szegedy)
+ *     normalises every channel by the mean and the biased variance over the samples and
+ *     positions of the replica's own shard (each replica sees only its shard, so these
+ *     statistics are per shard), y = gamma * (x - mean) / sqrt(var + eps) + beta, eps = 1e-3
+ *     (TensorFlow's default); its gradients follow from that definition by the chain rule.
+ *     Because the statistics are per shard, the average of the replica gradients of a network
+ *     with batch normalisation is not the full-batch gradient.  The residual addition sums the
+ *     previous layer's output and the output of an earlier layer of the same shape (He et al.);
+ *     its gradient reaches both.
  *
  * The paper gives no formula for any of these; the code below is the textbook definition of
  * each, written as direct loops in double precision.  Readings taken where the paper is silent:
@@ -55,6 +65,10 @@
 #define ORC_FC 0
 #define ORC_CONV 1
 #define ORC_MAXPOOL 2
+#define ORC_BN 3  /* batch normalisation: params gamma[c] (as W) and beta[c] (as b) */
+#define ORC_ADD 4 /* residual addition: k = index of the earlier layer whose output is added */
+
+#define ORC_BN_EPS 1e-3
 
 #define ORC_OK 0
 #define ORC_EINVAL -1
@@ -153,6 +167,22 @@ int orc_plan(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, orc
             g->oc = c;
             g->oh = (h - g->k) / g->s + 1;
             g->ow = (w - g->k) / g->s + 1;
+        } else if (L[i].kind == ORC_BN) {
+            if (L[i].out != 0 && L[i].out != c) return ORC_EINVAL;
+            g->k = 1; g->s = 1; g->p = 0; g->g = 1;
+            g->oc = c; g->oh = h; g->ow = w;
+            g->w_len = c;
+            g->b_len = c;
+        } else if (L[i].kind == ORC_ADD) {
+            /* the source is an earlier layer (not the previous one) of this layer's input shape,
+             * and no layer is the source of two additions */
+            int src = L[i].k;
+            if (src < 0 || src > i - 2) return ORC_EINVAL;
+            if (G[src].oc != c || G[src].oh != h || G[src].ow != w) return ORC_EINVAL;
+            for (int j = src + 1; j < i; j++)
+                if (G[j].kind == ORC_ADD && G[j].k == src) return ORC_EINVAL;
+            g->k = src; g->s = 1; g->p = 0; g->g = 1;
+            g->oc = c; g->oh = h; g->ow = w;
         } else {
             return ORC_EINVAL;
         }
@@ -351,6 +381,64 @@ void orc_maxpool_bwd(int N, int C, int H, int W, int K, int S, const int32_t* ar
         }
 }
 
+/* Batch normalisation of one shard, NCHW with N samples: for every channel the mean and the
+ * biased variance over (n, h, w), inv = 1 / sqrt(var + eps), y = gamma (x - mean) inv + beta.
+ * mean and inv are returned for the backward pass. */
+void orc_bn_fwd(int N, int C, int HW, const double* x, const double* gamma, const double* beta,
+                double* y, double* mean, double* inv)
+{
+    const double M = (double)N * HW;
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < C; c++) {
+        double s = 0.0;
+        for (int n = 0; n < N; n++)
+            for (int t = 0; t < HW; t++) s += x[((long)n * C + c) * HW + t];
+        const double m = s / M;
+        double v = 0.0;
+        for (int n = 0; n < N; n++)
+            for (int t = 0; t < HW; t++) {
+                const double d = x[((long)n * C + c) * HW + t] - m;
+                v += d * d;
+            }
+        const double iv = 1.0 / sqrt(v / M + ORC_BN_EPS);
+        mean[c] = m;
+        inv[c] = iv;
+        for (int n = 0; n < N; n++)
+            for (int t = 0; t < HW; t++) {
+                const long o = ((long)n * C + c) * HW + t;
+                y[o] = gamma[c] * (x[o] - m) * iv + beta[c];
+            }
+    }
+}
+
+/* Gradients of batch normalisation with the statistics of the same shard (the chain rule through
+ * mean and variance): with xhat = (x - mean) inv and M = N*H*W,
+ * dgamma = sum dy xhat, dbeta = sum dy, dx = gamma inv (dy - dbeta / M - xhat dgamma / M). */
+void orc_bn_bwd(int N, int C, int HW, const double* x, const double* gamma, const double* mean,
+                const double* inv, const double* dy, double* dx, double* dgamma, double* dbeta)
+{
+    const double M = (double)N * HW;
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < C; c++) {
+        double sd = 0.0, sdx = 0.0;
+        for (int n = 0; n < N; n++)
+            for (int t = 0; t < HW; t++) {
+                const long o = ((long)n * C + c) * HW + t;
+                sd += dy[o];
+                sdx += dy[o] * (x[o] - mean[c]) * inv[c];
+            }
+        dgamma[c] = sdx;
+        dbeta[c] = sd;
+        if (!dx) continue;
+        for (int n = 0; n < N; n++)
+            for (int t = 0; t < HW; t++) {
+                const long o = ((long)n * C + c) * HW + t;
+                const double xh = (x[o] - mean[c]) * inv[c];
+                dx[o] = gamma[c] * inv[c] * (dy[o] - sd / M - xh * sdx / M);
+            }
+    }
+}
+
 /* Softmax cross-entropy per sample: loss[n] = logsumexp(z[n]) - z[n][y[n]];
  * dz[n][c] = (softmax(z[n])[c] - [c == y[n]]) * scale.  logsumexp subtracts the row maximum. */
 void orc_softmax_xent(int N, int NC, const double* z, const int32_t* y, double scale,
@@ -396,7 +484,12 @@ int orc_init_glorot(int in_c, int in_h, int in_w, int n_layers, const orc_layer*
     if (rc) { free(G); return rc; }
     for (int l = 0; l < n_layers; l++) {
         orc_geom* g = &G[l];
-        if (g->kind == ORC_MAXPOOL) continue;
+        if (g->kind == ORC_MAXPOOL || g->kind == ORC_ADD) continue;
+        if (g->kind == ORC_BN) { /* gamma = 1, beta = 0: the identity at the start */
+            for (long i = 0; i < g->w_len; i++) w[g->w_off + i] = 1.0f;
+            for (long i = 0; i < g->b_len; i++) w[g->b_off + i] = 0.0f;
+            continue;
+        }
         double fan_in, fan_out;
         if (g->kind == ORC_CONV) {
             fan_in = (double)(g->c / g->g) * g->k * g->k;
@@ -482,12 +575,15 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
     double** e = (double**)calloc((size_t)n_layers + 1, sizeof(double*));  /* error bounds */
     double** z = (double**)calloc((size_t)n_layers, sizeof(double*));      /* pre-activations */
     int32_t** am = (int32_t**)calloc((size_t)n_layers, sizeof(int32_t*));  /* pool argmax */
+    double** bnm = (double**)calloc((size_t)n_layers, sizeof(double*));    /* BN mean */
+    double** bni = (double**)calloc((size_t)n_layers, sizeof(double*));    /* BN 1/std */
+    double** skipg = (double**)calloc((size_t)n_layers, sizeof(double*));  /* residual grads */
     double* lossn = (double*)malloc(sizeof(double) * (size_t)Nb);
     double* dbuf = NULL;
     double* dbuf2 = NULL;
     double* gw = (double*)malloc(sizeof(double) * (size_t)P);
     if (!act_off || !pool_off || !relu_off || !wq || (track && !wabs) || !gsum || !a || !e || !z ||
-        !am || !lossn || !gw) {
+        !am || !bnm || !bni || !skipg || !lossn || !gw) {
         rc = ORC_ENOMEM;
         goto done;
     }
@@ -507,8 +603,18 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
             z[l] = (double*)malloc(sizeof(double) * (size_t)sz);
             if (track) e[l + 1] = (double*)calloc((size_t)sz, sizeof(double));
             if (G[l].kind == ORC_MAXPOOL) am[l] = (int32_t*)malloc(sizeof(int32_t) * (size_t)sz);
+            if (G[l].kind == ORC_BN) {
+                bnm[l] = (double*)malloc(sizeof(double) * (size_t)G[l].c);
+                bni[l] = (double*)malloc(sizeof(double) * (size_t)G[l].c);
+            }
+            if (G[l].kind == ORC_ADD) {
+                const int src = G[l].k;
+                skipg[src] = (double*)malloc(sizeof(double) * (size_t)(act_size(&G[src]) * Nb));
+                if (!skipg[src]) { rc = ORC_ENOMEM; goto done; }
+            }
             if (!a[l + 1] || !z[l] || (track && !e[l + 1]) ||
-                (G[l].kind == ORC_MAXPOOL && !am[l])) {
+                (G[l].kind == ORC_MAXPOOL && !am[l]) ||
+                (G[l].kind == ORC_BN && (!bnm[l] || !bni[l]))) {
                 rc = ORC_ENOMEM;
                 goto done;
             }
@@ -523,12 +629,19 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
         wq[i] = bf16 ? rnd_bf16((double)w[i]) : (double)w[i];
         if (track) wabs[i] = fabs(wq[i]);
     }
-    /* biases are added in float by both sides; they are never rounded to bfloat16 */
-    for (int l = 0; l < n_layers; l++)
+    /* biases are added in float by both sides; they are never rounded to bfloat16, and
+     * neither are the batch-normalisation scales (elementwise float arithmetic, no product) */
+    for (int l = 0; l < n_layers; l++) {
         for (long i = 0; i < G[l].b_len; i++) {
             wq[G[l].b_off + i] = (double)w[G[l].b_off + i];
             if (track) wabs[G[l].b_off + i] = fabs((double)w[G[l].b_off + i]);
         }
+        if (G[l].kind == ORC_BN)
+            for (long i = 0; i < G[l].w_len; i++) {
+                wq[G[l].w_off + i] = (double)w[G[l].w_off + i];
+                if (track) wabs[G[l].w_off + i] = fabs((double)w[G[l].w_off + i]);
+            }
+    }
 
     double loss_total = 0.0;
     for (int r = 0; r < R; r++) {
@@ -574,6 +687,44 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                     }
                 }
             } else {
+                const double us = ldexp(1.0, -24) + (bf16 && !last ? ldexp(1.0, -8) : ldexp(1.0, -24));
+                if (g->kind == ORC_BN) {
+                    const int HW = g->h * g->w;
+                    orc_bn_fwd(Nb, g->c, HW, a[l], wq + g->w_off, wq + g->b_off, z[l], bnm[l],
+                               bni[l]);
+                    if (track)
+                        for (int c = 0; c < g->c; c++) {
+                            /* error of a float evaluation: a few roundings of each term, the
+                             * input's own error, and its effect on the mean and the scale */
+                            double emax = 0.0;
+                            for (int n = 0; n < Nb; n++)
+                                for (int t = 0; t < HW; t++) {
+                                    const double ev = e[l][((long)n * g->c + c) * HW + t];
+                                    if (ev > emax) emax = ev;
+                                }
+                            const double gm = fabs(wq[g->w_off + c]), iv = bni[l][c];
+                            for (int n = 0; n < Nb; n++)
+                                for (int t = 0; t < HW; t++) {
+                                    const long o = ((long)n * g->c + c) * HW + t;
+                                    const double xh = fabs((a[l][o] - bnm[l][c]) * iv);
+                                    const double ez = 16.0 * ldexp(1.0, -24) *
+                                                          (gm * xh + fabs(wq[g->b_off + c])) +
+                                                      gm * iv * (e[l][o] + emax) +
+                                                      2.0 * gm * xh * emax * iv;
+                                    e[l + 1][o] = ez + 2.0 * us * (fabs(z[l][o]) + ez);
+                                    dbuf2[o] = ez;
+                                }
+                        }
+                } else if (g->kind == ORC_ADD) {
+                    const double* sa = a[g->k + 1];
+                    for (long t = 0; t < sz; t++) z[l][t] = a[l][t] + sa[t];
+                    if (track)
+                        for (long t = 0; t < sz; t++) {
+                            const double ez = e[l][t] + e[g->k + 1][t] + ldexp(1.0, -24) * fabs(z[l][t]);
+                            e[l + 1][t] = ez + 2.0 * us * (fabs(z[l][t]) + ez);
+                            dbuf2[t] = ez;
+                        }
+                } else {
                 layer_fwd(g, Nb, a[l], wq + g->w_off, wq + g->b_off, z[l]);
                 if (track) {
                     /* forward error bound of a float evaluation in any summation order:
@@ -586,12 +737,12 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                     for (long t = 0; t < insz; t++) absa[t] = fabs(a[l][t]);
                     layer_fwd(g, Nb, absa, wabs + g->w_off, wabs + g->b_off, e[l + 1]);
                     layer_fwd(g, Nb, e[l], wabs + g->w_off, NULL, dbuf2);
-                    double us = ldexp(1.0, -24) + (bf16 && !last ? ldexp(1.0, -8) : ldexp(1.0, -24));
                     for (long t = 0; t < sz; t++) {
                         double ez = gam * e[l + 1][t] + dbuf2[t];
                         e[l + 1][t] = ez + 2.0 * us * (fabs(z[l][t]) + ez);
                         dbuf2[t] = ez;     /* bound of the pre-activation itself */
                     }
+                }
                 }
                 for (long t = 0; t < sz; t++) {
                     double zt = z[l][t];
@@ -641,12 +792,31 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
             long sz = act_size(g) * Nb;
             long insz = (long)g->c * g->h * g->w * Nb;
             double* dnext = (dcur == dbuf) ? dbuf2 : dbuf;
+            /* a layer whose output a residual addition also read: its output gradient is the
+             * sum of the two paths (each stored in the storage precision, the sum rounded) */
+            if (skipg[l])
+                for (long t = 0; t < sz; t++) dcur[t] = store(dcur[t] + skipg[l][t]);
             if (g->relu)
                 for (long t = 0; t < sz; t++)
                     if (z[l][t] <= 0.0) dcur[t] = 0.0;
             if (g->kind == ORC_MAXPOOL) {
                 orc_maxpool_bwd(Nb, g->c, g->h, g->w, g->k, g->s, am[l], dcur, dnext);
                 for (long t = 0; t < insz; t++) dnext[t] = store(dnext[t]);
+            } else if (g->kind == ORC_ADD) {
+                /* the gradient reaches the previous layer and the source layer unchanged */
+                for (long t = 0; t < sz; t++) skipg[g->k][t] = dcur[t];
+                for (long t = 0; t < insz; t++) dnext[t] = dcur[t];
+            } else if (g->kind == ORC_BN) {
+                double* dx = (l > 0) ? dnext : NULL;
+                orc_bn_bwd(Nb, g->c, g->h * g->w, a[l], wq + g->w_off, bnm[l], bni[l], dcur, dx,
+                           gw + g->w_off, gw + g->b_off);
+                if (dx)
+                    for (long t = 0; t < insz; t++) dx[t] = store(dx[t]);
+                for (long i = 0; i < g->w_len + g->b_len; i++) {
+                    float gf = (float)gw[g->w_off + i];
+                    if (grads) grads[(long)r * P + g->w_off + i] = gf;
+                    gsum[g->w_off + i] += (double)gf;
+                }
             } else {
                 double* dx = (l > 0) ? dnext : NULL;
                 if (g->kind == ORC_CONV)
@@ -689,7 +859,10 @@ done:
     if (e) for (int l = 0; l <= n_layers; l++) free(e[l]);
     if (z) for (int l = 0; l < n_layers; l++) free(z[l]);
     if (am) for (int l = 0; l < n_layers; l++) free(am[l]);
-    free(a); free(e); free(z); free(am);
+    if (bnm) for (int l = 0; l < n_layers; l++) free(bnm[l]);
+    if (bni) for (int l = 0; l < n_layers; l++) free(bni[l]);
+    if (skipg) for (int l = 0; l < n_layers; l++) free(skipg[l]);
+    free(a); free(e); free(z); free(am); free(bnm); free(bni); free(skipg);
     free(act_off); free(pool_off); free(relu_off);
     free(wq); free(wabs); free(gsum); free(lossn); free(dbuf); free(dbuf2); free(gw); free(G);
     return rc;

@@ -2,8 +2,8 @@
 
 The oracle is plain C in ``mtx_oracle.c``; this module only marshals numpy arrays.  It takes the
 network as (C, H, W) plus a list of layer tuples (kind, out, k, stride, pad, groups, relu) with
-kind 0 = fully connected, 1 = convolution, 2 = max-pool, so it needs nothing from the GPU
-library.
+kind 0 = fully connected, 1 = convolution, 2 = max-pool, 3 = batch normalisation, 4 = residual
+addition of the output of layer k, so it needs nothing from the GPU library.
 """
 from __future__ import annotations
 
@@ -87,10 +87,16 @@ def geometry(in_shape, layers):
         elif kind == 0:
             oc, oh, ow = o, 1, 1
             wl, bl = o * c * h * w, o
+        elif kind == 3:  # batch normalisation: gamma, beta per channel
+            oc, oh, ow = c, h, w
+            wl, bl = c, c
+        elif kind == 4:  # residual addition of layer k's output
+            oc, oh, ow = c, h, w
+            wl, bl = 0, 0
         else:
             oc, oh, ow = c, (h - k) // s + 1, (w - k) // s + 1
             wl, bl = 0, 0
-        out.append(dict(kind=kind, relu=relu, in_shape=(c, h, w), out_shape=(oc, oh, ow),
+        out.append(dict(kind=kind, relu=relu, k=k, in_shape=(c, h, w), out_shape=(oc, oh, ow),
                         w_off=off, w_len=wl, b_off=off + wl, b_len=bl))
         off += wl + bl
         c, h, w = oc, oh, ow

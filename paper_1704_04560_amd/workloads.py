@@ -26,7 +26,7 @@ from typing import List, Tuple
 
 import numpy as np
 
-FC, CONV, MAXPOOL = 0, 1, 2
+FC, CONV, MAXPOOL, BN, ADD = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 
 STREAM_X, STREAM_LABELS, STREAM_W, STREAM_V, STREAM_G, STREAM_S2 = 0, 1, 2, 3, 4, 5
@@ -53,6 +53,16 @@ def conv(out, k, stride=1, pad=0, groups=1, relu=False):
 
 def maxpool(k, stride):
     return Layer(MAXPOOL, 0, k, stride, 0, 1, False)
+
+
+def bn(relu=False):
+    """Batch normalisation over the shard, gamma and beta per channel."""
+    return Layer(BN, 0, 0, 1, 0, 1, relu)
+
+
+def add(src, relu=False):
+    """Residual addition of the output of layer `src` (an earlier layer of the same shape)."""
+    return Layer(ADD, 0, src, 1, 0, 1, relu)
 
 
 @dataclass(frozen=True)

@@ -269,3 +269,124 @@ def test_relu_hint_accepts_only_values_within_the_error_bound():
     same = base.relu_mask.astype(np.int8)
     ok = orc.train_step(net.in_shape, layers, 1, x, y, w, None, 0.0, 0.0, relu_hint=same)
     assert np.array_equal(ok.gavg, base.gavg)
+
+
+# ---- batch normalisation and residual addition (the building blocks of Table II's ResNet-50) --
+
+def _residual_net(dtype=wl.F32):
+    """A residual block with batch normalisation: conv-BN-ReLU-conv-BN, added to the first
+    BN-ReLU output, ReLU; then pooling, a 1x1 convolution with BN-ReLU and the classifier."""
+    layers = (wl.conv(4, 3, pad=1), wl.bn(relu=True), wl.conv(4, 3, pad=1), wl.bn(),
+              wl.add(1, relu=True), wl.maxpool(2, 2), wl.conv(6, 1), wl.bn(relu=True), wl.fc(5))
+    net = wl.Net("residual", (3, 8, 8), layers, dtype, "normal")
+    return net, wl.layer_tuples(net)
+
+
+def _perturbed_params(net, layers, seed):
+    """Glorot weights (BN: gamma = 1, beta = 0) moved off their initial values, so that every
+    parameter, the BN scales and shifts included, takes part."""
+    geo = orc.geometry(net.in_shape, layers)
+    w = orc.init_glorot(net.in_shape, layers, seed=seed)
+    g = np.random.default_rng(seed + 1)
+    for gg in geo:
+        if gg["kind"] == 3:
+            w[gg["w_off"]:gg["w_off"] + gg["w_len"]] = g.uniform(0.5, 1.5, gg["w_len"])
+        if gg["b_len"]:
+            w[gg["b_off"]:gg["b_off"] + gg["b_len"]] = g.normal(0, 0.1, gg["b_len"])
+    return geo, w
+
+
+@pytest.mark.parametrize("R", [1, 2])
+def test_residual_bn_step_matches_torch_autograd(R):
+    """Every shard's loss and gradient against torch float64 autograd (F.batch_norm in training
+    mode over the shard's samples, tensor addition for the residual)."""
+    net, layers = _residual_net()
+    geo, w = _perturbed_params(net, layers, 3)
+    x, y = wl.make_batch(net, 6 * R, seed=5)
+    res = orc.train_step(net.in_shape, layers, R, x, y, w, None, 0.01, 0.0, prec="exact")
+    gref, lref = torch_ref.shard_grads(layers, geo, w, x, y, R)
+    for r in range(R):
+        assert abs(res.shard_loss[r] - lref[r]) <= 1e-6 * abs(lref[r])
+        assert _rel(res.grads[r], gref[r]) < 2e-7
+        for gg in geo:  # every parameter tensor on its own, the BN ones included
+            sl = slice(gg["w_off"], gg["b_off"] + gg["b_len"])
+            if gg["w_len"]:
+                assert _rel(res.grads[r][sl], gref[r][sl]) < 1e-6, gg
+
+
+def test_residual_bn_finite_differences():
+    net, layers = _residual_net()
+    geo, w = _perturbed_params(net, layers, 7)
+    P = w.size
+    x, y = wl.make_batch(net, 6, seed=9)
+
+    def run(wv):
+        return orc.train_step(net.in_shape, layers, 2, x, y, wv, None, 0.0, 0.0, prec="exact",
+                              want_grads=False, want_decisions=True)
+
+    base = run(w)
+    checked = 0
+    for i in np.random.default_rng(2).choice(P, size=80, replace=False):
+        h = 1e-5
+        wp, wm = w.copy(), w.copy()
+        wp[i] += h
+        wm[i] -= h
+        rp, rm = run(wp), run(wm)
+        if not (np.array_equal(rp.pool_argmax, base.pool_argmax) and
+                np.array_equal(rm.pool_argmax, base.pool_argmax) and
+                np.array_equal(rp.relu_mask, base.relu_mask) and
+                np.array_equal(rm.relu_mask, base.relu_mask)):
+            continue
+        fd = (rp.loss - rm.loss) / (float(wp[i]) - float(wm[i]))
+        g = float(base.gavg[i])
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(g)) + 1e-7, (i, fd, g)
+        checked += 1
+    assert checked >= 50
+
+
+def test_bias_before_batch_norm_has_zero_gradient():
+    """Batch normalisation removes any per-channel constant from its input, so the bias of the
+    convolution that feeds it cannot change the loss: its gradient vanishes (to rounding)."""
+    net, layers = _residual_net()
+    geo, w = _perturbed_params(net, layers, 11)
+    x, y = wl.make_batch(net, 8, seed=12)
+    res = orc.train_step(net.in_shape, layers, 2, x, y, w, None, 0.0, 0.0, prec="exact")
+    for li in (0, 2, 6):  # the convolutions followed by BN
+        gg = geo[li]
+        gb = res.grads[:, gg["b_off"]:gg["b_off"] + gg["b_len"]]
+        gw = res.grads[:, gg["w_off"]:gg["w_off"] + gg["w_len"]]
+        assert np.abs(gb).max() <= 1e-6 * np.abs(gw).max(), li
+
+
+def test_shard_statistics_make_the_average_differ_from_the_full_batch_gradient():
+    """With batch normalisation each replica normalises by its own shard's statistics, so the
+    average of the R shard gradients is not the gradient of the full batch (unlike the networks
+    without it, test_shard_average_equals_full_batch_gradient); without BN the residual network
+    keeps that identity."""
+    net, layers = _residual_net()
+    geo, w = _perturbed_params(net, layers, 13)
+    x, y = wl.make_batch(net, 8, seed=14)
+    r4 = orc.train_step(net.in_shape, layers, 4, x, y, w, None, 0.0, 0.0, prec="exact")
+    r1 = orc.train_step(net.in_shape, layers, 1, x, y, w, None, 0.0, 0.0, prec="exact")
+    assert _rel(r4.gavg, r1.gavg) > 1e-3
+    plain = tuple(l for l in layers if l[0] != 3)
+    plain = tuple((4, 0, 0, 1, 0, 1, t[6]) if t[0] == 4 else t for t in plain)  # src 1 -> 0
+    P = orc.param_count(net.in_shape, plain)
+    wp = orc.init_glorot(net.in_shape, plain, seed=15)
+    p4 = orc.train_step(net.in_shape, plain, 4, x, y, wp, None, 0.0, 0.0, prec="exact")
+    p1 = orc.train_step(net.in_shape, plain, 1, x, y, wp, None, 0.0, 0.0, prec="exact")
+    assert P == wp.size and _rel(p4.gavg, p1.gavg) < 1e-6  # float rounding of each shard
+
+
+def test_residual_bn_layers_are_validated():
+    ok = [wl.layer_tuples(_residual_net()[0])]
+    orc.param_count((3, 8, 8), ok[0])
+    bad_src = list(ok[0])
+    bad_src[4] = (4, 0, 3, 1, 0, 1, 1)  # the previous layer is not a valid source
+    bad_shape = [wl.layer_tuples(wl.Net("x", (3, 8, 8), (wl.conv(4, 3, pad=1), wl.conv(4, 3),
+                                                         wl.add(0), wl.fc(2)), wl.F32, "normal"))]
+    bad_bn = list(ok[0])
+    bad_bn[1] = (3, 7, 0, 1, 0, 1, 1)  # BN out must equal its channel count
+    for L in (bad_src, bad_shape[0], bad_bn):
+        with pytest.raises(ValueError):
+            orc.param_count((3, 8, 8), L)

@@ -1,7 +1,8 @@
 """Double-precision torch autograd model of a network given as layer tuples.
 
 Used only to pin the CPU oracle: it is an independent implementation of the same definitions
-(torch's conv2d / max_pool2d / linear / cross_entropy and autograd), run on the CPU in float64.
+(torch's conv2d / max_pool2d / linear / batch_norm / cross_entropy and autograd), run on the
+CPU in float64.
 """
 import torch
 import torch.nn.functional as F
@@ -11,7 +12,7 @@ def split_params(geo, w):
     """Views of the flat parameter vector as per-layer (W, b) tensors in logical layout."""
     out = []
     for g in geo:
-        if g["kind"] == 2:
+        if g["kind"] in (2, 4):
             out.append(None)
             continue
         c, h, wd = g["in_shape"]
@@ -33,6 +34,10 @@ def forward(layers, geo, wt, x):
         elif kind == 0:
             a = a.reshape(a.shape[0], -1)
             a = F.linear(a, pr[0].view(o, -1), pr[1])
+        elif kind == 3:  # batch statistics of this forward's samples (one shard)
+            a = F.batch_norm(a, None, None, pr[0], pr[1], training=True, eps=1e-3)
+        elif kind == 4:
+            a = a + acts[k]
         else:
             a = F.max_pool2d(a, k, s)
         if relu:

@@ -12,8 +12,8 @@ Prints one JSON line.  `value` is samples/s of the whole job (one GPU); `rooflin
 kernel that takes the most time in the step, timed in place with HIP events on the step's
 stream (its `traffic` comes from a committed rocprofv3 counter summary of the same kernel
 sources, else null); `grad_avg_update` is the fused average + momentum kernel at the
-61M-element, 16-buffer size; `other_workloads` are short runs of the bf16 CIFAR and AlexNet
-workloads; `shard_sweep` is samples/s of the same workload at the same global batch for shard
+61M-element, 16-buffer size; `other_workloads` are short runs of the bf16 CIFAR, AlexNet and
+residual (batch-normalised) workloads; `shard_sweep` is samples/s of the same workload at the same global batch for shard
 counts R = 1 .. 16; `cpu_baseline` is the CPU oracle timed on a bounded sample of the same
 workload.
 """
@@ -42,6 +42,8 @@ def geometry(net):
             oc, oh, ow = l.out, (h + 2 * l.pad - l.k) // l.stride + 1, (w + 2 * l.pad - l.k) // l.stride + 1
         elif l.kind == wl.FC:
             oc, oh, ow = l.out, 1, 1
+        elif l.kind in (wl.BN, wl.ADD):
+            oc, oh, ow = c, h, w
         else:
             oc, oh, ow = c, (h - l.k) // l.stride + 1, (w - l.k) // l.stride + 1
         out.append(dict(layer=l, c=c, h=h, w=w, oc=oc, oh=oh, ow=ow))
@@ -72,6 +74,18 @@ def site_work(name, layer, geo, wkl, es):
             return "hbm", in_sz * es + out_sz * (es + 1)
         if name == "pool_bwd":
             return "hbm", out_sz * (es + 1) + in_sz * es * 2  # dy + argmax, mask + dx
+        if name == "bn_fwd":  # the statistics pass reads x
+            return "hbm", in_sz * es
+        if name == "bn_fwd_apply":  # x read, y written
+            return "hbm", 2 * in_sz * es
+        if name == "bn_bwd":  # x and dy read
+            return "hbm", 2 * in_sz * es
+        if name == "bn_bwd_apply":  # x, dy and the mask read, dx written
+            return "hbm", 4 * in_sz * es
+        if name in ("add_fwd", "skip_add"):  # two read, one written
+            return "hbm", 3 * out_sz * es
+        if name == "add_bwd":  # dy and two masks read, dx and the kept gradient written
+            return "hbm", 5 * out_sz * es
         return None, 0.0
     P = wkl_params(wkl)
     if name == "avg_update":
@@ -405,7 +419,7 @@ def main():
         out["grad_avg_update"] = microbench_avg_update(torch, mtx)
     if not args.no_extra:
         extra = {}
-        for name in ("cifar", "alexnet"):
+        for name in ("cifar", "alexnet", "resnet"):
             if name == args.workload:
                 continue
             e = measure(torch, mtx, wl, name, 20, 3)

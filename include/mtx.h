@@ -52,15 +52,24 @@ typedef enum {
 
 typedef enum { MTX_F32 = 0, MTX_BF16 = 1 } mtx_dtype;
 
-typedef enum { MTX_FC = 0, MTX_CONV = 1, MTX_MAXPOOL = 2 } mtx_kind;
+typedef enum { MTX_FC = 0, MTX_CONV = 1, MTX_MAXPOOL = 2, MTX_BN = 3, MTX_ADD = 4 } mtx_kind;
 
 /* One layer (Sec. I and Fig. 1: fully connected and convolution layers; pooling between
- * convolutions).
+ * convolutions; Table II's ResNet-50 adds batch normalisation and residual additions).
  *   MTX_FC:      out = number of outputs; relu = apply max(0, .) to the output.
  *   MTX_CONV:    out = output channels, k x k kernel, stride >= 1, zero padding pad >= 0,
  *                groups >= 1 dividing both channel counts; relu as above.
  *   MTX_MAXPOOL: k x k window (k <= 16), stride >= 1, no padding ("valid" windows); out,
  *                pad, groups and relu must be 0 (groups may also be 1).
+ *   MTX_BN:      batch normalisation with the statistics of each replica's shard (mean and
+ *                biased variance over its samples and positions, eps = 1e-3):
+ *                y = gamma (x - mean) / sqrt(var + eps) + beta; parameters gamma[c] (in the
+ *                place of W, initialised to 1) and beta[c] (in the place of b, 0); relu as
+ *                above; out may be 0 or the channel count, k, pad 0.  With per-shard statistics
+ *                the average of the shard gradients is not the full-batch gradient.
+ *   MTX_ADD:     residual addition y = x + (output of layer k), k an earlier layer other than
+ *                the previous one, with the same output shape; a layer is added at most once;
+ *                relu as above; no parameters.
  * The last layer must be MTX_FC without ReLU; its outputs are the class scores of a softmax
  * cross-entropy loss. */
 typedef struct {
@@ -237,9 +246,11 @@ int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float ep
  * recorded events and fills up to `capacity` entries, one per launch site of the step, in launch
  * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
  * Launch-site names: "prep_w" (weight layouts), "prep_x" (input layout), "fwd", "pool_fwd",
- * "softmax_xent" (with the loss mean), "wgrad" (weight and bias gradient), "dgrad", "pool_bwd",
- * "avg_update"; the second kernel of an operation is a site of its own: "<site>_reduce" (the
- * second pass of a split reduction) and "dgrad_col2im".  Timing adds one event pair per kernel;
+ * "bn_fwd", "add_fwd", "softmax_xent" (with the loss mean), "wgrad" (weight and bias gradient),
+ * "dgrad", "pool_bwd", "bn_bwd", "add_bwd", "skip_add", "avg_update"; the second kernel of an
+ * operation is a site of its own: "<site>_reduce" (the second pass of a split reduction),
+ * "dgrad_col2im" and "bn_fwd_apply" / "bn_bwd_apply" (the elementwise pass after the batch
+ * statistics).  Timing adds one event pair per kernel;
  * use it for measurement runs. */
 typedef struct {
     char name[32];

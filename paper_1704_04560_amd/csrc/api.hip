@@ -65,6 +65,9 @@ struct LayerPlan {
     size_t fw_off, bw_off;       // prepared forward / data-gradient weights (elements)
     bool run;                    // first convolution over the padded input (conv_fwd_run)
     RunGeom rg;                  // its padded input geometry
+    int src;                     // residual addition: the layer whose output is added
+    size_t stat_off;             // batch normalisation: per-shard (mean, 1/std) [R][C] floats
+    size_t skip_off;             // residual addition: gradient for the source layer [B][...]
 };
 
 constexpr size_t kNone = ~(size_t)0;
@@ -85,6 +88,7 @@ struct Plan {
     size_t prep_elems = 0;
     size_t xin_off = 0, xin_bytes = 0, prep_off = 0, jobs_off = 0, loss_off = 0;
     size_t partial_off = 0, partial_w_off = 0, col_off = 0, sync_off = 0;
+    size_t bn_part_off = 0, bn_coef_off = 0;  // batch normalisation scratch
     int n_wgrad = 0;             // layers with a weight gradient
     double gemm_flops = 0;       // multiply-adds x 2 of every matrix launch of a step
     size_t ws_bytes = 0;
@@ -112,6 +116,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     for (int i = 0; i < d->n_layers; ++i) {
         const mtx_layer& ly = d->layers[i];
         LayerPlan lp{};
+        lp.src = -1;
         lp.kind = ly.kind;
         lp.relu = ly.relu ? 1 : 0;
         lp.c = c; lp.h = h; lp.w = w;
@@ -148,6 +153,32 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             lp.oh = (h - ly.k) / ly.stride + 1;
             lp.ow = (w - ly.k) / ly.stride + 1;
             lp.w_len = 0; lp.b_len = 0;
+        } else if (ly.kind == MTX_BN) {
+            if ((ly.out != 0 && ly.out != c) || ly.k != 0 || ly.pad != 0 ||
+                (ly.stride != 0 && ly.stride != 1) || (ly.groups != 0 && ly.groups != 1))
+                return fail(MTX_EINVAL, "layer %d: batch normalisation takes only relu (out, if "
+                                        "given, must be its channel count)", i);
+            lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
+            lp.oc = c; lp.oh = h; lp.ow = w;
+            lp.w_len = c; lp.b_len = c;  // gamma, beta
+        } else if (ly.kind == MTX_ADD) {
+            const int src = ly.k;
+            if (src < 0 || src > i - 2)
+                return fail(MTX_EINVAL, "layer %d: the added layer must be an earlier layer "
+                                        "other than the previous one", i);
+            const LayerPlan& sp = pl.L[src];
+            if (sp.oc != c || sp.oh != h || sp.ow != w)
+                return fail(MTX_EINVAL, "layer %d: layer %d's output has another shape", i, src);
+            for (int j = src + 1; j < i; ++j)
+                if (pl.L[j].kind == MTX_ADD && pl.L[j].src == src)
+                    return fail(MTX_EINVAL, "layer %d: layer %d is already added once", i, src);
+            if (ly.out != 0 || ly.pad != 0 || (ly.stride != 0 && ly.stride != 1) ||
+                (ly.groups != 0 && ly.groups != 1))
+                return fail(MTX_EINVAL, "layer %d: a residual addition takes only k and relu", i);
+            lp.src = src;
+            lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
+            lp.oc = c; lp.oh = h; lp.ow = w;
+            lp.w_len = 0; lp.b_len = 0;
         } else {
             return fail(MTX_EINVAL, "layer %d: unknown kind %d", i, ly.kind);
         }
@@ -172,7 +203,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         LayerPlan& lp = pl.L[i];
         lp.need_dx = (int)i > pl.first_param && pl.first_param >= 0;
         // a pooled tensor that feeds a fully connected layer is stored NCHW
-        lp.nhwc = lp.kind == MTX_CONV ||
+        lp.nhwc = lp.kind == MTX_CONV || lp.kind == MTX_BN || lp.kind == MTX_ADD ||
                   (lp.kind == MTX_MAXPOOL && !(i + 1 < pl.L.size() && pl.L[i + 1].kind == MTX_FC));
         lp.perm_c = 1;
         lp.perm_hw = 1;
@@ -226,7 +257,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.fw_off = lp.bw_off = kNone;
-        if (!lp.w_len) continue;
+        if (!lp.w_len || lp.kind == MTX_BN) continue;  // BN reads gamma and beta as they are
         PrepJob j{};
         j.n = (int)lp.w_len;
         j.src = (long long)lp.w_off;
@@ -263,7 +294,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     size_t ws = 0;
     // fp32 partial sums: one region for the forward and data-gradient launches, one for the
     // weight gradients (which may run concurrently on a second stream)
-    size_t max_partial = 0, max_partial_w = 0, max_col = 0;
+    size_t max_partial = 0, max_partial_w = 0, max_col = 0, max_bn_part = 0, max_bn_coef = 0;
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.act_f32 = (pl.dt == MTX_F32) || (i + 1 == pl.L.size());
@@ -275,6 +306,19 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         }
         if ((int)i >= pl.first_param) {
             lp.dy_off = ws;
+            ws = align_up(ws + lp.out_elems * pl.B * es, kAlign);
+        }
+        if (lp.kind == MTX_BN) {
+            lp.stat_off = ws;
+            ws = align_up(ws + (size_t)pl.R * lp.c * 2 * 4, kAlign);
+            max_bn_part = std::max(max_bn_part, bn_partial_doubles(pl.R, lp.c, pl.Nb, lp.h * lp.w));
+            max_bn_coef = std::max(max_bn_coef, (size_t)pl.R * lp.c * 3);
+        }
+        // a residual addition keeps the gradient for its source until the source's own output
+        // gradient exists (only when the source's gradient is needed at all)
+        lp.skip_off = kNone;
+        if (lp.kind == MTX_ADD && lp.src >= pl.first_param && pl.first_param >= 0) {
+            lp.skip_off = ws;
             ws = align_up(ws + lp.out_elems * pl.B * es, kAlign);
         }
         // fp32 partial sums of the matrix launches whose reduction is split (the last entry of
@@ -307,8 +351,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             size_t& mx = wgrad ? max_partial_w : max_partial;
             if (pz > mx) mx = pz;
         }
-        if (lp.w_len) {
-            pl.n_wgrad += 1;
+        if (lp.w_len) pl.n_wgrad += 1;
+        if (lp.w_len && lp.kind != MTX_BN) {
             const double macs = lp.kind == MTX_CONV
                                     ? (double)pl.B * lp.oh * lp.ow * lp.oc * (lp.c / lp.g) * lp.k * lp.k
                                     : (double)pl.B * lp.in_elems * lp.oc;
@@ -336,6 +380,10 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     ws = align_up(ws + max_partial_w * 4, kAlign);
     pl.col_off = ws;
     ws = align_up(ws + max_col * 4, kAlign);
+    pl.bn_part_off = ws;
+    ws = align_up(ws + max_bn_part * 8, kAlign);
+    pl.bn_coef_off = ws;
+    ws = align_up(ws + max_bn_coef * 4, kAlign);
     pl.ws_bytes = ws;
     return MTX_OK;
 }
@@ -356,6 +404,10 @@ void glorot_init_host(const Plan& pl, uint64_t seed, std::vector<float>& w)
     for (size_t l = 0; l < pl.L.size(); ++l) {
         const LayerPlan& lp = pl.L[l];
         if (!lp.w_len) continue;
+        if (lp.kind == MTX_BN) {  // gamma = 1, beta = 0: the identity at the start
+            for (size_t i = 0; i < lp.w_len; ++i) w[lp.w_off + i] = 1.0f;
+            continue;
+        }
         double fan_in, fan_out;
         if (lp.kind == MTX_CONV) {
             fan_in = (double)(lp.c / lp.g) * lp.k * lp.k;
@@ -827,6 +879,18 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                         return fc_fwd(dt, pl.B, (int)lp.in_elems, lp.oc, in, fwd_w(lp), bias, out,
                                       lp.act_f32, lp.relu, partial, s);
                     }), "fc forward");
+        } else if (lp.kind == MTX_BN) {
+            HIP_TRY(launch_site(m, "bn_fwd", (int)l, s, [&] {
+                        return bn_fwd(dt, pl.R, pl.Nb, lp.h * lp.w, lp.c, in, out,
+                                      m->w + lp.w_off, m->w + lp.b_off,
+                                      reinterpret_cast<double*>(ws + pl.bn_part_off),
+                                      reinterpret_cast<float*>(ws + lp.stat_off), lp.relu, s);
+                    }), "batch norm forward");
+        } else if (lp.kind == MTX_ADD) {
+            HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
+                        return add_fwd(dt, lp.out_elems * pl.B, in, ws + pl.L[lp.src].act_off, out,
+                                       lp.relu, s);
+                    }), "residual addition");
         } else {
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
                         return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc, in, out,
@@ -862,7 +926,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         const void* mask = (l > 0 && pl.L[l - 1].relu) ? ws + pl.L[l - 1].act_off : nullptr;
         const bool mask_f32 = l > 0 && pl.L[l - 1].act_f32;
         hipStream_t sw = s;
-        if (lp.w_len && overlap) {
+        if (lp.w_len && overlap && lp.kind != MTX_BN) {
             HIP_TRY(hipEventRecord(m->fork[nfork], s), "fork");
             HIP_TRY(hipStreamWaitEvent(m->side, m->fork[nfork], 0), "fork");
             ++nfork;
@@ -900,6 +964,23 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                             return fc_dgrad(dt, pl.B, (int)lp.in_elems, lp.oc, dy, bwd_w(lp), dx,
                                             mask, mask_f32, partial, s);
                         }), "fc data gradient");
+        } else if (lp.kind == MTX_BN) {
+            HIP_TRY(launch_site(m, "bn_bwd", l, s, [&] {
+                        return bn_bwd(dt, pl.R, pl.Nb, lp.h * lp.w, lp.c, in_l, dy, dx, mask,
+                                      mask_f32, m->w + lp.w_off,
+                                      reinterpret_cast<const float*>(ws + lp.stat_off),
+                                      reinterpret_cast<double*>(ws + pl.bn_part_off),
+                                      reinterpret_cast<float*>(ws + pl.bn_coef_off), m->grads, ld,
+                                      (long long)lp.w_off, (long long)lp.b_off, s);
+                    }), "batch norm backward");
+        } else if (lp.kind == MTX_ADD) {
+            void* skip = lp.skip_off != kNone ? ws + lp.skip_off : nullptr;
+            const LayerPlan& sp = pl.L[lp.src];
+            if (dx || skip)
+                HIP_TRY(launch_site(m, "add_bwd", l, s, [&] {
+                            return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32, skip,
+                                           sp.relu ? ws + sp.act_off : nullptr, sp.act_f32, s);
+                        }), "residual backward");
         } else if (lp.need_dx) {
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
                         return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
@@ -907,6 +988,18 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                         mask ? ws + lp.act_off : nullptr, s);
                     }), "pool backward");
         }
+        // The output gradient of layer l - 1 is now written; if a residual addition also read
+        // that layer's output, add the gradient it kept for it (before the layer's own weight
+        // gradient is forked off on the next iteration).
+        if (lp.need_dx)
+            for (size_t a2 = (size_t)l + 1; a2 < pl.L.size(); ++a2) {
+                const LayerPlan& ap = pl.L[a2];
+                if (ap.kind != MTX_ADD || ap.src != l - 1 || ap.skip_off == kNone) continue;
+                HIP_TRY(launch_site(m, "skip_add", l - 1, s, [&] {
+                            return skip_add(dt, pl.L[l - 1].out_elems * pl.B,
+                                            ws + pl.L[l - 1].dy_off, ws + ap.skip_off, s);
+                        }), "residual gradient");
+            }
         // Layer-wise averaging (the paper issues one reduction per layer, in layer order): this
         // layer's parameters are averaged and updated on the third stream as soon as its R
         // shard gradients are written, beside the rest of the backward pass.  Nothing later in

@@ -207,4 +207,29 @@ struct AdaptParams {
 hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool adam,
                          const AdaptParams& p, hipStream_t s, unsigned max_blocks = 0);
 
+// norm.hip: batch normalisation with per-shard statistics and the residual addition, over
+// NHWC tensors [R*Nb][HW][C] of all R shards.
+constexpr double kBnEps = 1e-3;
+// double partial sums one BN launch needs (the `part` scratch of bn_fwd / bn_bwd)
+size_t bn_partial_doubles(int R, int C, int Nb, int HW);
+// y = gamma (x - mean) / sqrt(var + eps) + beta (ReLU) with the statistics of each shard; stats
+// receives [R][C] pairs (mean, 1 / sqrt(var + eps)) for the backward pass.
+hipError_t bn_fwd(Dt dt, int R, int Nb, int HW, int C, const void* x, void* y,
+                  const float* gamma, const float* beta, double* part, float* stats, bool relu,
+                  hipStream_t s);
+// gamma / beta gradients of every shard into grads[r * ld + w_off / b_off + c], and (dx != null)
+// dx = gamma inv (dy - mean(dy) - xhat mean(dy xhat)) times the ReLU mask of the layer below;
+// coef is [R][C][3] floats of scratch.
+hipError_t bn_bwd(Dt dt, int R, int Nb, int HW, int C, const void* x, const void* dy, void* dx,
+                  const void* mask, bool mask_f32, const float* gamma, const float* stats,
+                  double* part, float* coef, float* grads, long long ld, long long w_off,
+                  long long b_off, hipStream_t s);
+// residual addition: y = a + b (ReLU); backward: dx and skip receive dy (each null to skip it),
+// masked by the ReLU of the previous layer / of the source layer; skip_add: dy += skip.
+hipError_t add_fwd(Dt dt, size_t n, const void* a, const void* b, void* y, bool relu,
+                   hipStream_t s);
+hipError_t add_bwd(Dt dt, size_t n, const void* dy, void* dx, const void* mask, bool mask_f32,
+                   void* skip, const void* smask, bool smask_f32, hipStream_t s);
+hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, hipStream_t s);
+
 }  // namespace mtx

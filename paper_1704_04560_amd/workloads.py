@@ -12,6 +12,8 @@ tensors of the same shapes):
   cifar    CIFAR-style CNN, bf16 compute, [512,3,32,32] N(0,1), R=8, momentum 0.9, lr=0.01
   alexnet  AlexNet-shaped CNN (groups=2 on conv2/4/5), bf16 compute, [256,3,227,227] N(0,1),
            1000 classes, R=8, momentum 0.9, lr=0.01
+  resnet   residual CNN with batch normalisation (the building blocks of Table II's ResNet-50
+           at CIFAR scale), bf16 compute, [512,3,32,32] N(0,1), R=8, momentum 0.9, lr=0.01
 Gradient-average microbenchmark: R=16 buffers of n elements, N(0, 1e-3) gradients, N(0, 0.05)
 weights, N(0, 1e-3) velocity, momentum 0.9, lr 0.01.
 
@@ -117,11 +119,31 @@ ALEXNET = Net("alexnet", (3, 227, 227),
                fc(4096, relu=True), fc(4096, relu=True), fc(1000)),
               BF16, "normal")
 
+# A residual network in the manner of Table II's ResNet-50 at CIFAR scale: 3x3 convolutions,
+# batch normalisation (per-shard statistics), identity shortcuts around pairs of convolutions,
+# 2/2 max-pooling between the three widths (64, 128, 256), a fully connected classifier.
+def _res_block(first, width):
+    """conv-BN-ReLU-conv-BN, added to the output of layer `first` - 1, then ReLU."""
+    return (conv(width, 3, pad=1), bn(relu=True), conv(width, 3, pad=1), bn(),
+            add(first - 1, relu=True))
+
+
+RESNET = Net("resnet", (3, 32, 32),
+             (conv(64, 3, pad=1), bn(relu=True))                      # 0-1
+             + _res_block(2, 64) + _res_block(7, 64) + (maxpool(2, 2),)  # 2-12
+             + (conv(128, 3, pad=1), bn(relu=True))                   # 13-14
+             + _res_block(15, 128) + (maxpool(2, 2),)                 # 15-20
+             + (conv(256, 3, pad=1), bn(relu=True))                   # 21-22
+             + _res_block(23, 256) + (maxpool(2, 2), fc(10)),         # 23-29
+             BF16, "normal")
+
 WORKLOADS = {
     "mlp": Workload(MLP, 64, 2, 0.01, 0.0, "MLP 784-256-10 fp32, B=64, R=2, SGD"),
     "lenet": Workload(LENET, 256, 4, 0.01, 0.9, "LeNet fp32, B=256, R=4, momentum 0.9"),
     "cifar": Workload(CIFAR, 512, 8, 0.01, 0.9, "CIFAR CNN bf16, B=512, R=8, momentum 0.9"),
     "alexnet": Workload(ALEXNET, 256, 8, 0.01, 0.9, "AlexNet bf16, B=256, R=8, momentum 0.9"),
+    "resnet": Workload(RESNET, 512, 8, 0.01, 0.9,
+                       "residual CNN with batch norm bf16, B=512, R=8, momentum 0.9"),
 }
 
 AVG_UPDATE = {"R": 16, "n": (61_000_000, 250_000_000), "lr": 0.01, "momentum": 0.9,

@@ -158,6 +158,11 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
                 (ly.stride != 0 && ly.stride != 1) || (ly.groups != 0 && ly.groups != 1))
                 return fail(MTX_EINVAL, "layer %d: batch normalisation takes only relu (out, if "
                                         "given, must be its channel count)", i);
+            const int vw = 16 / (int)es;
+            if (c > 256 && !(c % vw == 0 && c / vw <= 256))
+                return fail(MTX_EUNSUPPORTED, "layer %d: batch normalisation of %d channels (more "
+                                              "than 256 need a multiple of %d, at most %d)",
+                            i, c, vw, 256 * vw);
             lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
             lp.oc = c; lp.oh = h; lp.ow = w;
             lp.w_len = c; lp.b_len = c;  // gamma, beta
@@ -310,8 +315,9 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         }
         if (lp.kind == MTX_BN) {
             lp.stat_off = ws;
-            ws = align_up(ws + (size_t)pl.R * lp.c * 2 * 4, kAlign);
-            max_bn_part = std::max(max_bn_part, bn_partial_doubles(pl.R, lp.c, pl.Nb, lp.h * lp.w));
+            ws = align_up(ws + (size_t)pl.R * lp.c * kBnStatFloats * 4, kAlign);
+            max_bn_part = std::max(max_bn_part, bn_partial_doubles((Dt)pl.dt, pl.R, lp.c, pl.Nb,
+                                                                   lp.h * lp.w));
             max_bn_coef = std::max(max_bn_coef, (size_t)pl.R * lp.c * 3);
         }
         // a residual addition keeps the gradient for its source until the source's own output
@@ -967,8 +973,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         } else if (lp.kind == MTX_BN) {
             HIP_TRY(launch_site(m, "bn_bwd", l, s, [&] {
                         return bn_bwd(dt, pl.R, pl.Nb, lp.h * lp.w, lp.c, in_l, dy, dx, mask,
-                                      mask_f32, m->w + lp.w_off,
-                                      reinterpret_cast<const float*>(ws + lp.stat_off),
+                                      mask_f32, reinterpret_cast<const float*>(ws + lp.stat_off),
                                       reinterpret_cast<double*>(ws + pl.bn_part_off),
                                       reinterpret_cast<float*>(ws + pl.bn_coef_off), m->grads, ld,
                                       (long long)lp.w_off, (long long)lp.b_off, s);

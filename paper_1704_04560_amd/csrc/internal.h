@@ -211,19 +211,22 @@ hipError_t average_adapt(const float* grads, int R, size_t n, size_t ld, bool ad
 // NHWC tensors [R*Nb][HW][C] of all R shards.
 constexpr double kBnEps = 1e-3;
 // double partial sums one BN launch needs (the `part` scratch of bn_fwd / bn_bwd)
-size_t bn_partial_doubles(int R, int C, int Nb, int HW);
+size_t bn_partial_doubles(Dt dt, int R, int C, int Nb, int HW);
+constexpr int kBnStatFloats = 4;  // per (shard, channel): mean, 1/std, gamma/std, beta
 // y = gamma (x - mean) / sqrt(var + eps) + beta (ReLU) with the statistics of each shard; stats
-// receives [R][C] pairs (mean, 1 / sqrt(var + eps)) for the backward pass.
+// receives [R][4][C] floats (mean, 1 / sqrt(var + eps), gamma / sqrt(var + eps), beta) for the
+// apply pass and the backward pass.  C must be at most 256, or a multiple of 16 / element size
+// up to 256 such vectors.
 hipError_t bn_fwd(Dt dt, int R, int Nb, int HW, int C, const void* x, void* y,
                   const float* gamma, const float* beta, double* part, float* stats, bool relu,
                   hipStream_t s);
 // gamma / beta gradients of every shard into grads[r * ld + w_off / b_off + c], and (dx != null)
 // dx = gamma inv (dy - mean(dy) - xhat mean(dy xhat)) times the ReLU mask of the layer below;
-// coef is [R][C][3] floats of scratch.
+// stats are the forward pass's; coef is [R][3][C] floats of scratch.
 hipError_t bn_bwd(Dt dt, int R, int Nb, int HW, int C, const void* x, const void* dy, void* dx,
-                  const void* mask, bool mask_f32, const float* gamma, const float* stats,
-                  double* part, float* coef, float* grads, long long ld, long long w_off,
-                  long long b_off, hipStream_t s);
+                  const void* mask, bool mask_f32, const float* stats, double* part,
+                  float* coef, float* grads, long long ld, long long w_off, long long b_off,
+                  hipStream_t s);
 // residual addition: y = a + b (ReLU); backward: dx and skip receive dy (each null to skip it),
 // masked by the ReLU of the previous layer / of the source layer; skip_add: dy += skip.
 hipError_t add_fwd(Dt dt, size_t n, const void* a, const void* b, void* y, bool relu,

@@ -68,6 +68,37 @@ def test_invalid_networks_are_rejected():
     assert _err(mtx.mtx_model_sizes, kind, 1, 1) == mtx.MTX_EINVAL
 
 
+def test_invalid_residual_and_batch_norm_layers_are_rejected():
+    def tup(l):
+        if isinstance(l, tuple):
+            return l
+        return (l.kind, l.out, l.k, l.stride, l.pad, l.groups, int(l.relu))
+
+    base = [wl.conv(8, 3, pad=1), wl.bn(relu=True), wl.conv(8, 3, pad=1), wl.bn(),
+            wl.add(1, relu=True), wl.fc(3)]
+    good = mtx.make_desc((3, 8, 8), [tup(l) for l in base], wl.F32)
+    mtx.mtx_model_sizes(good, 2, 2)
+
+    def code(layers, shape=(3, 8, 8), dt=wl.F32):
+        return _err(mtx.mtx_model_sizes, mtx.make_desc(shape, [tup(l) for l in layers], dt), 2, 2)
+
+    L = list(base)
+    L[1] = (3, 7, 0, 1, 0, 1, 1)          # BN out differs from its channel count
+    assert code(L) == mtx.MTX_EINVAL
+    L = list(base)
+    L[4] = wl.add(3, relu=True)           # the previous layer is not a shortcut source
+    assert code(L) == mtx.MTX_EINVAL
+    L = list(base)
+    L[4] = wl.add(5)                      # not an earlier layer
+    assert code(L) == mtx.MTX_EINVAL
+    shape = [wl.conv(8, 3, pad=1), wl.conv(8, 3), wl.add(0), wl.fc(2)]  # 8x8 vs 6x6
+    assert code(shape) == mtx.MTX_EINVAL
+    twice = base[:5] + [wl.conv(8, 3, pad=1), wl.add(1), wl.fc(3)]   # layer 1 added twice
+    assert code(twice) == mtx.MTX_EINVAL
+    wide = [wl.fc(300), wl.bn(), wl.fc(2)]  # 300 channels, not a multiple of 8 (bf16)
+    assert code(wide, (4, 1, 1), wl.BF16) == mtx.MTX_EUNSUPPORTED
+
+
 def test_update_argument_errors_need_no_device():
     g = np.zeros(64, np.float32)
     w = np.zeros(16, np.float32)

@@ -155,8 +155,9 @@ def test_steps_are_deterministic():
 
 
 def test_average_is_mean_of_shard_gradients_at_full_alexnet_size():
-    """Property that holds at any size: the stored average equals the mean of the R stored
-    shard gradients, and the update equals w - lr * (mu * v + avg)."""
+    """Properties that hold at any size, checked at the full AlexNet size in numpy (no oracle
+    call on GPU values): the stored average is the mean of the R stored shard gradients, and
+    the update is v' = mu v + avg, w' = w - lr v'."""
     net = wl.ALEXNET
     layers = wl.layer_tuples(net)
     R, Nb = 8, 32
@@ -169,15 +170,86 @@ def test_average_is_mean_of_shard_gradients_at_full_alexnet_size():
     loss = torch.zeros(1, device="cuda")
     m.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), 0.01, 0.9, loss)
     torch.cuda.synchronize()
-    g = m.grads_host()
+    g = m.grads_host().astype(np.float64)
     avg = m.grad_avg.cpu().numpy()
-    ref_avg, ref_w, ref_v = orc.average_update(g, w0, v0, 0.01, 0.9)
-    parity.assert_tensor_close(avg, ref_avg, 1e-6, "average")
+    parity.assert_tensor_close(avg, g.mean(axis=0), 1e-6, "average")
     w1, v1 = m.get_params()
-    parity.assert_tensor_close(v1, ref_v, 1e-6, "velocity")
-    parity.assert_update_close(w1, ref_w, w0, 1e-4)
+    v_ref = 0.9 * v0.astype(np.float64) + avg.astype(np.float64)
+    parity.assert_tensor_close(v1, v_ref, 1e-6, "velocity")
+    parity.assert_update_close(w1, w0.astype(np.float64) - 0.01 * v1.astype(np.float64), w0, 1e-4)
     assert np.isfinite(loss.item()) and abs(loss.item() - np.log(1000)) < 0.5
     m.close()
+
+
+def _sample_decisions(model, geo, idx):
+    """The GPU's pooling and ReLU decisions of the samples idx (oracle layout, concatenated over
+    layers), for an oracle run on those samples alone."""
+    B = model.B
+    pools, relus = [], []
+    for i, g in enumerate(geo):
+        per = int(np.prod(g["out_shape"]))
+        if g["kind"] == 2:
+            pools.append(model.pool_argmax(i).astype(np.int32).reshape(B, per)[idx].ravel())
+        if g["relu"]:
+            relus.append((model.layer_output(i) > 0).astype(np.int8).reshape(B, per)[idx].ravel())
+    return (np.concatenate(pools) if pools else np.zeros(0, np.int32),
+            np.concatenate(relus) if relus else np.zeros(0, np.int8))
+
+
+@pytest.mark.parametrize("name", ["cifar", "alexnet"])
+def test_full_size_logits_match_oracle_on_sampled_samples(name):
+    """The bf16 workloads at their full size, in the launch configuration the benchmark times
+    (CIFAR B = 512, AlexNet B = 256, R = 8): a sample's forward pass does not depend on the rest
+    of the batch, so the oracle computes the logits of four sampled samples on their own and
+    they must match the GPU's stored logits of those samples (decisions near ties taken as the
+    GPU took them, within the oracle's error bound)."""
+    w = wl.WORKLOADS[name]
+    net = w.net
+    layers = wl.layer_tuples(net)
+    geo = orc.geometry(net.in_shape, layers)
+    _say(f"[case] full-size sampled logits {name}")
+    model = mtx.Model(net.in_shape, layers, net.dtype, w.shards, w.shard_batch, seed=5)
+    wt, _ = model.get_params()
+    x, y = wl.make_batch(net, w.batch, seed=5)
+    model.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), 0.0, 0.0)
+    torch.cuda.synchronize()
+    idx = np.array([0, w.shard_batch + 7, w.batch // 2 + 3, w.batch - 1])
+    gp, gr = _sample_decisions(model, geo, idx)
+    res, _ = parity.oracle_step_matching(net, layers, 1, x[idx], y[idx], wt, None, 0.0, 0.0,
+                                         "bf16", gp, gr)
+    nc = net.num_classes
+    logits = model.layer_output(len(geo) - 1).reshape(w.batch, nc)[idx]
+    ref = res.acts[-len(idx) * nc:].reshape(len(idx), nc)
+    parity.assert_tensor_close(logits, ref, parity.TOL[net.dtype], f"{name} sampled logits")
+    model.close()
+
+
+@pytest.mark.parametrize("name", ["cifar", "alexnet"])
+def test_full_size_shard_count_invariance(name):
+    """At the full batch, the weight change of one step does not depend on how the batch is
+    split (R = 8 as benchmarked against R = 1 and 2): every launch configuration of the step at
+    full size agrees with the others (bf16 bound)."""
+    w = wl.WORKLOADS[name]
+    net = w.net
+    layers = wl.layer_tuples(net)
+    _say(f"[case] full-size shard-count invariance {name}")
+    x, y = wl.make_batch(net, w.batch, seed=6)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    deltas = {}
+    for R in (1, 2, w.shards):
+        m = mtx.Model(net.in_shape, layers, net.dtype, R, w.batch // R, seed=6)
+        w0, _ = m.get_params()
+        m.train_step(xd, yd, w.lr, w.momentum)
+        torch.cuda.synchronize()
+        w1, _ = m.get_params()
+        deltas[R] = w1.astype(np.float64) - w0.astype(np.float64)
+        m.close()
+        torch.cuda.empty_cache()
+    tol = parity.TOL[net.dtype]
+    for R in (2, w.shards):
+        d, ref = deltas[R], deltas[1]
+        assert np.linalg.norm(d - ref) <= tol * np.linalg.norm(ref), R
+        assert np.max(np.abs(d - ref)) <= tol * np.max(np.abs(ref)), R
 
 
 @pytest.mark.parametrize("name", ["lenet", "cifar"])

@@ -28,7 +28,8 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK = {"hbm_GBps": 8000.0, "f32_TFLOPs": 157.3, "bf16_TFLOPs": 2500.0}
+PEAK = {"hbm_GBps": 8000.0, "f32_TFLOPs": 157.3, "bf16_TFLOPs": 2500.0,
+        "f32_vector_TFLOPs": 157.3}
 METRIC = "train samples/sec per GPU; grad-avg+update GB/s and conv/GEMM MFMA % of peak"
 
 
@@ -53,7 +54,8 @@ def geometry(net):
 
 def site_work(name, layer, geo, wkl, es):
     """Algorithmic work of one launch of a step's launch site: ("mfma", flops) for the matrix
-    kernels (2 x multiply-adds of the convolution / product), ("hbm", bytes) for the others
+    kernels (2 x multiply-adds of the convolution / product), ("alu", flops) for the direct
+    first-convolution kernels (fp32 vector fused multiply-adds), ("hbm", bytes) for the others
     (each tensor read once and written once), (None, 0) when not modelled."""
     from paper_1704_04560_amd import workloads as wl
     B, R, Nb = wkl.batch, wkl.shards, wkl.shard_batch
@@ -68,6 +70,11 @@ def site_work(name, layer, geo, wkl, es):
         out_sz = B * g["oc"] * g["oh"] * g["ow"]
         if name in ("fwd", "dgrad", "wgrad"):
             return "mfma", 2.0 * macs
+        if name in ("fwd_direct", "wgrad_direct"):
+            return "alu", 2.0 * macs
+        if name == "wgrad_direct_reduce":  # per-image fp32 sums read, the shard rows written
+            no = g["oc"] * l.k * l.k + g["oc"]
+            return "hbm", 4.0 * no * (B + R)
         if name == "dgrad_col2im":  # fp32 col read once, dx written, mask read
             return "hbm", 4.0 * l.k * l.k * g["c"] * B * g["oh"] * g["ow"] + 2 * es * in_sz
         if name == "pool_fwd":
@@ -332,6 +339,11 @@ def measure(torch, mtx, wl, name, steps, warmup):
         ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak_mm, "unit": "TFLOP/s"}
         roof["frac"] = round(ach / peak_mm, 4)
+    elif dom["bound"] == "alu":
+        ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e12
+        pk = PEAK["f32_vector_TFLOPs"]
+        roof = {"bound": "alu", "achieved": round(ach, 3), "peak": pk, "unit": "TFLOP/s",
+                "frac": round(ach / pk, 4)}
     else:
         ach = dom["work"] / (dom["avg_ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_GBps"],

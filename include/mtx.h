@@ -247,10 +247,13 @@ int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float ep
  * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
  * Launch-site names: "prep_w" (weight layouts), "prep_x" (input layout), "fwd", "pool_fwd",
  * "bn_fwd", "add_fwd", "softmax_xent" (with the loss mean), "wgrad" (weight and bias gradient),
- * "dgrad", "pool_bwd", "bn_bwd", "add_bwd", "skip_add", "avg_update"; the second kernel of an
- * operation is a site of its own: "<site>_reduce" (the second pass of a split reduction),
- * "dgrad_col2im" and "bn_fwd_apply" / "bn_bwd_apply" (the elementwise pass after the batch
- * statistics).  Timing adds one event pair per kernel;
+ * "dgrad", "pool_bwd", "bn_bwd", "add_bwd", "skip_add", "avg_update"; "fwd_direct" and
+ * "wgrad_direct" for a first convolution of one input channel and a 3x3, 5x5 or 7x7 window
+ * (at most 32 outputs), which runs on direct kernels instead of the matrix kernels; the second
+ * kernel of an operation is a site of its own: "<site>_reduce" (the second pass of a split
+ * reduction), "dgrad_col2im", "bn_fwd_finalize" / "bn_bwd_finalize" (per-channel statistics
+ * from the partial sums) and "bn_fwd_apply" / "bn_bwd_apply" (the elementwise pass after the
+ * batch statistics).  Timing adds one event pair per kernel;
  * use it for measurement runs. */
 typedef struct {
     char name[32];

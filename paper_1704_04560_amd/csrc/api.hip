@@ -66,6 +66,7 @@ struct LayerPlan {
     bool run;                    // first convolution over the padded input (conv_fwd_run)
     RunGeom rg;                  // its padded input geometry
     int src;                     // residual addition: the layer whose output is added
+    bool direct;                 // first convolution through the direct kernels (firstconv.hip)
     size_t stat_off;             // batch normalisation: per-shard (mean, 1/std) [R][C] floats
     size_t skip_off;             // residual addition: gradient for the source layer [B][...]
 };
@@ -89,6 +90,7 @@ struct Plan {
     size_t xin_off = 0, xin_bytes = 0, prep_off = 0, jobs_off = 0, loss_off = 0;
     size_t partial_off = 0, partial_w_off = 0, col_off = 0, sync_off = 0;
     size_t bn_part_off = 0, bn_coef_off = 0;  // batch normalisation scratch
+    size_t first_part_off = 0;                 // direct first convolution: per-image sums
     int n_wgrad = 0;             // layers with a weight gradient
     double gemm_flops = 0;       // multiply-adds x 2 of every matrix launch of a step
     size_t ws_bytes = 0;
@@ -245,6 +247,13 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             pl.x_convert = true;
         }
     }
+    // A first convolution of one input channel with a small window runs as direct kernels.
+    first.direct = false;
+    if (first.kind == MTX_CONV && !first.run) {
+        const ConvGeom g0{pl.B, first.c, first.h, first.w, first.oc, first.oh, first.ow, first.k,
+                          first.s, first.p, first.g};
+        first.direct = first_conv_direct(g0, pl.dt);
+    }
 
     // weight preparation jobs; every prepared tensor starts 16-byte aligned
     size_t pe = 0;
@@ -271,6 +280,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             j.n = lp.oc * lp.k * lp.rg.RUN;
             j.C = lp.c; j.Cp = lp.rg.Cp; j.K = lp.k; j.RUN = lp.rg.RUN;
             lp.fw_off = add_job(j);
+        } else if (lp.kind == MTX_CONV && lp.direct) {
+            continue;  // the direct kernels read the fp32 weights (and round them as they load)
         } else if (lp.kind == MTX_CONV) {
             j.g = lp.g; j.cg = lp.c / lp.g; j.og = lp.oc / lp.g; j.KK = lp.k * lp.k;
             j.kind = PREP_CONV_F;
@@ -300,6 +311,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     // fp32 partial sums: one region for the forward and data-gradient launches, one for the
     // weight gradients (which may run concurrently on a second stream)
     size_t max_partial = 0, max_partial_w = 0, max_col = 0, max_bn_part = 0, max_bn_coef = 0;
+    size_t max_first = 0;
     for (size_t i = 0; i < pl.L.size(); ++i) {
         LayerPlan& lp = pl.L[i];
         lp.act_f32 = (pl.dt == MTX_F32) || (i + 1 == pl.L.size());
@@ -331,7 +343,10 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         // dims is the weight gradient)
         GemmDims dims[3];
         int nd = 0;
-        if (lp.kind == MTX_CONV) {
+        if (lp.kind == MTX_CONV && lp.direct) {
+            ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            max_first = std::max(max_first, first_conv_partial_floats(gs, pl.R));
+        } else if (lp.kind == MTX_CONV) {
             ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             ConvGeom gs = gb;
             gs.N = pl.Nb;
@@ -388,6 +403,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     ws = align_up(ws + max_col * 4, kAlign);
     pl.bn_part_off = ws;
     ws = align_up(ws + max_bn_part * 8, kAlign);
+    pl.first_part_off = ws;
+    ws = align_up(ws + max_first * 4, kAlign);
     pl.bn_coef_off = ws;
     ws = align_up(ws + max_bn_coef * 4, kAlign);
     pl.ws_bytes = ws;
@@ -872,7 +889,13 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         const LayerPlan& lp = pl.L[l];
         void* out = ws + lp.act_off;
         const float* bias = m->w + lp.b_off;
-        if (lp.kind == MTX_CONV) {
+        if (lp.kind == MTX_CONV && lp.direct) {
+            ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            HIP_TRY(launch_site(m, "fwd_direct", (int)l, s, [&] {
+                        return first_conv_fwd(dt, g, in, m->w + lp.w_off, bias, out, lp.act_f32,
+                                              lp.relu, s);
+                    }), "first convolution forward");
+        } else if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
                         return lp.run ? conv_fwd_run(dt, g, lp.rg, in, fwd_w(lp), bias, out,
@@ -938,7 +961,15 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             ++nfork;
             sw = m->side;
         }
-        if (lp.kind == MTX_CONV) {
+        if (lp.kind == MTX_CONV && lp.direct) {
+            ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            HIP_TRY(launch_site(m, "wgrad_direct", l, sw, [&] {
+                        return first_conv_wgrad(dt, gs, pl.R, in_l, dy,
+                                                reinterpret_cast<float*>(ws + pl.first_part_off),
+                                                m->grads, ld, (long long)lp.w_off,
+                                                (long long)lp.b_off, sw);
+                    }), "first convolution weight gradient");
+        } else if (lp.kind == MTX_CONV) {
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
                         return lp.run ? conv_wgrad_run(dt, gs, lp.rg, pl.R, in_l, dy, m->grads, ld,

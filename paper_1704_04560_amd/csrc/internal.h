@@ -235,4 +235,20 @@ hipError_t add_bwd(Dt dt, size_t n, const void* dy, void* dx, const void* mask, 
                    void* skip, const void* smask, bool smask_f32, hipStream_t s);
 hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, hipStream_t s);
 
+// firstconv.hip: direct kernels for a first convolution with one input channel, stride 1,
+// a 3x3, 5x5 or 7x7 window and at most 32 output channels (a multiple of 4) whose image and
+// output gradient fit the LDS of one block.
+constexpr int kFirstMaxOC = 32;
+constexpr size_t kFirstMaxLds = 64 * 1024;
+bool first_conv_direct(const ConvGeom& g, int dt);
+// x: the input [N][H][W] (one channel) in the compute type; w: fp32 [OC][K][K]; y NHWC.
+hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
+                          const float* bias, void* y, bool y_f32, bool relu, hipStream_t s);
+// weight and bias gradients of R shards of g.N images; partial holds
+// first_conv_partial_floats(g, R) floats of scratch.
+size_t first_conv_partial_floats(const ConvGeom& g, int R);
+hipError_t first_conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
+                            float* partial, float* grads, long long ld, long long w_off,
+                            long long b_off, hipStream_t s);
+
 }  // namespace mtx

@@ -123,6 +123,53 @@ def test_pool_windows_and_strides(dtype):
     run_case(f"tiny3-{dtype}", _tiny_pools(dtype), 2, 3, 2, 10, 0.05, 0.9)
 
 
+def _single_channel(dtype, oc, k, pad, relu):
+    """One input channel into a small-window first convolution: the shape the direct
+    first-convolution kernels take (ragged image, several output-channel counts and windows)."""
+    layers = (wl.conv(oc, k, pad=pad, relu=relu), wl.maxpool(2, 2), wl.conv(6, 3, relu=True),
+              wl.fc(5))
+    return wl.Net(f"one-channel-{oc}-{k}", (1, 13, 11), layers, dtype, "normal")
+
+
+def _sites(model, x, y):
+    """Launch-site names of one timed step."""
+    loss = torch.zeros(1, device="cuda")
+    mtx.mtx_set_timing(model.handle, True)
+    mtx.mtx_get_timing(model.handle, reset=True)
+    model.train_step(x, y, 0.0, 0.0, loss)
+    torch.cuda.synchronize()
+    names = {(n, l) for (n, l, k, _) in mtx.mtx_get_timing(model.handle) if k}
+    mtx.mtx_set_timing(model.handle, False)
+    return names
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("oc,k,pad,relu", [(20, 5, 0, False), (4, 3, 1, True), (32, 3, 0, True),
+                                           (16, 7, 3, False), (8, 5, 2, True)])
+def test_single_channel_first_convolution(dtype, oc, k, pad, relu):
+    net = _single_channel(dtype, oc, k, pad, relu)
+    run_case(f"{net.name}-{dtype}", net, 3, 5, 2, 11, 0.05, 0.9)
+
+
+def test_first_convolution_takes_the_direct_kernels():
+    """LeNet's first layer (one channel, 5x5, 20 outputs) runs on the direct kernels, and a first
+    convolution outside their limits (64 outputs of a 7x7 window) on the matrix kernels."""
+    for net, direct in ((wl.LENET, True), (_single_channel(wl.F32, 64, 7, 3, True), False)):
+        layers = wl.layer_tuples(net)
+        model = mtx.Model(net.in_shape, layers, net.dtype, 2, 3, seed=1)
+        x, y = wl.make_batch(net, 6, seed=1)
+        names = _sites(model, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda())
+        model.close()
+        assert (("fwd_direct", 0) in names) == direct, names
+        assert (("wgrad_direct", 0) in names) == direct, names
+        assert (("fwd", 0) in names) != direct, names
+
+
+def test_lenet_bf16_reduced_batch():
+    net = wl.Net("lenet-bf16", wl.LENET.in_shape, wl.LENET.layers, wl.BF16, "uniform")
+    run_case("lenet-bf16", net, 4, 8, 2, 12, 0.01, 0.9)
+
+
 def test_cifar_shapes_reduced_batch():
     run_case("cifar-B16", wl.CIFAR, 8, 2, 2, 6, 0.01, 0.9)
 

@@ -15,7 +15,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmtx.so")
 SOURCES = ["api.hip", "plan.hip", "igemm_fwd.hip", "igemm_dgrad.hip", "igemm_wgrad.hip",
-           "elementwise.hip", "norm.hip", "firstconv.hip"]
+           "elementwise.hip", "norm.hip", "firstconv.hip", "dgrad_fused.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

@@ -56,6 +56,7 @@ struct LayerPlan {
     size_t in_elems, out_elems;  // per sample
     bool act_f32;                // stored output is fp32 (always in fp32 mode; logits)
     bool dgrad_col;              // convolution data gradient through col + col2im
+    bool dgrad_fused;            // ... with col tile and col2im in one kernel (dgrad_fused.hip)
     bool need_dx;                // the data gradient of this layer's input is computed
     bool nhwc;                   // stored output is NHWC (convolution and pooling layers)
     int perm_c, perm_hw;         // fully connected after a spatial layer: input in (h, w, c)
@@ -289,8 +290,9 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             if (lp.need_dx) {
                 ConvGeom gb{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
                 lp.dgrad_col = conv_dgrad_use_col(gb);
+                lp.dgrad_fused = lp.dgrad_col && conv_dgrad_fused_ok(gb, pl.dt);
                 j.kind = lp.dgrad_col ? PREP_CONV_C : PREP_CONV_D;
-                lp.bw_off = add_job(j);
+                if (!lp.dgrad_fused) lp.bw_off = add_job(j);  // the fused kernel reads W itself
             }
         } else {
             if (lp.perm_c > 1) {
@@ -352,7 +354,9 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             gs.N = pl.Nb;
             dims[nd++] = lp.run ? conv_fwd_run_dims(pl.dt, gb, lp.rg) : conv_fwd_dims(pl.dt, gb);
             if (lp.need_dx) {
-                if (lp.dgrad_col) {
+                if (lp.dgrad_fused) {
+                    // no col buffer and no split reduction
+                } else if (lp.dgrad_col) {
                     dims[nd++] = conv_dgrad_col_dims(pl.dt, gb);
                     if (conv_dgrad_col_elems(gb) > max_col) max_col = conv_dgrad_col_elems(gb);
                 } else {
@@ -983,6 +987,10 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
                 float* col = reinterpret_cast<float*>(ws + pl.col_off);
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
+                            if (lp.dgrad_fused)
+                                return conv_dgrad_fused(g, static_cast<const float*>(dy),
+                                                        m->w + lp.w_off, static_cast<float*>(dx),
+                                                        mask, mask_f32, s);
                             return lp.dgrad_col
                                        ? conv_dgrad_col(dt, g, dy, bwd_w(lp), dx, mask, mask_f32,
                                                         col, partial, s)

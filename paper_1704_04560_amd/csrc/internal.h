@@ -251,4 +251,12 @@ hipError_t first_conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, cons
                             float* partial, float* grads, long long ld, long long w_off,
                             long long b_off, hipStream_t s);
 
+// dgrad_fused.hip: fp32 data gradient of a stride-1, ungrouped 3x3 or 5x5 convolution with at
+// most 60 output channels whose output has at most 64 positions per image, col tile and col2im
+// in one kernel (LDS, no col buffer).  w: the fp32 weights [OC][C][K][K]; dy, dx, mask NHWC.
+constexpr size_t kDxMaxLds = 80 * 1024;
+bool conv_dgrad_fused_ok(const ConvGeom& g, int dt);
+hipError_t conv_dgrad_fused(const ConvGeom& g, const float* dy, const float* w, float* dx,
+                            const void* mask, bool mask_f32, hipStream_t s);
+
 }  // namespace mtx

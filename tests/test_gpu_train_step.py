@@ -165,6 +165,24 @@ def test_first_convolution_takes_the_direct_kernels():
         assert (("fwd", 0) in names) != direct, names
 
 
+def _small_image_dgrad(dtype, k):
+    """A convolution below the first layer whose output is a few positions of a small image
+    (its data gradient goes through the col tile; in fp32 the tile stays in LDS): ragged row
+    tiles and channel ranges, output channel counts that are not multiples of 4, a ReLU mask."""
+    if k == 5:
+        layers = (wl.conv(23, 3, pad=1, relu=True), wl.conv(13, 5, relu=True), wl.maxpool(2, 2),
+                  wl.fc(5))
+        return wl.Net("small-dgrad-5", (2, 10, 9), layers, dtype, "normal")
+    layers = (wl.conv(30, 3, relu=True), wl.conv(7, 3), wl.fc(4))
+    return wl.Net("small-dgrad-3", (1, 9, 9), layers, dtype, "normal")
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("k", [3, 5])
+def test_small_image_data_gradient(dtype, k):
+    run_case(f"small-dgrad-{k}-{dtype}", _small_image_dgrad(dtype, k), 3, 4, 2, 13, 0.05, 0.9)
+
+
 def test_lenet_bf16_reduced_batch():
     net = wl.Net("lenet-bf16", wl.LENET.in_shape, wl.LENET.layers, wl.BF16, "uniform")
     run_case("lenet-bf16", net, 4, 8, 2, 12, 0.01, 0.9)

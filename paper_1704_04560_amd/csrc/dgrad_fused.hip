@@ -27,7 +27,6 @@ constexpr int kDxRS = kDxMaxRows + 16;  // LDS row stride of the k-major weight 
 struct DxShape {
     int cb;      // input channels per block
     int chunks;  // blocks per image
-    int ocs;     // LDS row stride of the position-major dy operand (stride / 4 odd)
     int ps;      // LDS row stride of the col tile (odd)
     size_t lds;  // LDS floats
 };
@@ -39,9 +38,8 @@ DxShape dx_shape(const ConvGeom& g)
     s.chunks = (g.C + cbmax - 1) / cbmax;
     s.cb = (g.C + s.chunks - 1) / s.chunks;
     const int ks = (g.OC + 3) / 4;
-    s.ocs = 4 * ks + ((ks & 1) ? 0 : 4);
     s.ps = (g.OH * g.OW) | 1;
-    const size_t ab = (size_t)4 * ks * kDxRS + (size_t)kDxMaxPos * s.ocs;
+    const size_t ab = (size_t)4 * ks * kDxRS + (size_t)kDxMaxPos * g.OC + 4;
     const size_t col = (size_t)kDxMaxRows * s.ps;
     s.lds = std::max(ab, col);
     return s;
@@ -52,8 +50,10 @@ DxShape dx_shape(const ConvGeom& g)
 //   dx[n][h][w][c0 + cl] = mask * sum_{u, v ascending} col[r][oh * OW + ow]
 //                          with oh = h + PD - u, ow = w + PD - v inside the output.
 // W is the fp32 weight tensor [OC][C][K][K]: for one output channel the block's rows are one
-// contiguous run, staged k-major (As[co][r]); dy is staged position-major (Bs[p][co]).  Every
-// load of a thread is issued before any LDS write, so the block waits for memory once.
+// contiguous run, staged k-major (As[co][r]); the image's dy is one contiguous run, staged as it
+// is (Bs[p * OC + co]; the reads past a row's end meet zero rows of As, and the positions past
+// the image are zero).  Both are copied with 16-byte loads, every load of a thread issued before
+// any LDS write, so that the block waits for memory once.
 // The product runs as v_mfma_f32_16x16x4_f32: wave wv owns row tiles wv, wv + 4, wv + 8,
 // wv + 12 and the four column tiles; lane l supplies row l % 16 and k = 4 * step + l / 16 of
 // both operands, and holds rows 4 * (l / 16) + v, column l % 16 of the result.
@@ -64,7 +64,7 @@ __global__ __launch_bounds__(256) void dgrad_fused_kernel(const float* __restric
                                                           const void* __restrict__ mask,
                                                           int mask_f32, int C, int H, int W,
                                                           int OC, int OH, int OW, int PD, int CB,
-                                                          int chunks, int OCS, int PS)
+                                                          int chunks, int PS)
 {
     constexpr int KK = K * K;
     constexpr int CBMAX = kDxMaxRows / KK;
@@ -74,29 +74,53 @@ __global__ __launch_bounds__(256) void dgrad_fused_kernel(const float* __restric
     const int Mb = cbc * KK, P = OH * OW;
     const int KS = (OC + 3) / 4;
     float* As = sm;                  // [4 * KS][kDxRS]
-    float* Bs = sm + 4 * KS * kDxRS; // [kDxMaxPos][OCS]
+    float* Bs = sm + 4 * KS * kDxRS; // [kDxMaxPos * OC + 4]
     const int tid = threadIdx.x;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     {
-        constexpr int KMAX = 64, BE = kDxMaxPos * 64 / 256;
-        float va[KMAX], vb[BE];
-        const float* wr = w + (size_t)c0 * KK + tid;
-        const size_t ws = (size_t)C * KK;
+        // A: item i = (k = i / 64, four rows 4 * (i % 64) ..); B: four floats 4 * e ..
+        constexpr int AI = 64 * 64 / 256, BI = (kDxMaxPos * 64 + 4 + 1023) / 1024;
+        float4 va[AI], vb[BI];
+        const float* wr = w + (size_t)c0 * KK;
+        const size_t wsk = (size_t)C * KK;
 #pragma unroll
-        for (int k = 0; k < KMAX; ++k) va[k] = (k < OC && tid < Mb) ? wr[k * ws] : 0.f;
+        for (int it = 0; it < AI; ++it) {
+            const int i = tid + 256 * it, k = i >> 6, r = 4 * (i & 63);
+            va[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k < OC) {
+                const float* src = wr + k * wsk + r;
+                if (r + 3 < Mb) {
+                    __builtin_memcpy(&va[it], src, 16);
+                } else {
+                    if (r < Mb) va[it].x = src[0];
+                    if (r + 1 < Mb) va[it].y = src[1];
+                    if (r + 2 < Mb) va[it].z = src[2];
+                }
+            }
+        }
         const float* dn = dy + (size_t)n * P * OC;
+        const int nb = P * OC, nz = kDxMaxPos * OC + 4;
 #pragma unroll
-        for (int e = 0; e < BE; ++e) {
-            const int f = tid + 256 * e, p = f >> 6, k = f & 63;
-            vb[e] = (p < P && k < OC) ? dn[p * OC + k] : 0.f;
+        for (int it = 0; it < BI; ++it) {
+            const int e = 4 * (tid + 256 * it);
+            vb[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (e + 3 < nb) {
+                __builtin_memcpy(&vb[it], dn + e, 16);
+            } else {
+                if (e < nb) vb[it].x = dn[e];
+                if (e + 1 < nb) vb[it].y = dn[e + 1];
+                if (e + 2 < nb) vb[it].z = dn[e + 2];
+            }
         }
 #pragma unroll
-        for (int k = 0; k < KMAX; ++k)
-            if (k < 4 * KS) As[k * kDxRS + tid] = va[k];
+        for (int it = 0; it < AI; ++it) {
+            const int i = tid + 256 * it, k = i >> 6, r = 4 * (i & 63);
+            if (k < 4 * KS) *reinterpret_cast<float4*>(As + k * kDxRS + r) = va[it];
+        }
 #pragma unroll
-        for (int e = 0; e < BE; ++e) {
-            const int f = tid + 256 * e, p = f >> 6, k = f & 63;
-            if (k < OCS) Bs[p * OCS + k] = vb[e];
+        for (int it = 0; it < BI; ++it) {
+            const int e = 4 * (tid + 256 * it);
+            if (e < nz) *reinterpret_cast<float4*>(Bs + e) = vb[it];
         }
     }
     __syncthreads();
@@ -108,10 +132,10 @@ __global__ __launch_bounds__(256) void dgrad_fused_kernel(const float* __restric
 #pragma unroll
         for (int t = 0; t < 4; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     const float* ap = As + lg * kDxRS + wv * 16 + lr;
-    const float* bp = Bs + lr * OCS + lg;
+    const float* bp = Bs + lr * OC + lg;
     float a[4], b[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) b[t] = bp[t * 16 * OCS];
+    for (int t = 0; t < 4; ++t) b[t] = bp[t * 16 * OC];
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = ap[i * 64];
     for (int ks = 0; ks < KS; ++ks) {
@@ -119,7 +143,7 @@ __global__ __launch_bounds__(256) void dgrad_fused_kernel(const float* __restric
         const int kn = ks + 1 < KS ? (ks + 1) * 4 : 0;
         float an[4], bn[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) bn[t] = bp[t * 16 * OCS + kn];
+        for (int t = 0; t < 4; ++t) bn[t] = bp[t * 16 * OC + kn];
 #pragma unroll
         for (int i = 0; i < 4; ++i) an[i] = ap[i * 64 + kn * kDxRS];
 #pragma unroll
@@ -194,7 +218,7 @@ hipError_t conv_dgrad_fused(const ConvGeom& g, const float* dy, const float* w, 
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, dim3(256), d.lds * 4, s, dy, w, dx, mask,
                            mask_f32 ? 1 : 0, g.C, g.H, g.W, g.OC, g.OH, g.OW, g.PD, d.cb,
-                           d.chunks, d.ocs, d.ps);
+                           d.chunks, d.ps);
     };
     if (g.K == 3) go(dgrad_fused_kernel<3>);
     else go(dgrad_fused_kernel<5>);

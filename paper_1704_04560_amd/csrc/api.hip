@@ -83,6 +83,7 @@ struct Plan {
     size_t P = 0, ld = 0;
     std::vector<LayerPlan> L;
     int first_param = -1;
+    bool pool_into_first = false;  // layer 1's max pooling feeds layer 0's direct weight gradient
     bool x_convert = false;      // the input is converted (layout and/or type) before use
     int x_c = 1, x_hw = 1;       // conversion as NCHW -> NHWC with these channels / positions
     std::vector<PrepJob> jobs;   // weight preparation
@@ -254,6 +255,16 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         const ConvGeom g0{pl.B, first.c, first.h, first.w, first.oc, first.oh, first.ow, first.k,
                           first.s, first.p, first.g};
         first.direct = first_conv_direct(g0, pl.dt);
+    }
+    // A max pooling right above such a layer (window = stride, NHWC output) hands its output
+    // gradient and decisions to the direct weight-gradient kernel, which forms the layer's output
+    // gradient itself: the pooling backward launch goes away.
+    pl.pool_into_first = false;
+    if (first.direct && pl.L.size() > 2) {
+        const LayerPlan& p1 = pl.L[1];
+        bool kept_for_0 = false;  // a residual addition whose source is layer 0
+        for (const LayerPlan& q : pl.L) kept_for_0 = kept_for_0 || (q.kind == MTX_ADD && q.src == 0);
+        pl.pool_into_first = p1.kind == MTX_MAXPOOL && p1.k == p1.s && p1.nhwc && !kept_for_0;
     }
 
     // weight preparation jobs; every prepared tensor starts 16-byte aligned
@@ -967,11 +978,19 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         }
         if (lp.kind == MTX_CONV && lp.direct) {
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            FirstPool fp{};
+            if (pl.pool_into_first) {
+                const LayerPlan& p1 = pl.L[1];
+                fp.dy = ws + p1.dy_off;
+                fp.argmax = reinterpret_cast<const uint8_t*>(ws + p1.am_off);
+                fp.gate = lp.relu ? ws + p1.act_off : nullptr;
+                fp.k = p1.k;
+            }
             HIP_TRY(launch_site(m, "wgrad_direct", l, sw, [&] {
                         return first_conv_wgrad(dt, gs, pl.R, in_l, dy,
                                                 reinterpret_cast<float*>(ws + pl.first_part_off),
                                                 m->grads, ld, (long long)lp.w_off,
-                                                (long long)lp.b_off, sw);
+                                                (long long)lp.b_off, sw, fp);
                     }), "first convolution weight gradient");
         } else if (lp.kind == MTX_CONV) {
             ConvGeom gs{pl.Nb, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
@@ -1025,7 +1044,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                             return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32, skip,
                                            sp.relu ? ws + sp.act_off : nullptr, sp.act_f32, s);
                         }), "residual backward");
-        } else if (lp.need_dx) {
+        } else if (lp.need_dx && !(l == 1 && pl.pool_into_first)) {
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
                         return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
                                         reinterpret_cast<const uint8_t*>(ws + lp.am_off), dy, dx,

@@ -140,7 +140,8 @@ __global__ __launch_bounds__(256) void first_conv_wgrad_kernel(const T* __restri
                                                                const T* __restrict__ dy, int H,
                                                                int W, int OC, int PD, int OH,
                                                                int OW,
-                                                               float* __restrict__ partial)
+                                                               float* __restrict__ partial,
+                                                               FirstPool pool)
 {
     constexpr int KK = K * K;
     extern __shared__ __attribute__((aligned(16))) float sm[];
@@ -149,11 +150,72 @@ __global__ __launch_bounds__(256) void first_conv_wgrad_kernel(const T* __restri
     const int n = blockIdx.x, NO = OC * KK + OC;
     const int tid = threadIdx.x;
     const T* xn = x + (size_t)n * H * W;
-    const T* dn = dy + (size_t)n * OH * OW * OC;
-    const int nd = OH * OW * OC;  // a multiple of 4; dn is 8-byte (bf16) / 16-byte aligned
+    if (!pool.dy) {
+        const T* dn = dy + (size_t)n * OH * OW * OC;
+        const int nd = OH * OW * OC;  // a multiple of 4; dn is 8-byte (bf16) / 16-byte aligned
 #pragma unroll 4
-    for (int e = tid * 4; e < nd; e += 1024)
-        *reinterpret_cast<float4*>(ds + e) = load4(dn + e);
+        for (int e = tid * 4; e < nd; e += 1024)
+            *reinterpret_cast<float4*>(ds + e) = load4(dn + e);
+    } else {
+        // The output gradient comes from the max pooling above (window = stride = PK, NHWC):
+        // every position of a window gets the window's gradient if it holds the window's
+        // maximum, else 0 (and the window passes nothing where a ReLU on this layer made the
+        // pooled output non-positive); positions no window covers get 0.
+        const int PK = pool.k, PH = OH / PK, PW = OW / PK, CG = OC / 4;
+        const int ng = PH * PW * CG;
+        const T* gp = static_cast<const T*>(pool.dy) + (size_t)n * PH * PW * OC;
+        const uint8_t* ap = pool.argmax + (size_t)n * PH * PW * OC;
+        const T* yp = static_cast<const T*>(pool.gate);
+        if (yp) yp += (size_t)n * PH * PW * OC;
+        constexpr int kU = 4;  // window groups per thread and batch: all loads before the stores
+        for (int b0 = 0; b0 < ng; b0 += 256 * kU) {
+            float4 gv[kU];
+            unsigned am[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int gi = b0 + 256 * u + tid;
+                gv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                am[u] = 0xffffffffu;
+                if (gi < ng) {
+                    const int o = (gi / CG) * OC + (gi % CG) * 4;
+                    gv[u] = load4(gp + o);
+                    am[u] = *reinterpret_cast<const unsigned*>(ap + o);
+                    if (yp) {
+                        const float4 y = load4(yp + o);
+                        if (!(y.x > 0.f)) gv[u].x = 0.f;
+                        if (!(y.y > 0.f)) gv[u].y = 0.f;
+                        if (!(y.z > 0.f)) gv[u].z = 0.f;
+                        if (!(y.w > 0.f)) gv[u].w = 0.f;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int gi = b0 + 256 * u + tid;
+                if (gi >= ng) continue;
+                const int pos = gi / CG, c0 = (gi % CG) * 4;
+                const int ph = pos / PW, pw = pos - ph * PW;
+                for (int a = 0; a < PK; ++a)
+                    for (int b = 0; b < PK; ++b) {
+                        const unsigned wpos = (unsigned)(a * PK + b);
+                        const float4 v = make_float4(
+                            (am[u] & 0xffu) == wpos ? gv[u].x : 0.f,
+                            ((am[u] >> 8) & 0xffu) == wpos ? gv[u].y : 0.f,
+                            ((am[u] >> 16) & 0xffu) == wpos ? gv[u].z : 0.f,
+                            (am[u] >> 24) == wpos ? gv[u].w : 0.f);
+                        const int oh = ph * PK + a, ow = pw * PK + b;
+                        *reinterpret_cast<float4*>(ds + (oh * OW + ow) * OC + c0) = v;
+                    }
+            }
+        }
+        if (OH != PH * PK || OW != PW * PK) {
+            for (int e = tid * 4; e < OH * OW * OC; e += 1024) {
+                const int pos = e / OC, oh = pos / OW, ow = pos - oh * OW;
+                if (oh >= PH * PK || ow >= PW * PK)
+                    *reinterpret_cast<float4*>(ds + e) = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+    }
     for (int i = tid; i < H * W; i += 256) xs[i] = to_f32<T>(xn[i]);
     __syncthreads();
     const int grp = tid >> 5, j = tid & 31;
@@ -280,15 +342,18 @@ size_t first_conv_partial_floats(const ConvGeom& g, int R)
 
 hipError_t first_conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
                             float* partial, float* grads, long long ld, long long w_off,
-                            long long b_off, hipStream_t s)
+                            long long b_off, hipStream_t s, const FirstPool& pool)
 {
+    if (pool.dy && (pool.k < 1 || g.OH / pool.k < 1 || g.OW / pool.k < 1 ||
+                    pool.k * pool.k > 255))
+        return hipErrorInvalidValue;
     if (!first_conv_direct(g, dt)) return hipErrorInvalidValue;
     const int NO = g.OC * g.K * g.K + g.OC;
     const size_t shm = first_conv_lds_floats(g) * 4;
     const dim3 grid(R * g.N);  // g.N images per shard
     auto go = [&](auto kern, const auto* xt, const auto* dt_) {
         hipLaunchKernelGGL(kern, grid, dim3(256), shm, s, xt, dt_, g.H, g.W, g.OC, g.PD, g.OH,
-                           g.OW, partial);
+                           g.OW, partial, pool);
     };
     if (dt == DT_F32) {
         const float* xf = static_cast<const float*>(x);

@@ -245,11 +245,20 @@ bool first_conv_direct(const ConvGeom& g, int dt);
 hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
                           const float* bias, void* y, bool y_f32, bool relu, hipStream_t s);
 // weight and bias gradients of R shards of g.N images; partial holds
-// first_conv_partial_floats(g, R) floats of scratch.
+// first_conv_partial_floats(g, R) floats of scratch.  With pool.dy set, the layer's output
+// gradient is not read from dy but formed from the max pooling above it (window = stride =
+// pool.k, NHWC): pool.dy its output gradient, pool.argmax its window positions, pool.gate its
+// output when this layer has a ReLU (else null).
+struct FirstPool {
+    const void* dy = nullptr;
+    const uint8_t* argmax = nullptr;
+    const void* gate = nullptr;
+    int k = 0;
+};
 size_t first_conv_partial_floats(const ConvGeom& g, int R);
 hipError_t first_conv_wgrad(Dt dt, const ConvGeom& g, int R, const void* x, const void* dy,
                             float* partial, float* grads, long long ld, long long w_off,
-                            long long b_off, hipStream_t s);
+                            long long b_off, hipStream_t s, const FirstPool& pool = FirstPool{});
 
 // dgrad_fused.hip: fp32 data gradient of a stride-1, ungrouped 3x3 or 5x5 convolution with at
 // most 60 output channels whose output has at most 64 positions per image, col tile and col2im

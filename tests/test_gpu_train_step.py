@@ -153,7 +153,8 @@ def test_single_channel_first_convolution(dtype, oc, k, pad, relu):
 
 def test_first_convolution_takes_the_direct_kernels():
     """LeNet's first layer (one channel, 5x5, 20 outputs) runs on the direct kernels, and a first
-    convolution outside their limits (64 outputs of a 7x7 window) on the matrix kernels."""
+    convolution outside their limits (64 outputs of a 7x7 window) on the matrix kernels; with the
+    direct kernels, the pooling above needs no backward launch of its own."""
     for net, direct in ((wl.LENET, True), (_single_channel(wl.F32, 64, 7, 3, True), False)):
         layers = wl.layer_tuples(net)
         model = mtx.Model(net.in_shape, layers, net.dtype, 2, 3, seed=1)
@@ -163,6 +164,8 @@ def test_first_convolution_takes_the_direct_kernels():
         assert (("fwd_direct", 0) in names) == direct, names
         assert (("wgrad_direct", 0) in names) == direct, names
         assert (("fwd", 0) in names) != direct, names
+        # the 2x2 pooling above hands its gradient to the direct kernel: no pooling backward
+        assert (("pool_bwd", 1) in names) != direct, names
 
 
 def _small_image_dgrad(dtype, k):

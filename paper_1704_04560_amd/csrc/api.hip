@@ -264,7 +264,10 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         const LayerPlan& p1 = pl.L[1];
         bool kept_for_0 = false;  // a residual addition whose source is layer 0
         for (const LayerPlan& q : pl.L) kept_for_0 = kept_for_0 || (q.kind == MTX_ADD && q.src == 0);
-        pl.pool_into_first = p1.kind == MTX_MAXPOOL && p1.k == p1.s && p1.nhwc && !kept_for_0;
+        const ConvGeom g0{pl.B, first.c, first.h, first.w, first.oc, first.oh, first.ow, first.k,
+                          first.s, first.p, first.g};
+        pl.pool_into_first = p1.kind == MTX_MAXPOOL && p1.k == p1.s && p1.nhwc && !kept_for_0 &&
+                             first_conv_pool_ok(g0, p1.k);
     }
 
     // weight preparation jobs; every prepared tensor starts 16-byte aligned
@@ -906,9 +909,15 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         const float* bias = m->w + lp.b_off;
         if (lp.kind == MTX_CONV && lp.direct) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
+            FirstPoolFwd fp{};
+            if (pl.pool_into_first) {
+                fp.y = ws + pl.L[1].act_off;
+                fp.argmax = reinterpret_cast<uint8_t*>(ws + pl.L[1].am_off);
+                fp.k = pl.L[1].k;
+            }
             HIP_TRY(launch_site(m, "fwd_direct", (int)l, s, [&] {
                         return first_conv_fwd(dt, g, in, m->w + lp.w_off, bias, out, lp.act_f32,
-                                              lp.relu, s);
+                                              lp.relu, s, fp);
                     }), "first convolution forward");
         } else if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
@@ -935,7 +944,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                         return add_fwd(dt, lp.out_elems * pl.B, in, ws + pl.L[lp.src].act_off, out,
                                        lp.relu, s);
                     }), "residual addition");
-        } else {
+        } else if (!(l == 1 && pl.pool_into_first)) {  // else computed with layer 0
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
                         return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc, in, out,
                                         reinterpret_cast<uint8_t*>(ws + lp.am_off), s);

@@ -22,18 +22,29 @@ static size_t first_conv_lds_floats(const ConvGeom& g)
 
 // Output rows per forward block: as many whole rows as fit in 256 lanes, evened out over the
 // image's rows
-static int first_conv_rows(const ConvGeom& g)
+// (with a pooling window pk fused in, a multiple of pk, so that no window straddles two blocks;
+// 0 when pk rows do not fit)
+static int first_conv_rows(const ConvGeom& g, int pk = 1)
 {
-    const int fit = std::max(1, std::min(g.OH, 256 / g.OW));
+    int fit = std::max(1, std::min(g.OH, 256 / g.OW));
+    fit -= fit % pk;
+    if (fit < 1) return 0;
     const int blocks = (g.OH + fit - 1) / fit;
-    return (g.OH + blocks - 1) / blocks;
+    const int rb = (g.OH + blocks - 1) / blocks;
+    return (rb + pk - 1) / pk * pk;
 }
 
 // LDS floats of the forward block: its input rows and its output tile
-static size_t first_conv_fwd_lds_floats(const ConvGeom& g)
+static size_t first_conv_fwd_lds_floats(const ConvGeom& g, int pk = 1)
 {
-    const int rb = first_conv_rows(g);
+    const int rb = first_conv_rows(g, pk);
     return ((size_t)(rb + g.K - 1) * g.W + 3) / 4 * 4 + (size_t)rb * g.OW * g.OC;
+}
+
+bool first_conv_pool_ok(const ConvGeom& g, int pk)
+{
+    return pk >= 1 && pk * pk <= 255 && g.OH / pk >= 1 && g.OW / pk >= 1 &&
+           first_conv_rows(g, pk) >= pk && first_conv_fwd_lds_floats(g, pk) * 4 <= kFirstMaxLds;
 }
 
 bool first_conv_direct(const ConvGeom& g, int)
@@ -78,7 +89,8 @@ __global__ __launch_bounds__(256) void first_conv_fwd_kernel(const T* __restrict
                                                              const float* __restrict__ bias,
                                                              TY* __restrict__ y, int H, int W,
                                                              int OC, int PD, int OH, int OW,
-                                                             int RB, int tiles, int relu)
+                                                             int RB, int tiles, int relu,
+                                                             FirstPoolFwd pool)
 {
     constexpr int KK = K * K;
     extern __shared__ __attribute__((aligned(16))) float sm[];
@@ -125,6 +137,34 @@ __global__ __launch_bounds__(256) void first_conv_fwd_kernel(const T* __restrict
     TY* yt = y + ((size_t)n * OH + oh0) * OW * OC;
     for (int e = threadIdx.x * 4; e < rows * OW * OC; e += blockDim.x * 4)
         store4(yt + e, *reinterpret_cast<const float4*>(ys + e));
+    if (!pool.y) return;
+    // The max pooling above (window = stride = PK, NHWC) over the block's rows (RB and oh0 are
+    // multiples of PK): per window and 4 channels, the first maximum in row-major window order
+    // of the stored (compute-type) outputs, and its window position.
+    const int PK = pool.k, PH = OH / PK, PW = OW / PK, CG = OC / 4;
+    const int pr0 = oh0 / PK, prows = min(rows / PK, PH - pr0);
+    TY* py = static_cast<TY*>(pool.y);
+    for (int gi = threadIdx.x; gi < prows * PW * CG; gi += blockDim.x) {
+        const int pos = gi / CG, c0 = (gi - pos * CG) * 4;
+        const int pr = pos / PW, pw = pos - pr * PW;
+        const float* w0 = ys + ((pr * PK) * OW + pw * PK) * OC + c0;
+        float bv[4];
+        unsigned bi[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bv[e] = to_f32<TY>(from_f32<TY>(w0[e]));
+        for (int a = 0; a < PK; ++a)
+            for (int b = 0; b < PK; ++b) {
+                const float* wp = w0 + (a * OW + b) * OC;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float tv = to_f32<TY>(from_f32<TY>(wp[e]));
+                    if (tv > bv[e]) { bv[e] = tv; bi[e] = (unsigned)(a * PK + b); }
+                }
+            }
+        const size_t o = (((size_t)n * PH + pr0 + pr) * PW + pw) * OC + c0;
+        store4(py + o, make_float4(bv[0], bv[1], bv[2], bv[3]));
+        *reinterpret_cast<unsigned*>(pool.argmax + o) = bi[0] | bi[1] << 8 | bi[2] << 16 | bi[3] << 24;
+    }
 }
 
 // One block per image n: partial[n][co * KK + kk] = sum over the image's output positions of
@@ -302,17 +342,21 @@ __global__ __launch_bounds__(256) void first_conv_wgrad_reduce_kernel(
 }
 
 hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
-                          const float* bias, void* y, bool y_f32, bool relu, hipStream_t s)
+                          const float* bias, void* y, bool y_f32, bool relu, hipStream_t s,
+                          const FirstPoolFwd& pool)
 {
     if (!first_conv_direct(g, dt)) return hipErrorInvalidValue;
-    const int rb = first_conv_rows(g);
+    const int pk = pool.y ? pool.k : 1;
+    if (pool.y && (!first_conv_pool_ok(g, pk) || (y_f32 && dt != DT_F32)))
+        return hipErrorInvalidValue;  // the pooled output has the conv output's type
+    const int rb = first_conv_rows(g, pk);
     const int tiles = (g.OH + rb - 1) / rb;
     const dim3 grid(tiles * g.N);
     const int threads = (rb * g.OW + 63) / 64 * 64;
-    const size_t shm = first_conv_fwd_lds_floats(g) * 4;
+    const size_t shm = first_conv_fwd_lds_floats(g, pk) * 4;
     auto go = [&](auto kern, const auto* xt, auto* yt) {
         hipLaunchKernelGGL(kern, grid, dim3(threads), shm, s, xt, w, bias, yt, g.H, g.W, g.OC,
-                           g.PD, g.OH, g.OW, rb, tiles, relu ? 1 : 0);
+                           g.PD, g.OH, g.OW, rb, tiles, relu ? 1 : 0, pool);
     };
     float* yf = static_cast<float*>(y);
     if (dt == DT_F32) {

@@ -242,8 +242,17 @@ constexpr int kFirstMaxOC = 32;
 constexpr size_t kFirstMaxLds = 64 * 1024;
 bool first_conv_direct(const ConvGeom& g, int dt);
 // x: the input [N][H][W] (one channel) in the compute type; w: fp32 [OC][K][K]; y NHWC.
+// With pool.y set, the max pooling above the layer (window = stride = pool.k, NHWC output of the
+// conv output's type) is computed too: pool.y its output, pool.argmax its window positions.
+struct FirstPoolFwd {
+    void* y = nullptr;
+    uint8_t* argmax = nullptr;
+    int k = 0;
+};
+bool first_conv_pool_ok(const ConvGeom& g, int pk);
 hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
-                          const float* bias, void* y, bool y_f32, bool relu, hipStream_t s);
+                          const float* bias, void* y, bool y_f32, bool relu, hipStream_t s,
+                          const FirstPoolFwd& pool = FirstPoolFwd{});
 // weight and bias gradients of R shards of g.N images; partial holds
 // first_conv_partial_floats(g, R) floats of scratch.  With pool.dy set, the layer's output
 // gradient is not read from dy but formed from the max pooling above it (window = stride =

@@ -151,6 +151,18 @@ def test_single_channel_first_convolution(dtype, oc, k, pad, relu):
     run_case(f"{net.name}-{dtype}", net, 3, 5, 2, 11, 0.05, 0.9)
 
 
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("pool_k,pool_s,relu", [(3, 3, True), (2, 1, True), (3, 3, False)])
+def test_single_channel_first_convolution_pool_windows(dtype, pool_k, pool_s, relu):
+    """The pooling above a direct first convolution: a 3x3/3 window (folded into the direct
+    kernels, with ragged rows and columns left over, with and without the ReLU gate) and an
+    overlapping 2x2/1 window (not folded: the pooling kernels run)."""
+    layers = (wl.conv(8, 5, pad=2, relu=relu), wl.maxpool(pool_k, pool_s), wl.conv(6, 3, relu=True),
+              wl.fc(5))
+    net = wl.Net(f"one-channel-pool{pool_k}{pool_s}", (1, 14, 13), layers, dtype, "normal")
+    run_case(f"{net.name}-{dtype}-{relu}", net, 2, 5, 2, 14, 0.05, 0.9)
+
+
 def test_first_convolution_takes_the_direct_kernels():
     """LeNet's first layer (one channel, 5x5, 20 outputs) runs on the direct kernels, and a first
     convolution outside their limits (64 outputs of a 7x7 window) on the matrix kernels; with the

@@ -887,11 +887,15 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                     : static_cast<const void*>(x);
 
     // ---- weights in the layouts the GEMMs read, input in the compute type and layout ----
-    HIP_TRY(launch_site(m, "prep_w", -1, s, [&] {
-                return prep_weights(dt, reinterpret_cast<const PrepJob*>(ws + pl.jobs_off),
-                                    (int)pl.jobs.size(), pl.prep_blocks, m->w, ws + pl.prep_off, s);
-            }), "weight preparation");
     const LayerPlan& l0 = pl.L.front();
+    // a direct first convolution carries the weight preparation in its own launch
+    const bool prep_with_first = l0.direct && !pl.jobs.empty();
+    if (!prep_with_first)
+        HIP_TRY(launch_site(m, "prep_w", -1, s, [&] {
+                    return prep_weights(dt, reinterpret_cast<const PrepJob*>(ws + pl.jobs_off),
+                                        (int)pl.jobs.size(), pl.prep_blocks, m->w,
+                                        ws + pl.prep_off, s);
+                }), "weight preparation");
     if (pl.x_convert)
         HIP_TRY(launch_site(m, "prep_x", -1, s, [&] {
                     return l0.run ? to_nhwc_padded(dt, x, ws + pl.xin_off, pl.B, l0.c, l0.h, l0.w,
@@ -915,10 +919,18 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                 fp.argmax = reinterpret_cast<uint8_t*>(ws + pl.L[1].am_off);
                 fp.k = pl.L[1].k;
             }
+            FirstPrep pp{};
+            if (prep_with_first) {
+                pp.jobs = reinterpret_cast<const PrepJob*>(ws + pl.jobs_off);
+                pp.njobs = (int)pl.jobs.size();
+                pp.blocks = pl.prep_blocks;
+                pp.w = m->w;
+                pp.dst = ws + pl.prep_off;
+            }
             HIP_TRY(launch_site(m, "fwd_direct", (int)l, s, [&] {
                         return first_conv_fwd(dt, g, in, m->w + lp.w_off, bias, out, lp.act_f32,
-                                              lp.relu, s, fp);
-                    }), "first convolution forward");
+                                              lp.relu, s, fp, pp);
+                    }), "first convolution forward (and the weight preparation)");
         } else if (lp.kind == MTX_CONV) {
             ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
             HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {

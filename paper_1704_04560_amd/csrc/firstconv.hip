@@ -9,6 +9,7 @@
 
 #include "device_common.h"
 #include "internal.h"
+#include "prep.h"
 
 namespace mtx {
 
@@ -90,11 +91,17 @@ __global__ __launch_bounds__(256) void first_conv_fwd_kernel(const T* __restrict
                                                              TY* __restrict__ y, int H, int W,
                                                              int OC, int PD, int OH, int OW,
                                                              int RB, int tiles, int relu,
-                                                             FirstPoolFwd pool)
+                                                             FirstPoolFwd pool, FirstPrep prep)
 {
+    if ((int)blockIdx.x >= prep.first) {
+        // the weight preparation rides on this launch (nothing of it is read here)
+        prep_block<T>(prep.jobs, prep.njobs, prep.w, static_cast<T*>(prep.dst),
+                      (int)blockIdx.x - prep.first);
+        return;
+    }
     constexpr int KK = K * K;
     extern __shared__ __attribute__((aligned(16))) float sm[];
-    const int n = blockIdx.x / tiles, oh0 = (blockIdx.x - n * tiles) * RB;
+    const int n = blockIdx.x / tiles, oh0 = (blockIdx.x - n * tiles) * RB;  // n < images
     const int rows = min(RB, OH - oh0);
     const int IR = RB + K - 1;
     float* xs = sm;                            // input rows oh0 - PD .. oh0 - PD + IR - 1
@@ -343,7 +350,7 @@ __global__ __launch_bounds__(256) void first_conv_wgrad_reduce_kernel(
 
 hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
                           const float* bias, void* y, bool y_f32, bool relu, hipStream_t s,
-                          const FirstPoolFwd& pool)
+                          const FirstPoolFwd& pool, const FirstPrep& prep)
 {
     if (!first_conv_direct(g, dt)) return hipErrorInvalidValue;
     const int pk = pool.y ? pool.k : 1;
@@ -351,12 +358,17 @@ hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* 
         return hipErrorInvalidValue;  // the pooled output has the conv output's type
     const int rb = first_conv_rows(g, pk);
     const int tiles = (g.OH + rb - 1) / rb;
-    const dim3 grid(tiles * g.N);
-    const int threads = (rb * g.OW + 63) / 64 * 64;
+    // blocks [0, tiles * N): the convolution; then the preparation blocks (256 threads each)
+    FirstPrep pr = prep;
+    pr.first = tiles * g.N;
+    if (pr.blocks < 0 || (pr.blocks > 0 && (!pr.jobs || pr.njobs < 1 || !pr.dst || !pr.w)))
+        return hipErrorInvalidValue;
+    const dim3 grid(tiles * g.N + pr.blocks);
+    const int threads = pr.blocks > 0 ? 256 : (rb * g.OW + 63) / 64 * 64;
     const size_t shm = first_conv_fwd_lds_floats(g, pk) * 4;
     auto go = [&](auto kern, const auto* xt, auto* yt) {
         hipLaunchKernelGGL(kern, grid, dim3(threads), shm, s, xt, w, bias, yt, g.H, g.W, g.OC,
-                           g.PD, g.OH, g.OW, rb, tiles, relu ? 1 : 0, pool);
+                           g.PD, g.OH, g.OW, rb, tiles, relu ? 1 : 0, pool, pr);
     };
     float* yf = static_cast<float*>(y);
     if (dt == DT_F32) {

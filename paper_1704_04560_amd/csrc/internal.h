@@ -249,10 +249,19 @@ struct FirstPoolFwd {
     uint8_t* argmax = nullptr;
     int k = 0;
 };
+// With prep.blocks > 0 the launch also runs the weight preparation (prep_weights' blocks
+// after its own; prep.first is set by the launcher).
+struct FirstPrep {
+    const PrepJob* jobs = nullptr;
+    int njobs = 0, blocks = 0, first = 0;
+    const float* w = nullptr;
+    void* dst = nullptr;
+};
 bool first_conv_pool_ok(const ConvGeom& g, int pk);
 hipError_t first_conv_fwd(Dt dt, const ConvGeom& g, const void* x, const float* w,
                           const float* bias, void* y, bool y_f32, bool relu, hipStream_t s,
-                          const FirstPoolFwd& pool = FirstPoolFwd{});
+                          const FirstPoolFwd& pool = FirstPoolFwd{},
+                          const FirstPrep& prep = FirstPrep{});
 // weight and bias gradients of R shards of g.N images; partial holds
 // first_conv_partial_floats(g, R) floats of scratch.  With pool.dy set, the layer's output
 // gradient is not read from dy but formed from the max pooling above it (window = stride =

@@ -210,93 +210,118 @@ int orc_param_count(int in_c, int in_h, int in_w, int n_layers, const orc_layer*
 /* ------------------------------------------------------------------------------------------ */
 
 /* Convolution, NCHW, weights [oc][c/g][k][k], zero padding p, stride s, g groups.
- * y[n][o][i][j] = b[o] + sum_{c' , u, v} W[o][c'][u][v] * x[n][grp*c/g + c'][i*s - p + u][j*s - p + v] */
+ * y[n][o][i][j] = b[o] + sum_{c' , u, v} W[o][c'][u][v] * x[n][grp*c/g + c'][i*s - p + u][j*s - p + v]
+ * Every output's sum is taken in ascending (c', u, v) order over the taps inside the image; a
+ * whole output row is carried along at once (one running sum per column). */
 void orc_conv_fwd(int N, int C, int H, int W, int OC, int K, int S, int P, int Gr,
                   const double* x, const double* w, const double* b, double* y)
 {
     int OH = (H + 2 * P - K) / S + 1, OW = (W + 2 * P - K) / S + 1;
     int cg = C / Gr, og = OC / Gr;
-#pragma omp parallel for collapse(2) schedule(static)
-    for (int n = 0; n < N; n++)
-        for (int o = 0; o < OC; o++) {
-            int grp = o / og;
-            for (int i = 0; i < OH; i++)
-                for (int j = 0; j < OW; j++) {
-                    double acc = b ? b[o] : 0.0;
+#pragma omp parallel
+    {
+        double* row = (double*)malloc(sizeof(double) * (size_t)OW);
+#pragma omp for collapse(2) schedule(static)
+        for (int n = 0; n < N; n++)
+            for (int o = 0; o < OC; o++) {
+                if (!row) continue;
+                int grp = o / og;
+                for (int i = 0; i < OH; i++) {
+                    for (int j = 0; j < OW; j++) row[j] = b ? b[o] : 0.0;
                     for (int cc = 0; cc < cg; cc++)
                         for (int u = 0; u < K; u++) {
                             int hi = i * S - P + u;
                             if (hi < 0 || hi >= H) continue;
+                            const double* xr = x + (((long)n * C + grp * cg + cc) * H + hi) * W;
                             for (int v = 0; v < K; v++) {
-                                int wi = j * S - P + v;
-                                if (wi < 0 || wi >= W) continue;
-                                acc += w[(((long)o * cg + cc) * K + u) * K + v] *
-                                       x[(((long)n * C + grp * cg + cc) * H + hi) * W + wi];
+                                const double wv = w[(((long)o * cg + cc) * K + u) * K + v];
+                                /* columns j whose tap j*S - P + v lies inside the row */
+                                int j0 = P - v > 0 ? (P - v + S - 1) / S : 0;
+                                int j1 = (W - 1 + P - v) >= 0 ? (W - 1 + P - v) / S + 1 : 0;
+                                if (j1 > OW) j1 = OW;
+                                for (int j = j0; j < j1; j++) row[j] += wv * xr[j * S - P + v];
                             }
                         }
-                    y[(((long)n * OC + o) * OH + i) * OW + j] = acc;
+                    for (int j = 0; j < OW; j++) y[(((long)n * OC + o) * OH + i) * OW + j] = row[j];
                 }
-        }
+            }
+        free(row);
+    }
 }
 
 /* Gradients of the convolution: dW = sum over samples and output positions of dy times the
- * input patch, db = sum of dy, dx = adjoint of the forward index map (dx may be NULL). */
+ * input patch, db = sum of dy, dx = adjoint of the forward index map (dx may be NULL).
+ * dW[o][c'][u][v] sums over (n, i, j) in ascending order (the K sums of one kernel row are
+ * carried along together); dx[n][c][h][w] gathers sum_{o in the group, i, j} dy[n][o][i][j] *
+ * W[o][c'][h - i*s + p][w - j*s + p] in ascending (o, i, j) order over the taps that exist. */
 void orc_conv_bwd(int N, int C, int H, int W, int OC, int K, int S, int P, int Gr,
                   const double* x, const double* w, const double* dy, double* dx, double* dw,
                   double* db)
 {
     int OH = (H + 2 * P - K) / S + 1, OW = (W + 2 * P - K) / S + 1;
     int cg = C / Gr, og = OC / Gr;
-#pragma omp parallel for schedule(static)
-    for (int o = 0; o < OC; o++) {
-        int grp = o / og;
-        double sb = 0.0;
-        for (int n = 0; n < N; n++)
-            for (int i = 0; i < OH; i++)
-                for (int j = 0; j < OW; j++) sb += dy[(((long)n * OC + o) * OH + i) * OW + j];
-        if (db) db[o] = sb;
-        for (int cc = 0; cc < cg; cc++)
-            for (int u = 0; u < K; u++)
-                for (int v = 0; v < K; v++) {
-                    double acc = 0.0;
+#pragma omp parallel
+    {
+        double* acc = (double*)malloc(sizeof(double) * (size_t)K);
+#pragma omp for schedule(static)
+        for (int o = 0; o < OC; o++) {
+            if (!acc) continue;
+            int grp = o / og;
+            double sb = 0.0;
+            for (int n = 0; n < N; n++)
+                for (int i = 0; i < OH; i++)
+                    for (int j = 0; j < OW; j++) sb += dy[(((long)n * OC + o) * OH + i) * OW + j];
+            if (db) db[o] = sb;
+            for (int cc = 0; cc < cg; cc++)
+                for (int u = 0; u < K; u++) {
+                    for (int v = 0; v < K; v++) acc[v] = 0.0;
                     for (int n = 0; n < N; n++)
                         for (int i = 0; i < OH; i++) {
                             int hi = i * S - P + u;
                             if (hi < 0 || hi >= H) continue;
+                            const double* dyr = dy + (((long)n * OC + o) * OH + i) * OW;
+                            const double* xr = x + (((long)n * C + grp * cg + cc) * H + hi) * W;
                             for (int j = 0; j < OW; j++) {
-                                int wi = j * S - P + v;
-                                if (wi < 0 || wi >= W) continue;
-                                acc += dy[(((long)n * OC + o) * OH + i) * OW + j] *
-                                       x[(((long)n * C + grp * cg + cc) * H + hi) * W + wi];
+                                const double d = dyr[j];
+                                for (int v = 0; v < K; v++) {
+                                    int wi = j * S - P + v;
+                                    if (wi < 0 || wi >= W) continue;
+                                    acc[v] += d * xr[wi];
+                                }
                             }
                         }
-                    dw[(((long)o * cg + cc) * K + u) * K + v] = acc;
-                }
-    }
-    if (!dx) return;
-#pragma omp parallel for schedule(static)
-    for (int n = 0; n < N; n++) {
-        double* dxn = dx + (long)n * C * H * W;
-        for (long t = 0; t < (long)C * H * W; t++) dxn[t] = 0.0;
-        for (int o = 0; o < OC; o++) {
-            int grp = o / og;
-            for (int i = 0; i < OH; i++)
-                for (int j = 0; j < OW; j++) {
-                    double g = dy[(((long)n * OC + o) * OH + i) * OW + j];
-                    for (int cc = 0; cc < cg; cc++)
-                        for (int u = 0; u < K; u++) {
-                            int hi = i * S - P + u;
-                            if (hi < 0 || hi >= H) continue;
-                            for (int v = 0; v < K; v++) {
-                                int wi = j * S - P + v;
-                                if (wi < 0 || wi >= W) continue;
-                                dxn[((long)(grp * cg + cc) * H + hi) * W + wi] +=
-                                    g * w[(((long)o * cg + cc) * K + u) * K + v];
-                            }
-                        }
+                    for (int v = 0; v < K; v++) dw[(((long)o * cg + cc) * K + u) * K + v] = acc[v];
                 }
         }
+        free(acc);
     }
+    if (!dx) return;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int n = 0; n < N; n++)
+        for (int c = 0; c < C; c++) {
+            int grp = c / cg, cc = c % cg;
+            for (int hi = 0; hi < H; hi++)
+                for (int wi = 0; wi < W; wi++) {
+                    /* outputs whose window covers (hi, wi): u = hi + p - i*s in [0, K) */
+                    int i0 = hi + P - K + 1 > 0 ? (hi + P - K + 1 + S - 1) / S : 0;
+                    int i1 = (hi + P) / S + 1;
+                    int j0 = wi + P - K + 1 > 0 ? (wi + P - K + 1 + S - 1) / S : 0;
+                    int j1 = (wi + P) / S + 1;
+                    if (i1 > OH) i1 = OH;
+                    if (j1 > OW) j1 = OW;
+                    double a = 0.0;
+                    for (int o = grp * og; o < (grp + 1) * og; o++)
+                        for (int i = i0; i < i1; i++) {
+                            int u = hi + P - i * S;
+                            for (int j = j0; j < j1; j++) {
+                                int v = wi + P - j * S;
+                                a += dy[(((long)n * OC + o) * OH + i) * OW + j] *
+                                     w[(((long)o * cg + cc) * K + u) * K + v];
+                            }
+                        }
+                    dx[(((long)n * C + c) * H + hi) * W + wi] = a;
+                }
+        }
 }
 
 /* Fully connected: y[n][o] = b[o] + sum_i W[o][i] x[n][i], W stored [out][in]. */
@@ -312,7 +337,9 @@ void orc_fc_fwd(int N, int IN, int OUT, const double* x, const double* w, const 
         }
 }
 
-/* dW[o][i] = sum_n dy[n][o] x[n][i]; db[o] = sum_n dy[n][o]; dx[n][i] = sum_o dy[n][o] W[o][i]. */
+/* dW[o][i] = sum_n dy[n][o] x[n][i]; db[o] = sum_n dy[n][o]; dx[n][i] = sum_o dy[n][o] W[o][i].
+ * Each sum runs in ascending order of its index (n, resp. o); a whole row of dW (resp. a chunk of
+ * a row of dx) is carried along at once. */
 void orc_fc_bwd(int N, int IN, int OUT, const double* x, const double* w, const double* dy,
                 double* dx, double* dw, double* db)
 {
@@ -321,19 +348,27 @@ void orc_fc_bwd(int N, int IN, int OUT, const double* x, const double* w, const 
         double sb = 0.0;
         for (int n = 0; n < N; n++) sb += dy[(long)n * OUT + o];
         if (db) db[o] = sb;
-        for (int i = 0; i < IN; i++) {
-            double acc = 0.0;
-            for (int n = 0; n < N; n++) acc += dy[(long)n * OUT + o] * x[(long)n * IN + i];
-            dw[(long)o * IN + i] = acc;
+        double* dwo = dw + (long)o * IN;
+        for (int i = 0; i < IN; i++) dwo[i] = 0.0;
+        for (int n = 0; n < N; n++) {
+            const double d = dy[(long)n * OUT + o];
+            const double* xn = x + (long)n * IN;
+            for (int i = 0; i < IN; i++) dwo[i] += d * xn[i];
         }
     }
     if (!dx) return;
+    const int CH = 256, nch = (IN + CH - 1) / CH;
 #pragma omp parallel for collapse(2) schedule(static)
     for (int n = 0; n < N; n++)
-        for (int i = 0; i < IN; i++) {
-            double acc = 0.0;
-            for (int o = 0; o < OUT; o++) acc += dy[(long)n * OUT + o] * w[(long)o * IN + i];
-            dx[(long)n * IN + i] = acc;
+        for (int ch = 0; ch < nch; ch++) {
+            const int i0 = ch * CH, i1 = i0 + CH < IN ? i0 + CH : IN;
+            double* dxn = dx + (long)n * IN;
+            for (int i = i0; i < i1; i++) dxn[i] = 0.0;
+            for (int o = 0; o < OUT; o++) {
+                const double d = dy[(long)n * OUT + o];
+                const double* wo = w + (long)o * IN;
+                for (int i = i0; i < i1; i++) dxn[i] += d * wo[i];
+            }
         }
 }
 
@@ -474,6 +509,9 @@ static uint64_t splitmix64_first(uint64_t key)
     return z ^ (z >> 31);
 }
 
+/* The generator on its own, for checking it against the published reference outputs. */
+uint64_t orc_splitmix64_first(uint64_t key) { return splitmix64_first(key); }
+
 int orc_init_glorot(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L,
                     uint64_t seed, float* w)
 {
@@ -540,12 +578,23 @@ static void layer_fwd(const orc_geom* g, int N, const double* a, const double* w
  *   max-pool decisions (int32 window index, concatenated over pool layers) and the ReLU
  *   decisions (int8, concatenated over ReLU layers).
  *   pool_hint / relu_hint (optional, same layout, -1 = no hint) replace a decision by another one
- *   only where the oracle's own rounding-error bound for a float computation of the forward pass
- *   admits both; any other hint makes the call fail with ORC_EHINT. */
+ *   only where both are plausible outcomes of a float evaluation of the forward pass; any other
+ *   hint makes the call fail with ORC_EHINT.  A hint is admitted when the gap it has to bridge
+ *   is within BOTH of these limits:
+ *     (1) the rigorous forward error bound of a float evaluation (propagated layer by layer);
+ *     (2) a window that does not grow with depth: hint_rel times the scale of the layer's own
+ *         values in this shard.  For a pooling window the gap is (oracle's maximum - hinted
+ *         element) and the window is 2 * hint_rel * max|pool input| (each of the two elements
+ *         may be off by hint_rel * max in an evaluation whose stored outputs agree with the
+ *         oracle's to hint_rel of the tensor's maximum); for a ReLU the gap is |pre-activation|
+ *         and the window is hint_rel * max(pre-activation, 0) (the layer's largest output).
+ *   hint_rel must be positive when hints are given: it is the per-tensor tolerance to which the
+ *   caller compares stored outputs, so a decision outside the window would also show up there. */
 int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, int R, int Nb,
                    int prec, const float* x, const int32_t* labels, const float* w,
                    const float* v, float lr, float mu, const int32_t* pool_hint,
-                   const int8_t* relu_hint, double* loss_out, float* shard_loss, float* grads,
+                   const int8_t* relu_hint, double hint_rel, double* loss_out, float* shard_loss,
+                   float* grads,
                    float* gavg, float* w_new, float* v_new, float* acts, int32_t* pool_argmax,
                    int8_t* relu_mask)
 {
@@ -558,6 +607,7 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
     const int B = R * Nb;
     const long in_sz = (long)in_c * in_h * in_w;
     const int track = (pool_hint || relu_hint) ? 1 : 0; /* error bounds needed for hints */
+    if (track && !(hint_rel > 0.0 && hint_rel < 1.0)) { free(G); return ORC_EINVAL; }
     if (prec < ORC_PREC_F32 || prec > ORC_PREC_EXACT) { free(G); return ORC_EINVAL; }
     const int bf16 = (prec == ORC_PREC_BF16);
     /* storage rounding of activations and data-gradients; final-layer outputs use `store32` */
@@ -671,6 +721,11 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                 if (pool_hint) {
                     const int32_t* hint = pool_hint + pool_off[l] + (long)r * sz;
                     long per = (long)g->oh * g->ow;
+                    const long insz = (long)g->c * g->h * g->w * Nb;
+                    double scale = 0.0; /* largest magnitude of this shard's pool input */
+                    for (long t = 0; t < insz; t++)
+                        if (fabs(a[l][t]) > scale) scale = fabs(a[l][t]);
+                    const double window = 2.0 * hint_rel * scale;
                     for (long t = 0; t < sz; t++) {
                         int hv = hint[t];
                         if (hv < 0 || hv == am[l][t]) continue;
@@ -681,7 +736,9 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                         long base = nc * g->h * g->w + (long)(i * g->s) * g->w + j * g->s;
                         long po = base + (long)(own / g->k) * g->w + own % g->k;
                         long ph = base + (long)(hv / g->k) * g->w + hv % g->k;
-                        if (a[l][po] - a[l][ph] > e[l][po] + e[l][ph]) { rc = ORC_EHINT; goto done; }
+                        double lim = e[l][po] + e[l][ph];
+                        if (window < lim) lim = window;
+                        if (a[l][po] - a[l][ph] > lim) { rc = ORC_EHINT; goto done; }
                         am[l][t] = hv;
                         a[l + 1][t] = a[l][ph];
                     }
@@ -744,6 +801,12 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                     }
                 }
                 }
+                double rwindow = 0.0; /* hint_rel times the layer's largest output here */
+                if (g->relu && relu_hint) {
+                    for (long t = 0; t < sz; t++)
+                        if (z[l][t] > rwindow) rwindow = z[l][t];
+                    rwindow *= hint_rel;
+                }
                 for (long t = 0; t < sz; t++) {
                     double zt = z[l][t];
                     int pass = 1;
@@ -752,7 +815,8 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                         if (relu_hint) {
                             int8_t hv = relu_hint[relu_off[l] + (long)r * sz + t];
                             if (hv >= 0 && hv != pass) {
-                                if (fabs(zt) > dbuf2[t]) { rc = ORC_EHINT; goto done; }
+                                const double lim = dbuf2[t] < rwindow ? dbuf2[t] : rwindow;
+                                if (fabs(zt) > lim) { rc = ORC_EHINT; goto done; }
                                 pass = hv;
                             }
                         }

@@ -36,6 +36,8 @@ def lib():
         _lib = C.CDLL(path)
         _lib.orc_round_bf16.restype = C.c_float
         _lib.orc_round_bf16.argtypes = [C.c_float]
+        _lib.orc_splitmix64_first.restype = C.c_uint64
+        _lib.orc_splitmix64_first.argtypes = [C.c_uint64]
     return _lib
 
 
@@ -53,6 +55,11 @@ def _layers(layers: Sequence[Sequence[int]]):
 
 def _f64(a):
     return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def splitmix64_first(key: int) -> int:
+    """First output of a SplitMix64 generator whose state is `key` (the oracle's init RNG)."""
+    return int(lib().orc_splitmix64_first(C.c_uint64(key)))
 
 
 def num_threads() -> int:
@@ -220,9 +227,16 @@ def decision_sizes(in_shape, layers, batch):
 
 PREC = {"f32": 0, "bf16": 1, "exact": 2}
 
+# Default window of a decision hint, relative to the scale of the layer's values: the per-tensor
+# tolerance of the comparisons of stored outputs in each precision mode.
+HINT_REL = {"f32": 1e-4, "bf16": 2e-2, "exact": 1e-4}
+
 
 def train_step(in_shape, layers, R, x, labels, w, v, lr, mu, prec="f32", want_grads=True,
-               want_acts=False, want_decisions=False, pool_hint=None, relu_hint=None):
+               want_acts=False, want_decisions=False, pool_hint=None, relu_hint=None,
+               hint_rel=None):
+    """One step of the oracle (see orc_train_step).  hint_rel is the window of a decision hint
+    relative to the layer's scale; by default HINT_REL[prec]."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     labels = np.ascontiguousarray(labels, dtype=np.int32)
     w = np.ascontiguousarray(w, dtype=np.float32)
@@ -251,10 +265,12 @@ def train_step(in_shape, layers, R, x, labels, w, v, lr, mu, prec="f32", want_gr
     rc = lib().orc_train_step(
         *[C.c_int(t) for t in in_shape], C.c_int(len(layers)), _layers(layers), C.c_int(R),
         C.c_int(Nb), C.c_int(PREC[prec]), _p(x), _p(labels), _p(w), _p(v),
-        C.c_float(lr), C.c_float(mu), _p(ph), _p(rh), C.byref(loss), _p(shard_loss), _p(grads),
+        C.c_float(lr), C.c_float(mu), _p(ph), _p(rh),
+        C.c_double(HINT_REL[prec] if hint_rel is None else hint_rel), C.byref(loss),
+        _p(shard_loss), _p(grads),
         _p(gavg), _p(w_new), _p(v_new), _p(acts), _p(pam), _p(rmask))
     if rc == EHINT:
-        raise HintRejected("a decision hint lies outside the oracle's rounding-error bound")
+        raise HintRejected("a decision hint lies outside the oracle's window for it")
     if rc:
         raise RuntimeError(f"orc_train_step rc={rc}")
     return StepResult(loss.value, shard_loss, grads, gavg, w_new, v_new if v is not None else None,

@@ -9,8 +9,12 @@ per element (the rounding of w' itself), so that an error in lr*v cannot hide un
 Decisions taken in floating point (max-pool window argmax, ReLU sign) can legitimately differ
 between two float evaluations of the same forward pass when two candidates are within rounding
 error of each other.  The GPU's decisions are therefore compared with the oracle's first;
-where they differ, the oracle is run again with the GPU's choice as a hint, and the oracle
-rejects any hint that its own forward error bound does not admit.
+where they differ, the oracle is run again with the GPU's choice as a hint.  The oracle admits a
+hint only if the gap it bridges is within both its rigorous forward error bound and a window of
+`tol` times the scale of that layer's values in the shard (2 tol for a pooling window, whose two
+elements may each be off by tol) -- the same tolerance to which every stored output is compared,
+so the window does not grow with depth.  In addition, at most HINT_CAP of a layer's decisions
+(and at least HINT_FLOOR) may be hinted; the counts are printed for every case.
 """
 from __future__ import annotations
 
@@ -19,6 +23,12 @@ import numpy as np
 from oracle import oracle as orc
 
 TOL = {0: 1e-4, 1: 2e-2}
+PREC_TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+# Largest share of one layer's decisions that may be taken from the GPU as hints, and the
+# number always allowed (a tiny layer with one near-tie).
+HINT_CAP = 0.01
+HINT_FLOOR = 4
 
 
 def rel_err(t, r):
@@ -65,12 +75,48 @@ def gpu_decisions(model, geo):
     return pool, relu
 
 
+def decision_layers(in_shape, layers, batch):
+    """(layer index, 'pool' | 'relu', offset, count) of every decision array segment, in the
+    oracle's concatenated layout for `batch` samples."""
+    out = []
+    po = ro = 0
+    for i, g in enumerate(orc.geometry(in_shape, layers)):
+        n = int(np.prod(g["out_shape"])) * batch
+        if g["kind"] == 2:
+            out.append((i, "pool", po, n))
+            po += n
+        if g["relu"]:
+            out.append((i, "relu", ro, n))
+            ro += n
+    return out
+
+
+def hint_counts(in_shape, layers, batch, ph, rh):
+    """Hinted decisions per layer: list of (layer, kind, hinted, decisions)."""
+    out = []
+    for (i, kind, off, n) in decision_layers(in_shape, layers, batch):
+        h = ph if kind == "pool" else rh
+        out.append((i, kind, int((h[off:off + n] >= 0).sum()), n))
+    return out
+
+
+def check_hint_counts(counts, tag=""):
+    """Print the per-layer hint counts and assert the cap."""
+    parts = [f"L{i}:{k}={c}/{n}" for (i, k, c, n) in counts if c]
+    print(f"[hints] {tag} {sum(c for (_, _, c, _) in counts)} hinted "
+          f"({', '.join(parts) if parts else 'none'})", flush=True)
+    for (i, k, c, n) in counts:
+        cap = max(HINT_FLOOR, int(HINT_CAP * n))
+        assert c <= cap, f"{tag}: layer {i} {k}: {c} of {n} decisions hinted (cap {cap})"
+
+
 def oracle_step_matching(net, layers, R, x, y, w, v, lr, mu, prec, gpu_pool, gpu_relu,
-                         max_rounds=8):
+                         max_rounds=8, tag=""):
     """Oracle step whose decisions match the GPU's wherever the GPU's are valid alternatives.
     A hinted decision can move values downstream by a rounding error and so expose further
     near-ties; hints are therefore accumulated over a few rounds until the decisions agree.
-    Returns (result, number of hinted decisions)."""
+    The window of a hint is the parity tolerance of the precision mode (PREC_TOL).
+    Returns (result, number of hinted decisions); the per-layer counts are printed and capped."""
     res = orc.train_step(net.in_shape, layers, R, x, y, w, v, lr, mu, prec=prec,
                          want_acts=True, want_decisions=True)
     ph = np.full(gpu_pool.shape, -1, np.int32)
@@ -79,11 +125,14 @@ def oracle_step_matching(net, layers, R, x, y, w, v, lr, mu, prec, gpu_pool, gpu
         dp = res.pool_argmax != gpu_pool
         dr = res.relu_mask != gpu_relu
         if not dp.any() and not dr.any():
+            check_hint_counts(hint_counts(net.in_shape, layers, x.shape[0], ph, rh), tag)
             return res, int((ph >= 0).sum() + (rh >= 0).sum())
         ph = np.where(dp, gpu_pool, ph).astype(np.int32)
         rh = np.where(dr, gpu_relu, rh).astype(np.int8)
+        check_hint_counts(hint_counts(net.in_shape, layers, x.shape[0], ph, rh), tag + " (round)")
         res = orc.train_step(net.in_shape, layers, R, x, y, w, v, lr, mu, prec=prec,
-                             want_acts=True, want_decisions=True, pool_hint=ph, relu_hint=rh)
+                             want_acts=True, want_decisions=True, pool_hint=ph, relu_hint=rh,
+                             hint_rel=PREC_TOL[prec])
     raise AssertionError("GPU and oracle decisions still differ after hinting: "
                          f"{int((res.pool_argmax != gpu_pool).sum())} pool, "
                          f"{int((res.relu_mask != gpu_relu).sum())} ReLU")

@@ -231,6 +231,48 @@ def test_bf16_mode_rounds_at_the_stated_points():
     assert abs(rb.loss - rx.loss) < 2e-2 * abs(rx.loss)
 
 
+def _bf16_case(name):
+    nets = {"cifar": (wl.CIFAR, 4, 2), "tiny": (_tiny_net()[0], 6, 3),
+            "residual": (_residual_net(wl.BF16)[0], 8, 2)}
+    net, B, R = nets[name]
+    layers = wl.layer_tuples(net)
+    geo = orc.geometry(net.in_shape, layers)
+    w = orc.init_glorot(net.in_shape, layers, seed=3)
+    g = np.random.default_rng(11)
+    for gg in geo:  # non-zero biases (BN shifts stay 0 at init) so that they are exercised
+        if gg["b_len"] and gg["kind"] != 3:
+            w[gg["b_off"]:gg["b_off"] + gg["b_len"]] = g.normal(0, 0.1, gg["b_len"])
+    x, y = wl.make_batch(net, B, seed=5)
+    res = orc.train_step(net.in_shape, layers, R, x, y, w, None, 0.01, 0.0, prec="bf16")
+    return net, layers, geo, w, x, y, R, res
+
+
+def _worst_layer_rel(res, gref, geo, R):
+    return max(_rel(res.grads[r][gg["w_off"]:gg["b_off"] + gg["b_len"]],
+                    gref[r][gg["w_off"]:gg["b_off"] + gg["b_len"]])
+               for r in range(R) for gg in geo if gg["w_len"])
+
+
+@pytest.mark.parametrize("name", ["cifar", "tiny", "residual"])
+def test_bf16_mode_gradients_match_an_independent_bf16_storage_model(name):
+    """Every rounding point of the bf16 mode, the gradient side included, against torch float64
+    autograd with bfloat16 storage emulated at exactly those points (torch_ref.forward_bf16):
+    x, W, every hidden output, the gradient of the loss with respect to the logits and every
+    stored data gradient (a residual source: the next layer's data gradient stored, then the sum
+    with the residual path's gradient stored again).  Both evaluate in float64, so they agree to
+    the float rounding of the output gradients; a model that omits the loss-gradient rounding or
+    the data-gradient roundings disagrees by 1e-3 or more, so a rounding dropped from (or added
+    to) the oracle cannot pass."""
+    net, layers, geo, w, x, y, R, res = _bf16_case(name)
+    gref, lref = torch_ref.shard_grads_bf16(layers, geo, w, x, y, R)
+    for r in range(R):
+        assert abs(res.shard_loss[r] - lref[r]) <= 1e-6 * abs(lref[r])
+    assert _worst_layer_rel(res, gref, geo, R) < 1e-6
+    for kw in ({"round_grads": False}, {"round_loss_grad": False}):
+        gmiss, _ = torch_ref.shard_grads_bf16(layers, geo, w, x, y, R, **kw)
+        assert _worst_layer_rel(res, gmiss, geo, R) > 1e-4, kw
+
+
 def test_pool_hint_accepts_only_ties_within_the_error_bound():
     # an input with exact ties inside the pooling windows of a conv-free net
     layers = [wl.maxpool(2, 2), wl.fc(3)]

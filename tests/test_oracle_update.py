@@ -73,6 +73,36 @@ def test_glorot_init_range_moments_and_determinism():
         assert np.all(w[g["b_off"]:g["b_off"] + g["b_len"]] == 0)
 
 
+# Published reference outputs of SplitMix64 (Steele, Lea and Flood 2014; the test vectors of
+# Vigna's public-domain splitmix64.c and of Java's SplittableRandom, which share the generator):
+# the first five outputs from state 1234567, and the first output from state 0.
+SPLITMIX64_1234567 = (6457827717110365317, 3203168211198807973, 9817491932198370423,
+                      4593380528125082431, 16408922859458223821)
+SPLITMIX64_0 = 0xE220A8397B1DCDAF
+GOLDEN_GAMMA = 0x9E3779B97F4A7C15
+
+
+def test_splitmix64_matches_published_reference_outputs():
+    """The init's generator against the published outputs.  Output k from state s is the first
+    output from state s + k * gamma (the generator adds gamma before every output)."""
+    M = (1 << 64) - 1
+    for k, ref in enumerate(SPLITMIX64_1234567):
+        assert orc.splitmix64_first((1234567 + k * GOLDEN_GAMMA) & M) == ref, k
+    assert orc.splitmix64_first(0) == SPLITMIX64_0
+
+
+def test_glorot_init_draws_from_the_pinned_generator():
+    """With seed 1234567, element 0 of layer 0 has key = seed, so its weight is
+    a * (2u - 1) with u = (top 24 bits of the published first output) / 2^24."""
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    w = orc.init_glorot(net.in_shape, layers, seed=1234567)
+    fan_in, fan_out = 1 * 5 * 5, 20 * 5 * 5  # LeNet conv1: 1 -> 20 channels, 5x5
+    a = np.sqrt(6.0 / (fan_in + fan_out))
+    u = (SPLITMIX64_1234567[0] >> 40) / 2.0 ** 24
+    assert w[0] == np.float32(a * (2 * u - 1))
+
+
 def test_bf16_rounding_matches_torch_and_ties_to_even():
     cases = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -7, -(1 + 2 ** -8), 3.0e38,
                       1e-40, 0.0, -0.0, np.inf, -np.inf], dtype=np.float32)

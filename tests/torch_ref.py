@@ -61,3 +61,98 @@ def shard_grads(layers, geo, w, x, y, R):
         gs.append(wt.grad.detach().clone())
         ls.append(loss.item())
     return torch.stack(gs).numpy(), ls
+
+
+# ---- bfloat16 storage emulation (the rounding points of the bf16 mode) -------------------------
+
+def bf16(t):
+    """Round to bfloat16 as an fp32 accumulator is stored: first to float, then to nearest even
+    bfloat16 (torch's float -> bfloat16 conversion), returned as float64."""
+    return t.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+def f32(t):
+    return t.to(torch.float32).to(torch.float64)
+
+
+class _RoundValue(torch.autograd.Function):
+    """Round the forward value; the gradient passes unchanged (the stored value is the one the
+    layer above reads, and its gradient is that of the stored value)."""
+
+    @staticmethod
+    def forward(ctx, t, to_bf16):
+        return bf16(t) if to_bf16 else f32(t)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g, None
+
+
+class _RoundGrad(torch.autograd.Function):
+    """Identity forward; the incoming gradient is rounded to bfloat16 (a stored data gradient)."""
+
+    @staticmethod
+    def forward(ctx, t):
+        return t.clone()
+
+    @staticmethod
+    def backward(ctx, g):
+        return bf16(g)
+
+
+def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True):
+    """The network's forward pass with the bf16 mode's storage: x and every W rounded to bf16
+    (biases and batch-normalisation scales stay float); every hidden layer's output rounded to
+    bf16 after bias and ReLU, and the gradient reaching it rounded to bf16 (a stored data
+    gradient; at a residual source the next layer's data gradient is stored, the residual
+    addition's gradient added to it and the sum stored again); the logits rounded
+    to float and the gradient of the loss with respect to them rounded to bf16.  The two flags
+    drop the gradient-side roundings (used to show that a test can see them)."""
+    a = _RoundValue.apply(x, True)
+    acts = []
+    n = len(layers)
+    for li, ((kind, o, k, s, p, gr, relu), g, pr) in enumerate(zip(layers, geo, split_params(geo, wt))):
+        if kind == 1:
+            c = g["in_shape"][0]
+            W = _RoundValue.apply(pr[0].view(o, c // gr, k, k), True)
+            a = F.conv2d(a, W, pr[1], stride=s, padding=p, groups=gr)
+        elif kind == 0:
+            a = a.reshape(a.shape[0], -1)
+            a = F.linear(a, _RoundValue.apply(pr[0].view(o, -1), True), pr[1])
+        elif kind == 3:
+            a = F.batch_norm(a, None, None, pr[0], pr[1], training=True, eps=1e-3)
+        elif kind == 4:
+            a = a + acts[k]
+        else:
+            a = F.max_pool2d(a, k, s)
+        if relu:
+            a = torch.relu(a)
+        last = li == n - 1
+        if kind != 2:  # a pooled value is one of its (already stored) inputs
+            a = _RoundValue.apply(a, not last)
+        if (round_loss_grad if last else round_grads):
+            a = _RoundGrad.apply(a)
+        acts.append(a)  # what a residual addition reads
+        if round_grads and not last:
+            # the next layer's data gradient is stored before a residual addition's gradient is
+            # added to it (a no-op where the next layer is the only reader)
+            a = _RoundGrad.apply(a)
+    return a, acts
+
+
+def shard_grads_bf16(layers, geo, w, x, y, R, **kw):
+    """Per-shard gradients of the shard-mean cross-entropy with the bf16 mode's storage, in
+    float64 arithmetic.  Returns ([R,P], losses)."""
+    w = torch.as_tensor(w, dtype=torch.float64)
+    x = torch.as_tensor(x, dtype=torch.float64)
+    y = torch.as_tensor(y, dtype=torch.long)
+    Nb = x.shape[0] // R
+    gs, ls = [], []
+    for r in range(R):
+        wt = w.clone().requires_grad_(True)
+        z, _ = forward_bf16(layers, geo, wt, x[r * Nb:(r + 1) * Nb], **kw)
+        loss = F.cross_entropy(z, y[r * Nb:(r + 1) * Nb], reduction="mean")
+        loss.backward()
+        gs.append(wt.grad.detach().clone())
+        ls.append(loss.item())
+    return torch.stack(gs).numpy(), ls

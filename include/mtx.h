@@ -265,6 +265,23 @@ typedef struct {
 int mtx_set_timing(mtx_model* m, int enable);
 int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count, int reset);
 
+/* Matrix-core launches of the last enqueued mtx_train_step (introspection for tests and
+ * measurement; not part of the method).  One entry per launch of the tiled MFMA kernel, in
+ * launch order: the launch site (as in mtx_get_timing: "fwd", "dgrad", "wgrad"), the layer, the
+ * output tile (rows x columns of the GEMM C[p][q] = sum_k P[p][k] Q[q][k]), the reduction tile,
+ * the number of reduction splits (> 1: a second kernel adds the fp32 partial sums), and flags:
+ * 1 = interleaved scheduling order, 2 = an operand loaded straight into LDS.  Host only, does
+ * not synchronise; fills up to `capacity` entries and sets *count to the number of launches. */
+typedef struct {
+    char site[32];
+    int layer;
+    int tile_rows, tile_cols, k_tile;
+    int splits;
+    int flags;
+} mtx_launch_info;
+
+int mtx_get_launches(const mtx_model* m, mtx_launch_info* out, int capacity, int* count);
+
 /* Free the host handle (device buffers stay with the caller).  NULL is allowed. */
 void mtx_free_model(mtx_model* m);
 

@@ -3,6 +3,7 @@
 // synchronous data-parallel SGD step on the caller's stream.
 #include "mtx.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -572,6 +573,8 @@ struct mtx_model {
     bool layerwise = false;         // average + update per layer on the third stream
     hipStream_t upd = nullptr;
     std::vector<hipEvent_t> wdone;  // per parameter layer: its weight gradients are done
+    std::vector<hipEvent_t> ddone;  // per parameter layer: the kernels on the caller's stream
+                                    // that read its master weights are done
     hipEvent_t upd_join = nullptr;  // every layer's update is done
     // update rule after the average (mtx_set_optimizer): momentum, or Adam / AdaGrad with their
     // first state in v, Adam's second moment in s2, and the number of steps taken since
@@ -579,6 +582,8 @@ struct mtx_model {
     float b1 = 0.9f, b2 = 0.999f, eps = 0.0f;
     float* s2 = nullptr;
     long long opt_step = 0;
+    // matrix launches of the last enqueued step (mtx_get_launches)
+    std::vector<mtx_launch_info> launches;
 };
 
 namespace {
@@ -630,9 +635,21 @@ hipError_t end_site(mtx_model* m, int idx, hipStream_t s)
 // Run one launch site (a callable returning hipError_t); with timing on, bracket it with an
 // event pair.  A site that launches several kernels marks the boundaries with timing_split, so
 // that every kernel is timed on its own.
+// Site whose launches are being enqueued, for the launch record.
+struct RecordCtx {
+    mtx_model* m = nullptr;
+    const char* name = nullptr;
+    int layer = -1;
+};
+thread_local RecordCtx g_rec;
+
 template <class F>
 hipError_t launch_site(mtx_model* m, const char* name, int layer, hipStream_t s, F&& f)
 {
+    g_rec = RecordCtx{m, name, layer};
+    struct Clear {
+        ~Clear() { g_rec = RecordCtx{}; }
+    } clear;
     if (!m->timer.on) return f();
     g_tctx.m = m;
     g_tctx.base = name;
@@ -652,6 +669,9 @@ void release_update_stream(mtx_model* m)
     for (hipEvent_t& e : m->wdone)
         if (e) (void)hipEventDestroy(e);
     m->wdone.clear();
+    for (hipEvent_t& e : m->ddone)
+        if (e) (void)hipEventDestroy(e);
+    m->ddone.clear();
     if (m->upd_join) (void)hipEventDestroy(m->upd_join);
     m->upd_join = nullptr;
     if (m->upd) (void)hipStreamDestroy(m->upd);
@@ -672,6 +692,21 @@ void destroy_streams(mtx_model* m)
 }  // namespace
 
 namespace mtx {
+void note_gemm(int fp, int fq, int bk, int splits, int flags)
+{
+    const RecordCtx& r = g_rec;
+    if (!r.m) return;
+    mtx_launch_info li{};
+    std::snprintf(li.site, sizeof li.site, "%s", r.name);
+    li.layer = r.layer;
+    li.tile_rows = 32 * fp;
+    li.tile_cols = 32 * fq;
+    li.k_tile = bk;
+    li.splits = splits;
+    li.flags = flags;
+    r.m->launches.push_back(li);
+}
+
 void timing_split(hipStream_t s, const char* part)
 {
     TimingCtx& c = g_tctx;
@@ -795,8 +830,11 @@ int mtx_set_layerwise_update(mtx_model* m, int enable)
             return hip_fail(e, "mtx_set_layerwise_update");
         }
         m->wdone.assign(m->pl.n_wgrad, nullptr);
-        for (size_t i = 0; i < m->wdone.size() && e == hipSuccess; ++i)
+        m->ddone.assign(m->pl.n_wgrad, nullptr);
+        for (size_t i = 0; i < m->wdone.size() && e == hipSuccess; ++i) {
             e = hipEventCreateWithFlags(&m->wdone[i], hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ddone[i], hipEventDisableTiming);
+        }
         if (e == hipSuccess) e = hipEventCreateWithFlags(&m->upd_join, hipEventDisableTiming);
         if (e != hipSuccess) {
             release_update_stream(m);
@@ -878,6 +916,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
 {
     const Plan& pl = m->pl;
     m->timer.cur = 0;
+    m->launches.clear();
     const Dt dt = (Dt)pl.dt;
     const bool bf = pl.dt == MTX_BF16;
     char* ws = m->ws;
@@ -1086,12 +1125,18 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             }
         // Layer-wise averaging (the paper issues one reduction per layer, in layer order): this
         // layer's parameters are averaged and updated on the third stream as soon as its R
-        // shard gradients are written, beside the rest of the backward pass.  Nothing later in
-        // the step reads this layer's master weights: the data gradients read the prepared
-        // copies.
+        // shard gradients are written, beside the rest of the backward pass.  The update waits
+        // for the layer's weight gradients (on sw) and for every kernel enqueued so far on s,
+        // among them the layer's own data gradient, which may read its master weights (the
+        // fused small-image data gradient does); later kernels read only other layers' weights
+        // or the prepared copies.
         if (lp.w_len && layerwise) {
             HIP_TRY(hipEventRecord(m->wdone[nlayer], sw), "layer gradients done");
             HIP_TRY(hipStreamWaitEvent(m->upd, m->wdone[nlayer], 0), "layer gradients done");
+            if (sw != s) {
+                HIP_TRY(hipEventRecord(m->ddone[nlayer], s), "layer data gradient done");
+                HIP_TRY(hipStreamWaitEvent(m->upd, m->ddone[nlayer], 0), "layer data gradient done");
+            }
             ++nlayer;
             const size_t off = lp.w_off, len = lp.w_len + lp.b_len;
             HIP_TRY(launch_site(m, "avg_update", l, m->upd, [&] {
@@ -1185,6 +1230,16 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
         gc.misses = GraphCache::kMaxMisses;  // capture is not possible here: stay eager
     }
     return enqueue_step(m, x, labels, lr, momentum, loss_out, s);
+}
+
+int mtx_get_launches(const mtx_model* m, mtx_launch_info* out, int capacity, int* count)
+{
+    if (!m || !count || capacity < 0 || (capacity > 0 && !out))
+        return fail(MTX_EINVAL, "invalid arguments");
+    const int n = (int)m->launches.size();
+    *count = n;
+    for (int i = 0; i < n && i < capacity; ++i) out[i] = m->launches[i];
+    return MTX_OK;
 }
 
 int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float eps, float* s2)

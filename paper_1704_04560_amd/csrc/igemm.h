@@ -928,14 +928,18 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
         if (n > kMaxTab) return hipErrorInvalidValue;  // the plan keeps chunks within the table
         shm = sizeof(TabEnt) * (size_t)n;
     }
-    if constexpr (PK == L_KD || QK == L_KD)
+    if constexpr (PK == L_KD || QK == L_KD) {
+        note_gemm(FP, FQ, BK, a.splits, kGemmDirectLds);
         hipLaunchKernelGGL((igemm_direct_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s,
                            a);
-    else if constexpr (Interleave<Op>::value && sizeof(typename Op::TT) == 2)
+    } else if constexpr (Interleave<Op>::value && sizeof(typename Op::TT) == 2) {
+        note_gemm(FP, FQ, BK, a.splits, kGemmInterleaved);
         hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK, true>), grid, dim3(256), shm, s,
                            a);
-    else
+    } else {
+        note_gemm(FP, FQ, BK, a.splits, 0);
         hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
     timing_split(s, "reduce");

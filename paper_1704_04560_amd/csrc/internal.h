@@ -136,6 +136,11 @@ hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_
 // this between them; with timing on, the kernels before and after are timed as separate sites
 // (the later one named <site>_<part>).  No effect otherwise.
 void timing_split(hipStream_t s, const char* part);
+// Launch record (api.hip): every matrix launch reports its shape to the model whose step is
+// being enqueued (mtx_get_launches).  flags: kGemmInterleaved, kGemmDirectLds.
+constexpr int kGemmInterleaved = 1;  // the interleaved scheduling order of igemm_kernel
+constexpr int kGemmDirectLds = 2;    // an operand loaded straight into LDS (igemm_direct_kernel)
+void note_gemm(int fp, int fq, int bk, int splits, int flags);
 
 // elementwise.hip
 

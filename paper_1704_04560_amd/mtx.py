@@ -26,7 +26,7 @@ EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_train_step", "mtx_average_g
            "mtx_set_params", "mtx_get_layer_output", "mtx_set_optimizer",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
            "mtx_set_layerwise_update", "mtx_set_timing",
-           "mtx_get_timing", "mtx_free_model", "mtx_last_error")
+           "mtx_get_timing", "mtx_get_launches", "mtx_free_model", "mtx_last_error")
 
 
 class MtxError(RuntimeError):
@@ -52,6 +52,15 @@ class mtx_sizes(C.Structure):
 class mtx_kernel_time(C.Structure):
     _fields_ = [("name", C.c_char * 32), ("layer", C.c_int), ("launches", C.c_int),
                 ("total_ms", C.c_double)]
+
+
+class mtx_launch_info(C.Structure):
+    _fields_ = [("site", C.c_char * 32), ("layer", C.c_int), ("tile_rows", C.c_int),
+                ("tile_cols", C.c_int), ("k_tile", C.c_int), ("splits", C.c_int),
+                ("flags", C.c_int)]
+
+
+MTX_GEMM_INTERLEAVED, MTX_GEMM_DIRECT_LDS = 1, 2
 
 
 class mtx_buffers(C.Structure):
@@ -91,6 +100,7 @@ def lib() -> C.CDLL:
             "mtx_set_overlap": (i32, [vp, i32]),
             "mtx_set_timing": (i32, [vp, i32]),
             "mtx_get_timing": (i32, [vp, C.POINTER(mtx_kernel_time), i32, C.POINTER(i32), i32]),
+            "mtx_get_launches": (i32, [vp, C.POINTER(mtx_launch_info), i32, C.POINTER(i32)]),
             "mtx_free_model": (None, [vp]),
             "mtx_last_error": (C.c_char_p, []),
         }
@@ -226,6 +236,18 @@ def mtx_get_timing(handle, reset: bool = False):
     _check(lib().mtx_get_timing(handle, buf, cap, C.byref(cnt), 1 if reset else 0))
     return [(buf[i].name.decode(), buf[i].layer, buf[i].launches, buf[i].total_ms)
             for i in range(min(cnt.value, cap))]
+
+
+def mtx_get_launches(handle):
+    """[dict(site, layer, tile_rows, tile_cols, k_tile, splits, flags)] per matrix launch of the
+    last enqueued training step."""
+    cap = 1024
+    buf = (mtx_launch_info * cap)()
+    cnt = C.c_int()
+    _check(lib().mtx_get_launches(handle, buf, cap, C.byref(cnt)))
+    return [dict(site=buf[i].site.decode(), layer=buf[i].layer, tile_rows=buf[i].tile_rows,
+                 tile_cols=buf[i].tile_cols, k_tile=buf[i].k_tile, splits=buf[i].splits,
+                 flags=buf[i].flags) for i in range(min(cnt.value, cap))]
 
 
 def mtx_free_model(handle):

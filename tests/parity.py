@@ -24,10 +24,17 @@ from oracle import oracle as orc
 
 TOL = {0: 1e-4, 1: 2e-2}
 PREC_TOL = {"f32": 1e-4, "bf16": 2e-2}
+# The 30-layer residual network with batch normalisation in bf16: an independent fp32
+# evaluation lies up to 2.2e-2 from the oracle at 64 samples per shard (test_oracle_spread.py),
+# so 2e-2 cannot be met by any fp32 evaluation; its tests use this bound instead.
+RESNET_TOL = 3e-2
 
 # Largest share of one layer's decisions that may be taken from the GPU as hints, and the
-# number always allowed (a tiny layer with one near-tie).
-HINT_CAP = 0.01
+# number always allowed (a tiny layer with one near-tie).  Measured: an independent evaluation
+# with fp32 sums and the same bf16 storage (torch CPU float32) differs from the oracle in up to
+# 1.3% of the last pooling layer's decisions of the 30-layer residual network, at most 0.1% in
+# the CIFAR and AlexNet workloads.
+HINT_CAP = 0.02
 HINT_FLOOR = 4
 
 

@@ -42,7 +42,7 @@ def run_case(tag, net, R, Nb, steps, seed, lr, mu, check_acts=True, tol=None):
         torch.cuda.synchronize()
         gp, gr = parity.gpu_decisions(model, geo)
         res, nh = parity.oracle_step_matching(net, layers, R, x, y, w, v if mu else None, lr, mu,
-                                              prec, gp, gr)
+                                              prec, gp, gr, tag=f"{tag} step {step}")
         hinted += nh
         parity.compare_step(model, net, layers, geo, R, res, w, v, mu, tol, float(loss_dev.item()),
                             check_acts=check_acts)
@@ -304,6 +304,78 @@ def test_full_size_logits_match_oracle_on_sampled_samples(name):
     model.close()
 
 
+def _shard_slice(model, geo, r):
+    """The GPU's pooling and ReLU decisions and stored outputs of shard r (oracle layout)."""
+    Nb = model.Nb
+    idx = np.arange(r * Nb, (r + 1) * Nb)
+    gp, gr = _sample_decisions(model, geo, idx)
+    acts = [model.layer_output(i).reshape(model.B, -1)[idx].ravel() for i in range(len(geo))]
+    return gp, gr, acts
+
+
+@pytest.mark.parametrize("name,shard", [("cifar", 0), ("cifar", 7), ("alexnet", 0),
+                                        ("alexnet", 7), ("resnet", 0), ("resnet", 7)])
+def test_full_size_shard_gradients_match_oracle(name, shard):
+    """The bf16 workloads at their full size in the launch configuration the benchmark times
+    (CIFAR B = 512, AlexNet B = 256, the residual network B = 512; R = 8): the whole batch runs on
+    the GPU, and the oracle runs shard 0, or shard R - 1, on its own (R = 1, the shard's samples;
+    the shard's gradient depends on nothing else, batch normalisation included, whose statistics
+    are the shard's).  Every layer's W and b gradient row of that shard, and every stored output
+    of its samples, must match at the bf16 bound, parity.RESNET_TOL for the residual network
+    (Sec. III-E: each replica's gradient is the sequential gradient of its shard).  The test prints the matrix launches it reached: the
+    weight gradients with split reductions and the interleaved schedule, and the data gradients
+    at the tile shapes the benchmark runs."""
+    w = wl.WORKLOADS[name]
+    net = w.net
+    layers = wl.layer_tuples(net)
+    geo = orc.geometry(net.in_shape, layers)
+    tol = parity.RESNET_TOL if name == "resnet" else parity.TOL[net.dtype]
+    _say(f"[case] full-size shard gradients {name} shard {shard}: B={w.batch} R={w.shards}")
+    model = mtx.Model(net.in_shape, layers, net.dtype, w.shards, w.shard_batch, seed=5)
+    wt, _ = model.get_params()
+    assert np.array_equal(wt.view(np.uint32),
+                          orc.init_glorot(net.in_shape, layers, 5).view(np.uint32))
+    x, y = wl.make_batch(net, w.batch, seed=5)
+    model.train_step(torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), w.lr, w.momentum)
+    torch.cuda.synchronize()
+    launches = mtx.mtx_get_launches(model.handle)
+    grads = model.grads_host()[shard].copy()
+    gp, gr, acts = _shard_slice(model, geo, shard)
+    model.close()
+    torch.cuda.empty_cache()
+    seen = sorted({(l["site"], l["tile_rows"], l["tile_cols"], l["splits"], l["flags"])
+                   for l in launches})
+    _say(f"[launches] {name}: " + ", ".join(f"{s}:{r}x{c}/s{sp}/f{f}" for s, r, c, sp, f in seen))
+    Nb = w.shard_batch
+    sl = slice(shard * Nb, (shard + 1) * Nb)
+    res, _ = parity.oracle_step_matching(net, layers, 1, x[sl], y[sl], wt, None, 0.0, 0.0, "bf16",
+                                         gp, gr, tag=f"{name} shard {shard}")
+    for gi, g in enumerate(geo):
+        if not g["w_len"]:
+            continue
+        for nm, off, ln in (("W", g["w_off"], g["w_len"]), ("b", g["b_off"], g["b_len"])):
+            s_ = slice(off, off + ln)
+            if nm == "b" and parity.zero_by_batch_norm(geo, gi):
+                wsl = slice(g["w_off"], g["w_off"] + g["w_len"])
+                parity._assert_noise(grads[s_], res.grads[0, s_],
+                                     float(np.max(np.abs(res.grads[0, wsl]))), tol,
+                                     f"layer {gi} b shard {shard}")
+                continue
+            parity.assert_tensor_close(grads[s_], res.grads[0, s_], tol,
+                                       f"{name} layer {gi} {nm} shard {shard}")
+    off = 0
+    for gi, g in enumerate(geo):
+        n = int(np.prod(g["out_shape"])) * Nb
+        parity.assert_tensor_close(acts[gi], res.acts[off:off + n], tol,
+                                   f"{name} layer {gi} output shard {shard}")
+        off += n
+    # the launches the benchmark times: split weight gradients with the interleaved schedule
+    assert any(l["site"] == "wgrad" and l["splits"] > 1 and l["flags"] & mtx.MTX_GEMM_INTERLEAVED
+               for l in launches), seen
+    assert any(l["site"] == "dgrad" and l["tile_rows"] * l["tile_cols"] >= 64 * 128
+               for l in launches), seen
+
+
 @pytest.mark.parametrize("name", ["cifar", "alexnet"])
 def test_full_size_shard_count_invariance(name):
     """At the full batch, the weight change of one step does not depend on how the batch is
@@ -366,7 +438,8 @@ def test_graph_replay_matches_direct_launches(name):
     b.close()
 
 
-@pytest.mark.parametrize("name,layerwise", [("lenet", False), ("tiny", False), ("tiny", True),
+@pytest.mark.parametrize("name,layerwise", [("lenet", False), ("lenet", True), ("tiny", False),
+                                            ("tiny", True),
                                             ("cifar", True), ("alexnet", False),
                                             ("alexnet", True), ("residual", True),
                                             ("resnet", False)])
@@ -620,13 +693,13 @@ def test_resnet_shapes_fp32_reduced_batch():
 
 
 def test_resnet_workload_reduced_batch():
-    """The residual workload itself (bf16) at B = 4, R = 2.  Its 28 bf16-stored activations and
-    data gradients in sequence let the two evaluation orders (fp32 on the GPU, double in the
-    oracle) round differently once their inputs differ, and the differences grow smoothly with
-    depth (measured: 4e-7 at the first layer to 1.7e-2 at the last residual block, worst weight
-    gradient 2.8e-2; the same shapes in fp32 agree to 1e-6).  The bound is therefore 4e-2, twice
-    the 2e-2 of the eleven-layer workloads."""
-    run_case("resnet", wl.RESNET, 2, 2, 1, seed=33, lr=0.01, mu=0.9, tol=4e-2)
+    """The residual workload itself (bf16) at B = 32, R = 2.  Its 28 bf16-stored activations and
+    data gradients in sequence, with per-shard batch normalisation, let any two fp32 evaluations
+    drift apart with depth: an independent fp32 evaluation on the CPU lies 1.7e-2 from the oracle
+    with 16 samples per shard, about 3e-2 with 4 (test_oracle_spread.py) and up to 2.2e-2 with
+    64.  The bound is parity.RESNET_TOL = 3e-2 (2e-2 is not attainable for this network),
+    and the reduced batch keeps 16 samples per shard."""
+    run_case("resnet", wl.RESNET, 2, 16, 1, seed=33, lr=0.01, mu=0.9, tol=parity.RESNET_TOL)
 
 
 def test_resnet_full_batch_runs_and_shards_are_independent():

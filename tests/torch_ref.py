@@ -60,19 +60,38 @@ def shard_grads(layers, geo, w, x, y, R):
         loss.backward()
         gs.append(wt.grad.detach().clone())
         ls.append(loss.item())
-    return torch.stack(gs).numpy(), ls
+    return torch.stack(gs).to(torch.float64).numpy(), ls
+
+
+def fp32_evaluation_bf16(layers, geo, w, x, y):
+    """One shard in float32 arithmetic (torch CPU: fp32 sums in torch's own order) with the bf16
+    mode's storage points -- an evaluation of the same step that is as legitimate as the GPU's.
+    Returns (gradient [P] as float64, stored outputs per layer, pool decisions, ReLU decisions)
+    in the oracle's layouts."""
+    wt = torch.as_tensor(w, dtype=torch.float32).clone().requires_grad_(True)
+    dec = []
+    z, acts = forward_bf16(layers, geo, wt, torch.as_tensor(x, dtype=torch.float32),
+                           decisions=dec)
+    F.cross_entropy(z, torch.as_tensor(y, dtype=torch.long), reduction="mean").backward()
+    pools = [d for k, d in dec if k == "pool"]
+    relus = [d for k, d in dec if k == "relu"]
+    import numpy as np
+    return (wt.grad.detach().to(torch.float64).numpy(),
+            [a.detach().to(torch.float64).numpy().ravel() for a in acts],
+            np.concatenate(pools).astype(np.int32) if pools else np.zeros(0, np.int32),
+            np.concatenate(relus).astype(np.int8) if relus else np.zeros(0, np.int8))
 
 
 # ---- bfloat16 storage emulation (the rounding points of the bf16 mode) -------------------------
 
 def bf16(t):
     """Round to bfloat16 as an fp32 accumulator is stored: first to float, then to nearest even
-    bfloat16 (torch's float -> bfloat16 conversion), returned as float64."""
-    return t.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    bfloat16 (torch's float -> bfloat16 conversion), returned in t's dtype."""
+    return t.to(torch.float32).to(torch.bfloat16).to(t.dtype)
 
 
 def f32(t):
-    return t.to(torch.float32).to(torch.float64)
+    return t.to(torch.float32).to(t.dtype)
 
 
 class _RoundValue(torch.autograd.Function):
@@ -100,14 +119,17 @@ class _RoundGrad(torch.autograd.Function):
         return bf16(g)
 
 
-def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True):
+def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True, decisions=None):
     """The network's forward pass with the bf16 mode's storage: x and every W rounded to bf16
     (biases and batch-normalisation scales stay float); every hidden layer's output rounded to
     bf16 after bias and ReLU, and the gradient reaching it rounded to bf16 (a stored data
     gradient; at a residual source the next layer's data gradient is stored, the residual
     addition's gradient added to it and the sum stored again); the logits rounded
     to float and the gradient of the loss with respect to them rounded to bf16.  The two flags
-    drop the gradient-side roundings (used to show that a test can see them)."""
+    drop the gradient-side roundings (used to show that a test can see them).  The arithmetic
+    is that of x's dtype: float64, or float32 for an evaluation with fp32 sums.  With a list as
+    `decisions`, the max-pool window positions (u*k + v, int32) and ReLU decisions (int8) are
+    appended to it per layer as ("pool" | "relu", array) in the oracle's layout."""
     a = _RoundValue.apply(x, True)
     acts = []
     n = len(layers)
@@ -124,8 +146,16 @@ def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True):
         elif kind == 4:
             a = a + acts[k]
         else:
-            a = F.max_pool2d(a, k, s)
+            W_ = a.shape[3]
+            a, idx = F.max_pool2d(a, k, s, return_indices=True)
+            if decisions is not None:
+                oh, ow = a.shape[2], a.shape[3]
+                u = idx // W_ - (torch.arange(oh) * s).view(1, 1, oh, 1)
+                v = idx % W_ - (torch.arange(ow) * s).view(1, 1, 1, ow)
+                decisions.append(("pool", (u * k + v).to(torch.int32).numpy().ravel()))
         if relu:
+            if decisions is not None:
+                decisions.append(("relu", (a > 0).to(torch.int8).numpy().ravel()))
             a = torch.relu(a)
         last = li == n - 1
         if kind != 2:  # a pooled value is one of its (already stored) inputs
@@ -140,11 +170,11 @@ def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True):
     return a, acts
 
 
-def shard_grads_bf16(layers, geo, w, x, y, R, **kw):
+def shard_grads_bf16(layers, geo, w, x, y, R, dtype=torch.float64, **kw):
     """Per-shard gradients of the shard-mean cross-entropy with the bf16 mode's storage, in
-    float64 arithmetic.  Returns ([R,P], losses)."""
-    w = torch.as_tensor(w, dtype=torch.float64)
-    x = torch.as_tensor(x, dtype=torch.float64)
+    float64 (or `dtype`) arithmetic.  Returns ([R,P], losses)."""
+    w = torch.as_tensor(w, dtype=dtype)
+    x = torch.as_tensor(x, dtype=dtype)
     y = torch.as_tensor(y, dtype=torch.long)
     Nb = x.shape[0] // R
     gs, ls = [], []
@@ -155,4 +185,23 @@ def shard_grads_bf16(layers, geo, w, x, y, R, **kw):
         loss.backward()
         gs.append(wt.grad.detach().clone())
         ls.append(loss.item())
-    return torch.stack(gs).numpy(), ls
+    return torch.stack(gs).to(torch.float64).numpy(), ls
+
+
+def fp32_evaluation_bf16(layers, geo, w, x, y):
+    """One shard in float32 arithmetic (torch CPU: fp32 sums in torch's own order) with the bf16
+    mode's storage points -- an evaluation of the same step that is as legitimate as the GPU's.
+    Returns (gradient [P] as float64, stored outputs per layer, pool decisions, ReLU decisions)
+    in the oracle's layouts."""
+    wt = torch.as_tensor(w, dtype=torch.float32).clone().requires_grad_(True)
+    dec = []
+    z, acts = forward_bf16(layers, geo, wt, torch.as_tensor(x, dtype=torch.float32),
+                           decisions=dec)
+    F.cross_entropy(z, torch.as_tensor(y, dtype=torch.long), reduction="mean").backward()
+    pools = [d for k, d in dec if k == "pool"]
+    relus = [d for k, d in dec if k == "relu"]
+    import numpy as np
+    return (wt.grad.detach().to(torch.float64).numpy(),
+            [a.detach().to(torch.float64).numpy().ravel() for a in acts],
+            np.concatenate(pools).astype(np.int32) if pools else np.zeros(0, np.int32),
+            np.concatenate(relus).astype(np.int8) if relus else np.zeros(0, np.int8))

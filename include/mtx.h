@@ -124,6 +124,21 @@ int mtx_model_sizes(const mtx_model_desc* desc, int R, int shard_batch, mtx_size
 int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
                    const mtx_buffers* bufs, void* stream, mtx_model** out);
 
+/* The same model creation for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops that must not call hipMalloc, harnesses that forbid it): the
+ * model's workspace is a static array of 64 MiB that the library holds on every device it runs
+ * on until the process ends, instead of a caller buffer.  bufs->workspace must be NULL and
+ * bufs->workspace_bytes 0; w, v, grads and grad_avg come from the caller as for mtx_init_model.
+ * A network whose workspace (mtx_model_sizes) exceeds 64 MiB returns MTX_ENOMEM, one with more
+ * than 16 weight layouts to prepare MTX_EUNSUPPORTED.  Neither this call nor the steps of the
+ * model allocate device memory.  All static models on one device share the one array: every
+ * mtx_train_step of such a model first re-writes what it needs there (its preparation jobs, the
+ * zeroed loss counter and padded input), so their steps may alternate, but steps of two static
+ * models that overlap in time on one device race, and mtx_get_layer_output /
+ * mtx_get_pool_argmax return the outputs of the last static step on the device. */
+int mtx_init_model_static(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                          const mtx_buffers* bufs, void* stream, mtx_model** out);
+
 /* One synchronous data-parallel SGD step on the whole batch (Sec. III-D.2, III-E):
  *   x [B][in_c][in_h][in_w] fp32 images, labels [B] int32 in [0, num_classes); shard r is
  *   rows r*shard_batch .. (r+1)*shard_batch-1.

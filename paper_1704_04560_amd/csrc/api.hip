@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -16,6 +17,11 @@
 #include "internal.h"
 
 using namespace mtx;
+
+// Workspace of the models created by mtx_init_model_static (see there): one array per device,
+// held until the process ends.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -430,6 +436,58 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     return MTX_OK;
 }
 
+// ---- the static workspace of mtx_init_model_static ------------------------------------------
+// A model created by mtx_init_model_static runs its steps in this array instead of a caller
+// workspace.  Host code must never pass the array's name to a kernel or a copy (on the host it
+// is only a stand-in symbol): the device address comes from hipGetSymbolAddress, once per
+// device, and is kept in g_scratch_ptr.
+constexpr int kStaticMaxJobs = 16;  // weight-preparation jobs re-written by every static step
+constexpr int kMaxDevices = 64;
+
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (resolved on first use).
+int static_scratch(char** out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(MTX_EUNSUPPORTED, "device %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = static_cast<char*>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return MTX_OK;
+}
+
+// What a static model re-establishes in the shared array before each step: its weight
+// preparation jobs, the zero loss counter, and (a first convolution over a padded input) the
+// zero padded input whose border the step never writes.
+struct StaticSetup {
+    PrepJob jobs[kStaticMaxJobs];
+    int njobs;
+    PrepJob* dst_jobs;
+    unsigned* sync;
+    uint4* zero;
+    unsigned long long zero_vecs;  // 16-byte vectors to clear at `zero`
+};
+
+__global__ __launch_bounds__(256) void static_setup_kernel(const StaticSetup a)
+{
+    const unsigned long long tid = (unsigned long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const unsigned long long nth = (unsigned long long)gridDim.x * blockDim.x;
+    if (blockIdx.x == 0) {
+        for (int j = threadIdx.x; j < a.njobs; j += blockDim.x) a.dst_jobs[j] = a.jobs[j];
+        if (threadIdx.x == 0) *a.sync = 0u;
+    }
+    for (unsigned long long i = tid; i < a.zero_vecs; i += nth) a.zero[i] = uint4{0u, 0u, 0u, 0u};
+}
+
 // First output of a SplitMix64 generator whose state is `key` (Steele, Lea & Flood 2014;
 // constants of Vigna's splitmix64.c).
 uint64_t splitmix64_first(uint64_t key)
@@ -584,6 +642,9 @@ struct mtx_model {
     long long opt_step = 0;
     // matrix launches of the last enqueued step (mtx_get_launches)
     std::vector<mtx_launch_info> launches;
+    // the workspace is the device's static array (mtx_init_model_static), shared with every
+    // other static model on the device: each step re-establishes what it needs there first
+    bool static_ws = false;
 };
 
 namespace {
@@ -732,8 +793,12 @@ int mtx_model_sizes(const mtx_model_desc* desc, int R, int shard_batch, mtx_size
     return MTX_OK;
 }
 
-int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
-                   const mtx_buffers* bufs, void* stream, mtx_model** out)
+}  // extern "C"
+
+// Shared by mtx_init_model (workspace from the caller) and mtx_init_model_static (static_ws:
+// the device's static array; bufs->workspace unused).
+static int init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                      const mtx_buffers* bufs, void* stream, mtx_model** out, char* static_ws)
 {
     if (!out) return fail(MTX_EINVAL, "out is NULL");
     *out = nullptr;
@@ -741,29 +806,41 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     Plan pl;
     int rc = make_plan(desc, R, shard_batch, pl);
     if (rc) return rc;
-    if (!bufs->w || !bufs->v || !bufs->grads || !bufs->grad_avg || !bufs->workspace)
+    if (!bufs->w || !bufs->v || !bufs->grads || !bufs->grad_avg ||
+        (!static_ws && !bufs->workspace))
         return fail(MTX_EINVAL, "a model buffer is NULL");
     if (!aligned(bufs->w, 16) || !aligned(bufs->v, 16) || !aligned(bufs->grads, 16) ||
-        !aligned(bufs->grad_avg, 16) || !aligned(bufs->workspace, 256))
+        !aligned(bufs->grad_avg, 16) || (!static_ws && !aligned(bufs->workspace, 256)))
         return fail(MTX_EINVAL, "model buffers must be 16-byte (workspace: 256-byte) aligned");
-    if (bufs->workspace_bytes < pl.ws_bytes)
+    if (static_ws) {
+        if (pl.ws_bytes > kStaticScratchBytes)
+            return fail(MTX_ENOMEM, "the network needs %zu bytes of workspace; the static "
+                                    "workspace holds %zu (use mtx_init_model)",
+                        pl.ws_bytes, kStaticScratchBytes);
+        if (pl.jobs.size() > (size_t)kStaticMaxJobs)
+            return fail(MTX_EUNSUPPORTED, "the network has %zu weight layouts to prepare; a "
+                                          "static model takes at most %d (use mtx_init_model)",
+                        pl.jobs.size(), kStaticMaxJobs);
+    } else if (bufs->workspace_bytes < pl.ws_bytes) {
         return fail(MTX_ENOMEM, "workspace too small: %zu bytes given, %zu needed",
                     bufs->workspace_bytes, pl.ws_bytes);
+    }
+    void* wsp = static_ws ? static_cast<void*>(static_ws) : bufs->workspace;
     const size_t pb = pl.P * 4, gb = pl.ld * 4 * pl.R;
     if (overlap(bufs->w, pb, bufs->v, pb) || overlap(bufs->w, pb, bufs->grads, gb) ||
         overlap(bufs->w, pb, bufs->grad_avg, pb) || overlap(bufs->v, pb, bufs->grads, gb) ||
         overlap(bufs->v, pb, bufs->grad_avg, pb) || overlap(bufs->grads, gb, bufs->grad_avg, pb) ||
-        overlap(bufs->workspace, pl.ws_bytes, bufs->w, pb) ||
-        overlap(bufs->workspace, pl.ws_bytes, bufs->v, pb) ||
-        overlap(bufs->workspace, pl.ws_bytes, bufs->grads, gb) ||
-        overlap(bufs->workspace, pl.ws_bytes, bufs->grad_avg, pb))
+        overlap(wsp, pl.ws_bytes, bufs->w, pb) || overlap(wsp, pl.ws_bytes, bufs->v, pb) ||
+        overlap(wsp, pl.ws_bytes, bufs->grads, gb) ||
+        overlap(wsp, pl.ws_bytes, bufs->grad_avg, pb))
         return fail(MTX_EINVAL, "model buffers overlap");
 
     mtx_model* m = new (std::nothrow) mtx_model;
     if (!m) return fail(MTX_ENOMEM, "host allocation failed");
     m->pl = std::move(pl);
     m->w = bufs->w; m->v = bufs->v; m->grads = bufs->grads; m->gavg = bufs->grad_avg;
-    m->ws = static_cast<char*>(bufs->workspace);
+    m->ws = static_cast<char*>(wsp);
+    m->static_ws = static_ws != nullptr;
     m->last_stream = static_cast<hipStream_t>(stream);
     // Measured on MI355X: running the weight gradients beside the data-gradient chain gains a
     // few percent when the step's matrix work is large (CIFAR-, AlexNet-sized steps) and loses
@@ -781,13 +858,16 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     if (e == hipSuccess) e = hipEventCreateWithFlags(&m->join, hipEventDisableTiming);
     if (e == hipSuccess) e = hipMemcpyAsync(m->w, w0.data(), pb, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(m->v, 0, pb, s);
-    if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
-    // the padded input's border and extra channels are never written by a step
-    if (e == hipSuccess && m->pl.L.front().run)
-        e = hipMemsetAsync(m->ws + m->pl.xin_off, 0, m->pl.xin_bytes, s);
-    if (e == hipSuccess && !m->pl.jobs.empty())
-        e = hipMemcpyAsync(m->ws + m->pl.jobs_off, m->pl.jobs.data(),
-                           m->pl.jobs.size() * sizeof(PrepJob), hipMemcpyHostToDevice, s);
+    // a static model sets up its part of the shared array at the start of every step instead
+    if (!m->static_ws) {
+        if (e == hipSuccess) e = hipMemsetAsync(m->ws + m->pl.sync_off, 0, kAlign, s);
+        // the padded input's border and extra channels are never written by a step
+        if (e == hipSuccess && m->pl.L.front().run)
+            e = hipMemsetAsync(m->ws + m->pl.xin_off, 0, m->pl.xin_bytes, s);
+        if (e == hipSuccess && !m->pl.jobs.empty())
+            e = hipMemcpyAsync(m->ws + m->pl.jobs_off, m->pl.jobs.data(),
+                               m->pl.jobs.size() * sizeof(PrepJob), hipMemcpyHostToDevice, s);
+    }
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         destroy_streams(m);
@@ -796,6 +876,27 @@ int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t 
     }
     *out = m;
     return MTX_OK;
+}
+
+extern "C" {
+
+int mtx_init_model(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                   const mtx_buffers* bufs, void* stream, mtx_model** out)
+{
+    return init_model(desc, R, shard_batch, seed, bufs, stream, out, nullptr);
+}
+
+int mtx_init_model_static(const mtx_model_desc* desc, int R, int shard_batch, uint64_t seed,
+                          const mtx_buffers* bufs, void* stream, mtx_model** out)
+{
+    if (out) *out = nullptr;
+    if (bufs && (bufs->workspace || bufs->workspace_bytes))
+        return fail(MTX_EINVAL, "a static model takes no workspace (workspace must be NULL, "
+                                "workspace_bytes 0)");
+    char* ws = nullptr;
+    const int rc = static_scratch(&ws);
+    if (rc) return rc;
+    return init_model(desc, R, shard_batch, seed, bufs, stream, out, ws);
 }
 
 void mtx_free_model(mtx_model* m)
@@ -920,6 +1021,23 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     const Dt dt = (Dt)pl.dt;
     const bool bf = pl.dt == MTX_BF16;
     char* ws = m->ws;
+    if (m->static_ws) {
+        // another static model may have used the array since this model's last step
+        StaticSetup su{};
+        su.njobs = (int)pl.jobs.size();
+        for (int j = 0; j < su.njobs; ++j) su.jobs[j] = pl.jobs[j];
+        su.dst_jobs = reinterpret_cast<PrepJob*>(ws + pl.jobs_off);
+        su.sync = reinterpret_cast<unsigned*>(ws + pl.sync_off);
+        const bool run0 = pl.L.front().run;
+        su.zero = reinterpret_cast<uint4*>(ws + pl.xin_off);
+        su.zero_vecs = run0 ? (pl.xin_bytes + 15) / 16 : 0;
+        const unsigned blocks = (unsigned)std::min<unsigned long long>(
+            1024ull, std::max<unsigned long long>(1ull, (su.zero_vecs + 255) / 256));
+        HIP_TRY(launch_site(m, "static_setup", -1, s, [&] {
+                    hipLaunchKernelGGL(static_setup_kernel, dim3(blocks), dim3(256), 0, s, su);
+                    return hipGetLastError();
+                }), "static workspace setup");
+    }
     const size_t es = bf ? 2 : 4;
     const char* prep = ws + pl.prep_off;
     const void* x_in = pl.x_convert ? static_cast<const void*>(ws + pl.xin_off)

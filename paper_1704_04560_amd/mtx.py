@@ -21,7 +21,7 @@ MTX_F32, MTX_BF16 = 0, 1
 MTX_FC, MTX_CONV, MTX_MAXPOOL, MTX_BN, MTX_ADD = 0, 1, 2, 3, 4
 MTX_OPT_MOMENTUM, MTX_OPT_ADAM, MTX_OPT_ADAGRAD = 0, 1, 2
 
-EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_train_step", "mtx_average_grads",
+EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_init_model_static", "mtx_train_step", "mtx_average_grads",
            "mtx_sgd_update", "mtx_adam_update", "mtx_adagrad_update", "mtx_get_params",
            "mtx_set_params", "mtx_get_layer_output", "mtx_set_optimizer",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
@@ -84,6 +84,8 @@ def lib() -> C.CDLL:
             "mtx_model_sizes": (i32, [C.POINTER(mtx_model_desc), i32, i32, C.POINTER(mtx_sizes)]),
             "mtx_init_model": (i32, [C.POINTER(mtx_model_desc), i32, i32, C.c_uint64,
                                      C.POINTER(mtx_buffers), vp, C.POINTER(vp)]),
+            "mtx_init_model_static": (i32, [C.POINTER(mtx_model_desc), i32, i32, C.c_uint64,
+                                            C.POINTER(mtx_buffers), vp, C.POINTER(vp)]),
             "mtx_train_step": (i32, [vp, vp, vp, f32, f32, vp, vp]),
             "mtx_average_grads": (i32, [vp, i32, sz, sz, vp, vp]),
             "mtx_sgd_update": (i32, [vp, vp, vp, i32, sz, sz, f32, f32, vp, vp]),
@@ -162,6 +164,14 @@ def mtx_init_model(desc, R, shard_batch, seed, w, v, grads, grad_avg, workspace,
     handle = C.c_void_p()
     _check(lib().mtx_init_model(C.byref(desc), R, shard_batch, C.c_uint64(seed), C.byref(bufs),
                                 _stream(stream), C.byref(handle)))
+    return handle
+
+
+def mtx_init_model_static(desc, R, shard_batch, seed, w, v, grads, grad_avg, stream=None):
+    bufs = mtx_buffers(_ptr(w), _ptr(v), _ptr(grads), _ptr(grad_avg), None, 0)
+    handle = C.c_void_p()
+    _check(lib().mtx_init_model_static(C.byref(desc), R, shard_batch, C.c_uint64(seed),
+                                       C.byref(bufs), _stream(stream), C.byref(handle)))
     return handle
 
 
@@ -259,7 +269,8 @@ def mtx_free_model(handle):
 class Model:
     """A network bound to caller-owned device buffers (allocated here with torch)."""
 
-    def __init__(self, in_shape, layers, compute, R, shard_batch, seed=0, stream=None):
+    def __init__(self, in_shape, layers, compute, R, shard_batch, seed=0, stream=None,
+                 static_workspace=False):
         import torch
         self.in_shape = tuple(in_shape)
         self.layers = [tuple(int(v) for v in t) for t in layers]
@@ -273,9 +284,14 @@ class Model:
         self.v = torch.empty(self.P, dtype=torch.float32, device=dev)
         self.grads = torch.empty(R * self.ld, dtype=torch.float32, device=dev)
         self.grad_avg = torch.empty(self.P, dtype=torch.float32, device=dev)
-        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=dev)
-        self.handle = mtx_init_model(self.desc, R, shard_batch, seed, self.w, self.v, self.grads,
-                                     self.grad_avg, self.workspace, stream)
+        if static_workspace:  # the library's static array (mtx_init_model_static)
+            self.workspace = None
+            self.handle = mtx_init_model_static(self.desc, R, shard_batch, seed, self.w, self.v,
+                                                self.grads, self.grad_avg, stream)
+        else:
+            self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=dev)
+            self.handle = mtx_init_model(self.desc, R, shard_batch, seed, self.w, self.v,
+                                         self.grads, self.grad_avg, self.workspace, stream)
         self._shapes = self._out_shapes()
 
     def _out_shapes(self):

@@ -150,3 +150,15 @@ def test_model_call_errors_need_no_device():
                                   C.byref(h))
     assert rc == mtx.MTX_ENOMEM
     assert b"workspace too small" in mtx.lib().mtx_last_error()
+
+
+def test_static_model_takes_no_workspace():
+    """mtx_init_model_static refuses a caller workspace before touching a device."""
+    L = wl.layer_tuples(wl.LENET)
+    d = mtx.make_desc((1, 28, 28), L, wl.F32)
+    bufs = mtx.mtx_buffers(16, 16, 16, 16, 256, 1024)
+    h = C.c_void_p()
+    rc = mtx.lib().mtx_init_model_static(C.byref(d), 1, 1, C.c_uint64(0), C.byref(bufs), None,
+                                         C.byref(h))
+    assert rc == mtx.MTX_EINVAL and not h.value
+    assert b"no workspace" in mtx.lib().mtx_last_error()

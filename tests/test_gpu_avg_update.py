@@ -79,6 +79,33 @@ def test_microbench_size_sampled():
     parity.assert_update_close(wd[it].cpu().numpy(), ref_w, w[idx], 1e-4)
 
 
+def test_microbench_250m_sampled_on_device_inputs():
+    """R = 16 buffers of 250,000,000 elements (the larger microbenchmark size; row offsets reach
+    15 x 10^9 bytes, beyond 32-bit byte offsets): inputs drawn on the device with a seeded torch
+    generator, the whole update on the GPU, then the sampled elements (every row at 20,000
+    indices plus the tail) copied to the host and checked against the oracle run on them."""
+    R, n = 16, 250_000_000
+    print(f"[case] sgd_update full size R={R} n={n}", flush=True)
+    gen = torch.Generator(device="cuda").manual_seed(250)
+    gd = torch.randn(R * n, device="cuda", generator=gen) * 1e-3
+    wd = torch.randn(n, device="cuda", generator=gen) * 0.05
+    vd = torch.randn(n, device="cuda", generator=gen) * 1e-3
+    idx = np.unique(np.concatenate([np.random.default_rng(1).choice(n, 20000, replace=False),
+                                    np.arange(n - 7, n)]))
+    it = torch.from_numpy(idx).cuda()
+    g_s = gd.view(R, n)[:, it].cpu().numpy()
+    w_s, v_s = wd[it].cpu().numpy(), vd[it].cpu().numpy()
+    ref_avg, ref_w, ref_v = orc.average_update(g_s, w_s, v_s, 0.01, 0.9)
+    avg = torch.empty(n, device="cuda")
+    mtx.mtx_sgd_update(wd, vd, gd, R, n, n, 0.01, 0.9, avg)
+    torch.cuda.synchronize()
+    parity.assert_tensor_close(avg[it].cpu().numpy(), ref_avg, 1e-6, "average")
+    parity.assert_tensor_close(vd[it].cpu().numpy(), ref_v, 1e-6, "velocity")
+    parity.assert_update_close(wd[it].cpu().numpy(), ref_w, w_s, 1e-4)
+    del gd, wd, vd, avg
+    torch.cuda.empty_cache()
+
+
 # ---- the average followed by Adam or AdaGrad ----------------------------------------------------
 
 ADAM = dict(lr=1e-3, b1=0.9, b2=0.999, eps=1e-8)

@@ -637,6 +637,13 @@ template <typename T> struct FcWgrad {
         return B.at16(s.ok & (k < c.kend), (c.b0 + k) * a.Qdim + s.off);
     }
     // grads[r][w_off + o * IN + i], or the bias
+    static constexpr bool ROW_STORE = true;  // row o is contiguous along i (staged row store)
+    __device__ static int row_len(const GemmArgs& a) { return a.C; }
+    __device__ static float* row_out(const GemmArgs& a, const Ctx& c, int q)
+    {
+        return static_cast<float*>(a.out) + (long long)c.r * a.out_ld + a.out_off +
+               (long long)q * a.C;
+    }
     __device__ static void store4(const GemmArgs& a, const Ctx& c, int p, int q, f32x4 acc, int np)
     {
         float* g = static_cast<float*>(a.out) + (long long)c.r * a.out_ld;

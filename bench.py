@@ -15,7 +15,8 @@ kernel that takes the most time in the step, timed in place with HIP events on t
 stream (its `traffic` comes from a committed rocprofv3 counter summary of the same kernel
 sources, else null); `grad_avg_update` is the fused average + momentum kernel at the
 61M- and 250M-element, 16-buffer sizes; `other_workloads` are short runs of the other
-workloads (MLP, LeNet, CIFAR, the residual network with batch normalisation); `shard_sweep` is
+workloads (MLP, LeNet, CIFAR, the residual network with batch normalisation, the bottleneck
+residual network with projection shortcuts); `shard_sweep` is
 samples/s of the LeNet workload at the same global batch for shard counts R = 1 .. 16;
 `cpu_baseline` is the CPU oracle timed on a bounded sample of the headline workload.
 """
@@ -45,7 +46,7 @@ def geometry(net):
             oc, oh, ow = l.out, (h + 2 * l.pad - l.k) // l.stride + 1, (w + 2 * l.pad - l.k) // l.stride + 1
         elif l.kind == wl.FC:
             oc, oh, ow = l.out, 1, 1
-        elif l.kind in (wl.BN, wl.ADD):
+        elif l.kind in (wl.BN, wl.ADD, wl.ADDP):
             oc, oh, ow = c, h, w
         else:
             oc, oh, ow = c, (h - l.k) // l.stride + 1, (w - l.k) // l.stride + 1
@@ -66,6 +67,8 @@ def site_work(name, layer, geo, wkl, es):
         l = g["layer"]
         if l.kind == wl.CONV:
             macs = B * g["oh"] * g["ow"] * g["oc"] * (g["c"] // l.groups) * l.k * l.k
+        elif l.kind == wl.ADDP:  # the projection: a 1x1 convolution of the source's output
+            macs = B * g["oh"] * g["ow"] * g["oc"] * geo[l.k]["oc"]
         else:
             macs = B * g["c"] * g["h"] * g["w"] * g["oc"]
         in_sz = B * g["c"] * g["h"] * g["w"]
@@ -92,6 +95,8 @@ def site_work(name, layer, geo, wkl, es):
         if name == "bn_bwd_apply":  # x, dy and the mask read, dx written
             return "hbm", 4 * in_sz * es
         if name in ("add_fwd", "skip_add"):  # two read, one written
+            return "hbm", 3 * out_sz * es
+        if name == "add_bwd" and l.kind == wl.ADDP:  # dy and the mask read, dx written
             return "hbm", 3 * out_sz * es
         if name == "add_bwd":  # dy and two masks read, dx and the kept gradient written
             return "hbm", 5 * out_sz * es
@@ -454,7 +459,7 @@ def main():
         out["grad_avg_update"] = microbench_avg_update(torch, mtx)
     if not args.no_extra:
         extra = {}
-        for name in ("mlp", "lenet", "cifar", "alexnet", "resnet"):
+        for name in ("mlp", "lenet", "cifar", "alexnet", "resnet", "bottleneck"):
             if name == args.workload:
                 continue
             e = measure(torch, mtx, wl, name, 50 if name in ("mlp", "lenet") else 20, 3)

@@ -52,7 +52,14 @@ typedef enum {
 
 typedef enum { MTX_F32 = 0, MTX_BF16 = 1 } mtx_dtype;
 
-typedef enum { MTX_FC = 0, MTX_CONV = 1, MTX_MAXPOOL = 2, MTX_BN = 3, MTX_ADD = 4 } mtx_kind;
+typedef enum {
+    MTX_FC = 0,
+    MTX_CONV = 1,
+    MTX_MAXPOOL = 2,
+    MTX_BN = 3,
+    MTX_ADD = 4,
+    MTX_ADDP = 5
+} mtx_kind;
 
 /* One layer (Sec. I and Fig. 1: fully connected and convolution layers; pooling between
  * convolutions; Table II's ResNet-50 adds batch normalisation and residual additions).
@@ -70,6 +77,13 @@ typedef enum { MTX_FC = 0, MTX_CONV = 1, MTX_MAXPOOL = 2, MTX_BN = 3, MTX_ADD = 
  *   MTX_ADD:     residual addition y = x + (output of layer k), k an earlier layer other than
  *                the previous one, with the same output shape; a layer is added at most once;
  *                relu as above; no parameters.
+ *   MTX_ADDP:    residual addition through a projection shortcut (the downsampling blocks of
+ *                ResNet-50, Table II): y = x + P, P = W * a_k + b, a 1x1 convolution of the
+ *                given stride (pad 0, groups 1) of the output a_k of an earlier layer k other
+ *                than the previous one, mapping it to this layer's shape; out = the channel
+ *                count of x; parameters W[out][channels of a_k] and b[out], Glorot-initialised
+ *                as a convolution's.  P is a stored output (bf16 in MTX_BF16 mode) before the
+ *                addition; a layer is the source of at most one addition; relu as above.
  * The last layer must be MTX_FC without ReLU; its outputs are the class scores of a softmax
  * cross-entropy loss. */
 typedef struct {

@@ -32,7 +32,10 @@
  *     Because the statistics are per shard, the average of the replica gradients of a network
  *     with batch normalisation is not the full-batch gradient.  The residual addition sums the
  *     previous layer's output and the output of an earlier layer of the same shape (He et al.);
- *     its gradient reaches both.
+ *     its gradient reaches both.  Where the block changes the shape (ResNet-50's downsampling
+ *     blocks), the shortcut is a projection: a 1x1 convolution of the given stride, with weights
+ *     and bias, of the earlier layer's output (He et al., the projection shortcut); its output is
+ *     a stored output like any convolution's, then added.
  *
  * The paper gives no formula for any of these; the code below is the textbook definition of
  * each, written as direct loops in double precision.  Readings taken where the paper is silent:
@@ -67,6 +70,9 @@
 #define ORC_MAXPOOL 2
 #define ORC_BN 3  /* batch normalisation: params gamma[c] (as W) and beta[c] (as b) */
 #define ORC_ADD 4 /* residual addition: k = index of the earlier layer whose output is added */
+#define ORC_ADDP 5 /* residual addition through a projection: k = the earlier layer, whose output
+                    * passes a 1x1 convolution of the given stride (weights W[out][c], bias b)
+                    * before it is added */
 
 #define ORC_BN_EPS 1e-3
 
@@ -173,15 +179,29 @@ int orc_plan(int in_c, int in_h, int in_w, int n_layers, const orc_layer* L, orc
             g->oc = c; g->oh = h; g->ow = w;
             g->w_len = c;
             g->b_len = c;
-        } else if (L[i].kind == ORC_ADD) {
-            /* the source is an earlier layer (not the previous one) of this layer's input shape,
-             * and no layer is the source of two additions */
+        } else if (L[i].kind == ORC_ADD || L[i].kind == ORC_ADDP) {
+            /* the source is an earlier layer (not the previous one), of this layer's input shape
+             * (plain addition) or of a shape that a 1x1 convolution of the given stride maps to
+             * it (projection, out = this layer's channel count); no layer is the source of two
+             * additions */
             int src = L[i].k;
             if (src < 0 || src > i - 2) return ORC_EINVAL;
-            if (G[src].oc != c || G[src].oh != h || G[src].ow != w) return ORC_EINVAL;
             for (int j = src + 1; j < i; j++)
-                if (G[j].kind == ORC_ADD && G[j].k == src) return ORC_EINVAL;
-            g->k = src; g->s = 1; g->p = 0; g->g = 1;
+                if ((G[j].kind == ORC_ADD || G[j].kind == ORC_ADDP) && G[j].k == src)
+                    return ORC_EINVAL;
+            if (L[i].kind == ORC_ADD) {
+                if (G[src].oc != c || G[src].oh != h || G[src].ow != w) return ORC_EINVAL;
+                g->s = 1;
+            } else {
+                const int s = L[i].stride;
+                if (s < 1 || L[i].out != c || L[i].pad != 0 || (L[i].groups != 0 && L[i].groups != 1))
+                    return ORC_EINVAL;
+                if ((G[src].oh - 1) / s + 1 != h || (G[src].ow - 1) / s + 1 != w) return ORC_EINVAL;
+                g->s = s;
+                g->w_len = (long)c * G[src].oc; /* W[out][c_src] */
+                g->b_len = c;
+            }
+            g->k = src; g->p = 0; g->g = 1;
             g->oc = c; g->oh = h; g->ow = w;
         } else {
             return ORC_EINVAL;
@@ -532,6 +552,9 @@ int orc_init_glorot(int in_c, int in_h, int in_w, int n_layers, const orc_layer*
         if (g->kind == ORC_CONV) {
             fan_in = (double)(g->c / g->g) * g->k * g->k;
             fan_out = (double)g->oc * g->k * g->k;
+        } else if (g->kind == ORC_ADDP) { /* a 1x1 convolution of the source's channels */
+            fan_in = (double)G[g->k].oc;
+            fan_out = (double)g->oc;
         } else {
             fan_in = (double)g->c * g->h * g->w;
             fan_out = (double)g->oc;
@@ -628,12 +651,13 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
     double** bnm = (double**)calloc((size_t)n_layers, sizeof(double*));    /* BN mean */
     double** bni = (double**)calloc((size_t)n_layers, sizeof(double*));    /* BN 1/std */
     double** skipg = (double**)calloc((size_t)n_layers, sizeof(double*));  /* residual grads */
+    double** proj = (double**)calloc((size_t)n_layers, sizeof(double*));   /* projection outputs */
     double* lossn = (double*)malloc(sizeof(double) * (size_t)Nb);
     double* dbuf = NULL;
     double* dbuf2 = NULL;
     double* gw = (double*)malloc(sizeof(double) * (size_t)P);
     if (!act_off || !pool_off || !relu_off || !wq || (track && !wabs) || !gsum || !a || !e || !z ||
-        !am || !bnm || !bni || !skipg || !lossn || !gw) {
+        !am || !bnm || !bni || !skipg || !proj || !lossn || !gw) {
         rc = ORC_ENOMEM;
         goto done;
     }
@@ -657,10 +681,14 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                 bnm[l] = (double*)malloc(sizeof(double) * (size_t)G[l].c);
                 bni[l] = (double*)malloc(sizeof(double) * (size_t)G[l].c);
             }
-            if (G[l].kind == ORC_ADD) {
+            if (G[l].kind == ORC_ADD || G[l].kind == ORC_ADDP) {
                 const int src = G[l].k;
                 skipg[src] = (double*)malloc(sizeof(double) * (size_t)(act_size(&G[src]) * Nb));
                 if (!skipg[src]) { rc = ORC_ENOMEM; goto done; }
+            }
+            if (G[l].kind == ORC_ADDP) {
+                proj[l] = (double*)malloc(sizeof(double) * (size_t)sz);
+                if (!proj[l]) { rc = ORC_ENOMEM; goto done; }
             }
             if (!a[l + 1] || !z[l] || (track && !e[l + 1]) ||
                 (G[l].kind == ORC_MAXPOOL && !am[l]) ||
@@ -772,6 +800,36 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                                     dbuf2[o] = ez;
                                 }
                         }
+                } else if (g->kind == ORC_ADDP) {
+                    /* the projection: a 1x1 convolution of stride s of the source's output, its
+                     * result stored like a convolution's output, then added */
+                    const orc_geom* gs = &G[g->k];
+                    const orc_geom pg = {ORC_CONV, 0, gs->oc, gs->oh, gs->ow, g->oc, g->oh, g->ow,
+                                         1, g->s, 0, 1, 0, 0, 0, 0};
+                    const double* sa = a[g->k + 1];
+                    layer_fwd(&pg, Nb, sa, wq + g->w_off, wq + g->b_off, proj[l]);
+                    if (track) {
+                        /* bound of the stored projection (as for a convolution), then of the sum */
+                        const double gam = gamma_f32(2 * ((long)gs->oc + 1));
+                        double* absa = dbuf;
+                        const long ssz = act_size(gs) * Nb;
+                        for (long t = 0; t < ssz; t++) absa[t] = fabs(sa[t]);
+                        layer_fwd(&pg, Nb, absa, wabs + g->w_off, wabs + g->b_off, dbuf2);
+                        double* ep = z[l]; /* scratch: z[l] is written below */
+                        layer_fwd(&pg, Nb, e[g->k + 1], wabs + g->w_off, NULL, ep);
+                        for (long t = 0; t < sz; t++) {
+                            const double ev = gam * dbuf2[t] + ep[t];
+                            dbuf2[t] = ev + us * (fabs(proj[l][t]) + ev); /* stored projection */
+                        }
+                    }
+                    for (long t = 0; t < sz; t++) proj[l][t] = store(proj[l][t]);
+                    for (long t = 0; t < sz; t++) z[l][t] = a[l][t] + proj[l][t];
+                    if (track)
+                        for (long t = 0; t < sz; t++) {
+                            const double ez = e[l][t] + dbuf2[t] + ldexp(1.0, -24) * fabs(z[l][t]);
+                            e[l + 1][t] = ez + 2.0 * us * (fabs(z[l][t]) + ez);
+                            dbuf2[t] = ez;
+                        }
                 } else if (g->kind == ORC_ADD) {
                     const double* sa = a[g->k + 1];
                     for (long t = 0; t < sz; t++) z[l][t] = a[l][t] + sa[t];
@@ -870,6 +928,19 @@ int orc_train_step(int in_c, int in_h, int in_w, int n_layers, const orc_layer* 
                 /* the gradient reaches the previous layer and the source layer unchanged */
                 for (long t = 0; t < sz; t++) skipg[g->k][t] = dcur[t];
                 for (long t = 0; t < insz; t++) dnext[t] = dcur[t];
+            } else if (g->kind == ORC_ADDP) {
+                /* unchanged to the previous layer; through the projection to the source (its
+                 * data gradient stored), and the projection's weight and bias gradients */
+                const orc_geom* gs = &G[g->k];
+                for (long t = 0; t < insz; t++) dnext[t] = dcur[t];
+                orc_conv_bwd(Nb, gs->oc, gs->oh, gs->ow, g->oc, 1, g->s, 0, 1, a[g->k + 1],
+                             wq + g->w_off, dcur, skipg[g->k], gw + g->w_off, gw + g->b_off);
+                for (long t = 0; t < act_size(gs) * Nb; t++) skipg[g->k][t] = store(skipg[g->k][t]);
+                for (long i = 0; i < g->w_len + g->b_len; i++) {
+                    float gf = (float)gw[g->w_off + i];
+                    if (grads) grads[(long)r * P + g->w_off + i] = gf;
+                    gsum[g->w_off + i] += (double)gf;
+                }
             } else if (g->kind == ORC_BN) {
                 double* dx = (l > 0) ? dnext : NULL;
                 orc_bn_bwd(Nb, g->c, g->h * g->w, a[l], wq + g->w_off, bnm[l], bni[l], dcur, dx,
@@ -926,7 +997,8 @@ done:
     if (bnm) for (int l = 0; l < n_layers; l++) free(bnm[l]);
     if (bni) for (int l = 0; l < n_layers; l++) free(bni[l]);
     if (skipg) for (int l = 0; l < n_layers; l++) free(skipg[l]);
-    free(a); free(e); free(z); free(am); free(bnm); free(bni); free(skipg);
+    if (proj) for (int l = 0; l < n_layers; l++) free(proj[l]);
+    free(a); free(e); free(z); free(am); free(bnm); free(bni); free(skipg); free(proj);
     free(act_off); free(pool_off); free(relu_off);
     free(wq); free(wabs); free(gsum); free(lossn); free(dbuf); free(dbuf2); free(gw); free(G);
     return rc;

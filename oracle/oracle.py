@@ -3,7 +3,8 @@
 The oracle is plain C in ``mtx_oracle.c``; this module only marshals numpy arrays.  It takes the
 network as (C, H, W) plus a list of layer tuples (kind, out, k, stride, pad, groups, relu) with
 kind 0 = fully connected, 1 = convolution, 2 = max-pool, 3 = batch normalisation, 4 = residual
-addition of the output of layer k, so it needs nothing from the GPU library.
+addition of the output of layer k, 5 = residual addition of layer k's output through a 1x1
+projection of the given stride, so it needs nothing from the GPU library.
 """
 from __future__ import annotations
 
@@ -100,6 +101,9 @@ def geometry(in_shape, layers):
         elif kind == 4:  # residual addition of layer k's output
             oc, oh, ow = c, h, w
             wl, bl = 0, 0
+        elif kind == 5:  # addition through a 1x1 projection of layer k's output
+            oc, oh, ow = c, h, w
+            wl, bl = o * out[k]["out_shape"][0], o
         else:
             oc, oh, ow = c, (h - k) // s + 1, (w - k) // s + 1
             wl, bl = 0, 0

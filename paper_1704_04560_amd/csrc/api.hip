@@ -77,6 +77,7 @@ struct LayerPlan {
     bool direct;                 // first convolution through the direct kernels (firstconv.hip)
     size_t stat_off;             // batch normalisation: per-shard (mean, 1/std) [R][C] floats
     size_t skip_off;             // residual addition: gradient for the source layer [B][...]
+    size_t proj_off;             // projection shortcut: its stored output [B][oh][ow][oc]
 };
 
 constexpr size_t kNone = ~(size_t)0;
@@ -104,6 +105,12 @@ struct Plan {
     double gemm_flops = 0;       // multiply-adds x 2 of every matrix launch of a step
     size_t ws_bytes = 0;
 };
+
+// The 1x1 convolution of a projection shortcut (layer lp, source sp) over N images.
+ConvGeom proj_geom(const LayerPlan& lp, const LayerPlan& sp, int N)
+{
+    return ConvGeom{N, sp.oc, sp.oh, sp.ow, lp.oc, lp.oh, lp.ow, 1, lp.s, 0, 1};
+}
 
 int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
 {
@@ -177,24 +184,38 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
             lp.oc = c; lp.oh = h; lp.ow = w;
             lp.w_len = c; lp.b_len = c;  // gamma, beta
-        } else if (ly.kind == MTX_ADD) {
+        } else if (ly.kind == MTX_ADD || ly.kind == MTX_ADDP) {
             const int src = ly.k;
             if (src < 0 || src > i - 2)
                 return fail(MTX_EINVAL, "layer %d: the added layer must be an earlier layer "
                                         "other than the previous one", i);
             const LayerPlan& sp = pl.L[src];
-            if (sp.oc != c || sp.oh != h || sp.ow != w)
-                return fail(MTX_EINVAL, "layer %d: layer %d's output has another shape", i, src);
             for (int j = src + 1; j < i; ++j)
-                if (pl.L[j].kind == MTX_ADD && pl.L[j].src == src)
+                if ((pl.L[j].kind == MTX_ADD || pl.L[j].kind == MTX_ADDP) && pl.L[j].src == src)
                     return fail(MTX_EINVAL, "layer %d: layer %d is already added once", i, src);
-            if (ly.out != 0 || ly.pad != 0 || (ly.stride != 0 && ly.stride != 1) ||
-                (ly.groups != 0 && ly.groups != 1))
-                return fail(MTX_EINVAL, "layer %d: a residual addition takes only k and relu", i);
+            if (ly.kind == MTX_ADD) {
+                if (sp.oc != c || sp.oh != h || sp.ow != w)
+                    return fail(MTX_EINVAL, "layer %d: layer %d's output has another shape", i, src);
+                if (ly.out != 0 || ly.pad != 0 || (ly.stride != 0 && ly.stride != 1) ||
+                    (ly.groups != 0 && ly.groups != 1))
+                    return fail(MTX_EINVAL, "layer %d: a residual addition takes only k and relu", i);
+                lp.s = 1;
+                lp.w_len = 0; lp.b_len = 0;
+            } else {
+                const int st = ly.stride;
+                if (st < 1 || ly.out != c || ly.pad != 0 || (ly.groups != 0 && ly.groups != 1))
+                    return fail(MTX_EINVAL, "layer %d: a projection shortcut takes k, out (the "
+                                            "previous layer's channel count), stride >= 1 and relu", i);
+                if ((sp.oh - 1) / st + 1 != h || (sp.ow - 1) / st + 1 != w)
+                    return fail(MTX_EINVAL, "layer %d: a 1x1 convolution of stride %d does not map "
+                                            "layer %d's output to this layer's shape", i, st, src);
+                lp.s = st;
+                lp.w_len = (size_t)c * sp.oc;  // W[out][c of the source], 1x1
+                lp.b_len = c;
+            }
             lp.src = src;
-            lp.k = 1; lp.s = 1; lp.p = 0; lp.g = 1;
+            lp.k = 1; lp.p = 0; lp.g = 1;
             lp.oc = c; lp.oh = h; lp.ow = w;
-            lp.w_len = 0; lp.b_len = 0;
         } else {
             return fail(MTX_EINVAL, "layer %d: unknown kind %d", i, ly.kind);
         }
@@ -220,6 +241,7 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         lp.need_dx = (int)i > pl.first_param && pl.first_param >= 0;
         // a pooled tensor that feeds a fully connected layer is stored NCHW
         lp.nhwc = lp.kind == MTX_CONV || lp.kind == MTX_BN || lp.kind == MTX_ADD ||
+                  lp.kind == MTX_ADDP ||
                   (lp.kind == MTX_MAXPOOL && !(i + 1 < pl.L.size() && pl.L[i + 1].kind == MTX_FC));
         lp.perm_c = 1;
         lp.perm_hw = 1;
@@ -270,7 +292,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
     if (first.direct && pl.L.size() > 2) {
         const LayerPlan& p1 = pl.L[1];
         bool kept_for_0 = false;  // a residual addition whose source is layer 0
-        for (const LayerPlan& q : pl.L) kept_for_0 = kept_for_0 || (q.kind == MTX_ADD && q.src == 0);
+        for (const LayerPlan& q : pl.L)
+            kept_for_0 = kept_for_0 || ((q.kind == MTX_ADD || q.kind == MTX_ADDP) && q.src == 0);
         const ConvGeom g0{pl.B, first.c, first.h, first.w, first.oc, first.oh, first.ow, first.k,
                           first.s, first.p, first.g};
         pl.pool_into_first = p1.kind == MTX_MAXPOOL && p1.k == p1.s && p1.nhwc && !kept_for_0 &&
@@ -304,6 +327,16 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             lp.fw_off = add_job(j);
         } else if (lp.kind == MTX_CONV && lp.direct) {
             continue;  // the direct kernels read the fp32 weights (and round them as they load)
+        } else if (lp.kind == MTX_ADDP) {
+            // the projection's 1x1 convolution: forward layout, and the data-gradient layout
+            // when the source's gradient is needed (its data gradient is an implicit GEMM)
+            j.g = 1; j.cg = pl.L[lp.src].oc; j.og = lp.oc; j.KK = 1;
+            j.kind = PREP_CONV_F;
+            lp.fw_off = add_job(j);
+            if (lp.src >= pl.first_param) {
+                j.kind = PREP_CONV_D;
+                lp.bw_off = add_job(j);
+            }
         } else if (lp.kind == MTX_CONV) {
             j.g = lp.g; j.cg = lp.c / lp.g; j.og = lp.oc / lp.g; j.KK = lp.k * lp.k;
             j.kind = PREP_CONV_F;
@@ -358,9 +391,15 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
         // a residual addition keeps the gradient for its source until the source's own output
         // gradient exists (only when the source's gradient is needed at all)
         lp.skip_off = kNone;
-        if (lp.kind == MTX_ADD && lp.src >= pl.first_param && pl.first_param >= 0) {
+        if ((lp.kind == MTX_ADD || lp.kind == MTX_ADDP) && lp.src >= pl.first_param &&
+            pl.first_param >= 0) {
             lp.skip_off = ws;
-            ws = align_up(ws + lp.out_elems * pl.B * es, kAlign);
+            ws = align_up(ws + pl.L[lp.src].out_elems * pl.B * es, kAlign);
+        }
+        lp.proj_off = kNone;
+        if (lp.kind == MTX_ADDP) {
+            lp.proj_off = ws;
+            ws = align_up(ws + lp.out_elems * pl.B * (lp.act_f32 ? 4 : es), kAlign);
         }
         // fp32 partial sums of the matrix launches whose reduction is split (the last entry of
         // dims is the weight gradient)
@@ -390,15 +429,25 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             dims[nd++] = fc_fwd_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
             if (lp.need_dx) dims[nd++] = fc_dgrad_dims(pl.dt, pl.B, (int)lp.in_elems, lp.oc);
             dims[nd++] = fc_wgrad_dims(pl.dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc);
+        } else if (lp.kind == MTX_ADDP) {
+            const LayerPlan& sp = pl.L[lp.src];
+            dims[nd++] = conv_fwd_dims(pl.dt, proj_geom(lp, sp, pl.B));
+            if (lp.src >= pl.first_param) dims[nd++] = conv_dgrad_dims(pl.dt, proj_geom(lp, sp, pl.B));
+            dims[nd++] = conv_wgrad_dims(pl.dt, proj_geom(lp, sp, pl.Nb), pl.R);
         }
         for (int k = 0; k < nd; ++k) {
             const size_t pz = partial_elems(pl.dt, dims[k]);
             const bool wgrad = k == nd - 1;
             size_t& mx = wgrad ? max_partial_w : max_partial;
             if (pz > mx) mx = pz;
+            // the first parameter layer's weight gradient runs on the caller's stream
+            if (wgrad && (int)i == pl.first_param && pz > max_partial) max_partial = pz;
         }
         if (lp.w_len) pl.n_wgrad += 1;
-        if (lp.w_len && lp.kind != MTX_BN) {
+        if (lp.w_len && lp.kind == MTX_ADDP) {
+            const double macs = (double)pl.B * lp.oh * lp.ow * lp.oc * pl.L[lp.src].oc;
+            pl.gemm_flops += 2.0 * macs * (lp.src >= pl.first_param ? 3 : 2);
+        } else if (lp.w_len && lp.kind != MTX_BN) {
             const double macs = lp.kind == MTX_CONV
                                     ? (double)pl.B * lp.oh * lp.ow * lp.oc * (lp.c / lp.g) * lp.k * lp.k
                                     : (double)pl.B * lp.in_elems * lp.oc;
@@ -512,6 +561,9 @@ void glorot_init_host(const Plan& pl, uint64_t seed, std::vector<float>& w)
         if (lp.kind == MTX_CONV) {
             fan_in = (double)(lp.c / lp.g) * lp.k * lp.k;
             fan_out = (double)lp.oc * lp.k * lp.k;
+        } else if (lp.kind == MTX_ADDP) {  // a 1x1 convolution of the source's channels
+            fan_in = (double)pl.L[lp.src].oc;
+            fan_out = (double)lp.oc;
         } else {
             fan_in = (double)lp.in_elems;
             fan_out = (double)lp.oc;
@@ -1113,6 +1165,17 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                         return add_fwd(dt, lp.out_elems * pl.B, in, ws + pl.L[lp.src].act_off, out,
                                        lp.relu, s);
                     }), "residual addition");
+        } else if (lp.kind == MTX_ADDP) {
+            // the projection (stored like a convolution's output), then the addition
+            const LayerPlan& sp = pl.L[lp.src];
+            void* pj = ws + lp.proj_off;
+            HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
+                        return conv_fwd(dt, proj_geom(lp, sp, pl.B), ws + sp.act_off, fwd_w(lp),
+                                        bias, pj, lp.act_f32, false, partial, s);
+                    }), "projection forward");
+            HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
+                        return add_fwd(dt, lp.out_elems * pl.B, in, pj, out, lp.relu, s);
+                    }), "projection addition");
         } else if (!(l == 1 && pl.pool_into_first)) {  // else computed with layer 0
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
                         return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc, in, out,
@@ -1148,7 +1211,12 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         const void* mask = (l > 0 && pl.L[l - 1].relu) ? ws + pl.L[l - 1].act_off : nullptr;
         const bool mask_f32 = l > 0 && pl.L[l - 1].act_f32;
         hipStream_t sw = s;
-        if (lp.w_len && overlap && lp.kind != MTX_BN) {
+        // The first parameter layer has no data gradient to run beside: its weight gradient runs
+        // on the caller's stream, beside the weight gradients still running on the second stream
+        // (measured on the AlexNet step: conv1's weight gradient no longer trails the others).
+        const bool side = lp.w_len && overlap && lp.kind != MTX_BN && l != pl.first_param;
+        float* part_wg = side ? partial_w : partial;
+        if (side) {
             HIP_TRY(hipEventRecord(m->fork[nfork], s), "fork");
             HIP_TRY(hipStreamWaitEvent(m->side, m->fork[nfork], 0), "fork");
             ++nfork;
@@ -1175,10 +1243,10 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
                         return lp.run ? conv_wgrad_run(dt, gs, lp.rg, pl.R, in_l, dy, m->grads, ld,
                                                        (long long)lp.w_off, (long long)lp.b_off,
-                                                       partial_w, sw)
+                                                       part_wg, sw)
                                       : conv_wgrad(dt, gs, pl.R, in_l, dy, m->grads, ld,
                                                    (long long)lp.w_off, (long long)lp.b_off,
-                                                   partial_w, sw);
+                                                   part_wg, sw);
                     }), "conv weight gradient");
             if (lp.need_dx) {
                 ConvGeom g{pl.B, lp.c, lp.h, lp.w, lp.oc, lp.oh, lp.ow, lp.k, lp.s, lp.p, lp.g};
@@ -1199,7 +1267,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
             HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
                         return fc_wgrad(dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc, lp.perm_c,
                                         lp.perm_hw, in_l, dy, m->grads, ld, (long long)lp.w_off,
-                                        (long long)lp.b_off, partial_w, sw);
+                                        (long long)lp.b_off, part_wg, sw);
                     }), "fc weight gradient");
             if (lp.need_dx)
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
@@ -1222,6 +1290,28 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                             return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32, skip,
                                            sp.relu ? ws + sp.act_off : nullptr, sp.act_f32, s);
                         }), "residual backward");
+        } else if (lp.kind == MTX_ADDP) {
+            // the previous layer's gradient is dy (times its ReLU mask); the projection's weight
+            // gradient (per shard, on the weight-gradient stream) and its data gradient, which
+            // becomes the gradient kept for the source (times the source's ReLU mask)
+            const LayerPlan& sp = pl.L[lp.src];
+            HIP_TRY(launch_site(m, "wgrad", l, sw, [&] {
+                        return conv_wgrad(dt, proj_geom(lp, sp, pl.Nb), pl.R, ws + sp.act_off, dy,
+                                          m->grads, ld, (long long)lp.w_off, (long long)lp.b_off,
+                                          part_wg, sw);
+                    }), "projection weight gradient");
+            if (dx)
+                HIP_TRY(launch_site(m, "add_bwd", l, s, [&] {
+                            return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32,
+                                           nullptr, nullptr, false, s);
+                        }), "projection addition backward");
+            if (lp.skip_off != kNone)
+                HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
+                            return conv_dgrad(dt, proj_geom(lp, sp, pl.B), dy, bwd_w(lp),
+                                              ws + lp.skip_off,
+                                              sp.relu ? ws + sp.act_off : nullptr, sp.act_f32,
+                                              partial, s);
+                        }), "projection data gradient");
         } else if (lp.need_dx && !(l == 1 && pl.pool_into_first)) {
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {
                         return pool_bwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc,
@@ -1235,7 +1325,9 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         if (lp.need_dx)
             for (size_t a2 = (size_t)l + 1; a2 < pl.L.size(); ++a2) {
                 const LayerPlan& ap = pl.L[a2];
-                if (ap.kind != MTX_ADD || ap.src != l - 1 || ap.skip_off == kNone) continue;
+                if ((ap.kind != MTX_ADD && ap.kind != MTX_ADDP) || ap.src != l - 1 ||
+                    ap.skip_off == kNone)
+                    continue;
                 HIP_TRY(launch_site(m, "skip_add", l - 1, s, [&] {
                             return skip_add(dt, pl.L[l - 1].out_elems * pl.B,
                                             ws + pl.L[l - 1].dy_off, ws + ap.skip_off, s);

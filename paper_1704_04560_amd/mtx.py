@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libmtx.so")
 
 MTX_OK, MTX_EINVAL, MTX_ENOMEM, MTX_EHIP, MTX_EUNSUPPORTED = 0, -1, -2, -3, -4
 MTX_F32, MTX_BF16 = 0, 1
-MTX_FC, MTX_CONV, MTX_MAXPOOL, MTX_BN, MTX_ADD = 0, 1, 2, 3, 4
+MTX_FC, MTX_CONV, MTX_MAXPOOL, MTX_BN, MTX_ADD, MTX_ADDP = 0, 1, 2, 3, 4, 5
 MTX_OPT_MOMENTUM, MTX_OPT_ADAM, MTX_OPT_ADAGRAD = 0, 1, 2
 
 EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_init_model_static", "mtx_train_step", "mtx_average_grads",
@@ -302,7 +302,7 @@ class Model:
                 c, h, w = o, (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
             elif kind == MTX_FC:
                 c, h, w = o, 1, 1
-            elif kind in (MTX_BN, MTX_ADD):
+            elif kind in (MTX_BN, MTX_ADD, MTX_ADDP):
                 pass
             else:
                 h, w = (h - k) // s + 1, (w - k) // s + 1

@@ -28,7 +28,7 @@ from typing import List, Tuple
 
 import numpy as np
 
-FC, CONV, MAXPOOL, BN, ADD = 0, 1, 2, 3, 4
+FC, CONV, MAXPOOL, BN, ADD, ADDP = 0, 1, 2, 3, 4, 5
 F32, BF16 = 0, 1
 
 STREAM_X, STREAM_LABELS, STREAM_W, STREAM_V, STREAM_G, STREAM_S2 = 0, 1, 2, 3, 4, 5
@@ -65,6 +65,13 @@ def bn(relu=False):
 def add(src, relu=False):
     """Residual addition of the output of layer `src` (an earlier layer of the same shape)."""
     return Layer(ADD, 0, src, 1, 0, 1, relu)
+
+
+def addp(src, out, stride=1, relu=False):
+    """Residual addition through a projection shortcut: the output of layer `src` passes a 1x1
+    convolution of the given stride (out = this layer's channel count, with weights and bias)
+    and is added to the previous layer's output (ResNet-50's downsampling blocks)."""
+    return Layer(ADDP, out, src, stride, 0, 1, relu)
 
 
 @dataclass(frozen=True)
@@ -128,6 +135,27 @@ def _res_block(first, width):
             add(first - 1, relu=True))
 
 
+# ResNet-50's bottleneck blocks at CIFAR scale: 1x1 - 3x3 - 1x1 convolutions with batch
+# normalisation, identity shortcuts within a stage and projection shortcuts (strided 1x1
+# convolutions) where a block changes width or resolution; the 3x3 convolution of a downsampling
+# block has stride 2.
+def _bottleneck(first, width, out, src, stride=1, proj=False):
+    """Layers first .. first+6: conv1x1-BN-ReLU, conv3x3(stride)-BN-ReLU, conv1x1-BN, shortcut
+    from layer src (projection or identity), ReLU."""
+    return (conv(width, 1), bn(relu=True), conv(width, 3, stride=stride, pad=1), bn(relu=True),
+            conv(out, 1), bn(),
+            addp(src, out, stride=stride, relu=True) if proj else add(src, relu=True))
+
+
+RESNET_BOTTLENECK = Net("resnet-bottleneck", (3, 32, 32),
+                        (conv(64, 3, pad=1), bn(relu=True))                  # 0-1
+                        + _bottleneck(2, 64, 256, 1, proj=True)              # 2-8
+                        + _bottleneck(9, 64, 256, 8)                         # 9-15
+                        + _bottleneck(16, 128, 512, 15, stride=2, proj=True)  # 16-22, 16x16
+                        + _bottleneck(23, 128, 512, 22)                      # 23-29
+                        + (maxpool(4, 4), fc(10)),                           # 30-31
+                        BF16, "normal")
+
 RESNET = Net("resnet", (3, 32, 32),
              (conv(64, 3, pad=1), bn(relu=True))                      # 0-1
              + _res_block(2, 64) + _res_block(7, 64) + (maxpool(2, 2),)  # 2-12
@@ -144,6 +172,9 @@ WORKLOADS = {
     "alexnet": Workload(ALEXNET, 256, 8, 0.01, 0.9, "AlexNet bf16, B=256, R=8, momentum 0.9"),
     "resnet": Workload(RESNET, 512, 8, 0.01, 0.9,
                        "residual CNN with batch norm bf16, B=512, R=8, momentum 0.9"),
+    "bottleneck": Workload(RESNET_BOTTLENECK, 256, 8, 0.01, 0.9,
+                           "bottleneck residual CNN with projection shortcuts bf16, B=256, R=8, "
+                           "momentum 0.9"),
 }
 
 AVG_UPDATE = {"R": 16, "n": (61_000_000, 250_000_000), "lr": 0.01, "momentum": 0.9,

@@ -21,13 +21,15 @@ def _say(msg):
     print(msg, flush=True)
 
 
-def run_case(tag, net, R, Nb, steps, seed, lr, mu, check_acts=True, tol=None):
+def run_case(tag, net, R, Nb, steps, seed, lr, mu, check_acts=True, tol=None, configure=None):
     layers = wl.layer_tuples(net)
     geo = orc.geometry(net.in_shape, layers)
     prec = "bf16" if net.dtype == wl.BF16 else "f32"
     tol = parity.TOL[net.dtype] if tol is None else tol
     _say(f"[case] {tag}: B={R * Nb} R={R} dtype={prec} steps={steps}")
     model = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=seed)
+    if configure is not None:
+        configure(model)
     w = orc.init_glorot(net.in_shape, layers, seed)
     v = np.zeros_like(w)
     wg, vg = model.get_params()
@@ -314,7 +316,8 @@ def _shard_slice(model, geo, r):
 
 
 @pytest.mark.parametrize("name,shard", [("cifar", 0), ("cifar", 7), ("alexnet", 0),
-                                        ("alexnet", 7), ("resnet", 0), ("resnet", 7)])
+                                        ("alexnet", 7), ("resnet", 0), ("resnet", 7),
+                                        ("bottleneck", 0)])
 def test_full_size_shard_gradients_match_oracle(name, shard):
     """The bf16 workloads at their full size in the launch configuration the benchmark times
     (CIFAR B = 512, AlexNet B = 256, the residual network B = 512; R = 8): the whole batch runs on
@@ -329,7 +332,7 @@ def test_full_size_shard_gradients_match_oracle(name, shard):
     net = w.net
     layers = wl.layer_tuples(net)
     geo = orc.geometry(net.in_shape, layers)
-    tol = parity.RESNET_TOL if name == "resnet" else parity.TOL[net.dtype]
+    tol = parity.RESNET_TOL if name in ("resnet", "bottleneck") else parity.TOL[net.dtype]
     _say(f"[case] full-size shard gradients {name} shard {shard}: B={w.batch} R={w.shards}")
     model = mtx.Model(net.in_shape, layers, net.dtype, w.shards, w.shard_batch, seed=5)
     wt, _ = model.get_params()
@@ -477,6 +480,22 @@ def test_overlapped_weight_gradients_match_one_stream(name, layerwise):
         assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
     a.close()
     b.close()
+
+
+def _layerwise(model):
+    mtx.mtx_set_overlap(model.handle, True)
+    mtx.mtx_set_layerwise_update(model.handle, True)
+
+
+@pytest.mark.parametrize("name,R,Nb", [("lenet", 4, 16), ("cifar", 8, 2), ("alexnet", 4, 1)])
+def test_layerwise_update_step_matches_oracle(name, R, Nb):
+    """Layer-wise average + update (Sec. III-D.2: one reduction per layer, in layer order; each
+    layer's parameters averaged and updated on the third stream as soon as its R shard gradients
+    are written, beside the rest of the backward pass, with the weight gradients on the second
+    stream) against the oracle's step: gradients, average, velocity, update and every output."""
+    net = {"lenet": wl.LENET, "cifar": wl.CIFAR, "alexnet": wl.ALEXNET}[name]
+    run_case(f"{name}-layerwise", net, R, Nb, 2, 41, 0.01, 0.9, check_acts=name != "alexnet",
+             configure=_layerwise)
 
 
 def test_layerwise_update_on_one_stream_matches():
@@ -683,6 +702,35 @@ def test_residual_batchnorm_network(dtype):
 @pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
 def test_residual_batchnorm_edge_layers(dtype):
     run_case("residual-edges", _residual_edges(dtype), 2, 5, 2, seed=32, lr=0.01, mu=0.9)
+
+
+def _projection(dtype):
+    """A downsampling block with a projection shortcut (strided 1x1 convolution of layer 1's
+    output added to the strided main path), an identity block, and a stride-1 projection whose
+    source has no ReLU, then pooling and the classifier."""
+    layers = (wl.conv(8, 3, pad=1), wl.bn(relu=True),
+              wl.conv(16, 3, stride=2, pad=1), wl.bn(), wl.addp(1, 16, stride=2, relu=True),
+              wl.conv(16, 3, pad=1), wl.bn(), wl.add(4, relu=True),
+              wl.conv(24, 1), wl.addp(6, 24), wl.maxpool(2, 2), wl.fc(5))
+    return wl.Net("projection", (3, 12, 12), layers, dtype, "normal")
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_projection_shortcut_network(dtype):
+    run_case(f"projection-{dtype}", _projection(dtype), 2, 4, 2, seed=35, lr=0.01, mu=0.9)
+
+
+def test_bottleneck_shapes_fp32_reduced_batch():
+    """The bottleneck workload's layer shapes (1x1-3x3-1x1 blocks, projection shortcuts, a
+    stride-2 downsampling block) with fp32 compute at B = 4, R = 2, to the fp32 bound."""
+    net = wl.Net("bottleneck-f32", wl.RESNET_BOTTLENECK.in_shape, wl.RESNET_BOTTLENECK.layers,
+                 wl.F32, "normal")
+    run_case("bottleneck fp32", net, 2, 2, 1, seed=36, lr=0.01, mu=0.9)
+
+
+def test_bottleneck_workload_reduced_batch():
+    run_case("bottleneck", wl.RESNET_BOTTLENECK, 2, 16, 1, seed=37, lr=0.01, mu=0.9,
+             tol=parity.RESNET_TOL)
 
 
 def test_resnet_shapes_fp32_reduced_batch():

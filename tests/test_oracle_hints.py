@@ -62,7 +62,7 @@ def _pool_gaps(name):
     the oracle's stored pool input."""
     net, layers, prec, R, Nb, w, x, y, res = _base(name)
     geo = orc.geometry(net.in_shape, layers)
-    li, _, off, n = _segment(net, layers, R * Nb, "pool")
+    li, _, off, n, _ = _segment(net, layers, R * Nb, "pool")
     c, h, wd = geo[li]["in_shape"]
     s = layers[li][3]
     aoff = sum(int(np.prod(g["out_shape"])) * R * Nb for g in geo[:li - 1])
@@ -76,7 +76,7 @@ def _pool_gaps(name):
 @pytest.mark.parametrize("name", list(CASES))
 def test_deepest_pool_forced_to_first_element_is_rejected(name):
     net, layers, prec, R, Nb, w, x, y, res = _base(name)
-    _, _, off, n = _segment(net, layers, R * Nb, "pool")
+    _, _, off, n, _ = _segment(net, layers, R * Nb, "pool")
     ph = np.full(res.pool_argmax.size, -1, np.int32)
     ph[off:off + n] = 0
     changed = int((res.pool_argmax[off:off + n] != 0).sum())
@@ -88,7 +88,7 @@ def test_deepest_pool_forced_to_first_element_is_rejected(name):
 @pytest.mark.parametrize("name", list(CASES))
 def test_deepest_relu_forced_on_is_rejected(name):
     net, layers, prec, R, Nb, w, x, y, res = _base(name)
-    _, _, off, n = _segment(net, layers, R * Nb, "relu")
+    _, _, off, n, _ = _segment(net, layers, R * Nb, "relu")
     rh = np.full(res.relu_mask.size, -1, np.int8)
     rh[off:off + n] = 1
     assert int((res.relu_mask[off:off + n] == 0).sum()) > n // 10
@@ -115,7 +115,7 @@ def _preactivations(name):
     """Pre-activations of the deepest ReLU layer for shard 0's samples: the same network with
     that layer's ReLU removed stores them as its output (the layers below are unchanged)."""
     net, layers, prec, R, Nb, w, x, y, res = _base(name)
-    li, _, off, n = _segment(net, layers, R * Nb, "relu")
+    li, _, off, n, _ = _segment(net, layers, R * Nb, "relu")
     lt = list(layers)
     lt[li] = tuple(lt[li][:6]) + (0,)
     geo = orc.geometry(net.in_shape, lt)

@@ -233,7 +233,8 @@ def test_bf16_mode_rounds_at_the_stated_points():
 
 def _bf16_case(name):
     nets = {"cifar": (wl.CIFAR, 4, 2), "tiny": (_tiny_net()[0], 6, 3),
-            "residual": (_residual_net(wl.BF16)[0], 8, 2)}
+            "residual": (_residual_net(wl.BF16)[0], 8, 2),
+            "projection": (_projection_net(wl.BF16)[0], 8, 2)}
     net, B, R = nets[name]
     layers = wl.layer_tuples(net)
     geo = orc.geometry(net.in_shape, layers)
@@ -253,7 +254,7 @@ def _worst_layer_rel(res, gref, geo, R):
                for r in range(R) for gg in geo if gg["w_len"])
 
 
-@pytest.mark.parametrize("name", ["cifar", "tiny", "residual"])
+@pytest.mark.parametrize("name", ["cifar", "tiny", "residual", "projection"])
 def test_bf16_mode_gradients_match_an_independent_bf16_storage_model(name):
     """Every rounding point of the bf16 mode, the gradient side included, against torch float64
     autograd with bfloat16 storage emulated at exactly those points (torch_ref.forward_bf16):
@@ -324,6 +325,17 @@ def _residual_net(dtype=wl.F32):
     return net, wl.layer_tuples(net)
 
 
+def _projection_net(dtype=wl.F32):
+    """A downsampling block with a projection shortcut (strided 1x1 convolution of layer 1's
+    output added to the strided main path), then an identity block, pooling and the classifier."""
+    layers = (wl.conv(4, 3, pad=1), wl.bn(relu=True),
+              wl.conv(8, 3, stride=2, pad=1), wl.bn(), wl.addp(1, 8, stride=2, relu=True),
+              wl.conv(8, 3, pad=1), wl.bn(), wl.add(4, relu=True),
+              wl.maxpool(2, 2), wl.fc(5))
+    net = wl.Net("projection", (3, 8, 8), layers, dtype, "normal")
+    return net, wl.layer_tuples(net)
+
+
 def _perturbed_params(net, layers, seed):
     """Glorot weights (BN: gamma = 1, beta = 0) moved off their initial values, so that every
     parameter, the BN scales and shifts included, takes part."""
@@ -339,10 +351,12 @@ def _perturbed_params(net, layers, seed):
 
 
 @pytest.mark.parametrize("R", [1, 2])
-def test_residual_bn_step_matches_torch_autograd(R):
+@pytest.mark.parametrize("netf", ["residual", "projection"])
+def test_residual_bn_step_matches_torch_autograd(R, netf):
     """Every shard's loss and gradient against torch float64 autograd (F.batch_norm in training
-    mode over the shard's samples, tensor addition for the residual)."""
-    net, layers = _residual_net()
+    mode over the shard's samples, tensor addition for the residual, F.conv2d with a 1x1 kernel
+    and the stride for the projection shortcut)."""
+    net, layers = _residual_net() if netf == "residual" else _projection_net()
     geo, w = _perturbed_params(net, layers, 3)
     x, y = wl.make_batch(net, 6 * R, seed=5)
     res = orc.train_step(net.in_shape, layers, R, x, y, w, None, 0.01, 0.0, prec="exact")
@@ -356,8 +370,9 @@ def test_residual_bn_step_matches_torch_autograd(R):
                 assert _rel(res.grads[r][sl], gref[r][sl]) < 1e-6, gg
 
 
-def test_residual_bn_finite_differences():
-    net, layers = _residual_net()
+@pytest.mark.parametrize("netf", ["residual", "projection"])
+def test_residual_bn_finite_differences(netf):
+    net, layers = _residual_net() if netf == "residual" else _projection_net()
     geo, w = _perturbed_params(net, layers, 7)
     P = w.size
     x, y = wl.make_batch(net, 6, seed=9)
@@ -418,6 +433,25 @@ def test_shard_statistics_make_the_average_differ_from_the_full_batch_gradient()
     p4 = orc.train_step(net.in_shape, plain, 4, x, y, wp, None, 0.0, 0.0, prec="exact")
     p1 = orc.train_step(net.in_shape, plain, 1, x, y, wp, None, 0.0, 0.0, prec="exact")
     assert P == wp.size and _rel(p4.gavg, p1.gavg) < 1e-6  # float rounding of each shard
+
+
+def test_projection_shortcut_layers_are_validated():
+    net, layers = _projection_net()
+    orc.param_count(net.in_shape, layers)
+    bad_out = list(layers)
+    bad_out[4] = (5, 6, 1, 2, 0, 1, 1)  # out must be this layer's channel count (8)
+    bad_stride = list(layers)
+    bad_stride[4] = (5, 8, 1, 1, 0, 1, 1)  # stride 1 maps 8x8 to 8x8, not to 4x4
+    bad_pad = list(layers)
+    bad_pad[4] = (5, 8, 1, 2, 1, 1, 1)
+    bad_src = list(layers)
+    bad_src[4] = (5, 8, 3, 2, 0, 1, 1)  # the previous layer is not a valid source
+    for L in (bad_out, bad_stride, bad_pad, bad_src):
+        with pytest.raises(ValueError):
+            orc.param_count(net.in_shape, L)
+    geo = orc.geometry(net.in_shape, layers)
+    assert geo[4]["w_len"] == 8 * 4 and geo[4]["b_len"] == 8
+    assert orc.param_count(net.in_shape, layers) == geo[-1]["b_off"] + geo[-1]["b_len"]
 
 
 def test_residual_bn_layers_are_validated():

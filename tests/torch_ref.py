@@ -38,6 +38,9 @@ def forward(layers, geo, wt, x):
             a = F.batch_norm(a, None, None, pr[0], pr[1], training=True, eps=1e-3)
         elif kind == 4:
             a = a + acts[k]
+        elif kind == 5:  # projection shortcut: 1x1 convolution of stride s of layer k's output
+            cs = acts[k].shape[1]
+            a = a + F.conv2d(acts[k], pr[0].view(o, cs, 1, 1), pr[1], stride=s)
         else:
             a = F.max_pool2d(a, k, s)
         if relu:
@@ -145,6 +148,11 @@ def forward_bf16(layers, geo, wt, x, round_grads=True, round_loss_grad=True, dec
             a = F.batch_norm(a, None, None, pr[0], pr[1], training=True, eps=1e-3)
         elif kind == 4:
             a = a + acts[k]
+        elif kind == 5:  # the projection's output is stored, then added; its data gradient
+            cs = acts[k].shape[1]  # is stored before it joins the source's other gradient
+            src = _RoundGrad.apply(acts[k]) if round_grads else acts[k]
+            pj = F.conv2d(src, _RoundValue.apply(pr[0].view(o, cs, 1, 1), True), pr[1], stride=s)
+            a = a + _RoundValue.apply(pj, True)
         else:
             W_ = a.shape[3]
             a, idx = F.max_pool2d(a, k, s, return_indices=True)

@@ -334,7 +334,8 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             j.kind = PREP_CONV_F;
             lp.fw_off = add_job(j);
             if (lp.src >= pl.first_param) {
-                j.kind = PREP_CONV_D;
+                lp.dgrad_col = conv_dgrad_use_col(proj_geom(lp, pl.L[lp.src], pl.B));
+                j.kind = lp.dgrad_col ? PREP_CONV_C : PREP_CONV_D;
                 lp.bw_off = add_job(j);
             }
         } else if (lp.kind == MTX_CONV) {
@@ -431,8 +432,14 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
             dims[nd++] = fc_wgrad_dims(pl.dt, pl.Nb, pl.R, (int)lp.in_elems, lp.oc);
         } else if (lp.kind == MTX_ADDP) {
             const LayerPlan& sp = pl.L[lp.src];
-            dims[nd++] = conv_fwd_dims(pl.dt, proj_geom(lp, sp, pl.B));
-            if (lp.src >= pl.first_param) dims[nd++] = conv_dgrad_dims(pl.dt, proj_geom(lp, sp, pl.B));
+            const ConvGeom gp = proj_geom(lp, sp, pl.B);
+            dims[nd++] = conv_fwd_dims(pl.dt, gp);
+            if (lp.src >= pl.first_param && lp.dgrad_col) {
+                dims[nd++] = conv_dgrad_col_dims(pl.dt, gp);
+                if (conv_dgrad_col_elems(gp) > max_col) max_col = conv_dgrad_col_elems(gp);
+            } else if (lp.src >= pl.first_param) {
+                dims[nd++] = conv_dgrad_dims(pl.dt, gp);
+            }
             dims[nd++] = conv_wgrad_dims(pl.dt, proj_geom(lp, sp, pl.Nb), pl.R);
         }
         for (int k = 0; k < nd; ++k) {
@@ -1307,10 +1314,15 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                         }), "projection addition backward");
             if (lp.skip_off != kNone)
                 HIP_TRY(launch_site(m, "dgrad", l, s, [&] {
-                            return conv_dgrad(dt, proj_geom(lp, sp, pl.B), dy, bwd_w(lp),
-                                              ws + lp.skip_off,
-                                              sp.relu ? ws + sp.act_off : nullptr, sp.act_f32,
-                                              partial, s);
+                            const ConvGeom gp = proj_geom(lp, sp, pl.B);
+                            const void* smask = sp.relu ? ws + sp.act_off : nullptr;
+                            return lp.dgrad_col
+                                       ? conv_dgrad_col(dt, gp, dy, bwd_w(lp), ws + lp.skip_off,
+                                                        smask, sp.act_f32,
+                                                        reinterpret_cast<float*>(ws + pl.col_off),
+                                                        partial, s)
+                                       : conv_dgrad(dt, gp, dy, bwd_w(lp), ws + lp.skip_off,
+                                                    smask, sp.act_f32, partial, s);
                         }), "projection data gradient");
         } else if (lp.need_dx && !(l == 1 && pl.pool_into_first)) {
             HIP_TRY(launch_site(m, "pool_bwd", l, s, [&] {

@@ -103,9 +103,12 @@ size_t conv_dgrad_col_elems(const ConvGeom& g)
 }
 bool conv_dgrad_use_col(const ConvGeom& g)
 {
-    // taps the implicit GEMM visits per useful multiply-add (stride 1: H*W / (OH*OW))
+    // taps the implicit GEMM visits per useful multiply-add (stride 1: H*W / (OH*OW)); a strided
+    // convolution always takes the col route: its implicit data gradient decodes every tap per
+    // element with scalar loads (measured: a 3x3 stride-2 layer of the bottleneck network
+    // 875 us implicit)
     const double waste = (double)g.H * g.W / ((double)g.OH * g.OW * g.S * g.S);
-    return waste >= 1.5 && conv_dgrad_col_elems(g) * 4 <= (size_t)512 << 20;
+    return (waste >= 1.5 || g.S > 1) && conv_dgrad_col_elems(g) * 4 <= (size_t)512 << 20;
 }
 GemmDims conv_fwd_run_dims(int dt, const ConvGeom& g, const RunGeom& r)
 {

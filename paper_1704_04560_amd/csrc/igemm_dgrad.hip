@@ -58,10 +58,83 @@ __global__ __launch_bounds__(256) void col2im_kernel(const GemmArgs a, const flo
     static_cast<T*>(a.out)[t] = from_f32<T>(acc);
 }
 
+// Four channels per thread (C and C/G multiples of 4, so that the four share a group and every
+// col row, dx row and mask row access is 16-byte aligned); the same taps in the same order as
+// col2im_kernel.  KT, ST > 0: kernel size and stride known at compile time (0: from a).
+template <typename T>
+__device__ __forceinline__ void load4(const void* p, long long i, float (&v)[4])
+{
+    if constexpr (sizeof(T) == 4) {
+        const float4 q = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else {
+        const uint2 q = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p) + i);
+        v[0] = bf16_to_f32((bf16_t)(q.x & 0xffffu)); v[1] = bf16_to_f32((bf16_t)(q.x >> 16));
+        v[2] = bf16_to_f32((bf16_t)(q.y & 0xffffu)); v[3] = bf16_to_f32((bf16_t)(q.y >> 16));
+    }
+}
+
+template <typename T, int KT, int ST>
+__global__ __launch_bounds__(256) void col2im_vec4_kernel(const GemmArgs a, const float* __restrict__ col)
+{
+    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long total = (long long)a.N * a.C * a.H * a.W / 4;
+    if (t >= total) return;
+    const unsigned e = (unsigned)t * 4u;
+    const unsigned pos = fdiv(a.fd_c, e), ci = e - pos * (unsigned)a.C;
+    const unsigned b = fdiv(a.fd_hw, pos), hw = pos - b * (unsigned)(a.H * a.W);
+    const unsigned hq = fdiv(a.fd_w, hw);
+    const int h = (int)hq, w = (int)(hw - hq * (unsigned)a.W);
+    const int grp = (int)ci / a.cg, cl = (int)ci - grp * a.cg;
+    const int K = KT > 0 ? KT : a.K, S = ST > 0 ? ST : a.S;
+    const long long Q = (long long)a.N * a.OH * a.OW, P = (long long)K * K * a.cg;
+    const float* cp = col + (long long)grp * Q * P + (long long)b * a.OH * a.OW * P + cl;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < K; ++u) {
+        const int th = h + a.PD - u;
+        const int oh = th / S;
+        if (th < 0 || oh * S != th || oh >= a.OH) continue;
+        for (int v = 0; v < K; ++v) {
+            const int tw = w + a.PD - v;
+            const int ow = tw / S;
+            if (tw < 0 || ow * S != tw || ow >= a.OW) continue;
+            const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(
+                cp + ((long long)oh * a.OW + ow) * P + (u * K + v) * a.cg));
+            acc[0] += x[0]; acc[1] += x[1]; acc[2] += x[2]; acc[3] += x[3];
+        }
+    }
+    if (a.mask) {
+        float m[4];
+        if (a.mask_f32) load4<float>(a.mask, (long long)e, m);
+        else load4<T>(a.mask, (long long)e, m);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (!(m[i] > 0.f)) acc[i] = 0.f;
+    }
+    if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + e) =
+            make_float4(acc[0], acc[1], acc[2], acc[3]);
+    } else {
+        uint2 q;
+        q.x = (unsigned)f32_to_bf16(acc[0]) | ((unsigned)f32_to_bf16(acc[1]) << 16);
+        q.y = (unsigned)f32_to_bf16(acc[2]) | ((unsigned)f32_to_bf16(acc[3]) << 16);
+        *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.out) + e) = q;
+    }
+}
+
 template <typename T>
 static void launch_col2im(const GemmArgs& c, const float* col, hipStream_t s)
 {
     const long long total = (long long)c.N * c.C * c.H * c.W;
+    if (c.C % 4 == 0 && c.cg % 4 == 0 && total < (1ll << 32)) {
+        dim3 grid((unsigned)((total / 4 + 255) / 256));
+        if (c.S == 1 && c.K == 3) hipLaunchKernelGGL((col2im_vec4_kernel<T, 3, 1>), grid, dim3(256), 0, s, c, col);
+        else if (c.S == 1 && c.K == 5) hipLaunchKernelGGL((col2im_vec4_kernel<T, 5, 1>), grid, dim3(256), 0, s, c, col);
+        else if (c.S == 2 && c.K == 3) hipLaunchKernelGGL((col2im_vec4_kernel<T, 3, 2>), grid, dim3(256), 0, s, c, col);
+        else if (c.S == 2 && c.K == 1) hipLaunchKernelGGL((col2im_vec4_kernel<T, 1, 2>), grid, dim3(256), 0, s, c, col);
+        else hipLaunchKernelGGL((col2im_vec4_kernel<T, 0, 0>), grid, dim3(256), 0, s, c, col);
+        return;
+    }
     dim3 grid((unsigned)((total + 255) / 256));
     if (c.S == 1 && c.K == 3) hipLaunchKernelGGL((col2im_kernel<T, 3>), grid, dim3(256), 0, s, c, col);
     else if (c.S == 1 && c.K == 5) hipLaunchKernelGGL((col2im_kernel<T, 5>), grid, dim3(256), 0, s, c, col);

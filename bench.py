@@ -56,55 +56,93 @@ def geometry(net):
 
 
 def site_work(name, layer, geo, wkl, es):
-    """Algorithmic work of one launch of a step's launch site: ("mfma", flops) for the matrix
-    kernels (2 x multiply-adds of the convolution / product), ("alu", flops) for the direct
-    first-convolution kernels (fp32 vector fused multiply-adds), ("hbm", bytes) for the others
-    (each tensor read once and written once), (None, 0) when not modelled."""
+    """Algorithmic work of one launch of a step's launch site: ("alu", flops) for the direct
+    first-convolution kernels (fp32 vector fused multiply-adds), ("hbm", bytes) for the
+    memory-bound ones (each tensor read once and written once), (None, 0) when not modelled.
+    A matrix launch is ("mfma", flops) (2 x multiply-adds of the convolution / product) when its
+    flops take longer at the MFMA peak than its algorithmic bytes at the HBM peak, else
+    ("hbm", bytes): operands read once, the output written once (a data gradient also reads
+    the ReLU mask; a weight gradient writes R fp32 gradient rows)."""
+    return _site_work(name, layer, geo, wkl, es)[:2]
+
+
+def matrix_flops(name, layer, geo, wkl):
+    """2 x multiply-adds of a matrix launch site (0 for the others)."""
+    from paper_1704_04560_amd import workloads as wl
+    if layer < 0 or name not in ("fwd", "dgrad", "wgrad"):
+        return 0.0
+    g = geo[layer]
+    l = g["layer"]
+    B = wkl.batch
+    if l.kind == wl.CONV:
+        return 2.0 * B * g["oh"] * g["ow"] * g["oc"] * (g["c"] // l.groups) * l.k * l.k
+    if l.kind == wl.ADDP:  # the projection: a 1x1 convolution of the source's output
+        return 2.0 * B * g["oh"] * g["ow"] * g["oc"] * geo[l.k]["oc"]
+    if l.kind == wl.FC:
+        return 2.0 * B * g["c"] * g["h"] * g["w"] * g["oc"]
+    return 0.0
+
+
+def _site_work(name, layer, geo, wkl, es):
     from paper_1704_04560_amd import workloads as wl
     B, R, Nb = wkl.batch, wkl.shards, wkl.shard_batch
     if layer >= 0:
         g = geo[layer]
         l = g["layer"]
-        if l.kind == wl.CONV:
-            macs = B * g["oh"] * g["ow"] * g["oc"] * (g["c"] // l.groups) * l.k * l.k
-        elif l.kind == wl.ADDP:  # the projection: a 1x1 convolution of the source's output
-            macs = B * g["oh"] * g["ow"] * g["oc"] * geo[l.k]["oc"]
-        else:
-            macs = B * g["c"] * g["h"] * g["w"] * g["oc"]
         in_sz = B * g["c"] * g["h"] * g["w"]
         out_sz = B * g["oc"] * g["oh"] * g["ow"]
-        if name in ("fwd", "dgrad", "wgrad"):
-            return "mfma", 2.0 * macs
+        if name in ("fwd", "dgrad", "wgrad") and l.kind in (wl.CONV, wl.FC, wl.ADDP):
+            flops = matrix_flops(name, layer, geo, wkl)
+            if l.kind == wl.ADDP:
+                src = geo[l.k]
+                x_sz, wn = B * src["oc"] * src["oh"] * src["ow"], g["oc"] * src["oc"]
+            elif l.kind == wl.CONV:
+                x_sz, wn = in_sz, g["oc"] * (g["c"] // l.groups) * l.k * l.k
+            else:
+                x_sz, wn = in_sz, g["oc"] * g["c"] * g["h"] * g["w"]
+            if name == "fwd":
+                nbytes = (x_sz + wn + out_sz) * es
+            elif name == "dgrad":
+                below = l.k if l.kind == wl.ADDP else layer - 1
+                mask = below >= 0 and geo[below]["layer"].relu
+                nbytes = (out_sz + wn + (2 if mask else 1) * x_sz) * es
+            else:
+                nbytes = (x_sz + out_sz) * es + R * (wn + g["oc"]) * 4
+            peak = PEAK["bf16_TFLOPs"] if es == 2 else PEAK["f32_TFLOPs"]
+            if flops / (peak * 1e12) >= nbytes / (PEAK["hbm_GBps"] * 1e9):
+                return "mfma", flops, flops
+            return "hbm", float(nbytes), flops
+        macs = matrix_flops("fwd", layer, geo, wkl) / 2 if l.kind == wl.CONV else 0.0
         if name in ("fwd_direct", "wgrad_direct"):
-            return "alu", 2.0 * macs
+            return "alu", 2.0 * macs, 0.0
         if name == "wgrad_direct_reduce":  # per-image fp32 sums read, the shard rows written
             no = g["oc"] * l.k * l.k + g["oc"]
-            return "hbm", 4.0 * no * (B + R)
+            return "hbm", 4.0 * no * (B + R), 0.0
         if name == "dgrad_col2im":  # fp32 col read once, dx written, mask read
-            return "hbm", 4.0 * l.k * l.k * g["c"] * B * g["oh"] * g["ow"] + 2 * es * in_sz
+            return "hbm", 4.0 * l.k * l.k * g["c"] * B * g["oh"] * g["ow"] + 2 * es * in_sz, 0.0
         if name == "pool_fwd":
-            return "hbm", in_sz * es + out_sz * (es + 1)
+            return "hbm", in_sz * es + out_sz * (es + 1), 0.0
         if name == "pool_bwd":
-            return "hbm", out_sz * (es + 1) + in_sz * es * 2  # dy + argmax, mask + dx
+            return "hbm", out_sz * (es + 1) + in_sz * es * 2, 0.0  # dy + argmax, mask + dx
         if name == "bn_fwd":  # the statistics pass reads x
-            return "hbm", in_sz * es
+            return "hbm", in_sz * es, 0.0
         if name == "bn_fwd_apply":  # x read, y written
-            return "hbm", 2 * in_sz * es
+            return "hbm", 2 * in_sz * es, 0.0
         if name == "bn_bwd":  # x and dy read
-            return "hbm", 2 * in_sz * es
+            return "hbm", 2 * in_sz * es, 0.0
         if name == "bn_bwd_apply":  # x, dy and the mask read, dx written
-            return "hbm", 4 * in_sz * es
+            return "hbm", 4 * in_sz * es, 0.0
         if name in ("add_fwd", "skip_add"):  # two read, one written
-            return "hbm", 3 * out_sz * es
+            return "hbm", 3 * out_sz * es, 0.0
         if name == "add_bwd" and l.kind == wl.ADDP:  # dy and the mask read, dx written
-            return "hbm", 3 * out_sz * es
+            return "hbm", 3 * out_sz * es, 0.0
         if name == "add_bwd":  # dy and two masks read, dx and the kept gradient written
-            return "hbm", 5 * out_sz * es
-        return None, 0.0
+            return "hbm", 5 * out_sz * es, 0.0
+        return None, 0.0, 0.0
     P = wkl_params(wkl)
     if name == "avg_update":
         mom = wkl.momentum != 0.0
-        return "hbm", (R + (5 if mom else 3)) * 4 * P
+        return "hbm", (R + (5 if mom else 3)) * 4 * P, 0.0
     if name == "prep_w":
         # every weight tensor is read once (fp32) and written once per layout it is prepared in
         # (convolutions below the first parameter layer need a data-gradient layout too)
@@ -117,14 +155,14 @@ def site_work(name, layer, geo, wkl, es):
                 tot += n * (4 + es) * (2 if i > first else 1)
             elif l.kind == wl.FC:
                 tot += g["oc"] * g["c"] * g["h"] * g["w"] * (4 + es)
-        return "hbm", tot
+        return "hbm", tot, 0.0
     if name == "prep_x":
         c, h, w = wkl.net.in_shape
-        return "hbm", (4 + es) * B * c * h * w
+        return "hbm", (4 + es) * B * c * h * w, 0.0
     if name == "softmax_xent":
         nc = wkl.net.num_classes
-        return "hbm", B * nc * (4 + es) + B * 4 + 4
-    return None, 0.0
+        return "hbm", B * nc * (4 + es) + B * 4 + 4, 0.0
+    return None, 0.0, 0.0
 
 
 _P = {}
@@ -357,9 +395,9 @@ def measure(torch, mtx, wl, name, steps, warmup):
     for (sname, layer, launches, total) in sites:
         if launches == 0:
             continue
-        bound, work = site_work(sname, layer, geo, wkl, es)
+        bound, work, mm = _site_work(sname, layer, geo, wkl, es)
         kernels.append(dict(name=sname, layer=layer, avg_ms=total / launches, bound=bound,
-                            work=work))
+                            work=work, mm_flops=mm))
     peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
     # the dominant kernel: the longest one whose algorithmic work is modelled
     dom = max((k for k in kernels if k["bound"]), key=lambda k: k["avg_ms"])
@@ -382,8 +420,8 @@ def measure(torch, mtx, wl, name, steps, warmup):
     roof["kernel_ms"] = round(dom["avg_ms"], 5)
     roof["work_per_launch"] = dom["work"]
 
-    mfma_ms = sum(k["avg_ms"] for k in kernels if k["bound"] == "mfma")
-    mfma_flops = sum(k["work"] for k in kernels if k["bound"] == "mfma")
+    mfma_ms = sum(k["avg_ms"] for k in kernels if k["mm_flops"])
+    mfma_flops = sum(k["mm_flops"] for k in kernels if k["mm_flops"])
     au = [k for k in kernels if k["name"] == "avg_update"][0]
     return {
         "wkl": wkl,
@@ -418,7 +456,7 @@ def main():
                          "byte counters can be scaled against a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no cross-GPU path (the all-reduce across "
+        print("bench.py measures one GPU: the library has no cross-GPU path (the all-reduce across "
               "GPUs is out of scope); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 

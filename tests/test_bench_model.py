@@ -1,0 +1,70 @@
+"""The benchmark's work model (algorithmic bytes and flops per launch, roofline bound) and its
+command line.  CPU only: no kernel runs."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_1704_04560_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _work(name, site, layer):
+    wkl = wl.WORKLOADS[name]
+    geo = bench.geometry(wkl.net)
+    es = 2 if wkl.net.dtype == wl.BF16 else 4
+    return bench._site_work(site, layer, geo, wkl, es)
+
+
+def test_gradient_average_moves_r_rows_plus_weights_and_momentum():
+    # Sec. III-E: R shard gradients read; w and v read and written; the average written
+    wkl = wl.WORKLOADS["alexnet"]
+    P = bench.wkl_params(wkl)
+    bound, nbytes, mm = _work("alexnet", "avg_update", -1)
+    assert bound == "hbm" and mm == 0.0
+    assert nbytes == (wkl.shards + 5) * 4 * P
+
+
+def test_alexnet_conv3_is_a_matrix_bound_launch():
+    # conv3: 256 x 13 x 13 outputs of 384 channels over a 3 x 3 x 256 window
+    bound, flops, mm = _work("alexnet", "wgrad", 4)
+    assert bound == "mfma"
+    assert flops == mm == 2.0 * 256 * 13 * 13 * 384 * 256 * 9
+
+
+def test_fully_connected_weight_gradient_is_bound_by_its_gradient_rows():
+    # FC6 (9216 -> 4096): the R fp32 gradient rows it writes outweigh its flops at the peaks
+    wkl = wl.WORKLOADS["alexnet"]
+    bound, nbytes, mm = _work("alexnet", "wgrad", 8)
+    assert bound == "hbm"
+    assert mm == 2.0 * 256 * 9216 * 4096
+    assert nbytes == (256 * 9216 + 256 * 4096) * 2 + wkl.shards * (9216 * 4096 + 4096) * 4
+
+
+def test_one_by_one_convolution_data_gradient_is_memory_bound():
+    # bottleneck layer 16: 1x1, 256 -> 128 channels at 32 x 32; dy, W, the mask and dx
+    bound, nbytes, mm = _work("bottleneck", "dgrad", 16)
+    assert bound == "hbm"
+    pos = 256 * 32 * 32
+    assert nbytes == (pos * 128 + 128 * 256 + 2 * pos * 256) * 2
+    assert mm == 2.0 * pos * 128 * 256
+
+
+def test_projection_counts_the_source_as_its_input():
+    # bottleneck layer 22: 1x1 stride-2 projection of layer 15's 256 x 32 x 32 output to 512
+    # channels at 16 x 16
+    bound, nbytes, mm = _work("bottleneck", "fwd", 22)
+    assert mm == 2.0 * 256 * 16 * 16 * 512 * 256
+    assert nbytes == (256 * 256 * 32 * 32 + 512 * 256 + 256 * 512 * 16 * 16) * 2
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode != 0
+    assert "--gpus 1" in r.stderr
+    assert not r.stdout.strip()

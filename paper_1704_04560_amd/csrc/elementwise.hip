@@ -704,10 +704,12 @@ __device__ __forceinline__ void avg_update_one(const float* __restrict__ grads, 
 
 // n elements in 16-byte vectors: a block walks spans of 2 x 256 vectors (each thread two, 4 KB
 // apart, so that every wave reads 1 KB contiguous per row and pass), issues the loads of w and v
-// and then of all R rows before adding the rows in ascending r; the n % 4 elements left over
-// are taken by the first thread of the grid.  Every access is nontemporal (each byte is read or
-// written once per call): measured at R = 16, n = 61M, 5.97 TB/s against 5.43 TB/s for one
-// vector per thread with cached w and v.
+// and then the rows, adding each row as it arrives in ascending r (the compiler keeps the loads
+// in flight and waits for them one by one; holding all R rows in registers first took 166
+// registers at R = 16 and three waves per SIMD instead of five: 5.48 against 5.97 TB/s); the
+// n % 4 elements left over are taken by the first thread of the grid.  Every access is
+// nontemporal (each byte is read or written once per call): measured at R = 16, n = 61M,
+// 5.97 TB/s against 5.43 TB/s for one vector per thread with cached w and v.
 template <int RT, bool MOM, bool AVG, bool UPD>
 __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__ grads, int Rrt,
                                                        long long n, long long ld,
@@ -736,20 +738,15 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
             }
         }
         if (RT > 0) {
-            f32x4 buf[RT > 0 ? RT : 1][U];
 #pragma unroll
             for (int r = 0; r < RT; ++r)
 #pragma unroll
                 for (int u = 0; u < U; ++u)
-                    if (ok[u])
-                        buf[r][u] = __builtin_nontemporal_load(g4 + r * ld4 + base + u * 256 +
-                                                               threadIdx.x);
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                s[u] = buf[0][u];
-#pragma unroll
-                for (int r = 1; r < RT; ++r) s[u] += buf[r][u];
-            }
+                    if (ok[u]) {
+                        const f32x4 x = __builtin_nontemporal_load(g4 + r * ld4 + base +
+                                                                   u * 256 + threadIdx.x);
+                        s[u] = r == 0 ? x : s[u] + x;
+                    }
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -796,6 +793,14 @@ __global__ __launch_bounds__(256) void avg_update_scalar(const float* __restrict
     avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
 }
 
+// Dynamic LDS that the streaming average kernels reserve without using it, so that at most five
+// 256-thread blocks share a compute unit (160 KB of LDS): fewer rows in flight at once keep the
+// HBM row buffers open longer.  Measured (momentum kernel, blocks per CU unlimited / 4 / 5 / 6):
+// R = 16, n = 61M 5.39 / 5.62 / 5.83 / 5.54 TB/s; R = 8, n = 61M 5.76 / 6.07 / 6.14 / 5.92;
+// R = 16, n = 250M 5.44 / 5.53 / 5.69 / 5.57.  A launch with a capped grid (the layer-wise update
+// beside other kernels) reserves nothing.
+constexpr size_t kStreamLds = 160 * 1024 / 5 - 1024;
+
 template <bool MOM, bool AVG, bool UPD>
 static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t ld, float* w,
                                     float* v, float lr, float mu, float* avg, unsigned max_blocks,
@@ -808,13 +813,14 @@ static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t 
         const long long nn = (long long)n;
         dim3 grid(grid_for(n / 4 + 1, 512));
         if (max_blocks && grid.x > max_blocks) grid.x = max_blocks;
+        const size_t lds = max_blocks ? 0 : kStreamLds;
         switch (R) {
-        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), 0, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
         }
     } else {
         hipLaunchKernelGGL((avg_update_scalar<MOM, AVG, UPD>), dim3(grid_for(n, 256)), dim3(256),
@@ -960,13 +966,14 @@ static hipError_t avg_adapt_launch(const float* grads, int R, size_t n, size_t l
     if (vec) {
         dim3 grid(grid_for(n / 4 + 1, 512));
         if (max_blocks && grid.x > max_blocks) grid.x = max_blocks;
+        const size_t lds = max_blocks ? 0 : kStreamLds;
         switch (R) {
-        case 1: hipLaunchKernelGGL((avg_adapt_vec4<1, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
-        case 2: hipLaunchKernelGGL((avg_adapt_vec4<2, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
-        case 4: hipLaunchKernelGGL((avg_adapt_vec4<4, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
-        case 8: hipLaunchKernelGGL((avg_adapt_vec4<8, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
-        case 16: hipLaunchKernelGGL((avg_adapt_vec4<16, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
-        default: hipLaunchKernelGGL((avg_adapt_vec4<0, ADAM, AVG>), grid, dim3(256), 0, s, grads, R, nn, ll, p); break;
+        case 1: hipLaunchKernelGGL((avg_adapt_vec4<1, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
+        case 2: hipLaunchKernelGGL((avg_adapt_vec4<2, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
+        case 4: hipLaunchKernelGGL((avg_adapt_vec4<4, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
+        case 8: hipLaunchKernelGGL((avg_adapt_vec4<8, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
+        case 16: hipLaunchKernelGGL((avg_adapt_vec4<16, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
+        default: hipLaunchKernelGGL((avg_adapt_vec4<0, ADAM, AVG>), grid, dim3(256), lds, s, grads, R, nn, ll, p); break;
         }
     } else {
         hipLaunchKernelGGL((avg_adapt_scalar<ADAM, AVG>), dim3(grid_for(n, 256)), dim3(256), 0, s,

@@ -558,7 +558,7 @@ def test_shard_count_invariance(net_name):
                                                         ("lenet", 1, 32, 10, 0.01, 0.9)])
 def test_free_running_trajectory_matches_oracle(net_name, R, Nb, steps, lr, mu):
     """Several steps with no state copied between the two sides (the analogue of the paper's
-    loss curves, Fig. 5): the GPU model and the oracle each start from the same initial weights
+    loss curves, Fig. 7): the GPU model and the oracle each start from the same initial weights
     and run `steps` steps on the same batches from their own state.  The per-step losses and
     the total weight change must agree to the parity tolerance; with fp32 compute the rounding
     differences that accumulate over the steps stay well inside it.  (bf16 steps are compared

@@ -241,6 +241,18 @@ int mtx_set_graph_replay(mtx_model* m, int enable);
  * on.  enable = 0 switches it off. */
 int mtx_set_overlap(mtx_model* m, int enable);
 
+/* Fused average + update of large fully connected layers (execution option, default on).  With
+ * the momentum rule (not Adam or AdaGrad) and without the layer-wise option, a fully connected
+ * layer of at least 2^20 parameters whose weight gradient has at least 512 output tiles and an
+ * unsplit reduction computes each output tile for all R shards in one block, writes the R shard
+ * rows as before, and averages and updates that tile's parameters (w, v, grad_avg) in the same
+ * launch, as Sec. III-D.2 reduces and updates one layer at a time; the average + update at the
+ * end of the step then covers only the other parameters.  Each element's arithmetic and order
+ * are those of mtx_sgd_update (the R stored fp32 values added in ascending r, divided by R, then
+ * the momentum rule), so the results are bit-identical either way.  enable = 0 switches it off.
+ * Returns MTX_EINVAL for a NULL model. */
+int mtx_set_fused_update(mtx_model* m, int enable);
+
 /* Layer-wise average + update (execution option, default off; Sec. III-D.2 reduces the
  * gradients one layer at a time, in layer order).  With it on, mtx_train_step averages and
  * updates each layer's parameters (its W and b slice of w, v, grad_avg) on a third stream of the
@@ -296,10 +308,11 @@ int mtx_get_timing(mtx_model* m, mtx_kernel_time* out, int capacity, int* count,
 
 /* Matrix-core launches of the last enqueued mtx_train_step (introspection for tests and
  * measurement; not part of the method).  One entry per launch of the tiled MFMA kernel, in
- * launch order: the launch site (as in mtx_get_timing: "fwd", "dgrad", "wgrad"), the layer, the
- * output tile (rows x columns of the GEMM C[p][q] = sum_k P[p][k] Q[q][k]), the reduction tile,
- * the number of reduction splits (> 1: a second kernel adds the fp32 partial sums), and flags:
- * 1 = interleaved scheduling order, 2 = an operand loaded straight into LDS.  Host only, does
+ * launch order: the launch site (as in mtx_get_timing: "fwd", "dgrad", "wgrad", "wgrad_update"),
+ * the layer, the output tile (rows x columns of the GEMM C[p][q] = sum_k P[p][k] Q[q][k]), the
+ * reduction tile, the number of reduction splits (> 1: a second kernel adds the fp32 partial
+ * sums), and flags: 1 = interleaved scheduling order, 2 = an operand loaded straight into LDS,
+ * 4 = the weight gradient fused with the average + update (mtx_set_fused_update).  Host only, does
  * not synchronise; fills up to `capacity` entries and sets *count to the number of launches. */
 typedef struct {
     char site[32];

@@ -616,6 +616,46 @@ template <class Op, class = void> struct Interleave : std::false_type {};
 template <class Op>
 struct Interleave<Op, std::void_t<decltype(Op::INTERLEAVE)>> : std::bool_constant<Op::INTERLEAVE> {};
 
+// An operation that declares FUSE_UPDATE = true (the fully connected weight gradient fused with
+// the average + update) is launched with one block per output tile for all R shards: the block
+// computes and stores the shards' tiles in ascending r, keeps their running fp32 sum, and then
+// averages and updates the tile's parameters itself.
+template <class Op, class = void> struct FuseUpdate : std::false_type {};
+template <class Op>
+struct FuseUpdate<Op, std::void_t<decltype(Op::FUSE_UPDATE)>> : std::bool_constant<Op::FUSE_UPDATE> {};
+
+// Average + update of four consecutive parameters (16-byte aligned) or of one, with the same
+// arithmetic as the stand-alone average + update kernel: g = sum / R, v = mu * v + g (skipped
+// for plain SGD), w = w - lr * v, each a single fp32 rounding.
+__device__ __forceinline__ void fused_update4(const GemmArgs& a, long long idx, f32x4 sum)
+{
+    const float fr = (float)a.R;
+    f32x4 g = {sum[0] / fr, sum[1] / fr, sum[2] / fr, sum[3] / fr};
+    f32x4 w = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.upd_w + idx));
+    __builtin_nontemporal_store(g, reinterpret_cast<f32x4*>(a.upd_avg + idx));
+    if (a.upd_v) {
+        f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.upd_v + idx));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = fmaf(a.upd_mu, v[e], g[e]);
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(a.upd_v + idx));
+        g = v;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = fmaf(-a.upd_lr, g[e], w[e]);
+    __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(a.upd_w + idx));
+}
+__device__ __forceinline__ void fused_update1(const GemmArgs& a, long long idx, float sum)
+{
+    float g = sum / (float)a.R;
+    a.upd_avg[idx] = g;
+    if (a.upd_v) {
+        const float vn = fmaf(a.upd_mu, a.upd_v[idx], g);
+        a.upd_v[idx] = vn;
+        g = vn;
+    }
+    a.upd_w[idx] = fmaf(-a.upd_lr, g, a.upd_w[idx]);
+}
+
 template <class Op, int FP, int FQ, int BK, int PK, int QK, bool SCHED = false>
 __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 {
@@ -628,116 +668,216 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     typedef typename TP::L LP;
     typedef typename TQ::L LQ;
     static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
+    constexpr bool FUSE = FuseUpdate<Op>::value;
+    static_assert(!(FUSE && Op::TAB), "a fused update takes no index table");
+    // the staged row store: output rows q contiguous along p, both operand tiles at least 8 KB
+    constexpr bool STAGED = RowStore<Op>::value && FP == 4 && FQ == 4 &&
+                            TP::ELEMS * sizeof(T) >= 8192 && TQ::ELEMS * sizeof(T) >= 8192;
 
     __shared__ __attribute__((aligned(16))) T sP[TP::ELEMS];
     __shared__ __attribute__((aligned(16))) T sQ[TQ::ELEMS];
     extern __shared__ TabEnt tab[];  // sized at launch
 
     const TileId tile = xcd_tile<Op::SHARE_Q>();
-    Ctx c;
-    decode_z(a, c, tile.bz);
-    const int p0 = tile.by * BP, q0 = tile.bx * BQ;
-    const int tid = threadIdx.x;
+    const bool split = a.splits > 1;
 
-    if constexpr (Op::TAB) {
-        // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
-        constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
-        const int n = a.kchunk / TS;
-        for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
-        c.tab = tab;
-        __syncthreads();
-    }
+    f32x4 acc[FP][FQ], sum[FUSE ? FP : 1][FUSE ? FQ : 1];
+    const int nrep = FUSE ? a.R : 1;
+    for (int rep = 0; rep < nrep; ++rep) {
+        // With several shards per block the index arithmetic below is made to depend on the
+        // shard through an opaque zero, so that the compiler recomputes it per shard instead of
+        // holding every address of the tile in registers across the loop (308 registers against
+        // 152, one wave per SIMD).
+        int oz = 0;
+        if constexpr (FUSE) asm volatile("s_mov_b32 %0, 0" : "=s"(oz));
+        const int p0 = tile.by * BP + oz, q0 = tile.bx * BQ + oz;
+        const int tid = threadIdx.x + oz;
+        const int wave = tid >> 6, lane = tid & 63;
+        const int wp = wave >> 1, wq = wave & 1;
+        const int lr = lane & 15, lg = lane >> 4;
+        // first p of this wave's rows, and whether the wave may use the staged row store
+        const int pw = p0 + wp * 16 * FP;
+        bool staged_ok = false;
+        if constexpr (STAGED) staged_ok = !split && a.vec_out && pw + 16 * FP <= Op::row_len(a);
+        float* st = nullptr;  // this wave's 4 KB of staging space (the operand tiles, after the loop)
+        if constexpr (STAGED)
+            st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
+                 (wave & 1) * 1024;
+        Ctx c;
+        decode_z(a, c, FUSE ? rep : tile.bz);
 
-    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
-    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
-    Loader<Op, true, PK, BP, BK> lp;
-    Loader<Op, false, QK, BQ, BK> lq;
-    lp.init(a, c, tid, p0);
-    lq.init(a, c, tid, q0);
-
-    const int wave = tid >> 6, lane = tid & 63;
-    const int wp = wave >> 1, wq = wave & 1;
-    const int lr = lane & 15, lg = lane >> 4;
-
-    f32x4 acc[FP][FQ];
-#pragma unroll
-    for (int i = 0; i < FP; ++i)
-#pragma unroll
-        for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    int k0 = c.kbeg;
-    if (k0 < c.kend) {
-        lp.load(a, bufP, c, tid, p0, k0);
-        lq.load(a, bufQ, c, tid, q0, k0);
-    }
-    for (; k0 < c.kend; k0 += BK) {
-        lp.stage(sP, tid);
-        lq.stage(sQ, tid);
-        __syncthreads();
-        if (k0 + BK < c.kend) {
-            lp.load(a, bufP, c, tid, p0, k0 + BK);
-            lq.load(a, bufQ, c, tid, q0, k0 + BK);
+        if constexpr (Op::TAB) {
+            // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
+            constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+            const int n = a.kchunk / TS;
+            for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
+            c.tab = tab;
+            __syncthreads();
         }
+
+        const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+        const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
+        Loader<Op, true, PK, BP, BK> lp;
+        Loader<Op, false, QK, BQ, BK> lq;
+        lp.init(a, c, tid, p0);
+        lq.init(a, c, tid, q0);
+
 #pragma unroll
-        for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
-            typename M::frag fa[FP], fb[FQ];
+        for (int i = 0; i < FP; ++i)
 #pragma unroll
-            for (int i = 0; i < FP; ++i)
-                fa[i] = LP::template frag<typename M::frag>(sP, wp * 16 * FP + i * 16, lr, lg,
-                                                            kc, M::KSTEP);
-#pragma unroll
-            for (int j = 0; j < FQ; ++j)
-                fb[j] = LQ::template frag<typename M::frag>(sQ, wq * 16 * FQ + j * 16, lr, lg,
-                                                            kc, M::KSTEP);
-#pragma unroll
-            for (int i = 0; i < FP; ++i)
-#pragma unroll
-                for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+            for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        int k0 = c.kbeg;
+        if (k0 < c.kend) {
+            lp.load(a, bufP, c, tid, p0, k0);
+            lq.load(a, bufQ, c, tid, q0, k0);
         }
-        if constexpr (SCHED) {
-            // Scheduling order: the first k chunk's fragment reads, then one fragment read of a
-            // later chunk and one global load after each MFMA, so that their latencies overlap
-            // the MFMAs instead of being waited for in clusters (measured: the bf16 convolution
-            // weight gradients, whose operands both come through k-major tiles, run 10-25%
-            // faster; forward and data-gradient kernels, and the output-bound fully connected
-            // weight gradients, run slower with it).
-            constexpr int NM = FP * FQ * (BK / M::KSTEP);
-            __builtin_amdgcn_sched_group_barrier(0x100, FP + FQ, 0);  // LDS reads
+        for (; k0 < c.kend; k0 += BK) {
+            lp.stage(sP, tid);
+            lq.stage(sQ, tid);
+            __syncthreads();
+            if (k0 + BK < c.kend) {
+                lp.load(a, bufP, c, tid, p0, k0 + BK);
+                lq.load(a, bufQ, c, tid, q0, k0 + BK);
+            }
 #pragma unroll
-            for (int m = 0; m < NM; ++m) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+            for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
+                typename M::frag fa[FP], fb[FQ];
+#pragma unroll
+                for (int i = 0; i < FP; ++i)
+                    fa[i] = LP::template frag<typename M::frag>(sP, wp * 16 * FP + i * 16, lr, lg,
+                                                                kc, M::KSTEP);
+#pragma unroll
+                for (int j = 0; j < FQ; ++j)
+                    fb[j] = LQ::template frag<typename M::frag>(sQ, wq * 16 * FQ + j * 16, lr, lg,
+                                                                kc, M::KSTEP);
+#pragma unroll
+                for (int i = 0; i < FP; ++i)
+#pragma unroll
+                    for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+            }
+            if constexpr (SCHED) {
+                // Scheduling order: the first k chunk's fragment reads, then one fragment read of
+                // a later chunk and one global load after each MFMA, so that their latencies
+                // overlap the MFMAs instead of being waited for in clusters (measured: the bf16
+                // convolution weight gradients, whose operands both come through k-major tiles,
+                // run 10-25% faster; forward and data-gradient kernels, and the output-bound fully
+                // connected weight gradients, run slower with it).
+                constexpr int NM = FP * FQ * (BK / M::KSTEP);
+                __builtin_amdgcn_sched_group_barrier(0x100, FP + FQ, 0);  // LDS reads
+#pragma unroll
+                for (int m = 0; m < NM; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+                    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+                }
+            }
+            __syncthreads();
+        }
+
+        bool stored = false;
+        if constexpr (STAGED) {
+            if (staged_ok) {
+                stored = true;
+                // Output rows q of the operation are contiguous along p (the fully connected weight
+                // gradient: one row per output unit).  A wave whose 64 p are all inside the rows
+                // stages each 16-row slice of its tile in LDS (4 KB: 16 rows x 16 chunks of 16
+                // bytes, chunk c of row r at slot c ^ r) and writes it back as 4 rows x 256
+                // contiguous bytes per store instruction instead of 16 rows x 64 bytes, nontemporal
+                // (only the average + update at the end of the step reads the rows again, and not
+                // even it when the update is fused).
+                // Measured on the AlexNet step: 3.57 ms with the fragment stores, 3.38 ms staged,
+                // 3.25 ms staged and nontemporal.  The main loop ended with a barrier, so the operand
+                // tiles are free; waves 0, 1 use sP, waves 2, 3 use sQ.
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) {
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+                    for (int i = 0; i < FP; ++i)  // row lr, chunk i * 4 + lg
+                        *reinterpret_cast<f32x4*>(st + lr * 64 + (((i * 4 + lg) ^ lr) << 2)) =
+                            acc[i][j];
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+                    for (int it = 0; it < 4; ++it) {
+                        const int r = it * 4 + (lane >> 4), ch = lane & 15;
+                        const f32x4 v = *reinterpret_cast<const f32x4*>(st + r * 64 + ((ch ^ r) << 2));
+                        const int q = q0 + wq * 16 * FQ + j * 16 + r;
+                        if (q < a.Qdim)
+                            __builtin_nontemporal_store(
+                                v, reinterpret_cast<f32x4*>(Op::row_out(a, c, q) + pw + ch * 4));
+                    }
+                }
             }
         }
-        __syncthreads();
+        if (!stored) {
+            float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
+#pragma unroll
+            for (int i = 0; i < FP; ++i) {
+                const int p = pw + i * 16 + lg * 4;
+                if (p >= a.Pdim) continue;
+                const int np = min(4, a.Pdim - p);
+                if (split) {
+#pragma unroll
+                    for (int j = 0; j < FQ; ++j) {
+                        const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                        if (q >= a.Qdim) continue;
+                        // partial sums are stored [z][q][p]
+                        float* o = part + (long long)q * a.Pdim + p;
+                        if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
+                        else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
+                    }
+                } else {
+                    const f32x4 rb = row_bias<Op>(a, c, p, np);
+#pragma unroll
+                    for (int j = 0; j < FQ; ++j) {
+                        const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                        if (q >= a.Qdim) continue;
+                        // without a bias the stored value is the sum itself (no 0 added, which
+                        // would turn -0 into +0: a fused update sums exactly what is stored)
+                        Op::store4(a, c, p, q, Op::HAS_BIAS ? acc[i][j] + rb : acc[i][j], np);
+                    }
+                }
+            }
+        }
+        if constexpr (FUSE) {
+            // running sum of the stored shard values in ascending r, as the stand-alone average
+            // adds the gradient rows
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) sum[i][j] = rep == 0 ? acc[i][j] : sum[i][j] + acc[i][j];
+            __syncthreads();  // the staging space is the next shard's operand tiles
+        }
     }
 
-    const bool split = a.splits > 1;
-    if constexpr (RowStore<Op>::value && FP == 4 && FQ == 4 &&
-                  TP::ELEMS * sizeof(T) >= 8192 && TQ::ELEMS * sizeof(T) >= 8192) {
-        // Output rows q of the operation are contiguous along p (the fully connected weight
-        // gradient: one row per output unit).  A wave whose 64 p are all inside the rows stages
-        // each 16-row slice of its tile in LDS (4 KB: 16 rows x 16 chunks of 16 bytes, chunk c of
-        // row r at slot c ^ r) and writes it back as 4 rows x 256 contiguous bytes per store
-        // instruction instead of 16 rows x 64 bytes, nontemporal (the rows are read again only
-        // by the average + update at the end of the step).  Measured on the AlexNet step: 3.57 ms
-        // with the fragment stores, 3.38 ms staged, 3.25 ms staged and nontemporal.  The main
-        // loop ended with a barrier, so the operand tiles are free; waves 0, 1 use sP, waves 2, 3
-        // use sQ.
+    if constexpr (FUSE) {
+        const int p0 = tile.by * BP, q0 = tile.bx * BQ;
+        const int tid = threadIdx.x;
+        const int wave = tid >> 6, lane = tid & 63;
+        const int wp = wave >> 1, wq = wave & 1;
+        const int lr = lane & 15, lg = lane >> 4;
         const int pw = p0 + wp * 16 * FP;
-        if (!split && a.vec_out && pw + 16 * FP <= Op::row_len(a)) {
-            float* st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
-                        (wave & 1) * 1024;
+        bool staged_ok = false;
+        if constexpr (STAGED) staged_ok = !split && a.vec_out && pw + 16 * FP <= Op::row_len(a);
+        float* st = nullptr;
+        if constexpr (STAGED)
+            st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
+                 (wave & 1) * 1024;
+        if (staged_ok) {
+            // the same staging, then 16-byte runs of one row: parameters out_off + q * C + p
 #pragma unroll
             for (int j = 0; j < FQ; ++j) {
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                 __builtin_amdgcn_wave_barrier();
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-                for (int i = 0; i < FP; ++i)  // row lr, chunk i * 4 + lg
+                for (int i = 0; i < FP; ++i)
                     *reinterpret_cast<f32x4*>(st + lr * 64 + (((i * 4 + lg) ^ lr) << 2)) =
-                        acc[i][j];
+                        sum[i][j];
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                 __builtin_amdgcn_wave_barrier();
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -747,36 +887,23 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
                     const f32x4 v = *reinterpret_cast<const f32x4*>(st + r * 64 + ((ch ^ r) << 2));
                     const int q = q0 + wq * 16 * FQ + j * 16 + r;
                     if (q < a.Qdim)
-                        __builtin_nontemporal_store(
-                            v, reinterpret_cast<f32x4*>(Op::row_out(a, c, q) + pw + ch * 4));
+                        fused_update4(a, a.out_off + (long long)q * Op::row_len(a) + pw + ch * 4, v);
                 }
             }
-            return;
-        }
-    }
-    float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
-#pragma unroll
-    for (int i = 0; i < FP; ++i) {
-        const int p = p0 + wp * 16 * FP + i * 16 + lg * 4;
-        if (p >= a.Pdim) continue;
-        const int np = min(4, a.Pdim - p);
-        if (split) {
-#pragma unroll
-            for (int j = 0; j < FQ; ++j) {
-                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-                if (q >= a.Qdim) continue;
-                // partial sums are stored [z][q][p]
-                float* o = part + (long long)q * a.Pdim + p;
-                if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
-                else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
-            }
         } else {
-            const f32x4 rb = row_bias<Op>(a, c, p, np);
 #pragma unroll
-            for (int j = 0; j < FQ; ++j) {
-                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-                if (q >= a.Qdim) continue;
-                Op::store4(a, c, p, q, acc[i][j] + rb, np);
+            for (int i = 0; i < FP; ++i) {
+                const int p = pw + i * 16 + lg * 4;
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) {
+                    const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                    if (q >= a.Qdim) continue;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const long long idx = Op::param_index(a, p + e, q);
+                        if (idx >= 0) fused_update1(a, idx, sum[i][j][e]);
+                    }
+                }
             }
         }
     }
@@ -983,7 +1110,7 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
         hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK, true>), grid, dim3(256), shm, s,
                            a);
     } else {
-        note_gemm(FP, FQ, BK, a.splits, 0);
+        note_gemm(FP, FQ, BK, a.splits, FuseUpdate<Op>::value ? kGemmFusedUpdate : 0);
         hipLaunchKernelGGL((igemm_kernel<Op, FP, FQ, BK, PK, QK>), grid, dim3(256), shm, s, a);
     }
     hipError_t e = hipGetLastError();

@@ -657,6 +657,20 @@ template <typename T> struct FcWgrad {
             else g[row + p + i] = acc[i];
         }
     }
+    // parameter of output (p, q) in a gradient row (W[q][p], or b[q] for the bias row), -1 outside
+    __device__ static long long param_index(const GemmArgs& a, int p, int q)
+    {
+        if (p < a.C) return a.out_off + (long long)q * a.C + p;
+        return p == a.C ? a.bias_off + q : -1;
+    }
+};
+
+// The same weight gradient for all R shards of one output tile per block, followed by the
+// average of the R stored values and the optimizer step of the tile's parameters (Sec. III-D.2:
+// each layer's reduction and update; the momentum rule of the stand-alone kernel, element by
+// element the same arithmetic).
+template <typename T> struct FcWgradUpd : FcWgrad<T> {
+    static constexpr bool FUSE_UPDATE = true;
 };
 
 }  // namespace mtx

@@ -64,6 +64,12 @@ struct GemmArgs {
     unsigned a_bytes;      // size of tensor a in bytes (buffer-load range)
     unsigned b_bytes;      // size of tensor b in bytes
     int Hp, Wp, Cp, RUN;   // first-layer convolution over a padded input (see conv_fwd_run)
+    // weight gradient fused with the average + update (FcWgradUpd): the model's w, v (null
+    // for plain SGD) and grad_avg, indexed like a gradient row, and the step's lr and momentum
+    float* upd_w;
+    float* upd_v;
+    float* upd_avg;
+    float upd_lr, upd_mu;
     FastDiv fd_ohw, fd_ow, fd_hw, fd_w, fd_c;
     FastDiv fd_run;
     FastDiv fd_kcg, fd_cg, fd_kog, fd_og;  // K*cg, cg, K*og, og (index tables)
@@ -131,15 +137,24 @@ hipError_t fc_dgrad(Dt dt, int B, int IN, int OUT, const void* dy, const void* w
 hipError_t fc_wgrad(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
                     const void* x, const void* dy, float* grads, long long ld, long long w_off,
                     long long b_off, float* partial, hipStream_t s);
+// The fully connected weight gradient of all R shards fused with the average + update of the
+// layer's parameters (w, v: null or ignored when mu == 0, avg; indexed like a gradient row);
+// fc_wgrad_update_ok tells whether the layer's plan allows it (an unsplit reduction).
+bool fc_wgrad_update_ok(Dt dt, int Nb, int R, int IN, int OUT);
+hipError_t fc_wgrad_update(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,
+                           const void* x, const void* dy, float* grads, long long ld,
+                           long long w_off, long long b_off, float* w, float* v, float* avg,
+                           float lr, float mu, hipStream_t s);
 
 // Kernel timing (api.hip): a launcher that enqueues several kernels for one operation calls
 // this between them; with timing on, the kernels before and after are timed as separate sites
 // (the later one named <site>_<part>).  No effect otherwise.
 void timing_split(hipStream_t s, const char* part);
 // Launch record (api.hip): every matrix launch reports its shape to the model whose step is
-// being enqueued (mtx_get_launches).  flags: kGemmInterleaved, kGemmDirectLds.
+// being enqueued (mtx_get_launches).  flags: kGemmInterleaved, kGemmDirectLds, kGemmFusedUpdate.
 constexpr int kGemmInterleaved = 1;  // the interleaved scheduling order of igemm_kernel
 constexpr int kGemmDirectLds = 2;    // an operand loaded straight into LDS (igemm_direct_kernel)
+constexpr int kGemmFusedUpdate = 4;  // the weight gradient fused with the average + update
 void note_gemm(int fp, int fq, int bk, int splits, int flags);
 
 // elementwise.hip

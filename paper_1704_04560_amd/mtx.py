@@ -25,7 +25,7 @@ EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_init_model_static", "mtx_tr
            "mtx_sgd_update", "mtx_adam_update", "mtx_adagrad_update", "mtx_get_params",
            "mtx_set_params", "mtx_get_layer_output", "mtx_set_optimizer",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
-           "mtx_set_layerwise_update", "mtx_set_timing",
+           "mtx_set_layerwise_update", "mtx_set_fused_update", "mtx_set_timing",
            "mtx_get_timing", "mtx_get_launches", "mtx_free_model", "mtx_last_error")
 
 
@@ -60,7 +60,7 @@ class mtx_launch_info(C.Structure):
                 ("flags", C.c_int)]
 
 
-MTX_GEMM_INTERLEAVED, MTX_GEMM_DIRECT_LDS = 1, 2
+MTX_GEMM_INTERLEAVED, MTX_GEMM_DIRECT_LDS, MTX_GEMM_FUSED_UPDATE = 1, 2, 4
 
 
 class mtx_buffers(C.Structure):
@@ -99,6 +99,7 @@ def lib() -> C.CDLL:
             "mtx_set_graph_replay": (i32, [vp, i32]),
             "mtx_set_optimizer": (i32, [vp, i32, f32, f32, f32, vp]),
             "mtx_set_layerwise_update": (i32, [vp, i32]),
+            "mtx_set_fused_update": (i32, [vp, i32]),
             "mtx_set_overlap": (i32, [vp, i32]),
             "mtx_set_timing": (i32, [vp, i32]),
             "mtx_get_timing": (i32, [vp, C.POINTER(mtx_kernel_time), i32, C.POINTER(i32), i32]),
@@ -232,6 +233,10 @@ def mtx_set_overlap(handle, enable: bool):
 
 def mtx_set_layerwise_update(handle, enable: bool):
     _check(lib().mtx_set_layerwise_update(handle, 1 if enable else 0))
+
+
+def mtx_set_fused_update(handle, enable: bool):
+    _check(lib().mtx_set_fused_update(handle, 1 if enable else 0))
 
 
 def mtx_set_timing(handle, enable: bool):

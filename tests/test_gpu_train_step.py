@@ -482,6 +482,59 @@ def test_overlapped_weight_gradients_match_one_stream(name, layerwise):
     b.close()
 
 
+def _wide_fc(dtype):
+    """Two large fully connected layers (4.2 M and 1.05 M parameters) before a small classifier:
+    the large ones carry their own average + update, the classifier's parameters come last."""
+    return wl.Net("wide-fc", (2048, 1, 1), (wl.fc(2048, relu=True), wl.fc(512, relu=True),
+                                           wl.fc(10)), dtype, "normal")
+
+
+@pytest.mark.parametrize("name,R,Nb,mu", [("wide-f32", 2, 8, 0.9), ("wide-bf16", 4, 4, 0.0),
+                                           ("alexnet", 2, 2, 0.9), ("alexnet", 8, 1, 0.0),
+                                           ("lenet", 4, 16, 0.9)])
+def test_fused_fc_update_is_bit_identical(name, R, Nb, mu):
+    """Large fully connected layers average and update their own parameters in their
+    weight-gradient launch (all R shards of a tile in one block); the shard rows, the average,
+    the velocity and the weights are bit-identical to the stand-alone average + update over all
+    parameters, with momentum and with plain SGD, over direct and graph-replayed steps.  The
+    launch record shows which launches were fused: layers of at least 2^20 parameters only."""
+    net = {"wide-f32": _wide_fc(wl.F32), "wide-bf16": _wide_fc(wl.BF16), "alexnet": wl.ALEXNET,
+           "lenet": wl.LENET}[name]
+    expect = {"wide-f32": [0, 1], "wide-bf16": [0, 1], "alexnet": [8, 9, 10], "lenet": []}[name]
+    layers = wl.layer_tuples(net)
+    _say(f"[case] fused fc update {name} R={R} Nb={Nb} mu={mu}")
+    a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=6)
+    b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=6)
+    mtx.mtx_set_fused_update(b.handle, False)
+    mtx.mtx_set_graph_replay(a.handle, True)
+    x, y = wl.make_batch(net, R * Nb, seed=6)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    v0 = a.get_params()[1].copy()
+    for step in range(3):
+        if step == 2:
+            mtx.mtx_set_graph_replay(a.handle, False)
+        a.train_step(xd, yd, 0.01, mu)
+        b.train_step(xd, yd, 0.01, mu)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.grads_host().view(np.uint32), b.grads_host().view(np.uint32)), step
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
+        ga, gb = a.grad_avg.cpu().numpy(), b.grad_avg.cpu().numpy()
+        assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
+    if mu == 0.0:  # plain SGD leaves v alone
+        assert np.array_equal(a.get_params()[1].view(np.uint32), v0.view(np.uint32))
+    fused = [l for l in mtx.mtx_get_launches(a.handle) if l["flags"] & mtx.MTX_GEMM_FUSED_UPDATE]
+    plain = [l for l in mtx.mtx_get_launches(b.handle) if l["flags"] & mtx.MTX_GEMM_FUSED_UPDATE]
+    _say("[launches] fused: " + ", ".join(f"{l['site']}:L{l['layer']}:{l['tile_rows']}x"
+                                          f"{l['tile_cols']}" for l in fused))
+    assert sorted(l["layer"] for l in fused) == expect and not plain
+    assert all(l["site"] == "wgrad_update" and l["splits"] == 1 for l in fused)
+    a.close()
+    b.close()
+
+
 def _layerwise(model):
     mtx.mtx_set_overlap(model.handle, True)
     mtx.mtx_set_layerwise_update(model.handle, True)

@@ -55,21 +55,24 @@ def geometry(net):
     return out
 
 
-def site_work(name, layer, geo, wkl, es):
+def site_work(name, layer, geo, wkl, es, fused=()):
     """Algorithmic work of one launch of a step's launch site: ("alu", flops) for the direct
     first-convolution kernels (fp32 vector fused multiply-adds), ("hbm", bytes) for the
     memory-bound ones (each tensor read once and written once), (None, 0) when not modelled.
     A matrix launch is ("mfma", flops) (2 x multiply-adds of the convolution / product) when its
     flops take longer at the MFMA peak than its algorithmic bytes at the HBM peak, else
     ("hbm", bytes): operands read once, the output written once (a data gradient also reads
-    the ReLU mask; a weight gradient writes R fp32 gradient rows)."""
-    return _site_work(name, layer, geo, wkl, es)[:2]
+    the ReLU mask; a weight gradient writes R fp32 gradient rows; a weight gradient fused with
+    the average + update, "wgrad_update", also reads w and v and writes the average, v and w).
+    "avg_update" is the whole step's stand-alone average + update over the parameters of the
+    layers not in `fused`."""
+    return _site_work(name, layer, geo, wkl, es, fused)[:2]
 
 
 def matrix_flops(name, layer, geo, wkl):
     """2 x multiply-adds of a matrix launch site (0 for the others)."""
     from paper_1704_04560_amd import workloads as wl
-    if layer < 0 or name not in ("fwd", "dgrad", "wgrad"):
+    if layer < 0 or name not in ("fwd", "dgrad", "wgrad", "wgrad_update"):
         return 0.0
     g = geo[layer]
     l = g["layer"]
@@ -83,7 +86,23 @@ def matrix_flops(name, layer, geo, wkl):
     return 0.0
 
 
-def _site_work(name, layer, geo, wkl, es):
+def layer_params(geo, layer):
+    """Parameters (W and b) of one layer."""
+    from paper_1704_04560_amd import workloads as wl
+    g = geo[layer]
+    l = g["layer"]
+    if l.kind == wl.CONV:
+        return g["oc"] * (g["c"] // l.groups) * l.k * l.k + g["oc"]
+    if l.kind == wl.FC:
+        return g["oc"] * g["c"] * g["h"] * g["w"] + g["oc"]
+    if l.kind == wl.ADDP:
+        return g["oc"] * geo[l.k]["oc"] + g["oc"]
+    if l.kind == wl.BN:
+        return 2 * g["c"]
+    return 0
+
+
+def _site_work(name, layer, geo, wkl, es, fused=()):
     from paper_1704_04560_amd import workloads as wl
     B, R, Nb = wkl.batch, wkl.shards, wkl.shard_batch
     if layer >= 0:
@@ -91,7 +110,7 @@ def _site_work(name, layer, geo, wkl, es):
         l = g["layer"]
         in_sz = B * g["c"] * g["h"] * g["w"]
         out_sz = B * g["oc"] * g["oh"] * g["ow"]
-        if name in ("fwd", "dgrad", "wgrad") and l.kind in (wl.CONV, wl.FC, wl.ADDP):
+        if name in ("fwd", "dgrad", "wgrad", "wgrad_update") and l.kind in (wl.CONV, wl.FC, wl.ADDP):
             flops = matrix_flops(name, layer, geo, wkl)
             if l.kind == wl.ADDP:
                 src = geo[l.k]
@@ -108,6 +127,8 @@ def _site_work(name, layer, geo, wkl, es):
                 nbytes = (out_sz + wn + (2 if mask else 1) * x_sz) * es
             else:
                 nbytes = (x_sz + out_sz) * es + R * (wn + g["oc"]) * 4
+                if name == "wgrad_update":  # w (and v) read, the average, v and w written
+                    nbytes += (wn + g["oc"]) * (20 if wkl.momentum != 0.0 else 12)
             peak = PEAK["bf16_TFLOPs"] if es == 2 else PEAK["f32_TFLOPs"]
             if flops / (peak * 1e12) >= nbytes / (PEAK["hbm_GBps"] * 1e9):
                 return "mfma", flops, flops
@@ -140,8 +161,9 @@ def _site_work(name, layer, geo, wkl, es):
             return "hbm", 5 * out_sz * es, 0.0
         return None, 0.0, 0.0
     P = wkl_params(wkl)
-    if name == "avg_update":
+    if name == "avg_update":  # the whole step's share (the caller divides by its launches)
         mom = wkl.momentum != 0.0
+        P -= sum(layer_params(geo, f) for f in fused)
         return "hbm", (R + (5 if mom else 3)) * 4 * P, 0.0
     if name == "prep_w":
         # every weight tensor is read once (fp32) and written once per layout it is prepared in
@@ -392,10 +414,14 @@ def measure(torch, mtx, wl, name, steps, warmup):
     es = 2 if net.dtype == wl.BF16 else 4
     geo = geometry(net)
     kernels = []
+    fused = sorted({layer for (sname, layer, launches, _) in sites
+                    if sname == "wgrad_update" and launches})
     for (sname, layer, launches, total) in sites:
         if launches == 0:
             continue
-        bound, work, mm = _site_work(sname, layer, geo, wkl, es)
+        bound, work, mm = _site_work(sname, layer, geo, wkl, es, fused)
+        if sname == "avg_update":  # launches per step: one per contiguous parameter range
+            work /= max(1, round(launches / steps))
         kernels.append(dict(name=sname, layer=layer, avg_ms=total / launches, bound=bound,
                             work=work, mm_flops=mm))
     peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
@@ -422,7 +448,7 @@ def measure(torch, mtx, wl, name, steps, warmup):
 
     mfma_ms = sum(k["avg_ms"] for k in kernels if k["mm_flops"])
     mfma_flops = sum(k["mm_flops"] for k in kernels if k["mm_flops"])
-    au = [k for k in kernels if k["name"] == "avg_update"][0]
+    au = [k for k in kernels if k["name"] == "avg_update"]
     return {
         "wkl": wkl,
         "value": round(wkl.batch / (ms * 1e-3), 1),
@@ -432,8 +458,11 @@ def measure(torch, mtx, wl, name, steps, warmup):
         "gemm_mfma": {"achieved_TFLOPs": round(mfma_flops / (mfma_ms * 1e-3) / 1e12, 3),
                       "peak_TFLOPs": peak_mm,
                       "frac": round(mfma_flops / (mfma_ms * 1e-3) / 1e12 / peak_mm, 4)},
-        "step_avg_update": {"GBps": round(au["work"] / (au["avg_ms"] * 1e-3) / 1e9, 1),
-                            "ms": round(au["avg_ms"], 5)},
+        "step_avg_update": ({"GBps": round(au[0]["work"] / (au[0]["avg_ms"] * 1e-3) / 1e9, 1),
+                             "ms": round(au[0]["avg_ms"], 5),
+                             "params": int(au[0]["work"] / (4 * (wkl.shards + (5 if wkl.momentum else 3))))}
+                            if au else None),
+        "fused_update_layers": fused,
         "kernel_ms_sum": round(sum(k["avg_ms"] for k in kernels), 5),
         "ms_per_step_with_kernel_events": round(ms_events, 5),
         "kernels": [{"name": k["name"], "layer": k["layer"], "ms": round(k["avg_ms"], 5)}

@@ -13,11 +13,11 @@ from paper_1704_04560_amd import workloads as wl
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _work(name, site, layer):
+def _work(name, site, layer, fused=()):
     wkl = wl.WORKLOADS[name]
     geo = bench.geometry(wkl.net)
     es = 2 if wkl.net.dtype == wl.BF16 else 4
-    return bench._site_work(site, layer, geo, wkl, es)
+    return bench._site_work(site, layer, geo, wkl, es, fused)
 
 
 def test_gradient_average_moves_r_rows_plus_weights_and_momentum():
@@ -43,6 +43,25 @@ def test_fully_connected_weight_gradient_is_bound_by_its_gradient_rows():
     assert bound == "hbm"
     assert mm == 2.0 * 256 * 9216 * 4096
     assert nbytes == (256 * 9216 + 256 * 4096) * 2 + wkl.shards * (9216 * 4096 + 4096) * 4
+
+
+def test_fused_weight_gradient_adds_the_update_traffic():
+    # FC6 fused with the average + update: w and v read, the average, v and w written
+    wkl = wl.WORKLOADS["alexnet"]
+    _, plain, _ = _work("alexnet", "wgrad", 8)
+    bound, fused, mm = _work("alexnet", "wgrad_update", 8)
+    assert bound == "hbm" and mm == 2.0 * 256 * 9216 * 4096
+    assert fused - plain == (9216 * 4096 + 4096) * 20
+
+
+def test_average_after_fused_layers_covers_the_rest():
+    # with the three fc layers fused, the stand-alone average + update moves only the
+    # convolutions' parameters (60,965,224 in all, 58,631,144 of them in the fc layers)
+    wkl = wl.WORKLOADS["alexnet"]
+    _, nbytes, _ = _work("alexnet", "avg_update", -1, fused=(8, 9, 10))
+    fc = (9216 * 4096 + 4096) + (4096 * 4096 + 4096) + (4096 * 1000 + 1000)
+    assert fc == 58631144
+    assert nbytes == (wkl.shards + 5) * 4 * (60965224 - fc)
 
 
 def test_one_by_one_convolution_data_gradient_is_memory_bound():

@@ -243,8 +243,9 @@ int mtx_set_overlap(mtx_model* m, int enable);
 
 /* Fused average + update of large fully connected layers (execution option, default on).  With
  * the momentum rule (not Adam or AdaGrad) and without the layer-wise option, a fully connected
- * layer of at least 2^20 parameters whose weight gradient has at least 512 output tiles and an
- * unsplit reduction computes each output tile for all R shards in one block, writes the R shard
+ * layer of at least 2^20 parameters whose weight gradient has at least 512 output tiles of
+ * 128 x 128 and an unsplit reduction computes each output tile for all R shards in one block,
+ * writes the R shard
  * rows as before, and averages and updates that tile's parameters (w, v, grad_avg) in the same
  * launch, as Sec. III-D.2 reduces and updates one layer at a time; the average + update at the
  * end of the step then covers only the other parameters.  Each element's arithmetic and order

@@ -683,6 +683,28 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 
     f32x4 acc[FP][FQ], sum[FUSE ? FP : 1][FUSE ? FQ : 1];
     const int nrep = FUSE ? a.R : 1;
+    Ctx c;
+    decode_z(a, c, FUSE ? 0 : tile.bz);
+    if constexpr (Op::TAB) {
+        // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
+        constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+        const int n = a.kchunk / TS;
+        for (int j = threadIdx.x; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
+        c.tab = tab;
+        __syncthreads();
+    }
+    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
+    // (a fused operation's loader state does not depend on the shard, only its loads do)
+    Loader<Op, true, PK, BP, BK> lp;
+    Loader<Op, false, QK, BQ, BK> lq;
+    lp.init(a, c, threadIdx.x, tile.by * BP);
+    lq.init(a, c, threadIdx.x, tile.bx * BQ);
+    int k0 = c.kbeg;
+    if (k0 < c.kend) {
+        lp.load(a, bufP, c, threadIdx.x, tile.by * BP, k0);
+        lq.load(a, bufQ, c, threadIdx.x, tile.bx * BQ, k0);
+    }
     for (int rep = 0; rep < nrep; ++rep) {
         // With several shards per block the index arithmetic below is made to depend on the
         // shard through an opaque zero, so that the compiler recomputes it per shard instead of
@@ -703,35 +725,16 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
         if constexpr (STAGED)
             st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
                  (wave & 1) * 1024;
-        Ctx c;
-        decode_z(a, c, FUSE ? rep : tile.bz);
-
-        if constexpr (Op::TAB) {
-            // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
-            constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
-            const int n = a.kchunk / TS;
-            for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
-            c.tab = tab;
-            __syncthreads();
-        }
-
-        const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
-        const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
-        Loader<Op, true, PK, BP, BK> lp;
-        Loader<Op, false, QK, BQ, BK> lq;
-        lp.init(a, c, tid, p0);
-        lq.init(a, c, tid, q0);
+        // the next shard's context: its first operand tiles are loaded during this shard's last
+        // products and stores
+        Ctx cn = c;
+        if (FUSE && rep + 1 < nrep) decode_z(a, cn, rep + 1);
 
 #pragma unroll
         for (int i = 0; i < FP; ++i)
 #pragma unroll
             for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        int k0 = c.kbeg;
-        if (k0 < c.kend) {
-            lp.load(a, bufP, c, tid, p0, k0);
-            lq.load(a, bufQ, c, tid, q0, k0);
-        }
         for (; k0 < c.kend; k0 += BK) {
             lp.stage(sP, tid);
             lq.stage(sQ, tid);
@@ -739,6 +742,9 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
             if (k0 + BK < c.kend) {
                 lp.load(a, bufP, c, tid, p0, k0 + BK);
                 lq.load(a, bufQ, c, tid, q0, k0 + BK);
+            } else if (FUSE && rep + 1 < nrep && cn.kbeg < cn.kend) {
+                lp.load(a, bufP, cn, tid, p0, cn.kbeg);
+                lq.load(a, bufQ, cn, tid, q0, cn.kbeg);
             }
 #pragma unroll
             for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
@@ -851,6 +857,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
 #pragma unroll
                 for (int j = 0; j < FQ; ++j) sum[i][j] = rep == 0 ? acc[i][j] : sum[i][j] + acc[i][j];
             __syncthreads();  // the staging space is the next shard's operand tiles
+            c = cn;
+            k0 = c.kbeg;
         }
     }
 

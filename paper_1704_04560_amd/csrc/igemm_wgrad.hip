@@ -101,15 +101,18 @@ static GemmDims fc_wgrad_update_dims(int dt, int Nb, int R, int IN, int OUT)
 
 bool fc_wgrad_update_ok(Dt dt, int Nb, int R, int IN, int OUT)
 {
-    // Only for layers large enough to be bound by their gradient rows (at least 2^20 parameters)
-    // and to keep two blocks per compute unit busy with one block per tile (measured: LeNet's
-    // 400 K-parameter fc layer fused took the step from 0.154 to 0.174 ms; AlexNet's fc layers
-    // fused took it from 3.21 to 3.09 ms).
+    // Only for layers large enough to be bound by their gradient rows (at least 2^20 parameters),
+    // planned with 128 x 128 tiles (the staged row store) and enough of them to keep two blocks
+    // per compute unit busy with one block per tile.  Measured: LeNet's 400 K-parameter fc layer
+    // fused took the step from 0.154 to 0.174 ms; AlexNet's FC8 (4 M parameters, 64 x 128 tiles)
+    // 0.105 ms fused against 0.065 ms for its weight gradient and share of the average; FC6 and
+    // FC7 fused took the step from 3.21 to 3.10 ms.
     const GemmDims d = fc_wgrad_update_dims(dt, Nb, R, IN, OUT);
     const GemmPlan g = plan_for(dt, d);
     const long long tiles = (long long)((d.P + 32 * g.FP - 1) / (32 * g.FP)) *
                             ((d.Q + 32 * g.FQ - 1) / (32 * g.FQ));
-    return g.splits == 1 && R >= 1 && tiles >= 512 && (long long)(IN + 1) * OUT >= (1ll << 20);
+    return g.splits == 1 && g.FP == 4 && g.FQ == 4 && R >= 1 && tiles >= 512 &&
+           (long long)(IN + 1) * OUT >= (1ll << 20);
 }
 
 hipError_t fc_wgrad_update(Dt dt, int Nb, int R, int IN, int OUT, int perm_c, int perm_hw,

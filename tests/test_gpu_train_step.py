@@ -483,9 +483,10 @@ def test_overlapped_weight_gradients_match_one_stream(name, layerwise):
 
 
 def _wide_fc(dtype):
-    """Two large fully connected layers (4.2 M and 1.05 M parameters) before a small classifier:
-    the large ones carry their own average + update, the classifier's parameters come last."""
-    return wl.Net("wide-fc", (2048, 1, 1), (wl.fc(2048, relu=True), wl.fc(512, relu=True),
+    """A large fully connected layer (8.4 M parameters, 528 tiles of 128 x 128) that carries
+    its own average + update, then a 1.05 M-parameter one (too few 128 x 128 tiles: not fused)
+    and a small classifier, whose parameters the stand-alone average + update covers."""
+    return wl.Net("wide-fc", (4096, 1, 1), (wl.fc(2048, relu=True), wl.fc(512, relu=True),
                                            wl.fc(10)), dtype, "normal")
 
 
@@ -497,10 +498,11 @@ def test_fused_fc_update_is_bit_identical(name, R, Nb, mu):
     weight-gradient launch (all R shards of a tile in one block); the shard rows, the average,
     the velocity and the weights are bit-identical to the stand-alone average + update over all
     parameters, with momentum and with plain SGD, over direct and graph-replayed steps.  The
-    launch record shows which launches were fused: layers of at least 2^20 parameters only."""
+    launch record shows which launches were fused: layers of at least 2^20 parameters with at
+    least 512 tiles of 128 x 128 only."""
     net = {"wide-f32": _wide_fc(wl.F32), "wide-bf16": _wide_fc(wl.BF16), "alexnet": wl.ALEXNET,
            "lenet": wl.LENET}[name]
-    expect = {"wide-f32": [0, 1], "wide-bf16": [0, 1], "alexnet": [8, 9, 10], "lenet": []}[name]
+    expect = {"wide-f32": [0], "wide-bf16": [0], "alexnet": [8, 9], "lenet": []}[name]
     layers = wl.layer_tuples(net)
     _say(f"[case] fused fc update {name} R={R} Nb={Nb} mu={mu}")
     a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=6)

@@ -670,71 +670,168 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
     static_assert(BK % M::KSTEP == 0 && 256 % BK == 0, "BK");
     constexpr bool FUSE = FuseUpdate<Op>::value;
     static_assert(!(FUSE && Op::TAB), "a fused update takes no index table");
-    // the staged row store: output rows q contiguous along p, both operand tiles at least 8 KB
+    // the staged row store: output rows q contiguous along p, and 4 KB of staging per wave (the
+    // operand tiles after the main loop, or, fused, a region of its own)
     constexpr bool STAGED = RowStore<Op>::value && FP == 4 && FQ == 4 &&
-                            TP::ELEMS * sizeof(T) >= 8192 && TQ::ELEMS * sizeof(T) >= 8192;
+                            (FUSE || (TP::ELEMS * sizeof(T) >= 8192 && TQ::ELEMS * sizeof(T) >= 8192));
 
     __shared__ __attribute__((aligned(16))) T sP[TP::ELEMS];
     __shared__ __attribute__((aligned(16))) T sQ[TQ::ELEMS];
+    __shared__ __attribute__((aligned(16))) float stg[FUSE ? 4096 : 4];
     extern __shared__ TabEnt tab[];  // sized at launch
 
     const TileId tile = xcd_tile<Op::SHARE_Q>();
     const bool split = a.splits > 1;
 
-    f32x4 acc[FP][FQ], sum[FUSE ? FP : 1][FUSE ? FQ : 1];
-    const int nrep = FUSE ? a.R : 1;
-    Ctx c;
-    decode_z(a, c, FUSE ? 0 : tile.bz);
-    if constexpr (Op::TAB) {
-        // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
-        constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
-        const int n = a.kchunk / TS;
-        for (int j = threadIdx.x; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
-        c.tab = tab;
-        __syncthreads();
-    }
-    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
-    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
-    // (a fused operation's loader state does not depend on the shard, only its loads do)
-    Loader<Op, true, PK, BP, BK> lp;
-    Loader<Op, false, QK, BQ, BK> lq;
-    lp.init(a, c, threadIdx.x, tile.by * BP);
-    lq.init(a, c, threadIdx.x, tile.bx * BQ);
-    int k0 = c.kbeg;
-    if (k0 < c.kend) {
-        lp.load(a, bufP, c, threadIdx.x, tile.by * BP, k0);
-        lq.load(a, bufQ, c, threadIdx.x, tile.bx * BQ, k0);
-    }
-    for (int rep = 0; rep < nrep; ++rep) {
-        // With several shards per block the index arithmetic below is made to depend on the
-        // shard through an opaque zero, so that the compiler recomputes it per shard instead of
-        // holding every address of the tile in registers across the loop (308 registers against
-        // 152, one wave per SIMD).
-        int oz = 0;
-        if constexpr (FUSE) asm volatile("s_mov_b32 %0, 0" : "=s"(oz));
-        const int p0 = tile.by * BP + oz, q0 = tile.bx * BQ + oz;
-        const int tid = threadIdx.x + oz;
+    // products of one k tile from the operand tiles in LDS
+    auto products = [&](f32x4 (&acc)[FP][FQ], int wp, int wq, int lr, int lg) {
+#pragma unroll
+        for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
+            typename M::frag fa[FP], fb[FQ];
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+                fa[i] = LP::template frag<typename M::frag>(sP, wp * 16 * FP + i * 16, lr, lg, kc,
+                                                            M::KSTEP);
+#pragma unroll
+            for (int j = 0; j < FQ; ++j)
+                fb[j] = LQ::template frag<typename M::frag>(sQ, wq * 16 * FQ + j * 16, lr, lg, kc,
+                                                            M::KSTEP);
+#pragma unroll
+            for (int i = 0; i < FP; ++i)
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
+        }
+        if constexpr (SCHED) {
+            // Scheduling order: the first k chunk's fragment reads, then one fragment read of a
+            // later chunk and one global load after each MFMA, so that their latencies overlap
+            // the MFMAs instead of being waited for in clusters (measured: the bf16 convolution
+            // weight gradients, whose operands both come through k-major tiles, run 10-25%
+            // faster; forward and data-gradient kernels, and the output-bound fully connected
+            // weight gradients, run slower with it).
+            constexpr int NM = FP * FQ * (BK / M::KSTEP);
+            __builtin_amdgcn_sched_group_barrier(0x100, FP + FQ, 0);  // LDS reads
+#pragma unroll
+            for (int m = 0; m < NM; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+            }
+        }
+    };
+
+    // Output rows q of the operation are contiguous along p (the fully connected weight
+    // gradient: one row per output unit).  A wave whose 64 p are all inside the rows stages each
+    // 16-row slice of its tile in LDS (4 KB: 16 rows x 16 chunks of 16 bytes, chunk c of row r at
+    // slot c ^ r) and hands it back as 4 rows x 256 contiguous bytes per instruction instead of
+    // 16 rows x 64 bytes: emit(q, p, v) gets row q's 4 values from p on.
+    auto staged_rows = [&](const f32x4 (&val)[FP][FQ], float* st, int pw, int q0, int wq,
+                           int lane, auto&& emit) {
+        const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+        for (int j = 0; j < FQ; ++j) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+            for (int i = 0; i < FP; ++i)  // row lr, chunk i * 4 + lg
+                *reinterpret_cast<f32x4*>(st + lr * 64 + (((i * 4 + lg) ^ lr) << 2)) = val[i][j];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+                const int r = it * 4 + (lane >> 4), ch = lane & 15;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(st + r * 64 + ((ch ^ r) << 2));
+                const int q = q0 + wq * 16 * FQ + j * 16 + r;
+                if (q < a.Qdim) emit(q, pw + ch * 4, v);
+            }
+        }
+    };
+
+    // The epilogue: the staged row store (nontemporal: only the average + update at the end of
+    // the step reads the rows again, and not even it when the update is fused; measured on the
+    // AlexNet step: 3.57 ms with the fragment stores, 3.38 ms staged, 3.25 ms staged and
+    // nontemporal), else fp32 partial sums of a split reduction, else the operation's store.
+    auto store_out = [&](const Ctx& c, const f32x4 (&acc)[FP][FQ], int p0, int q0, int tid,
+                         float* st) {
         const int wave = tid >> 6, lane = tid & 63;
         const int wp = wave >> 1, wq = wave & 1;
         const int lr = lane & 15, lg = lane >> 4;
-        // first p of this wave's rows, and whether the wave may use the staged row store
         const int pw = p0 + wp * 16 * FP;
-        bool staged_ok = false;
-        if constexpr (STAGED) staged_ok = !split && a.vec_out && pw + 16 * FP <= Op::row_len(a);
-        float* st = nullptr;  // this wave's 4 KB of staging space (the operand tiles, after the loop)
-        if constexpr (STAGED)
-            st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
-                 (wave & 1) * 1024;
-        // the next shard's context: its first operand tiles are loaded during this shard's last
-        // products and stores
-        Ctx cn = c;
-        if (FUSE && rep + 1 < nrep) decode_z(a, cn, rep + 1);
+        if constexpr (STAGED) {
+            if (!split && a.vec_out && pw + 16 * FP <= Op::row_len(a)) {
+                staged_rows(acc, st, pw, q0, wq, lane, [&](int q, int p, f32x4 v) {
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(Op::row_out(a, c, q) + p));
+                });
+                return;
+            }
+        }
+        float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
+#pragma unroll
+        for (int i = 0; i < FP; ++i) {
+            const int p = pw + i * 16 + lg * 4;
+            if (p >= a.Pdim) continue;
+            const int np = min(4, a.Pdim - p);
+            if (split) {
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) {
+                    const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                    if (q >= a.Qdim) continue;
+                    // partial sums are stored [z][q][p]
+                    float* o = part + (long long)q * a.Pdim + p;
+                    if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
+                    else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
+                }
+            } else {
+                const f32x4 rb = row_bias<Op>(a, c, p, np);
+#pragma unroll
+                for (int j = 0; j < FQ; ++j) {
+                    const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                    if (q >= a.Qdim) continue;
+                    // without a bias the stored value is the sum itself (no 0 added, which would
+                    // turn -0 into +0: a fused update sums exactly what is stored)
+                    Op::store4(a, c, p, q, Op::HAS_BIAS ? acc[i][j] + rb : acc[i][j], np);
+                }
+            }
+        }
+    };
 
+    const Buf<T> bufP(Op::P_IS_A ? a.a : a.b, Op::P_IS_A ? a.a_bytes : a.b_bytes);
+    const Buf<T> bufQ(Op::P_IS_A ? a.b : a.a, Op::P_IS_A ? a.b_bytes : a.a_bytes);
+    Loader<Op, true, PK, BP, BK> lp;
+    Loader<Op, false, QK, BQ, BK> lq;
+
+    if constexpr (!FUSE) {
+        Ctx c;
+        decode_z(a, c, tile.bz);
+        const int p0 = tile.by * BP, q0 = tile.bx * BQ;
+        const int tid = threadIdx.x;
+        const int wave = tid >> 6, lane = tid & 63;
+        const int wp = wave >> 1, wq = wave & 1;
+        const int lr = lane & 15, lg = lane >> 4;
+
+        if constexpr (Op::TAB) {
+            // entry j stands for k = kbeg + j * TS (one per 16-byte chunk for vector Q loads)
+            constexpr int TS = (Op::TAB_CHUNK && QK == L_KV) ? VEC : 1;
+            const int n = a.kchunk / TS;
+            for (int j = tid; j < n; j += 256) tab[j] = Op::tab_entry(a, c, c.kbeg + j * TS);
+            c.tab = tab;
+            __syncthreads();
+        }
+        lp.init(a, c, tid, p0);
+        lq.init(a, c, tid, q0);
+
+        f32x4 acc[FP][FQ];
 #pragma unroll
         for (int i = 0; i < FP; ++i)
 #pragma unroll
             for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+        int k0 = c.kbeg;
+        if (k0 < c.kend) {
+            lp.load(a, bufP, c, tid, p0, k0);
+            lq.load(a, bufQ, c, tid, q0, k0);
+        }
         for (; k0 < c.kend; k0 += BK) {
             lp.stage(sP, tid);
             lq.stage(sQ, tid);
@@ -742,175 +839,105 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
             if (k0 + BK < c.kend) {
                 lp.load(a, bufP, c, tid, p0, k0 + BK);
                 lq.load(a, bufQ, c, tid, q0, k0 + BK);
-            } else if (FUSE && rep + 1 < nrep && cn.kbeg < cn.kend) {
-                lp.load(a, bufP, cn, tid, p0, cn.kbeg);
-                lq.load(a, bufQ, cn, tid, q0, cn.kbeg);
             }
-#pragma unroll
-            for (int kc = 0; kc < BK / M::KSTEP; ++kc) {
-                typename M::frag fa[FP], fb[FQ];
-#pragma unroll
-                for (int i = 0; i < FP; ++i)
-                    fa[i] = LP::template frag<typename M::frag>(sP, wp * 16 * FP + i * 16, lr, lg,
-                                                                kc, M::KSTEP);
-#pragma unroll
-                for (int j = 0; j < FQ; ++j)
-                    fb[j] = LQ::template frag<typename M::frag>(sQ, wq * 16 * FQ + j * 16, lr, lg,
-                                                                kc, M::KSTEP);
-#pragma unroll
-                for (int i = 0; i < FP; ++i)
-#pragma unroll
-                    for (int j = 0; j < FQ; ++j) M::run(acc[i][j], fa[i], fb[j]);
-            }
-            if constexpr (SCHED) {
-                // Scheduling order: the first k chunk's fragment reads, then one fragment read of
-                // a later chunk and one global load after each MFMA, so that their latencies
-                // overlap the MFMAs instead of being waited for in clusters (measured: the bf16
-                // convolution weight gradients, whose operands both come through k-major tiles,
-                // run 10-25% faster; forward and data-gradient kernels, and the output-bound fully
-                // connected weight gradients, run slower with it).
-                constexpr int NM = FP * FQ * (BK / M::KSTEP);
-                __builtin_amdgcn_sched_group_barrier(0x100, FP + FQ, 0);  // LDS reads
-#pragma unroll
-                for (int m = 0; m < NM; ++m) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-                    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
-                }
-            }
+            products(acc, wp, wq, lr, lg);
             __syncthreads();
         }
+        // the main loop ended with a barrier, so the operand tiles are free for the staging:
+        // waves 0, 1 use sP, waves 2, 3 use sQ
+        float* st = nullptr;
+        if constexpr (STAGED)
+            st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
+                 (wave & 1) * 1024;
+        store_out(c, acc, p0, q0, tid, st);
+    } else {
+        // All R shards of one output tile (blockIdx.z = 0): the shards' tiles in ascending r, each
+        // stored as above, their fp32 sum kept in registers, then the tile's average + update.
+        // The next shard's first operand tile is loaded during the current shard's products and
+        // staged into LDS before the current shard's stores are issued, so that waiting for the
+        // loads never waits for the stores (loads and stores share one counter).
+        Ctx c;
+        decode_z(a, c, 0);
+        lp.init(a, c, threadIdx.x, tile.by * BP);  // a fused operation's loader state does not
+        lq.init(a, c, threadIdx.x, tile.bx * BQ);  // depend on the shard, only its loads do
+        lp.load(a, bufP, c, threadIdx.x, tile.by * BP, c.kbeg);
+        lq.load(a, bufQ, c, threadIdx.x, tile.bx * BQ, c.kbeg);
+        lp.stage(sP, threadIdx.x);
+        lq.stage(sQ, threadIdx.x);
+        __syncthreads();
+        f32x4 sum[FP][FQ];
+        for (int rep = 0; rep < a.R; ++rep) {
+            // The index arithmetic is made to depend on the shard through an opaque zero, so
+            // that the compiler recomputes it per shard instead of holding every address of the
+            // tile in registers across the loop (308 registers against 152).
+            int oz;
+            asm volatile("s_mov_b32 %0, 0" : "=s"(oz));
+            const int p0 = tile.by * BP + oz, q0 = tile.bx * BQ + oz;
+            const int tid = threadIdx.x + oz;
+            const int wave = tid >> 6, lane = tid & 63;
+            const int wp = wave >> 1, wq = wave & 1;
+            const int lr = lane & 15, lg = lane >> 4;
+            Ctx cn = c;
+            if (rep + 1 < a.R) decode_z(a, cn, rep + 1);
 
-        bool stored = false;
-        if constexpr (STAGED) {
-            if (staged_ok) {
-                stored = true;
-                // Output rows q of the operation are contiguous along p (the fully connected weight
-                // gradient: one row per output unit).  A wave whose 64 p are all inside the rows
-                // stages each 16-row slice of its tile in LDS (4 KB: 16 rows x 16 chunks of 16
-                // bytes, chunk c of row r at slot c ^ r) and writes it back as 4 rows x 256
-                // contiguous bytes per store instruction instead of 16 rows x 64 bytes, nontemporal
-                // (only the average + update at the end of the step reads the rows again, and not
-                // even it when the update is fused).
-                // Measured on the AlexNet step: 3.57 ms with the fragment stores, 3.38 ms staged,
-                // 3.25 ms staged and nontemporal.  The main loop ended with a barrier, so the operand
-                // tiles are free; waves 0, 1 use sP, waves 2, 3 use sQ.
+            f32x4 acc[FP][FQ];
 #pragma unroll
-                for (int j = 0; j < FQ; ++j) {
-                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                    __builtin_amdgcn_wave_barrier();
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            for (int i = 0; i < FP; ++i)
 #pragma unroll
-                    for (int i = 0; i < FP; ++i)  // row lr, chunk i * 4 + lg
-                        *reinterpret_cast<f32x4*>(st + lr * 64 + (((i * 4 + lg) ^ lr) << 2)) =
-                            acc[i][j];
-                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                    __builtin_amdgcn_wave_barrier();
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-                    for (int it = 0; it < 4; ++it) {
-                        const int r = it * 4 + (lane >> 4), ch = lane & 15;
-                        const f32x4 v = *reinterpret_cast<const f32x4*>(st + r * 64 + ((ch ^ r) << 2));
-                        const int q = q0 + wq * 16 * FQ + j * 16 + r;
-                        if (q < a.Qdim)
-                            __builtin_nontemporal_store(
-                                v, reinterpret_cast<f32x4*>(Op::row_out(a, c, q) + pw + ch * 4));
-                    }
+                for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int k0 = c.kbeg; k0 < c.kend; k0 += BK) {
+                const bool more = k0 + BK < c.kend, next = more || rep + 1 < a.R;
+                if (more) {
+                    lp.load(a, bufP, c, tid, p0, k0 + BK);
+                    lq.load(a, bufQ, c, tid, q0, k0 + BK);
+                } else if (next) {
+                    lp.load(a, bufP, cn, tid, p0, cn.kbeg);
+                    lq.load(a, bufQ, cn, tid, q0, cn.kbeg);
+                }
+                products(acc, wp, wq, lr, lg);
+                __syncthreads();
+                if (next) {
+                    lp.stage(sP, tid);
+                    lq.stage(sQ, tid);
+                    __syncthreads();
                 }
             }
-        }
-        if (!stored) {
-            float* part = a.partial + (long long)tile.bz * a.Pdim * a.Qdim;
-#pragma unroll
-            for (int i = 0; i < FP; ++i) {
-                const int p = pw + i * 16 + lg * 4;
-                if (p >= a.Pdim) continue;
-                const int np = min(4, a.Pdim - p);
-                if (split) {
-#pragma unroll
-                    for (int j = 0; j < FQ; ++j) {
-                        const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-                        if (q >= a.Qdim) continue;
-                        // partial sums are stored [z][q][p]
-                        float* o = part + (long long)q * a.Pdim + p;
-                        if (np == 4 && (a.Pdim & 3) == 0) *reinterpret_cast<f32x4*>(o) = acc[i][j];
-                        else for (int v = 0; v < np; ++v) o[v] = acc[i][j][v];
-                    }
-                } else {
-                    const f32x4 rb = row_bias<Op>(a, c, p, np);
-#pragma unroll
-                    for (int j = 0; j < FQ; ++j) {
-                        const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-                        if (q >= a.Qdim) continue;
-                        // without a bias the stored value is the sum itself (no 0 added, which
-                        // would turn -0 into +0: a fused update sums exactly what is stored)
-                        Op::store4(a, c, p, q, Op::HAS_BIAS ? acc[i][j] + rb : acc[i][j], np);
-                    }
-                }
-            }
-        }
-        if constexpr (FUSE) {
+            store_out(c, acc, p0, q0, tid, stg + wave * 1024);
             // running sum of the stored shard values in ascending r, as the stand-alone average
             // adds the gradient rows
 #pragma unroll
             for (int i = 0; i < FP; ++i)
 #pragma unroll
                 for (int j = 0; j < FQ; ++j) sum[i][j] = rep == 0 ? acc[i][j] : sum[i][j] + acc[i][j];
-            __syncthreads();  // the staging space is the next shard's operand tiles
             c = cn;
-            k0 = c.kbeg;
         }
-    }
 
-    if constexpr (FUSE) {
+        // the tile's average + update: parameters out_off + q * C + p (or the bias)
         const int p0 = tile.by * BP, q0 = tile.bx * BQ;
         const int tid = threadIdx.x;
         const int wave = tid >> 6, lane = tid & 63;
         const int wp = wave >> 1, wq = wave & 1;
         const int lr = lane & 15, lg = lane >> 4;
         const int pw = p0 + wp * 16 * FP;
-        bool staged_ok = false;
-        if constexpr (STAGED) staged_ok = !split && a.vec_out && pw + 16 * FP <= Op::row_len(a);
-        float* st = nullptr;
-        if constexpr (STAGED)
-            st = reinterpret_cast<float*>(wave < 2 ? static_cast<T*>(sP) : static_cast<T*>(sQ)) +
-                 (wave & 1) * 1024;
-        if (staged_ok) {
-            // the same staging, then 16-byte runs of one row: parameters out_off + q * C + p
+        if constexpr (STAGED) {
+            if (a.vec_out && pw + 16 * FP <= Op::row_len(a)) {
+                staged_rows(sum, stg + wave * 1024, pw, q0, wq, lane, [&](int q, int p, f32x4 v) {
+                    fused_update4(a, a.out_off + (long long)q * Op::row_len(a) + p, v);
+                });
+                return;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < FP; ++i) {
+            const int p = pw + i * 16 + lg * 4;
 #pragma unroll
             for (int j = 0; j < FQ; ++j) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                const int q = q0 + wq * 16 * FQ + j * 16 + lr;
+                if (q >= a.Qdim) continue;
 #pragma unroll
-                for (int i = 0; i < FP; ++i)
-                    *reinterpret_cast<f32x4*>(st + lr * 64 + (((i * 4 + lg) ^ lr) << 2)) =
-                        sum[i][j];
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-                for (int it = 0; it < 4; ++it) {
-                    const int r = it * 4 + (lane >> 4), ch = lane & 15;
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(st + r * 64 + ((ch ^ r) << 2));
-                    const int q = q0 + wq * 16 * FQ + j * 16 + r;
-                    if (q < a.Qdim)
-                        fused_update4(a, a.out_off + (long long)q * Op::row_len(a) + pw + ch * 4, v);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < FP; ++i) {
-                const int p = pw + i * 16 + lg * 4;
-#pragma unroll
-                for (int j = 0; j < FQ; ++j) {
-                    const int q = q0 + wq * 16 * FQ + j * 16 + lr;
-                    if (q >= a.Qdim) continue;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const long long idx = Op::param_index(a, p + e, q);
-                        if (idx >= 0) fused_update1(a, idx, sum[i][j][e]);
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    const long long idx = Op::param_index(a, p + e, q);
+                    if (idx >= 0) fused_update1(a, idx, sum[i][j][e]);
                 }
             }
         }

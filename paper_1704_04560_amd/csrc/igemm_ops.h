@@ -595,7 +595,10 @@ template <typename T> struct FcDgrad {
 template <typename T> struct FcWgrad {
     typedef T TT;
     static constexpr bool P_IS_A = false;
-    static constexpr bool SHARE_Q = false;
+    // neighbouring blocks of an XCD take the p tiles of one q tile: they write consecutive
+    // 512-byte pieces of the same gradient rows (the operands, K = one shard's samples, are
+    // small); AlexNet FC6 with the fused update 0.429 -> 0.400 ms
+    static constexpr bool SHARE_Q = true;
     static constexpr bool HAS_BIAS = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
     struct PR { int i; bool ok, bias; };

@@ -24,10 +24,12 @@ static long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 // Tile: the largest of 128x128, 64x128, 64x64, 32x128, 32x64 (rows x columns) that gives at
 // least two blocks per compute unit, or at least 64 tiles and a reduction long enough for splits
 // to fill the GPU (the smallest tile when none does); rows are limited by P.  Reduction splits
-// then double until the launch fills one wave of resident blocks (about 2 per compute unit for
-// the larger tiles, 4 for the smaller ones), keeping at least 8 k tiles per split: more splits
-// cost more in fp32 partial sums than they gain in fill (measured).  kmax (an LDS table limit)
-// can force more splits; the fp32 partial sums are capped at 64M elements.
+// then double until the launch has one block per compute unit for the larger tiles, two for the
+// smaller ones, keeping at least 8 k tiles per split: more splits cost more in fp32 partial sums
+// (written, then read back by a second kernel) than they gain in fill (measured: filling two
+// and four per compute unit instead made CIFAR's step 2% slower; half of this, AlexNet's and
+// LeNet's 2-5% slower).  kmax (an LDS table limit) can force more splits; the fp32 partial sums
+// are capped at 64M elements.
 GemmPlan plan_for(int dt, const GemmDims& d)
 {
     constexpr long long kTargetTiles = 512, kTargetBlocks = 1024, kMaxPartial = 64ll << 20;
@@ -57,7 +59,7 @@ GemmPlan plan_for(int dt, const GemmDims& d)
     const long long t = tiles(g.FP, g.FQ);
     const long long ktiles = cdiv(d.K, g.BK);
     long long splits = 1;
-    const long long slots = 256ll * (g.FP * g.FQ >= 8 ? 2 : 4);
+    const long long slots = 256ll * (g.FP * g.FQ >= 8 ? 1 : 2);
     while (t * splits < slots && ktiles >= 8 * 2 * splits && splits < 256) splits *= 2;
     const long long per_split = (long long)d.P * d.Q * d.Z;
     while (splits > 1 && splits * per_split > kMaxPartial) splits /= 2;

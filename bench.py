@@ -416,14 +416,22 @@ def measure(torch, mtx, wl, name, steps, warmup):
     kernels = []
     fused = sorted({layer for (sname, layer, launches, _) in sites
                     if sname == "wgrad_update" and launches})
+    # one entry per (site, layer): the stand-alone average + update can be several launches of
+    # a step (one per contiguous range of parameters not updated by a fused launch)
+    merged = {}
+    for (sname, layer, launches, total) in sites:
+        n0, t0 = merged.get((sname, layer), (0, 0.0))
+        merged[(sname, layer)] = (n0 + launches, t0 + total)
+    sites = [(sname, layer, n, t) for (sname, layer), (n, t) in merged.items()]
     for (sname, layer, launches, total) in sites:
         if launches == 0:
             continue
         bound, work, mm = _site_work(sname, layer, geo, wkl, es, fused)
+        per_step = max(1, round(launches / steps))
         if sname == "avg_update":  # launches per step: one per contiguous parameter range
-            work /= max(1, round(launches / steps))
+            work /= per_step
         kernels.append(dict(name=sname, layer=layer, avg_ms=total / launches, bound=bound,
-                            work=work, mm_flops=mm))
+                            work=work, mm_flops=mm, per_step=per_step))
     peak_mm = PEAK["bf16_TFLOPs"] if net.dtype == wl.BF16 else PEAK["f32_TFLOPs"]
     # the dominant kernel: the longest one whose algorithmic work is modelled
     dom = max((k for k in kernels if k["bound"]), key=lambda k: k["avg_ms"])
@@ -458,9 +466,11 @@ def measure(torch, mtx, wl, name, steps, warmup):
         "gemm_mfma": {"achieved_TFLOPs": round(mfma_flops / (mfma_ms * 1e-3) / 1e12, 3),
                       "peak_TFLOPs": peak_mm,
                       "frac": round(mfma_flops / (mfma_ms * 1e-3) / 1e12 / peak_mm, 4)},
+        # the stand-alone average + update of the step: all its launches together
         "step_avg_update": ({"GBps": round(au[0]["work"] / (au[0]["avg_ms"] * 1e-3) / 1e9, 1),
-                             "ms": round(au[0]["avg_ms"], 5),
-                             "params": int(au[0]["work"] / (4 * (wkl.shards + (5 if wkl.momentum else 3))))}
+                             "ms": round(au[0]["avg_ms"] * au[0]["per_step"], 5),
+                             "launches": au[0]["per_step"],
+                             "params": wkl_params(wkl) - sum(layer_params(geo, f) for f in fused)}
                             if au else None),
         "fused_update_layers": fused,
         "kernel_ms_sum": round(sum(k["avg_ms"] for k in kernels), 5),

@@ -47,7 +47,8 @@ typedef enum {
     MTX_EINVAL = -1,       /* invalid argument (null pointer, bad size, misaligned pointer) */
     MTX_ENOMEM = -2,       /* host allocation failed, or a caller buffer is too small */
     MTX_EHIP = -3,         /* a HIP runtime call failed */
-    MTX_EUNSUPPORTED = -4  /* a valid network the library does not implement */
+    MTX_EUNSUPPORTED = -4, /* a valid network the library does not implement */
+    MTX_ENONFINITE = -5    /* the non-finite check found a non-finite gradient average */
 } mtx_status;
 
 typedef enum { MTX_F32 = 0, MTX_BF16 = 1 } mtx_dtype;
@@ -240,6 +241,17 @@ int mtx_set_graph_replay(mtx_model* m, int enable);
  * not depend on this option.  Steps run on the caller's stream alone while kernel timing is
  * on.  enable = 0 switches it off. */
 int mtx_set_overlap(mtx_model* m, int enable);
+
+/* Non-finite check (option, default off; for training loops that must not let an overflow
+ * into the weights).  With it on, mtx_train_step averages the R shard gradients into grad_avg
+ * first and flags any average that is not finite (Inf or NaN), then applies the momentum rule
+ * from grad_avg only if nothing was flagged (the same values as without the check), waits for
+ * the step (a synchronisation of the caller's stream) and returns MTX_ENONFINITE when the update
+ * was skipped: w and v are then unchanged, grads and grad_avg hold the step's values.  The check
+ * needs the momentum rule and a caller's stream that is not being captured (MTX_EUNSUPPORTED
+ * otherwise); the fused and layer-wise updates are not used while it is on.  Returns MTX_EINVAL
+ * for a NULL model. */
+int mtx_set_nonfinite_check(mtx_model* m, int enable);
 
 /* Fused average + update of large fully connected layers (execution option, default on).  With
  * the momentum rule (not Adam or AdaGrad) and without the layer-wise option, a fully connected

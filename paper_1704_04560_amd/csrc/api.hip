@@ -696,6 +696,8 @@ struct mtx_model {
     // the fully connected layers at the end of the parameter list carry their own average +
     // update in their weight-gradient launch (mtx_set_fused_update)
     bool fuse_update = true;
+    // the non-finite check (mtx_set_nonfinite_check): average, flag, update unless flagged
+    bool check_finite = false;
     // update rule after the average (mtx_set_optimizer): momentum, or Adam / AdaGrad with their
     // first state in v, Adam's second moment in s2, and the number of steps taken since
     int opt = MTX_OPT_MOMENTUM;
@@ -981,6 +983,14 @@ int mtx_set_overlap(mtx_model* m, int enable)
     return MTX_OK;
 }
 
+int mtx_set_nonfinite_check(mtx_model* m, int enable)
+{
+    if (!m) return fail(MTX_EINVAL, "model is NULL");
+    m->check_finite = enable != 0;
+    m->graph.reset();  // the captured launch sequence depends on it
+    return MTX_OK;
+}
+
 int mtx_set_fused_update(mtx_model* m, int enable)
 {
     if (!m) return fail(MTX_EINVAL, "model is NULL");
@@ -1217,7 +1227,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     // output gradient and input, so (unless kernels are being timed) it runs on the second
     // stream, forked after its output gradient is written and joined before the update.
     const bool overlap = m->overlap && !m->timer.on;
-    const bool layerwise = m->layerwise && m->upd && !m->timer.on;
+    const bool layerwise = m->layerwise && m->upd && !m->timer.on && !m->check_finite;
     float* partial_w = overlap ? reinterpret_cast<float*>(ws + pl.partial_w_off) : partial;
     const long long ld = (long long)pl.ld;
     int nfork = 0, nlayer = 0;
@@ -1230,7 +1240,8 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     std::vector<char> fused(pl.L.size(), 0);
     std::vector<std::pair<size_t, size_t>> rest;
     {
-        const bool can = m->fuse_update && m->opt == MTX_OPT_MOMENTUM && !layerwise;
+        const bool can = m->fuse_update && m->opt == MTX_OPT_MOMENTUM && !layerwise &&
+                         !m->check_finite;
         size_t beg = 0;
         for (size_t l = 0; l < pl.L.size(); ++l) {
             const LayerPlan& lp = pl.L[l];
@@ -1421,6 +1432,22 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         return MTX_OK;
     }
     // ---- average of the R shard gradients fused with the optimizer step ----
+    if (m->check_finite) {
+        // the average first, with a flag for a non-finite value; then the momentum update from
+        // the stored average (g = avg / 1: the same values as the fused pass), which does
+        // nothing while the flag is set
+        int* flag = reinterpret_cast<int*>(ws + pl.sync_off + 64);
+        HIP_TRY(set_flag(flag, 0, s), "non-finite flag");
+        HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {
+                    return average_update(m->grads, pl.R, pl.P, pl.ld, m->w, m->v, lr, momentum,
+                                          m->gavg, false, s, 0, nullptr, flag);
+                }), "average");
+        HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {
+                    return average_update(m->gavg, 1, pl.P, pl.ld, m->w, m->v, lr, momentum,
+                                          nullptr, true, s, 0, flag, nullptr);
+                }), "update");
+        return MTX_OK;
+    }
     for (const auto& rg : rest)
         HIP_TRY(launch_site(m, "avg_update", -1, s, [&] {
                     return update_slice(m, rg.first, rg.second, lr, momentum, s, 0);
@@ -1464,6 +1491,9 @@ static bool capture_step(mtx_model* m, const float* x, const int32_t* labels, fl
     return true;
 }
 
+static int step_dispatch(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                         float momentum, float* loss_out, hipStream_t s, bool caller_capturing);
+
 int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr,
                    float momentum, float* loss_out, void* stream)
 {
@@ -1474,13 +1504,34 @@ int mtx_train_step(mtx_model* m, const float* x, const int32_t* labels, float lr
     if (!std::isfinite(lr) || !std::isfinite(momentum))
         return fail(MTX_EINVAL, "lr and momentum must be finite");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    m->last_stream = s;
-    ++m->opt_step;
     GraphCache& gc = m->graph;
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     const bool caller_capturing =
         hipStreamIsCapturing(s, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone;
     (void)hipGetLastError();
+    if (m->check_finite && (m->opt != MTX_OPT_MOMENTUM || caller_capturing))
+        return fail(MTX_EUNSUPPORTED, "the non-finite check needs the momentum rule and a stream "
+                                      "that is not being captured");
+    m->last_stream = s;
+    ++m->opt_step;
+    if (m->check_finite) {
+        const int rc = step_dispatch(m, x, labels, lr, momentum, loss_out, s, caller_capturing);
+        if (rc != MTX_OK) return rc;
+        int flag = 0;
+        HIP_TRY(hipMemcpyAsync(&flag, m->ws + m->pl.sync_off + 64, sizeof flag,
+                               hipMemcpyDeviceToHost, s), "non-finite flag");
+        HIP_TRY(hipStreamSynchronize(s), "non-finite flag");
+        if (flag) return fail(MTX_ENONFINITE, "the gradient average is not finite: w and v kept");
+        return MTX_OK;
+    }
+    return step_dispatch(m, x, labels, lr, momentum, loss_out, s, caller_capturing);
+}
+
+// The step on stream s: replayed from the model's graph, captured into it, or enqueued directly.
+static int step_dispatch(mtx_model* m, const float* x, const int32_t* labels, float lr,
+                         float momentum, float* loss_out, hipStream_t s, bool caller_capturing)
+{
+    GraphCache& gc = m->graph;
     // Adam's bias correction changes every step, so its steps are not replayed from a graph
     if (gc.enabled && !m->timer.on && !caller_capturing && m->opt != MTX_OPT_ADAM &&
         gc.misses < GraphCache::kMaxMisses) {

@@ -682,16 +682,24 @@ hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// The non-finite check of a step: an average-only pass sets *nonfinite when any average is not
+// finite; the update pass that follows does nothing while *skip is set.  Both null otherwise.
+struct FiniteGuard {
+    const int* skip;
+    int* nonfinite;
+};
+
 template <bool MOM, bool AVG, bool UPD>
 __device__ __forceinline__ void avg_update_one(const float* __restrict__ grads, int R, long long ld,
                                                long long i, float* __restrict__ w,
                                                float* __restrict__ v, float lr, float mu,
-                                               float* __restrict__ avg)
+                                               float* __restrict__ avg, int* nonfinite)
 {
     float s = grads[i];
     for (int r = 1; r < R; ++r) s += grads[(long long)r * ld + i];
     float g = s / (float)R;
     if (AVG) avg[i] = g;
+    if (AVG && !UPD && nonfinite && !__builtin_isfinite(g)) *nonfinite = 1;
     if (UPD) {
         if (MOM) {
             const float vn = fmaf(mu, v[i], g);
@@ -715,8 +723,9 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
                                                        long long n, long long ld,
                                                        float* __restrict__ w,
                                                        float* __restrict__ v, float lr, float mu,
-                                                       float* __restrict__ avg)
+                                                       float* __restrict__ avg, FiniteGuard fg)
 {
+    if (UPD && fg.skip && *fg.skip) return;
     constexpr int U = 2;
     const long long n4 = n / 4, ld4 = ld / 4;
     const int R = RT > 0 ? RT : Rrt;
@@ -763,6 +772,10 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
             if (!ok[u]) continue;
             f32x4 g = {s[u][0] / fr, s[u][1] / fr, s[u][2] / fr, s[u][3] / fr};
             if (AVG) __builtin_nontemporal_store(g, reinterpret_cast<f32x4*>(avg) + t);
+            if (AVG && !UPD && fg.nonfinite &&
+                !(__builtin_isfinite(g[0]) && __builtin_isfinite(g[1]) && __builtin_isfinite(g[2]) &&
+                  __builtin_isfinite(g[3])))
+                *fg.nonfinite = 1;
             if (UPD) {
                 if (MOM) {
 #pragma unroll
@@ -778,7 +791,7 @@ __global__ __launch_bounds__(256) void avg_update_vec4(const float* __restrict__
     }
     if (blockIdx.x == 0 && threadIdx.x == 0)
         for (long long i = 4 * n4; i < n; ++i)
-            avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
+            avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg, fg.nonfinite);
 }
 
 template <bool MOM, bool AVG, bool UPD>
@@ -786,11 +799,13 @@ __global__ __launch_bounds__(256) void avg_update_scalar(const float* __restrict
                                                          long long n, long long ld,
                                                          float* __restrict__ w,
                                                          float* __restrict__ v, float lr,
-                                                         float mu, float* __restrict__ avg)
+                                                         float mu, float* __restrict__ avg,
+                                                         FiniteGuard fg)
 {
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
-    avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg);
+    if (UPD && fg.skip && *fg.skip) return;
+    avg_update_one<MOM, AVG, UPD>(grads, R, ld, i, w, v, lr, mu, avg, fg.nonfinite);
 }
 
 // Dynamic LDS that the streaming average kernels reserve without using it, so that at most five
@@ -804,7 +819,7 @@ constexpr size_t kStreamLds = 160 * 1024 / 5 - 1024;
 template <bool MOM, bool AVG, bool UPD>
 static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t ld, float* w,
                                     float* v, float lr, float mu, float* avg, unsigned max_blocks,
-                                    hipStream_t s)
+                                    hipStream_t s, FiniteGuard fg)
 {
     auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
     const bool vec = (ld % 4 == 0) && al(grads) && (!AVG || al(avg)) && (!UPD || al(w)) &&
@@ -815,33 +830,45 @@ static hipError_t avg_update_launch(const float* grads, int R, size_t n, size_t 
         if (max_blocks && grid.x > max_blocks) grid.x = max_blocks;
         const size_t lds = max_blocks ? 0 : kStreamLds;
         switch (R) {
-        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
-        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg); break;
+        case 1: hipLaunchKernelGGL((avg_update_vec4<1, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
+        case 2: hipLaunchKernelGGL((avg_update_vec4<2, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
+        case 4: hipLaunchKernelGGL((avg_update_vec4<4, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
+        case 8: hipLaunchKernelGGL((avg_update_vec4<8, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
+        case 16: hipLaunchKernelGGL((avg_update_vec4<16, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
+        default: hipLaunchKernelGGL((avg_update_vec4<0, MOM, AVG, UPD>), grid, dim3(256), lds, s, grads, R, nn, (long long)ld, w, v, lr, mu, avg, fg); break;
         }
     } else {
         hipLaunchKernelGGL((avg_update_scalar<MOM, AVG, UPD>), dim3(grid_for(n, 256)), dim3(256),
-                           0, s, grads, R, (long long)n, (long long)ld, w, v, lr, mu, avg);
+                           0, s, grads, R, (long long)n, (long long)ld, w, v, lr, mu, avg, fg);
     }
     return hipGetLastError();
 }
 
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
                           float lr, float mu, float* avg, bool update, hipStream_t s,
-                          unsigned max_blocks)
+                          unsigned max_blocks, const int* skip, int* nonfinite)
 {
     const bool mom = update && mu != 0.0f;
     const bool wavg = avg != nullptr;
-    if (!update) return avg_update_launch<false, true, false>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
+    const FiniteGuard fg{skip, nonfinite};
+    if (!update) return avg_update_launch<false, true, false>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s, fg);
     if (mom) {
-        if (wavg) return avg_update_launch<true, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
-        return avg_update_launch<true, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
+        if (wavg) return avg_update_launch<true, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s, fg);
+        return avg_update_launch<true, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s, fg);
     }
-    if (wavg) return avg_update_launch<false, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
-    return avg_update_launch<false, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s);
+    if (wavg) return avg_update_launch<false, true, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s, fg);
+    return avg_update_launch<false, false, true>(grads, R, n, ld, w, v, lr, mu, avg, max_blocks, s, fg);
+}
+
+__global__ void set_int_kernel(int* p, int value)
+{
+    if (threadIdx.x == 0) *p = value;
+}
+
+hipError_t set_flag(int* p, int value, hipStream_t s)
+{
+    hipLaunchKernelGGL(set_int_kernel, dim3(1), dim3(64), 0, s, p, value);
+    return hipGetLastError();
 }
 
 

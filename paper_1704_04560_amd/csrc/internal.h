@@ -208,10 +208,14 @@ hipError_t softmax_xent(Dt dt, int B, int NC, int Nb, const float* logits,
                         const int32_t* labels, void* dz, float* block_sums, unsigned* sync,
                         float* loss_out, hipStream_t s);
 // max_blocks > 0 caps the grid (the kernel strides over the range), so that an update running
-// beside other kernels occupies only part of the GPU.
+// beside other kernels occupies only part of the GPU.  nonfinite (average only, update false):
+// set to 1 when an average is not finite; skip (update): the launch does nothing while *skip.
 hipError_t average_update(const float* grads, int R, size_t n, size_t ld, float* w, float* v,
                           float lr, float mu, float* avg, bool update, hipStream_t s,
-                          unsigned max_blocks = 0);
+                          unsigned max_blocks = 0, const int* skip = nullptr,
+                          int* nonfinite = nullptr);
+// *p = value, as a kernel (graph-capturable, unlike a memset node)
+hipError_t set_flag(int* p, int value, hipStream_t s);
 
 // Parameters of the adaptive updates after the average (Adam: s1 = first moment m, s2 =
 // second moment v; AdaGrad: s1 = accumulated squared gradients, s2 unused).  c1 = 1 - b1,

@@ -16,7 +16,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmtx.so")
 
-MTX_OK, MTX_EINVAL, MTX_ENOMEM, MTX_EHIP, MTX_EUNSUPPORTED = 0, -1, -2, -3, -4
+MTX_OK, MTX_EINVAL, MTX_ENOMEM, MTX_EHIP, MTX_EUNSUPPORTED, MTX_ENONFINITE = 0, -1, -2, -3, -4, -5
 MTX_F32, MTX_BF16 = 0, 1
 MTX_FC, MTX_CONV, MTX_MAXPOOL, MTX_BN, MTX_ADD, MTX_ADDP = 0, 1, 2, 3, 4, 5
 MTX_OPT_MOMENTUM, MTX_OPT_ADAM, MTX_OPT_ADAGRAD = 0, 1, 2
@@ -25,7 +25,8 @@ EXPORTS = ("mtx_model_sizes", "mtx_init_model", "mtx_init_model_static", "mtx_tr
            "mtx_sgd_update", "mtx_adam_update", "mtx_adagrad_update", "mtx_get_params",
            "mtx_set_params", "mtx_get_layer_output", "mtx_set_optimizer",
            "mtx_get_pool_argmax", "mtx_set_graph_replay", "mtx_set_overlap",
-           "mtx_set_layerwise_update", "mtx_set_fused_update", "mtx_set_timing",
+           "mtx_set_layerwise_update", "mtx_set_fused_update", "mtx_set_nonfinite_check",
+           "mtx_set_timing",
            "mtx_get_timing", "mtx_get_launches", "mtx_free_model", "mtx_last_error")
 
 
@@ -100,6 +101,7 @@ def lib() -> C.CDLL:
             "mtx_set_optimizer": (i32, [vp, i32, f32, f32, f32, vp]),
             "mtx_set_layerwise_update": (i32, [vp, i32]),
             "mtx_set_fused_update": (i32, [vp, i32]),
+            "mtx_set_nonfinite_check": (i32, [vp, i32]),
             "mtx_set_overlap": (i32, [vp, i32]),
             "mtx_set_timing": (i32, [vp, i32]),
             "mtx_get_timing": (i32, [vp, C.POINTER(mtx_kernel_time), i32, C.POINTER(i32), i32]),
@@ -237,6 +239,10 @@ def mtx_set_layerwise_update(handle, enable: bool):
 
 def mtx_set_fused_update(handle, enable: bool):
     _check(lib().mtx_set_fused_update(handle, 1 if enable else 0))
+
+
+def mtx_set_nonfinite_check(handle, enable: bool):
+    _check(lib().mtx_set_nonfinite_check(handle, 1 if enable else 0))
 
 
 def mtx_set_timing(handle, enable: bool):

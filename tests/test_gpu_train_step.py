@@ -537,6 +537,70 @@ def test_fused_fc_update_is_bit_identical(name, R, Nb, mu):
     b.close()
 
 
+@pytest.mark.parametrize("name,R,Nb", [("lenet", 4, 8), ("alexnet", 2, 2)])
+def test_nonfinite_check_is_bit_identical_when_finite(name, R, Nb):
+    """With the non-finite check on, a step averages first, flags non-finite averages and then
+    updates from the stored average: w, v, the average and the shard rows are bit-identical to
+    the fused average + update (and, for AlexNet, to the fused fc updates) when all is finite."""
+    net = {"lenet": wl.LENET, "alexnet": wl.ALEXNET}[name]
+    layers = wl.layer_tuples(net)
+    _say(f"[case] non-finite check, finite step {name} R={R} Nb={Nb}")
+    a = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=8)
+    b = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=8)
+    mtx.mtx_set_nonfinite_check(a.handle, True)
+    x, y = wl.make_batch(net, R * Nb, seed=8)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    for step in range(2):
+        a.train_step(xd, yd, 0.01, 0.9)
+        b.train_step(xd, yd, 0.01, 0.9)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.grads_host().view(np.uint32), b.grads_host().view(np.uint32)), step
+        wa, va = a.get_params()
+        wb, vb = b.get_params()
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), step
+        assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)), step
+        ga, gb = a.grad_avg.cpu().numpy(), b.grad_avg.cpu().numpy()
+        assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32)), step
+    a.close()
+    b.close()
+
+
+def test_nonfinite_check_skips_the_update():
+    """An input with an infinite value makes the gradient average non-finite: the step returns
+    MTX_ENONFINITE and leaves w and v as they were; the next finite step updates as usual.  The
+    check refuses the adaptive update rules."""
+    net = wl.LENET
+    layers = wl.layer_tuples(net)
+    R, Nb = 2, 4
+    _say("[case] non-finite check, infinite input")
+    m = mtx.Model(net.in_shape, layers, net.dtype, R, Nb, seed=9)
+    mtx.mtx_set_nonfinite_check(m.handle, True)
+    x, y = wl.make_batch(net, R * Nb, seed=9)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    m.train_step(xd, yd, 0.01, 0.9)  # finite: v becomes non-zero
+    torch.cuda.synchronize()
+    w0, v0 = m.get_params()
+    assert np.any(v0 != 0)
+    bad = x.copy()
+    bad[1, 0, 3, 5] = np.inf
+    with pytest.raises(mtx.MtxError) as err:
+        m.train_step(torch.from_numpy(bad).cuda(), yd, 0.01, 0.9)
+    assert err.value.code == mtx.MTX_ENONFINITE
+    w1, v1 = m.get_params()
+    assert np.array_equal(w1.view(np.uint32), w0.view(np.uint32))
+    assert np.array_equal(v1.view(np.uint32), v0.view(np.uint32))
+    assert not np.all(np.isfinite(m.grad_avg.cpu().numpy()))
+    m.train_step(xd, yd, 0.01, 0.9)
+    torch.cuda.synchronize()
+    w2, _ = m.get_params()
+    assert np.all(np.isfinite(w2)) and not np.array_equal(w2, w0)
+    m.set_optimizer(mtx.MTX_OPT_ADAM, *ADAM)
+    with pytest.raises(mtx.MtxError) as err:
+        m.train_step(xd, yd, 1e-3, 0.0)
+    assert err.value.code == mtx.MTX_EUNSUPPORTED
+    m.close()
+
+
 def _layerwise(model):
     mtx.mtx_set_overlap(model.handle, True)
     mtx.mtx_set_layerwise_update(model.handle, True)

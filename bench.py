@@ -288,6 +288,18 @@ def microbench_avg_update(torch, mtx, reps=20):
     return out
 
 
+def _cpu_model():
+    """The host CPU's model name (for the oracle baseline's record)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wkl, budget_s=12.0):
     """The CPU oracle on a bounded sample of the workload.  AlexNet: one shard of the step (its
     32 samples, R = 1) timed once; a step is R such shards, so samples/s = shard samples / shard
@@ -314,7 +326,7 @@ def cpu_baseline(wkl, budget_s=12.0):
             if el >= budget_s:
                 break
         return {"value": round(shards * nb / el, 3), "unit": "samples/s",
-                "cores": orc.num_threads(), "kind": "oracle",
+                "cores": orc.num_threads(), "cpu": _cpu_model(), "kind": "oracle",
                 "sample": f"{shards} shards of the step, each {nb} samples run as R = 1 "
                           f"({prec}), {el:.1f} s; a step is {R} such shards "
                           f"(x{R} extrapolated)"}
@@ -332,7 +344,7 @@ def cpu_baseline(wkl, budget_s=12.0):
         if el >= budget_s:
             break
     return {"value": round(steps * R * nb / el, 3), "unit": "samples/s",
-            "cores": orc.num_threads(), "kind": "oracle",
+            "cores": orc.num_threads(), "cpu": _cpu_model(), "kind": "oracle",
             "sample": f"{steps} oracle steps of {R} shards x {nb} samples ({prec}), {el:.1f} s"}
 
 
@@ -401,6 +413,19 @@ def measure(torch, mtx, wl, name, steps, warmup):
     # timed region: K steps as a training loop runs them
     ms = timed(steps)
     assert torch.isfinite(loss).item(), "non-finite loss"
+    # the spread of single steps: K more steps, each between its own event pair
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record(stream)
+        model.train_step(xd, yd, wkl.lr, wkl.momentum, loss, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    single = sorted(a.elapsed_time(b) for a, b in evs)
+
+    def pct(q):
+        return round(single[min(len(single) - 1, int(q * (len(single) - 1) + 0.5))], 5)
     # second timed region of K steps with a HIP event pair around every kernel (on the step's
     # stream), for the per-kernel durations behind the roofline figures
     mtx.mtx_set_timing(model.handle, True)
@@ -475,6 +500,8 @@ def measure(torch, mtx, wl, name, steps, warmup):
         "fused_update_layers": fused,
         "kernel_ms_sum": round(sum(k["avg_ms"] for k in kernels), 5),
         "ms_per_step_with_kernel_events": round(ms_events, 5),
+        "step_ms_single": {"median": pct(0.5), "p10": pct(0.1), "p90": pct(0.9),
+                           "steps": len(single)},
         "kernels": [{"name": k["name"], "layer": k["layer"], "ms": round(k["avg_ms"], 5)}
                     for k in kernels],
     }
@@ -543,7 +570,8 @@ def main():
             extra[name] = {"workload": e["wkl"].description, "samples_per_s": e["value"],
                            "ms_per_step": e["ms_per_step"], "dtype": e["dtype"],
                            "roofline": e["roofline"], "gemm_mfma": e["gemm_mfma"],
-                           "step_avg_update": e["step_avg_update"]}
+                           "step_avg_update": e["step_avg_update"],
+                           "step_ms_single": e["step_ms_single"]}
             torch.cuda.empty_cache()
         out["other_workloads"] = extra
     if not args.no_extra:

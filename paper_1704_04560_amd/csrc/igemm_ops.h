@@ -124,6 +124,13 @@ template <typename T> struct ConvFwd {
         for (int i = 0; i < 4; ++i) v[i] = a.relu ? fmaxf(acc[i], 0.f) : acc[i];
         store_vals<T>(a.out, a.out_f32, q * a.OC + co, v, np, a.vec_out);
     }
+    static constexpr bool ROW_EPI = true, EPI_RELU = true, EPI_MASK = false;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx& c, int p, int q)
+    {
+        return (long long)q * a.OC + c.grp * a.og + p;
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return a.OC % 8 == 0 && a.og % 8 == 0; }
+    __device__ static bool out_f32(const GemmArgs& a) { return a.out_f32; }
 };
 
 // ------------------------------------------------------------------------------------------
@@ -217,6 +224,13 @@ template <typename T, bool STRIDE1> struct ConvDgrad {
         apply_mask<T>(a, idx, v, np);
         store_vals<T>(a.out, false, idx, v, np, a.vec_out);
     }
+    static constexpr bool ROW_EPI = true, EPI_RELU = false, EPI_MASK = true;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx& c, int p, int q)
+    {
+        return (long long)q * a.C + c.grp * a.cg + p;
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return a.C % 8 == 0 && a.cg % 8 == 0; }
+    __device__ static bool out_f32(const GemmArgs&) { return false; }
 };
 
 // ------------------------------------------------------------------------------------------
@@ -278,6 +292,13 @@ template <typename T> struct ConvDgradCol {
         if (np == 4 && a.vec_out) *reinterpret_cast<f32x4*>(o) = acc;
         else for (int i = 0; i < np; ++i) o[i] = acc[i];
     }
+    static constexpr bool ROW_EPI = true, EPI_RELU = false, EPI_MASK = false;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx& c, int p, int q)
+    {
+        return ((long long)c.grp * a.Qdim + q) * a.Pdim + p;
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return a.Pdim % 8 == 0; }
+    __device__ static bool out_f32(const GemmArgs&) { return true; }
 };
 
 // ------------------------------------------------------------------------------------------
@@ -420,6 +441,13 @@ template <typename T> struct ConvFwdRun {
     {
         ConvFwd<T>::store4(a, c, p, q, acc, np);
     }
+    static constexpr bool ROW_EPI = true, EPI_RELU = true, EPI_MASK = false;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx& c, int p, int q)
+    {
+        return ConvFwd<T>::out_index(a, c, p, q);
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return ConvFwd<T>::rows8(a); }
+    __device__ static bool out_f32(const GemmArgs& a) { return a.out_f32; }
 };
 
 // Weight gradient of one shard for the same layer: p = output channel, q = (u, j) plus the
@@ -542,6 +570,14 @@ template <typename T> struct FcFwd {
         for (int i = 0; i < 4; ++i) v[i] = a.relu ? fmaxf(acc[i], 0.f) : acc[i];
         store_vals<T>(a.out, a.out_f32, q * a.Pdim + p, v, np, a.vec_out);
     }
+    // staged row epilogue (see igemm_kernel): rows q contiguous along p
+    static constexpr bool ROW_EPI = true, EPI_RELU = true, EPI_MASK = false;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx&, int p, int q)
+    {
+        return (long long)q * a.Pdim + p;
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return a.Pdim % 8 == 0; }
+    __device__ static bool out_f32(const GemmArgs& a) { return a.out_f32; }
 };
 
 // Data gradient: p = input feature i, q = sample, k = output unit o.  P = W^T (tensor b, rows
@@ -585,6 +621,13 @@ template <typename T> struct FcDgrad {
         apply_mask<T>(a, idx, v, np);
         store_vals<T>(a.out, false, idx, v, np, a.vec_out);
     }
+    static constexpr bool ROW_EPI = true, EPI_RELU = false, EPI_MASK = true;
+    __device__ static long long out_index(const GemmArgs& a, const Ctx&, int p, int q)
+    {
+        return (long long)q * a.Pdim + p;
+    }
+    __device__ static bool rows8(const GemmArgs& a) { return a.Pdim % 8 == 0; }
+    __device__ static bool out_f32(const GemmArgs&) { return false; }
 };
 
 // Weight gradient of one shard: p = input feature i (logical (c, h, w) order) plus the bias

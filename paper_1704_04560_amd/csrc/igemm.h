@@ -1281,10 +1281,14 @@ static hipError_t launch_tile(const GemmArgs& a, int gz, hipStream_t s)
     return hipGetLastError();
 }
 
-// Tile shapes (FP, FQ) in {(1,2), (1,4), (2,2), (2,4), (4,4)}, k tile 32 or 64.
+// Tile shapes (FP, FQ) in {(1,2), (1,4), (2,2), (2,4), (3,4), (4,4)}, k tile 32 or 64; the
+// 96-row tile only for bf16 with the P operand loaded along k (its rows need not be a power of
+// two), else the 128-row tile (the plan's splits and chunks hold for either).
 template <class Op, int BK, int PK, int QK>
 static hipError_t launch_shape_bk(const GemmArgs& a, const GemmPlan& g, int gz, hipStream_t s)
 {
+    if constexpr (sizeof(typename Op::TT) == 2 && (PK == L_KV || PK == L_SK))
+        if (g.FP == 3) return launch_tile<Op, 3, 4, BK, PK, QK>(a, gz, s);
     if (g.FP == 1) {
         if (g.FQ == 4) return launch_tile<Op, 1, 4, BK, PK, QK>(a, gz, s);
         return launch_tile<Op, 1, 2, BK, PK, QK>(a, gz, s);

@@ -43,9 +43,15 @@ GemmPlan plan_for(int dt, const GemmDims& d)
     auto bk_of = [&](int fp, int fq) {
         return (d.K <= 32 || (dt == DT_F32 && fp == 4 && fq == 4)) ? 32 : 64;
     };
+    // bf16: 96-row tiles instead of 128-row ones when P is a multiple of 96 but not of 128
+    // (96 or 192 output channels: AlexNet's conv1 and grouped conv4), so that no MFMA rows are
+    // padding
+    const bool rows96 = dt == DT_BF16 && d.P > 64 && d.P % 96 == 0 && d.P % 128 != 0;
     g.FP = 1;
     g.FQ = 2;
-    for (const auto& c : cand) {
+    for (const auto& c0 : cand) {
+        int c[2] = {c0[0], c0[1]};
+        if (rows96 && c[0] == 4) c[0] = 3;
         if (c[0] > fpmax) continue;
         const long long t = tiles(c[0], c[1]);
         const long long ks = std::min(cdiv(d.K, bk_of(c[0], c[1])) / 8, 32ll);

@@ -462,6 +462,7 @@ template <typename T, int KT, int ST>
 __global__ __launch_bounds__(256) void pool_bwd_nchw_kernel(int C, int H, int W, int Kr, int Sr,
                                                             int OH, int OW, int cb, int pst,
                                                             int rows, FastDiv fcb, FastDiv fw,
+                                                            FastDiv fs,
                                                             const uint8_t* __restrict__ argmax,
                                                             const T* __restrict__ dy,
                                                             const T* __restrict__ gate,
@@ -486,14 +487,17 @@ __global__ __launch_bounds__(256) void pool_bwd_nchw_kernel(int C, int H, int W,
     }
     __syncthreads();
     const int cnt = (h1 - h0) * W * cb;
+    // (the window ranges divide non-negative values by the stride: by a constant, or with the
+    // fast division by an invariant integer)
+    auto divs = [&](int v) { return ST > 0 ? v / ST : (int)fdivu(fs, (unsigned)v); };
     for (int e = threadIdx.x; e < cnt; e += 256) {
         const unsigned hw = fdivu(fcb, (unsigned)e), cl = (unsigned)e - hw * (unsigned)cb;
         const unsigned hr = fdivu(fw, hw);
         const int h = h0 + (int)hr, w = (int)(hw - hr * (unsigned)W);
-        const int jlo = w - K + 1 <= 0 ? 0 : (w - K + 1 + S - 1) / S;
-        const int jhi = min(w / S, OW - 1);
-        const int il = max(ilo, h - K + 1 <= 0 ? 0 : (h - K + 1 + S - 1) / S);
-        const int ih = min(h / S, OH - 1);
+        const int jlo = w - K + 1 <= 0 ? 0 : divs(w - K + 1 + S - 1);
+        const int jhi = min(divs(w), OW - 1);
+        const int il = max(ilo, h - K + 1 <= 0 ? 0 : divs(h - K + 1 + S - 1));
+        const int ih = min(divs(h), OH - 1);
         float acc = 0.f;
         for (int i = il; i <= ih; ++i)
             for (int j = jlo; j <= jhi; ++j) {
@@ -529,15 +533,19 @@ static void pool_bwd_launch(int N, int C, int H, int W, int K, int S, bool dy_nc
             const size_t shm = (size_t)cb * pst * (sizeof(float) + 1);
             dim3 g((unsigned)(C / cb), (unsigned)N, (unsigned)((H + rows - 1) / rows));
             const FastDiv fcb = make_fastdiv((unsigned)cb), fw = make_fastdiv((unsigned)W);
+            const FastDiv fs = make_fastdiv((unsigned)S);
             if (K == 2 && S == 2)
                 hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 2, 2>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
             else if (K == 3 && S == 2)
                 hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 3, 2>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+            else if (K == 4 && S == 4)
+                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 4, 4>), g, b, shm, s, C, H, W, K, S,
+                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
             else
                 hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 0, 0>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, argmax, d, gt, o);
+                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
             return;
         }
     }

@@ -55,7 +55,9 @@ GemmPlan plan_for(int dt, const GemmDims& d)
         if (c[0] > fpmax) continue;
         const long long t = tiles(c[0], c[1]);
         const long long ks = std::min(cdiv(d.K, bk_of(c[0], c[1])) / 8, 32ll);
-        if (t >= kTargetTiles || (t >= 64 && t * ks >= kTargetBlocks)) {
+        // (one 96-row tile stands for two 64-row ones, so it needs half as many tiles)
+        const long long tmin = c[0] == 3 ? 32 : 64;
+        if (t >= kTargetTiles || (t >= tmin && t * ks >= kTargetBlocks)) {
             g.FP = c[0];
             g.FQ = c[1];
             break;

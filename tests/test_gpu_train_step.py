@@ -377,6 +377,10 @@ def test_full_size_shard_gradients_match_oracle(name, shard):
                for l in launches), seen
     assert any(l["site"] == "dgrad" and l["tile_rows"] * l["tile_cols"] >= 64 * 128
                for l in launches), seen
+    if name == "alexnet":
+        # conv1's 96 output channels: the 96-row weight-gradient tile with row-along loads
+        assert any(l["site"] == "wgrad" and l["tile_rows"] == 96 and l["splits"] > 1
+                   for l in launches), seen
 
 
 @pytest.mark.parametrize("name", ["cifar", "alexnet"])

@@ -104,26 +104,42 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const T* __restrict__ x
         }
         const T* xb = x + (long long)r * M * C + c0;
         const T* gb = BWD ? dy + (long long)r * M * C + c0 : nullptr;
-        for (long long i0 = r0 + rl; i0 < r1; i0 += (long long)kUnroll * lanes) {
-            float xv[kUnroll][W], gv[kUnroll][W];
+        // Raw rows (W elements each), loaded one batch of kUnroll rows ahead: the loads of the
+        // next batch are in flight while this one is added (with one batch at a time, each
+        // thread waited a full memory round trip per batch).  Rows past the range read as zeros.
+        typedef std::conditional_t<(W > 1), u32x4v, T> Raw;
+        auto load_batch = [&](long long i0, Raw (&rx)[kUnroll], Raw (&rg)[kUnroll]) {
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const long long i = i0 + (long long)u * lanes;
-                const bool ok = i < r1;
-                if constexpr (W > 1) {
-                    if (ok) {
-                        load_vec<T, W>(xb + i * C, xv[u]);
-                        if (BWD) load_vec<T, W>(gb + i * C, gv[u]);
-                    }
-                } else {
-                    if (ok) {
-                        xv[u][0] = to_f32<T>(xb[i * C]);
-                        if (BWD) gv[u][0] = to_f32<T>(gb[i * C]);
-                    }
+                rx[u] = Raw{};
+                rg[u] = Raw{};
+                if (i < r1) {
+                    rx[u] = *reinterpret_cast<const Raw*>(xb + i * C);
+                    if (BWD) rg[u] = *reinterpret_cast<const Raw*>(gb + i * C);
                 }
-                if (!ok)
+            }
+        };
+        auto unpack = [&](const Raw& raw, float (&v)[W]) {
+            const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-                    for (int k = 0; k < W; ++k) xv[u][k] = gv[u][k] = 0.f;
+            for (int k = 0; k < W; ++k) v[k] = to_f32<T>(e[k]);
+        };
+        const long long step = (long long)kUnroll * lanes;
+        Raw cx[kUnroll], cg[kUnroll];
+        long long i0 = r0 + rl;
+        if (i0 < r1) load_batch(i0, cx, cg);
+        for (; i0 < r1; i0 += step) {
+            Raw nx[kUnroll], ng[kUnroll];
+            if (i0 + step < r1) load_batch(i0 + step, nx, ng);
+            float xv[kUnroll][W], gv[kUnroll][W];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                unpack(cx[u], xv[u]);
+                if (BWD) unpack(cg[u], gv[u]);
+                else
+#pragma unroll
+                    for (int k = 0; k < W; ++k) gv[u][k] = 0.f;
             }
             float fa[W], fb[W];
 #pragma unroll
@@ -144,6 +160,11 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const T* __restrict__ x
             for (int k = 0; k < W; ++k) {
                 da[k] += (double)fa[k];
                 db[k] += (double)fb[k];
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                cx[u] = nx[u];
+                cg[u] = ng[u];
             }
         }
     }

@@ -78,6 +78,8 @@ struct LayerPlan {
     size_t stat_off;             // batch normalisation: per-shard (mean, 1/std) [R][C] floats
     size_t skip_off;             // residual addition: gradient for the source layer [B][...]
     size_t proj_off;             // projection shortcut: its stored output [B][oh][ow][oc]
+    bool dy_shared;              // residual addition: the previous layer's output gradient is
+                                 // this layer's own buffer (no copy is made)
 };
 
 constexpr size_t kNone = ~(size_t)0;
@@ -460,6 +462,24 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
                                     : (double)pl.B * lp.in_elems * lp.oc;
             pl.gemm_flops += 2.0 * macs * (lp.need_dx ? 3 : 2);
         }
+    }
+    // A residual addition passes its output gradient to the previous layer unchanged when that
+    // layer has no ReLU (its output is not read by any other addition): the previous layer then
+    // reads the addition's gradient buffer itself instead of a copy (the batch normalisation
+    // before each addition of the residual networks: one tensor written and read less).
+    for (size_t i = 1; i < pl.L.size(); ++i) {
+        LayerPlan& lp = pl.L[i];
+        lp.dy_shared = false;
+        if ((lp.kind != MTX_ADD && lp.kind != MTX_ADDP) || !lp.need_dx || pl.L[i - 1].relu)
+            continue;
+        bool other = false;
+        for (size_t j = 0; j < pl.L.size(); ++j)
+            if ((pl.L[j].kind == MTX_ADD || pl.L[j].kind == MTX_ADDP) &&
+                pl.L[j].src == (int)i - 1)
+                other = true;
+        if (other) continue;
+        pl.L[i - 1].dy_off = lp.dy_off;
+        lp.dy_shared = true;
     }
     if (pl.x_convert) {
         pl.xin_off = ws;
@@ -1347,9 +1367,10 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
         } else if (lp.kind == MTX_ADD) {
             void* skip = lp.skip_off != kNone ? ws + lp.skip_off : nullptr;
             const LayerPlan& sp = pl.L[lp.src];
-            if (dx || skip)
+            void* dxc = lp.dy_shared ? nullptr : dx;  // (shared: dx is dy itself)
+            if (dxc || skip)
                 HIP_TRY(launch_site(m, "add_bwd", l, s, [&] {
-                            return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32, skip,
+                            return add_bwd(dt, lp.out_elems * pl.B, dy, dxc, mask, mask_f32, skip,
                                            sp.relu ? ws + sp.act_off : nullptr, sp.act_f32, s);
                         }), "residual backward");
         } else if (lp.kind == MTX_ADDP) {
@@ -1362,7 +1383,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                           m->grads, ld, (long long)lp.w_off, (long long)lp.b_off,
                                           part_wg, sw);
                     }), "projection weight gradient");
-            if (dx)
+            if (dx && !lp.dy_shared)
                 HIP_TRY(launch_site(m, "add_bwd", l, s, [&] {
                             return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32,
                                            nullptr, nullptr, false, s);

@@ -76,7 +76,7 @@ struct LayerPlan {
     int src;                     // residual addition: the layer whose output is added
     bool direct;                 // first convolution through the direct kernels (firstconv.hip)
     size_t stat_off;             // batch normalisation: per-shard (mean, 1/std) [R][C] floats
-    size_t skip_off;             // residual addition: gradient for the source layer [B][...]
+    size_t skip_off;             // projection shortcut: gradient for the source layer [B][...]
     size_t proj_off;             // projection shortcut: its stored output [B][oh][ow][oc]
     bool dy_shared;              // residual addition: the previous layer's output gradient is
                                  // this layer's own buffer (no copy is made)
@@ -391,11 +391,12 @@ int make_plan(const mtx_model_desc* d, int R, int Nb, Plan& pl)
                                                                    lp.h * lp.w));
             max_bn_coef = std::max(max_bn_coef, (size_t)pl.R * lp.c * 3);
         }
-        // a residual addition keeps the gradient for its source until the source's own output
-        // gradient exists (only when the source's gradient is needed at all)
+        // a projection shortcut keeps the gradient for its source (its data gradient) until the
+        // source's own output gradient exists (only when the source's gradient is needed at
+        // all); an identity addition's share is its own output gradient, which stays unchanged
+        // until the end of the step, so it needs no buffer of its own
         lp.skip_off = kNone;
-        if ((lp.kind == MTX_ADD || lp.kind == MTX_ADDP) && lp.src >= pl.first_param &&
-            pl.first_param >= 0) {
+        if (lp.kind == MTX_ADDP && lp.src >= pl.first_param && pl.first_param >= 0) {
             lp.skip_off = ws;
             ws = align_up(ws + pl.L[lp.src].out_elems * pl.B * es, kAlign);
         }
@@ -1365,13 +1366,12 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                       (long long)lp.w_off, (long long)lp.b_off, s);
                     }), "batch norm backward");
         } else if (lp.kind == MTX_ADD) {
-            void* skip = lp.skip_off != kNone ? ws + lp.skip_off : nullptr;
-            const LayerPlan& sp = pl.L[lp.src];
-            void* dxc = lp.dy_shared ? nullptr : dx;  // (shared: dx is dy itself)
-            if (dxc || skip)
+            // the previous layer's share: dy (times its ReLU mask), unless it reads dy itself;
+            // the source's share is added from dy when the source's gradient is written
+            if (dx && !lp.dy_shared)
                 HIP_TRY(launch_site(m, "add_bwd", l, s, [&] {
-                            return add_bwd(dt, lp.out_elems * pl.B, dy, dxc, mask, mask_f32, skip,
-                                           sp.relu ? ws + sp.act_off : nullptr, sp.act_f32, s);
+                            return add_bwd(dt, lp.out_elems * pl.B, dy, dx, mask, mask_f32,
+                                           nullptr, nullptr, false, s);
                         }), "residual backward");
         } else if (lp.kind == MTX_ADDP) {
             // the previous layer's gradient is dy (times its ReLU mask); the projection's weight
@@ -1408,17 +1408,22 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                     }), "pool backward");
         }
         // The output gradient of layer l - 1 is now written; if a residual addition also read
-        // that layer's output, add the gradient it kept for it (before the layer's own weight
-        // gradient is forked off on the next iteration).
+        // that layer's output, add its share (before the layer's own weight gradient is forked
+        // off on the next iteration): an identity addition's output gradient, times the ReLU
+        // mask of layer l - 1, or a projection's data gradient, which has the mask applied.
         if (lp.need_dx)
             for (size_t a2 = (size_t)l + 1; a2 < pl.L.size(); ++a2) {
                 const LayerPlan& ap = pl.L[a2];
-                if ((ap.kind != MTX_ADD && ap.kind != MTX_ADDP) || ap.src != l - 1 ||
-                    ap.skip_off == kNone)
+                if (ap.src != l - 1 || (ap.kind != MTX_ADD && ap.kind != MTX_ADDP) ||
+                    (ap.kind == MTX_ADDP && ap.skip_off == kNone))
                     continue;
+                const LayerPlan& sp = pl.L[l - 1];
+                const bool ident = ap.kind == MTX_ADD;
                 HIP_TRY(launch_site(m, "skip_add", l - 1, s, [&] {
-                            return skip_add(dt, pl.L[l - 1].out_elems * pl.B,
-                                            ws + pl.L[l - 1].dy_off, ws + ap.skip_off, s);
+                            return skip_add(dt, sp.out_elems * pl.B, ws + sp.dy_off,
+                                            ws + (ident ? ap.dy_off : ap.skip_off),
+                                            ident && sp.relu ? ws + sp.act_off : nullptr,
+                                            sp.act_f32, s);
                         }), "residual gradient");
             }
         // Layer-wise averaging (the paper issues one reduction per layer, in layer order): this

@@ -257,7 +257,9 @@ hipError_t add_fwd(Dt dt, size_t n, const void* a, const void* b, void* y, bool 
                    hipStream_t s);
 hipError_t add_bwd(Dt dt, size_t n, const void* dy, void* dx, const void* mask, bool mask_f32,
                    void* skip, const void* smask, bool smask_f32, hipStream_t s);
-hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, hipStream_t s);
+// dy += skip where smask (the source's stored output, its ReLU) is positive; null: everywhere
+hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, const void* smask,
+                    bool smask_f32, hipStream_t s);
 
 // firstconv.hip: direct kernels for a first convolution with one input channel, stride 1,
 // a 3x3, 5x5 or 7x7 window and at most 32 output channels (a multiple of 4) whose image and

@@ -463,14 +463,17 @@ __global__ __launch_bounds__(256) void add_bwd_kernel(const T* __restrict__ dy,
     if (skip) skip[t] = mask_pass<T>(smask, smask_f32, t) ? g : from_f32<T>(0.f);
 }
 
+// dy += skip where the source's ReLU passed (smask: its stored output; null: everywhere)
 template <typename T>
 __global__ __launch_bounds__(256) void skip_add_kernel(T* __restrict__ dy,
                                                        const T* __restrict__ skip,
+                                                       const void* smask, int smask_f32,
                                                        unsigned total)
 {
     const unsigned t = blockIdx.x * 256 + threadIdx.x;
     if (t >= total) return;
-    dy[t] = from_f32<T>(to_f32<T>(dy[t]) + to_f32<T>(skip[t]));
+    const float g = mask_pass<T>(smask, smask_f32, t) ? to_f32<T>(skip[t]) : 0.f;
+    dy[t] = from_f32<T>(to_f32<T>(dy[t]) + g);
 }
 
 // 16-byte variants: V consecutive elements per thread (n a multiple of V).
@@ -538,17 +541,20 @@ __global__ __launch_bounds__(256) void add_bwd_vec_kernel(const T* __restrict__ 
 template <typename T>
 __global__ __launch_bounds__(256) void skip_add_vec_kernel(T* __restrict__ dy,
                                                            const T* __restrict__ skip,
+                                                           const void* smask, int smask_f32,
                                                            unsigned nvec)
 {
     constexpr int V = 16 / sizeof(T);
     const unsigned t = blockIdx.x * 256 + threadIdx.x;
     if (t >= nvec) return;
-    float a[V], b[V];
-    load_vec<T, V>(dy + (size_t)t * V, a);
-    load_vec<T, V>(skip + (size_t)t * V, b);
+    const size_t e = (size_t)t * V;
+    float a[V], b[V], m[V];
+    load_vec<T, V>(dy + e, a);
+    load_vec<T, V>(skip + e, b);
+    load_mask<T, V>(smask, smask_f32, e, m);
 #pragma unroll
-    for (int k = 0; k < V; ++k) a[k] += b[k];
-    store_vec<T, V>(dy + (size_t)t * V, a);
+    for (int k = 0; k < V; ++k) a[k] += m[k] > 0.f ? b[k] : 0.f;
+    store_vec<T, V>(dy + e, a);
 }
 
 hipError_t add_fwd(Dt dt, size_t n, const void* a, const void* b, void* y, bool relu,
@@ -615,28 +621,33 @@ hipError_t add_bwd(Dt dt, size_t n, const void* dy, void* dx, const void* mask, 
     return hipGetLastError();
 }
 
-hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, hipStream_t s)
+hipError_t skip_add(Dt dt, size_t n, void* dy, const void* skip, const void* smask,
+                    bool smask_f32, hipStream_t s)
 {
     const size_t V = dt == DT_F32 ? 4 : 8;
+    const int mf = smask_f32 ? 1 : 0;
     if (n % V == 0) {
         const unsigned nv = (unsigned)(n / V);
         const dim3 g((nv + 255) / 256);
         if (dt == DT_F32)
             hipLaunchKernelGGL((skip_add_vec_kernel<float>), g, dim3(256), 0, s,
-                               static_cast<float*>(dy), static_cast<const float*>(skip), nv);
+                               static_cast<float*>(dy), static_cast<const float*>(skip), smask,
+                               mf, nv);
         else
             hipLaunchKernelGGL((skip_add_vec_kernel<bf16_t>), g, dim3(256), 0, s,
-                               static_cast<bf16_t*>(dy), static_cast<const bf16_t*>(skip), nv);
+                               static_cast<bf16_t*>(dy), static_cast<const bf16_t*>(skip), smask,
+                               mf, nv);
         return hipGetLastError();
     }
     const unsigned total = (unsigned)n;
     const dim3 g((total + 255) / 256);
     if (dt == DT_F32)
         hipLaunchKernelGGL((skip_add_kernel<float>), g, dim3(256), 0, s, static_cast<float*>(dy),
-                           static_cast<const float*>(skip), total);
+                           static_cast<const float*>(skip), smask, mf, total);
     else
         hipLaunchKernelGGL((skip_add_kernel<bf16_t>), g, dim3(256), 0, s,
-                           static_cast<bf16_t*>(dy), static_cast<const bf16_t*>(skip), total);
+                           static_cast<bf16_t*>(dy), static_cast<const bf16_t*>(skip), smask, mf,
+                           total);
     return hipGetLastError();
 }
 

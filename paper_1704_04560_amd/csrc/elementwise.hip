@@ -458,7 +458,7 @@ __global__ __launch_bounds__(256) void pool_bwd_s2_kernel(int total, int C, int 
 // per (position, channel), channels fastest, gathers in ascending window order and writes NHWC.
 constexpr int kPoolCB = 64;            // channels per block at most
 constexpr size_t kPoolLds = 64 << 10;  // LDS bytes per block at most
-template <typename T, int KT, int ST>
+template <typename T, int KT, int ST, int CV>
 __global__ __launch_bounds__(256) void pool_bwd_nchw_kernel(int C, int H, int W, int Kr, int Sr,
                                                             int OH, int OW, int cb, int pst,
                                                             int rows, FastDiv fcb, FastDiv fw,
@@ -486,25 +486,41 @@ __global__ __launch_bounds__(256) void pool_bwd_nchw_kernel(int C, int H, int W,
         sa[cl * pst + ij] = argmax[g];
     }
     __syncthreads();
-    const int cnt = (h1 - h0) * W * cb;
+    // one thread per (position, CV channels), channel groups fastest; CV = 8 (bf16) or 4 (fp32)
+    // channels go out as one 16-byte store (one 2-byte store per thread made the store
+    // instructions, not the bytes, the limit: 75 us for the 67 MB input gradient of the
+    // bottleneck network's 4/4 pooling)
+    const int cbv = cb / CV;  // fcb divides by cbv
+    const int cnt = (h1 - h0) * W * cbv;
     // (the window ranges divide non-negative values by the stride: by a constant, or with the
     // fast division by an invariant integer)
     auto divs = [&](int v) { return ST > 0 ? v / ST : (int)fdivu(fs, (unsigned)v); };
     for (int e = threadIdx.x; e < cnt; e += 256) {
-        const unsigned hw = fdivu(fcb, (unsigned)e), cl = (unsigned)e - hw * (unsigned)cb;
+        const unsigned hw = fdivu(fcb, (unsigned)e), cg = (unsigned)e - hw * (unsigned)cbv;
         const unsigned hr = fdivu(fw, hw);
         const int h = h0 + (int)hr, w = (int)(hw - hr * (unsigned)W);
         const int jlo = w - K + 1 <= 0 ? 0 : divs(w - K + 1 + S - 1);
         const int jhi = min(divs(w), OW - 1);
         const int il = max(ilo, h - K + 1 <= 0 ? 0 : divs(h - K + 1 + S - 1));
         const int ih = min(divs(h), OH - 1);
-        float acc = 0.f;
+        const int cl0 = (int)cg * CV;
+        float acc[CV];
+#pragma unroll
+        for (int k = 0; k < CV; ++k) acc[k] = 0.f;
         for (int i = il; i <= ih; ++i)
             for (int j = jlo; j <= jhi; ++j) {
-                const int idx = (int)cl * pst + (i - ilo) * OW + j;
-                if (sa[idx] == (uint8_t)((h - i * S) * K + (w - j * S))) acc += sg[idx];
+                const int wi = (i - ilo) * OW + j;
+                const uint8_t code = (uint8_t)((h - i * S) * K + (w - j * S));
+#pragma unroll
+                for (int k = 0; k < CV; ++k) {
+                    const int idx = (cl0 + k) * pst + wi;
+                    if (sa[idx] == code) acc[k] += sg[idx];
+                }
             }
-        dx[(((long long)n * H + h) * W + w) * C + cb0 + (int)cl] = from_f32<T>(acc);
+        Chans<T, CV> out;
+#pragma unroll
+        for (int k = 0; k < CV; ++k) out.v[k] = from_f32<T>(acc[k]);
+        store_chans<T, CV>(dx + (((long long)n * H + h) * W + w) * C + cb0 + cl0, out);
     }
 }
 
@@ -532,20 +548,27 @@ static void pool_bwd_launch(int N, int C, int H, int W, int K, int S, bool dy_nc
             const int rows = (H + bands - 1) / bands;
             const size_t shm = (size_t)cb * pst * (sizeof(float) + 1);
             dim3 g((unsigned)(C / cb), (unsigned)N, (unsigned)((H + rows - 1) / rows));
-            const FastDiv fcb = make_fastdiv((unsigned)cb), fw = make_fastdiv((unsigned)W);
-            const FastDiv fs = make_fastdiv((unsigned)S);
-            if (K == 2 && S == 2)
-                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 2, 2>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
-            else if (K == 3 && S == 2)
-                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 3, 2>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
-            else if (K == 4 && S == 4)
-                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 4, 4>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
-            else
-                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 0, 0>), g, b, shm, s, C, H, W, K, S,
-                                   OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+            const FastDiv fw = make_fastdiv((unsigned)W), fs = make_fastdiv((unsigned)S);
+            constexpr int V = 16 / sizeof(T);
+            if (cb % V == 0) {
+                const FastDiv fcb = make_fastdiv((unsigned)(cb / V));
+                if (K == 2 && S == 2)
+                    hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 2, 2, V>), g, b, shm, s, C, H, W,
+                                       K, S, OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+                else if (K == 3 && S == 2)
+                    hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 3, 2, V>), g, b, shm, s, C, H, W,
+                                       K, S, OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+                else if (K == 4 && S == 4)
+                    hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 4, 4, V>), g, b, shm, s, C, H, W,
+                                       K, S, OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+                else
+                    hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 0, 0, V>), g, b, shm, s, C, H, W,
+                                       K, S, OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+            } else {
+                const FastDiv fcb = make_fastdiv((unsigned)cb);
+                hipLaunchKernelGGL((pool_bwd_nchw_kernel<T, 0, 0, 1>), g, b, shm, s, C, H, W, K,
+                                   S, OH, OW, cb, pst, rows, fcb, fw, fs, argmax, d, gt, o);
+            }
             return;
         }
     }

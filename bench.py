@@ -153,12 +153,15 @@ def _site_work(name, layer, geo, wkl, es, fused=()):
             return "hbm", 2 * in_sz * es, 0.0
         if name == "bn_bwd_apply":  # x, dy and the mask read, dx written
             return "hbm", 4 * in_sz * es, 0.0
-        if name in ("add_fwd", "skip_add"):  # two read, one written
+        if name == "add_fwd":  # two read, one written
             return "hbm", 3 * out_sz * es, 0.0
-        if name == "add_bwd" and l.kind == wl.ADDP:  # dy and the mask read, dx written
+        if name == "skip_add":
+            # the source's gradient and the shortcut's share read, the sum written; an identity
+            # shortcut's share is the addition's own output gradient, times the source's ReLU mask
+            ident = any(h["layer"].kind == wl.ADD and h["layer"].k == layer for h in geo)
+            return "hbm", (4 if ident and l.relu else 3) * out_sz * es, 0.0
+        if name == "add_bwd":  # dy and the mask read, dx written (runs only where not shared)
             return "hbm", 3 * out_sz * es, 0.0
-        if name == "add_bwd":  # dy and two masks read, dx and the kept gradient written
-            return "hbm", 5 * out_sz * es, 0.0
         return None, 0.0, 0.0
     P = wkl_params(wkl)
     if name == "avg_update":  # the whole step's share (the caller divides by its launches)

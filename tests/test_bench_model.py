@@ -87,3 +87,13 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.returncode != 0
     assert "--gpus 1" in r.stderr
     assert not r.stdout.strip()
+
+
+def test_identity_shortcut_share_reads_the_source_mask():
+    # bottleneck layer 15 adds layer 8's output (a projection block's ReLU output, 256 x 32 x 32):
+    # the share added into layer 8's gradient is layer 15's own output gradient, times layer 8's
+    # ReLU mask, so the launch reads three tensors and writes one
+    bound, nbytes, mm = _work("bottleneck", "skip_add", 8)
+    assert bound == "hbm" and mm == 0.0
+    assert nbytes == 4 * 256 * 256 * 32 * 32 * 2
+

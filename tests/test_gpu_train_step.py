@@ -496,14 +496,15 @@ def _wide_fc(dtype):
 
 @pytest.mark.parametrize("name,R,Nb,mu", [("wide-f32", 2, 8, 0.9), ("wide-bf16", 4, 4, 0.0),
                                            ("alexnet", 2, 2, 0.9), ("alexnet", 8, 1, 0.0),
-                                           ("lenet", 4, 16, 0.9)])
+                                           ("alexnet", 8, 32, 0.9), ("lenet", 4, 16, 0.9)])
 def test_fused_fc_update_is_bit_identical(name, R, Nb, mu):
     """Large fully connected layers average and update their own parameters in their
     weight-gradient launch (all R shards of a tile in one block); the shard rows, the average,
     the velocity and the weights are bit-identical to the stand-alone average + update over all
     parameters, with momentum and with plain SGD, over direct and graph-replayed steps.  The
     launch record shows which launches were fused: layers of at least 2^20 parameters with at
-    least 512 tiles of 128 x 128 only."""
+    least 512 tiles of 128 x 128 only; at the full AlexNet size too, where the weight gradients
+    run on the second stream."""
     net = {"wide-f32": _wide_fc(wl.F32), "wide-bf16": _wide_fc(wl.BF16), "alexnet": wl.ALEXNET,
            "lenet": wl.LENET}[name]
     expect = {"wide-f32": [0], "wide-bf16": [0], "alexnet": [8, 9], "lenet": []}[name]

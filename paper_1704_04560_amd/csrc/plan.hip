@@ -22,8 +22,9 @@ int vec_elems(int dt) { return dt == DT_F32 ? 4 : 8; }
 static long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
 // Tile: the largest of 128x128, 64x128, 64x64, 32x128, 32x64 (rows x columns) that gives at
-// least two blocks per compute unit, or at least 64 tiles and a reduction long enough for splits
-// to fill the GPU (the smallest tile when none does); rows are limited by P.  Reduction splits
+// least two blocks per compute unit, or at least 64 tiles (32 for the 96- and 128-row tiles of
+// 128 columns) and a reduction long enough for splits to fill the GPU (the smallest tile when
+// none does); rows are limited by P.  Reduction splits
 // then double until the launch has one block per compute unit for the larger tiles, two for the
 // smaller ones, keeping at least 8 k tiles per split: more splits cost more in fp32 partial sums
 // (written, then read back by a second kernel) than they gain in fill (measured: filling two
@@ -55,8 +56,11 @@ GemmPlan plan_for(int dt, const GemmDims& d)
         if (c[0] > fpmax) continue;
         const long long t = tiles(c[0], c[1]);
         const long long ks = std::min(cdiv(d.K, bk_of(c[0], c[1])) / 8, 32ll);
-        // (one 96-row tile stands for two 64-row ones, so it needs half as many tiles)
-        const long long tmin = c[0] == 3 ? 32 : 64;
+        // (one 96-row tile stands for two 64-row ones, so it needs half as many tiles; so does
+        // the 128 x 128 tile, whose products per LDS byte are twice those of 64 x 64 ones: the
+        // CIFAR conv3 weight gradient, 40 tiles over 128 x 577, 74 -> 59 us. Not the 64 x 128
+        // tile, which measured slower at 32-63 tiles: CIFAR conv2 112 -> 124 us)
+        const long long tmin = c[0] * c[1] >= 12 ? 32 : 64;
         if (t >= kTargetTiles || (t >= tmin && t * ks >= kTargetBlocks)) {
             g.FP = c[0];
             g.FQ = c[1];

@@ -147,8 +147,10 @@ def _site_work(name, layer, geo, wkl, es, fused=()):
             return "hbm", out_sz * (es + 1) + in_sz * es * 2, 0.0  # dy + argmax, mask + dx
         if name == "bn_fwd":  # the statistics pass reads x
             return "hbm", in_sz * es, 0.0
-        if name == "bn_fwd_apply":  # x read, y written
-            return "hbm", 2 * in_sz * es, 0.0
+        if name == "bn_fwd_apply":  # x read, y written; with the residual addition that
+            # follows, computed in the same pass, also its other operand read and its sum written
+            nxt = geo[layer + 1]["layer"].kind if layer + 1 < len(geo) else None
+            return "hbm", (4 if nxt in (wl.ADD, wl.ADDP) else 2) * in_sz * es, 0.0
         if name == "bn_bwd":  # x and dy read
             return "hbm", 2 * in_sz * es, 0.0
         if name == "bn_bwd_apply":  # x, dy and the mask read, dx written

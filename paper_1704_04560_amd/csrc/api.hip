@@ -1165,6 +1165,7 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
     float* partial = reinterpret_cast<float*>(ws + pl.partial_off);
     // ---- forward, all R shards at once (the weights are shared) ----
     const void* in = x_in;
+    std::vector<char> add_done(pl.L.size(), 0);  // computed with the layer before it
     for (size_t l = 0; l < pl.L.size(); ++l) {
         const LayerPlan& lp = pl.L[l];
         void* out = ws + lp.act_off;
@@ -1203,28 +1204,52 @@ static int enqueue_step(mtx_model* m, const float* x, const int32_t* labels, flo
                                       lp.act_f32, lp.relu, partial, s);
                     }), "fc forward");
         } else if (lp.kind == MTX_BN) {
+            // A residual addition right after the batch normalisation is computed in the same
+            // pass as its normalised output (which is still stored): the addition does not
+            // read that output back.  A projection shortcut's convolution runs first.
+            const LayerPlan* ap = l + 1 < pl.L.size() ? &pl.L[l + 1] : nullptr;
+            const bool with_add = ap && (ap->kind == MTX_ADD || ap->kind == MTX_ADDP) &&
+                                  !ap->act_f32 == !lp.act_f32;
+            const void* other = nullptr;
+            if (with_add && ap->kind == MTX_ADDP) {
+                const LayerPlan& sp = pl.L[ap->src];
+                HIP_TRY(launch_site(m, "fwd", (int)l + 1, s, [&] {
+                            return conv_fwd(dt, proj_geom(*ap, sp, pl.B), ws + sp.act_off,
+                                            fwd_w(*ap), m->w + ap->b_off, ws + ap->proj_off,
+                                            ap->act_f32, false, partial, s);
+                        }), "projection forward");
+                other = ws + ap->proj_off;
+            } else if (with_add) {
+                other = ws + pl.L[ap->src].act_off;
+            }
+            if (with_add) add_done[l + 1] = 1;
             HIP_TRY(launch_site(m, "bn_fwd", (int)l, s, [&] {
                         return bn_fwd(dt, pl.R, pl.Nb, lp.h * lp.w, lp.c, in, out,
                                       m->w + lp.w_off, m->w + lp.b_off,
                                       reinterpret_cast<double*>(ws + pl.bn_part_off),
-                                      reinterpret_cast<float*>(ws + lp.stat_off), lp.relu, s);
+                                      reinterpret_cast<float*>(ws + lp.stat_off), lp.relu, s,
+                                      other, with_add ? ws + ap->act_off : nullptr,
+                                      with_add && ap->relu);
                     }), "batch norm forward");
         } else if (lp.kind == MTX_ADD) {
-            HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
-                        return add_fwd(dt, lp.out_elems * pl.B, in, ws + pl.L[lp.src].act_off, out,
-                                       lp.relu, s);
-                    }), "residual addition");
+            if (!add_done[l])
+                HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
+                            return add_fwd(dt, lp.out_elems * pl.B, in,
+                                           ws + pl.L[lp.src].act_off, out, lp.relu, s);
+                        }), "residual addition");
         } else if (lp.kind == MTX_ADDP) {
             // the projection (stored like a convolution's output), then the addition
             const LayerPlan& sp = pl.L[lp.src];
             void* pj = ws + lp.proj_off;
-            HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
-                        return conv_fwd(dt, proj_geom(lp, sp, pl.B), ws + sp.act_off, fwd_w(lp),
-                                        bias, pj, lp.act_f32, false, partial, s);
-                    }), "projection forward");
-            HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
-                        return add_fwd(dt, lp.out_elems * pl.B, in, pj, out, lp.relu, s);
-                    }), "projection addition");
+            if (!add_done[l]) {
+                HIP_TRY(launch_site(m, "fwd", (int)l, s, [&] {
+                            return conv_fwd(dt, proj_geom(lp, sp, pl.B), ws + sp.act_off,
+                                            fwd_w(lp), bias, pj, lp.act_f32, false, partial, s);
+                        }), "projection forward");
+                HIP_TRY(launch_site(m, "add_fwd", (int)l, s, [&] {
+                            return add_fwd(dt, lp.out_elems * pl.B, in, pj, out, lp.relu, s);
+                        }), "projection addition");
+            }
         } else if (!(l == 1 && pl.pool_into_first)) {  // else computed with layer 0
             HIP_TRY(launch_site(m, "pool_fwd", (int)l, s, [&] {
                         return pool_fwd(dt, pl.B, lp.c, lp.h, lp.w, lp.k, lp.s, !lp.nhwc, in, out,

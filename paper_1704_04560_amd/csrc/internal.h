@@ -241,9 +241,12 @@ constexpr int kBnStatFloats = 4;  // per (shard, channel): mean, 1/std, gamma/st
 // receives [R][4][C] floats (mean, 1 / sqrt(var + eps), gamma / sqrt(var + eps), beta) for the
 // apply pass and the backward pass.  C must be at most 256, or a multiple of 16 / element size
 // up to 256 such vectors.
+// skip (nullable): the residual addition that follows, z = y + skip (relu2: then ReLU), in the
+// same pass over y
 hipError_t bn_fwd(Dt dt, int R, int Nb, int HW, int C, const void* x, void* y,
                   const float* gamma, const float* beta, double* part, float* stats, bool relu,
-                  hipStream_t s);
+                  hipStream_t s, const void* skip = nullptr, void* z = nullptr,
+                  bool relu2 = false);
 // gamma / beta gradients of every shard into grads[r * ld + w_off / b_off + c], and (dx != null)
 // dx = gamma inv (dy - mean(dy) - xhat mean(dy xhat)) times the ReLU mask of the layer below;
 // stats are the forward pass's; coef is [R][3][C] floats of scratch.

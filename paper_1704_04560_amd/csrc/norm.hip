@@ -241,10 +241,14 @@ __global__ __launch_bounds__(256) void bn_finalize_kernel(
 // y = (x - mean) * scale + shift, ReLU, stored in the compute type; W consecutive channels per
 // thread (the element index t counts groups of W).
 template <typename T, int W>
+// (skip != null: the residual addition that follows, z = y + skip with its own ReLU flag, in the
+// same pass: y as stored, plus skip, rounded once -- the arithmetic of add_fwd_kernel)
 __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ x, T* __restrict__ y,
                                                        const float* __restrict__ stats,
                                                        unsigned rows_per_shard, int C,
-                                                       unsigned n, int relu)
+                                                       unsigned n, int relu,
+                                                       const T* __restrict__ skip,
+                                                       T* __restrict__ z, int relu2)
 {
     const unsigned t = blockIdx.x * 256 + threadIdx.x;
     if (t >= n) return;
@@ -270,6 +274,18 @@ __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ x, 
     }
     if constexpr (W > 1) store_vec<T, W>(y + e, v);
     else y[e] = from_f32<T>(v[0]);
+    if (skip) {
+        float b[W];
+        if constexpr (W > 1) load_vec<T, W>(skip + e, b);
+        else b[0] = to_f32<T>(skip[e]);
+#pragma unroll
+        for (int k = 0; k < W; ++k) {
+            v[k] = to_f32<T>(from_f32<T>(v[k])) + b[k];
+            if (relu2) v[k] = fmaxf(v[k], 0.f);
+        }
+        if constexpr (W > 1) store_vec<T, W>(z + e, v);
+        else z[e] = from_f32<T>(v[0]);
+    }
 }
 
 template <typename T, int W>
@@ -341,8 +357,10 @@ size_t bn_partial_doubles(Dt dt, int R, int C, int Nb, int HW)
 template <typename T>
 static hipError_t bn_fwd_t(int R, int Nb, int HW, int C, const void* x, void* y,
                            const float* gamma, const float* beta, double* part, float* stats,
-                           bool relu, hipStream_t s)
+                           bool relu, hipStream_t s, const void* skip, void* z, bool relu2)
 {
+    const T* sk = static_cast<const T*>(skip);
+    T* zt = static_cast<T*>(z);
     constexpr int V = 16 / sizeof(T);
     const long long M = (long long)Nb * HW;
     const int S = bn_splits(R, C, M, sizeof(T));
@@ -364,21 +382,26 @@ static hipError_t bn_fwd_t(int R, int Nb, int HW, int C, const void* x, void* y,
     if (vec) {
         const unsigned n = (unsigned)(total / V);
         hipLaunchKernelGGL((bn_apply_kernel<T, V>), dim3((n + 255) / 256), dim3(256), 0, s, xt,
-                           static_cast<T*>(y), stats, (unsigned)M, C, n, relu ? 1 : 0);
+                           static_cast<T*>(y), stats, (unsigned)M, C, n, relu ? 1 : 0, sk, zt,
+                           relu2 ? 1 : 0);
     } else {
         const unsigned n = (unsigned)total;
         hipLaunchKernelGGL((bn_apply_kernel<T, 1>), dim3((n + 255) / 256), dim3(256), 0, s, xt,
-                           static_cast<T*>(y), stats, (unsigned)M, C, n, relu ? 1 : 0);
+                           static_cast<T*>(y), stats, (unsigned)M, C, n, relu ? 1 : 0, sk, zt,
+                           relu2 ? 1 : 0);
     }
     return hipGetLastError();
 }
 
 hipError_t bn_fwd(Dt dt, int R, int Nb, int HW, int C, const void* x, void* y,
                   const float* gamma, const float* beta, double* part, float* stats, bool relu,
-                  hipStream_t s)
+                  hipStream_t s, const void* skip, void* z, bool relu2)
 {
-    if (dt == DT_F32) return bn_fwd_t<float>(R, Nb, HW, C, x, y, gamma, beta, part, stats, relu, s);
-    return bn_fwd_t<bf16_t>(R, Nb, HW, C, x, y, gamma, beta, part, stats, relu, s);
+    if (dt == DT_F32)
+        return bn_fwd_t<float>(R, Nb, HW, C, x, y, gamma, beta, part, stats, relu, s, skip, z,
+                               relu2);
+    return bn_fwd_t<bf16_t>(R, Nb, HW, C, x, y, gamma, beta, part, stats, relu, s, skip, z,
+                            relu2);
 }
 
 template <typename T>

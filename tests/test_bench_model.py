@@ -97,3 +97,12 @@ def test_identity_shortcut_share_reads_the_source_mask():
     assert bound == "hbm" and mm == 0.0
     assert nbytes == 4 * 256 * 256 * 32 * 32 * 2
 
+
+
+def test_batch_norm_apply_carries_the_following_addition():
+    # bottleneck layer 14 (BN over 256 x 32 x 32) is followed by layer 15's identity addition,
+    # computed in the same pass: x and the shortcut read, the BN output and the sum written
+    bound, nbytes, mm = _work("bottleneck", "bn_fwd_apply", 14)
+    assert bound == "hbm" and nbytes == 4 * 256 * 256 * 32 * 32 * 2
+    # layer 12's BN (ReLU, then a convolution) moves x and y only
+    assert _work("bottleneck", "bn_fwd_apply", 12)[1] == 2 * 256 * 64 * 32 * 32 * 2

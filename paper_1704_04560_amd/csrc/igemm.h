@@ -689,6 +689,16 @@ __device__ __forceinline__ void row_epi8(const GemmArgs& a, const Ctx& c, int p,
 }
 
 // An operation that declares INTERLEAVE = true gets the interleaved scheduling order below.
+// An operation that declares DEEP_PREFETCH = true (the bf16 fully connected forward: a product
+// over a long k for a few hundred output tiles, one block per compute unit, one wave per SIMD)
+// keeps three k tiles of loads in flight in registers instead of one: with no other wave to
+// run, a loop that issues the next tile's loads only one tile ahead waits for most of a memory
+// round trip every k tile (AlexNet FC6 / FC7 / FC8 forward 43 / 33 / 17 -> 40 / 27 / 14 us).
+// Not the data gradient: its 288 blocks of FC6 then need two rounds (46 -> 67 us).
+template <class Op, class = void> struct DeepPrefetch : std::false_type {};
+template <class Op>
+struct DeepPrefetch<Op, std::void_t<decltype(Op::DEEP_PREFETCH)>> : std::bool_constant<Op::DEEP_PREFETCH> {};
+
 template <class Op, class = void> struct Interleave : std::false_type {};
 template <class Op>
 struct Interleave<Op, std::void_t<decltype(Op::INTERLEAVE)>> : std::bool_constant<Op::INTERLEAVE> {};
@@ -942,20 +952,56 @@ __global__ __launch_bounds__(256) void igemm_kernel(const GemmArgs a)
             for (int j = 0; j < FQ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
         int k0 = c.kbeg;
-        if (k0 < c.kend) {
-            lp.load(a, bufP, c, tid, p0, k0);
-            lq.load(a, bufQ, c, tid, q0, k0);
-        }
-        for (; k0 < c.kend; k0 += BK) {
-            lp.stage(sP, tid);
-            lq.stage(sQ, tid);
-            __syncthreads();
-            if (k0 + BK < c.kend) {
-                lp.load(a, bufP, c, tid, p0, k0 + BK);
-                lq.load(a, bufQ, c, tid, q0, k0 + BK);
+        if constexpr (DeepPrefetch<Op>::value) {
+            // three register stages: stage i holds k tile t with t mod 3 == i; once tile t is
+            // staged into LDS its registers take the loads of tile t + 3
+            Loader<Op, true, PK, BP, BK> lp1, lp2;
+            Loader<Op, false, QK, BQ, BK> lq1, lq2;
+            lp1.init(a, c, tid, p0);
+            lq1.init(a, c, tid, q0);
+            lp2.init(a, c, tid, p0);
+            lq2.init(a, c, tid, q0);
+            auto issue = [&](auto& xp, auto& xq, int k) {
+                if (k < c.kend) {
+                    xp.load(a, bufP, c, tid, p0, k);
+                    xq.load(a, bufQ, c, tid, q0, k);
+                }
+            };
+            issue(lp, lq, k0);
+            issue(lp1, lq1, k0 + BK);
+            issue(lp2, lq2, k0 + 2 * BK);
+            auto step = [&](auto& xp, auto& xq) {
+                xp.stage(sP, tid);
+                xq.stage(sQ, tid);
+                __syncthreads();
+                issue(xp, xq, k0 + 3 * BK);
+                products(acc, wp, wq, lr, lg);
+                __syncthreads();
+                k0 += BK;
+                return k0 < c.kend;
+            };
+            if (k0 < c.kend)
+                for (;;) {
+                    if (!step(lp, lq)) break;
+                    if (!step(lp1, lq1)) break;
+                    if (!step(lp2, lq2)) break;
+                }
+        } else {
+            if (k0 < c.kend) {
+                lp.load(a, bufP, c, tid, p0, k0);
+                lq.load(a, bufQ, c, tid, q0, k0);
             }
-            products(acc, wp, wq, lr, lg);
-            __syncthreads();
+            for (; k0 < c.kend; k0 += BK) {
+                lp.stage(sP, tid);
+                lq.stage(sQ, tid);
+                __syncthreads();
+                if (k0 + BK < c.kend) {
+                    lp.load(a, bufP, c, tid, p0, k0 + BK);
+                    lq.load(a, bufQ, c, tid, q0, k0 + BK);
+                }
+                products(acc, wp, wq, lr, lg);
+                __syncthreads();
+            }
         }
         // the main loop ended with a barrier, so the operand tiles are free for the staging:
         // waves 0, 1 use sP, waves 2, 3 use sQ

@@ -534,6 +534,7 @@ template <typename T> struct FcFwd {
     static constexpr bool P_IS_A = false;
     static constexpr bool SHARE_Q = false;
     static constexpr bool TAB = false, TAB_CHUNK = false;
+    static constexpr bool DEEP_PREFETCH = sizeof(T) == 2;  // few blocks: loads 3 k tiles ahead
     struct PK { int k; bool ok; };
     __device__ static PK pk(const GemmArgs&, const Ctx& c, int k) { return PK{k, k < c.kend}; }
     __device__ static T p_sk(const GemmArgs& a, const Buf<T>& B, const Ctx&, const PK& s, int p)

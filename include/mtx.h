@@ -301,7 +301,10 @@ int mtx_set_optimizer(mtx_model* m, int kind, float beta1, float beta2, float ep
  * order; *count receives the number of sites.  reset != 0 clears the accumulated times.
  * Launch-site names: "prep_w" (weight layouts), "prep_x" (input layout), "fwd", "pool_fwd",
  * "bn_fwd", "add_fwd", "softmax_xent" (with the loss mean), "wgrad" (weight and bias gradient),
- * "dgrad", "pool_bwd", "bn_bwd", "add_bwd", "skip_add", "avg_update"; "fwd_direct" and
+ * "dgrad", "pool_bwd", "bn_bwd", "add_bwd", "skip_add", "avg_update" (a residual addition right
+ * after a batch normalisation is computed in that layer's "bn_fwd_apply" and has no "add_fwd"
+ * of its own; "add_bwd" runs only where the previous layer's gradient is not the addition's
+ * own buffer; "skip_add" adds a shortcut's share into its source's gradient); "fwd_direct" and
  * "wgrad_direct" for a first convolution of one input channel and a 3x3, 5x5 or 7x7 window
  * (at most 32 outputs), which runs on direct kernels instead of the matrix kernels; the second
  * kernel of an operation is a site of its own: "<site>_reduce" (the second pass of a split

@@ -281,11 +281,99 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, 
     for (int e = 0; e < CV; ++e) argmax[o + e] = bi[e];
 }
 
+// NCHW output (the pooled tensor feeds a fully connected layer): a block takes one sample and cb
+// channels (a multiple of CV), computes their cb x P outputs (P = OH*OW; one task per position
+// and CV channels, the same window rule as above) into LDS in the output's [channel][position]
+// order, and writes them -- one contiguous range of y and one of argmax -- with 16-byte stores
+// (one thread per position writing its CV channels to CV planes made 16 scattered narrow stores
+// per thread: AlexNet pool3 ran at a third of the HBM rate).
+constexpr int kPoolFwdCB = 64;              // channels per block at most
+constexpr size_t kPoolFwdLds = 48 << 10;    // LDS bytes per block at most
+template <typename T, int KT, int ST, int CV>
+__global__ __launch_bounds__(256) void pool_fwd_nchw_kernel(int C, int H, int W, int Kr, int Sr,
+                                                            int OH, int OW, int cb, FastDiv fcg,
+                                                            const T* __restrict__ x,
+                                                            T* __restrict__ y,
+                                                            uint8_t* __restrict__ argmax)
+{
+    extern __shared__ __attribute__((aligned(16))) unsigned char pool_smem[];
+    const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
+    const int P = OH * OW, cgs = cb / CV;
+    T* sy = reinterpret_cast<T*>(pool_smem);
+    uint8_t* sa = pool_smem + (((size_t)cb * P * sizeof(T) + 15) & ~(size_t)15);
+    const int n = blockIdx.y, cb0 = blockIdx.x * cb;
+    for (int tk = threadIdx.x; tk < P * cgs; tk += 256) {
+        const unsigned pos = fdivu(fcg, (unsigned)tk), cg = (unsigned)tk - pos * (unsigned)cgs;
+        const unsigned i = pos / (unsigned)OW, j = pos - i * (unsigned)OW;
+        const int c0 = cb0 + (int)cg * CV;
+        const T* xp = x + (((long long)n * H + (int)i * S) * W + (int)j * S) * C + c0;
+        const int rs = W * C;
+        Chans<T, CV> best = load_chans<T, CV>(xp);
+        float bv[CV];
+        uint8_t bi[CV];
+#pragma unroll
+        for (int e = 0; e < CV; ++e) { bv[e] = to_f32<T>(best.v[e]); bi[e] = 0; }
+        for (int u = 0; u < K; ++u)
+            for (int v = 0; v < K; ++v) {
+                const Chans<T, CV> cur = load_chans<T, CV>(xp + u * rs + v * C);
+#pragma unroll
+                for (int e = 0; e < CV; ++e) {
+                    const float tv = to_f32<T>(cur.v[e]);
+                    if (tv > bv[e]) { bv[e] = tv; best.v[e] = cur.v[e]; bi[e] = (uint8_t)(u * K + v); }
+                }
+            }
+#pragma unroll
+        for (int e = 0; e < CV; ++e) {
+            sy[((int)cg * CV + e) * P + (int)pos] = best.v[e];
+            sa[((int)cg * CV + e) * P + (int)pos] = bi[e];
+        }
+    }
+    __syncthreads();
+    const long long base = ((long long)n * C + cb0) * P;
+    const int cnt = cb * P;
+    T* yo = y + base;
+    uint8_t* ao = argmax + base;
+    constexpr int VE = 16 / (int)sizeof(T);
+    if (base % VE == 0 && cnt % VE == 0)
+        for (int e = threadIdx.x; e < cnt / VE; e += 256)
+            *reinterpret_cast<uint4*>(yo + (long long)e * VE) = *reinterpret_cast<const uint4*>(sy + e * VE);
+    else
+        for (int e = threadIdx.x; e < cnt; e += 256) yo[e] = sy[e];
+    if (base % 16 == 0 && cnt % 16 == 0)
+        for (int e = threadIdx.x; e < cnt / 16; e += 256)
+            *reinterpret_cast<uint4*>(ao + (long long)e * 16) = *reinterpret_cast<const uint4*>(sa + e * 16);
+    else
+        for (int e = threadIdx.x; e < cnt; e += 256) ao[e] = sa[e];
+}
+
 template <typename T, int CV>
 static void pool_fwd_launch(int N, int C, int H, int W, int K, int S, bool out_nchw,
                             const void* x, void* y, uint8_t* argmax, hipStream_t s)
 {
     const int OH = (H - K) / S + 1, OW = (W - K) / S + 1;
+    if (out_nchw && CV > 1) {
+        // channels per block: the largest multiple of CV dividing C within the limits
+        const size_t P = (size_t)OH * OW;
+        int cb = 0;
+        for (int c = std::min(kPoolFwdCB, C); c >= CV && !cb; --c)
+            if (C % c == 0 && c % CV == 0 &&
+                (((size_t)c * P * sizeof(T) + 15) & ~(size_t)15) + (size_t)c * P <= kPoolFwdLds)
+                cb = c;
+        if (cb > 0) {
+            const size_t shm = (((size_t)cb * P * sizeof(T) + 15) & ~(size_t)15) + (size_t)cb * P;
+            const dim3 g((unsigned)(C / cb), (unsigned)N);
+            const FastDiv fcg = make_fastdiv((unsigned)(cb / CV));
+            const T* xx = static_cast<const T*>(x);
+            T* yy = static_cast<T*>(y);
+            if (K == 3 && S == 2)
+                hipLaunchKernelGGL((pool_fwd_nchw_kernel<T, 3, 2, CV>), g, dim3(256), shm, s, C, H,
+                                   W, K, S, OH, OW, cb, fcg, xx, yy, argmax);
+            else
+                hipLaunchKernelGGL((pool_fwd_nchw_kernel<T, 0, 0, CV>), g, dim3(256), shm, s, C, H,
+                                   W, K, S, OH, OW, cb, fcg, xx, yy, argmax);
+            return;
+        }
+    }
     const int total = N * OH * OW * (C / CV);
     const FastDiv fcv = make_fastdiv((unsigned)(C / CV)), fow = make_fastdiv((unsigned)OW),
                   foh = make_fastdiv((unsigned)OH);

@@ -244,7 +244,13 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(int total, int C, int H, 
                                                        uint8_t* __restrict__ argmax)
 {
     const int K = KT > 0 ? KT : Kr, S = ST > 0 ? ST : Sr;
-    const int t = blockIdx.x * 256 + threadIdx.x;  // over N*OH*OW*(C/CV)
+    // overlapping windows (S < K): blocks numbered so that each of the 8 XCDs (blocks go to them
+    // round-robin) takes one contiguous range of outputs, and neighbouring output rows, which
+    // read the same input rows, share that XCD's L2 (AlexNet's 3/2 poolings 50.6 / 32.9 ->
+    // 47.8 / 31.2 us; disjoint 2/2 windows gain nothing from it)
+    const unsigned nb = gridDim.x, hb = blockIdx.x, xq = nb / 8, xr = nb % 8, xx = hb % 8;
+    const unsigned bid = S < K ? xx * xq + min(xx, xr) + hb / 8 : hb;
+    const int t = (int)bid * 256 + threadIdx.x;  // over N*OH*OW*(C/CV)
     if (t >= total) return;
     const unsigned CG = (unsigned)(C / CV);
     const unsigned pos = fdivu(fcv, (unsigned)t), c0 = ((unsigned)t - pos * CG) * CV;

@@ -125,6 +125,16 @@ def test_pool_windows_and_strides(dtype):
     run_case(f"tiny3-{dtype}", _tiny_pools(dtype), 2, 3, 2, 10, 0.05, 0.9)
 
 
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_pool_before_fc_with_an_odd_channel_group(dtype):
+    """A 3/2 pooling of 24 channels to 3 x 3 positions feeding a fully connected layer: the
+    pooled output is NCHW, a block takes all 24 channels (not a power of two), and its 216
+    outputs start at offsets that are not 16-byte aligned in the argmax tensor."""
+    layers = (wl.conv(24, 3, pad=1, relu=True), wl.maxpool(3, 2), wl.fc(5))
+    net = wl.Net("pool-odd", (3, 7, 7), layers, dtype, "normal")
+    run_case(f"pool-odd-{dtype}", net, 2, 3, 2, 12, 0.05, 0.9)
+
+
 def _single_channel(dtype, oc, k, pad, relu):
     """One input channel into a small-window first convolution: the shape the direct
     first-convolution kernels take (ragged image, several output-channel counts and windows)."""
